@@ -1,0 +1,69 @@
+/*
+ * CPU oracle for the STAR decode-rescheduling hot path: declarations.
+ *
+ * TEST INFRASTRUCTURE ONLY (see star_oracle.c).  This header belongs to the
+ * oracle alone; the HIP library neither includes nor mirrors it.
+ *
+ * All pointers are host memory.  Matrices are row-major.  Functions return 0
+ * on success and -1 on a malformed argument.
+ */
+#ifndef STAR_ORACLE_H
+#define STAR_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { STAR_ORACLE_F32 = 0, STAR_ORACLE_BF16 = 1 };          /* input element type */
+enum { STAR_ORACLE_RELU = 0, STAR_ORACLE_GELU = 1 };         /* hidden activation  */
+enum { STAR_ORACLE_BAD_INST = 1, STAR_ORACLE_BAD_CUR = 2, STAR_ORACLE_BAD_REM = 4 };
+
+/* Predictor head (Section 3.2, Eq. 1-2; length bins of Section 5.5).
+ * hidden [B,d], w1 [m,d], w2 [nb,m] in `dtype` (bf16 as uint16 bits);
+ * b1 [m], b2 [nb] fp32 or NULL; bin_values [nb] fp32.
+ * expected [B] <- E = sum_j softmax(z2)_j v_j.
+ * ema_alpha in [0,1]; 0 disables smoothing.  With smoothing, ema_state [B]
+ * (fp64, caller-owned) is set to E when ema_init, else to a E + (1-a) state.
+ * rem_len [B] (or NULL) <- clamp(round-half-even(smoothed E), 1, len_max).
+ * z1_out [B,m] / z2_out [B,nb] (or NULL) receive the pre-activation and the
+ * bin logits for inspection. */
+int star_oracle_predict(int64_t B, int64_t d, int64_t m, int64_t nb, int dtype, int act,
+                        const void* hidden, const void* w1, const float* b1,
+                        const void* w2, const float* b2, const float* bin_values,
+                        double ema_alpha, int ema_init, double* ema_state,
+                        int64_t len_max, double* expected, int32_t* rem_len,
+                        double* z1_out, double* z2_out);
+
+/* Load curves (Section 4.2, Eq. 4 and the worker-side summary of the
+ * complexity analysis).  load [n,K]: load[i,k] = sum over decode steps
+ * t in [k b, (k+1) b) of sum_{r in B_i, t < rem_r} (cur_r + t).
+ * Requests with inst_of outside [0,n), cur_len < 1 or rem_len < 1 are
+ * skipped; the OR of their STAR_ORACLE_BAD_* flags goes to *flags_out. */
+int star_oracle_project_load(int64_t N, int64_t n, int64_t b, int64_t K,
+                             const int32_t* cur_len, const int32_t* rem_len,
+                             const int32_t* inst_of, int64_t* load, int32_t* flags_out);
+
+/* Candidate scores [N,n] (Algorithm 1, best-feasible selection, with the
+ * projected peak as the figure of merit): for t != inst(r), the maximum over
+ * buckets of load[t] plus r's own bucketed curve; for t == inst(r), the
+ * maximum of load[t].  Skipped requests get a row of -1. */
+int star_oracle_score(int64_t N, int64_t n, int64_t b, int64_t K,
+                      const int32_t* cur_len, const int32_t* rem_len, const int32_t* inst_of,
+                      const int64_t* load, int64_t* scores);
+
+/* Ranking of all migrations (t != inst(r)) by (score, r, t) ascending.
+ * best_target[r] / best_score[r]: the smallest key of request r, or -1.
+ * topk_*[q], q < top_k: the q-th smallest key, or -1 past the end.
+ * Any output pointer may be NULL. */
+int star_oracle_rank(int64_t N, int64_t n, const int32_t* cur_len, const int32_t* rem_len,
+                     const int32_t* inst_of, const int64_t* scores, int64_t top_k,
+                     int32_t* best_target, int64_t* best_score,
+                     int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score);
+
+int star_oracle_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

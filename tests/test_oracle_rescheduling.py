@@ -1,0 +1,219 @@
+"""Pins of the CPU oracle's load projection, scoring and ranking.
+
+The load model is Section 4.2's: a request with N(r) current tokens and
+N^(r) predicted remaining steps holds N(r)+t tokens at step t < N^(r); the
+token load of instance i at step t is the sum over its batch B_i (Eq. 4's
+N^_i(B_{i,t})), and N_i(B_i) = sum N(r) is the current load.  A candidate
+(r, s, t) of Algorithm 1 is scored by the peak of instance t's curve after r
+joins it.  The pins are a hand-worked example, closed forms, conservation
+under migration, brute-force reassignment, the current-load-balancing special
+case, and library sorts.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from paper_2510_13668_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _example():
+    return json.load(open(os.path.join(GOLDEN, "round_worked_example.json")))
+
+
+def test_worked_example(oracle_mod):
+    ex = _example()
+    rq = ex["requests"]
+    cur, rem, inst = (np.array(rq[k], np.int32) for k in ("cur_len", "rem_len", "inst_of"))
+    out = oracle_mod.round_(cur, rem, inst, n_inst=2, bucket=ex["bucket"],
+                            n_buckets=ex["n_buckets"], top_k=3)
+    np.testing.assert_array_equal(out["load"], ex["load"])
+    np.testing.assert_array_equal(out["scores"], ex["scores"])
+    np.testing.assert_array_equal(out["best_target"], ex["best_target"])
+    np.testing.assert_array_equal(out["best_score"], ex["best_score"])
+    ranked = np.stack([out["topk_score"], out["topk_req"], out["topk_tgt"]], 1)
+    np.testing.assert_array_equal(ranked, ex["ranked"])
+    one, _ = oracle_mod.project_load(cur, rem, np.zeros(3, np.int32), n_inst=1,
+                                     bucket=ex["bucket"], n_buckets=ex["n_buckets"])
+    np.testing.assert_array_equal(one[0], ex["load_all_on_one_instance"])
+    b1, _ = oracle_mod.project_load(cur, rem, inst, n_inst=2, bucket=1, n_buckets=1)
+    np.testing.assert_array_equal(b1[:, 0], ex["current_load_b1"])
+
+
+@pytest.mark.parametrize("b,K", [(1, 1), (1, 17), (4, 5), (64, 8), (7, 3)])
+def test_single_request_total_is_arithmetic_series(oracle_mod, b, K):
+    """sum_k L[k] = sum_{t < l'} (c + t) = l' c + l'(l'-1)/2 with l' = min(l, H)."""
+    H = b * K
+    rng = np.random.default_rng(b * 100 + K)
+    lens = sorted({1, b, 2 * b, H - 1, H, H + 1, 3 * H} | set(rng.integers(1, 3 * H + 2, 8).tolist()))
+    for ell in lens:
+        if ell < 1:
+            continue
+        c = int(rng.integers(1, 5000))
+        load, flags = oracle_mod.project_load(np.array([c], np.int32), np.array([ell], np.int32),
+                                              np.zeros(1, np.int32), n_inst=1, bucket=b,
+                                              n_buckets=K)
+        assert flags == 0
+        lp = min(ell, H)
+        assert int(load.sum()) == lp * c + lp * (lp - 1) // 2
+
+
+def test_bucket_closed_forms(oracle_mod):
+    """Bucket k of one request: b c + b^2 k + b(b-1)/2 while full, mu c + mu k b
+    + mu(mu-1)/2 for the partial bucket of mu steps, zero after."""
+    rng = np.random.default_rng(11)
+    for _ in range(200):
+        b = int(rng.integers(1, 9))
+        K = int(rng.integers(1, 12))
+        c = int(rng.integers(1, 10000))
+        ell = int(rng.integers(1, b * K + 5))
+        load, _ = oracle_mod.project_load(np.array([c], np.int32), np.array([ell], np.int32),
+                                          np.zeros(1, np.int32), n_inst=1, bucket=b, n_buckets=K)
+        lp = min(ell, b * K)
+        ke, mu = divmod(lp, b)
+        want = np.zeros(K, np.int64)
+        for k in range(K):
+            if k < ke:
+                want[k] = b * c + b * b * k + b * (b - 1) // 2
+            elif k == ke:
+                want[k] = mu * c + mu * ke * b + mu * (mu - 1) // 2
+        np.testing.assert_array_equal(load[0], want)
+
+
+def test_current_load_is_bucket_zero_at_unit_buckets(oracle_mod):
+    """b = 1: L_i[0] = N_i(B_i) = sum_{r in B_i} N(r)."""
+    rng = np.random.default_rng(12)
+    cur, rem, inst = synth.random_requests(rng, 300, 7, cur_hi=9000, len_hi=500)
+    load, _ = oracle_mod.project_load(cur, rem, inst, n_inst=7, bucket=1, n_buckets=50)
+    want = np.bincount(inst, weights=cur.astype(np.float64), minlength=7)
+    np.testing.assert_array_equal(load[:, 0], want.astype(np.int64))
+
+
+def test_active_count_at_unit_buckets(oracle_mod):
+    """b = 1: L[t+1] - L[t] = (#requests alive at t+1) - (sum of c+t over the ones ending at t+1)."""
+    rng = np.random.default_rng(13)
+    cur, rem, inst = synth.random_requests(rng, 40, 1, cur_hi=100, len_hi=30)
+    load, _ = oracle_mod.project_load(cur, rem, inst, n_inst=1, bucket=1, n_buckets=40)
+    for t in range(39):
+        alive_next = rem > t + 1
+        ending = rem == t + 1
+        delta = int(alive_next.sum()) - int((cur[ending].astype(np.int64) + t).sum())
+        assert load[0, t + 1] - load[0, t] == delta
+
+
+def test_additivity_permutation_and_empty_instances(oracle_mod):
+    rng = np.random.default_rng(14)
+    cur, rem, inst = synth.random_requests(rng, 120, 6, cur_hi=3000, len_hi=900, empty_inst=2)
+    kw = dict(n_inst=6, bucket=16, n_buckets=40)
+    load, _ = oracle_mod.project_load(cur, rem, inst, **kw)
+    assert not load[4:].any()
+    # one instance's curve = sum of each of its requests' curves
+    for i in range(4):
+        acc = np.zeros(40, np.int64)
+        for r in np.nonzero(inst == i)[0]:
+            one, _ = oracle_mod.project_load(cur[r:r + 1], rem[r:r + 1], np.zeros(1, np.int32),
+                                             n_inst=1, bucket=16, n_buckets=40)
+            acc += one[0]
+        np.testing.assert_array_equal(load[i], acc)
+    perm = rng.permutation(120)
+    load2, _ = oracle_mod.project_load(cur[perm], rem[perm], inst[perm], **kw)
+    np.testing.assert_array_equal(load, load2)
+
+
+def test_invalid_requests_are_skipped_and_flagged(oracle_mod):
+    cur = np.array([5, 0, 7, 9, 3], np.int32)
+    rem = np.array([4, 4, -1, 2, 6], np.int32)
+    inst = np.array([0, 1, 1, 3, 1], np.int32)
+    load, flags = oracle_mod.project_load(cur, rem, inst, n_inst=2, bucket=2, n_buckets=3)
+    assert flags == (oracle_mod.BAD_CUR | oracle_mod.BAD_REM | oracle_mod.BAD_INST)
+    ok = np.array([0, 4], np.int64)
+    ref, _ = oracle_mod.project_load(cur[ok], rem[ok], inst[ok], n_inst=2, bucket=2, n_buckets=3)
+    np.testing.assert_array_equal(load, ref)
+    scores = oracle_mod.score(cur, rem, inst, load, bucket=2)
+    assert (scores[[1, 2, 3]] == -1).all()
+    rk = oracle_mod.rank(cur, rem, inst, scores, top_k=4)
+    assert list(rk["best_target"][[1, 2, 3]]) == [-1, -1, -1]
+    assert set(rk["topk_req"][rk["topk_req"] >= 0].tolist()) <= {0, 4}
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_scores_equal_brute_force_reassignment(oracle_mod, seed):
+    """Moving r from s to t and rebuilding every curve from scratch: the peak of
+    t's new curve is s(r, t), the source's curve loses exactly what the target
+    gains (total occupancy is conserved), and staying scores s's own peak."""
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(1, 5))
+    N = int(rng.integers(1, 9))
+    b = int(rng.integers(1, 6))
+    K = int(rng.integers(1, 9))
+    cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=200, len_hi=b * K + 4)
+    load, _ = oracle_mod.project_load(cur, rem, inst, n_inst=n, bucket=b, n_buckets=K)
+    scores = oracle_mod.score(cur, rem, inst, load, bucket=b)
+    for r in range(N):
+        s = inst[r]
+        for t in range(n):
+            if t == s:
+                assert scores[r, t] == load[t].max()
+                continue
+            moved = inst.copy()
+            moved[r] = t
+            after, _ = oracle_mod.project_load(cur, rem, moved, n_inst=n, bucket=b, n_buckets=K)
+            assert scores[r, t] == after[t].max()
+            assert after[s].sum() + after[t].sum() == load[s].sum() + load[t].sum()
+            own, _ = oracle_mod.project_load(cur[r:r + 1], rem[r:r + 1], np.zeros(1, np.int32),
+                                             n_inst=1, bucket=b, n_buckets=K)
+            assert scores[r, t] >= load[t].max() and scores[r, t] >= own[0].max()
+
+
+def test_unit_horizon_is_current_load_balancing(oracle_mod):
+    """K = 1, b = 1: s(r, t) = N_t(B_t) + N(r), and the best target is the
+    least-loaded other instance (the current-load baseline of Section 2)."""
+    rng = np.random.default_rng(15)
+    n = 9
+    cur, rem, inst = synth.random_requests(rng, 200, n, cur_hi=4000, len_hi=50)
+    out = oracle_mod.round_(cur, rem, inst, n_inst=n, bucket=1, n_buckets=1, top_k=5)
+    Nt = np.bincount(inst, weights=cur.astype(np.float64), minlength=n).astype(np.int64)
+    for r in range(200):
+        for t in range(n):
+            want = Nt[t] if t == inst[r] else Nt[t] + cur[r]
+            assert out["scores"][r, t] == want
+        others = np.array([Nt[t] if t != inst[r] else np.iinfo(np.int64).max for t in range(n)])
+        assert out["best_target"][r] == int(np.argmin(others))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_ranking_against_library_sort(oracle_mod, seed):
+    rng = np.random.default_rng(200 + seed)
+    n = int(rng.integers(2, 7))
+    N = int(rng.integers(1, 60))
+    cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=50, len_hi=40)
+    if seed % 2 == 0:                       # duplicated requests force ties
+        cur[N // 2:] = cur[0]
+        rem[N // 2:] = rem[0]
+        inst[N // 2:] = inst[0]
+    out = oracle_mod.round_(cur, rem, inst, n_inst=n, bucket=4, n_buckets=12, top_k=37)
+    S = out["scores"]
+    rr, tt = np.meshgrid(np.arange(N), np.arange(n), indexing="ij")
+    keep = tt != inst[:, None]
+    s, r, t = S[keep], rr[keep], tt[keep]
+    order = np.lexsort((t, r, s))
+    k = min(37, len(order))
+    np.testing.assert_array_equal(out["topk_score"][:k], s[order][:k])
+    np.testing.assert_array_equal(out["topk_req"][:k], r[order][:k])
+    np.testing.assert_array_equal(out["topk_tgt"][:k], t[order][:k])
+    assert (out["topk_req"][k:] == -1).all()
+    masked = np.where(keep, S, np.iinfo(np.int64).max)
+    np.testing.assert_array_equal(out["best_target"], np.argmin(masked, axis=1))
+    np.testing.assert_array_equal(out["best_score"], masked.min(axis=1))
+
+
+def test_single_instance_has_no_migrations(oracle_mod):
+    cur = np.array([3, 4, 5], np.int32)
+    rem = np.array([2, 2, 2], np.int32)
+    out = oracle_mod.round_(cur, rem, np.zeros(3, np.int32), n_inst=1, bucket=1, n_buckets=4,
+                            top_k=4)
+    assert (out["best_target"] == -1).all() and (out["topk_req"] == -1).all()
+    assert (out["scores"][:, 0] == out["load"][0].max()).all()
