@@ -1,0 +1,231 @@
+"""Benchmark of one STAR rescheduling round on one MI355X.
+
+A step is one full pass of the hot path over one decode step of the
+continuous-mode workload (1024 concurrent requests on 8 decode instances,
+bf16 hidden states [1024, 4096] from an AR(1) process, head 4096 -> 512
+(GELU) -> 64 length bins with EMA alpha 0.2, horizon 16384 steps in 64-step
+buckets, all 1024 x 8 candidates scored, top-256 ranked):
+    star_predict -> star_project_load -> star_score_migrations.
+Inputs for 200 decode steps are staged in HBM before timing.  The metric is
+requests predicted + scored per second (= 1024 / seconds per round) and
+microseconds per round.
+
+Prints ONE JSON line.  Usage:
+    python bench.py [--gpus 1] [--steps 200] [--warmup 10] [--mode graph|eager]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "requests predicted+scored/sec at B=1024,d=4096; µs per reschedule round"
+WORKLOAD = "continuous"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--mode", choices=("graph", "eager"), default="graph")
+    ap.add_argument("--cpu-rounds", type=int, default=20,
+                    help="rounds of the CPU oracle timed for the baseline (0 = skip)")
+    return ap.parse_args()
+
+
+class HipEvents:
+    """Raw hipEvent_t handles (timing events on an explicit stream)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self, n):
+        out = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            if self.hip.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            out.append(e)
+        return out
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def destroy(self, evs):
+        for e in evs:
+            self.hip.hipEventDestroy(e)
+
+
+def cpu_baseline(x, wl, rounds: int):
+    """The CPU oracle on the first `rounds` decode steps of the same workload."""
+    import oracle
+    state = np.zeros(wl.n_req, np.float64)
+    t0 = time.perf_counter()
+    for s in range(rounds):
+        out = oracle.predict(x.hidden[s], x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act,
+                             ema_alpha=wl.ema_alpha, ema_init=(s == 0), ema_state=state,
+                             len_max=wl.len_max)
+        oracle.round_((x.cur_len + s).astype(np.int32), out["rem_len"], x.inst_of,
+                      n_inst=wl.n_inst, bucket=wl.bucket, n_buckets=wl.n_buckets, top_k=wl.top_k)
+    dt = time.perf_counter() - t0
+    return {"value": wl.n_req * rounds / dt, "unit": "requests/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"first {rounds} of the 200 decode steps, all {wl.n_req} requests, full "
+                      f"round (fp64 head, per-step int64 curves, direct peak per candidate, "
+                      f"full sort); {dt:.2f} s"}
+
+
+def main():
+    args = _parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this hot path runs on one GPU (decode instances are data, not devices); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2510_13668_amd import star, synth
+
+    dev = "cuda"
+    wl = synth.WORKLOADS[WORKLOAD]
+    S = wl.steps
+    x = synth.make_inputs(wl)                       # 200 staged decode steps
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    hid = bf(x.hidden)                              # [200, 1024, 4096] bf16, 1.68 GB
+    w1, w2 = bf(x.w1), bf(x.w2)
+    bins = torch.from_numpy(x.bin_values).to(dev)
+    cur_steps = torch.from_numpy(np.stack([x.cur_len + s for s in range(S)]).astype(np.int32)).to(dev)
+    inst = torch.from_numpy(x.inst_of).to(dev)
+
+    N, d, m, nb = wl.n_req, wl.d_model, wl.d_hidden, wl.n_bins
+    n, b, K, top_k = wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k
+    ema = torch.zeros(N, dtype=torch.float32, device=dev)
+    expected = torch.empty(N, dtype=torch.float32, device=dev)
+    rem = torch.empty(N, dtype=torch.int32, device=dev)
+    load = torch.empty((n, K), dtype=torch.int64, device=dev)
+    scores = torch.empty((N, n), dtype=torch.int64, device=dev)
+    best_t = torch.empty(N, dtype=torch.int32, device=dev)
+    best_s = torch.empty(N, dtype=torch.int64, device=dev)
+    tr = torch.empty(top_k, dtype=torch.int32, device=dev)
+    tt = torch.empty(top_k, dtype=torch.int32, device=dev)
+    ts = torch.empty(top_k, dtype=torch.int64, device=dev)
+
+    pp = star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, False, wl.len_max)
+    pp_init = star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, True, wl.len_max)
+    lp = star.load_params(N, n, b, K)
+    sp = star.score_params(N, n, b, K, top_k)
+    ws_p = star.Workspace(star.predict_workspace_size(pp))
+    ws_l = star.Workspace(star.project_load_workspace_size(lp))
+    ws_s = star.Workspace(star.score_workspace_size(sp))
+
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+
+    def round_(slot, params=pp):
+        star.predict(params, hid[slot], w1, None, w2, None, bins, ema, expected, rem, ws_p, stream)
+        star.project_load(lp, cur_steps[slot], rem, inst, load, ws_l, stream)
+        star.score_migrations(sp, cur_steps[slot], rem, inst, load, scores, best_t, best_s,
+                              tr, tt, ts, ws_s, stream)
+
+    with torch.cuda.stream(stream):
+        round_(0, pp_init)                          # first decode step initialises the EMA
+    graphs = None
+    if args.mode == "graph":
+        graphs = []
+        for slot in range(S):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                round_(slot)
+            graphs.append(g)
+    torch.cuda.synchronize()
+
+    def run_step(i):
+        slot = (i + 1) % S
+        if graphs is not None:
+            with torch.cuda.stream(stream):
+                graphs[slot].replay()
+        else:
+            round_(slot)
+
+    for i in range(args.warmup):
+        run_step(i)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for i in range(args.steps):
+        run_step(args.warmup + i)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+
+    # Dominant kernel (first-layer GEMM) timed with HIP events recorded by the
+    # library around that kernel on the same stream, over `steps` eager rounds.
+    he = HipEvents()
+    evs = he.create(2 * args.steps)
+    arrs = [(ctypes.c_void_p * 2)(evs[2 * i].value, evs[2 * i + 1].value) for i in range(args.steps)]
+    pps = [star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, False, wl.len_max,
+                               ctypes.cast(a, ctypes.c_void_p)) for a in arrs]
+    e_start = torch.cuda.Event(enable_timing=True)
+    e_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e_start.record(stream)
+    for i in range(args.steps):
+        round_((i + 1) % S, pps[i])
+    e_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step_eager = e_start.elapsed_time(e_end) / args.steps
+    gemm_ms = [he.elapsed_ms(evs[2 * i], evs[2 * i + 1]) for i in range(args.steps)]
+    he.destroy(evs)
+    gemm_avg_s = float(np.mean(gemm_ms)) * 1e-3
+    flops = 2.0 * N * d * m
+    achieved = flops / gemm_avg_s / 1e12
+
+    out = {
+        "metric": METRIC,
+        "value": N / (ms_step * 1e-3),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "us_per_round": ms_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "continuous: 1024 requests on 8 instances, hidden bf16 [1024,4096] "
+                               "AR(1) rho=0.95 over 200 staged decode steps, head 4096->512 GELU->64 "
+                               "bins, EMA 0.2, horizon 16384 in 64-step buckets, 1024x8 candidates, "
+                               "top-256",
+                   "n_req": N, "d_model": d, "d_hidden": m, "n_bins": nb, "n_inst": n,
+                   "horizon": wl.horizon, "bucket": b, "top_k": top_k, "mode": args.mode},
+        "us_per_round_eager": ms_step_eager * 1e3,
+        "roofline": {"kernel": "gemm1_splitk_kernel<2> (bf16 MFMA, H[1024,4096] x W1[512,4096]^T)",
+                     "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "avg_kernel_us": gemm_avg_s * 1e6, "algorithmic_flop": flops},
+    }
+    if args.cpu_rounds > 0:
+        out["cpu_baseline"] = cpu_baseline(x, wl, min(args.cpu_rounds, S))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

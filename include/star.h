@@ -1,0 +1,180 @@
+/*
+ * libstar -- MI355X (gfx950) hot path of STAR's decode-phase rescheduler
+ * (arXiv 2510.13668): remaining-length prediction, load projection and
+ * migration-candidate scoring for one rescheduling round.
+ *
+ * Vocabulary (Section 4.2, problem formulation):
+ *   instances I = {0..n_inst-1}; request r sits on instance inst_of[r]
+ *   (its batch B_i); N(r) = cur_len[r] is its current token count;
+ *   N^(r) = rem_len[r] its predicted remaining generation length; the load of
+ *   instance i at future decode step t is N^_i(B_{i,t}) = sum over r in B_i
+ *   with t < N^(r) of (N(r) + t)  (Eq. 4's per-step term).
+ *
+ * Conventions shared by every entry point
+ *   - Every array pointer is DEVICE memory owned by the caller; parameter
+ *     structs and status outputs are host memory.  The library never
+ *     allocates or frees device memory.
+ *   - Calls validate their scalar arguments synchronously (returning a
+ *     negative star_status before anything is launched), then enqueue
+ *     kernels on `stream` (a hipStream_t; NULL = the null stream) and
+ *     return.  Results are valid once the stream has reached that point.
+ *   - `ws` is a caller-owned device workspace of at least the size reported
+ *     by the matching *_workspace_size() call, 256-byte aligned.  Its first
+ *     256 bytes are a header that must be zero before first use
+ *     (star_workspace_init) and that the library keeps consistent across
+ *     calls (a sticky device-error word).  The rest is scratch.  Calls
+ *     sharing a workspace must be ordered (same stream, or synchronised).
+ *   - Array CONTENTS that break a documented precondition (instance index
+ *     out of range, cur_len < 1, rem_len < 1) are detected on the device:
+ *     the offending request is left out of every curve, score and ranking,
+ *     and a STAR_DEV_* bit is OR-ed into the workspace's error word, read
+ *     back by star_read_device_error.
+ *   - No call prints, aborts or throws.
+ */
+#ifndef STAR_H
+#define STAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define STAR_ABI_VERSION 1
+#define STAR_WS_HEADER_BYTES 256
+#define STAR_MAX_TOP_K 1024
+
+typedef enum {
+    STAR_OK = 0,
+    STAR_ERR_INVALID_ARG = -1,   /* null pointer, non-positive size, bad enum */
+    STAR_ERR_UNSUPPORTED = -2,   /* shape or alignment outside what the kernels handle */
+    STAR_ERR_OVERFLOW = -3,      /* sizes whose int64 loads could overflow */
+    STAR_ERR_WORKSPACE = -4,     /* workspace null, misaligned or too small */
+    STAR_ERR_HIP = -5            /* a HIP runtime call or kernel launch failed */
+} star_status;
+
+/* bits of the device-error word */
+enum { STAR_DEV_BAD_INST = 1, STAR_DEV_BAD_CUR = 2, STAR_DEV_BAD_REM = 4 };
+
+typedef enum { STAR_F32 = 0, STAR_BF16 = 1 } star_dtype;
+typedef enum { STAR_ACT_RELU = 0, STAR_ACT_GELU_ERF = 1 } star_act;
+
+/* ------------------------------------------------------------------------
+ * (a) Remaining-length predictor head.
+ *
+ * Section 3.2 feeds the last-layer, last-token hidden state h (size d) of
+ * each running request to a small MLP (Eq. 2) to estimate the distribution
+ * p(Y | S) of the remaining length Y (Eq. 1).  Here the head is
+ *     a1 = act(W1 h + b1)                 W1: [m, d]
+ *     z  = W2 a1 + b2                     W2: [nb, m]   (one logit per bin)
+ *     p  = softmax(z);  E = sum_j p_j v_j (mean of p over length bins v_j,
+ *                                          the binned targets of Section 5.5)
+ * and, for continuous prediction (Section 3.3), an exponential moving
+ * average across calls: y = alpha E + (1 - alpha) y_prev.
+ * Finally rem_len = clamp(round_half_even(y), 1, len_max), the N^(r) that
+ * (b) and (c) consume.
+ *
+ * Precision: bf16 or fp32 operands (dtype applies to hidden, w1 and w2);
+ * fp32 accumulation; a1 enters the second product as a bf16 hi/lo pair
+ * (bf16 path) or fp32; fp32 softmax and EMA.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    int32_t n_req;      /* B >= 0 rows of hidden */
+    int32_t d_model;    /* d >= 1; multiple of 8 (bf16) or 4 (fp32) */
+    int32_t d_hidden;   /* m in [1, 2048]; multiple of 8 (bf16) or 4 (fp32) */
+    int32_t n_bins;     /* nb in [1, 256] */
+    int32_t dtype;      /* star_dtype of hidden, w1, w2 */
+    int32_t act;        /* star_act */
+    float   ema_alpha;  /* 0 disables smoothing; else in (0, 1] */
+    int32_t ema_init;   /* 1: y := E this call (first step); 0: blend with ema_state */
+    int32_t len_max;    /* >= 1, upper clamp of rem_len */
+    void*   timing_events; /* NULL, or a host array of two hipEvent_t recorded
+                              on `stream` just before and just after the
+                              first-layer GEMM kernel (per-kernel timing) */
+} star_predict_params;
+
+size_t star_predict_workspace_size(const star_predict_params* p);
+
+/* hidden [B, d], w1 [m, d], w2 [nb, m]: row-major, 16-byte aligned.
+ * b1 [m], b2 [nb]: fp32 or NULL (zero).  bin_values [nb]: fp32.
+ * ema_state [B]: fp32 in/out, required iff ema_alpha > 0.
+ * expected_len [B]: fp32 out, the unsmoothed E.
+ * rem_len [B]: int32 out, or NULL. */
+star_status star_predict(const star_predict_params* p, const void* hidden, const void* w1,
+                         const float* b1, const void* w2, const float* b2,
+                         const float* bin_values, float* ema_state, float* expected_len,
+                         int32_t* rem_len, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * (b) Per-instance predicted load curves.
+ *
+ * Worker-side future-load simulation of Section 4.2's complexity analysis,
+ * over a horizon of H = bucket * n_buckets decode steps grouped in buckets
+ * of `bucket` steps:
+ *     load[i, k] = sum_{t = k*bucket}^{(k+1)*bucket - 1}
+ *                  sum_{r in B_i, t < rem_len[r]} (cur_len[r] + t)
+ * (int64 token-steps; with bucket = 1, load[i, 0] = N_i(B_i)).
+ * cur_len, rem_len, inst_of: int32 [n_req], any order.
+ * load: int64 [n_inst, n_buckets], fully overwritten.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    int32_t n_req;      /* N >= 0 */
+    int32_t n_inst;     /* n >= 1 */
+    int32_t bucket;     /* b >= 1 */
+    int32_t n_buckets;  /* K >= 1; b * K <= 2^30 */
+} star_load_params;
+
+size_t star_project_load_workspace_size(const star_load_params* p);
+
+star_status star_project_load(const star_load_params* p, const int32_t* cur_len,
+                              const int32_t* rem_len, const int32_t* inst_of, int64_t* load,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * (c) Migration candidates scored by projected peak load, and ranked.
+ *
+ * Algorithm 1 (candidate enumeration and best-feasible selection) applied
+ * to every request -> instance pair.  For request r on s = inst_of[r]:
+ *     scores[r, t] = max_k (load[t, k] + R_r[k])   for t != s,
+ *     scores[r, s] = max_k load[s, k]              (staying: r is already in it),
+ * where R_r is r's own bucketed curve as defined in (b).  `load` must be
+ * the curves of these same requests (normally star_project_load's output).
+ * Migrations (t != s) are ranked by the key (score, r, t) ascending:
+ *     best_target[r] / best_score[r]: r's smallest key, or -1 / -1 when r
+ *         has none (n_inst == 1 or r invalid);
+ *     topk_*[q], q < top_k: the q-th smallest key overall, -1 past the end.
+ * Outputs: scores int64 [n_req, n_inst] or NULL; best_target int32 [n_req]
+ * or NULL; best_score int64 [n_req] or NULL; topk_req/topk_tgt int32 and
+ * topk_score int64 [top_k], all three non-NULL iff top_k > 0.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    star_load_params load;  /* same meaning as for star_project_load */
+    int32_t top_k;          /* 0 .. STAR_MAX_TOP_K */
+} star_score_params;
+
+size_t star_score_workspace_size(const star_score_params* p);
+
+star_status star_score_migrations(const star_score_params* p, const int32_t* cur_len,
+                                  const int32_t* rem_len, const int32_t* inst_of,
+                                  const int64_t* load, int64_t* scores, int32_t* best_target,
+                                  int64_t* best_score, int32_t* topk_req, int32_t* topk_tgt,
+                                  int64_t* topk_score, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Housekeeping.
+ * ---------------------------------------------------------------------- */
+/* Zero the workspace header on `stream` (a fill kernel, no memset node). */
+star_status star_workspace_init(void* ws, size_t ws_bytes, void* stream);
+
+/* Synchronise `stream`, return the workspace's device-error word (OR of
+ * STAR_DEV_* bits since the last read) in *code, and clear it. */
+star_status star_read_device_error(void* ws, void* stream, int32_t* code);
+
+const char* star_status_string(star_status s);
+int32_t star_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* STAR_H */

@@ -45,6 +45,11 @@ def _load():
     return _lib
 
 
+def threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().star_oracle_threads())
+
+
 def _ptr(a: Optional[np.ndarray]):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 

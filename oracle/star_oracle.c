@@ -22,6 +22,9 @@
  *            (Eq. 4); request r holds N(r)+t tokens while t < N^(r).
  */
 #include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -253,3 +256,12 @@ int star_oracle_rank(int64_t N, int64_t n, const int32_t* cur, const int32_t* re
 }
 
 int star_oracle_abi_version(void) { return 1; }
+
+/* Threads an OpenMP parallel region of the oracle uses (1 without OpenMP). */
+int star_oracle_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

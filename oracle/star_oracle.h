@@ -62,6 +62,7 @@ int star_oracle_rank(int64_t N, int64_t n, const int32_t* cur_len, const int32_t
                      int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score);
 
 int star_oracle_abi_version(void);
+int star_oracle_threads(void);
 
 #ifdef __cplusplus
 }

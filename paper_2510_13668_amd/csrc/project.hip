@@ -1,0 +1,123 @@
+// (b) Per-instance predicted load curves on gfx950.
+//
+// Section 4.2 (problem formulation, Eq. 4): request r with N(r) = c current
+// tokens and N^(r) = l remaining steps holds c + t tokens at future step
+// t < l.  Over a horizon of H = b K steps in buckets of b steps, with
+// l' = min(l, H), k_e = l' div b and mu = l' mod b, r contributes
+//     b c + b(b-1)/2 + b^2 k          to every full bucket k < k_e,
+//     mu c + mu k_e b + mu(mu-1)/2    to the partial bucket k_e (mu > 0),
+// i.e. sum_{t in bucket}(c + t).  So an instance's curve is
+//     L[k] = S_A(k) + b^2 k S_n(k) + D_P[k],
+// with S_A(k) / S_n(k) the sum of alpha_r = b c + b(b-1)/2 / the count over
+// its requests with k_e > k (suffix sums of histograms indexed by k_e), and
+// D_P the partial-bucket histogram.
+//
+// One workgroup per (instance, bucket chunk): it streams every request
+// (coalesced int32 reads), scatters its own instance's requests into LDS
+// histograms with int64 LDS atomics, runs a block-wide suffix scan and
+// writes its chunk of load[i, :].  Requests whose k_e lies beyond the chunk
+// are folded into one overflow slot, so chunks are independent.
+#include "star_common.hpp"
+#include "star_internal.hpp"
+
+namespace star {
+
+constexpr int PL_THREADS = 512;
+constexpr int PL_CHUNK = 1024;
+
+__global__ __launch_bounds__(PL_THREADS) void project_load_kernel(
+    const int32_t* __restrict__ cur, const int32_t* __restrict__ rem,
+    const int32_t* __restrict__ inst, int N, int n, int b, int K, int chunk,
+    int64_t* __restrict__ load, int32_t* __restrict__ err_word) {
+    __shared__ int64_t hA[PL_CHUNK + 1];   // alpha_r by k_e (slot len: k_e >= chunk end)
+    __shared__ int64_t hN[PL_CHUNK + 1];   // request count by k_e
+    __shared__ int64_t hP[PL_CHUNK];       // partial-bucket contributions
+    __shared__ int64_t tmp[PL_THREADS / 64 + 1];
+
+    const int tid = threadIdx.x;
+    const int i = blockIdx.x;
+    const int c = blockIdx.y;
+    const int64_t k0 = (int64_t)c * chunk;
+    const int64_t k1 = k0 + chunk < K ? k0 + chunk : K;
+    const int len = (int)(k1 - k0);
+    const int64_t H = (int64_t)b * K;
+    const int64_t alpha0 = (int64_t)b * (b - 1) / 2;
+
+    for (int j = tid; j <= len; j += PL_THREADS) {
+        hA[j] = 0;
+        hN[j] = 0;
+        if (j < len) hP[j] = 0;
+    }
+    __syncthreads();
+
+    int32_t bad = 0;
+    for (int r = tid; r < N; r += PL_THREADS) {
+        const int s = inst[r];
+        const int cr = cur[r];
+        const int lr = rem[r];
+        int32_t f = 0;
+        if (s < 0 || s >= n) f |= STAR_DEV_BAD_INST;
+        if (cr < 1) f |= STAR_DEV_BAD_CUR;
+        if (lr < 1) f |= STAR_DEV_BAD_REM;
+        bad |= f;
+        if (f || s != i) continue;
+        const int64_t lp = (int64_t)lr < H ? (int64_t)lr : H;
+        const int64_t ke = lp / b;
+        const int64_t mu = lp - ke * b;
+        if (ke > k0) {
+            const int j = (int)((ke < k1 ? ke : k1) - k0);          // 1..len
+            atomicAdd((unsigned long long*)&hA[j], (unsigned long long)((int64_t)b * cr + alpha0));
+            atomicAdd((unsigned long long*)&hN[j], 1ull);
+        }
+        if (mu > 0 && ke >= k0 && ke < k1) {
+            const int64_t pr = mu * cr + mu * ke * b + mu * (mu - 1) / 2;
+            atomicAdd((unsigned long long*)&hP[ke - k0], (unsigned long long)pr);
+        }
+    }
+    if (i == 0 && c == 0) {
+        bad = wave_or_i32(bad);
+        if ((tid & 63) == 0) report_error(err_word, bad);
+    }
+    __syncthreads();
+
+    // Suffix sums over x[q] = h[q + 1], q in [0, len): thread t owns the
+    // reversed positions p in [t*seg, (t+1)*seg), q = len - 1 - p.
+    const int seg = (len + PL_THREADS - 1) / PL_THREADS;
+    const int p0 = tid * seg;
+    const int p1 = p0 + seg < len ? p0 + seg : len;
+    int64_t la = 0, ln = 0;
+    for (int p = p0; p < p1; ++p) {
+        const int q = len - 1 - p;
+        la += hA[q + 1];
+        ln += hN[q + 1];
+    }
+    int64_t ra = block_exclusive_scan_i64(la, OpAdd(), 0, tmp, (int64_t*)nullptr);
+    int64_t rn = block_exclusive_scan_i64(ln, OpAdd(), 0, tmp, (int64_t*)nullptr);
+    const int64_t bb = (int64_t)b * b;
+    int64_t* out = load + (int64_t)i * K;
+    for (int p = p0; p < p1; ++p) {
+        const int q = len - 1 - p;
+        ra += hA[q + 1];
+        rn += hN[q + 1];
+        const int64_t k = k0 + q;
+        out[k] = ra + bb * k * rn + hP[q];
+    }
+}
+
+LoadPlan plan_load(const star_load_params& p) {
+    LoadPlan pl;
+    pl.chunk = p.n_buckets < PL_CHUNK ? p.n_buckets : PL_CHUNK;
+    pl.n_chunks = (int)ceil_div(p.n_buckets, pl.chunk);
+    return pl;
+}
+
+hipError_t launch_project_load(const star_load_params& p, const LoadPlan& pl, const int32_t* cur,
+                               const int32_t* rem, const int32_t* inst, int64_t* load,
+                               int32_t* err_word, hipStream_t stream) {
+    hipLaunchKernelGGL(project_load_kernel, dim3(p.n_inst, pl.n_chunks), dim3(PL_THREADS), 0,
+                       stream, cur, rem, inst, p.n_req, p.n_inst, p.bucket, p.n_buckets, pl.chunk,
+                       load, err_word);
+    return hipGetLastError();
+}
+
+}  // namespace star

@@ -1,0 +1,202 @@
+// C-ABI of libstar: argument validation, workspace layout and launches.
+// Every check that can be made from scalars happens here, synchronously,
+// before anything is enqueued; see include/star.h for the contract.
+#include <math.h>
+#include <stdint.h>
+
+#include "star_common.hpp"
+#include "star_internal.hpp"
+
+#define STAR_API extern "C" __attribute__((visibility("default")))
+
+namespace star {
+
+__global__ void fill_zero_kernel(uint32_t* p, size_t words) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < words;
+         i += (size_t)gridDim.x * blockDim.x)
+        p[i] = 0u;
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream) {
+    const size_t words = bytes / 4;
+    if (words == 0) return hipSuccess;
+    size_t blocks = (words + 255) / 256;
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       (uint32_t*)p, words);
+    return hipGetLastError();
+}
+
+static bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+static star_status check_ws(const void* ws, size_t ws_bytes, size_t need) {
+    if (!ws || !aligned(ws, 256) || ws_bytes < need) return STAR_ERR_WORKSPACE;
+    return STAR_OK;
+}
+
+static star_status check_load_params(const star_load_params* p) {
+    if (!p) return STAR_ERR_INVALID_ARG;
+    if (p->n_req < 0 || p->n_inst < 1 || p->bucket < 1 || p->n_buckets < 1)
+        return STAR_ERR_INVALID_ARG;
+    const int64_t H = (int64_t)p->bucket * p->n_buckets;
+    if (H > ((int64_t)1 << 30)) return STAR_ERR_UNSUPPORTED;
+    // Every load, score and intermediate is at most (N + 1) b (c_max + H) + b H
+    // with c_max < 2^31; keep that below 2^62.
+    const __int128 bound = (__int128)(p->n_req + 1) * p->bucket * (((__int128)1 << 31) + H) +
+                           (__int128)p->bucket * H;
+    if (bound >= ((__int128)1 << 62)) return STAR_ERR_OVERFLOW;
+    return STAR_OK;
+}
+
+static star_status check_predict_params(const star_predict_params* p) {
+    if (!p) return STAR_ERR_INVALID_ARG;
+    if (p->n_req < 0 || p->d_model < 1 || p->d_hidden < 1 || p->n_bins < 1 || p->len_max < 1)
+        return STAR_ERR_INVALID_ARG;
+    if (p->dtype != STAR_F32 && p->dtype != STAR_BF16) return STAR_ERR_INVALID_ARG;
+    if (p->act != STAR_ACT_RELU && p->act != STAR_ACT_GELU_ERF) return STAR_ERR_INVALID_ARG;
+    if (!(p->ema_alpha >= 0.0f && p->ema_alpha <= 1.0f)) return STAR_ERR_INVALID_ARG;
+    if (p->ema_init != 0 && p->ema_init != 1) return STAR_ERR_INVALID_ARG;
+    const int vec = p->dtype == STAR_BF16 ? 8 : 4;      // elements per 16-byte load
+    if (p->d_model % vec || p->d_hidden % vec) return STAR_ERR_UNSUPPORTED;
+    if (p->d_hidden > 2048 || p->n_bins > 256) return STAR_ERR_UNSUPPORTED;
+    return STAR_OK;
+}
+
+}  // namespace star
+
+using namespace star;
+
+STAR_API int32_t star_abi_version(void) { return STAR_ABI_VERSION; }
+
+STAR_API const char* star_status_string(star_status s) {
+    switch (s) {
+        case STAR_OK: return "STAR_OK";
+        case STAR_ERR_INVALID_ARG: return "STAR_ERR_INVALID_ARG: null pointer, bad size or bad enum";
+        case STAR_ERR_UNSUPPORTED: return "STAR_ERR_UNSUPPORTED: shape or alignment not handled";
+        case STAR_ERR_OVERFLOW: return "STAR_ERR_OVERFLOW: int64 loads could overflow at these sizes";
+        case STAR_ERR_WORKSPACE: return "STAR_ERR_WORKSPACE: workspace null, misaligned or too small";
+        case STAR_ERR_HIP: return "STAR_ERR_HIP: HIP runtime or launch failure";
+    }
+    return "unknown star_status";
+}
+
+// ---------------------------------------------------------------------------
+// predictor
+// ---------------------------------------------------------------------------
+STAR_API size_t star_predict_workspace_size(const star_predict_params* p) {
+    if (check_predict_params(p) != STAR_OK) return 0;
+    return STAR_WS_HEADER_BYTES + align_up(plan_predict(*p).partial_bytes, 256);
+}
+
+STAR_API star_status star_predict(const star_predict_params* p, const void* hidden,
+                                  const void* w1, const float* b1, const void* w2,
+                                  const float* b2, const float* bin_values, float* ema_state,
+                                  float* expected_len, int32_t* rem_len, void* ws,
+                                  size_t ws_bytes, void* stream) {
+    star_status st = check_predict_params(p);
+    if (st != STAR_OK) return st;
+    if (p->n_req > 0) {
+        if (!hidden || !w1 || !w2 || !bin_values || !expected_len) return STAR_ERR_INVALID_ARG;
+        if (p->ema_alpha > 0.0f && !ema_state) return STAR_ERR_INVALID_ARG;
+        if (!aligned(hidden, 16) || !aligned(w1, 16) || !aligned(w2, 16))
+            return STAR_ERR_UNSUPPORTED;
+    }
+    const PredictPlan pl = plan_predict(*p);
+    st = check_ws(ws, ws_bytes, STAR_WS_HEADER_BYTES + align_up(pl.partial_bytes, 256));
+    if (st != STAR_OK) return st;
+    float* partials = (float*)((char*)ws + STAR_WS_HEADER_BYTES);
+    hipError_t e = launch_predict(*p, pl, hidden, w1, b1, w2, b2, bin_values, ema_state,
+                                  expected_len, rem_len, partials, (hipStream_t)stream);
+    return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// load projection
+// ---------------------------------------------------------------------------
+STAR_API size_t star_project_load_workspace_size(const star_load_params* p) {
+    if (check_load_params(p) != STAR_OK) return 0;
+    return STAR_WS_HEADER_BYTES;
+}
+
+STAR_API star_status star_project_load(const star_load_params* p, const int32_t* cur_len,
+                                       const int32_t* rem_len, const int32_t* inst_of,
+                                       int64_t* load, void* ws, size_t ws_bytes, void* stream) {
+    star_status st = check_load_params(p);
+    if (st != STAR_OK) return st;
+    if (!load) return STAR_ERR_INVALID_ARG;
+    if (p->n_req > 0 && (!cur_len || !rem_len || !inst_of)) return STAR_ERR_INVALID_ARG;
+    st = check_ws(ws, ws_bytes, STAR_WS_HEADER_BYTES);
+    if (st != STAR_OK) return st;
+    const LoadPlan pl = plan_load(*p);
+    int32_t* err = (int32_t*)((char*)ws + kHdrErrorWord);
+    hipError_t e = launch_project_load(*p, pl, cur_len, rem_len, inst_of, load, err,
+                                       (hipStream_t)stream);
+    return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// scoring and ranking
+// ---------------------------------------------------------------------------
+static star_status check_score_params(const star_score_params* p) {
+    if (!p) return STAR_ERR_INVALID_ARG;
+    star_status st = check_load_params(&p->load);
+    if (st != STAR_OK) return st;
+    if (p->top_k < 0 || p->top_k > STAR_MAX_TOP_K) return STAR_ERR_INVALID_ARG;
+    if (p->load.n_inst > 4096) return STAR_ERR_UNSUPPORTED;
+    if ((int64_t)p->load.n_req * p->load.n_inst >= ((int64_t)1 << 31)) return STAR_ERR_UNSUPPORTED;
+    return STAR_OK;
+}
+
+STAR_API size_t star_score_workspace_size(const star_score_params* p) {
+    if (check_score_params(p) != STAR_OK) return 0;
+    return plan_score(*p).total;
+}
+
+STAR_API star_status star_score_migrations(const star_score_params* p, const int32_t* cur_len,
+                                           const int32_t* rem_len, const int32_t* inst_of,
+                                           const int64_t* load, int64_t* scores,
+                                           int32_t* best_target, int64_t* best_score,
+                                           int32_t* topk_req, int32_t* topk_tgt,
+                                           int64_t* topk_score, void* ws, size_t ws_bytes,
+                                           void* stream) {
+    star_status st = check_score_params(p);
+    if (st != STAR_OK) return st;
+    if (!load) return STAR_ERR_INVALID_ARG;
+    if (p->load.n_req > 0 && (!cur_len || !rem_len || !inst_of)) return STAR_ERR_INVALID_ARG;
+    const bool any_topk = topk_req || topk_tgt || topk_score;
+    const bool all_topk = topk_req && topk_tgt && topk_score;
+    if (p->top_k > 0 ? !all_topk : any_topk) return STAR_ERR_INVALID_ARG;
+    const ScorePlan pl = plan_score(*p);
+    st = check_ws(ws, ws_bytes, pl.total);
+    if (st != STAR_OK) return st;
+    int32_t* err = (int32_t*)((char*)ws + kHdrErrorWord);
+    hipError_t e = launch_score(*p, pl, cur_len, rem_len, inst_of, load, scores, best_target,
+                                best_score, topk_req, topk_tgt, topk_score, (char*)ws, err,
+                                (hipStream_t)stream);
+    return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// housekeeping
+// ---------------------------------------------------------------------------
+STAR_API star_status star_workspace_init(void* ws, size_t ws_bytes, void* stream) {
+    star_status st = check_ws(ws, ws_bytes, STAR_WS_HEADER_BYTES);
+    if (st != STAR_OK) return st;
+    return launch_fill_zero(ws, STAR_WS_HEADER_BYTES, (hipStream_t)stream) == hipSuccess
+               ? STAR_OK
+               : STAR_ERR_HIP;
+}
+
+STAR_API star_status star_read_device_error(void* ws, void* stream, int32_t* code) {
+    if (!code) return STAR_ERR_INVALID_ARG;
+    if (!ws || !aligned(ws, 256)) return STAR_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    if (hipStreamSynchronize(s) != hipSuccess) return STAR_ERR_HIP;
+    int32_t v = 0;
+    if (hipMemcpy(&v, (char*)ws + kHdrErrorWord, sizeof v, hipMemcpyDeviceToHost) != hipSuccess)
+        return STAR_ERR_HIP;
+    if (launch_fill_zero((char*)ws + kHdrErrorWord, 4, s) != hipSuccess) return STAR_ERR_HIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return STAR_ERR_HIP;
+    *code = v;
+    return STAR_OK;
+}

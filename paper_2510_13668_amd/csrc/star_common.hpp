@@ -1,0 +1,100 @@
+// Internal helpers shared by the gfx950 kernels of libstar.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "star.h"
+
+namespace star {
+
+constexpr int kWave = 64;
+
+// Workspace header layout (STAR_WS_HEADER_BYTES bytes at the start of every
+// workspace).
+constexpr size_t kHdrErrorWord = 0;   // int32: sticky OR of STAR_DEV_* bits
+
+__host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+typedef short bf16x8 __attribute__((ext_vector_type(8)));     // raw bits, 16 bytes
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));  // MFMA operand type
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ inline uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// ---------------------------------------------------------------------------
+// wavefront reductions (64 lanes)
+// ---------------------------------------------------------------------------
+__device__ inline float wave_max_f32(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+__device__ inline float wave_sum_f32(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+__device__ inline int32_t wave_or_i32(int32_t v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o, kWave);
+    return v;
+}
+
+// Inclusive scan across the wave (lane order), for a commutative,
+// associative op on int64.
+template <class Op>
+__device__ inline int64_t wave_inclusive_scan_i64(int64_t v, Op op) {
+    const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        int64_t u = __shfl_up(v, o, kWave);
+        if (lane >= o) v = op(v, u);
+    }
+    return v;
+}
+
+struct OpAdd { __device__ int64_t operator()(int64_t a, int64_t b) const { return a + b; } };
+struct OpMax { __device__ int64_t operator()(int64_t a, int64_t b) const { return a > b ? a : b; } };
+
+// Block-wide exclusive scan of one int64 per thread (thread order), using
+// `tmp` (>= blockDim/64 + 1 int64 of LDS).  Returns the exclusive prefix;
+// *total receives the block aggregate.  `ident` is the op's identity.
+template <class Op>
+__device__ inline int64_t block_exclusive_scan_i64(int64_t v, Op op, int64_t ident,
+                                                   int64_t* tmp, int64_t* total) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wid = threadIdx.x / kWave;
+    const int nw = (blockDim.x + kWave - 1) / kWave;
+    int64_t inc = wave_inclusive_scan_i64(v, op);
+    if (lane == kWave - 1) tmp[wid] = inc;
+    __syncthreads();
+    if (wid == 0) {
+        int64_t w = lane < nw ? tmp[lane] : ident;
+        int64_t wi = wave_inclusive_scan_i64(w, op);
+        if (lane < nw) tmp[lane] = wi;              // inclusive totals per wave
+    }
+    __syncthreads();
+    int64_t before = wid > 0 ? tmp[wid - 1] : ident;
+    int64_t excl_in_wave = __shfl_up(inc, 1, kWave);
+    if (lane == 0) excl_in_wave = ident;
+    int64_t res = op(before, excl_in_wave);
+    if (total) *total = tmp[nw - 1];
+    __syncthreads();
+    return res;
+}
+
+// Device-error reporting: OR `bits` into the workspace error word.
+__device__ inline void report_error(int32_t* err_word, int32_t bits) {
+    if (bits) atomicOr(err_word, bits);
+}
+
+}  // namespace star

@@ -1,0 +1,48 @@
+// Internal launch interfaces between the C-ABI layer and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "star.h"
+
+namespace star {
+
+struct PredictPlan {
+    int tiles_m = 0, tiles_n = 0, ktiles = 0, splits = 1;
+    size_t partial_bytes = 0;   // fp32 split-K partials [splits, B, m]
+    size_t head_lds = 0;        // dynamic LDS of the head kernel
+};
+PredictPlan plan_predict(const star_predict_params& p);
+hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, const void* hidden,
+                          const void* w1, const float* b1, const void* w2, const float* b2,
+                          const float* bins, float* ema_state, float* expected, int32_t* rem_len,
+                          float* partials, hipStream_t stream);
+
+struct LoadPlan {
+    int chunk = 0;       // buckets per workgroup
+    int n_chunks = 0;
+};
+LoadPlan plan_load(const star_load_params& p);
+hipError_t launch_project_load(const star_load_params& p, const LoadPlan& pl,
+                               const int32_t* cur, const int32_t* rem, const int32_t* inst,
+                               int64_t* load, int32_t* err_word, hipStream_t stream);
+
+struct ScorePlan {
+    int rpb = 0;          // requests per scoring workgroup
+    int groups = 0;       // scoring workgroups
+    int sort_n = 0;       // local sort size (power of two)
+    int kp = 0;           // padded top-k list length (power of two), 0 if top_k == 0
+    size_t pm_off = 0, sm_off = 0, list_s_off = 0, list_i_off = 0, total = 0;
+};
+ScorePlan plan_score(const star_score_params& p);
+hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const int32_t* cur,
+                        const int32_t* rem, const int32_t* inst, const int64_t* load,
+                        int64_t* scores, int32_t* best_target, int64_t* best_score,
+                        int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score, char* ws,
+                        int32_t* err_word, hipStream_t stream);
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
+
+}  // namespace star

@@ -1,0 +1,194 @@
+"""Python binding of libstar (ctypes; argument marshalling only).
+
+Every function here forwards torch tensors' device pointers and the current
+HIP stream to the C-ABI entry point of the same name in ``libstar.so``; all
+arithmetic runs in the library's gfx950 kernels.  There is no fallback: if
+the library is missing, importing the binding's entry points raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libstar.so")
+
+STAR_OK = 0
+STAR_WS_HEADER_BYTES = 256
+STAR_MAX_TOP_K = 1024
+F32, BF16 = 0, 1
+ACT_RELU, ACT_GELU = 0, 1
+DEV_BAD_INST, DEV_BAD_CUR, DEV_BAD_REM = 1, 2, 4
+
+_i32 = ctypes.c_int32
+_P = ctypes.c_void_p
+
+
+class PredictParams(ctypes.Structure):
+    _fields_ = [("n_req", _i32), ("d_model", _i32), ("d_hidden", _i32), ("n_bins", _i32),
+                ("dtype", _i32), ("act", _i32), ("ema_alpha", ctypes.c_float),
+                ("ema_init", _i32), ("len_max", _i32), ("timing_events", _P)]
+
+
+class LoadParams(ctypes.Structure):
+    _fields_ = [("n_req", _i32), ("n_inst", _i32), ("bucket", _i32), ("n_buckets", _i32)]
+
+
+class ScoreParams(ctypes.Structure):
+    _fields_ = [("load", LoadParams), ("top_k", _i32)]
+
+
+class StarError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn}: {msg} ({status})")
+        self.status = status
+
+
+class StarLibraryMissing(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libstar.so (raises StarLibraryMissing if it was not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise StarLibraryMissing(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2510_13668_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.star_abi_version.restype = _i32
+        L.star_status_string.restype = ctypes.c_char_p
+        L.star_status_string.argtypes = [ctypes.c_int]
+        L.star_predict_workspace_size.restype = ctypes.c_size_t
+        L.star_predict_workspace_size.argtypes = [ctypes.POINTER(PredictParams)]
+        L.star_project_load_workspace_size.restype = ctypes.c_size_t
+        L.star_project_load_workspace_size.argtypes = [ctypes.POINTER(LoadParams)]
+        L.star_score_workspace_size.restype = ctypes.c_size_t
+        L.star_score_workspace_size.argtypes = [ctypes.POINTER(ScoreParams)]
+        L.star_predict.restype = ctypes.c_int
+        L.star_predict.argtypes = [ctypes.POINTER(PredictParams)] + [_P] * 10 + [ctypes.c_size_t, _P]
+        L.star_project_load.restype = ctypes.c_int
+        L.star_project_load.argtypes = [ctypes.POINTER(LoadParams)] + [_P] * 5 + [ctypes.c_size_t, _P]
+        L.star_score_migrations.restype = ctypes.c_int
+        L.star_score_migrations.argtypes = ([ctypes.POINTER(ScoreParams)] + [_P] * 11 +
+                                            [ctypes.c_size_t, _P])
+        L.star_workspace_init.restype = ctypes.c_int
+        L.star_workspace_init.argtypes = [_P, ctypes.c_size_t, _P]
+        L.star_read_device_error.restype = ctypes.c_int
+        L.star_read_device_error.argtypes = [_P, _P, ctypes.POINTER(_i32)]
+        _lib = L
+    return _lib
+
+
+def _check(fn: str, st: int):
+    if st != STAR_OK:
+        raise StarError(fn, st, lib().star_status_string(st).decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libstar must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None and t.device.type != "cuda":
+            raise ValueError("libstar takes device tensors")
+
+
+# ---------------------------------------------------------------------------
+# workspace
+# ---------------------------------------------------------------------------
+class Workspace:
+    """Caller-owned device workspace (header zeroed on creation)."""
+
+    def __init__(self, nbytes: int, device=None, stream=None):
+        nbytes = max(int(nbytes), STAR_WS_HEADER_BYTES)
+        self.buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device or "cuda")
+        off = (-self.buf.data_ptr()) % 256
+        self.ptr = self.buf.data_ptr() + off
+        self.nbytes = nbytes
+        _check("star_workspace_init", lib().star_workspace_init(ctypes.c_void_p(self.ptr),
+                                                                 self.nbytes, _stream(stream)))
+
+    def read_device_error(self, stream=None) -> int:
+        code = _i32(0)
+        _check("star_read_device_error",
+               lib().star_read_device_error(ctypes.c_void_p(self.ptr), _stream(stream),
+                                            ctypes.byref(code)))
+        return code.value
+
+
+# ---------------------------------------------------------------------------
+# (a) predictor
+# ---------------------------------------------------------------------------
+def predict_params(n_req, d_model, d_hidden, n_bins, dtype, act, ema_alpha=0.0, ema_init=False,
+                   len_max=1 << 30, timing_events=None) -> PredictParams:
+    return PredictParams(n_req, d_model, d_hidden, n_bins, dtype, act, float(ema_alpha),
+                         int(bool(ema_init)), int(len_max), timing_events)
+
+
+def predict_workspace_size(p: PredictParams) -> int:
+    return lib().star_predict_workspace_size(ctypes.byref(p))
+
+
+def predict(p: PredictParams, hidden, w1, b1, w2, b2, bin_values, ema_state, expected_len,
+            rem_len, ws: Workspace, stream=None):
+    _dev(hidden, w1, b1, w2, b2, bin_values, ema_state, expected_len, rem_len)
+    _check("star_predict", lib().star_predict(
+        ctypes.byref(p), _ptr(hidden), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
+        _ptr(bin_values), _ptr(ema_state), _ptr(expected_len), _ptr(rem_len),
+        ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# (b) load projection
+# ---------------------------------------------------------------------------
+def load_params(n_req, n_inst, bucket, n_buckets) -> LoadParams:
+    return LoadParams(n_req, n_inst, bucket, n_buckets)
+
+
+def project_load_workspace_size(p: LoadParams) -> int:
+    return lib().star_project_load_workspace_size(ctypes.byref(p))
+
+
+def project_load(p: LoadParams, cur_len, rem_len, inst_of, load, ws: Workspace, stream=None):
+    _dev(cur_len, rem_len, inst_of, load)
+    _check("star_project_load", lib().star_project_load(
+        ctypes.byref(p), _ptr(cur_len), _ptr(rem_len), _ptr(inst_of), _ptr(load),
+        ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# (c) scoring and ranking
+# ---------------------------------------------------------------------------
+def score_params(n_req, n_inst, bucket, n_buckets, top_k) -> ScoreParams:
+    return ScoreParams(LoadParams(n_req, n_inst, bucket, n_buckets), top_k)
+
+
+def score_workspace_size(p: ScoreParams) -> int:
+    return lib().star_score_workspace_size(ctypes.byref(p))
+
+
+def score_migrations(p: ScoreParams, cur_len, rem_len, inst_of, load, scores, best_target,
+                     best_score, topk_req, topk_tgt, topk_score, ws: Workspace, stream=None):
+    _dev(cur_len, rem_len, inst_of, load, scores, best_target, best_score, topk_req, topk_tgt,
+         topk_score)
+    _check("star_score_migrations", lib().star_score_migrations(
+        ctypes.byref(p), _ptr(cur_len), _ptr(rem_len), _ptr(inst_of), _ptr(load), _ptr(scores),
+        _ptr(best_target), _ptr(best_score), _ptr(topk_req), _ptr(topk_tgt), _ptr(topk_score),
+        ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))

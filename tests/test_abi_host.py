@@ -1,0 +1,124 @@
+"""Host-side contract of libstar.so: symbols and synchronous validation.
+
+No test here launches a kernel: every call below is rejected by the scalar
+checks that run before anything is enqueued, so the suite runs without a GPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2510_13668_amd import star
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "star.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(star.LIB_PATH):
+        from paper_2510_13668_amd import build
+        build.build()
+    return star.lib()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(star_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared_functions()
+    assert {"star_predict", "star_project_load", "star_score_migrations"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_abi_version_and_status_strings(L):
+    assert L.star_abi_version() == 1
+    for s in (0, -1, -2, -3, -4, -5):
+        assert L.star_status_string(s).decode().startswith("STAR_")
+    assert b"unknown" in L.star_status_string(-99)
+
+
+def _pp(**kw):
+    base = dict(n_req=1024, d_model=4096, d_hidden=512, n_bins=64, dtype=star.BF16,
+                act=star.ACT_GELU, ema_alpha=0.2, ema_init=False, len_max=16384)
+    base.update(kw)
+    return star.predict_params(**base)
+
+
+FAKE = ctypes.c_void_p(1 << 20)   # never dereferenced: validation fails first
+
+
+def _predict(L, p, ws_bytes=1 << 30, ws=FAKE, **ptrs):
+    args = {k: FAKE for k in ("hidden", "w1", "w2", "bins", "ema", "expected")}
+    args.update(ptrs)
+    return L.star_predict(ctypes.byref(p) if p is not None else None, args["hidden"], args["w1"],
+                          None, args["w2"], None, args["bins"], args["ema"], args["expected"],
+                          None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_req=-1), -1), (dict(d_model=0), -1), (dict(d_hidden=0), -1), (dict(n_bins=0), -1),
+    (dict(dtype=7), -1), (dict(act=3), -1), (dict(ema_alpha=1.5), -1),
+    (dict(ema_alpha=float("nan")), -1), (dict(len_max=0), -1),
+    (dict(d_model=4100), -2), (dict(d_hidden=3000), -2), (dict(n_bins=300), -2),
+    (dict(d_hidden=516), -2),
+])
+def test_predict_rejects_bad_scalars(L, kw, status):
+    assert _predict(L, _pp(**kw)) == status
+
+
+def test_predict_rejects_null_pointers_and_workspace(L):
+    assert _predict(L, None) == -1
+    assert _predict(L, _pp(), hidden=None) == -1
+    assert _predict(L, _pp(ema_alpha=0.2), ema=None) == -1
+    assert _predict(L, _pp(), hidden=ctypes.c_void_p((1 << 20) + 2)) == -2   # misaligned
+    p = _pp()
+    need = star.predict_workspace_size(p)
+    # 8 K-splits of a [1024, 512] fp32 partial product plus the header
+    assert need == 256 + 8 * 1024 * 512 * 4
+    assert _predict(L, p, ws_bytes=need - 1) == -4
+    assert _predict(L, p, ws=None) == -4
+    assert _predict(L, p, ws=ctypes.c_void_p((1 << 20) + 64)) == -4   # not 256-aligned
+
+
+def test_load_and_score_validation(L):
+    lp = star.load_params(1024, 8, 64, 256)
+    assert star.project_load_workspace_size(lp) == 256
+    f = FAKE
+    assert L.star_project_load(ctypes.byref(star.load_params(1, 0, 1, 1)), f, f, f, f, f, 256, None) == -1
+    assert L.star_project_load(ctypes.byref(star.load_params(1, 1, 0, 1)), f, f, f, f, f, 256, None) == -1
+    assert L.star_project_load(ctypes.byref(lp), None, f, f, f, f, 256, None) == -1
+    assert L.star_project_load(ctypes.byref(lp), f, f, f, None, f, 256, None) == -1
+    assert L.star_project_load(ctypes.byref(lp), f, f, f, f, f, 255, None) == -4
+    # horizon above 2^30 steps
+    assert L.star_project_load(ctypes.byref(star.load_params(1, 1, 1 << 16, 1 << 15)), f, f, f, f, f,
+                               256, None) == -2
+    # (N+1) b (2^31 + H) >= 2^62
+    big = star.load_params(1 << 26, 8, 64, 256)
+    assert L.star_project_load(ctypes.byref(big), f, f, f, f, f, 256, None) == -3
+
+    sp = star.score_params(1024, 8, 64, 256, 256)
+    need = star.score_workspace_size(sp)
+    assert need > 256
+    args = [f] * 10
+    assert L.star_score_migrations(ctypes.byref(sp), *args, f, need - 1, None) == -4
+    nk = star.score_params(1024, 8, 64, 256, 0)
+    # top-k outputs must be NULL iff top_k == 0
+    assert L.star_score_migrations(ctypes.byref(nk), *args, f, 1 << 30, None) == -1
+    assert L.star_score_migrations(ctypes.byref(sp), *args[:7], None, f, f, f, 1 << 30, None) == -1
+    assert L.star_score_migrations(ctypes.byref(star.score_params(4, 2, 1, 1, 2000)), *args, f,
+                                   1 << 30, None) == -1
+    assert L.star_score_migrations(ctypes.byref(star.score_params(4, 5000, 1, 1, 1)), *args, f,
+                                   1 << 30, None) == -2
+
+
+def test_read_device_error_rejects_bad_args(L):
+    code = ctypes.c_int32(0)
+    assert L.star_read_device_error(FAKE, None, None) == -1
+    assert L.star_read_device_error(None, None, ctypes.byref(code)) == -4
+    assert L.star_workspace_init(FAKE, 100, None) == -4

@@ -1,0 +1,169 @@
+"""GPU parity of (a), the predictor head, against the fp64 oracle.
+
+Bar: expected lengths within 2e-2 relative on every checked row; rem_len
+within that tolerance plus one rounding step (round-half-even of nearly equal
+values may land on different integers).  Small shapes are checked row by row
+in full; the full-size workloads are checked on sampled rows (rows are
+independent), in the launch configuration the benchmark uses.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2510_13668_amd import synth
+from gpu_util import Predictor, assert_lengths_close, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _check_rem(rem_gpu, y_ref, len_max):
+    ref = np.clip(np.rint(y_ref), 1, len_max)
+    assert np.all(np.abs(rem_gpu - ref) <= 0.02 * ref + 1), "rem_len"
+    assert rem_gpu.min() >= 1 and rem_gpu.max() <= len_max
+
+
+def _run_case(hidden, w1, w2, bins, *, dtype, act, b1=None, b2=None, len_max, sample=None):
+    B = hidden.shape[0]
+    pr = Predictor(w1, w2, bins, dtype=dtype, act=act, b1=b1, b2=b2, n_req=B, len_max=len_max)
+    pr.run(to_dev(hidden, dtype == synth.BF16))
+    torch.cuda.synchronize()
+    e_gpu = pr.expected.cpu().numpy()
+    rem_gpu = pr.rem.cpu().numpy()
+    rows = np.arange(B) if sample is None else sample
+    ref = oracle.predict(hidden[rows], w1, w2, bins, dtype=dtype, act=act, b1=b1, b2=b2,
+                         len_max=len_max)
+    err = assert_lengths_close(e_gpu[rows], ref["expected"])
+    _check_rem(rem_gpu[rows], ref["expected"], len_max)
+    return err
+
+
+@pytest.mark.parametrize("with_bias", [False, True])
+def test_tiny_fp32_relu_all_rows(with_bias):
+    wl = synth.WORKLOADS["tiny"]
+    x = synth.make_inputs(wl, with_bias=with_bias)
+    print(f"tiny fp32 bias={with_bias}", flush=True)
+    err = _run_case(x.hidden, x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, b1=x.b1,
+                    b2=x.b2, len_max=wl.len_max)
+    assert err < 1e-4          # fp32 operands, fp32 accumulation
+
+
+@pytest.mark.parametrize("with_bias", [False, True])
+def test_8b_batch_bf16_all_rows(with_bias):
+    wl = synth.WORKLOADS["8b_batch"]
+    x = synth.make_inputs(wl, with_bias=with_bias)
+    print(f"8b_batch bias={with_bias}", flush=True)
+    _run_case(x.hidden, x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, b1=x.b1, b2=x.b2,
+              len_max=wl.len_max)
+
+
+def test_peaky_softmax_bf16():
+    """W2 scaled 16x: logits far from flat stress max-subtraction and exp."""
+    wl = synth.WORKLOADS["8b_batch"]
+    x = synth.make_inputs(wl, with_bias=True, w2_scale=16.0)
+    print("8b_batch peaky", flush=True)
+    _run_case(x.hidden, x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, b1=x.b1, b2=x.b2,
+              len_max=wl.len_max)
+
+
+@pytest.mark.parametrize("dtype,act,B,d,m,nb", [
+    (synth.BF16, synth.ACT_GELU, 100, 136, 72, 20),     # ragged rows, K tail, m tail, bins
+    (synth.BF16, synth.ACT_RELU, 1, 8, 8, 1),           # minimal
+    (synth.BF16, synth.ACT_GELU, 300, 4096, 520, 256),  # several tiles, max bins
+    (synth.BF16, synth.ACT_GELU, 17, 64, 2048, 33),     # max hidden width
+    (synth.F32, synth.ACT_RELU, 100, 132, 76, 20),
+    (synth.F32, synth.ACT_GELU, 129, 1028, 260, 64),
+])
+def test_ragged_shapes(dtype, act, B, d, m, nb):
+    rng = np.random.default_rng(B * 7 + d + m + nb)
+    h = rng.standard_normal((B, d)).astype(np.float32)
+    w1 = (rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32)
+    w2 = (rng.standard_normal((nb, m)) * 4 / np.sqrt(m)).astype(np.float32)
+    b1 = (rng.standard_normal(m) * 0.1).astype(np.float32)
+    b2 = (rng.standard_normal(nb) * 0.1).astype(np.float32)
+    if dtype == synth.BF16:
+        h, w1, w2 = (synth.f32_to_bf16_bits(a) for a in (h, w1, w2))
+    bins = synth.bin_values(nb, 1.0, 32768.0)
+    print(f"ragged dtype={dtype} B={B} d={d} m={m} nb={nb}", flush=True)
+    _run_case(h, w1, w2, bins, dtype=dtype, act=act, b1=b1, b2=b2, len_max=32768)
+
+
+def test_empty_batch():
+    wl = synth.WORKLOADS["8b_batch"]
+    rng = np.random.default_rng(0)
+    w1 = synth.f32_to_bf16_bits(rng.standard_normal((64, 64)).astype(np.float32))
+    w2 = synth.f32_to_bf16_bits(rng.standard_normal((8, 64)).astype(np.float32))
+    pr = Predictor(w1, w2, synth.bin_values(8, 1, 100), dtype=synth.BF16, act=synth.ACT_GELU,
+                   n_req=0, len_max=100)
+    pr.run(torch.empty((0, 64), dtype=torch.bfloat16, device="cuda"))
+    torch.cuda.synchronize()
+    assert wl is not None
+
+
+@pytest.mark.parametrize("name", ["32b_long_mix", "rebalance_scan"])
+def test_full_size_sampled_rows(name):
+    wl = synth.WORKLOADS[name]
+    x = synth.make_inputs(wl)
+    rng = np.random.default_rng(99)
+    sample = np.sort(np.concatenate([rng.choice(wl.n_req, 200, replace=False),
+                                     [0, wl.n_req - 1]]))
+    print(f"{name} full size, {len(sample)} sampled rows", flush=True)
+    _run_case(x.hidden, x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act,
+              len_max=wl.len_max, sample=sample)
+
+
+def test_continuous_mode_ema_200_steps():
+    """AR(1) hidden states over 200 decode steps, EMA alpha = 0.2: E and the
+    smoothed state within 2e-2 at every step on sampled rows."""
+    wl = synth.WORKLOADS["continuous"]
+    x = synth.make_inputs(wl)
+    S = x.hidden.shape[0]
+    rows = np.array([0, 1, 127, 128, 500, 777, 1022, 1023])
+    pr = Predictor(x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, n_req=wl.n_req,
+                   len_max=wl.len_max, ema_alpha=wl.ema_alpha)
+    state = np.zeros(len(rows), np.float64)
+    worst = 0.0
+    hid_dev = to_dev(x.hidden, True)
+    print(f"continuous {S} steps", flush=True)
+    for s in range(S):
+        pr.run(hid_dev[s], ema_init=(s == 0))
+        torch.cuda.synchronize()
+        ref = oracle.predict(x.hidden[s][rows], x.w1, x.w2, x.bin_values, dtype=wl.dtype,
+                             act=wl.act, ema_alpha=wl.ema_alpha, ema_init=(s == 0),
+                             ema_state=state, len_max=wl.len_max)
+        worst = max(worst, assert_lengths_close(pr.expected.cpu().numpy()[rows], ref["expected"]))
+        worst = max(worst, assert_lengths_close(pr.ema.cpu().numpy()[rows], state, what="ema"))
+        _check_rem(pr.rem.cpu().numpy()[rows], state, wl.len_max)
+    print(f"continuous worst rel err {worst:.3e}", flush=True)
+
+
+def test_deterministic_and_resumable():
+    """Two runs are bit-identical; 3 steps + restored EMA state + 3 steps equals
+    6 straight steps bit for bit."""
+    wl = synth.WORKLOADS["continuous"]
+    x = synth.make_inputs(wl, steps=6)
+    hid = to_dev(x.hidden, True)
+    outs = []
+    for _ in range(2):
+        pr = Predictor(x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, n_req=wl.n_req,
+                       len_max=wl.len_max, ema_alpha=wl.ema_alpha)
+        for s in range(6):
+            pr.run(hid[s], ema_init=(s == 0))
+        outs.append((pr.expected.cpu().numpy().copy(), pr.ema.cpu().numpy().copy(),
+                     pr.rem.cpu().numpy().copy()))
+        if _ == 0:
+            saved = None
+    for a, b in zip(*outs):
+        np.testing.assert_array_equal(a, b)
+    pr = Predictor(x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, n_req=wl.n_req,
+                   len_max=wl.len_max, ema_alpha=wl.ema_alpha)
+    for s in range(3):
+        pr.run(hid[s], ema_init=(s == 0))
+    saved = pr.ema.cpu().clone()
+    pr2 = Predictor(x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, n_req=wl.n_req,
+                    len_max=wl.len_max, ema_alpha=wl.ema_alpha)
+    pr2.ema.copy_(saved.to("cuda"))
+    for s in range(3, 6):
+        pr2.run(hid[s])
+    np.testing.assert_array_equal(pr2.ema.cpu().numpy(), outs[0][1])
+    np.testing.assert_array_equal(pr2.rem.cpu().numpy(), outs[0][2])

@@ -1,0 +1,210 @@
+"""GPU parity of (b) load projection and (c) scoring/ranking against the
+oracle: bit-exact load curves, scores, best targets and top-k triples, at the
+five workloads' full sizes and on adversarial inputs; plus the chained round
+(a) -> (b) -> (c), device-error reporting and HIP-graph replay."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2510_13668_amd import star, synth
+from gpu_util import Predictor, Rescheduler, assert_round_equal, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_round(cur, rem, inst, n, b, K, top_k, want_scores=True):
+    rs = Rescheduler(len(cur), n, b, K, top_k, want_scores)
+    rs.run(to_dev(cur), to_dev(rem), to_dev(inst))
+    out = rs.result()
+    out["error"] = rs.ws_load.read_device_error() | rs.ws_score.read_device_error()
+    return out
+
+
+def _check(cur, rem, inst, n, b, K, top_k, want_scores=True):
+    print(f"round N={len(cur)} n={n} b={b} K={K} top_k={top_k}", flush=True)
+    gpu = _gpu_round(cur, rem, inst, n, b, K, top_k, want_scores)
+    ref = oracle.round_(cur, rem, inst, n_inst=n, bucket=b, n_buckets=K, top_k=top_k)
+    assert_round_equal(gpu, ref)
+    assert gpu["error"] == ref["flags"]
+    return gpu, ref
+
+
+@pytest.mark.parametrize("name", ["8b_batch", "32b_long_mix", "continuous", "rebalance_scan"])
+def test_workload_true_lengths(name):
+    """Oracle-predictor mode: the workload's true remaining lengths."""
+    wl = synth.WORKLOADS[name]
+    x = synth.make_inputs(wl, steps=1, n_req=1)
+    _check(x.cur_len, x.true_len, x.inst_of, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k)
+
+
+def test_long_output_stress_mix():
+    rng = np.random.default_rng(5)
+    N, n = 4096, 16
+    rem = synth.draw_true_len(rng, "long_output_stress", N, 32768)
+    cur = rng.integers(1, 32768, size=N, endpoint=True).astype(np.int32)
+    inst = rng.integers(0, n, size=N).astype(np.int32)
+    _check(cur, rem, inst, n, 64, 512, 256)
+
+
+def test_tiny_chained_from_gpu_prediction():
+    """(a) -> (b) -> (c) on the tiny workload; the oracle's (b)(c) consume the
+    GPU's integer rem_len, the bit-exact contract for chained rounds."""
+    wl = synth.WORKLOADS["tiny"]
+    x = synth.make_inputs(wl)
+    pr = Predictor(x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, n_req=wl.n_req,
+                   len_max=wl.len_max)
+    pr.run(to_dev(x.hidden))
+    rem_dev = pr.rem
+    rs = Rescheduler(wl.n_req, wl.n_inst, wl.bucket, wl.n_buckets, min(256, wl.n_req * 3))
+    cur_dev, inst_dev = to_dev(x.cur_len), to_dev(x.inst_of)
+    rs.run(cur_dev, rem_dev, inst_dev)
+    gpu = rs.result()
+    rem = pr.rem.cpu().numpy()
+    ref = oracle.round_(x.cur_len, rem, x.inst_of, n_inst=wl.n_inst, bucket=wl.bucket,
+                        n_buckets=wl.n_buckets, top_k=min(256, wl.n_req * 3))
+    assert_round_equal(gpu, ref)
+
+
+def test_continuous_chained_steps():
+    """Continuous mode: cur_len grows by one token per decode step; (b)(c) on
+    the GPU's own predictions, ten steps."""
+    wl = synth.WORKLOADS["continuous"]
+    x = synth.make_inputs(wl, steps=10)
+    pr = Predictor(x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, n_req=wl.n_req,
+                   len_max=wl.len_max, ema_alpha=wl.ema_alpha)
+    rs = Rescheduler(wl.n_req, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k)
+    hid = to_dev(x.hidden, True)
+    inst_dev = to_dev(x.inst_of)
+    for s in range(10):
+        cur = (x.cur_len + s).astype(np.int32)
+        pr.run(hid[s], ema_init=(s == 0))
+        rs.run(to_dev(cur), pr.rem, inst_dev)
+        gpu = rs.result()
+        ref = oracle.round_(cur, pr.rem.cpu().numpy(), x.inst_of, n_inst=wl.n_inst,
+                            bucket=wl.bucket, n_buckets=wl.n_buckets, top_k=wl.top_k)
+        assert_round_equal(gpu, ref)
+
+
+ADVERSARIAL = [
+    # (label, N, n, b, K, top_k, cur_hi, len_hi, contiguous, empty_inst)
+    ("shuffled", 700, 8, 64, 256, 256, 8192, 20000, False, 0),
+    ("uneven_empty", 300, 9, 16, 100, 64, 4000, 2500, False, 4),
+    ("unit_buckets_long_K", 200, 4, 1, 4096, 256, 2048, 5000, False, 0),
+    ("ragged_chunks", 150, 3, 1, 3000, 100, 500, 3500, False, 0),
+    ("single_bucket", 400, 6, 7, 1, 512, 9000, 30, False, 0),
+    ("unit_horizon", 128, 5, 1, 1, 77, 3000, 3, False, 0),
+    ("one_instance", 50, 1, 4, 10, 8, 100, 60, True, 0),
+    ("more_topk_than_candidates", 10, 3, 2, 5, 1000, 50, 12, False, 0),
+    ("no_topk", 333, 7, 32, 64, 0, 5000, 3000, False, 0),
+    ("topk_one", 333, 7, 32, 64, 1, 5000, 3000, False, 0),
+    ("many_instances", 600, 300, 8, 40, 1024, 3000, 400, False, 0),
+    ("big_bucket", 64, 4, 1000, 3, 16, 100000, 5000, True, 0),
+]
+
+
+@pytest.mark.parametrize("case", ADVERSARIAL, ids=[c[0] for c in ADVERSARIAL])
+def test_adversarial(case):
+    label, N, n, b, K, top_k, cur_hi, len_hi, contiguous, empty = case
+    rng = np.random.default_rng(zlib.crc32(label.encode()))
+    cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=cur_hi, len_hi=len_hi,
+                                           contiguous=contiguous, empty_inst=empty)
+    H = b * K
+    # lengths at and around the horizon and bucket boundaries
+    special = np.array([1, b, 2 * b, H - 1, H, H + 1, 3 * H], np.int64)
+    m = min(len(special), N)
+    rem[:m] = np.clip(special[:m], 1, 2 ** 31 - 1).astype(np.int32)
+    _check(cur, rem, inst, n, b, K, top_k)
+
+
+def test_ties_from_duplicated_requests():
+    rng = np.random.default_rng(3)
+    N, n = 256, 8
+    cur = np.full(N, 1000, np.int32)
+    rem = np.full(N, 777, np.int32)
+    inst = rng.integers(0, n, N).astype(np.int32)
+    cur[::3] = 5
+    rem[::5] = 64
+    _check(cur, rem, inst, n, 64, 32, 300)
+
+
+def test_invalid_requests_are_skipped_and_reported():
+    rng = np.random.default_rng(4)
+    N, n = 500, 6
+    cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=3000, len_hi=3000)
+    inst[10] = n          # out of range
+    inst[11] = -1
+    cur[20] = 0
+    rem[30] = 0
+    rem[31] = -5
+    gpu, ref = _check(cur, rem, inst, n, 64, 64, 128)
+    assert gpu["error"] == star.DEV_BAD_INST | star.DEV_BAD_CUR | star.DEV_BAD_REM
+    assert (gpu["best_target"][[10, 11, 20, 30, 31]] == -1).all()
+
+
+def test_empty_request_set():
+    gpu = _gpu_round(np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32),
+                     4, 8, 16, 10)
+    assert (gpu["load"] == 0).all()
+    assert (gpu["topk_req"] == -1).all()
+
+
+def test_error_word_clears_after_read():
+    rs = Rescheduler(4, 2, 1, 4, 2)
+    bad = to_dev(np.array([0, 5, 1, 1], np.int32))
+    ok = to_dev(np.array([1, 1, 1, 1], np.int32))
+    rs.run(ok, ok, bad)
+    assert rs.ws_load.read_device_error() == star.DEV_BAD_INST
+    assert rs.ws_load.read_device_error() == 0
+    rs.run(ok, ok, to_dev(np.array([0, 1, 1, 0], np.int32)))
+    assert rs.ws_load.read_device_error() == 0
+
+
+def test_graph_replay_matches_eager():
+    """The continuous-mode round captured once as a HIP graph and replayed
+    several times, with eager work and synchronisations in between; every
+    replay equals the eager result."""
+    wl = synth.WORKLOADS["continuous"]
+    x = synth.make_inputs(wl, steps=3)
+    hid = to_dev(x.hidden, True)
+    pr = Predictor(x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, n_req=wl.n_req,
+                   len_max=wl.len_max, ema_alpha=wl.ema_alpha)
+    rs = Rescheduler(wl.n_req, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k)
+    cur = to_dev(x.cur_len)
+    inst = to_dev(x.inst_of)
+    src = hid[1].clone()
+
+    def step(s):
+        pr.run(src, stream=s)
+        rs.run(cur, pr.rem, inst, stream=s)
+
+    # eager reference from a known EMA state
+    pr.run(hid[0], ema_init=True)
+    ema0 = pr.ema.clone()
+    step(None)
+    torch.cuda.synchronize()
+    want = rs.result()
+    want_ema = pr.ema.cpu().numpy().copy()
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        pr.ema.copy_(ema0)
+        step(s)          # warm-up on the capture stream
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=s):
+        step(s)
+    for rep in range(4):
+        pr.ema.copy_(ema0)
+        rs.load.fill_(-7)
+        rs.best_target.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = rs.result()
+        assert_round_equal(got, want)
+        np.testing.assert_array_equal(pr.ema.cpu().numpy(), want_ema)
+        _ = torch.ones(1000, device="cuda").sum().item()    # unrelated eager work between replays
