@@ -19,11 +19,12 @@
  *     kernels on `stream` (a hipStream_t; NULL = the null stream) and
  *     return.  Results are valid once the stream has reached that point.
  *   - `ws` is a caller-owned device workspace of at least the size reported
- *     by the matching *_workspace_size() call, 256-byte aligned.  Its first
- *     256 bytes are a header that must be zero before first use
- *     (star_workspace_init) and that the library keeps consistent across
- *     calls (a sticky device-error word).  The rest is scratch.  Calls
- *     sharing a workspace must be ordered (same stream, or synchronised).
+ *     by the matching *_workspace_size() call, 256-byte aligned, zeroed once
+ *     before first use (star_workspace_init).  Its first 256 bytes hold a
+ *     sticky device-error word; star_score_migrations also keeps merge
+ *     tickets there that it returns to zero before each call completes.
+ *     The rest is scratch.  Calls sharing a workspace must be ordered (same
+ *     stream, or synchronised); concurrent calls need distinct workspaces.
  *   - Array CONTENTS that break a documented precondition (instance index
  *     out of range, cur_len < 1, rem_len < 1) are detected on the device:
  *     the offending request is left out of every curve, score and ranking,
@@ -164,7 +165,9 @@ star_status star_score_migrations(const star_score_params* p, const int32_t* cur
 /* ------------------------------------------------------------------------
  * Housekeeping.
  * ---------------------------------------------------------------------- */
-/* Zero the workspace header on `stream` (a fill kernel, no memset node). */
+/* Zero the whole workspace on `stream` (a fill kernel, no memset node).
+ * Call once after allocating a workspace; the library keeps its bookkeeping
+ * (error word, merge tickets) consistent from then on. */
 star_status star_workspace_init(void* ws, size_t ws_bytes, void* stream);
 
 /* Synchronise `stream`, return the workspace's device-error word (OR of

@@ -32,14 +32,27 @@ CFLAGS = [
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *CFLAGS, "-Rpass-analysis=kernel-resource-usage", "-fno-caret-diagnostics",
+           "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
-    err = "\n".join(l for l in r.stderr.splitlines() if noise not in l)
+    lines = [l for l in r.stderr.splitlines() if noise not in l]
+    usage = [l for l in lines if "kernel-resource-usage" in l]
+    err = "\n".join(l for l in lines if "kernel-resource-usage" not in l)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{err}")
+    # every kernel must keep its state in registers and LDS: private (scratch)
+    # memory in a hot loop costs a global-memory round trip per access
+    kernel = None
+    for l in usage:
+        if "Function Name:" in l:
+            kernel = l.split("Function Name:")[1].split("[")[0].strip()
+        elif "ScratchSize [bytes/lane]:" in l:
+            n = int(l.split("ScratchSize [bytes/lane]:")[1].split("[")[0])
+            if n:
+                raise RuntimeError(f"{src}: kernel {kernel} uses {n} bytes/lane of scratch")
     if err.strip() and verbose:
         print(err, file=sys.stderr)
     return obj

@@ -11,9 +11,11 @@
 //   double-buffered LDS fed by 16-byte global loads, split-K so that small
 //   batches still launch ~256 workgroups.  Partials are fp32, reduced later
 //   in a fixed order (deterministic results).
-// Kernel 2 (head): 16 rows per workgroup: fixed-order split-K reduction,
-//   bias, activation, the bin GEMM (bf16 MFMA 16x16x32 on a hi/lo split of
-//   a1, or fp32 FMA), softmax, expectation, EMA, round-half-even, clamp.
+// Kernel 2 (head): 4 rows per workgroup (many workgroups, so the split-K
+//   partial reads have plenty of loads in flight): fixed-order split-K
+//   reduction, bias, activation, the bin GEMM (bf16 MFMA 16x16x32 on a hi/lo
+//   split of a1, or fp32 FMA), softmax, expectation, EMA, round-half-even,
+//   clamp.
 #include "star_common.hpp"
 #include "star_internal.hpp"
 
@@ -30,6 +32,7 @@ constexpr int G1_TILE = G1_BM * G1_ROW;        // one operand tile (bytes)
 constexpr int G1_THREADS = 256;
 constexpr int G1_CHUNKS = G1_BM * G1_KBYTES / 16 / G1_THREADS;   // 16-byte chunks per thread per operand
 
+
 template <int kElemBytes> struct G1Elem;
 template <> struct G1Elem<2> { static constexpr int BK = 64; };   // bf16
 template <> struct G1Elem<4> { static constexpr int BK = 32; };   // fp32
@@ -43,11 +46,133 @@ __device__ inline int xcd_logical_block(int bid, int nblk) {
     return x * q + (x < r ? x : r) + bid / 8;
 }
 
+// One K-tile of both operands staged in registers: 4 x 16 bytes per thread
+// per operand (plain members, so the stages stay in VGPRs).
+struct G1Stage {
+    uint4 a0, a1, a2, a3, b0, b1, b2, b3;
+};
+static_assert(G1_CHUNKS == 4, "G1Stage holds four 16-byte chunks per operand");
+
+struct G1Ctx {
+    const char* A;
+    const char* W;
+    int M, N, tm, tn, tid;
+    int64_t row_bytes;
+};
+
+// Loads are unconditional (addresses clamped into the operands) so the
+// compiler can count them and wait only for the stage it is about to store;
+// out-of-range values are zeroed when they are written to LDS.
+__device__ __forceinline__ uint4 g1_load(const G1Ctx& c, const char* base, int rows, int row0,
+                                         int p, int64_t kb) {
+    const int ch = c.tid + p * G1_THREADS;
+    const int row = row0 + (ch >> 3);
+    const int64_t off = kb + (ch & 7) * 16;
+    const int64_t ko = off < c.row_bytes ? off : 0;
+    return *(const uint4*)(base + (int64_t)(row < rows ? row : rows - 1) * c.row_bytes + ko);
+}
+
+__device__ __forceinline__ void g1_load_stage(const G1Ctx& c, int kt, G1Stage& s) {
+    const int64_t kb = (int64_t)kt * G1_KBYTES;
+    const int ra = c.tm * G1_BM, rb = c.tn * G1_BN;
+    s.a0 = g1_load(c, c.A, c.M, ra, 0, kb);
+    s.b0 = g1_load(c, c.W, c.N, rb, 0, kb);
+    s.a1 = g1_load(c, c.A, c.M, ra, 1, kb);
+    s.b1 = g1_load(c, c.W, c.N, rb, 1, kb);
+    s.a2 = g1_load(c, c.A, c.M, ra, 2, kb);
+    s.b2 = g1_load(c, c.W, c.N, rb, 2, kb);
+    s.a3 = g1_load(c, c.A, c.M, ra, 3, kb);
+    s.b3 = g1_load(c, c.W, c.N, rb, 3, kb);
+}
+
+__device__ __forceinline__ void g1_store_chunk(const G1Ctx& c, char* la, char* lb, int p,
+                                               int64_t kb, uint4 va, uint4 vb) {
+    const int ch = c.tid + p * G1_THREADS;
+    const int row = ch >> 3;
+    const int cb = (ch & 7) * 16;
+    const bool kin = kb + cb < c.row_bytes;
+    // bitwise masks, not a select of uint4 structs (which would go through memory)
+    const uint32_t ma = (kin && c.tm * G1_BM + row < c.M) ? 0xFFFFFFFFu : 0u;
+    const uint32_t mb = (kin && c.tn * G1_BN + row < c.N) ? 0xFFFFFFFFu : 0u;
+    *(uint4*)(la + row * G1_ROW + cb) = make_uint4(va.x & ma, va.y & ma, va.z & ma, va.w & ma);
+    *(uint4*)(lb + row * G1_ROW + cb) = make_uint4(vb.x & mb, vb.y & mb, vb.z & mb, vb.w & mb);
+}
+
+__device__ __forceinline__ void g1_store_stage(const G1Ctx& c, char* la, char* lb, int kt,
+                                               const G1Stage& s) {
+    const int64_t kb = (int64_t)kt * G1_KBYTES;
+    g1_store_chunk(c, la, lb, 0, kb, s.a0, s.b0);
+    g1_store_chunk(c, la, lb, 1, kb, s.a1, s.b1);
+    g1_store_chunk(c, la, lb, 2, kb, s.a2, s.b2);
+    g1_store_chunk(c, la, lb, 3, kb, s.a3, s.b3);
+}
+
+template <int kElemBytes>
+__device__ __forceinline__ void g1_compute(const char* la, const char* lb, int wm, int wn,
+                                           int lane, f32x16 (&acc)[2][2]) {
+    constexpr int BK = G1Elem<kElemBytes>::BK;
+    const int r32 = lane & 31;
+    const int khalf = lane >> 5;   // which half of the MFMA's K slice this lane feeds
+    if constexpr (kElemBytes == 2) {
+        // v_mfma_f32_32x32x16_bf16: lane feeds row (lane%32), k = 8*(lane/32)..+7
+#pragma unroll
+        for (int kk = 0; kk < BK / 16; ++kk) {
+            const int koff = (kk * 16 + khalf * 8) * 2;
+            bf16x8_t a[2], b[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                a[i] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(la + (wm * 64 + i * 32 + r32) * G1_ROW + koff));
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                b[j] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(lb + (wn * 64 + j * 32 + r32) * G1_ROW + koff));
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+    } else {
+        // v_mfma_f32_32x32x2_f32: lane feeds row (lane%32), k = lane/32
+#pragma unroll
+        for (int kk = 0; kk < BK / 2; ++kk) {
+            const int koff = (kk * 2 + khalf) * 4;
+            float a[2], b[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) a[i] = *(const float*)(la + (wm * 64 + i * 32 + r32) * G1_ROW + koff);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) b[j] = *(const float*)(lb + (wn * 64 + j * 32 + r32) * G1_ROW + koff);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+    }
+}
+
+// One pipeline step: stage s holds tile i; write it to LDS buffer i % 2,
+// barrier, refill s with tile i + 3 (or re-read tile i -- a cache hit --
+// past the end, so that every step issues exactly one stage of loads), and
+// multiply buffer i % 2.  A buffer is rewritten two steps after its last
+// use, and every thread has passed the intervening barrier only after
+// finishing that use.
+template <int kElemBytes>
+__device__ __forceinline__ void g1_step(const G1Ctx& c, char (*lds)[2][G1_TILE], int kt0, int nk,
+                                        int i, G1Stage& s, int wm, int wn, int lane,
+                                        f32x16 (&acc)[2][2]) {
+    const int buf = i & 1;
+    g1_store_stage(c, lds[buf][0], lds[buf][1], kt0 + i, s);
+    __syncthreads();
+    g1_load_stage(c, kt0 + (i + 3 < nk ? i + 3 : i), s);
+    g1_compute<kElemBytes>(lds[buf][0], lds[buf][1], wm, wn, lane, acc);
+}
+
+// Three K-tiles of global loads are in flight ahead of the tile being
+// multiplied (register staging, two LDS buffers, one barrier per K-tile).
 template <int kElemBytes>
 __global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
     const char* __restrict__ A, const char* __restrict__ W, float* __restrict__ P,
     int M, int N, int Kd, int splits, int tiles_n, int ktiles) {
-    constexpr int BK = G1Elem<kElemBytes>::BK;
     __shared__ __attribute__((aligned(16))) char lds[2][2][G1_TILE];
 
     const int tid = threadIdx.x;
@@ -62,38 +187,11 @@ __global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
     const int tm = tile / tiles_n, tn = tile % tiles_n;
     const int kt0 = (int)((int64_t)split * ktiles / splits);
     const int kt1 = (int)((int64_t)(split + 1) * ktiles / splits);
+    const int nk = kt1 - kt0;
 
-    const int64_t row_bytes = (int64_t)Kd * kElemBytes;
-    const int64_t kd_bytes = row_bytes;
-
-    // global -> register staging for one K-tile (both operands)
-    uint4 ra[G1_CHUNKS], rb[G1_CHUNKS];
-    auto load_tile = [&](int kt) {
-        const int64_t kb = (int64_t)kt * G1_KBYTES;
-#pragma unroll
-        for (int p = 0; p < G1_CHUNKS; ++p) {
-            const int c = tid + p * G1_THREADS;
-            const int row = c >> 3;
-            const int cb = (c & 7) * 16;
-            const int ga = tm * G1_BM + row;
-            const int gb = tn * G1_BN + row;
-            const bool kin = kb + cb < kd_bytes;
-            ra[p] = (ga < M && kin) ? *(const uint4*)(A + (int64_t)ga * row_bytes + kb + cb)
-                                    : make_uint4(0, 0, 0, 0);
-            rb[p] = (gb < N && kin) ? *(const uint4*)(W + (int64_t)gb * row_bytes + kb + cb)
-                                    : make_uint4(0, 0, 0, 0);
-        }
-    };
-    auto store_tile = [&](int buf) {
-#pragma unroll
-        for (int p = 0; p < G1_CHUNKS; ++p) {
-            const int c = tid + p * G1_THREADS;
-            const int row = c >> 3;
-            const int cb = (c & 7) * 16;
-            *(uint4*)(&lds[buf][0][row * G1_ROW + cb]) = ra[p];
-            *(uint4*)(&lds[buf][1][row * G1_ROW + cb]) = rb[p];
-        }
-    };
+    G1Ctx c;
+    c.A = A; c.W = W; c.M = M; c.N = N; c.tm = tm; c.tn = tn; c.tid = tid;
+    c.row_bytes = (int64_t)Kd * kElemBytes;
 
     f32x16 acc[2][2];
 #pragma unroll
@@ -104,56 +202,21 @@ __global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
     const int r32 = lane & 31;
-    const int khalf = lane >> 5;   // which half of the MFMA's K slice this lane feeds
+    const int khalf = lane >> 5;
 
-    if (kt0 < kt1) {
-        load_tile(kt0);
-        store_tile(0);
-        __syncthreads();
-        for (int kt = kt0; kt < kt1; ++kt) {
-            const int buf = (kt - kt0) & 1;
-            const bool more = kt + 1 < kt1;
-            if (more) load_tile(kt + 1);
-            const char* la = lds[buf][0];
-            const char* lb = lds[buf][1];
-            if constexpr (kElemBytes == 2) {
-                // v_mfma_f32_32x32x16_bf16: lane feeds row (lane%32), k = 8*(lane/32)..+7
-#pragma unroll
-                for (int kk = 0; kk < BK / 16; ++kk) {
-                    const int koff = (kk * 16 + khalf * 8) * 2;
-                    bf16x8_t a[2], b[2];
-#pragma unroll
-                    for (int i = 0; i < 2; ++i)
-                        a[i] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(la + (wm * 64 + i * 32 + r32) * G1_ROW + koff));
-#pragma unroll
-                    for (int j = 0; j < 2; ++j)
-                        b[j] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(lb + (wn * 64 + j * 32 + r32) * G1_ROW + koff));
-#pragma unroll
-                    for (int i = 0; i < 2; ++i)
-#pragma unroll
-                        for (int j = 0; j < 2; ++j)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-                }
-            } else {
-                // v_mfma_f32_32x32x2_f32: lane feeds row (lane%32), k = lane/32
-#pragma unroll
-                for (int kk = 0; kk < BK / 2; ++kk) {
-                    const int koff = (kk * 2 + khalf) * 4;
-                    float a[2], b[2];
-#pragma unroll
-                    for (int i = 0; i < 2; ++i) a[i] = *(const float*)(la + (wm * 64 + i * 32 + r32) * G1_ROW + koff);
-#pragma unroll
-                    for (int j = 0; j < 2; ++j) b[j] = *(const float*)(lb + (wn * 64 + j * 32 + r32) * G1_ROW + koff);
-#pragma unroll
-                    for (int i = 0; i < 2; ++i)
-#pragma unroll
-                        for (int j = 0; j < 2; ++j)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
-                }
-            }
-            if (more) store_tile(buf ^ 1);
-            __syncthreads();
+    if (nk > 0) {
+        G1Stage s0, s1, s2;
+        g1_load_stage(c, kt0, s0);
+        g1_load_stage(c, kt0 + (1 < nk ? 1 : 0), s1);
+        g1_load_stage(c, kt0 + (2 < nk ? 2 : 0), s2);
+        int i = 0;
+        for (; i + 3 <= nk; i += 3) {
+            g1_step<kElemBytes>(c, lds, kt0, nk, i, s0, wm, wn, lane, acc);
+            g1_step<kElemBytes>(c, lds, kt0, nk, i + 1, s1, wm, wn, lane, acc);
+            g1_step<kElemBytes>(c, lds, kt0, nk, i + 2, s2, wm, wn, lane, acc);
         }
+        if (i < nk) g1_step<kElemBytes>(c, lds, kt0, nk, i, s0, wm, wn, lane, acc);
+        if (i + 1 < nk) g1_step<kElemBytes>(c, lds, kt0, nk, i + 1, s1, wm, wn, lane, acc);
     }
 
     // epilogue: 32x32 accumulator layout -- element v of lane l is
@@ -175,17 +238,21 @@ __global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
 // ---------------------------------------------------------------------------
 // head
 // ---------------------------------------------------------------------------
-constexpr int HD_RB = 16;
+constexpr int HD_RB = 4;          // rows per workgroup (one wave per row in the softmax)
 constexpr int HD_THREADS = 256;
+constexpr int HD_BATCH = 2;       // float4 items per thread whose partial loads are in flight together
+constexpr int HD_W2PF = 16;       // W2 fragments (K-steps of 32) loaded per wave at a time
 
 __device__ inline float apply_act(float x, int act) {
     if (act == STAR_ACT_RELU) return x > 0.0f ? x : 0.0f;
     return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
 }
 
-template <bool kBF16>
+// kS = number of split-K partial planes (compile time, so that all of a
+// thread's partial loads are issued before the first is consumed).
+template <bool kBF16, int kS>
 __global__ __launch_bounds__(HD_THREADS) void head_kernel(
-    const float* __restrict__ P, int splits, int B, int m, int nb, const float* __restrict__ b1,
+    const float* __restrict__ P, int B, int m, int nb, const float* __restrict__ b1,
     const void* __restrict__ w2, const float* __restrict__ b2, const float* __restrict__ bins,
     int act, float ema_alpha, int ema_init, float* __restrict__ ema_state,
     float* __restrict__ expected, int32_t* __restrict__ rem_len, int len_max) {
@@ -203,26 +270,85 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     float* a32 = (float*)smem;
     float* z = kBF16 ? (float*)(alo + HD_RB * astride) : (float*)(a32 + HD_RB * m);
 
-    const int64_t plane = (int64_t)B * m;
-    // 1) fixed-order split-K reduction, bias, activation
-    for (int r = 0; r < HD_RB; ++r) {
-        const int gr = row0 + r;
-        for (int u = tid; u < (kBF16 ? mpad : m); u += HD_THREADS) {
-            float a = 0.0f;
-            if (gr < B && u < m) {
-                const float* src = P + (int64_t)gr * m + u;
-                float s = src[0];
-                for (int q = 1; q < splits; ++q) s += src[q * plane];
-                if (b1) s += b1[u];
-                a = apply_act(s, act);
+    // 0) everything phases 2 and 3 read from global memory is requested now,
+    //    so that its latency overlaps the split-K reads
+    const int r16 = lane & 15;
+    const int kq = lane >> 4;
+    const int j0 = wid * 16 + r16;                // this lane's bin in the wave's first block
+    bf16x8 wf0[HD_W2PF];
+    if constexpr (kBF16) {
+        const uint16_t* W2 = (const uint16_t*)w2;
+        // Loads are unconditional (clamped indices) so none of them is waited
+        // for before it is used.  An out-of-range fragment reads W2[0, 0..7]:
+        // it only ever meets zero K-padding of a1 or lands in a column >= nb,
+        // which is discarded.
+#pragma unroll
+        for (int u = 0; u < HD_W2PF; ++u) {
+            const int k = u * 32 + kq * 8;
+            const bool in = j0 < nb && k < m;
+            wf0[u] = *(const bf16x8*)(W2 + (in ? (int64_t)j0 * m + k : 0));
+        }
+    }
+    float binv[4];                                // used only where lane + 64 i < nb
+#pragma unroll
+    for (int i = 0; i < 4; ++i) binv[i] = bins[lane + 64 * i < nb ? lane + 64 * i : nb - 1];
+    const float b2v = b2 ? b2[j0 < nb ? j0 : nb - 1] : 0.0f;
+    const int my_row = row0 + wid;                // the row this wave finishes in phase 3
+    const float ema_prev = (ema_alpha > 0.0f && !ema_init) ? ema_state[my_row < B ? my_row : B - 1] : 0.0f;
+
+    // 1) fixed-order split-K reduction, bias, activation (float4 items)
+    const int m4 = m >> 2;
+    const int items = HD_RB * m4;
+    const int64_t plane4 = (int64_t)B * m4;
+    const float4* P4 = (const float4*)P;
+    for (int base = 0; base < items; base += HD_BATCH * HD_THREADS) {
+        float4 v[HD_BATCH][kS];
+        float4 bv[HD_BATCH];
+        int row[HD_BATCH], c4[HD_BATCH];
+        bool ok[HD_BATCH];
+#pragma unroll
+        for (int i = 0; i < HD_BATCH; ++i) {
+            const int e = base + i * HD_THREADS + tid;
+            row[i] = e / m4;
+            c4[i] = e - row[i] * m4;
+            ok[i] = e < items && row0 + row[i] < B;
+            const int64_t off = ok[i] ? (int64_t)(row0 + row[i]) * m4 + c4[i] : 0;
+#pragma unroll
+            for (int q = 0; q < kS; ++q) v[i][q] = P4[q * plane4 + off];
+            bv[i] = b1 ? *(const float4*)(b1 + 4 * c4[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < HD_BATCH; ++i) {
+            const int e = base + i * HD_THREADS + tid;
+            if (e >= items) continue;
+            float4 sum = v[i][0];
+#pragma unroll
+            for (int q = 1; q < kS; ++q) {
+                sum.x += v[i][q].x; sum.y += v[i][q].y; sum.z += v[i][q].z; sum.w += v[i][q].w;
             }
+            float a[4] = {sum.x + bv[i].x, sum.y + bv[i].y, sum.z + bv[i].z, sum.w + bv[i].w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) a[j] = ok[i] ? apply_act(a[j], act) : 0.0f;
             if constexpr (kBF16) {
-                const uint16_t hi = f32_to_bf16_rne(a);
-                ahi[r * astride + u] = hi;
-                alo[r * astride + u] = f32_to_bf16_rne(a - bf16_to_f32(hi));
+                uint16_t h[4], l[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    h[j] = f32_to_bf16_rne(a[j]);
+                    l[j] = f32_to_bf16_rne(a[j] - bf16_to_f32(h[j]));
+                }
+                const int o = row[i] * astride + 4 * c4[i];
+                *(uint2*)(ahi + o) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+                *(uint2*)(alo + o) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
             } else {
-                a32[r * m + u] = a;
+                *(float4*)(a32 + row[i] * m + 4 * c4[i]) = make_float4(a[0], a[1], a[2], a[3]);
             }
+        }
+    }
+    if constexpr (kBF16) {      // zero K padding [m, mpad)
+        for (int e = tid; e < HD_RB * (mpad - m); e += HD_THREADS) {
+            const int r = e / (mpad - m), u = m + e % (mpad - m);
+            ahi[r * astride + u] = 0;
+            alo[r * astride + u] = 0;
         }
     }
     __syncthreads();
@@ -230,29 +356,54 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     // 2) bin logits
     if constexpr (kBF16) {
         // v_mfma_f32_16x16x32_bf16: lane feeds row (lane%16), k = 8*(lane/16)..+7;
-        // accumulator element v of lane l is row 4*(l/16)+v, column l%16.
+        // accumulator element v of lane l is row 4*(l/16)+v, column l%16.  Only
+        // rows < HD_RB are real; the other A rows are fed as zeros.
         const uint16_t* W2 = (const uint16_t*)w2;
-        const int r16 = lane & 15;
-        const int kq = lane >> 4;
+        const bool arow = r16 < HD_RB;
         for (int nblk = wid; nblk * 16 < nb; nblk += HD_THREADS / 64) {
             const int j = nblk * 16 + r16;
             f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 4
-            for (int k0 = 0; k0 < mpad; k0 += 32) {
-                const int k = k0 + kq * 8;
-                bf16x8 bw = {0, 0, 0, 0, 0, 0, 0, 0};
-                if (j < nb && k < m) bw = *(const bf16x8*)(W2 + (int64_t)j * m + k);
-                const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, bw);
-                const bf16x8_t h = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(ahi + r16 * astride + k));
-                const bf16x8_t l = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(alo + r16 * astride + k));
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(h, bv, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(l, bv, acc, 0, 0, 0);
+            for (int kb = 0; kb < mpad; kb += 32 * HD_W2PF) {
+                bf16x8 wf[HD_W2PF];
+                if (nblk == wid && kb == 0) {
+#pragma unroll
+                    for (int u = 0; u < HD_W2PF; ++u) wf[u] = wf0[u];
+                } else {
+#pragma unroll
+                    for (int u = 0; u < HD_W2PF; ++u) {
+                        const int k = kb + u * 32 + kq * 8;
+                        wf[u] = (j < nb && k < m) ? *(const bf16x8*)(W2 + (int64_t)j * m + k)
+                                                  : bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+                    }
+                }
+                // all of this chunk's a1 fragments are read from LDS first, so
+                // their latencies overlap; rows >= HD_RB read row 0 and are
+                // zeroed afterwards (their MFMA rows are discarded anyway)
+                bf16x8 hv[HD_W2PF], lv[HD_W2PF];
+                const int arow_off = (arow ? r16 : 0) * astride;
+#pragma unroll
+                for (int u = 0; u < HD_W2PF; ++u) {
+                    const int k = (kb + u * 32 < mpad ? kb + u * 32 : 0) + kq * 8;
+                    hv[u] = *(const bf16x8*)(ahi + arow_off + k);
+                    lv[u] = *(const bf16x8*)(alo + arow_off + k);
+                }
+                const bf16x8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+                for (int u = 0; u < HD_W2PF; ++u) {
+                    if (kb + u * 32 >= mpad) break;          // uniform: mpad % 32 == 0
+                    const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, wf[u]);
+                    const bf16x8 h = arow ? hv[u] : zero8;
+                    const bf16x8 l = arow ? lv[u] : zero8;
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, h), bv, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, l), bv, acc, 0, 0, 0);
+                }
             }
             const int col = nblk * 16 + r16;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int row = 4 * kq + v;
-                if (col < nb) z[row * nbpad + col] = acc[v] + (b2 ? b2[col] : 0.0f);
+                const float bias = nblk == wid ? b2v : (b2 && col < nb ? b2[col] : 0.0f);
+                if (row < HD_RB && col < nb) z[row * nbpad + col] = acc[v] + bias;
             }
         }
     } else {
@@ -276,10 +427,14 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
         for (int j = lane; j < nb; j += 64) zmax = fmaxf(zmax, z[r * nbpad + j]);
         zmax = wave_max_f32(zmax);
         float den = 0.0f, num = 0.0f;
-        for (int j = lane; j < nb; j += 64) {
-            const float e = expf(z[r * nbpad + j] - zmax);
-            den += e;
-            num += e * bins[j];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int j = lane + 64 * i;
+            if (j < nb) {
+                const float e = expf(z[r * nbpad + j] - zmax);
+                den += e;
+                num += e * binv[i];
+            }
         }
         den = wave_sum_f32(den);
         num = wave_sum_f32(num);
@@ -288,7 +443,8 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
             expected[gr] = E;
             float y = E;
             if (ema_alpha > 0.0f) {
-                y = ema_init ? E : ema_alpha * E + (1.0f - ema_alpha) * ema_state[gr];
+                const float prev = r == wid ? ema_prev : ema_state[gr];
+                y = ema_init ? E : ema_alpha * E + (1.0f - ema_alpha) * prev;
                 ema_state[gr] = y;
             }
             if (rem_len) {
@@ -316,10 +472,10 @@ PredictPlan plan_predict(const star_predict_params& p) {
     const int tiles = pl.tiles_m * pl.tiles_n;
     int s = 1;
     if (tiles > 0 && tiles < 192) {
-        s = 256 / tiles;
-        if (s > 16) s = 16;
-        if (s > pl.ktiles / 2) s = pl.ktiles / 2;
-        if (s < 1) s = 1;
+        int want = 256 / tiles;
+        if (want > 16) want = 16;
+        if (want > pl.ktiles / 2) want = pl.ktiles / 2;
+        while (s * 2 <= want) s *= 2;          // a power of two in [1, 16]
     }
     pl.splits = s;
     pl.partial_bytes = (size_t)s * (size_t)p.n_req * (size_t)p.d_hidden * sizeof(float);
@@ -330,6 +486,38 @@ PredictPlan plan_predict(const star_predict_params& p) {
     else
         pl.head_lds = (size_t)HD_RB * p.d_hidden * 4 + (size_t)HD_RB * nbpad * 4;
     return pl;
+}
+
+template <bool kBF16, int kS>
+static hipError_t launch_head_s(const star_predict_params& p, const PredictPlan& pl, dim3 grid,
+                                const float* partials, const float* b1, const void* w2,
+                                const float* b2, const float* bins, float* ema_state,
+                                float* expected, int32_t* rem_len, hipStream_t stream) {
+    if (pl.head_lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)head_kernel<kBF16, kS>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)pl.head_lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((head_kernel<kBF16, kS>), grid, dim3(HD_THREADS), pl.head_lds, stream,
+                       partials, p.n_req, p.d_hidden, p.n_bins, b1, w2, b2, bins, p.act,
+                       p.ema_alpha, p.ema_init, ema_state, expected, rem_len, p.len_max);
+    return hipGetLastError();
+}
+
+template <bool kBF16>
+static hipError_t launch_head(const star_predict_params& p, const PredictPlan& pl, dim3 grid,
+                              const float* partials, const float* b1, const void* w2,
+                              const float* b2, const float* bins, float* ema_state,
+                              float* expected, int32_t* rem_len, hipStream_t stream) {
+    switch (pl.splits) {
+        case 1: return launch_head_s<kBF16, 1>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
+        case 2: return launch_head_s<kBF16, 2>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
+        case 4: return launch_head_s<kBF16, 4>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
+        case 8: return launch_head_s<kBF16, 8>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
+        case 16: return launch_head_s<kBF16, 16>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
+    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, const void* hidden,
@@ -359,26 +547,11 @@ hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, c
         if (e != hipSuccess) return e;
     }
     const dim3 g2((unsigned)ceil_div(p.n_req, HD_RB));
-    if (p.dtype == STAR_BF16) {
-        if (pl.head_lds > 64 * 1024) {
-            e = hipFuncSetAttribute((const void*)head_kernel<true>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.head_lds);
-            if (e != hipSuccess) return e;
-        }
-        hipLaunchKernelGGL(head_kernel<true>, g2, dim3(HD_THREADS), pl.head_lds, stream, partials,
-                           pl.splits, p.n_req, p.d_hidden, p.n_bins, b1, w2, b2, bins, p.act,
-                           p.ema_alpha, p.ema_init, ema_state, expected, rem_len, p.len_max);
-    } else {
-        if (pl.head_lds > 64 * 1024) {
-            e = hipFuncSetAttribute((const void*)head_kernel<false>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.head_lds);
-            if (e != hipSuccess) return e;
-        }
-        hipLaunchKernelGGL(head_kernel<false>, g2, dim3(HD_THREADS), pl.head_lds, stream, partials,
-                           pl.splits, p.n_req, p.d_hidden, p.n_bins, b1, w2, b2, bins, p.act,
-                           p.ema_alpha, p.ema_init, ema_state, expected, rem_len, p.len_max);
-    }
-    return hipGetLastError();
+    return p.dtype == STAR_BF16 ? launch_head<true>(p, pl, g2, partials, b1, w2, b2, bins,
+                                                    ema_state, expected, rem_len, stream)
+                                : launch_head<false>(p, pl, g2, partials, b1, w2, b2, bins,
+                                                     ema_state, expected, rem_len, stream);
 }
 
 }  // namespace star
+

@@ -24,6 +24,7 @@ namespace star {
 
 constexpr int PL_THREADS = 512;
 constexpr int PL_CHUNK = 1024;
+constexpr int PL_RBATCH = 4;      // requests per thread whose reads are in flight together
 
 __global__ __launch_bounds__(PL_THREADS) void project_load_kernel(
     const int32_t* __restrict__ cur, const int32_t* __restrict__ rem,
@@ -43,35 +44,56 @@ __global__ __launch_bounds__(PL_THREADS) void project_load_kernel(
     const int64_t H = (int64_t)b * K;
     const int64_t alpha0 = (int64_t)b * (b - 1) / 2;
 
-    for (int j = tid; j <= len; j += PL_THREADS) {
-        hA[j] = 0;
-        hN[j] = 0;
-        if (j < len) hP[j] = 0;
-    }
-    __syncthreads();
-
-    int32_t bad = 0;
-    for (int r = tid; r < N; r += PL_THREADS) {
-        const int s = inst[r];
-        const int cr = cur[r];
-        const int lr = rem[r];
-        int32_t f = 0;
-        if (s < 0 || s >= n) f |= STAR_DEV_BAD_INST;
-        if (cr < 1) f |= STAR_DEV_BAD_CUR;
-        if (lr < 1) f |= STAR_DEV_BAD_REM;
-        bad |= f;
-        if (f || s != i) continue;
-        const int64_t lp = (int64_t)lr < H ? (int64_t)lr : H;
-        const int64_t ke = lp / b;
-        const int64_t mu = lp - ke * b;
-        if (ke > k0) {
-            const int j = (int)((ke < k1 ? ke : k1) - k0);          // 1..len
-            atomicAdd((unsigned long long*)&hA[j], (unsigned long long)((int64_t)b * cr + alpha0));
-            atomicAdd((unsigned long long*)&hN[j], 1ull);
+    auto clear_lds = [&]() {
+        for (int j = tid; j <= len; j += PL_THREADS) {
+            hA[j] = 0;
+            hN[j] = 0;
+            if (j < len) hP[j] = 0;
         }
-        if (mu > 0 && ke >= k0 && ke < k1) {
-            const int64_t pr = mu * cr + mu * ke * b + mu * (mu - 1) / 2;
-            atomicAdd((unsigned long long*)&hP[ke - k0], (unsigned long long)pr);
+        __syncthreads();
+    };
+    if (N == 0) clear_lds();
+
+    // Requests are read PL_RBATCH per thread at a time, all loads issued
+    // before the first is used (indices clamped, so the loads are
+    // unconditional); the first batch is in flight while LDS is cleared.
+    int32_t bad = 0;
+    for (int base = 0; base < N; base += PL_THREADS * PL_RBATCH) {
+        int sv[PL_RBATCH], cv[PL_RBATCH], lv[PL_RBATCH];
+#pragma unroll
+        for (int j = 0; j < PL_RBATCH; ++j) {
+            const int r = base + j * PL_THREADS + tid;
+            const int rc = r < N ? r : N - 1;
+            sv[j] = inst[rc];
+            cv[j] = cur[rc];
+            lv[j] = rem[rc];
+        }
+        if (base == 0) clear_lds();
+#pragma unroll
+        for (int j = 0; j < PL_RBATCH; ++j) {
+            const int r = base + j * PL_THREADS + tid;
+            if (r >= N) continue;
+            const int s = sv[j];
+            const int cr = cv[j];
+            const int lr = lv[j];
+            int32_t f = 0;
+            if (s < 0 || s >= n) f |= STAR_DEV_BAD_INST;
+            if (cr < 1) f |= STAR_DEV_BAD_CUR;
+            if (lr < 1) f |= STAR_DEV_BAD_REM;
+            bad |= f;
+            if (f || s != i) continue;
+            const int64_t lp = (int64_t)lr < H ? (int64_t)lr : H;
+            const int64_t ke = lp / b;
+            const int64_t mu = lp - ke * b;
+            if (ke > k0) {
+                const int jj = (int)((ke < k1 ? ke : k1) - k0);          // 1..len
+                atomicAdd((unsigned long long*)&hA[jj], (unsigned long long)((int64_t)b * cr + alpha0));
+                atomicAdd((unsigned long long*)&hN[jj], 1ull);
+            }
+            if (mu > 0 && ke >= k0 && ke < k1) {
+                const int64_t pr = mu * cr + mu * ke * b + mu * (mu - 1) / 2;
+                atomicAdd((unsigned long long*)&hP[ke - k0], (unsigned long long)pr);
+            }
         }
     }
     if (i == 0 && c == 0) {
@@ -91,8 +113,8 @@ __global__ __launch_bounds__(PL_THREADS) void project_load_kernel(
         la += hA[q + 1];
         ln += hN[q + 1];
     }
-    int64_t ra = block_exclusive_scan_i64(la, OpAdd(), 0, tmp, (int64_t*)nullptr);
-    int64_t rn = block_exclusive_scan_i64(ln, OpAdd(), 0, tmp, (int64_t*)nullptr);
+    int64_t ra = block_exclusive_scan_i64<PL_THREADS>(la, OpAdd(), 0, tmp, (int64_t*)nullptr);
+    int64_t rn = block_exclusive_scan_i64<PL_THREADS>(ln, OpAdd(), 0, tmp, (int64_t*)nullptr);
     const int64_t bb = (int64_t)b * b;
     int64_t* out = load + (int64_t)i * K;
     for (int p = p0; p < p1; ++p) {

@@ -149,7 +149,8 @@ static star_status check_score_params(const star_score_params* p) {
 
 STAR_API size_t star_score_workspace_size(const star_score_params* p) {
     if (check_score_params(p) != STAR_OK) return 0;
-    return plan_score(*p).total;
+    const ScorePlan pl = plan_score(*p);
+    return pl.topk_ok ? pl.total : 0;
 }
 
 STAR_API star_status star_score_migrations(const star_score_params* p, const int32_t* cur_len,
@@ -167,6 +168,7 @@ STAR_API star_status star_score_migrations(const star_score_params* p, const int
     const bool all_topk = topk_req && topk_tgt && topk_score;
     if (p->top_k > 0 ? !all_topk : any_topk) return STAR_ERR_INVALID_ARG;
     const ScorePlan pl = plan_score(*p);
+    if (!pl.topk_ok) return STAR_ERR_UNSUPPORTED;
     st = check_ws(ws, ws_bytes, pl.total);
     if (st != STAR_OK) return st;
     int32_t* err = (int32_t*)((char*)ws + kHdrErrorWord);
@@ -182,7 +184,7 @@ STAR_API star_status star_score_migrations(const star_score_params* p, const int
 STAR_API star_status star_workspace_init(void* ws, size_t ws_bytes, void* stream) {
     star_status st = check_ws(ws, ws_bytes, STAR_WS_HEADER_BYTES);
     if (st != STAR_OK) return st;
-    return launch_fill_zero(ws, STAR_WS_HEADER_BYTES, (hipStream_t)stream) == hipSuccess
+    return launch_fill_zero(ws, ws_bytes, (hipStream_t)stream) == hipSuccess
                ? STAR_OK
                : STAR_ERR_HIP;
 }

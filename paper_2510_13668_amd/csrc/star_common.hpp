@@ -49,6 +49,51 @@ __device__ inline int32_t wave_or_i32(int32_t v) {
     return v;
 }
 
+// ---------------------------------------------------------------------------
+// DPP wavefront scans (gfx9 data-parallel primitives: row shifts within 16
+// lanes, then row broadcasts of lanes 15 and 31).  A lane whose source lane
+// is out of range or masked off receives `ident`.  DPP moves cost a few
+// cycles, against ~80 for a ds_bpermute-based shuffle.
+// ---------------------------------------------------------------------------
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
+
+template <int kCtrl, int kRowMask>
+__device__ inline int dpp_i32(int v, int ident) {
+    return __builtin_amdgcn_update_dpp(ident, v, kCtrl, kRowMask, 0xF, false);
+}
+
+// Inclusive prefix sum over the 64 lanes (lane order).
+__device__ inline int wave_incl_add_i32(int v) {
+    v += dpp_i32<kDppRowShr1, 0xF>(v, 0);
+    v += dpp_i32<kDppRowShr2, 0xF>(v, 0);
+    v += dpp_i32<kDppRowShr4, 0xF>(v, 0);
+    v += dpp_i32<kDppRowShr8, 0xF>(v, 0);
+    v += dpp_i32<kDppRowBcast15, 0xA>(v, 0);
+    v += dpp_i32<kDppRowBcast31, 0xC>(v, 0);
+    return v;
+}
+
+template <int kCtrl, int kRowMask>
+__device__ inline int64_t dpp_max_step_i64(int64_t v) {
+    const int lo = (int)(uint32_t)v, hi = (int)(v >> 32);
+    const int slo = dpp_i32<kCtrl, kRowMask>(lo, lo);   // masked / out-of-range: own value
+    const int shi = dpp_i32<kCtrl, kRowMask>(hi, hi);
+    const int64_t u = (int64_t)(((uint64_t)(uint32_t)shi << 32) | (uint32_t)slo);
+    return u > v ? u : v;
+}
+
+// Inclusive prefix max over the 64 lanes (lane order).
+__device__ inline int64_t wave_incl_max_i64(int64_t v) {
+    v = dpp_max_step_i64<kDppRowShr1, 0xF>(v);
+    v = dpp_max_step_i64<kDppRowShr2, 0xF>(v);
+    v = dpp_max_step_i64<kDppRowShr4, 0xF>(v);
+    v = dpp_max_step_i64<kDppRowShr8, 0xF>(v);
+    v = dpp_max_step_i64<kDppRowBcast15, 0xA>(v);
+    v = dpp_max_step_i64<kDppRowBcast31, 0xC>(v);
+    return v;
+}
+
 // Inclusive scan across the wave (lane order), for a commutative,
 // associative op on int64.
 template <class Op>
@@ -62,18 +107,30 @@ __device__ inline int64_t wave_inclusive_scan_i64(int64_t v, Op op) {
     return v;
 }
 
+// Inclusive max-scan across the wave in reverse lane order (lane 63 first).
+__device__ inline int64_t wave_inclusive_scan_rev_i64(int64_t v) {
+    const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        int64_t u = __shfl_down(v, o, kWave);
+        if (lane + o < kWave) v = v > u ? v : u;
+    }
+    return v;
+}
+
 struct OpAdd { __device__ int64_t operator()(int64_t a, int64_t b) const { return a + b; } };
 struct OpMax { __device__ int64_t operator()(int64_t a, int64_t b) const { return a > b ? a : b; } };
 
-// Block-wide exclusive scan of one int64 per thread (thread order), using
-// `tmp` (>= blockDim/64 + 1 int64 of LDS).  Returns the exclusive prefix;
-// *total receives the block aggregate.  `ident` is the op's identity.
-template <class Op>
+// Block-wide exclusive scan of one int64 per thread (thread order) for a
+// block of kThreads threads, using `tmp` (>= kThreads/64 + 1 int64 of LDS).
+// Returns the exclusive prefix; *total receives the block aggregate.
+// `ident` is the op's identity.
+template <int kThreads, class Op>
 __device__ inline int64_t block_exclusive_scan_i64(int64_t v, Op op, int64_t ident,
                                                    int64_t* tmp, int64_t* total) {
+    constexpr int nw = (kThreads + kWave - 1) / kWave;
     const int lane = threadIdx.x & (kWave - 1);
     const int wid = threadIdx.x / kWave;
-    const int nw = (blockDim.x + kWave - 1) / kWave;
     int64_t inc = wave_inclusive_scan_i64(v, op);
     if (lane == kWave - 1) tmp[wid] = inc;
     __syncthreads();

@@ -30,11 +30,15 @@ hipError_t launch_project_load(const star_load_params& p, const LoadPlan& pl,
                                int64_t* load, int32_t* err_word, hipStream_t stream);
 
 struct ScorePlan {
+    bool fused = false;   // PM/SM built in LDS by the scoring kernel
     int rpb = 0;          // requests per scoring workgroup
+    int cand = 0;         // candidates per scoring workgroup (rpb * n)
     int groups = 0;       // scoring workgroups
-    int sort_n = 0;       // local sort size (power of two)
-    int kp = 0;           // padded top-k list length (power of two), 0 if top_k == 0
-    size_t pm_off = 0, sm_off = 0, list_s_off = 0, list_i_off = 0, total = 0;
+    bool topk_direct = false;  // top-k over all migrations (else over the k best requests' ones)
+    int topk_rj = 1;      // keys per top-k thread (power of two)
+    bool topk_ok = true;  // sizes within what the top-k kernel holds
+    size_t pm_off = 0, sm_off = 0, scores_off = 0, bscore_off = 0, btarget_off = 0, total = 0;
+    size_t lds = 0;       // dynamic LDS of the scoring kernel
 };
 ScorePlan plan_score(const star_score_params& p);
 hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const int32_t* cur,

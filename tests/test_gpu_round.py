@@ -119,9 +119,11 @@ def test_adversarial(case):
     _check(cur, rem, inst, n, b, K, top_k)
 
 
-def test_ties_from_duplicated_requests():
+@pytest.mark.parametrize("N", [256, 6000])
+def test_ties_from_duplicated_requests(N):
+    """Many equal scores; N = 6000 takes the two-stage (pruned) ranking."""
     rng = np.random.default_rng(3)
-    N, n = 256, 8
+    n = 8
     cur = np.full(N, 1000, np.int32)
     rem = np.full(N, 777, np.int32)
     inst = rng.integers(0, n, N).astype(np.int32)
