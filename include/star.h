@@ -3,7 +3,7 @@
  * (arXiv 2510.13668): remaining-length prediction, load projection and
  * migration-candidate scoring for one rescheduling round.
  *
- * Vocabulary (Section 4.2, problem formulation):
+ * Vocabulary (Section 5.2, problem formulation):
  *   instances I = {0..n_inst-1}; request r sits on instance inst_of[r]
  *   (its batch B_i); N(r) = cur_len[r] is its current token count;
  *   N^(r) = rem_len[r] its predicted remaining generation length; the load of
@@ -21,9 +21,7 @@
  *   - `ws` is a caller-owned device workspace of at least the size reported
  *     by the matching *_workspace_size() call, 256-byte aligned, zeroed once
  *     before first use (star_workspace_init).  Its first 256 bytes hold a
- *     sticky device-error word; star_score_migrations also keeps merge
- *     tickets there that it returns to zero before each call completes.
- *     The rest is scratch.  Calls sharing a workspace must be ordered (same
+ *     sticky device-error word; the rest is scratch.  Calls sharing a workspace must be ordered (same
  *     stream, or synchronised); concurrent calls need distinct workspaces.
  *   - Array CONTENTS that break a documented precondition (instance index
  *     out of range, cur_len < 1, rem_len < 1) are detected on the device:
@@ -64,14 +62,14 @@ typedef enum { STAR_ACT_RELU = 0, STAR_ACT_GELU_ERF = 1 } star_act;
 /* ------------------------------------------------------------------------
  * (a) Remaining-length predictor head.
  *
- * Section 3.2 feeds the last-layer, last-token hidden state h (size d) of
+ * Section 4.2 feeds the last-layer, last-token hidden state h (size d) of
  * each running request to a small MLP (Eq. 2) to estimate the distribution
  * p(Y | S) of the remaining length Y (Eq. 1).  Here the head is
  *     a1 = act(W1 h + b1)                 W1: [m, d]
  *     z  = W2 a1 + b2                     W2: [nb, m]   (one logit per bin)
  *     p  = softmax(z);  E = sum_j p_j v_j (mean of p over length bins v_j,
- *                                          the binned targets of Section 5.5)
- * and, for continuous prediction (Section 3.3), an exponential moving
+ *                                          the binned targets of Section 6.5)
+ * and, for continuous prediction (Section 4.3), an exponential moving
  * average across calls: y = alpha E + (1 - alpha) y_prev.
  * Finally rem_len = clamp(round_half_even(y), 1, len_max), the N^(r) that
  * (b) and (c) consume.
@@ -110,7 +108,7 @@ star_status star_predict(const star_predict_params* p, const void* hidden, const
 /* ------------------------------------------------------------------------
  * (b) Per-instance predicted load curves.
  *
- * Worker-side future-load simulation of Section 4.2's complexity analysis,
+ * Worker-side future-load simulation of Section 5.2's complexity analysis,
  * over a horizon of H = bucket * n_buckets decode steps grouped in buckets
  * of `bucket` steps:
  *     load[i, k] = sum_{t = k*bucket}^{(k+1)*bucket - 1}
@@ -166,8 +164,8 @@ star_status star_score_migrations(const star_score_params* p, const int32_t* cur
  * Housekeeping.
  * ---------------------------------------------------------------------- */
 /* Zero the whole workspace on `stream` (a fill kernel, no memset node).
- * Call once after allocating a workspace; the library keeps its bookkeeping
- * (error word, merge tickets) consistent from then on. */
+ * Call once after allocating a workspace; the error word then stays
+ * consistent across calls. */
 star_status star_workspace_init(void* ws, size_t ws_bytes, void* stream);
 
 /* Synchronise `stream`, return the workspace's device-error word (OR of

@@ -14,7 +14,7 @@
  * migration candidate, and a full sort for the ranking.
  *
  * Symbols:
- *   N(r)     current tokens of request r  (cur_len; Section 4.2, problem
+ *   N(r)     current tokens of request r  (cur_len; Section 5.2, problem
  *            formulation)
  *   N^(r)    predicted remaining length   (rem_len; same passage)
  *   B_i      requests on instance i       (inst_of)

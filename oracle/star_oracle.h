@@ -19,7 +19,7 @@ enum { STAR_ORACLE_F32 = 0, STAR_ORACLE_BF16 = 1 };          /* input element ty
 enum { STAR_ORACLE_RELU = 0, STAR_ORACLE_GELU = 1 };         /* hidden activation  */
 enum { STAR_ORACLE_BAD_INST = 1, STAR_ORACLE_BAD_CUR = 2, STAR_ORACLE_BAD_REM = 4 };
 
-/* Predictor head (Section 3.2, Eq. 1-2; length bins of Section 5.5).
+/* Predictor head (Section 4.2, Eq. 1-2; length bins of Section 6.5).
  * hidden [B,d], w1 [m,d], w2 [nb,m] in `dtype` (bf16 as uint16 bits);
  * b1 [m], b2 [nb] fp32 or NULL; bin_values [nb] fp32.
  * expected [B] <- E = sum_j softmax(z2)_j v_j.
@@ -35,7 +35,7 @@ int star_oracle_predict(int64_t B, int64_t d, int64_t m, int64_t nb, int dtype, 
                         int64_t len_max, double* expected, int32_t* rem_len,
                         double* z1_out, double* z2_out);
 
-/* Load curves (Section 4.2, Eq. 4 and the worker-side summary of the
+/* Load curves (Section 5.2, Eq. 4 and the worker-side summary of the
  * complexity analysis).  load [n,K]: load[i,k] = sum over decode steps
  * t in [k b, (k+1) b) of sum_{r in B_i, t < rem_r} (cur_r + t).
  * Requests with inst_of outside [0,n), cur_len < 1 or rem_len < 1 are

@@ -1,9 +1,9 @@
 // (a) Remaining-length predictor head on gfx950.
 //
-// Section 3.2 (Eq. 1-2): the last-layer, last-token hidden state of every
+// Section 4.2 (Eq. 1-2): the last-layer, last-token hidden state of every
 // running request goes through a small MLP.  Here: a1 = act(W1 h + b1),
 // logits = W2 a1 + b2 over length bins, p = softmax, E = sum p_j v_j, then
-// the continuous-prediction smoothing of Section 3.3 and integerisation.
+// the continuous-prediction smoothing of Section 4.3 and integerisation.
 //
 // Kernel 1 (gemm1_splitk): Z1 partials = H W1^T over a K-slice, on MFMA.
 //   128x128 output tile per 256-thread workgroup (4 waves, 64x64 each as

@@ -1,6 +1,6 @@
 // (b) Per-instance predicted load curves on gfx950.
 //
-// Section 4.2 (problem formulation, Eq. 4): request r with N(r) = c current
+// Section 5.2 (problem formulation, Eq. 4): request r with N(r) = c current
 // tokens and N^(r) = l remaining steps holds c + t tokens at future step
 // t < l.  Over a horizon of H = b K steps in buckets of b steps, with
 // l' = min(l, H), k_e = l' div b and mu = l' mod b, r contributes

@@ -11,7 +11,7 @@
 //     max(PM_t[k_e] + alpha_r,  L_t[k_e] + P_r,  SM_t[k_e + 1])
 // (terms outside [0, K) dropped): three gathers per candidate instead of a
 // K-long scan.  This is the scheduler-side incremental update of the
-// complexity analysis in Section 4.2 taken to O(1) per candidate.
+// complexity analysis in Section 5.2 taken to O(1) per candidate.
 //
 // Kernel score (many workgroups, each a block of requests against every
 // target): PM/SM from LDS when all curves fit there (built per workgroup

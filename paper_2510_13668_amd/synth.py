@@ -5,11 +5,11 @@ oracle's callers.  It draws random numbers and shapes them into the arrays a
 rescheduling round consumes; it holds none of the method's arithmetic (no
 predictor, no load projection, no scoring).
 
-Workload shapes follow the five decode-batch configurations the build is
-measured on (tiny fp32 case; 8B-class batch; 32B-class long-reasoning mix;
-continuous mode over 200 decode steps; 64-instance rebalancing scan).  The
+Five decode-batch workloads: a tiny fp32 case; an 8B-class batch; a
+32B-class long-reasoning mix; continuous mode over 200 decode steps; a
+64-instance rebalancing scan.  The
 paper's own workloads are ShareGPT / Alpaca outputs of DeepSeek-R1-Distill
-(Section 5.1, Table 2); those datasets and models are not used: lognormal,
+(Section 6.1, Table 2); those datasets and models are not used: lognormal,
 lognormal-mixture and Pareto draws of the remaining length stand in for them.
 
 Conventions
@@ -148,7 +148,7 @@ def draw_true_len(rng: np.random.Generator, law: str, n: int, cap: int) -> np.nd
         x = 64.0 * u ** (-1.0 / 1.5)
     elif law == "long_output_stress":
         # Shape taken from published output-length statistics only: a light
-        # lognormal body plus a block of near-cap outputs (Section 3, Table 2).
+        # lognormal body plus a block of near-cap outputs (Section 2.2 and Table 2).
         pick = rng.random(size=n) < 0.827
         a = rng.lognormal(7.16, 0.67, size=n)
         b = rng.uniform(30000.0, 32768.0, size=n)

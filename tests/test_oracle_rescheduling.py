@@ -1,6 +1,6 @@
 """Pins of the CPU oracle's load projection, scoring and ranking.
 
-The load model is Section 4.2's: a request with N(r) current tokens and
+The load model is Section 5.2's: a request with N(r) current tokens and
 N^(r) predicted remaining steps holds N(r)+t tokens at step t < N^(r); the
 token load of instance i at step t is the sum over its batch B_i (Eq. 4's
 N^_i(B_{i,t})), and N_i(B_i) = sum N(r) is the current load.  A candidate
@@ -170,7 +170,7 @@ def test_scores_equal_brute_force_reassignment(oracle_mod, seed):
 
 def test_unit_horizon_is_current_load_balancing(oracle_mod):
     """K = 1, b = 1: s(r, t) = N_t(B_t) + N(r), and the best target is the
-    least-loaded other instance (the current-load baseline of Section 2)."""
+    least-loaded other instance (the current-load baseline of Section 2.2)."""
     rng = np.random.default_rng(15)
     n = 9
     cur, rem, inst = synth.random_requests(rng, 200, n, cur_hi=4000, len_hi=50)
