@@ -7,28 +7,34 @@
 // mu(mu-1)/2, r's own curve is R_r[k] = alpha_r + b^2 k (k < k_e),
 // P_r (k = k_e), 0 (k > k_e).  With, per instance t,
 //     PM_t[k] = max_{j<k} (L_t[j] + b^2 j),   SM_t[k] = max_{j>=k} L_t[j],
-// the peak of L_t + R_r is
-//     max(PM_t[k_e] + alpha_r,  L_t[k_e] + P_r,  SM_t[k_e + 1])
-// (terms outside [0, K) dropped): three gathers per candidate instead of a
-// K-long scan.  This is the scheduler-side incremental update of the
+// (PM_t[0] = SM_t[K] = -inf) the peak of L_t + R_r is
+//     max(PM_t[k_e] + alpha_r,  L_t[k_e] + P_r,  SM_t[min(k_e + 1, K)])
+// (the middle term only for k_e < K): three gathers per candidate instead
+// of a K-long scan.  This is the scheduler-side incremental update of the
 // complexity analysis in Section 5.2 taken to O(1) per candidate.
 //
-// Kernel score (many workgroups, each a block of requests against every
-// target): PM/SM from LDS when all curves fit there (built per workgroup
-// with DPP wavefront scans), else from a separate prep kernel; writes every
-// score and each request's best migration (the smallest key
-// (score, r*n + t) over t != s; keys are a total order).
+// Migrations (t != s) are ranked by the key (score, r*n + t), a total order.
+// The k smallest are found by a block radix select: 12-bit digits of the
+// key packed as ((score - min score) << ibits) | (r*n + t), LDS
+// histograms, DPP scans, stopping as soon as the bin that holds the k-th key
+// is needed whole; the <= k winners are then put in order by a bucket sort
+// on their top 12 bits (LDS counts, offsets, scatter, and a rank count only
+// among equal buckets).
 //
-// Kernel top-k (one workgroup of 1024 threads): the k smallest keys.
-// Exact pruning: a migration in the global top-k belongs to one of the k
-// requests whose best key is smallest (its key is >= its request's best
-// key, and k distinct requests have best keys below the k-th smallest
-// migration key otherwise).  So when N(n-1) is large, a block radix select
-// over the N best keys first picks those k requests, and only their
-// k(n-1) migrations are ranked.  Radix select: 11-bit digits over the key
-// (score - min score, then r*n + t), LDS histograms, DPP scans; the winners
-// are then ordered by counting ranks.  No sorting network, no cross-
-// workgroup synchronisation.
+// Three paths:
+//  * small rounds (N <= 1024, N n <= 8192, curves fit LDS): ONE workgroup of
+//    512 threads loads the curves, builds PM/SM, scores every candidate with
+//    the keys in registers, takes each request's best move with LDS atomics
+//    and runs the selection.  No intermediate array goes through HBM.
+//  * otherwise many workgroups score blocks of requests (PM/SM built in LDS
+//    per workgroup, or by a prep kernel for large curve sets), writing
+//    scores and best moves; then one 1024-thread workgroup selects, over all
+//    migrations when they fit its registers, else with exact pruning: a
+//    migration in the global top-k belongs to one of the k requests whose
+//    best key is smallest (its key is >= its request's best key, and k
+//    distinct requests have best keys below the k-th smallest migration key
+//    otherwise), so the k requests are selected first and only their k(n-1)
+//    migrations are ranked.
 #include "star_common.hpp"
 #include "star_internal.hpp"
 
@@ -40,10 +46,20 @@ constexpr int SC_THREADS = 256;
 constexpr int SC_CAND = 256;                 // target candidates per scoring workgroup
 constexpr int SC_FUSED_ENTRIES = 2600;       // n*(K+1) up to which PM/SM live in LDS
 constexpr int SC_LBATCH = (SC_FUSED_ENTRIES + SC_THREADS - 1) / SC_THREADS;  // curve reads per thread
-constexpr int TK_THREADS = 1024;
-constexpr int TK_DIGIT = 11;                 // radix-select digit width
-constexpr int TK_BINS = 1 << TK_DIGIT;
-constexpr int TK_MAX_KEYS = 16 * TK_THREADS; // migrations the direct top-k holds in registers
+
+constexpr int SEL_DIGIT = 12;                // radix-select digit width
+constexpr int SEL_BINS = 1 << SEL_DIGIT;
+constexpr int SEL_SBATCH = 8;                // reads per thread in flight when streaming keys
+
+constexpr int TK_THREADS = 1024;             // top-k workgroup of the multi-workgroup path
+constexpr int TK_RJ = 8;                     // keys per thread held in registers there
+constexpr int TK_REG_KEYS = TK_RJ * TK_THREADS;
+
+constexpr int SS_THREADS = 512;              // the one workgroup of the small path
+constexpr int SS_RJ = 16;                    // candidates per thread
+constexpr int SS_MAX_REQ = 1024;
+constexpr int SS_LBATCH = (SC_FUSED_ENTRIES + SS_THREADS - 1) / SS_THREADS;
+constexpr int SS_RBATCH = SS_MAX_REQ / SS_THREADS;
 
 constexpr int64_t kInfS = INT64_MAX;
 constexpr uint32_t kInfI = 0xFFFFFFFFu;
@@ -52,6 +68,101 @@ __device__ inline int64_t imax(int64_t a, int64_t b) { return a > b ? a : b; }
 
 __device__ inline bool key_less(int64_t s0, uint32_t i0, int64_t s1, uint32_t i1) {
     return s0 < s1 || (s0 == s1 && i0 < i1);
+}
+
+__device__ inline int bit_length(uint64_t x) { return x ? 64 - __clzll((long long)x) : 0; }
+
+// q = x / d for d >= 1 with m = floor((2^32 - 1) / d) + 1 (m = 0 encodes
+// d = 1): the multiply-high estimate is exact or one too large (x + d < 2^32).
+__device__ inline uint32_t fast_div(uint32_t x, uint32_t d, uint32_t m) {
+    if (m == 0) return x;
+    const uint32_t q = __umulhi(x, m);
+    return q * d > x ? q - 1 : q;
+}
+static uint32_t div_magic(uint32_t d) { return d == 1 ? 0u : (uint32_t)(0xFFFFFFFFull / d) + 1u; }
+
+__device__ inline int64_t readlane_i64(int64_t v, int lane) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), lane);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Value of lane l - 1 (lane 0 gets `ident`): DPP wave_shr:1.
+__device__ inline int64_t wave_shr1_i64(int64_t v, int64_t ident) {
+    constexpr int kWaveShr1 = 0x138;
+    const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)ident, (int)(uint32_t)v, kWaveShr1,
+                                               0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp((int)(ident >> 32), (int)(v >> 32), kWaveShr1, 0xF,
+                                               0xF, false);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// Per-request terms (Section 5.2 load model); invalid requests (instance
+// out of range, c < 1, l < 1) get s = -1 and zero terms.
+struct ReqTerms {
+    int64_t alpha, p;
+    int ke, s;
+    int32_t bad;
+};
+__device__ inline ReqTerms request_terms(int s, int c, int l, int n, int b, int64_t H) {
+    ReqTerms q;
+    q.bad = 0;
+    if (s < 0 || s >= n) q.bad |= STAR_DEV_BAD_INST;
+    if (c < 1) q.bad |= STAR_DEV_BAD_CUR;
+    if (l < 1) q.bad |= STAR_DEV_BAD_REM;
+    const int64_t lp = (int64_t)l < H ? (int64_t)l : H;
+    const int64_t ke = lp / b;
+    const int64_t mu = lp - ke * b;
+    const bool ok = q.bad == 0;
+    q.s = ok ? s : -1;
+    q.ke = ok ? (int)ke : 0;
+    q.alpha = ok ? (int64_t)b * c + (int64_t)b * (b - 1) / 2 : 0;
+    q.p = ok ? mu * c + mu * ke * b + mu * (mu - 1) / 2 : 0;
+    return q;
+}
+
+// PM/SM of instances t = w, w + nw, ... (one wave each) from curves in LDS
+// with row stride K+1 (entry K of each row is padding): 64-bucket chunks,
+// one DPP wavefront max-scan per chunk, carried across chunks; reads and
+// writes are consecutive per lane (no bank conflicts).
+__device__ inline void build_pm_sm(const int64_t* lL, int64_t* lPM, int64_t* lSM, int n, int K,
+                                   int64_t bb, int w, int nw) {
+    const int lane = threadIdx.x & 63;
+    const int K1 = K + 1;
+    for (int t = w; t < n; t += nw) {
+        const int64_t* L = lL + t * K1;
+        int64_t* pm = lPM + t * K1;
+        int64_t* sm = lSM + t * K1;
+        int64_t carry = INT64_MIN;
+        for (int c = 0; c < K; c += 64) {                // PM: exclusive prefix max of L[j] + b^2 j
+            const int j = c + lane;
+            const int64_t x = j < K ? L[j] + bb * j : INT64_MIN;
+            const int64_t inc = imax(wave_incl_max_i64(x), carry);
+            const int64_t ex = wave_shr1_i64(inc, carry);
+            if (j < K) pm[j] = ex;
+            carry = readlane_i64(inc, 63);
+        }
+        if (lane == 0) pm[K] = carry;
+        carry = INT64_MIN;
+        for (int c = 0; c < K; c += 64) {                // SM: inclusive suffix max of L[j]
+            const int j = K - 1 - (c + lane);
+            const int64_t x = j >= 0 ? L[j] : INT64_MIN;
+            const int64_t inc = imax(wave_incl_max_i64(x), carry);
+            if (j >= 0) sm[j] = inc;
+            carry = readlane_i64(inc, 63);
+        }
+        if (lane == 0) sm[K] = INT64_MIN;
+    }
+}
+
+// Score of moving a request with terms (ke, alpha, p) to t, from PM/SM rows
+// of stride K+1 and a curve row L_t whose entry K reads as -inf.
+__device__ inline int64_t move_score(const int64_t* pm_t, const int64_t* sm_t, int64_t l_ke, int ke,
+                                     int K, int64_t alpha, int64_t p) {
+    const int64_t a = pm_t[ke] + alpha;              // PM_t[0] = -inf + alpha: no overflow
+    const int64_t m = l_ke + p;
+    const int64_t c = sm_t[ke + 1 < K ? ke + 1 : K];
+    return imax(imax(a, m), c);
 }
 
 // ---------------------------------------------------------------------------
@@ -104,7 +215,7 @@ __global__ __launch_bounds__(PREP_THREADS) void score_prep_kernel(const int64_t*
 }
 
 // ---------------------------------------------------------------------------
-// score
+// score (multi-workgroup path)
 // ---------------------------------------------------------------------------
 struct ScoreArgs {
     const int32_t* cur;
@@ -118,6 +229,7 @@ struct ScoreArgs {
     int64_t* best_score;
     int32_t* err_word;
     int N, n, b, K, rpb, cand;
+    uint32_t magic_K;
 };
 
 template <bool kFused>
@@ -145,7 +257,6 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
     const int row0 = blockIdx.x * rpb;
     const int64_t H = (int64_t)b * K;
     const int64_t bb = (int64_t)b * b;
-    const int64_t bb2 = (int64_t)b * (b - 1) / 2;
 
     // 0) per-request values; curves into LDS.  All reads are issued before
     //    the first is used (clamped indices, unconditional loads).
@@ -174,29 +285,13 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
         for (int j = 0; j < 2; ++j) {
             const int q = q0 + j * SC_THREADS + tid;
             if (q >= rpb) continue;
-            const int r = row0 + q;
-            int s = -1;
-            if (r < a.N) {
-                s = sv[j];
-                const int cr = cv[j];
-                const int lr = rv[j];
-                int32_t f = 0;
-                if (s < 0 || s >= n) f |= STAR_DEV_BAD_INST;
-                if (cr < 1) f |= STAR_DEV_BAD_CUR;
-                if (lr < 1) f |= STAR_DEV_BAD_REM;
-                bad |= f;
-                if (f) {
-                    s = -1;
-                } else {
-                    const int64_t lp = (int64_t)lr < H ? (int64_t)lr : H;
-                    const int64_t ke = lp / b;
-                    const int64_t mu = lp - ke * b;
-                    r_alpha[q] = (int64_t)b * cr + bb2;
-                    r_p[q] = mu * cr + mu * ke * b + mu * (mu - 1) / 2;
-                    r_ke[q] = (int32_t)ke;
-                }
-            }
-            r_s[q] = s;
+            const bool live = row0 + q < a.N;
+            const ReqTerms rt = request_terms(sv[j], cv[j], rv[j], n, b, H);
+            bad |= live ? rt.bad : 0;
+            r_s[q] = live ? rt.s : -1;
+            r_ke[q] = rt.ke;
+            r_alpha[q] = rt.alpha;
+            r_p[q] = rt.p;
         }
     }
     bad = wave_or_i32(bad);
@@ -206,52 +301,17 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
         for (int j = 0; j < SC_LBATCH; ++j) {
             const int e = j * SC_THREADS + tid;
             if (e < nK) {
-                const int t = e / K, k = e - t * K;
-                lL[t * K1 + k] = lv[j];
+                const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
+                lL[t * K1 + (e - t * K)] = lv[j];
             }
         }
+        for (int t = tid; t < n; t += SC_THREADS) lL[t * K1 + K] = INT64_MIN;
         __syncthreads();
-        // Per instance (one wave each, round robin): every lane reduces a
-        // contiguous segment of SEG buckets serially, one DPP wavefront scan
-        // combines the 64 segment maxima, and a second serial pass writes.
-        // For the suffix maxima lane l takes segment 63 - l, so that a
-        // prefix scan over lanes is a suffix scan over buckets.
-        const int SEG = (K + 63) >> 6;
-        for (int t = wid; t < n; t += SC_THREADS / 64) {
-            const int64_t* L = lL + t * K1;
-            int64_t* pm = lPM + t * K1;
-            int64_t* sm = lSM + t * K1;
-            const int f0 = lane * SEG;
-            const int f1 = f0 + SEG < K ? f0 + SEG : K;
-            const int g0 = (63 - lane) * SEG;
-            const int g1 = g0 + SEG < K ? g0 + SEG : K;
-            int64_t fwd = INT64_MIN, bwd = INT64_MIN;
-            for (int u = 0; u < SEG; ++u) {
-                if (f0 + u < f1) fwd = imax(fwd, L[f0 + u] + bb * (f0 + u));
-                if (g0 + u < g1) bwd = imax(bwd, L[g0 + u]);
-            }
-            const int64_t finc = wave_incl_max_i64(fwd);
-            const int64_t binc = wave_incl_max_i64(bwd);
-            int64_t fex = __shfl_up(finc, 1, 64);
-            int64_t bex = __shfl_up(binc, 1, 64);
-            if (lane == 0) { fex = INT64_MIN; bex = INT64_MIN; }
-            for (int j = f0; j < f1; ++j) {
-                pm[j] = fex;
-                fex = imax(fex, L[j] + bb * j);
-            }
-            for (int j = g1 - 1; j >= g0; --j) {
-                bex = imax(bex, L[j]);
-                sm[j] = bex;
-            }
-            if (lane == 63) pm[K] = finc;
-            if (lane == 0) sm[K] = INT64_MIN;
-        }
+        build_pm_sm(lL, lPM, lSM, n, K, bb, wid, SC_THREADS / 64);
     }
     __syncthreads();
-    const int64_t* gL = kFused ? lL : a.load;
     const int64_t* gPM = kFused ? lPM : a.PM;
     const int64_t* gSM = kFused ? lSM : a.SM;
-    const int Ls = kFused ? K1 : K;              // row stride of the curve array
 
     // 1) candidates -> scores and keys (self-candidates and invalid requests
     //    get the +inf key)
@@ -262,20 +322,20 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
         const int r = row0 + q;
         if (r < a.N) {
             const int s = r_s[q];
-            int64_t sc = -1;
-            if (s >= 0) {
-                const int64_t* sm = gSM + (int64_t)t * K1;
-                if (t == s) {
-                    sc = sm[0];
-                } else {
-                    const int ke = r_ke[q];
-                    sc = INT64_MIN;
-                    if (ke >= 1) sc = imax(sc, gPM[(int64_t)t * K1 + ke] + r_alpha[q]);
-                    if (ke < K) sc = imax(sc, gL[(int64_t)t * Ls + ke] + r_p[q]);
-                    if (ke + 1 < K) sc = imax(sc, sm[ke + 1]);
-                    key_s = sc;
-                    key_i = (uint32_t)((int64_t)r * n + t);
-                }
+            const int ke = r_ke[q];
+            int64_t l_ke;
+            if constexpr (kFused) {
+                l_ke = lL[t * K1 + ke];                    // entry K is -inf
+            } else {
+                l_ke = ke < K ? a.load[(int64_t)t * K + (ke < K ? ke : K - 1)] : INT64_MIN;
+            }
+            const int64_t* pm_t = gPM + (int64_t)t * K1;
+            const int64_t* sm_t = gSM + (int64_t)t * K1;
+            const int64_t mv = move_score(pm_t, sm_t, l_ke, ke, K, r_alpha[q], r_p[q]);
+            const int64_t sc = s < 0 ? -1 : (t == s ? sm_t[0] : mv);
+            if (s >= 0 && t != s) {
+                key_s = sc;
+                key_i = (uint32_t)((int64_t)r * n + t);
             }
             if (a.scores) a.scores[(int64_t)r * n + t] = sc;
         }
@@ -301,81 +361,78 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// top-k: block-wide helpers (1024 threads)
+// block-wide helpers for a workgroup of kT threads (full exec mask)
 // ---------------------------------------------------------------------------
-struct TkShared {
-    int hist[TK_BINS];
-    int wsum[TK_THREADS / 64];
-    int64_t red64[TK_THREADS / 64];
-    int64_t bcast[4];
+template <int kT>
+struct alignas(16) SelShared {
+    static constexpr int W = kT / 64;
+    int hist[SEL_BINS];           // digit histogram (int4-accessed); bucket offsets when ordering
+    int fill[SEL_BINS];           // bucket fill counters when ordering
+    int wcnt[W];
+    int64_t wlo[W];
+    int64_t whi[W];
+    alignas(16) int bcast[4];
 };
 
-// Sum of one int over the block; every thread gets the total.
-__device__ inline int block_sum_i32(int v, TkShared& sh) {
+__device__ inline int wave_total_add_i32(int v) {
+    return __builtin_amdgcn_readlane(wave_incl_add_i32(v), 63);
+}
+
+// Count, min and max over the block in one LDS round; every thread gets them.
+template <int kT>
+__device__ inline void block_stats(int cnt, int64_t lo, int64_t hi, SelShared<kT>& sh, int* total,
+                                   int64_t* mn, int64_t* mx) {
+    constexpr int W = kT / 64;
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    v = wave_incl_add_i32(v);
-    if (lane == 63) sh.wsum[wid] = v;
+    cnt = wave_total_add_i32(cnt);
+    const int64_t nlo = readlane_i64(wave_incl_max_i64(-lo), 63);
+    hi = readlane_i64(wave_incl_max_i64(hi), 63);
+    if (lane == 0) {
+        sh.wcnt[wid] = cnt;
+        sh.wlo[wid] = -nlo;
+        sh.whi[wid] = hi;
+    }
     __syncthreads();
-    int t = 0;
-#pragma unroll
-    for (int w = 0; w < TK_THREADS / 64; ++w) t += sh.wsum[w];
+    const int c = lane < W ? sh.wcnt[lane] : 0;
+    const int64_t l = lane < W ? -sh.wlo[lane] : -kInfS;
+    const int64_t h = lane < W ? sh.whi[lane] : -1;
+    *total = wave_total_add_i32(c);
+    *mn = -readlane_i64(wave_incl_max_i64(l), 63);
+    *mx = readlane_i64(wave_incl_max_i64(h), 63);
     __syncthreads();
-    return t;
 }
 
 // Exclusive prefix of one int over the block (thread order); *total = sum.
-__device__ inline int block_excl_i32(int v, TkShared& sh, int* total) {
+template <int kT>
+__device__ inline int block_excl_i32(int v, SelShared<kT>& sh, int* total) {
+    constexpr int W = kT / 64;
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
     const int inc = wave_incl_add_i32(v);
-    if (lane == 63) sh.wsum[wid] = inc;
+    if (lane == 63) sh.wcnt[wid] = inc;
     __syncthreads();
-    int before = 0, all = 0;
-#pragma unroll
-    for (int w = 0; w < TK_THREADS / 64; ++w) {
-        const int x = sh.wsum[w];
-        before += w < wid ? x : 0;
-        all += x;
-    }
+    const int xs = wave_incl_add_i32(lane < W ? sh.wcnt[lane] : 0);
+    const int before = wid > 0 ? __builtin_amdgcn_readlane(xs, wid - 1) : 0;
+    *total = __builtin_amdgcn_readlane(xs, W - 1);
     __syncthreads();
-    *total = all;
     return before + inc - v;
 }
 
-// Min (kMin) or max of one int64 over the block; every thread gets it.
-template <bool kMin>
-__device__ inline int64_t block_minmax_i64(int64_t v, TkShared& sh) {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const int64_t u = __shfl_xor(v, o, 64);
-        v = kMin ? (u < v ? u : v) : (u > v ? u : v);
-    }
-    if (lane == 0) sh.red64[wid] = v;
-    __syncthreads();
-    int64_t r = sh.red64[0];
-#pragma unroll
-    for (int w = 1; w < TK_THREADS / 64; ++w) {
-        const int64_t x = sh.red64[w];
-        r = kMin ? (x < r ? x : r) : (x > r ? x : r);
-    }
-    __syncthreads();
-    return r;
-}
-
-// Key sources for block_select.  A source visits this thread's keys
-// (s, i), s >= 0, calling f(s, i); s == kInfS marks "no key".
+// ---------------------------------------------------------------------------
+// key sources: visit(f) calls f(s, i) on each of this thread's keys; s ==
+// kInfS marks "no key".  Every thread makes the same calls (uniform control).
+// ---------------------------------------------------------------------------
 template <int RJ>
-struct RegKeys {                  // keys held in registers
+struct RegKeys {                  // up to RJ keys in registers (nj slots used)
     int64_t s[RJ];
     uint32_t i[RJ];
+    int nj;
     template <class F>
     __device__ inline void visit(F&& f) const {
 #pragma unroll
-        for (int j = 0; j < RJ; ++j) f(s[j], i[j]);
+        for (int j = 0; j < RJ; ++j)
+            if (j < nj) f(s[j], i[j]);
     }
 };
-
-constexpr int TK_SBATCH = 8;      // global reads per thread in flight in a streaming visit
 
 struct BestKeys {                 // (best score, r) of every request with a migration
     const int64_t* best_score;
@@ -383,18 +440,18 @@ struct BestKeys {                 // (best score, r) of every request with a mig
     int N;
     template <class F>
     __device__ inline void visit(F&& f) const {
-        for (int r0 = 0; r0 < N; r0 += TK_THREADS * TK_SBATCH) {
-            int64_t bs[TK_SBATCH];
-            int32_t bt[TK_SBATCH];
+        for (int r0 = 0; r0 < N; r0 += TK_THREADS * SEL_SBATCH) {
+            int64_t bs[SEL_SBATCH];
+            int32_t bt[SEL_SBATCH];
 #pragma unroll
-            for (int u = 0; u < TK_SBATCH; ++u) {
+            for (int u = 0; u < SEL_SBATCH; ++u) {
                 const int r = r0 + u * TK_THREADS + (int)threadIdx.x;
                 const int rc = r < N ? r : N - 1;
                 bs[u] = best_score[rc];
                 bt[u] = best_target[rc];
             }
 #pragma unroll
-            for (int u = 0; u < TK_SBATCH; ++u) {
+            for (int u = 0; u < SEL_SBATCH; ++u) {
                 const int r = r0 + u * TK_THREADS + (int)threadIdx.x;
                 const bool ok = r < N && bt[u] >= 0;
                 f(ok ? bs[u] : kInfS, ok ? (uint32_t)r : kInfI);
@@ -403,29 +460,48 @@ struct BestKeys {                 // (best score, r) of every request with a mig
     }
 };
 
-struct PrunedKeys {               // every migration of the requests rk[0..nr)
-    const int64_t* scores;
+struct TopkArgs {
+    const int32_t* inst;
+    const int64_t* scores;        // [N, n] (caller's array or workspace copy)
+    const int32_t* best_target;   // [N]
+    const int64_t* best_score;    // [N]
+    int32_t* topk_req;
+    int32_t* topk_tgt;
+    int64_t* topk_score;
+    int N, n, top_k;
+    uint32_t magic_n, magic_n1;   // fast_div multipliers for n and n - 1
+};
+
+// Migration e of the pruned set: the v-th other instance of request rk[q],
+// with (q, v) = divmod(e, n - 1).
+__device__ inline void pruned_key(const TopkArgs& a, const int32_t* rk, const int32_t* rk_inst,
+                                  uint32_t e, int64_t* s, uint32_t* i) {
+    const uint32_t n1 = (uint32_t)a.n - 1;
+    const uint32_t q = fast_div(e, n1, a.magic_n1);
+    const int v = (int)(e - q * n1);
+    const int r = rk[q];
+    const int t = v < rk_inst[q] ? v : v + 1;             // skip staying put
+    *i = (uint32_t)((int64_t)r * a.n + t);
+    *s = a.scores[(int64_t)r * a.n + t];
+}
+
+struct PrunedKeys {               // every migration of the requests rk[0..nr), streamed
+    const TopkArgs* a;
     const int32_t* rk;            // LDS: request ids
     const int32_t* rk_inst;       // LDS: their instances
-    int nr, n;
+    int M;                        // nr * (n - 1)
     template <class F>
     __device__ inline void visit(F&& f) const {
-        const int M = nr * (n - 1);
-        for (int e0 = 0; e0 < M; e0 += TK_THREADS * TK_SBATCH) {
-            int64_t sv[TK_SBATCH];
-            uint32_t iv[TK_SBATCH];
+        for (int e0 = 0; e0 < M; e0 += TK_THREADS * SEL_SBATCH) {
+            int64_t sv[SEL_SBATCH];
+            uint32_t iv[SEL_SBATCH];
 #pragma unroll
-            for (int u = 0; u < TK_SBATCH; ++u) {
+            for (int u = 0; u < SEL_SBATCH; ++u) {
                 const int e = e0 + u * TK_THREADS + (int)threadIdx.x;
-                const int ec = e < M ? e : M - 1;
-                const int q = ec / (n - 1), v = ec - q * (n - 1);
-                const int r = rk[q];
-                const int t = v < rk_inst[q] ? v : v + 1;     // skip staying put
-                iv[u] = (uint32_t)((int64_t)r * n + t);
-                sv[u] = scores[(int64_t)r * n + t];
+                pruned_key(*a, rk, rk_inst, (uint32_t)(e < M ? e : M - 1), &sv[u], &iv[u]);
             }
 #pragma unroll
-            for (int u = 0; u < TK_SBATCH; ++u) {
+            for (int u = 0; u < SEL_SBATCH; ++u) {
                 const int e = e0 + u * TK_THREADS + (int)threadIdx.x;
                 f(e < M ? sv[u] : kInfS, e < M ? iv[u] : kInfI);
             }
@@ -433,40 +509,158 @@ struct PrunedKeys {               // every migration of the requests rk[0..nr)
     }
 };
 
-// Returns the upper bound U = (us, ui) such that exactly min(k, #keys)
-// keys of the source are <= U.
-template <class Src>
-__device__ void block_select(const Src& src, int k, TkShared& sh, int64_t* us, uint32_t* ui) {
-    int mine = 0;
-    int64_t lo = kInfS, hi = -1;
-    src.visit([&](int64_t s, uint32_t) {
-        if (s != kInfS) {
-            ++mine;
-            lo = s < lo ? s : lo;
-            hi = s > hi ? s : hi;
+// Register loaders of the 1024-thread top-k (all reads issued first).
+__device__ inline void load_migrations(RegKeys<TK_RJ>& k, const TopkArgs& a) {
+    const int M = a.N * a.n;
+    k.nj = (M + TK_THREADS - 1) / TK_THREADS;
+    int32_t iv[TK_RJ], bv[TK_RJ];
+    uint32_t qv[TK_RJ];
+#pragma unroll
+    for (int j = 0; j < TK_RJ; ++j) {
+        if (j < k.nj) {
+            const int e = j * TK_THREADS + (int)threadIdx.x;
+            const uint32_t ec = (uint32_t)(e < M ? e : M - 1);
+            qv[j] = fast_div(ec, (uint32_t)a.n, a.magic_n);
+            k.s[j] = a.scores[ec];
+            iv[j] = a.inst[qv[j]];
+            bv[j] = a.best_target[qv[j]];
         }
-    });
-    const int total = block_sum_i32(mine, sh);
-    if (total <= k) {                              // every key is a winner
-        *us = kInfS - 1;
-        *ui = kInfI;
-        return;
     }
-    const int64_t smin = block_minmax_i64<true>(lo, sh);
-    const int64_t smax = block_minmax_i64<false>(hi, sh);
-    const uint64_t range = (uint64_t)(smax - smin);
-    int sbits = 0;
-    while (sbits < 64 && (range >> sbits) != 0) ++sbits;
+#pragma unroll
+    for (int j = 0; j < TK_RJ; ++j) {
+        if (j < k.nj) {
+            const int e = j * TK_THREADS + (int)threadIdx.x;
+            const bool ok = e < M && bv[j] >= 0 && (int)((uint32_t)e - qv[j] * (uint32_t)a.n) != iv[j];
+            k.s[j] = ok ? k.s[j] : kInfS;
+            k.i[j] = ok ? (uint32_t)e : kInfI;
+        }
+    }
+}
 
-    // digits over the (sbits + 32)-bit value (d << 32) | i, d = s - smin
-    uint64_t pd = 0, md = 0;                       // chosen prefix / mask on d
-    uint32_t pi = 0, mi = 0;                       // chosen prefix / mask on i
+__device__ inline void load_best(RegKeys<TK_RJ>& k, const TopkArgs& a) {
+    k.nj = (a.N + TK_THREADS - 1) / TK_THREADS;
+    int32_t bt[TK_RJ];
+#pragma unroll
+    for (int j = 0; j < TK_RJ; ++j) {
+        if (j < k.nj) {
+            const int r = j * TK_THREADS + (int)threadIdx.x;
+            const int rc = r < a.N ? r : a.N - 1;
+            k.s[j] = a.best_score[rc];
+            bt[j] = a.best_target[rc];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < TK_RJ; ++j) {
+        if (j < k.nj) {
+            const int r = j * TK_THREADS + (int)threadIdx.x;
+            const bool ok = r < a.N && bt[j] >= 0;
+            k.s[j] = ok ? k.s[j] : kInfS;
+            k.i[j] = ok ? (uint32_t)r : kInfI;
+        }
+    }
+}
+
+__device__ inline void load_pruned(RegKeys<TK_RJ>& k, const TopkArgs& a, const int32_t* rk,
+                                   const int32_t* rk_inst, int M) {
+    k.nj = (M + TK_THREADS - 1) / TK_THREADS;
+#pragma unroll
+    for (int j = 0; j < TK_RJ; ++j) {
+        if (j < k.nj) {
+            const int e = j * TK_THREADS + (int)threadIdx.x;
+            pruned_key(a, rk, rk_inst, (uint32_t)(e < M ? e : M - 1), &k.s[j], &k.i[j]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < TK_RJ; ++j) {
+        if (j < k.nj) {
+            const int e = j * TK_THREADS + (int)threadIdx.x;
+            k.s[j] = e < M ? k.s[j] : kInfS;
+            k.i[j] = e < M ? k.i[j] : kInfI;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// radix select
+// ---------------------------------------------------------------------------
+template <int kT>
+__device__ inline void clear_bins(int* h) {
+    for (int q = threadIdx.x * 4; q < SEL_BINS; q += kT * 4) *(int4*)&h[q] = make_int4(0, 0, 0, 0);
+}
+
+// The bin holding the kk-th key (1-based); updates kk to the rank inside it,
+// *cnt = its size.
+template <int kT>
+__device__ inline uint32_t find_bin(SelShared<kT>& sh, int* kk, int* cnt) {
+    constexpr int PER = SEL_BINS / kT;
+    static_assert(PER % 4 == 0, "int4 of bins per thread");
+    int c[PER], own = 0;
+#pragma unroll
+    for (int u = 0; u < PER; u += 4) {
+        const int4 c4 = *(const int4*)&sh.hist[threadIdx.x * PER + u];
+        c[u] = c4.x; c[u + 1] = c4.y; c[u + 2] = c4.z; c[u + 3] = c4.w;
+        own += c4.x + c4.y + c4.z + c4.w;
+    }
+    int tot;
+    int before = block_excl_i32<kT>(own, sh, &tot);
+    const int want = *kk;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        if (before < want && want <= before + c[u]) {
+            sh.bcast[0] = threadIdx.x * PER + u;
+            sh.bcast[1] = want - before;
+            sh.bcast[2] = c[u];
+        }
+        before += c[u];
+    }
+    __syncthreads();
+    const int4 b4 = *(const int4*)sh.bcast;
+    *kk = b4.y;
+    *cnt = b4.z;
+    __syncthreads();
+    return (uint32_t)b4.x;
+}
+
+// Keys packed as v = ((s - smin) << ibits) | i (nbits bits), a 64-bit value
+// that orders like (s, i).  Returns the bound U on v.
+template <int kT, class Src>
+__device__ uint64_t select_packed(const Src& src, int k, int64_t smin, int nbits, int ibits,
+                                  SelShared<kT>& sh) {
+    uint64_t prefix = 0;                  // v >> pos == prefix for the keys still in play
+    int kk = k, pos = nbits;
+    while (pos > 0) {
+        const int lowbit = pos > SEL_DIGIT ? pos - SEL_DIGIT : 0;
+        const uint32_t mask = (1u << (pos - lowbit)) - 1;
+        clear_bins<kT>(sh.hist);
+        __syncthreads();
+        src.visit([&](int64_t s, uint32_t i) {
+            if (s == kInfS) return;
+            const uint64_t v = ((uint64_t)(s - smin) << ibits) | i;
+            if (pos < 64 && (v >> pos) != prefix) return;
+            atomicAdd(&sh.hist[(uint32_t)(v >> lowbit) & mask], 1);
+        });
+        __syncthreads();
+        int cnt;
+        const uint32_t bin = find_bin<kT>(sh, &kk, &cnt);
+        prefix = (prefix << (pos - lowbit)) | bin;
+        pos = lowbit;
+        if (cnt == kk) break;             // the whole bin is needed
+    }
+    return (prefix << pos) | ((1ull << pos) - 1);
+}
+
+// Wide keys (score range and index need more than 64 bits): digits over the
+// (sbits + 32)-bit value (d << 32) | i, d = s - smin.  Returns U as (us, ui).
+template <int kT, class Src>
+__device__ void select_wide(const Src& src, int k, int64_t smin, int sbits, SelShared<kT>& sh,
+                            int64_t* us, uint32_t* ui) {
+    uint64_t pd = 0, md = 0;              // chosen prefix / mask on d
+    uint32_t pi = 0, mi = 0;              // chosen prefix / mask on i
     int kk = k;
-    bool done = false;
-    for (int pos = sbits + 32; pos > 0 && !done; pos -= TK_DIGIT) {
-        const int lowbit = pos > TK_DIGIT ? pos - TK_DIGIT : 0;     // digit bits [lowbit, pos)
+    for (int pos = sbits + 32; pos > 0;) {
+        const int lowbit = pos > SEL_DIGIT ? pos - SEL_DIGIT : 0;     // digit bits [lowbit, pos)
         const int width = pos - lowbit;
-        for (int b = threadIdx.x; b < TK_BINS; b += TK_THREADS) sh.hist[b] = 0;
+        clear_bins<kT>(sh.hist);
         __syncthreads();
         src.visit([&](int64_t s, uint32_t i) {
             if (s == kInfS) return;
@@ -476,34 +670,11 @@ __device__ void block_select(const Src& src, int k, TkShared& sh, int64_t* us, u
             if (lowbit >= 32) dig = (uint32_t)(d >> (lowbit - 32));
             else if (pos <= 32) dig = i >> lowbit;
             else dig = (uint32_t)((d << (32 - lowbit)) | (i >> lowbit));
-            dig &= (1u << width) - 1;
-            atomicAdd(&sh.hist[dig], 1);
+            atomicAdd(&sh.hist[dig & ((1u << width) - 1)], 1);
         });
         __syncthreads();
-        // find the bin holding the kk-th key: each thread owns PER bins
-        constexpr int PER = TK_BINS / TK_THREADS;
-        int c[PER], own = 0;
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            c[u] = sh.hist[threadIdx.x * PER + u];
-            own += c[u];
-        }
-        int tot;
-        int before = block_excl_i32(own, sh, &tot);
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            if (before < kk && kk <= before + c[u]) {
-                sh.bcast[0] = threadIdx.x * PER + u;
-                sh.bcast[1] = kk - before;
-                sh.bcast[2] = c[u];
-            }
-            before += c[u];
-        }
-        __syncthreads();
-        const uint32_t bin = (uint32_t)sh.bcast[0];
-        kk = (int)sh.bcast[1];
-        const int cnt = (int)sh.bcast[2];
-        __syncthreads();
+        int cnt;
+        const uint32_t bin = find_bin<kT>(sh, &kk, &cnt);
         for (int bit = lowbit; bit < pos; ++bit) {  // extend the prefix by this digit
             const uint32_t v = (bin >> (bit - lowbit)) & 1u;
             if (bit >= 32) {
@@ -514,27 +685,63 @@ __device__ void block_select(const Src& src, int k, TkShared& sh, int64_t* us, u
                 pi |= v << bit;
             }
         }
-        done = cnt == kk;                          // the whole bin is needed
+        pos = lowbit;
+        if (cnt == kk) break;
     }
-    // U: the prefix with every unchosen bit set (within the sbits bits every
-    // d has); no overflow since smin + 2^sbits <= 2 smax + 1 < 2^63
+    // U: the prefix with every unchosen bit set, within the sbits bits every
+    // d has (smin + 2^sbits - 1 <= 2 smax < 2^63: no overflow)
     uint64_t du = pd | ~md;
     du &= sbits >= 64 ? ~0ull : ((1ull << sbits) - 1);
     *us = smin + (int64_t)du;
     *ui = pi | ~mi;
 }
 
+// Given the source's count / min / max, the bound U = (us, ui) such that
+// exactly min(k, total) keys are <= U.  ibits: bits of the largest index.
+template <int kT, class Src>
+__device__ void select_bound(const Src& src, int k, int ibits, int total, int64_t smin,
+                             int64_t smax, SelShared<kT>& sh, int64_t* us, uint32_t* ui) {
+    if (total <= k) {                     // every key is a winner
+        *us = kInfS - 1;
+        *ui = kInfI;
+        return;
+    }
+    const int sbits = bit_length((uint64_t)(smax - smin));
+    if (sbits + ibits <= 64) {
+        const uint64_t U = select_packed<kT>(src, k, smin, sbits + ibits, ibits, sh);
+        *us = smin + (int64_t)(U >> ibits);
+        *ui = (uint32_t)(U & ((1ull << ibits) - 1));
+    } else {
+        select_wide<kT>(src, k, smin, sbits, sh, us, ui);
+    }
+}
+
+template <int kT, class Src>
+__device__ void source_stats(const Src& src, SelShared<kT>& sh, int* total, int64_t* smin,
+                             int64_t* smax) {
+    int mine = 0;
+    int64_t lo = kInfS, hi = -1;
+    src.visit([&](int64_t s, uint32_t) {
+        if (s != kInfS) {
+            ++mine;
+            lo = s < lo ? s : lo;
+            hi = s > hi ? s : hi;
+        }
+    });
+    block_stats<kT>(mine, lo, hi, sh, total, smin, smax);
+}
+
 // Writes the source's keys <= U to (os, oi) in thread order; returns their
 // count (every thread gets it).
-template <class Src>
-__device__ int block_gather(const Src& src, int64_t us, uint32_t ui, TkShared& sh, int64_t* os,
-                            uint32_t* oi, int cap) {
+template <int kT, class Src>
+__device__ int block_gather(const Src& src, int64_t us, uint32_t ui, SelShared<kT>& sh,
+                            int64_t* os, uint32_t* oi, int cap) {
     int mine = 0;
     src.visit([&](int64_t s, uint32_t i) {
         if (s != kInfS && !key_less(us, ui, s, i)) ++mine;
     });
     int total;
-    int at = block_excl_i32(mine, sh, &total);
+    int at = block_excl_i32<kT>(mine, sh, &total);
     src.visit([&](int64_t s, uint32_t i) {
         if (s != kInfS && !key_less(us, ui, s, i)) {
             if (at < cap) {
@@ -548,96 +755,324 @@ __device__ int block_gather(const Src& src, int64_t us, uint32_t ui, TkShared& s
     return total < cap ? total : cap;
 }
 
-// ---------------------------------------------------------------------------
-// top-k kernel
-// ---------------------------------------------------------------------------
-struct TopkArgs {
-    const int32_t* inst;
-    const int64_t* scores;        // [N, n] (caller's array or workspace copy)
-    const int32_t* best_target;   // [N]
-    const int64_t* best_score;    // [N]
-    int32_t* topk_req;
-    int32_t* topk_tgt;
-    int64_t* topk_score;
-    int N, n, top_k;
-};
-
-__device__ inline void rank_and_write(const TopkArgs& a, const int64_t* ws_s, const uint32_t* ws_i,
-                                      int nw) {
-    for (int w = threadIdx.x; w < nw; w += TK_THREADS) {
-        const int64_t xs = ws_s[w];
-        const uint32_t xi = ws_i[w];
-        int rank = 0;
-        for (int j = 0; j < nw; ++j) rank += key_less(ws_s[j], ws_i[j], xs, xi) ? 1 : 0;
-        a.topk_req[rank] = (int32_t)(xi / (uint32_t)a.n);
-        a.topk_tgt[rank] = (int32_t)(xi % (uint32_t)a.n);
-        a.topk_score[rank] = xs;
+// Puts the nw winners (ws_s, ws_i), all with score in [smin, smax_w], in key
+// order and writes them as (i / n, i % n, s); -1 past nw up to top_k.
+// Bucket sort on the top SEL_DIGIT bits of the packed key, then a rank
+// count among the members of each bucket.
+template <int kT>
+__device__ void order_and_write(const int64_t* ws_s, const uint32_t* ws_i, int nw, int64_t smin,
+                                int64_t smax_w, int ibits, int n, uint32_t magic_n,
+                                int32_t* out_r, int32_t* out_t, int64_t* out_s, int top_k,
+                                SelShared<kT>& sh, uint64_t* sv) {
+    const int tid = threadIdx.x;
+    const int sbits = nw > 0 ? bit_length((uint64_t)(smax_w - smin)) : 0;
+    const uint64_t imask = (1ull << ibits) - 1;
+    if (nw > 0 && sbits + ibits <= 64) {
+        const int nbits = sbits + ibits;
+        const int shift = nbits > SEL_DIGIT ? nbits - SEL_DIGIT : 0;
+        clear_bins<kT>(sh.hist);
+        clear_bins<kT>(sh.fill);
+        __syncthreads();
+        for (int p = tid; p < nw; p += kT) {
+            const uint64_t v = ((uint64_t)(ws_s[p] - smin) << ibits) | ws_i[p];
+            atomicAdd(&sh.hist[(uint32_t)(v >> shift)], 1);
+        }
+        __syncthreads();
+        {                                                   // counts -> exclusive offsets
+            constexpr int PER = SEL_BINS / kT;
+            int c[PER], own = 0;
+#pragma unroll
+            for (int u = 0; u < PER; ++u) {
+                c[u] = sh.hist[tid * PER + u];
+                own += c[u];
+            }
+            int tot;
+            int before = block_excl_i32<kT>(own, sh, &tot);
+#pragma unroll
+            for (int u = 0; u < PER; ++u) {
+                sh.hist[tid * PER + u] = before;
+                before += c[u];
+            }
+        }
+        __syncthreads();
+        for (int p = tid; p < nw; p += kT) {
+            const uint64_t v = ((uint64_t)(ws_s[p] - smin) << ibits) | ws_i[p];
+            const uint32_t bkt = (uint32_t)(v >> shift);
+            sv[sh.hist[bkt] + atomicAdd(&sh.fill[bkt], 1)] = v;
+        }
+        __syncthreads();
+        for (int q = tid; q < nw; q += kT) {
+            const uint64_t v = sv[q];
+            const uint32_t bkt = (uint32_t)(v >> shift);
+            const int lo = sh.hist[bkt], cnt = sh.fill[bkt];
+            int rank = 0;
+            for (int j = lo; j < lo + cnt; ++j) rank += sv[j] < v ? 1 : 0;
+            const int pos = lo + rank;
+            const uint32_t i = (uint32_t)(v & imask);
+            const uint32_t r = fast_div(i, (uint32_t)n, magic_n);
+            out_r[pos] = (int32_t)r;
+            out_t[pos] = (int32_t)(i - r * (uint32_t)n);
+            out_s[pos] = smin + (int64_t)(v >> ibits);
+        }
+    } else if (nw > 0) {                                    // rank count over all winners
+        for (int w = tid; w < nw; w += kT) {
+            const int64_t xs = ws_s[w];
+            const uint32_t xi = ws_i[w];
+            int rank = 0;
+            for (int j = 0; j < nw; ++j) rank += key_less(ws_s[j], ws_i[j], xs, xi) ? 1 : 0;
+            const uint32_t r = fast_div(xi, (uint32_t)n, magic_n);
+            out_r[rank] = (int32_t)r;
+            out_t[rank] = (int32_t)(xi - r * (uint32_t)n);
+            out_s[rank] = xs;
+        }
     }
-    for (int q = nw + threadIdx.x; q < a.top_k; q += TK_THREADS) {
-        a.topk_req[q] = -1;
-        a.topk_tgt[q] = -1;
-        a.topk_score[q] = -1;
+    for (int q = nw + tid; q < top_k; q += kT) {
+        out_r[q] = -1;
+        out_t[q] = -1;
+        out_s[q] = -1;
     }
 }
 
-// Every migration of every request held in registers (N n <= RJ * 1024).
-template <int RJ>
+// Full selection over a source: stats, bound, gather, order, write.
+template <int kT, class Src>
+__device__ int select_top(const Src& src, int k, int ibits, SelShared<kT>& sh, int64_t* ws_s,
+                          uint32_t* ws_i, int64_t* smin_out, int64_t* smax_w_out) {
+    int total;
+    int64_t smin, smax, us;
+    uint32_t ui;
+    source_stats<kT>(src, sh, &total, &smin, &smax);
+    select_bound<kT>(src, k, ibits, total, smin, smax, sh, &us, &ui);
+    *smin_out = smin;
+    *smax_w_out = us < smax ? us : smax;
+    return block_gather<kT>(src, us, ui, sh, ws_s, ws_i, STAR_MAX_TOP_K);
+}
+
+// ---------------------------------------------------------------------------
+// top-k kernels of the multi-workgroup path (one workgroup)
+// ---------------------------------------------------------------------------
+// Every migration held in registers (N n <= TK_REG_KEYS).
 __global__ __launch_bounds__(TK_THREADS) void topk_direct_kernel(TopkArgs a) {
-    __shared__ TkShared sh;
+    __shared__ SelShared<TK_THREADS> sh;
     __shared__ int64_t ws_s[STAR_MAX_TOP_K];
     __shared__ uint32_t ws_i[STAR_MAX_TOP_K];
-    const int tid = threadIdx.x;
-    const int n = a.n, M = a.N * a.n;
-    RegKeys<RJ> keys;
-    {
-        int64_t sv[RJ];
-        int32_t iv[RJ], bv[RJ];
-#pragma unroll
-        for (int j = 0; j < RJ; ++j) {
-            const int e = j * TK_THREADS + tid;
-            const int ec = e < M ? e : M - 1;
-            sv[j] = a.scores[ec];
-            iv[j] = a.inst[ec / n];
-            bv[j] = a.best_target[ec / n];
-        }
-#pragma unroll
-        for (int j = 0; j < RJ; ++j) {
-            const int e = j * TK_THREADS + tid;
-            const bool ok = e < M && bv[j] >= 0 && (e % n) != iv[j];
-            keys.s[j] = ok ? sv[j] : kInfS;
-            keys.i[j] = ok ? (uint32_t)e : kInfI;
-        }
-    }
-    int64_t us;
-    uint32_t ui;
-    block_select(keys, a.top_k, sh, &us, &ui);
-    const int nw = block_gather(keys, us, ui, sh, ws_s, ws_i, STAR_MAX_TOP_K);
-    rank_and_write(a, ws_s, ws_i, nw);
+    __shared__ uint64_t sv[STAR_MAX_TOP_K];
+    RegKeys<TK_RJ> keys;
+    load_migrations(keys, a);
+    const int ibits = bit_length((uint64_t)(a.N * a.n - 1));
+    int64_t smin, smax_w;
+    const int nw = select_top<TK_THREADS>(keys, a.top_k, ibits, sh, ws_s, ws_i, &smin, &smax_w);
+    order_and_write<TK_THREADS>(ws_s, ws_i, nw, smin, smax_w, ibits, a.n, a.magic_n, a.topk_req,
+                                a.topk_tgt, a.topk_score, a.top_k, sh, sv);
 }
 
 // First the k requests with the smallest best keys, then the k smallest of
-// their migrations (both streamed from global memory).
+// their migrations; each stage in registers when it fits, else streamed.
+template <bool kReg1, bool kReg2>
 __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
-    __shared__ TkShared sh;
+    __shared__ SelShared<TK_THREADS> sh;
     __shared__ int64_t ws_s[STAR_MAX_TOP_K];
     __shared__ uint32_t ws_i[STAR_MAX_TOP_K];
+    __shared__ uint64_t sv[STAR_MAX_TOP_K];
     __shared__ int32_t rk[STAR_MAX_TOP_K];
     __shared__ int32_t rk_inst[STAR_MAX_TOP_K];
-    BestKeys bk{a.best_score, a.best_target, a.N};
-    int64_t us;
-    uint32_t ui;
-    block_select(bk, a.top_k, sh, &us, &ui);
-    const int nr = block_gather(bk, us, ui, sh, ws_s, ws_i, STAR_MAX_TOP_K);
+    int nr;
+    int64_t smin, smax_w;
+    const int ib1 = bit_length((uint64_t)(a.N - 1));
+    if constexpr (kReg1) {
+        RegKeys<TK_RJ> keys;
+        load_best(keys, a);
+        nr = select_top<TK_THREADS>(keys, a.top_k, ib1, sh, ws_s, ws_i, &smin, &smax_w);
+    } else {
+        BestKeys bk{a.best_score, a.best_target, a.N};
+        nr = select_top<TK_THREADS>(bk, a.top_k, ib1, sh, ws_s, ws_i, &smin, &smax_w);
+    }
     for (int q = threadIdx.x; q < nr; q += TK_THREADS) {
         const int r = (int)ws_i[q];
         rk[q] = r;
         rk_inst[q] = a.inst[r];
     }
     __syncthreads();
-    PrunedKeys pk{a.scores, rk, rk_inst, nr, a.n};
-    block_select(pk, a.top_k, sh, &us, &ui);
-    const int nw = block_gather(pk, us, ui, sh, ws_s, ws_i, STAR_MAX_TOP_K);
-    rank_and_write(a, ws_s, ws_i, nw);
+    const int M = nr * (a.n - 1);
+    const int ib2 = bit_length((uint64_t)((int64_t)a.N * a.n - 1));
+    int nw;
+    if constexpr (kReg2) {
+        RegKeys<TK_RJ> keys;
+        load_pruned(keys, a, rk, rk_inst, M);
+        nw = select_top<TK_THREADS>(keys, a.top_k, ib2, sh, ws_s, ws_i, &smin, &smax_w);
+    } else {
+        PrunedKeys pk{&a, rk, rk_inst, M};
+        nw = select_top<TK_THREADS>(pk, a.top_k, ib2, sh, ws_s, ws_i, &smin, &smax_w);
+    }
+    order_and_write<TK_THREADS>(ws_s, ws_i, nw, smin, smax_w, ib2, a.n, a.magic_n, a.topk_req,
+                                a.topk_tgt, a.topk_score, a.top_k, sh, sv);
+}
+
+// ---------------------------------------------------------------------------
+// small rounds: one workgroup scores and ranks
+// ---------------------------------------------------------------------------
+struct SmallArgs {
+    const int32_t* cur;
+    const int32_t* rem;
+    const int32_t* inst;
+    const int64_t* load;
+    int64_t* scores;              // [N, n] or NULL
+    int32_t* best_target;         // [N] or NULL
+    int64_t* best_score;          // [N] or NULL
+    int32_t* topk_req;            // [top_k] (top_k > 0)
+    int32_t* topk_tgt;
+    int64_t* topk_score;
+    int32_t* err_word;
+    int N, n, b, K, top_k;
+    uint32_t magic_n, magic_K;
+};
+
+// Dynamic LDS: [L | PM | SM] (n (K+1) int64 each), alpha[N], p[N] (int64),
+// best[N] (uint64), ke[N], s[N] (int32).
+constexpr size_t SS_STATIC_LDS = sizeof(SelShared<SS_THREADS>) + STAR_MAX_TOP_K * (8 + 4 + 8);
+static size_t small_lds_bytes(int N, int n, int K) {
+    return (size_t)3 * n * (K + 1) * 8 + (size_t)N * (8 + 8 + 8 + 4 + 4);
+}
+
+__global__ __launch_bounds__(SS_THREADS) void score_small_kernel(SmallArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ SelShared<SS_THREADS> sh;
+    __shared__ int64_t ws_s[STAR_MAX_TOP_K];
+    __shared__ uint32_t ws_i[STAR_MAX_TOP_K];
+    __shared__ uint64_t sv[STAR_MAX_TOP_K];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int N = a.N, n = a.n, b = a.b, K = a.K, K1 = K + 1, E = n * K1;
+    int64_t* lL = (int64_t*)smem;
+    int64_t* lPM = lL + E;
+    int64_t* lSM = lPM + E;
+    int64_t* r_alpha = lSM + E;
+    int64_t* r_p = r_alpha + N;
+    uint64_t* r_best = (uint64_t*)(r_p + N);
+    int32_t* r_ke = (int32_t*)(r_best + N);
+    int32_t* r_s = r_ke + N;
+    const int64_t H = (int64_t)b * K;
+    const int64_t bb = (int64_t)b * b;
+
+    // 0) curves and requests: every read issued before the first is used
+    const int nK = n * K;
+    int64_t lv[SS_LBATCH];
+#pragma unroll
+    for (int j = 0; j < SS_LBATCH; ++j) {
+        const int e = j * SS_THREADS + tid;
+        lv[j] = a.load[e < nK ? e : nK - 1];
+    }
+    int sv_[SS_RBATCH], cv[SS_RBATCH], rv[SS_RBATCH];
+#pragma unroll
+    for (int j = 0; j < SS_RBATCH; ++j) {
+        const int r = j * SS_THREADS + tid;
+        const int rc = r < N ? r : N - 1;
+        sv_[j] = a.inst[rc];
+        cv[j] = a.cur[rc];
+        rv[j] = a.rem[rc];
+    }
+    int32_t bad = 0;
+#pragma unroll
+    for (int j = 0; j < SS_RBATCH; ++j) {
+        const int r = j * SS_THREADS + tid;
+        if (r < N) {
+            const ReqTerms rt = request_terms(sv_[j], cv[j], rv[j], n, b, H);
+            bad |= rt.bad;
+            r_s[r] = rt.s;
+            r_ke[r] = rt.ke;
+            r_alpha[r] = rt.alpha;
+            r_p[r] = rt.p;
+            r_best[r] = ~0ull;
+        }
+    }
+    bad = wave_or_i32(bad);
+    if (lane == 0) report_error(a.err_word, bad);
+#pragma unroll
+    for (int j = 0; j < SS_LBATCH; ++j) {
+        const int e = j * SS_THREADS + tid;
+        if (e < nK) {
+            const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
+            lL[t * K1 + (e - t * K)] = lv[j];
+        }
+    }
+    for (int t = tid; t < n; t += SS_THREADS) lL[t * K1 + K] = INT64_MIN;
+    __syncthreads();
+
+    // 1) PM/SM
+    build_pm_sm(lL, lPM, lSM, n, K, bb, wid, SS_THREADS / 64);
+    __syncthreads();
+
+    // 2) every candidate e = r n + t: score (written out), migration key in
+    //    registers
+    const int M = N * n;
+    RegKeys<SS_RJ> keys;
+    keys.nj = (M + SS_THREADS - 1) / SS_THREADS;
+#pragma unroll
+    for (int j = 0; j < SS_RJ; ++j) {
+        if (j < keys.nj) {
+            const int e = j * SS_THREADS + tid;
+            const uint32_t ec = (uint32_t)(e < M ? e : M - 1);
+            const int r = (int)fast_div(ec, (uint32_t)n, a.magic_n);
+            const int t = (int)ec - r * n;
+            const int s = r_s[r], ke = r_ke[r];
+            const int64_t* pm_t = lPM + t * K1;
+            const int64_t* sm_t = lSM + t * K1;
+            const int64_t mv = move_score(pm_t, sm_t, lL[t * K1 + ke], ke, K, r_alpha[r], r_p[r]);
+            const int64_t sc = s < 0 ? -1 : (t == s ? sm_t[0] : mv);
+            if (e < M && a.scores) a.scores[e] = sc;
+            const bool mig = e < M && s >= 0 && t != s;
+            keys.s[j] = mig ? sc : kInfS;
+            keys.i[j] = mig ? (uint32_t)e : kInfI;
+        }
+    }
+
+    // 3) best move per request: LDS atomic min of ((score - smin) << tbits) | t
+    //    when that fits 64 bits, else of (score - smin) and then of t among
+    //    the moves that reach it
+    int total;
+    int64_t smin, smax;
+    source_stats<SS_THREADS>(keys, sh, &total, &smin, &smax);
+    const int tbits = bit_length((uint64_t)(n - 1));
+    const uint64_t tmask = (1ull << tbits) - 1;
+    const bool packed = total > 0 && bit_length((uint64_t)(smax - smin)) + tbits <= 64;
+    if (total > 0) {
+        keys.visit([&](int64_t s, uint32_t i) {
+            if (s == kInfS) return;
+            const uint32_t r = fast_div(i, (uint32_t)n, a.magic_n);
+            const uint64_t d = (uint64_t)(s - smin);
+            atomicMin((unsigned long long*)&r_best[r],
+                      (unsigned long long)(packed ? (d << tbits) | (i - r * (uint32_t)n) : d));
+        });
+        if (!packed) {
+            for (int r = tid; r < N; r += SS_THREADS) r_ke[r] = -1;   // min target, as unsigned
+            __syncthreads();
+            keys.visit([&](int64_t s, uint32_t i) {
+                if (s == kInfS) return;
+                const uint32_t r = fast_div(i, (uint32_t)n, a.magic_n);
+                if ((uint64_t)(s - smin) == r_best[r])
+                    atomicMin((unsigned int*)&r_ke[r], i - r * (uint32_t)n);
+            });
+        }
+    }
+    __syncthreads();
+    for (int r = tid; r < N; r += SS_THREADS) {
+        const uint64_t v = r_best[r];
+        const bool none = v == ~0ull;
+        const int64_t bs = none ? -1 : smin + (int64_t)(packed ? v >> tbits : v);
+        const int32_t bt = none ? -1 : (packed ? (int32_t)(v & tmask) : r_ke[r]);
+        if (a.best_target) a.best_target[r] = bt;
+        if (a.best_score) a.best_score[r] = bs;
+    }
+
+    // 4) top-k
+    if (a.top_k > 0) {
+        const int ibits = bit_length((uint64_t)(M - 1));
+        int64_t us;
+        uint32_t ui;
+        select_bound<SS_THREADS>(keys, a.top_k, ibits, total, smin, smax, sh, &us, &ui);
+        const int nw = block_gather<SS_THREADS>(keys, us, ui, sh, ws_s, ws_i, STAR_MAX_TOP_K);
+        order_and_write<SS_THREADS>(ws_s, ws_i, nw, smin, us < smax ? us : smax, ibits, n,
+                                    a.magic_n, a.topk_req, a.topk_tgt, a.topk_score, a.top_k, sh,
+                                    sv);
+    }
 }
 
 __global__ void fill_i32_kernel(int32_t* p, int count, int32_t v) {
@@ -653,20 +1088,23 @@ ScorePlan plan_score(const star_score_params& p) {
     const int N = p.load.n_req;
     const int K1 = p.load.n_buckets + 1;
     pl.fused = (int64_t)n * K1 <= SC_FUSED_ENTRIES;
+    pl.small = pl.fused && N <= SS_MAX_REQ && (int64_t)N * n <= (int64_t)SS_RJ * SS_THREADS;
     pl.rpb = SC_CAND / n > 1 ? SC_CAND / n : 1;
     if (N > 0 && pl.rpb > N) pl.rpb = N;
     pl.cand = pl.rpb * n;
     pl.groups = N > 0 ? (int)ceil_div(N, pl.rpb) : 0;
     // top-k: select over all migrations when they fit one workgroup's
     // registers, else over the k requests with the smallest best keys first
-    const int64_t migr = (int64_t)N * n;
-    pl.topk_direct = migr <= TK_MAX_KEYS;
-    int rj = 1;
-    while ((int64_t)rj * TK_THREADS < migr && rj < TK_MAX_KEYS / TK_THREADS) rj *= 2;
-    pl.topk_rj = rj;
-    pl.topk_ok = true;
+    pl.topk_direct = (int64_t)N * n <= TK_REG_KEYS;
+    pl.topk_reg1 = N <= TK_REG_KEYS;
+    pl.topk_reg2 = (int64_t)p.top_k * (n - 1) <= TK_REG_KEYS;
 
     size_t off = STAR_WS_HEADER_BYTES;
+    if (pl.small) {
+        pl.total = off;
+        pl.lds = small_lds_bytes(N, n, p.load.n_buckets);
+        return pl;
+    }
     pl.pm_off = off;
     if (!pl.fused) off = align_up(off + (size_t)n * K1 * 8, 256);
     pl.sm_off = off;
@@ -682,13 +1120,17 @@ ScorePlan plan_score(const star_score_params& p) {
     return pl;
 }
 
+// Dynamic LDS beyond the default needs the kernel's limit raised (static +
+// dynamic stays within the 160 KB of a gfx950 CU).
+static hipError_t set_lds(const void* fn, size_t lds, size_t static_lds) {
+    if (lds + static_lds <= 64 * 1024) return hipSuccess;
+    return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+}
+
 template <bool kFused>
 static hipError_t launch_score_kernel(const ScorePlan& pl, const ScoreArgs& a, hipStream_t stream) {
-    if (pl.lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)score_kernel<kFused>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
-        if (e != hipSuccess) return e;
-    }
+    hipError_t e = set_lds((const void*)score_kernel<kFused>, pl.lds, 0);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(score_kernel<kFused>, dim3(pl.groups), dim3(SC_THREADS), pl.lds, stream, a);
     return hipGetLastError();
 }
@@ -698,9 +1140,9 @@ static hipError_t fill_i32(int32_t* p, int count, int32_t v, hipStream_t stream)
     return hipGetLastError();
 }
 
-template <int RJ>
-static hipError_t launch_topk_rj(const TopkArgs& a, hipStream_t stream) {
-    hipLaunchKernelGGL(topk_direct_kernel<RJ>, dim3(1), dim3(TK_THREADS), 0, stream, a);
+template <bool R1, bool R2>
+static hipError_t launch_topk_pruned(const TopkArgs& a, hipStream_t stream) {
+    hipLaunchKernelGGL((topk_pruned_kernel<R1, R2>), dim3(1), dim3(TK_THREADS), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -719,6 +1161,20 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
         }
         return hipSuccess;
     }
+    if (pl.small) {
+        SmallArgs s = {};
+        s.cur = cur; s.rem = rem; s.inst = inst; s.load = load;
+        s.scores = scores; s.best_target = best_target; s.best_score = best_score;
+        s.topk_req = topk_req; s.topk_tgt = topk_tgt; s.topk_score = topk_score;
+        s.err_word = err_word;
+        s.N = lp.n_req; s.n = lp.n_inst; s.b = lp.bucket; s.K = lp.n_buckets; s.top_k = p.top_k;
+        s.magic_n = div_magic((uint32_t)lp.n_inst);
+        s.magic_K = div_magic((uint32_t)lp.n_buckets);
+        hipError_t e = set_lds((const void*)score_small_kernel, pl.lds, SS_STATIC_LDS);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(score_small_kernel, dim3(1), dim3(SS_THREADS), pl.lds, stream, s);
+        return hipGetLastError();
+    }
     const bool need_all = p.top_k > 0;           // the top-k kernel reads scores and best moves
     ScoreArgs a = {};
     a.cur = cur; a.rem = rem; a.inst = inst; a.load = load;
@@ -730,6 +1186,7 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     a.err_word = err_word;
     a.N = lp.n_req; a.n = lp.n_inst; a.b = lp.bucket; a.K = lp.n_buckets;
     a.rpb = pl.rpb; a.cand = pl.cand;
+    a.magic_K = div_magic((uint32_t)lp.n_buckets);
     hipError_t e;
     if (pl.fused) {
         e = launch_score_kernel<true>(pl, a, stream);
@@ -755,18 +1212,16 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     t.best_score = a.best_score;
     t.topk_req = topk_req; t.topk_tgt = topk_tgt; t.topk_score = topk_score;
     t.N = lp.n_req; t.n = lp.n_inst; t.top_k = p.top_k;
-    if (!pl.topk_direct) {
-        hipLaunchKernelGGL(topk_pruned_kernel, dim3(1), dim3(TK_THREADS), 0, stream, t);
+    t.magic_n = div_magic((uint32_t)lp.n_inst);
+    t.magic_n1 = div_magic((uint32_t)lp.n_inst - 1);
+    if (pl.topk_direct) {
+        hipLaunchKernelGGL(topk_direct_kernel, dim3(1), dim3(TK_THREADS), 0, stream, t);
         return hipGetLastError();
     }
-    switch (pl.topk_rj) {
-        case 1: return launch_topk_rj<1>(t, stream);
-        case 2: return launch_topk_rj<2>(t, stream);
-        case 4: return launch_topk_rj<4>(t, stream);
-        case 8: return launch_topk_rj<8>(t, stream);
-        case 16: return launch_topk_rj<16>(t, stream);
-    }
-    return hipErrorInvalidValue;
+    if (pl.topk_reg1) return pl.topk_reg2 ? launch_topk_pruned<true, true>(t, stream)
+                                          : launch_topk_pruned<true, false>(t, stream);
+    return pl.topk_reg2 ? launch_topk_pruned<false, true>(t, stream)
+                        : launch_topk_pruned<false, false>(t, stream);
 }
 
 }  // namespace star

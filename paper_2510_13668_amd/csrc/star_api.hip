@@ -149,8 +149,7 @@ static star_status check_score_params(const star_score_params* p) {
 
 STAR_API size_t star_score_workspace_size(const star_score_params* p) {
     if (check_score_params(p) != STAR_OK) return 0;
-    const ScorePlan pl = plan_score(*p);
-    return pl.topk_ok ? pl.total : 0;
+    return plan_score(*p).total;
 }
 
 STAR_API star_status star_score_migrations(const star_score_params* p, const int32_t* cur_len,
@@ -168,7 +167,6 @@ STAR_API star_status star_score_migrations(const star_score_params* p, const int
     const bool all_topk = topk_req && topk_tgt && topk_score;
     if (p->top_k > 0 ? !all_topk : any_topk) return STAR_ERR_INVALID_ARG;
     const ScorePlan pl = plan_score(*p);
-    if (!pl.topk_ok) return STAR_ERR_UNSUPPORTED;
     st = check_ws(ws, ws_bytes, pl.total);
     if (st != STAR_OK) return st;
     int32_t* err = (int32_t*)((char*)ws + kHdrErrorWord);

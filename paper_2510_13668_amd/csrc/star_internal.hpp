@@ -31,14 +31,15 @@ hipError_t launch_project_load(const star_load_params& p, const LoadPlan& pl,
 
 struct ScorePlan {
     bool fused = false;   // PM/SM built in LDS by the scoring kernel
+    bool small = false;   // one workgroup scores and ranks everything
     int rpb = 0;          // requests per scoring workgroup
     int cand = 0;         // candidates per scoring workgroup (rpb * n)
     int groups = 0;       // scoring workgroups
     bool topk_direct = false;  // top-k over all migrations (else over the k best requests' ones)
-    int topk_rj = 1;      // keys per top-k thread (power of two)
-    bool topk_ok = true;  // sizes within what the top-k kernel holds
+    bool topk_reg1 = false;    // pruned top-k: best keys fit registers
+    bool topk_reg2 = false;    // pruned top-k: the k requests' migrations fit registers
     size_t pm_off = 0, sm_off = 0, scores_off = 0, bscore_off = 0, btarget_off = 0, total = 0;
-    size_t lds = 0;       // dynamic LDS of the scoring kernel
+    size_t lds = 0;       // dynamic LDS of the scoring kernel (or of the small path's one)
 };
 ScorePlan plan_score(const star_score_params& p);
 hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const int32_t* cur,

@@ -102,6 +102,8 @@ ADVERSARIAL = [
     ("topk_one", 333, 7, 32, 64, 1, 5000, 3000, False, 0),
     ("many_instances", 600, 300, 8, 40, 1024, 3000, 400, False, 0),
     ("big_bucket", 64, 4, 1000, 3, 16, 100000, 5000, True, 0),
+    # many scoring workgroups with all curves in LDS, top-k over every migration
+    ("multi_block_direct", 2000, 4, 16, 64, 256, 5000, 1200, False, 0),
 ]
 
 
@@ -130,6 +132,48 @@ def test_ties_from_duplicated_requests(N):
     cur[::3] = 5
     rem[::5] = 64
     _check(cur, rem, inst, n, 64, 32, 300)
+
+
+def _key_bits(ref, inst, n):
+    """Bits of the widest packed ranking key: score range, then r*n + t."""
+    sc = ref["scores"]
+    mask = np.ones(sc.shape, bool)
+    mask[np.arange(len(inst)), inst] = False
+    v = sc[mask]
+    return int(v.max() - v.min()).bit_length() + int(sc.size - 1).bit_length()
+
+
+@pytest.mark.parametrize("N,heavy,b,top_k", [(1024, 900, 16384, 256), (128, 100, 2 ** 18, 1024)])
+def test_wide_keys_one_workgroup(N, heavy, b, top_k):
+    """One heavily loaded instance of huge requests beside light ones: scores
+    spread over > 2^54, so the ranking key needs more than 64 bits and the
+    wide radix select runs (one-workgroup path); with top_k above the number
+    of migrations every key wins and the ordering falls back to rank counts."""
+    rng = np.random.default_rng(11)
+    n, K = 8, 2
+    inst = np.concatenate([np.zeros(heavy, np.int32),
+                           rng.integers(1, n, size=N - heavy).astype(np.int32)])
+    cur = np.concatenate([rng.integers(2 ** 30, 2 ** 31 - 1, size=heavy, endpoint=True),
+                          rng.integers(1, 1000, size=N - heavy, endpoint=True)]).astype(np.int32)
+    rem = rng.integers(1, 2 * b * K, size=N, endpoint=True).astype(np.int32)
+    gpu, ref = _check(cur, rem, inst, n, b, K, top_k)
+    assert _key_bits(ref, inst, n) > 64
+
+
+def test_wide_keys_many_instances():
+    """Two requests with huge buckets over 1024 instances: the best-move key
+    ((score - min) << target bits | t) no longer fits 64 bits, so the
+    two-step best-move reduction runs."""
+    N, n, b, K = 2, 1024, 2 ** 28, 1
+    cur = np.array([2 ** 31 - 1, 2 ** 31 - 1], np.int32)
+    rem = np.array([b, b // 2 + 3], np.int32)
+    inst = np.array([0, 5], np.int32)
+    gpu, ref = _check(cur, rem, inst, n, b, K, 16)
+    sc = ref["scores"]
+    mask = np.ones(sc.shape, bool)
+    mask[np.arange(N), inst] = False
+    v = sc[mask]
+    assert int(v.max() - v.min()).bit_length() + int(n - 1).bit_length() > 64
 
 
 def test_invalid_requests_are_skipped_and_reported():
