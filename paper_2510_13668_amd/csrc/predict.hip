@@ -30,6 +30,7 @@ constexpr int G1_KBYTES = 128;                 // bytes of K per LDS row
 constexpr int G1_ROW = G1_KBYTES + 16;         // padded LDS row (bytes)
 constexpr int G1_TILE = G1_BM * G1_ROW;        // one operand tile (bytes)
 constexpr int G1_THREADS = 256;
+constexpr int G1_STAGES = 3;                   // K-tiles of loads in flight ahead of the multiply
 constexpr int G1_CHUNKS = G1_BM * G1_KBYTES / 16 / G1_THREADS;   // 16-byte chunks per thread per operand
 
 
@@ -151,25 +152,25 @@ __device__ __forceinline__ void g1_compute(const char* la, const char* lb, int w
 }
 
 // One pipeline step: stage s holds tile i; write it to LDS buffer i % 2,
-// barrier, refill s with tile i + 3 (or re-read tile i -- a cache hit --
+// barrier, refill s with tile i + NS (or re-read tile i -- a cache hit --
 // past the end, so that every step issues exactly one stage of loads), and
 // multiply buffer i % 2.  A buffer is rewritten two steps after its last
 // use, and every thread has passed the intervening barrier only after
 // finishing that use.
-template <int kElemBytes>
+template <int kElemBytes, int NS>
 __device__ __forceinline__ void g1_step(const G1Ctx& c, char (*lds)[2][G1_TILE], int kt0, int nk,
                                         int i, G1Stage& s, int wm, int wn, int lane,
                                         f32x16 (&acc)[2][2]) {
     const int buf = i & 1;
     g1_store_stage(c, lds[buf][0], lds[buf][1], kt0 + i, s);
     __syncthreads();
-    g1_load_stage(c, kt0 + (i + 3 < nk ? i + 3 : i), s);
+    g1_load_stage(c, kt0 + (i + NS < nk ? i + NS : i), s);
     g1_compute<kElemBytes>(lds[buf][0], lds[buf][1], wm, wn, lane, acc);
 }
 
-// Three K-tiles of global loads are in flight ahead of the tile being
+// NS K-tiles of global loads are in flight ahead of the tile being
 // multiplied (register staging, two LDS buffers, one barrier per K-tile).
-template <int kElemBytes>
+template <int kElemBytes, int NS>
 __global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
     const char* __restrict__ A, const char* __restrict__ W, float* __restrict__ P,
     int M, int N, int Kd, int splits, int tiles_n, int ktiles) {
@@ -205,18 +206,18 @@ __global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
     const int khalf = lane >> 5;
 
     if (nk > 0) {
-        G1Stage s0, s1, s2;
-        g1_load_stage(c, kt0, s0);
-        g1_load_stage(c, kt0 + (1 < nk ? 1 : 0), s1);
-        g1_load_stage(c, kt0 + (2 < nk ? 2 : 0), s2);
+        G1Stage st[NS];
+#pragma unroll
+        for (int u = 0; u < NS; ++u) g1_load_stage(c, kt0 + (u < nk ? u : 0), st[u]);
         int i = 0;
-        for (; i + 3 <= nk; i += 3) {
-            g1_step<kElemBytes>(c, lds, kt0, nk, i, s0, wm, wn, lane, acc);
-            g1_step<kElemBytes>(c, lds, kt0, nk, i + 1, s1, wm, wn, lane, acc);
-            g1_step<kElemBytes>(c, lds, kt0, nk, i + 2, s2, wm, wn, lane, acc);
+        for (; i + NS <= nk; i += NS) {
+#pragma unroll
+            for (int u = 0; u < NS; ++u)
+                g1_step<kElemBytes, NS>(c, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
         }
-        if (i < nk) g1_step<kElemBytes>(c, lds, kt0, nk, i, s0, wm, wn, lane, acc);
-        if (i + 1 < nk) g1_step<kElemBytes>(c, lds, kt0, nk, i + 1, s1, wm, wn, lane, acc);
+#pragma unroll
+        for (int u = 0; u < NS - 1; ++u)
+            if (i + u < nk) g1_step<kElemBytes, NS>(c, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
     }
 
     // epilogue: 32x32 accumulator layout -- element v of lane l is
@@ -533,11 +534,11 @@ hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, c
     }
     const dim3 g1(pl.tiles_m * pl.tiles_n * pl.splits);
     if (p.dtype == STAR_BF16)
-        hipLaunchKernelGGL(gemm1_splitk_kernel<2>, g1, dim3(G1_THREADS), 0, stream,
+        hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES>), g1, dim3(G1_THREADS), 0, stream,
                            (const char*)hidden, (const char*)w1, partials, p.n_req, p.d_hidden,
                            p.d_model, pl.splits, pl.tiles_n, pl.ktiles);
     else
-        hipLaunchKernelGGL(gemm1_splitk_kernel<4>, g1, dim3(G1_THREADS), 0, stream,
+        hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES>), g1, dim3(G1_THREADS), 0, stream,
                            (const char*)hidden, (const char*)w1, partials, p.n_req, p.d_hidden,
                            p.d_model, pl.splits, pl.tiles_n, pl.ktiles);
     e = hipGetLastError();

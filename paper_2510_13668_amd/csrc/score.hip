@@ -61,6 +61,10 @@ constexpr int SS_MAX_REQ = 1024;
 constexpr int SS_LBATCH = (SC_FUSED_ENTRIES + SS_THREADS - 1) / SS_THREADS;
 constexpr int SS_RBATCH = SS_MAX_REQ / SS_THREADS;
 
+constexpr int RK_CODES = 1024;               // key codes (monotone in score - base)
+constexpr int RK_MAX_GROUPS = 1024;          // scoring workgroups the ranking kernel can take
+constexpr int RK_BCAP = 4096;                // boundary-code keys gathered into LDS
+
 constexpr int64_t kInfS = INT64_MAX;
 constexpr uint32_t kInfI = 0xFFFFFFFFu;
 
@@ -121,38 +125,136 @@ __device__ inline ReqTerms request_terms(int s, int c, int l, int n, int b, int6
     return q;
 }
 
-// PM/SM of instances t = w, w + nw, ... (one wave each) from curves in LDS
-// with row stride K+1 (entry K of each row is padding): 64-bucket chunks,
-// one DPP wavefront max-scan per chunk, carried across chunks; reads and
-// writes are consecutive per lane (no bank conflicts).
+// Inclusive prefix max over the 32 lanes of each half wave (lane order):
+// DPP row shifts, then row 1 / row 3 take lane 15 of row 0 / row 2.
+__device__ inline int64_t half_incl_max_i64(int64_t v) {
+    v = dpp_max_step_i64<kDppRowShr1, 0xF>(v);
+    v = dpp_max_step_i64<kDppRowShr2, 0xF>(v);
+    v = dpp_max_step_i64<kDppRowShr4, 0xF>(v);
+    v = dpp_max_step_i64<kDppRowShr8, 0xF>(v);
+    v = dpp_max_step_i64<kDppRowBcast15, 0xA>(v);
+    return v;
+}
+
+// PM/SM of every instance from curves in LDS with row stride K+1 (entry K
+// of each row is padding).  Each instance is taken by a group of 32 lanes
+// (half a wave; kT/32 instances at a time); lane l owns a run of S =
+// ceil(K/32) consecutive buckets: a max over its run, one DPP scan across
+// the 32 runs, then a pass that writes.  Runs are read PMSM_BATCH entries at
+// a time so that their LDS reads are in flight together.  For SM the runs
+// are numbered from the end of the curve.
+constexpr int PMSM_BATCH = 8;
+template <int kT>
 __device__ inline void build_pm_sm(const int64_t* lL, int64_t* lPM, int64_t* lSM, int n, int K,
-                                   int64_t bb, int w, int nw) {
-    const int lane = threadIdx.x & 63;
+                                   int64_t bb) {
+    const int l = threadIdx.x & 31;
     const int K1 = K + 1;
-    for (int t = w; t < n; t += nw) {
-        const int64_t* L = lL + t * K1;
-        int64_t* pm = lPM + t * K1;
-        int64_t* sm = lSM + t * K1;
-        int64_t carry = INT64_MIN;
-        for (int c = 0; c < K; c += 64) {                // PM: exclusive prefix max of L[j] + b^2 j
-            const int j = c + lane;
-            const int64_t x = j < K ? L[j] + bb * j : INT64_MIN;
-            const int64_t inc = imax(wave_incl_max_i64(x), carry);
-            const int64_t ex = wave_shr1_i64(inc, carry);
-            if (j < K) pm[j] = ex;
-            carry = readlane_i64(inc, 63);
+    const int S = (K + 31) >> 5;
+    for (int t0 = 0; t0 < n; t0 += kT / 32) {
+        const int t = t0 + (int)(threadIdx.x >> 5);
+        const bool live = t < n;
+        const int tc = live ? t : 0;
+        const int64_t* L = lL + tc * K1;
+        int64_t* pm = lPM + tc * K1;
+        int64_t* sm = lSM + tc * K1;
+        const int j0 = l * S;
+        const int j1 = j0 + S < K ? j0 + S : K;      // run [j0, j1) (empty past the end)
+        // PM: exclusive prefix max of L[j] + b^2 j
+        int64_t run = INT64_MIN;
+        for (int jb = j0; jb < j1; jb += PMSM_BATCH) {
+            int64_t x[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int j = jb + u;
+                x[u] = L[j < j1 ? j : j0];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u)
+                if (jb + u < j1) run = imax(run, x[u] + bb * (jb + u));
         }
-        if (lane == 0) pm[K] = carry;
-        carry = INT64_MIN;
-        for (int c = 0; c < K; c += 64) {                // SM: inclusive suffix max of L[j]
-            const int j = K - 1 - (c + lane);
-            const int64_t x = j >= 0 ? L[j] : INT64_MIN;
-            const int64_t inc = imax(wave_incl_max_i64(x), carry);
-            if (j >= 0) sm[j] = inc;
-            carry = readlane_i64(inc, 63);
+        const int64_t pinc = half_incl_max_i64(run);
+        const int64_t pex = wave_shr1_i64(pinc, INT64_MIN);
+        run = l == 0 ? INT64_MIN : pex;
+        for (int jb = j0; jb < j1; jb += PMSM_BATCH) {
+            int64_t x[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int j = jb + u;
+                x[u] = L[j < j1 ? j : j0];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int j = jb + u;
+                if (j < j1) {
+                    if (live) pm[j] = run;
+                    run = imax(run, x[u] + bb * j);
+                }
+            }
         }
-        if (lane == 0) sm[K] = INT64_MIN;
+        if (live && l == 31) pm[K] = pinc;
+        // SM: inclusive suffix max of L[j]; lane l takes j = K-1-j0 down to K-j1
+        const int q0 = K - 1 - j0, q1 = K - j1;      // run [q1, q0], walked downwards
+        run = INT64_MIN;
+        for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {
+            int64_t x[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int j = jb - u;
+                x[u] = L[j >= q1 ? j : q0];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u)
+                if (jb - u >= q1) run = imax(run, x[u]);
+        }
+        const int64_t sinc = half_incl_max_i64(run);
+        const int64_t sex = wave_shr1_i64(sinc, INT64_MIN);
+        run = l == 0 ? INT64_MIN : sex;
+        for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {
+            int64_t x[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int j = jb - u;
+                x[u] = L[j >= q1 ? j : q0];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int j = jb - u;
+                if (j >= q1) {
+                    run = imax(run, x[u]);
+                    if (live) sm[j] = run;
+                }
+            }
+        }
+        if (live && l == 0) sm[K] = INT64_MIN;
     }
+}
+
+// Minimum of a 64-bit value over aligned groups of g lanes (g a power of
+// two, 2..64); every lane of a group gets it.  DPP quad permutes for lane
+// distances 1 and 2, row shifts under bank masks for 4 and 8, and
+// ds_bpermute-based shuffles above.
+template <int kCtrl, int kBankMask>
+__device__ inline uint64_t dpp_u64(uint64_t old, uint64_t v) {
+    const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)old, (int)(uint32_t)v, kCtrl, 0xF,
+                                               kBankMask, false);
+    const int hi = __builtin_amdgcn_update_dpp((int)(old >> 32), (int)(v >> 32), kCtrl, 0xF,
+                                               kBankMask, false);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+__device__ inline uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+__device__ inline uint64_t group_min_u64(uint64_t v, int g) {
+    constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E;      // quad_perm [1,0,3,2], [2,3,0,1]
+    constexpr int kRowShr4 = 0x114, kRowShl4 = 0x104, kRowShr8 = 0x118, kRowShl8 = 0x108;
+    if (g > 1) v = umin64(v, dpp_u64<kQuadXor1, 0xF>(v, v));
+    if (g > 2) v = umin64(v, dpp_u64<kQuadXor2, 0xF>(v, v));
+    if (g > 4) v = umin64(v, dpp_u64<kRowShl4, 0x5>(dpp_u64<kRowShr4, 0xA>(v, v), v));
+    if (g > 8) v = umin64(v, dpp_u64<kRowShl8, 0x3>(dpp_u64<kRowShr8, 0xC>(v, v), v));
+    for (int o = 16; o < g; o <<= 1) {
+        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o, 64);
+        const uint32_t hi = (uint32_t)__shfl_xor((int)(v >> 32), o, 64);
+        v = umin64(v, ((uint64_t)hi << 32) | lo);
+    }
+    return v;
 }
 
 // Score of moving a request with terms (ke, alpha, p) to t, from PM/SM rows
@@ -229,7 +331,7 @@ struct ScoreArgs {
     int64_t* best_score;
     int32_t* err_word;
     int N, n, b, K, rpb, cand;
-    uint32_t magic_K;
+    uint32_t magic_K, magic_n;
 };
 
 template <bool kFused>
@@ -307,7 +409,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
         }
         for (int t = tid; t < n; t += SC_THREADS) lL[t * K1 + K] = INT64_MIN;
         __syncthreads();
-        build_pm_sm(lL, lPM, lSM, n, K, bb, wid, SC_THREADS / 64);
+        build_pm_sm<SC_THREADS>(lL, lPM, lSM, n, K, bb);
     }
     __syncthreads();
     const int64_t* gPM = kFused ? lPM : a.PM;
@@ -422,15 +524,13 @@ __device__ inline int block_excl_i32(int v, SelShared<kT>& sh, int* total) {
 // kInfS marks "no key".  Every thread makes the same calls (uniform control).
 // ---------------------------------------------------------------------------
 template <int RJ>
-struct RegKeys {                  // up to RJ keys in registers (nj slots used)
+struct RegKeys {                  // RJ keys in registers (unused slots hold kInfS)
     int64_t s[RJ];
     uint32_t i[RJ];
-    int nj;
     template <class F>
     __device__ inline void visit(F&& f) const {
 #pragma unroll
-        for (int j = 0; j < RJ; ++j)
-            if (j < nj) f(s[j], i[j]);
+        for (int j = 0; j < RJ; ++j) f(s[j], i[j]);
     }
 };
 
@@ -509,74 +609,66 @@ struct PrunedKeys {               // every migration of the requests rk[0..nr), 
     }
 };
 
-// Register loaders of the 1024-thread top-k (all reads issued first).
+// Register loaders of the 1024-thread top-k: every slot is loaded (clamped
+// index) and masked afterwards, so the reads are issued together.
 __device__ inline void load_migrations(RegKeys<TK_RJ>& k, const TopkArgs& a) {
-    const int M = a.N * a.n;
-    k.nj = (M + TK_THREADS - 1) / TK_THREADS;
+    const int M = a.N * a.n;                               // >= 1
     int32_t iv[TK_RJ], bv[TK_RJ];
     uint32_t qv[TK_RJ];
 #pragma unroll
     for (int j = 0; j < TK_RJ; ++j) {
-        if (j < k.nj) {
-            const int e = j * TK_THREADS + (int)threadIdx.x;
-            const uint32_t ec = (uint32_t)(e < M ? e : M - 1);
-            qv[j] = fast_div(ec, (uint32_t)a.n, a.magic_n);
-            k.s[j] = a.scores[ec];
-            iv[j] = a.inst[qv[j]];
-            bv[j] = a.best_target[qv[j]];
-        }
+        const int e = j * TK_THREADS + (int)threadIdx.x;
+        const uint32_t ec = (uint32_t)(e < M ? e : M - 1);
+        qv[j] = fast_div(ec, (uint32_t)a.n, a.magic_n);
+        k.s[j] = a.scores[ec];
+        iv[j] = a.inst[qv[j]];
+        bv[j] = a.best_target[qv[j]];
     }
 #pragma unroll
     for (int j = 0; j < TK_RJ; ++j) {
-        if (j < k.nj) {
-            const int e = j * TK_THREADS + (int)threadIdx.x;
-            const bool ok = e < M && bv[j] >= 0 && (int)((uint32_t)e - qv[j] * (uint32_t)a.n) != iv[j];
-            k.s[j] = ok ? k.s[j] : kInfS;
-            k.i[j] = ok ? (uint32_t)e : kInfI;
-        }
+        const int e = j * TK_THREADS + (int)threadIdx.x;
+        const bool ok = e < M && bv[j] >= 0 && (int)((uint32_t)e - qv[j] * (uint32_t)a.n) != iv[j];
+        k.s[j] = ok ? k.s[j] : kInfS;
+        k.i[j] = ok ? (uint32_t)e : kInfI;
     }
 }
 
 __device__ inline void load_best(RegKeys<TK_RJ>& k, const TopkArgs& a) {
-    k.nj = (a.N + TK_THREADS - 1) / TK_THREADS;
     int32_t bt[TK_RJ];
 #pragma unroll
     for (int j = 0; j < TK_RJ; ++j) {
-        if (j < k.nj) {
-            const int r = j * TK_THREADS + (int)threadIdx.x;
-            const int rc = r < a.N ? r : a.N - 1;
-            k.s[j] = a.best_score[rc];
-            bt[j] = a.best_target[rc];
-        }
+        const int r = j * TK_THREADS + (int)threadIdx.x;
+        const int rc = r < a.N ? r : a.N - 1;              // N >= 1
+        k.s[j] = a.best_score[rc];
+        bt[j] = a.best_target[rc];
     }
 #pragma unroll
     for (int j = 0; j < TK_RJ; ++j) {
-        if (j < k.nj) {
-            const int r = j * TK_THREADS + (int)threadIdx.x;
-            const bool ok = r < a.N && bt[j] >= 0;
-            k.s[j] = ok ? k.s[j] : kInfS;
-            k.i[j] = ok ? (uint32_t)r : kInfI;
-        }
+        const int r = j * TK_THREADS + (int)threadIdx.x;
+        const bool ok = r < a.N && bt[j] >= 0;
+        k.s[j] = ok ? k.s[j] : kInfS;
+        k.i[j] = ok ? (uint32_t)r : kInfI;
     }
 }
 
 __device__ inline void load_pruned(RegKeys<TK_RJ>& k, const TopkArgs& a, const int32_t* rk,
                                    const int32_t* rk_inst, int M) {
-    k.nj = (M + TK_THREADS - 1) / TK_THREADS;
 #pragma unroll
     for (int j = 0; j < TK_RJ; ++j) {
-        if (j < k.nj) {
-            const int e = j * TK_THREADS + (int)threadIdx.x;
-            pruned_key(a, rk, rk_inst, (uint32_t)(e < M ? e : M - 1), &k.s[j], &k.i[j]);
-        }
+        k.s[j] = kInfS;
+        k.i[j] = kInfI;
+    }
+    if (M == 0) return;                                    // no request has a migration
+#pragma unroll
+    for (int j = 0; j < TK_RJ; ++j) {
+        const int e = j * TK_THREADS + (int)threadIdx.x;
+        pruned_key(a, rk, rk_inst, (uint32_t)(e < M ? e : M - 1), &k.s[j], &k.i[j]);
     }
 #pragma unroll
     for (int j = 0; j < TK_RJ; ++j) {
-        if (j < k.nj) {
-            const int e = j * TK_THREADS + (int)threadIdx.x;
-            k.s[j] = e < M ? k.s[j] : kInfS;
-            k.i[j] = e < M ? k.i[j] : kInfI;
-        }
+        const int e = j * TK_THREADS + (int)threadIdx.x;
+        k.s[j] = e < M ? k.s[j] : kInfS;
+        k.i[j] = e < M ? k.i[j] : kInfI;
     }
 }
 
@@ -768,10 +860,17 @@ __device__ void order_and_write(const int64_t* ws_s, const uint32_t* ws_i, int n
     const int sbits = nw > 0 ? bit_length((uint64_t)(smax_w - smin)) : 0;
     const uint64_t imask = (1ull << ibits) - 1;
     if (nw > 0 && sbits + ibits <= 64) {
+        // about two buckets per winner (at least one per thread, at most
+        // SEL_BINS): the scan below touches only those
+        int bb = kT;
+        while (bb < 2 * nw && bb < SEL_BINS) bb <<= 1;
+        const int bbits = bit_length((uint64_t)(bb - 1));
         const int nbits = sbits + ibits;
-        const int shift = nbits > SEL_DIGIT ? nbits - SEL_DIGIT : 0;
-        clear_bins<kT>(sh.hist);
-        clear_bins<kT>(sh.fill);
+        const int shift = nbits > bbits ? nbits - bbits : 0;
+        for (int q = tid; q < bb; q += kT) {
+            sh.hist[q] = 0;
+            sh.fill[q] = 0;
+        }
         __syncthreads();
         for (int p = tid; p < nw; p += kT) {
             const uint64_t v = ((uint64_t)(ws_s[p] - smin) << ibits) | ws_i[p];
@@ -780,17 +879,18 @@ __device__ void order_and_write(const int64_t* ws_s, const uint32_t* ws_i, int n
         __syncthreads();
         {                                                   // counts -> exclusive offsets
             constexpr int PER = SEL_BINS / kT;
+            const int per = bb / kT;                        // 1 .. PER
             int c[PER], own = 0;
 #pragma unroll
             for (int u = 0; u < PER; ++u) {
-                c[u] = sh.hist[tid * PER + u];
+                c[u] = u < per ? sh.hist[tid * per + u] : 0;
                 own += c[u];
             }
             int tot;
             int before = block_excl_i32<kT>(own, sh, &tot);
 #pragma unroll
             for (int u = 0; u < PER; ++u) {
-                sh.hist[tid * PER + u] = before;
+                if (u < per) sh.hist[tid * per + u] = before;
                 before += c[u];
             }
         }
@@ -908,6 +1008,365 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// score + first ranking stage (many workgroups), then one workgroup ranks
+// ---------------------------------------------------------------------------
+// A key's code is a monotone 10-bit summary of d = score - base (base: the
+// smallest target peak, which no migration score is below): the position of
+// d's leading one and the four bits after it.  Keys with a smaller code are
+// smaller keys, so the k smallest keys are all keys whose code is below some
+// c*, plus the smallest few of those with code c*.
+__device__ inline uint32_t key_code(uint64_t d) {
+    const int e = bit_length(d);                         // 0..63
+    if (e <= 4) return (uint32_t)d;
+    return ((uint32_t)(e - 4) << 4) | (uint32_t)((d >> (e - 5)) & 15);   // < 960
+}
+
+struct RankArgs {
+    uint32_t* ghist;              // [RK_CODES] counts over all groups (zero on entry)
+    int64_t* base;                // the code base, written by group 0
+    int64_t* keys_s;              // [groups, cand] each group's migrations in code order
+    uint32_t* keys_i;
+    int32_t* offs;                // [groups, RK_CODES + 1] exclusive code offsets per group
+};
+
+// Fused scoring (all curves in LDS) plus each group's migration keys sorted
+// by code (a counting sort in LDS), its code offsets and the global code
+// histogram.
+__global__ __launch_bounds__(SC_THREADS) void score_rank_kernel(ScoreArgs a, RankArgs rk) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ int lhist[RK_CODES];
+    __shared__ int wtot[SC_THREADS / 64];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int n = a.n, K = a.K, b = a.b;
+    const int K1 = K + 1;
+    const int cand = a.cand;                       // rpb * n <= SC_THREADS: one per thread
+    const int rpb = a.rpb;
+
+    int64_t* lL = (int64_t*)smem;
+    int64_t* lPM = lL + n * K1;
+    int64_t* lSM = lPM + n * K1;
+    int64_t* ks = lSM + n * K1;
+    int64_t* r_alpha = ks + cand;
+    int64_t* r_p = r_alpha + rpb;
+    uint32_t* ki = (uint32_t*)(r_p + rpb);
+    int32_t* r_ke = (int32_t*)(ki + cand);
+    int32_t* r_s = r_ke + rpb;
+
+    const int g = blockIdx.x;
+    const int row0 = g * rpb;
+    const int64_t H = (int64_t)b * K;
+    const int64_t bb = (int64_t)b * b;
+
+    // 0) curves and per-request terms (all reads issued first)
+    const int nK = n * K;
+    int64_t lv[SC_LBATCH];
+#pragma unroll
+    for (int j = 0; j < SC_LBATCH; ++j) {
+        const int e = j * SC_THREADS + tid;
+        lv[j] = a.load[e < nK ? e : nK - 1];
+    }
+    int32_t bad = 0;
+    {
+        const int q = tid;                           // rpb <= SC_THREADS
+        int r = row0 + q;
+        r = r < a.N ? r : a.N - 1;
+        const int sv = a.inst[r], cv = a.cur[r], rv = a.rem[r];
+        if (q < rpb) {
+            const bool live = row0 + q < a.N;
+            const ReqTerms rt = request_terms(sv, cv, rv, n, b, H);
+            bad = live ? rt.bad : 0;
+            r_s[q] = live ? rt.s : -1;
+            r_ke[q] = rt.ke;
+            r_alpha[q] = rt.alpha;
+            r_p[q] = rt.p;
+        }
+    }
+    bad = wave_or_i32(bad);
+    if (lane == 0) report_error(a.err_word, bad);
+#pragma unroll
+    for (int j = 0; j < SC_LBATCH; ++j) {
+        const int e = j * SC_THREADS + tid;
+        if (e < nK) {
+            const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
+            lL[t * K1 + (e - t * K)] = lv[j];
+        }
+    }
+    for (int t = tid; t < n; t += SC_THREADS) lL[t * K1 + K] = INT64_MIN;
+    for (int c = tid; c < RK_CODES; c += SC_THREADS) lhist[c] = 0;
+    __syncthreads();
+    build_pm_sm<SC_THREADS>(lL, lPM, lSM, n, K, bb);
+    __syncthreads();
+
+    // 1) this thread's candidate e = q n + t
+    int64_t base = INT64_MAX;                         // smallest target peak
+    for (int t = 0; t < n; ++t) {
+        const int64_t v = lSM[t * K1];
+        base = v < base ? v : base;
+    }
+    const int e = tid;
+    const uint32_t ec = (uint32_t)(e < cand ? e : cand - 1);
+    const int q = (int)fast_div(ec, (uint32_t)n, a.magic_n);
+    const int t = (int)ec - q * n;
+    const int r = row0 + q;
+    const bool live = e < cand && r < a.N;
+    const int s = r_s[q], ke = r_ke[q];
+    const int64_t* pm_t = lPM + t * K1;
+    const int64_t* sm_t = lSM + t * K1;
+    const int64_t mv = move_score(pm_t, sm_t, lL[t * K1 + ke], ke, K, r_alpha[q], r_p[q]);
+    const int64_t sc = s < 0 ? -1 : (t == s ? sm_t[0] : mv);
+    const bool mig = live && s >= 0 && t != s;
+    if (live && a.scores) a.scores[(int64_t)r * n + t] = sc;
+    if (e < cand) {
+        ks[e] = mig ? sc : kInfS;
+        ki[e] = mig ? (uint32_t)((int64_t)r * n + t) : kInfI;
+    }
+    // code and rank of this key among the group's keys of equal code
+    const uint32_t code = mig ? key_code((uint64_t)(sc - base)) : 0;
+    const int lrank = mig ? atomicAdd(&lhist[code], 1) : 0;
+    __syncthreads();
+
+    // 2) best migration per request: smallest (score, t) over t != s
+    for (int qq = tid; qq < rpb; qq += SC_THREADS) {
+        const int rr = row0 + qq;
+        if (rr >= a.N) continue;
+        int64_t bs = kInfS;
+        uint32_t bi = kInfI;
+        for (int tt = 0; tt < n; ++tt) {
+            const int ee = qq * n + tt;
+            if (key_less(ks[ee], ki[ee], bs, bi)) { bs = ks[ee]; bi = ki[ee]; }
+        }
+        const bool none = bi == kInfI;
+        if (a.best_target) a.best_target[rr] = none ? -1 : (int32_t)(bi - (uint32_t)((int64_t)rr * n));
+        if (a.best_score) a.best_score[rr] = none ? -1 : bs;
+    }
+
+    // 3) code histogram -> exclusive offsets (4 codes per thread), global counts
+    constexpr int PER = RK_CODES / SC_THREADS;
+    int c4[PER], own = 0;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        c4[u] = lhist[tid * PER + u];
+        own += c4[u];
+    }
+    const int inc = wave_incl_add_i32(own);
+    if (lane == 63) wtot[tid >> 6] = inc;
+    __syncthreads();
+    int before = inc - own;
+    for (int w = 0; w < (tid >> 6); ++w) before += wtot[w];
+    int32_t* go = rk.offs + (int64_t)g * (RK_CODES + 1);
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int c = tid * PER + u;
+        go[c] = before;
+        if (c4[u]) atomicAdd(&rk.ghist[c], (uint32_t)c4[u]);
+        lhist[c] = before;                            // now the offset
+        before += c4[u];
+    }
+    if (tid == SC_THREADS - 1) go[RK_CODES] = before;  // this group's migration count
+    if (g == 0 && tid == 0) *rk.base = base;
+    __syncthreads();
+    if (mig) {
+        const int64_t at = (int64_t)g * cand + lhist[code] + lrank;
+        rk.keys_s[at] = sc;
+        rk.keys_i[at] = (uint32_t)((int64_t)r * n + t);
+    }
+}
+
+struct FinalArgs {
+    uint32_t* ghist;              // zeroed here after use
+    const int32_t* offs;
+    const int64_t* keys_s;
+    const uint32_t* keys_i;
+    int32_t* topk_req;
+    int32_t* topk_tgt;
+    int64_t* topk_score;
+    int groups, cand, n, top_k, ibits;
+    uint32_t magic_n;
+};
+
+constexpr int RK_THREADS = 256;               // the ranking workgroup
+
+// Keys of code c* of every group, streamed: slot x of the flattened
+// [groups, cand] array is one when lo[w] <= j < hi[w] (w, j = divmod(x, cand)).
+struct BoundaryKeys {
+    const FinalArgs* a;
+    const int32_t* lo;            // LDS [groups]
+    const int32_t* hi;
+    template <class F>
+    __device__ inline void visit(F&& f) const {
+        const int X = a->groups * a->cand;
+        for (int x0 = 0; x0 < X; x0 += RK_THREADS * SEL_SBATCH) {
+            int64_t sv[SEL_SBATCH];
+            uint32_t iv[SEL_SBATCH];
+            bool ok[SEL_SBATCH];
+#pragma unroll
+            for (int u = 0; u < SEL_SBATCH; ++u) {
+                const int x = x0 + u * RK_THREADS + (int)threadIdx.x;
+                const int xc = x < X ? x : X - 1;
+                const int w = xc / a->cand, j = xc - w * a->cand;
+                ok[u] = x < X && j >= lo[w] && j < hi[w];
+                sv[u] = a->keys_s[xc];
+                iv[u] = a->keys_i[xc];
+            }
+#pragma unroll
+            for (int u = 0; u < SEL_SBATCH; ++u) f(ok[u] ? sv[u] : kInfS, ok[u] ? iv[u] : kInfI);
+        }
+    }
+};
+
+// Position p of a concatenation whose part w starts at pre[w] (pre[0] = 0,
+// nondecreasing, parts 0..G-1): the part holding p.
+__device__ inline int find_part(const int32_t* pre, int G, int p) {
+    int lo = 0, hi = G - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (pre[mid] <= p) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(RK_THREADS) void rank_final_kernel(FinalArgs a) {
+    __shared__ SelShared<RK_THREADS> sh;
+    __shared__ int64_t ws_s[STAR_MAX_TOP_K];
+    __shared__ uint32_t ws_i[STAR_MAX_TOP_K];
+    __shared__ uint64_t sv[STAR_MAX_TOP_K];
+    __shared__ int32_t lo_w[RK_MAX_GROUPS], hi_w[RK_MAX_GROUPS];
+    __shared__ int32_t pre_a[RK_MAX_GROUPS], pre_b[RK_MAX_GROUPS];
+    __shared__ int64_t bs_s[RK_BCAP];
+    __shared__ uint32_t bs_i[RK_BCAP];
+    const int tid = threadIdx.x;
+    const int G = a.groups;
+
+    // 1) c*: the code holding the k-th smallest key (four codes per thread);
+    //    the histogram is zeroed for the next call
+    constexpr int CPT = RK_CODES / RK_THREADS;
+    int hc[CPT], own = 0;
+#pragma unroll
+    for (int u = 0; u < CPT; ++u) {
+        hc[u] = (int)a.ghist[tid * CPT + u];
+        own += hc[u];
+    }
+#pragma unroll
+    for (int u = 0; u < CPT; ++u) a.ghist[tid * CPT + u] = 0;
+    int total;
+    int ex = block_excl_i32<RK_THREADS>(own, sh, &total);
+    const int k = a.top_k < total ? a.top_k : total;
+    if (tid == 0) sh.bcast[0] = RK_CODES;             // all keys win when total <= k
+    __syncthreads();
+    if (k < total) {
+#pragma unroll
+        for (int u = 0; u < CPT; ++u) {
+            if (ex < k && k <= ex + hc[u]) sh.bcast[0] = tid * CPT + u;
+            ex += hc[u];
+        }
+    }
+    __syncthreads();
+    const int cstar = sh.bcast[0];
+
+    // 2) per group: keys below c* ([0, lo)) and at c* ([lo, hi)); thread
+    //    tid owns the groups [tid*GPT, tid*GPT + GPT)
+    const int GPT = (G + RK_THREADS - 1) / RK_THREADS;
+    int sa = 0, sb = 0;
+    for (int u = 0; u < GPT; ++u) {
+        const int w = tid * GPT + u;
+        if (w < G) {
+            const int32_t* o = a.offs + (int64_t)w * (RK_CODES + 1);
+            const int l = o[cstar];
+            const int h = cstar < RK_CODES ? o[cstar + 1] : l;
+            lo_w[w] = l;
+            hi_w[w] = h;
+            sa += l;
+            sb += h - l;
+        }
+    }
+    int na, nb;
+    int pa = block_excl_i32<RK_THREADS>(sa, sh, &na);
+    int pb = block_excl_i32<RK_THREADS>(sb, sh, &nb);
+    for (int u = 0; u < GPT; ++u) {
+        const int w = tid * GPT + u;
+        if (w < G) {
+            pre_a[w] = pa;
+            pre_b[w] = pb;
+            pa += lo_w[w];
+            pb += hi_w[w] - lo_w[w];
+        }
+    }
+    __syncthreads();
+
+    // 3) every key below c* wins (na < k <= STAR_MAX_TOP_K)
+    for (int p = tid; p < na; p += RK_THREADS) {
+        const int w = find_part(pre_a, G, p);
+        const int64_t x = (int64_t)w * a.cand + (p - pre_a[w]);
+        ws_s[p] = a.keys_s[x];
+        ws_i[p] = a.keys_i[x];
+    }
+
+    // 4) the k - na smallest keys of code c*
+    const int need = k - na;
+    int nw = na;
+    if (need > 0 && nb <= RK_BCAP) {
+        for (int p = tid; p < nb; p += RK_THREADS) {
+            const int w = find_part(pre_b, G, p);
+            const int64_t x = (int64_t)w * a.cand + lo_w[w] + (p - pre_b[w]);
+            bs_s[p] = a.keys_s[x];
+            bs_i[p] = a.keys_i[x];
+        }
+        __syncthreads();
+        if (nb <= RK_THREADS) {
+            // few keys: each one's rank among them, directly
+            if (tid < nb) {
+                const int64_t xs = bs_s[tid];
+                const uint32_t xi = bs_i[tid];
+                int rank = 0;
+                for (int q = 0; q < nb; ++q) rank += key_less(bs_s[q], bs_i[q], xs, xi) ? 1 : 0;
+                if (rank < need) {
+                    ws_s[na + rank] = xs;
+                    ws_i[na + rank] = xi;
+                }
+            }
+            nw += need;
+        } else {
+            RegKeys<RK_BCAP / RK_THREADS> keys;
+#pragma unroll
+            for (int j = 0; j < RK_BCAP / RK_THREADS; ++j) {
+                const int p = j * RK_THREADS + tid;
+                keys.s[j] = p < nb ? bs_s[p] : kInfS;
+                keys.i[j] = p < nb ? bs_i[p] : kInfI;
+            }
+            int cnt;
+            int64_t us, smin, smax;
+            uint32_t ui;
+            source_stats<RK_THREADS>(keys, sh, &cnt, &smin, &smax);
+            select_bound<RK_THREADS>(keys, need, a.ibits, cnt, smin, smax, sh, &us, &ui);
+            nw += block_gather<RK_THREADS>(keys, us, ui, sh, ws_s + na, ws_i + na,
+                                           STAR_MAX_TOP_K - na);
+        }
+    } else if (need > 0) {
+        BoundaryKeys src{&a, lo_w, hi_w};
+        int cnt;
+        int64_t us, smin, smax;
+        uint32_t ui;
+        source_stats<RK_THREADS>(src, sh, &cnt, &smin, &smax);
+        select_bound<RK_THREADS>(src, need, a.ibits, cnt, smin, smax, sh, &us, &ui);
+        nw += block_gather<RK_THREADS>(src, us, ui, sh, ws_s + na, ws_i + na, STAR_MAX_TOP_K - na);
+    }
+    __syncthreads();
+
+    // 5) order the winners and write them out
+    int64_t lo = kInfS, hi = -1;
+    for (int p = tid; p < nw; p += RK_THREADS) {
+        lo = ws_s[p] < lo ? ws_s[p] : lo;
+        hi = ws_s[p] > hi ? ws_s[p] : hi;
+    }
+    int cntw;
+    int64_t wmin, wmax;
+    block_stats<RK_THREADS>(0, lo, hi, sh, &cntw, &wmin, &wmax);
+    order_and_write<RK_THREADS>(ws_s, ws_i, nw, wmin, wmax, a.ibits, a.n, a.magic_n, a.topk_req,
+                                a.topk_tgt, a.topk_score, a.top_k, sh, sv);
+}
+
+// ---------------------------------------------------------------------------
 // small rounds: one workgroup scores and ranks
 // ---------------------------------------------------------------------------
 struct SmallArgs {
@@ -926,29 +1385,31 @@ struct SmallArgs {
     uint32_t magic_n, magic_K;
 };
 
-// Dynamic LDS: [L | PM | SM] (n (K+1) int64 each), alpha[N], p[N] (int64),
-// best[N] (uint64), ke[N], s[N] (int32).
+// Dynamic LDS: [L | PM | SM] (n (K+1) int64 each), then per request
+// {alpha, p} (2 x int64), best (uint64) and {ke, s} (2 x int32).
 constexpr size_t SS_STATIC_LDS = sizeof(SelShared<SS_THREADS>) + STAR_MAX_TOP_K * (8 + 4 + 8);
 static size_t small_lds_bytes(int N, int n, int K) {
-    return (size_t)3 * n * (K + 1) * 8 + (size_t)N * (8 + 8 + 8 + 4 + 4);
+    const size_t E = ((size_t)n * (K + 1) + 1) & ~(size_t)1;   // even: keeps {alpha, p} 16-B aligned
+    return 3 * E * 8 + (size_t)N * (16 + 8 + 8);
 }
 
-__global__ __launch_bounds__(SS_THREADS) void score_small_kernel(SmallArgs a) {
+// One workgroup of 8 waves (two per SIMD): up to 256 VGPRs per lane, so the
+// candidate slots' LDS round trips can all be in flight.
+__global__ __launch_bounds__(SS_THREADS) __attribute__((amdgpu_waves_per_eu(1, 2)))
+void score_small_kernel(SmallArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ SelShared<SS_THREADS> sh;
     __shared__ int64_t ws_s[STAR_MAX_TOP_K];
     __shared__ uint32_t ws_i[STAR_MAX_TOP_K];
     __shared__ uint64_t sv[STAR_MAX_TOP_K];
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int N = a.N, n = a.n, b = a.b, K = a.K, K1 = K + 1, E = n * K1;
+    const int N = a.N, n = a.n, b = a.b, K = a.K, K1 = K + 1, E = (n * K1 + 1) & ~1;
     int64_t* lL = (int64_t*)smem;
     int64_t* lPM = lL + E;
     int64_t* lSM = lPM + E;
-    int64_t* r_alpha = lSM + E;
-    int64_t* r_p = r_alpha + N;
-    uint64_t* r_best = (uint64_t*)(r_p + N);
-    int32_t* r_ke = (int32_t*)(r_best + N);
-    int32_t* r_s = r_ke + N;
+    longlong2* r_ap = (longlong2*)(lSM + E);           // {alpha, p}; E * 3 * 8 keeps 16-B alignment
+    uint64_t* r_best = (uint64_t*)(r_ap + N);
+    int2* r_ks = (int2*)(r_best + N);                   // {ke, s}
     const int64_t H = (int64_t)b * K;
     const int64_t bb = (int64_t)b * b;
 
@@ -976,10 +1437,8 @@ __global__ __launch_bounds__(SS_THREADS) void score_small_kernel(SmallArgs a) {
         if (r < N) {
             const ReqTerms rt = request_terms(sv_[j], cv[j], rv[j], n, b, H);
             bad |= rt.bad;
-            r_s[r] = rt.s;
-            r_ke[r] = rt.ke;
-            r_alpha[r] = rt.alpha;
-            r_p[r] = rt.p;
+            r_ks[r] = make_int2(rt.ke, rt.s);
+            r_ap[r] = make_longlong2(rt.alpha, rt.p);
             r_best[r] = ~0ull;
         }
     }
@@ -997,43 +1456,83 @@ __global__ __launch_bounds__(SS_THREADS) void score_small_kernel(SmallArgs a) {
     __syncthreads();
 
     // 1) PM/SM
-    build_pm_sm(lL, lPM, lSM, n, K, bb, wid, SS_THREADS / 64);
+    build_pm_sm<SS_THREADS>(lL, lPM, lSM, n, K, bb);
     __syncthreads();
 
     // 2) every candidate e = r n + t: score (written out), migration key in
-    //    registers
+    //    registers.  All slots are computed (clamped index) and masked.
+    //    Slots go eight at a time, their LDS reads issued in two batches
+    //    (request terms, then the three curve gathers); stores come after.
     const int M = N * n;
     RegKeys<SS_RJ> keys;
-    keys.nj = (M + SS_THREADS - 1) / SS_THREADS;
+    int64_t scv[SS_RJ];
+    constexpr int SB = 8;
 #pragma unroll
-    for (int j = 0; j < SS_RJ; ++j) {
-        if (j < keys.nj) {
-            const int e = j * SS_THREADS + tid;
+    for (int h = 0; h < SS_RJ; h += SB) {
+        int tt[SB];
+        int2 ks[SB];
+        longlong2 ap[SB];
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int e = (h + u) * SS_THREADS + tid;
             const uint32_t ec = (uint32_t)(e < M ? e : M - 1);
             const int r = (int)fast_div(ec, (uint32_t)n, a.magic_n);
-            const int t = (int)ec - r * n;
-            const int s = r_s[r], ke = r_ke[r];
-            const int64_t* pm_t = lPM + t * K1;
-            const int64_t* sm_t = lSM + t * K1;
-            const int64_t mv = move_score(pm_t, sm_t, lL[t * K1 + ke], ke, K, r_alpha[r], r_p[r]);
-            const int64_t sc = s < 0 ? -1 : (t == s ? sm_t[0] : mv);
-            if (e < M && a.scores) a.scores[e] = sc;
+            tt[u] = (int)ec - r * n;
+            ks[u] = r_ks[r];
+            ap[u] = r_ap[r];
+        }
+        int64_t g0[SB], g1[SB], g2[SB], g3[SB];
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int base = tt[u] * K1, ke = ks[u].x;
+            g0[u] = lPM[base + ke];
+            g1[u] = lL[base + ke];                                  // entry K is -inf
+            g2[u] = lSM[base + (ke + 1 < K ? ke + 1 : K)];
+            g3[u] = lSM[base];
+        }
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int e = (h + u) * SS_THREADS + tid;
+            const int s = ks[u].y, t = tt[u];
+            const int64_t mv = imax(imax(g0[u] + ap[u].x, g1[u] + ap[u].y), g2[u]);
+            scv[h + u] = s < 0 ? -1 : (t == s ? g3[u] : mv);
             const bool mig = e < M && s >= 0 && t != s;
-            keys.s[j] = mig ? sc : kInfS;
-            keys.i[j] = mig ? (uint32_t)e : kInfI;
+            keys.s[h + u] = mig ? scv[h + u] : kInfS;
+            keys.i[h + u] = mig ? (uint32_t)e : kInfI;
+        }
+    }
+    if (a.scores) {
+#pragma unroll
+        for (int j = 0; j < SS_RJ; ++j) {
+            const int e = j * SS_THREADS + tid;
+            if (e < M) a.scores[e] = scv[j];
         }
     }
 
-    // 3) best move per request: LDS atomic min of ((score - smin) << tbits) | t
-    //    when that fits 64 bits, else of (score - smin) and then of t among
-    //    the moves that reach it
+    // 3) best move per request, as the minimum of ((score - smin) << tbits) | t
+    //    when that fits 64 bits: over the request's group of n lanes when n
+    //    divides 64 (candidates e = r n + t are consecutive lanes), else by
+    //    LDS atomic min; wider keys take the minimum of (score - smin) and then
+    //    of t among the moves that reach it.
     int total;
     int64_t smin, smax;
     source_stats<SS_THREADS>(keys, sh, &total, &smin, &smax);
     const int tbits = bit_length((uint64_t)(n - 1));
     const uint64_t tmask = (1ull << tbits) - 1;
     const bool packed = total > 0 && bit_length((uint64_t)(smax - smin)) + tbits <= 64;
-    if (total > 0) {
+    const bool grouped = packed && (64 % n) == 0;
+    if (grouped) {
+#pragma unroll
+        for (int j = 0; j < SS_RJ; ++j) {
+            const int e = j * SS_THREADS + tid;
+            const uint32_t r = fast_div((uint32_t)e, (uint32_t)n, a.magic_n);
+            const uint64_t v = keys.s[j] == kInfS
+                                   ? ~0ull
+                                   : ((uint64_t)(keys.s[j] - smin) << tbits) | ((uint32_t)e - r * n);
+            const uint64_t g = group_min_u64(v, n);
+            if (e < M && (lane & (n - 1)) == 0) r_best[r] = g;
+        }
+    } else if (total > 0) {
         keys.visit([&](int64_t s, uint32_t i) {
             if (s == kInfS) return;
             const uint32_t r = fast_div(i, (uint32_t)n, a.magic_n);
@@ -1042,13 +1541,13 @@ __global__ __launch_bounds__(SS_THREADS) void score_small_kernel(SmallArgs a) {
                       (unsigned long long)(packed ? (d << tbits) | (i - r * (uint32_t)n) : d));
         });
         if (!packed) {
-            for (int r = tid; r < N; r += SS_THREADS) r_ke[r] = -1;   // min target, as unsigned
+            for (int r = tid; r < N; r += SS_THREADS) r_ks[r].x = -1;  // min target, as unsigned
             __syncthreads();
             keys.visit([&](int64_t s, uint32_t i) {
                 if (s == kInfS) return;
                 const uint32_t r = fast_div(i, (uint32_t)n, a.magic_n);
                 if ((uint64_t)(s - smin) == r_best[r])
-                    atomicMin((unsigned int*)&r_ke[r], i - r * (uint32_t)n);
+                    atomicMin((unsigned int*)&r_ks[r].x, i - r * (uint32_t)n);
             });
         }
     }
@@ -1057,7 +1556,7 @@ __global__ __launch_bounds__(SS_THREADS) void score_small_kernel(SmallArgs a) {
         const uint64_t v = r_best[r];
         const bool none = v == ~0ull;
         const int64_t bs = none ? -1 : smin + (int64_t)(packed ? v >> tbits : v);
-        const int32_t bt = none ? -1 : (packed ? (int32_t)(v & tmask) : r_ke[r]);
+        const int32_t bt = none ? -1 : (packed ? (int32_t)(v & tmask) : r_ks[r].x);
         if (a.best_target) a.best_target[r] = bt;
         if (a.best_score) a.best_score[r] = bs;
     }
@@ -1100,6 +1599,25 @@ ScorePlan plan_score(const star_score_params& p) {
     pl.topk_reg2 = (int64_t)p.top_k * (n - 1) <= TK_REG_KEYS;
 
     size_t off = STAR_WS_HEADER_BYTES;
+    // fused scoring with the two-stage ranking: the scoring workgroups sort
+    // their keys by code, one workgroup ranks
+    pl.rank2 = pl.fused && p.top_k > 0 && pl.groups <= RK_MAX_GROUPS && pl.cand <= SC_THREADS;
+    if (pl.rank2) {
+        pl.small = false;
+        pl.ghist_off = off;
+        off = align_up(off + RK_CODES * 4, 256);
+        pl.base_off = off;
+        off = align_up(off + 8, 256);
+        pl.keys_s_off = off;
+        off = align_up(off + (size_t)pl.groups * pl.cand * 8, 256);
+        pl.keys_i_off = off;
+        off = align_up(off + (size_t)pl.groups * pl.cand * 4, 256);
+        pl.offs_off = off;
+        off = align_up(off + (size_t)pl.groups * (RK_CODES + 1) * 4, 256);
+        pl.total = off;
+        pl.lds = (size_t)3 * n * K1 * 8 + (size_t)pl.cand * 12 + (size_t)pl.rpb * 24;
+        return pl;
+    }
     if (pl.small) {
         pl.total = off;
         pl.lds = small_lds_bytes(N, n, p.load.n_buckets);
@@ -1161,6 +1679,39 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
         }
         return hipSuccess;
     }
+    if (pl.rank2) {
+        ScoreArgs a = {};
+        a.cur = cur; a.rem = rem; a.inst = inst; a.load = load;
+        a.scores = scores; a.best_target = best_target; a.best_score = best_score;
+        a.err_word = err_word;
+        a.N = lp.n_req; a.n = lp.n_inst; a.b = lp.bucket; a.K = lp.n_buckets;
+        a.rpb = pl.rpb; a.cand = pl.cand;
+        a.magic_K = div_magic((uint32_t)lp.n_buckets);
+        a.magic_n = div_magic((uint32_t)lp.n_inst);
+        RankArgs rk;
+        rk.ghist = (uint32_t*)(ws + pl.ghist_off);
+        rk.base = (int64_t*)(ws + pl.base_off);
+        rk.keys_s = (int64_t*)(ws + pl.keys_s_off);
+        rk.keys_i = (uint32_t*)(ws + pl.keys_i_off);
+        rk.offs = (int32_t*)(ws + pl.offs_off);
+        hipError_t e = set_lds((const void*)score_rank_kernel, pl.lds, RK_CODES * 4 + 64);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(score_rank_kernel, dim3(pl.groups), dim3(SC_THREADS), pl.lds, stream, a, rk);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        FinalArgs f = {};
+        f.ghist = rk.ghist;
+        f.offs = rk.offs;
+        f.keys_s = rk.keys_s;
+        f.keys_i = rk.keys_i;
+        f.topk_req = topk_req; f.topk_tgt = topk_tgt; f.topk_score = topk_score;
+        f.groups = pl.groups; f.cand = pl.cand; f.n = lp.n_inst; f.top_k = p.top_k;
+        f.ibits = 0;
+        for (int64_t x = (int64_t)lp.n_req * lp.n_inst - 1; x > 0; x >>= 1) ++f.ibits;
+        f.magic_n = div_magic((uint32_t)lp.n_inst);
+        hipLaunchKernelGGL(rank_final_kernel, dim3(1), dim3(RK_THREADS), 0, stream, f);
+        return hipGetLastError();
+    }
     if (pl.small) {
         SmallArgs s = {};
         s.cur = cur; s.rem = rem; s.inst = inst; s.load = load;
@@ -1187,6 +1738,7 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     a.N = lp.n_req; a.n = lp.n_inst; a.b = lp.bucket; a.K = lp.n_buckets;
     a.rpb = pl.rpb; a.cand = pl.cand;
     a.magic_K = div_magic((uint32_t)lp.n_buckets);
+    a.magic_n = div_magic((uint32_t)lp.n_inst);
     hipError_t e;
     if (pl.fused) {
         e = launch_score_kernel<true>(pl, a, stream);

@@ -32,6 +32,8 @@ hipError_t launch_project_load(const star_load_params& p, const LoadPlan& pl,
 struct ScorePlan {
     bool fused = false;   // PM/SM built in LDS by the scoring kernel
     bool small = false;   // one workgroup scores and ranks everything
+    bool rank2 = false;   // fused scoring that code-sorts its keys, then one ranking workgroup
+    size_t ghist_off = 0, base_off = 0, keys_s_off = 0, keys_i_off = 0, offs_off = 0;
     int rpb = 0;          // requests per scoring workgroup
     int cand = 0;         // candidates per scoring workgroup (rpb * n)
     int groups = 0;       // scoring workgroups

@@ -102,9 +102,11 @@ def test_load_and_score_validation(L):
     big = star.load_params(1 << 26, 8, 64, 256)
     assert L.star_project_load(ctypes.byref(big), f, f, f, f, f, 256, None) == -3
 
-    # small rounds run in one workgroup with no scratch beyond the header;
-    # larger ones keep scores, best moves (and PM/SM) in the workspace
-    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 256)) == 256
+    # ranking keeps per-workgroup sorted keys (or scores and best moves, and
+    # PM/SM for large curve sets) in the workspace; without a top-k and with
+    # the curves in LDS only the header is needed
+    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 0)) >= 256
+    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 256)) > 256
     sp = star.score_params(4096, 16, 64, 512, 256)
     need = star.score_workspace_size(sp)
     assert need > 256
