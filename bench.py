@@ -35,10 +35,48 @@ def _parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--mode", choices=("graph", "eager"), default="graph")
+    ap.add_argument("--mode", choices=("graph", "eager"), default="eager",
+                    help="which timing gives `value` (the other is reported beside it)")
     ap.add_argument("--cpu-rounds", type=int, default=20,
                     help="rounds of the CPU oracle timed for the baseline (0 = skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device-to-device copy of known size (the "
+                         "reference for scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
     return ap.parse_args()
+
+
+COPY_BYTES = 256 << 20
+COPY_REPS = 8
+TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                            "gemm1_continuous_traffic.json")
+GEMM1_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2510_13668_amd",
+                            "csrc", "predict.hip")
+
+
+def copy_calibration():
+    """COPY_REPS copies of COPY_BYTES between two device buffers."""
+    import torch
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(COPY_REPS):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "reps": COPY_REPS}), flush=True)
+
+
+def measured_traffic():
+    """HBM bytes per first-layer GEMM launch from the committed counter runs,
+    or None when the kernel source changed since they were taken."""
+    import hashlib
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        with open(GEMM1_SOURCE, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    return t["traffic_bytes"] if t.get("source_sha256") == sha else None
 
 
 class HipEvents:
@@ -96,6 +134,9 @@ def cpu_baseline(x, wl, rounds: int):
 
 def main():
     args = _parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: this hot path runs on one GPU (decode instances are data, not devices); "
@@ -148,35 +189,37 @@ def main():
 
     with torch.cuda.stream(stream):
         round_(0, pp_init)                          # first decode step initialises the EMA
-    graphs = None
-    if args.mode == "graph":
-        graphs = []
-        for slot in range(S):
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g, stream=stream):
-                round_(slot)
-            graphs.append(g)
-    torch.cuda.synchronize()
-
-    def run_step(i):
-        slot = (i + 1) % S
-        if graphs is not None:
-            with torch.cuda.stream(stream):
-                graphs[slot].replay()
-        else:
+    graphs = []
+    for slot in range(S):                           # one captured round per staged step
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
             round_(slot)
+        graphs.append(g)
+    torch.cuda.synchronize()
 
-    for i in range(args.warmup):
-        run_step(i)
-    torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record(stream)
-    for i in range(args.steps):
-        run_step(args.warmup + i)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    ms_step = t_start.elapsed_time(t_end) / args.steps
+    def timed(mode):
+        """Milliseconds per round over args.steps rounds after args.warmup."""
+        def run_step(i):
+            slot = (i + 1) % S
+            if mode == "graph":
+                with torch.cuda.stream(stream):
+                    graphs[slot].replay()
+            else:
+                round_(slot)
+        for i in range(args.warmup):
+            run_step(i)
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for i in range(args.steps):
+            run_step(args.warmup + i)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / args.steps
+
+    ms_mode = {m: timed(m) for m in ("eager", "graph")}
+    ms_step = ms_mode[args.mode]
 
     # Dominant kernel (first-layer GEMM) timed with HIP events recorded by the
     # library around that kernel on the same stream, over `steps` eager rounds.
@@ -185,15 +228,10 @@ def main():
     arrs = [(ctypes.c_void_p * 2)(evs[2 * i].value, evs[2 * i + 1].value) for i in range(args.steps)]
     pps = [star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, False, wl.len_max,
                                ctypes.cast(a, ctypes.c_void_p)) for a in arrs]
-    e_start = torch.cuda.Event(enable_timing=True)
-    e_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    e_start.record(stream)
     for i in range(args.steps):
         round_((i + 1) % S, pps[i])
-    e_end.record(stream)
     torch.cuda.synchronize()
-    ms_step_eager = e_start.elapsed_time(e_end) / args.steps
     gemm_ms = [he.elapsed_ms(evs[2 * i], evs[2 * i + 1]) for i in range(args.steps)]
     he.destroy(evs)
     gemm_avg_s = float(np.mean(gemm_ms)) * 1e-3
@@ -219,11 +257,14 @@ def main():
                                "bins, EMA 0.2, horizon 16384 in 64-step buckets, 1024x8 candidates, "
                                "top-256",
                    "n_req": N, "d_model": d, "d_hidden": m, "n_bins": nb, "n_inst": n,
-                   "horizon": wl.horizon, "bucket": b, "top_k": top_k, "mode": args.mode},
-        "us_per_round_eager": ms_step_eager * 1e3,
-        "roofline": {"kernel": "gemm1_splitk_kernel<2> (bf16 MFMA, H[1024,4096] x W1[512,4096]^T)",
+                   "horizon": wl.horizon, "bucket": b, "top_k": top_k,
+                   "mode": args.mode + " (one stream, inputs resident in HBM)"},
+        "us_per_round_eager": ms_mode["eager"] * 1e3,
+        "us_per_round_graph": ms_mode["graph"] * 1e3,
+        "roofline": {"kernel": "gemm1_splitk_kernel (bf16 MFMA, H[1024,4096] x W1[512,4096]^T)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": measured_traffic(),
                      "avg_kernel_us": gemm_avg_s * 1e6, "algorithmic_flop": flops},
     }
     if args.cpu_rounds > 0:
