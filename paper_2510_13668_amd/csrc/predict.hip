@@ -31,6 +31,7 @@ constexpr int G1_ROW = G1_KBYTES + 16;         // padded LDS row (bytes)
 constexpr int G1_TILE = G1_BM * G1_ROW;        // one operand tile (bytes)
 constexpr int G1_THREADS = 256;
 constexpr int G1_STAGES = 3;                   // K-tiles of loads in flight ahead of the multiply
+constexpr int G1_OUT_ROW = G1_BN + 8;          // floats per LDS row of the output tile
 constexpr int G1_CHUNKS = G1_BM * G1_KBYTES / 16 / G1_THREADS;   // 16-byte chunks per thread per operand
 
 
@@ -53,6 +54,7 @@ struct G1Stage {
     uint4 a0, a1, a2, a3, b0, b1, b2, b3;
 };
 static_assert(G1_CHUNKS == 4, "G1Stage holds four 16-byte chunks per operand");
+static_assert(G1_BM * G1_OUT_ROW * 4 <= 2 * 2 * G1_TILE, "output tile fits the operand buffers");
 
 struct G1Ctx {
     const char* A;
@@ -162,9 +164,14 @@ __device__ __forceinline__ void g1_step(const G1Ctx& c, char (*lds)[2][G1_TILE],
                                         int i, G1Stage& s, int wm, int wn, int lane,
                                         f32x16 (&acc)[2][2]) {
     const int buf = i & 1;
+    // scheduling fences keep each phase in place: otherwise the compiler
+    // hoists the next stage's masking into the multiply, which then waits
+    // for loads issued only one step earlier
+    __builtin_amdgcn_sched_barrier(0);
     g1_store_stage(c, lds[buf][0], lds[buf][1], kt0 + i, s);
     __syncthreads();
     g1_load_stage(c, kt0 + (i + NS < nk ? i + NS : i), s);
+    __builtin_amdgcn_sched_barrier(0);
     g1_compute<kElemBytes>(lds[buf][0], lds[buf][1], wm, wn, lane, acc);
 }
 
@@ -220,20 +227,35 @@ __global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
             if (i + u < nk) g1_step<kElemBytes, NS>(c, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
     }
 
-    // epilogue: 32x32 accumulator layout -- element v of lane l is
-    // row 8*(v/4) + 4*(l/32) + v%4, column l%32 of the block.
-    float* out = P + (int64_t)split * M * N;
+    // epilogue: the 32x32 accumulator layout (element v of lane l is row
+    // 8*(v/4) + 4*(l/32) + v%4, column l%32 of its block) goes through LDS
+    // (the operand buffers, free now) so that global stores are whole
+    // 16-byte row chunks.  LDS rows hold G1_OUT_ROW floats (the padding puts
+    // the two 4-row halves of a store on disjoint banks).
+    __syncthreads();
+    float* otile = (float*)&lds[0][0][0];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            const int col = tn * G1_BN + wn * 64 + j * 32 + r32;
+            const int col = wn * 64 + j * 32 + r32;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int row = tm * G1_BM + wm * 64 + i * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
-                if (row < M && col < N) out[(int64_t)row * N + col] = acc[i][j][v];
+                const int row = wm * 64 + i * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
+                otile[row * G1_OUT_ROW + col] = acc[i][j][v];
             }
         }
+    __syncthreads();
+    float* out = P + (int64_t)split * M * N;
+    constexpr int CH = G1_BM * G1_BN / 4;             // float4 chunks in the tile
+#pragma unroll
+    for (int it = 0; it < CH / G1_THREADS; ++it) {
+        const int ch = it * G1_THREADS + tid;
+        const int row = ch / (G1_BN / 4), c4 = ch % (G1_BN / 4);
+        const int grow = tm * G1_BM + row, gcol = tn * G1_BN + c4 * 4;
+        if (grow < M && gcol < N)                     // N % 4 == 0: chunks never straddle N
+            *(float4*)&out[(int64_t)grow * N + gcol] = *(const float4*)&otile[row * G1_OUT_ROW + c4 * 4];
+    }
 }
 
 // ---------------------------------------------------------------------------

@@ -138,8 +138,8 @@ __device__ inline int64_t half_incl_max_i64(int64_t v) {
 
 // PM/SM of every instance from curves in LDS with row stride K+1 (entry K
 // of each row is padding).  Each instance is taken by a group of 32 lanes
-// (half a wave; kT/32 instances at a time); lane l owns a run of S =
-// ceil(K/32) consecutive buckets: a max over its run, one DPP scan across
+// (half a wave; kT/32 instances at a time); lane l owns a run of S (odd,
+// >= ceil(K/32)) consecutive buckets: a max over its run, one DPP scan across
 // the 32 runs, then a pass that writes.  Runs are read PMSM_BATCH entries at
 // a time so that their LDS reads are in flight together.  For SM the runs
 // are numbered from the end of the curve.
@@ -149,7 +149,10 @@ __device__ inline void build_pm_sm(const int64_t* lL, int64_t* lPM, int64_t* lSM
                                    int64_t bb) {
     const int l = threadIdx.x & 31;
     const int K1 = K + 1;
-    const int S = (K + 31) >> 5;
+    // run length: at least ceil(K/32), and odd, so that the 32 lanes' runs
+    // start on different LDS banks (an even stride of 2^j buckets would put
+    // them on a few banks only)
+    const int S = ((K + 31) >> 5) | 1;
     for (int t0 = 0; t0 < n; t0 += kT / 32) {
         const int t = t0 + (int)(threadIdx.x >> 5);
         const bool live = t < n;
@@ -1402,7 +1405,7 @@ void score_small_kernel(SmallArgs a) {
     __shared__ int64_t ws_s[STAR_MAX_TOP_K];
     __shared__ uint32_t ws_i[STAR_MAX_TOP_K];
     __shared__ uint64_t sv[STAR_MAX_TOP_K];
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
     const int N = a.N, n = a.n, b = a.b, K = a.K, K1 = K + 1, E = (n * K1 + 1) & ~1;
     int64_t* lL = (int64_t*)smem;
     int64_t* lPM = lL + E;
