@@ -38,8 +38,13 @@ def _load():
         lib.star_oracle_project_load.argtypes = [_I64, _I64, _I64, _I64, _P, _P, _P, _P, _P]
         lib.star_oracle_score.argtypes = [_I64, _I64, _I64, _I64, _P, _P, _P, _P, _P]
         lib.star_oracle_rank.argtypes = [_I64, _I64, _P, _P, _P, _P, _I64, _P, _P, _P, _P, _P]
+        lib.star_oracle_score_variance.argtypes = [_I64, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P]
+        lib.star_oracle_select_variance.argtypes = [_I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P]
+        lib.star_oracle_plan.argtypes = [_I64, _I64, _I64, _I64, _P, _P, _P, _P, _P, _I64, _I64,
+                                         ctypes.c_int, _I64, _I64, ctypes.c_int, _I64, _P, _P, _P]
         for f in ("star_oracle_predict", "star_oracle_project_load", "star_oracle_score",
-                  "star_oracle_rank"):
+                  "star_oracle_rank", "star_oracle_score_variance",
+                  "star_oracle_select_variance", "star_oracle_plan"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -159,3 +164,95 @@ def round_(cur_len, rem_len, inst_of, *, n_inst: int, bucket: int, n_buckets: in
     out = rank(cur_len, rem_len, inst_of, scores, top_k=top_k)
     out.update(load=load, scores=scores, flags=flags)
     return out
+
+
+# --------------------------------------------------------------------------
+# time-weighted variance objective and Algorithm 1 end to end
+# --------------------------------------------------------------------------
+def i128_values(pairs: np.ndarray) -> np.ndarray:
+    """(low, high) int64 pairs of 128-bit two's complement values -> Python ints."""
+    pairs = np.asarray(pairs, dtype=np.int64)
+    lo = pairs[..., 0].astype(np.uint64).astype(object)
+    hi = pairs[..., 1].astype(object)
+    return hi * (1 << 64) + lo
+
+
+def score_variance(cur_len, rem_len, inst_of, load, beta, *, bucket: int):
+    """Exact gains [N, n] (Python ints): (n/2) x the change of sum_k beta_k Var_k."""
+    cur = _c(cur_len, np.int32)
+    rem = _c(rem_len, np.int32)
+    inst = _c(inst_of, np.int32)
+    load = _c(load, np.int64)
+    beta = _c(beta, np.uint16)
+    n, K = load.shape
+    N = cur.shape[0]
+    assert beta.shape == (K,)
+    gain = np.empty((N, n, 2), np.int64)
+    rc = _load().star_oracle_score_variance(N, n, bucket, K, _ptr(cur), _ptr(rem), _ptr(inst),
+                                            _ptr(load), _ptr(beta), _ptr(gain))
+    if rc == -2:
+        raise OverflowError("star_oracle_score_variance: values beyond the exact range")
+    if rc != 0:
+        raise ValueError(f"star_oracle_score_variance failed ({rc})")
+    return i128_values(gain)
+
+
+def select_variance(cur_len, rem_len, inst_of, gain):
+    """Full-sort selection over exact gains [N, n] (Python ints).
+
+    Returns dict(best_target [N] i32, best_gain [N] object, move (r, s, t),
+    move_gain int).
+    """
+    cur = _c(cur_len, np.int32)
+    rem = _c(rem_len, np.int32)
+    inst = _c(inst_of, np.int32)
+    g = np.asarray(gain, dtype=object)
+    N, n = g.shape
+    pairs = np.empty((N, n, 2), np.int64)
+    flat = g.reshape(-1)
+    pv = pairs.reshape(-1, 2)
+    for e, v in enumerate(flat):
+        u = int(v) & ((1 << 128) - 1)
+        lo, hi = u & ((1 << 64) - 1), u >> 64
+        pv[e, 0] = lo - (1 << 64) if lo >= (1 << 63) else lo
+        pv[e, 1] = hi - (1 << 64) if hi >= (1 << 63) else hi
+    bt = np.empty(N, np.int32)
+    bg = np.empty((N, 2), np.int64)
+    mv = np.empty(3, np.int32)
+    mg = np.empty(2, np.int64)
+    rc = _load().star_oracle_select_variance(N, n, _ptr(cur), _ptr(rem), _ptr(inst), _ptr(pairs),
+                                             _ptr(bt), _ptr(bg), _ptr(mv), _ptr(mg))
+    if rc != 0:
+        raise ValueError("star_oracle_select_variance: malformed arguments")
+    return {"best_target": bt, "best_gain": i128_values(bg), "move": tuple(int(x) for x in mv),
+            "move_gain": int(i128_values(mg))}
+
+
+def plan(cur_len, rem_len, inst_of, beta, *, n_inst: int, bucket: int, n_buckets: int,
+         theta=(0, 1), u_mode: int = 0, min_rem: int = 0, mem_cap: int = (1 << 62),
+         mem_mode: int = 0, max_moves: int = 1):
+    """Algorithm 1 repeated up to ``max_moves`` times.
+
+    Returns dict(moves [(r, s, t)], gains [int], inst_of (final), load (final)).
+    """
+    cur = _c(cur_len, np.int32)
+    rem = _c(rem_len, np.int32)
+    inst = np.array(inst_of, dtype=np.int32, copy=True)
+    beta = _c(beta, np.uint16)
+    N = cur.shape[0]
+    load = np.empty((n_inst, n_buckets), np.int64)
+    moves = np.empty((max(max_moves, 1), 3), np.int32)
+    gains = np.empty((max(max_moves, 1), 2), np.int64)
+    cnt = np.zeros(1, np.int64)
+    rc = _load().star_oracle_plan(N, n_inst, bucket, n_buckets, _ptr(cur), _ptr(rem), _ptr(inst),
+                                  _ptr(load), _ptr(beta), int(theta[0]), int(theta[1]),
+                                  int(u_mode), int(min_rem), int(mem_cap), int(mem_mode),
+                                  int(max_moves), _ptr(moves), _ptr(gains), _ptr(cnt))
+    if rc == -2:
+        raise OverflowError("star_oracle_plan: values beyond the exact range")
+    if rc != 0:
+        raise ValueError(f"star_oracle_plan failed ({rc})")
+    m = int(cnt[0])
+    return {"moves": [tuple(int(x) for x in moves[q]) for q in range(m)],
+            "gains": [int(v) for v in i128_values(gains[:m])] if m else [],
+            "inst_of": inst, "load": load}

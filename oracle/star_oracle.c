@@ -255,6 +255,275 @@ int star_oracle_rank(int64_t N, int64_t n, const int32_t* cur, const int32_t* re
     return 0;
 }
 
+/* ---------------------------------------------------------------------- */
+/* (f1) time-weighted variance change of each migration                    */
+/* ---------------------------------------------------------------------- */
+/* Section 5.2 states the objective as the variance of the instances' token
+ * loads now plus a beta-weighted sum of the variances of their predicted
+ * loads at future steps (Eq. 3-4).  Over bucketed curves this is
+ *     Phi = sum_k beta_k Var_i(L_i[k]),   Var = population variance over i.
+ * n^2 Var_k = n sum_i L_i[k]^2 - (sum_i L_i[k])^2 is an integer, so
+ * n^2 Phi is an integer; a migration's change of n^2 Phi is always a
+ * multiple of 2n, and the oracle reports gain = change / (2n), i.e.
+ * (n/2) times the change of Phi (negative = the variance falls).
+ *
+ * Arithmetic: 128-bit two's complement.  Sums, differences and products are
+ * taken modulo 2^128 (unsigned __int128) and read back as signed, which is
+ * exact whenever the final value lies in (-2^127, 2^127); the function
+ * refuses inputs whose bound (from the actual curves) exceeds 2^125. */
+typedef unsigned __int128 u128;
+typedef __int128 s128;
+
+/* n^2 Var of one bucket over the n instance values v[0..n) */
+static u128 n2_var(const int64_t* v, int64_t n) {
+    u128 sum = 0, sq = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        sum += (u128)(s128)v[i];
+        sq += (u128)((s128)v[i] * (s128)v[i]);
+    }
+    return (u128)n * sq - sum * sum;
+}
+
+/* r's own bucketed curve, one decode step at a time (as in the scores) */
+static void own_curve(int64_t b, int64_t K, int32_t cur, int32_t rem, int64_t* own) {
+    const int64_t H = b * K;
+    for (int64_t k = 0; k < K; ++k) own[k] = 0;
+    for (int64_t t = 0; t < H && t < (int64_t)rem; ++t) own[t / b] += (int64_t)cur + t;
+}
+
+/* |change of n^2 Phi| <= 2n beta_max sum_k R_k (R_k + 2 max|L|) for any r;
+ * returns 0 when every candidate of this round stays below 2^125. */
+static int variance_in_range(int64_t N, int64_t n, int64_t b, int64_t K, const int32_t* cur,
+                             const int32_t* rem, const int32_t* inst, const int64_t* load,
+                             const uint16_t* beta) {
+    long double lmax = 0, bmax = 0;
+    for (int64_t e = 0; e < n * K; ++e) {
+        long double a = fabsl((long double)load[e]);
+        if (a > lmax) lmax = a;
+    }
+    for (int64_t k = 0; k < K; ++k)
+        if ((long double)beta[k] > bmax) bmax = (long double)beta[k];
+    int64_t* own = (int64_t*)malloc(sizeof(int64_t) * (size_t)K);
+    long double worst = 0;
+    for (int64_t r = 0; r < N; ++r) {
+        if (request_flags(r, n, cur, rem, inst)) continue;
+        own_curve(b, K, cur[r], rem[r], own);
+        long double acc = 0;
+        for (int64_t k = 0; k < K; ++k)
+            acc += (long double)own[k] * ((long double)own[k] + 2.0L * lmax);
+        if (acc > worst) worst = acc;
+    }
+    free(own);
+    return 2.0L * (long double)n * bmax * worst < ldexpl(1.0L, 125) ? 0 : -1;
+}
+
+/* change of n^2 Phi when r (on s, own curve `own`) moves to t: the full
+ * weighted variance of the moved curves minus that of the current ones */
+static s128 phi_change(int64_t n, int64_t K, const int64_t* load, const uint16_t* beta,
+                       int64_t s, int64_t t, const int64_t* own, int64_t* before,
+                       int64_t* after) {
+    u128 total = 0;
+    for (int64_t k = 0; k < K; ++k) {
+        for (int64_t i = 0; i < n; ++i) {
+            before[i] = load[i * K + k];
+            after[i] = load[i * K + k];
+        }
+        after[s] -= own[k];
+        after[t] += own[k];
+        total += (u128)beta[k] * (n2_var(after, n) - n2_var(before, n));
+    }
+    return (s128)total;
+}
+
+int star_oracle_score_variance(int64_t N, int64_t n, int64_t b, int64_t K,
+                               const int32_t* cur, const int32_t* rem, const int32_t* inst,
+                               const int64_t* load, const uint16_t* beta, int64_t* gain) {
+    if (N < 0 || n < 1 || b < 1 || K < 1) return -1;
+    if (variance_in_range(N, n, b, K, cur, rem, inst, load, beta)) return -2;
+    int bad = 0;
+
+    #pragma omp parallel for schedule(dynamic, 4) reduction(| : bad)
+    for (int64_t r = 0; r < N; ++r) {
+        int64_t* own = (int64_t*)malloc(sizeof(int64_t) * (size_t)K);
+        int64_t* before = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
+        int64_t* after = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
+        const int valid = request_flags(r, n, cur, rem, inst) == 0;
+        if (valid) own_curve(b, K, cur[r], rem[r], own);
+        for (int64_t t = 0; t < n; ++t) {
+            s128 g = 0;                           /* staying put changes nothing */
+            if (valid && t != inst[r]) {
+                s128 d = phi_change(n, K, load, beta, inst[r], t, own, before, after);
+                if (d % (2 * n) != 0) bad = 1;    /* impossible for consistent curves */
+                g = d / (2 * n);
+            }
+            gain[2 * (r * n + t)] = (int64_t)(uint64_t)(u128)g;
+            gain[2 * (r * n + t) + 1] = (int64_t)(g >> 64);
+        }
+        free(own);
+        free(before);
+        free(after);
+    }
+    return bad ? -3 : 0;
+}
+
+/* ---------------------------------------------------------------------- */
+/* (f1) best target per request and the best feasible migration            */
+/* ---------------------------------------------------------------------- */
+typedef struct { s128 g; int64_t r; int64_t t; } vtriple;
+
+static int cmp_vtriple(const void* a, const void* b) {
+    const vtriple* x = (const vtriple*)a;
+    const vtriple* y = (const vtriple*)b;
+    if (x->g != y->g) return x->g < y->g ? -1 : 1;
+    if (x->r != y->r) return x->r < y->r ? -1 : 1;
+    if (x->t != y->t) return x->t < y->t ? -1 : 1;
+    return 0;
+}
+
+static s128 read_gain(const int64_t* gain, int64_t e) {
+    return (s128)(((u128)(uint64_t)gain[2 * e + 1] << 64) | (u128)(uint64_t)gain[2 * e]);
+}
+
+static void write_gain(int64_t* out, s128 g) {
+    out[0] = (int64_t)(uint64_t)(u128)g;
+    out[1] = (int64_t)(g >> 64);
+}
+
+int star_oracle_select_variance(int64_t N, int64_t n, const int32_t* cur, const int32_t* rem,
+                                const int32_t* inst, const int64_t* gain,
+                                int32_t* best_target, int64_t* best_gain, int32_t* move,
+                                int64_t* move_gain) {
+    if (N < 0 || n < 1) return -1;
+    int64_t cap = N * (n - 1);
+    vtriple* all = (vtriple*)malloc(sizeof(vtriple) * (size_t)(cap > 0 ? cap : 1));
+    int64_t cnt = 0;
+    for (int64_t r = 0; r < N; ++r) {
+        if (request_flags(r, n, cur, rem, inst)) continue;
+        for (int64_t t = 0; t < n; ++t) {
+            if (t == inst[r]) continue;
+            all[cnt].g = read_gain(gain, r * n + t);
+            all[cnt].r = r;
+            all[cnt].t = t;
+            ++cnt;
+        }
+    }
+    qsort(all, (size_t)cnt, sizeof(vtriple), cmp_vtriple);
+    for (int64_t r = 0; r < N; ++r) {
+        if (best_target) best_target[r] = -1;
+        if (best_gain) write_gain(best_gain + 2 * r, 0);
+    }
+    for (int64_t e = cnt - 1; e >= 0; --e) {
+        if (best_target) best_target[all[e].r] = (int32_t)all[e].t;
+        if (best_gain) write_gain(best_gain + 2 * all[e].r, all[e].g);
+    }
+    /* the best feasible migration: largest reduction, taken only if it
+     * reduces the objective at all (the running maximum starts at zero) */
+    if (move) {
+        const int take = cnt > 0 && all[0].g < 0;
+        move[0] = take ? (int32_t)all[0].r : -1;
+        move[1] = take ? inst[all[0].r] : -1;
+        move[2] = take ? (int32_t)all[0].t : -1;
+        if (move_gain) write_gain(move_gain, take ? all[0].g : 0);
+    }
+    free(all);
+    return 0;
+}
+
+/* ---------------------------------------------------------------------- */
+/* (f2) Algorithm 1 end to end, one migration per pass, repeated           */
+/* ---------------------------------------------------------------------- */
+/* Each pass is one scheduler interval with no decode progress in between:
+ *   classification: w_i = sum_k beta_k L_i[k]; mean w = (1/n) sum_i w_i;
+ *     O = {i : w_i > (1 + theta) mean w};
+ *     U = {i : N_i(B_i) < (1 + theta) mean w} (u_mode 0, as printed), or
+ *         {i : w_i < (1 - theta) mean w}      (u_mode 1);
+ *     theta = theta_num / theta_den, all comparisons cross-multiplied;
+ *   enumeration: (r, s, t) with s in O, t in U, t != s, r on s valid,
+ *     rem_r > min_rem, and N_t(B_t) + rem_r (mem_mode 0, as printed) or
+ *     N_t(B_t) + cur_r + rem_r (mem_mode 1) <= mem_cap;
+ *   selection: the candidate with the smallest (gain, r, t) among gain < 0;
+ *   execution: inst_of[r] = t, and every curve is projected again from
+ *     scratch by per-step summation.
+ * Stops after max_moves passes, when O is empty, or when no candidate
+ * lowers the objective. */
+int star_oracle_plan(int64_t N, int64_t n, int64_t b, int64_t K, const int32_t* cur,
+                     const int32_t* rem, int32_t* inst, int64_t* load, const uint16_t* beta,
+                     int64_t theta_num, int64_t theta_den, int u_mode, int64_t min_rem,
+                     int64_t mem_cap, int mem_mode, int64_t max_moves, int32_t* moves,
+                     int64_t* move_gains, int64_t* n_moves) {
+    if (N < 0 || n < 1 || b < 1 || K < 1 || theta_num < 0 || theta_den < 1 || max_moves < 0)
+        return -1;
+    if (u_mode != 0 && u_mode != 1) return -1;
+    if (mem_mode != 0 && mem_mode != 1) return -1;
+    int32_t flags = 0;
+    if (star_oracle_project_load(N, n, b, K, cur, rem, inst, load, &flags)) return -1;
+    int64_t* own = (int64_t*)malloc(sizeof(int64_t) * (size_t)K);
+    int64_t* before = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
+    int64_t* after = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
+    s128* w = (s128*)malloc(sizeof(s128) * (size_t)n);
+    int64_t* now = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
+    char* over = (char*)malloc((size_t)n);
+    char* under = (char*)malloc((size_t)n);
+    int rc = 0;
+    int64_t done = 0;
+    while (done < max_moves) {
+        if (variance_in_range(N, n, b, K, cur, rem, inst, load, beta)) { rc = -2; break; }
+        /* phase 1: classification */
+        s128 wsum = 0;
+        for (int64_t i = 0; i < n; ++i) {
+            w[i] = 0;
+            for (int64_t k = 0; k < K; ++k) w[i] += (s128)beta[k] * (s128)load[i * K + k];
+            wsum += w[i];
+            now[i] = 0;
+        }
+        for (int64_t r = 0; r < N; ++r)
+            if (!request_flags(r, n, cur, rem, inst)) now[inst[r]] += cur[r];
+        int any_over = 0;
+        for (int64_t i = 0; i < n; ++i) {
+            /* x > (1 + theta) mean  <=>  n den x > (den + num) sum */
+            over[i] = (s128)n * theta_den * w[i] > (s128)(theta_den + theta_num) * wsum;
+            if (u_mode == 0)
+                under[i] = (s128)n * theta_den * now[i] < (s128)(theta_den + theta_num) * wsum;
+            else
+                under[i] = (s128)n * theta_den * w[i] < (s128)(theta_den - theta_num) * wsum;
+            any_over |= over[i];
+        }
+        if (!any_over) break;
+        /* phases 2-3: enumerate the filtered candidates, keep the best */
+        int have = 0;
+        s128 bg = 0;
+        int64_t br = -1, bt = -1;
+        for (int64_t r = 0; r < N; ++r) {
+            if (request_flags(r, n, cur, rem, inst)) continue;
+            const int64_t s = inst[r];
+            if (!over[s] || (int64_t)rem[r] <= min_rem) continue;
+            own_curve(b, K, cur[r], rem[r], own);
+            for (int64_t t = 0; t < n; ++t) {
+                if (t == s || !under[t]) continue;
+                const int64_t need = now[t] + rem[r] + (mem_mode ? (int64_t)cur[r] : 0);
+                if (need > mem_cap) continue;
+                s128 d = phi_change(n, K, load, beta, s, t, own, before, after);
+                if (d % (2 * n) != 0) { rc = -3; break; }
+                s128 g = d / (2 * n);
+                /* candidates arrive in (r, t) order: strict < keeps the first */
+                if (g < 0 && (!have || g < bg)) { have = 1; bg = g; br = r; bt = t; }
+            }
+            if (rc) break;
+        }
+        if (rc || !have) break;
+        moves[3 * done] = (int32_t)br;
+        moves[3 * done + 1] = inst[br];
+        moves[3 * done + 2] = (int32_t)bt;
+        write_gain(move_gains + 2 * done, bg);
+        inst[br] = (int32_t)bt;
+        ++done;
+        star_oracle_project_load(N, n, b, K, cur, rem, inst, load, &flags);
+    }
+    *n_moves = done;
+    free(own); free(before); free(after); free(w); free(now); free(over); free(under);
+    return rc;
+}
+
 int star_oracle_abi_version(void) { return 1; }
 
 /* Threads an OpenMP parallel region of the oracle uses (1 without OpenMP). */

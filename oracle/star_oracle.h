@@ -61,6 +61,43 @@ int star_oracle_rank(int64_t N, int64_t n, const int32_t* cur_len, const int32_t
                      int32_t* best_target, int64_t* best_score,
                      int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score);
 
+/* Time-weighted variance change of every migration (Section 5.2, Eq. 3-4;
+ * Algorithm 1's best-feasible selection with prediction).  beta [K] are the
+ * bucket weights (16-bit fixed point; only their ratios matter).  For r on
+ * s and t != s, gain[r,t] = (change of n^2 Phi) / (2n) when r's curve moves
+ * from s to t, Phi = sum_k beta_k Var_i(load[i,k]); 0 for t == s and for
+ * skipped requests.  gain is [N*n] 128-bit two's complement values stored as
+ * (low, high) int64 pairs.  Returns -2 when the values could leave the
+ * exactly representable range, -3 if a change is not a multiple of 2n. */
+int star_oracle_score_variance(int64_t N, int64_t n, int64_t b, int64_t K,
+                               const int32_t* cur_len, const int32_t* rem_len,
+                               const int32_t* inst_of, const int64_t* load,
+                               const uint16_t* beta, int64_t* gain);
+
+/* Selection over those gains by (gain, r, t) ascending, t != inst(r):
+ * best_target[r] / best_gain[r] (pairs): r's smallest key, or -1 / 0;
+ * move[3] = (r, s, t) of the smallest key overall if its gain is negative,
+ * else (-1, -1, -1), with its gain in move_gain[2] (0 when none). */
+int star_oracle_select_variance(int64_t N, int64_t n, const int32_t* cur_len,
+                                const int32_t* rem_len, const int32_t* inst_of,
+                                const int64_t* gain, int32_t* best_target, int64_t* best_gain,
+                                int32_t* move, int64_t* move_gain);
+
+/* Algorithm 1 end to end, repeated: classification with threshold
+ * theta = theta_num / theta_den, candidate filters (rem_len > min_rem;
+ * memory check against mem_cap), best-feasible selection on the variance
+ * gain, and execution, up to max_moves times.  inst_of is updated in place;
+ * load [n,K] receives the final curves.  moves [3*max_moves] get (r, s, t)
+ * per executed migration, move_gains [2*max_moves] their gains, *n_moves the
+ * count.  u_mode 0: U = {current load < (1+theta) mean w} as printed;
+ * 1: U = {w_i < (1-theta) mean w}.  mem_mode 0: N_t + rem_r <= mem_cap as
+ * printed; 1: N_t + cur_r + rem_r <= mem_cap. */
+int star_oracle_plan(int64_t N, int64_t n, int64_t b, int64_t K, const int32_t* cur_len,
+                     const int32_t* rem_len, int32_t* inst_of, int64_t* load,
+                     const uint16_t* beta, int64_t theta_num, int64_t theta_den, int u_mode,
+                     int64_t min_rem, int64_t mem_cap, int mem_mode, int64_t max_moves,
+                     int32_t* moves, int64_t* move_gains, int64_t* n_moves);
+
 int star_oracle_abi_version(void);
 int star_oracle_threads(void);
 

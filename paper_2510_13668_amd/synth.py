@@ -125,6 +125,17 @@ def bin_values(n_bins: int, lo: float, hi: float) -> np.ndarray:
     return v
 
 
+def bucket_weights(n_buckets: int, halvings: float = 8.0) -> np.ndarray:
+    """Bucket weights beta_k for the time-weighted variance objective (uint16).
+
+    beta_k = max(1, round(65535 * 2**(-halvings * k / K))): full weight now,
+    halving every K/halvings buckets, so the far horizon still counts.
+    """
+    k = np.arange(n_buckets, dtype=np.float64)
+    w = np.rint(65535.0 * np.exp2(-halvings * k / max(n_buckets, 1)))
+    return np.maximum(w, 1.0).astype(np.uint16)
+
+
 def _streams(seed: int):
     children = np.random.SeedSequence(seed).spawn(len(STREAMS))
     return {name: np.random.default_rng(c) for name, c in zip(STREAMS, children)}
