@@ -161,6 +161,51 @@ star_status star_score_migrations(const star_score_params* p, const int32_t* cur
                                   int64_t* topk_score, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * (f1) Migration candidates scored by the change of the time-weighted load
+ * variance.
+ *
+ * Section 5.2 sets the migration objective to the variance of the
+ * instances' token loads now plus a beta-weighted sum of the variances of
+ * their predicted loads at later steps (Eq. 3-4); Algorithm 1's best-feasible
+ * selection executes the candidate that reduces it most, if any does.  Over
+ * the bucketed curves of (b), Phi = sum_k beta_k Var_i(load[i, k]) (population
+ * variance over instances; bucket 0 holds the current step, so the paper's
+ * separate current-variance term is beta_0's share).  Moving request r
+ * (own curve R_r as in (c)) from s = inst_of[r] to t changes Phi by 2G/n with
+ *     gain[r, t] = G = sum_k beta_k R_r[k] (R_r[k] + load[t, k] - load[s, k]),
+ * reported exactly as a 128-bit integer; gain[r, s] = 0, and rows of invalid
+ * requests are 0.  Negative = the variance falls.
+ *   beta: uint16 [n_buckets] device array, the weights in fixed point (only
+ *         their ratios matter; 0 ignores a bucket).
+ *   best_target[r] / best_gain[r]: r's smallest key (gain, t) over t != s,
+ *         or -1 / 0 when r has none; the target may raise the variance.
+ *   best_move: ONE device star_move: the smallest key (gain, r, t) with
+ *         gain < 0 over all migrations, src = inst_of[req]; or
+ *         req = src = tgt = -1, gain 0 when no migration lowers Phi.
+ * Any of gain, best_target, best_gain, best_move may be NULL.
+ * STAR_ERR_OVERFLOW also when some gain could reach 2^126 in magnitude
+ * (bounded from n_req, bucket, n_buckets and the worst int32 cur_len).
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    uint64_t lo;   /* two's complement: value = hi * 2^64 + lo */
+    int64_t hi;
+} star_i128;
+
+typedef struct {
+    int32_t req, src, tgt;
+    int32_t reserved;
+    star_i128 gain;
+} star_move;
+
+size_t star_score_variance_workspace_size(const star_load_params* p);
+
+star_status star_score_variance(const star_load_params* p, const int32_t* cur_len,
+                                const int32_t* rem_len, const int32_t* inst_of,
+                                const int64_t* load, const uint16_t* beta, star_i128* gain,
+                                int32_t* best_target, star_i128* best_gain,
+                                star_move* best_move, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Housekeeping.
  * ---------------------------------------------------------------------- */
 /* Zero the whole workspace on `stream` (a fill kernel, no memset node).

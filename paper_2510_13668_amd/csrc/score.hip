@@ -101,30 +101,6 @@ __device__ inline int64_t wave_shr1_i64(int64_t v, int64_t ident) {
     return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
-// Per-request terms (Section 5.2 load model); invalid requests (instance
-// out of range, c < 1, l < 1) get s = -1 and zero terms.
-struct ReqTerms {
-    int64_t alpha, p;
-    int ke, s;
-    int32_t bad;
-};
-__device__ inline ReqTerms request_terms(int s, int c, int l, int n, int b, int64_t H) {
-    ReqTerms q;
-    q.bad = 0;
-    if (s < 0 || s >= n) q.bad |= STAR_DEV_BAD_INST;
-    if (c < 1) q.bad |= STAR_DEV_BAD_CUR;
-    if (l < 1) q.bad |= STAR_DEV_BAD_REM;
-    const int64_t lp = (int64_t)l < H ? (int64_t)l : H;
-    const int64_t ke = lp / b;
-    const int64_t mu = lp - ke * b;
-    const bool ok = q.bad == 0;
-    q.s = ok ? s : -1;
-    q.ke = ok ? (int)ke : 0;
-    q.alpha = ok ? (int64_t)b * c + (int64_t)b * (b - 1) / 2 : 0;
-    q.p = ok ? mu * c + mu * ke * b + mu * (mu - 1) / 2 : 0;
-    return q;
-}
-
 // Inclusive prefix max over the 32 lanes of each half wave (lane order):
 // DPP row shifts, then row 1 / row 3 take lane 15 of row 0 / row 2.
 __device__ inline int64_t half_incl_max_i64(int64_t v) {
@@ -342,7 +318,6 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wid = tid >> 6;
     const int n = a.n, K = a.K, b = a.b;
     const int K1 = K + 1;
     const int cand = a.cand;                       // rpb * n keys in this workgroup

@@ -177,6 +177,50 @@ STAR_API star_status star_score_migrations(const star_score_params* p, const int
 }
 
 // ---------------------------------------------------------------------------
+// time-weighted variance gains
+// ---------------------------------------------------------------------------
+static star_status check_variance_params(const star_load_params* p) {
+    star_status st = check_load_params(p);
+    if (st != STAR_OK) return st;
+    if ((int64_t)p->n_req * p->n_inst >= ((int64_t)1 << 31)) return STAR_ERR_UNSUPPORTED;
+    // |G| <= beta_max * sum_k R_k * (R_max + L_max), with R_k summing to at
+    // most H (c_max + H), R_max = b (c_max + H), L_max = N R_max, c_max < 2^31.
+    const long double cH = 2147483648.0L + (long double)p->bucket * p->n_buckets;
+    const long double H = (long double)p->bucket * p->n_buckets;
+    const long double rmax = (long double)p->bucket * cH;
+    const long double bound = 65535.0L * H * cH * ((long double)p->n_req + 1.0L) * rmax;
+    if (!(bound < ldexpl(1.0L, 126))) return STAR_ERR_OVERFLOW;
+    return STAR_OK;
+}
+
+STAR_API size_t star_score_variance_workspace_size(const star_load_params* p) {
+    if (check_variance_params(p) != STAR_OK) return 0;
+    return plan_variance(*p).total;
+}
+
+STAR_API star_status star_score_variance(const star_load_params* p, const int32_t* cur_len,
+                                         const int32_t* rem_len, const int32_t* inst_of,
+                                         const int64_t* load, const uint16_t* beta,
+                                         star_i128* gain, int32_t* best_target,
+                                         star_i128* best_gain, star_move* best_move, void* ws,
+                                         size_t ws_bytes, void* stream) {
+    star_status st = check_variance_params(p);
+    if (st != STAR_OK) return st;
+    if (!load || !beta) return STAR_ERR_INVALID_ARG;
+    if (p->n_req > 0 && (!cur_len || !rem_len || !inst_of)) return STAR_ERR_INVALID_ARG;
+    if (!aligned(gain, 16) || !aligned(best_gain, 16) || !aligned(best_move, 16))
+        return STAR_ERR_UNSUPPORTED;
+    const VarPlan pl = plan_variance(*p);
+    st = check_ws(ws, ws_bytes, pl.total);
+    if (st != STAR_OK) return st;
+    int32_t* err = (int32_t*)((char*)ws + kHdrErrorWord);
+    hipError_t e = launch_variance(*p, pl, cur_len, rem_len, inst_of, load, beta, gain,
+                                   best_target, best_gain, best_move, (char*)ws, err,
+                                   (hipStream_t)stream);
+    return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
 // housekeeping
 // ---------------------------------------------------------------------------
 STAR_API star_status star_workspace_init(void* ws, size_t ws_bytes, void* stream) {

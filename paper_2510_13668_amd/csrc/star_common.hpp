@@ -149,6 +149,33 @@ __device__ inline int64_t block_exclusive_scan_i64(int64_t v, Op op, int64_t ide
     return res;
 }
 
+// Per-request terms of Section 5.2's load model.  With l' = min(l, H),
+// k_e = l' div b and mu = l' mod b, request r's own bucketed curve is
+// alpha + b^2 k for k < k_e (alpha = b c + b(b-1)/2), p = mu c + mu k_e b +
+// mu(mu-1)/2 at k = k_e, and 0 beyond.  Invalid requests (instance out of
+// range, c < 1, l < 1) get s = -1 and zero terms.
+struct ReqTerms {
+    int64_t alpha, p;
+    int ke, s;
+    int32_t bad;
+};
+__device__ inline ReqTerms request_terms(int s, int c, int l, int n, int b, int64_t H) {
+    ReqTerms q;
+    q.bad = 0;
+    if (s < 0 || s >= n) q.bad |= STAR_DEV_BAD_INST;
+    if (c < 1) q.bad |= STAR_DEV_BAD_CUR;
+    if (l < 1) q.bad |= STAR_DEV_BAD_REM;
+    const int64_t lp = (int64_t)l < H ? (int64_t)l : H;
+    const int64_t ke = lp / b;
+    const int64_t mu = lp - ke * b;
+    const bool ok = q.bad == 0;
+    q.s = ok ? s : -1;
+    q.ke = ok ? (int)ke : 0;
+    q.alpha = ok ? (int64_t)b * c + (int64_t)b * (b - 1) / 2 : 0;
+    q.p = ok ? mu * c + mu * ke * b + mu * (mu - 1) / 2 : 0;
+    return q;
+}
+
 // Device-error reporting: OR `bits` into the workspace error word.
 __device__ inline void report_error(int32_t* err_word, int32_t bits) {
     if (bits) atomicOr(err_word, bits);

@@ -50,6 +50,19 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
                         int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score, char* ws,
                         int32_t* err_word, hipStream_t stream);
 
+struct VarPlan {
+    int lpr_log2 = 0;     // lanes per request (log2)
+    int groups = 0;       // request groups (one wave each)
+    int blocks = 0;       // scoring workgroups
+    size_t qa_off = 0, qb_off = 0, bs_off = 0, part_off = 0, total = 0;
+};
+VarPlan plan_variance(const star_load_params& p);
+hipError_t launch_variance(const star_load_params& p, const VarPlan& pl, const int32_t* cur,
+                           const int32_t* rem, const int32_t* inst, const int64_t* load,
+                           const uint16_t* beta, star_i128* gain, int32_t* best_target,
+                           star_i128* best_gain, star_move* move, char* ws, int32_t* err,
+                           hipStream_t stream);
+
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 
 }  // namespace star

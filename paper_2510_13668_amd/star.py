@@ -78,6 +78,11 @@ def lib():
         L.star_score_migrations.restype = ctypes.c_int
         L.star_score_migrations.argtypes = ([ctypes.POINTER(ScoreParams)] + [_P] * 11 +
                                             [ctypes.c_size_t, _P])
+        L.star_score_variance_workspace_size.restype = ctypes.c_size_t
+        L.star_score_variance_workspace_size.argtypes = [ctypes.POINTER(LoadParams)]
+        L.star_score_variance.restype = ctypes.c_int
+        L.star_score_variance.argtypes = ([ctypes.POINTER(LoadParams)] + [_P] * 10 +
+                                          [ctypes.c_size_t, _P])
         L.star_workspace_init.restype = ctypes.c_int
         L.star_workspace_init.argtypes = [_P, ctypes.c_size_t, _P]
         L.star_read_device_error.restype = ctypes.c_int
@@ -192,3 +197,31 @@ def score_migrations(p: ScoreParams, cur_len, rem_len, inst_of, load, scores, be
         ctypes.byref(p), _ptr(cur_len), _ptr(rem_len), _ptr(inst_of), _ptr(load), _ptr(scores),
         _ptr(best_target), _ptr(best_score), _ptr(topk_req), _ptr(topk_tgt), _ptr(topk_score),
         ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# time-weighted variance gains
+# ---------------------------------------------------------------------------
+MOVE_FIELDS = 8   # star_move as int32 words: req, src, tgt, reserved, gain (4 words)
+
+
+def score_variance_workspace_size(p: LoadParams) -> int:
+    return int(lib().star_score_variance_workspace_size(ctypes.byref(p)))
+
+
+def score_variance(p: LoadParams, cur_len, rem_len, inst_of, load, beta, gain, best_target,
+                   best_gain, best_move, ws: Workspace, stream=None):
+    """star_score_variance.  128-bit outputs are int64 tensors with a trailing
+    dimension of 2 (low word, high word): gain [N, n, 2], best_gain [N, 2];
+    best_move is an int32 tensor of MOVE_FIELDS words.  beta is int16 bits of
+    the uint16 weights [K]."""
+    _dev(cur_len, rem_len, inst_of, load, beta, gain, best_target, best_gain, best_move)
+    _check("star_score_variance", lib().star_score_variance(
+        ctypes.byref(p), _ptr(cur_len), _ptr(rem_len), _ptr(inst_of), _ptr(load), _ptr(beta),
+        _ptr(gain), _ptr(best_target), _ptr(best_gain), _ptr(best_move),
+        ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))
+
+
+def i128_to_int(lo: int, hi: int) -> int:
+    """One (low, high) int64 pair of a 128-bit two's complement value."""
+    return (int(hi) << 64) + (int(lo) & ((1 << 64) - 1))

@@ -122,6 +122,28 @@ def test_load_and_score_validation(L):
                                    1 << 30, None) == -2
 
 
+def test_score_variance_validation(L):
+    f = FAKE
+    lp = star.load_params(1024, 8, 64, 256)
+    need = star.score_variance_workspace_size(lp)
+    # 128-bit prefix tables: two per instance and one for the weights, K + 1 each
+    assert need >= 256 + (2 * 8 + 3) * 257 * 16
+    args = [f] * 9            # cur, rem, inst, load, beta, gain, best_target, best_gain, move
+    assert L.star_score_variance(ctypes.byref(lp), *args, f, need - 1, None) == -4
+    assert L.star_score_variance(ctypes.byref(lp), *args[:4], None, *args[5:], f, need, None) == -1
+    assert L.star_score_variance(ctypes.byref(lp), *args[:3], None, *args[4:], f, need, None) == -1
+    odd = ctypes.c_void_p((1 << 20) + 8)
+    assert L.star_score_variance(ctypes.byref(lp), *args[:5], odd, *args[6:], f, need, None) == -2
+    assert L.star_score_variance(None, *args, f, need, None) == -1
+    # gains that could reach 2^126: refused although int64 curves would fit
+    big = star.load_params(1 << 18, 8, 1 << 10, 1 << 20)
+    assert L.star_project_load(ctypes.byref(big), f, f, f, f, f, 256, None) != -3
+    assert L.star_score_variance(ctypes.byref(big), *args, f, 1 << 40, None) == -3
+    assert star.score_variance_workspace_size(big) == 0
+    # the largest rebalancing scan (32768 requests, 64 instances, 1024 buckets of 64) fits
+    assert star.score_variance_workspace_size(star.load_params(32768, 64, 64, 1024)) > 0
+
+
 def test_read_device_error_rejects_bad_args(L):
     code = ctypes.c_int32(0)
     assert L.star_read_device_error(FAKE, None, None) == -1
