@@ -12,6 +12,12 @@ microseconds per round.
 
 Prints ONE JSON line.  Usage:
     python bench.py [--gpus 1] [--steps 200] [--warmup 10] [--mode graph|eager]
+
+``--path variance [--workload NAME]`` measures the time-weighted variance
+objective instead: per step, star_project_load -> star_score_variance (every
+migration's exact gain, each request's best target, the best feasible
+move) on a workload's true remaining lengths, as the paper's oracle-predictor
+runs do; one JSON line of its own.
 """
 from __future__ import annotations
 
@@ -39,6 +45,11 @@ def _parse():
                     help="which timing gives `value` (the other is reported beside it)")
     ap.add_argument("--cpu-rounds", type=int, default=20,
                     help="rounds of the CPU oracle timed for the baseline (0 = skip)")
+    ap.add_argument("--path", choices=("round", "variance"), default="round",
+                    help="round: the full rescheduling round; variance: projection + "
+                         "variance-gain scoring")
+    ap.add_argument("--workload", default="rebalance_scan",
+                    help="workload of --path variance")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device-to-device copy of known size (the "
                          "reference for scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -132,6 +143,141 @@ def cpu_baseline(x, wl, rounds: int):
                       f"full sort); {dt:.2f} s"}
 
 
+VAR_STEPS = 16    # staged decode steps of the variance path (cur + s, rem - s)
+
+
+def variance_inputs(wl):
+    """Per-request arrays of the variance path: current lengths, true
+    remaining lengths (a seeded draw where the workload has none) and
+    instances, advanced by one decode step per staged step."""
+    from paper_2510_13668_amd import synth
+    x = synth.make_inputs(wl, steps=1, n_req=1)
+    rem = x.true_len
+    if rem is None:
+        rem = np.random.default_rng(0).integers(1, wl.horizon, size=wl.n_req,
+                                                endpoint=True).astype(np.int32)
+    cur = np.stack([x.cur_len + s for s in range(VAR_STEPS)]).astype(np.int32)
+    rem = np.stack([np.maximum(rem - s, 1) for s in range(VAR_STEPS)]).astype(np.int32)
+    return cur, rem, x.inst_of
+
+
+def variance_cpu_baseline(wl, cur, rem, inst, beta, sample: int):
+    """The oracle on one step: the full projection, then the variance gains
+    and the selection for `sample` requests; scaled to requests/s."""
+    import oracle
+    t0 = time.perf_counter()
+    load, _ = oracle.project_load(cur, rem, inst, n_inst=wl.n_inst, bucket=wl.bucket,
+                                  n_buckets=wl.n_buckets)
+    t_proj = time.perf_counter() - t0
+    idx = np.linspace(0, wl.n_req - 1, sample).astype(np.int64)
+    t0 = time.perf_counter()
+    g = oracle.score_variance(cur[idx], rem[idx], inst[idx], load, beta, bucket=wl.bucket)
+    oracle.select_variance(cur[idx], rem[idx], inst[idx], g)
+    t_score = time.perf_counter() - t0
+    per_req = t_proj / wl.n_req + t_score / sample
+    return {"value": 1.0 / per_req, "unit": "requests/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"one decode step: projection of all {wl.n_req} requests ({t_proj:.2f} s) "
+                      f"plus exact variance gains (full weighted variance of the moved curves "
+                      f"per candidate) and the full-sort selection for {sample} evenly spaced "
+                      f"requests ({t_score:.2f} s)"}
+
+
+def bench_variance(args):
+    import torch
+    from paper_2510_13668_amd import star, synth
+
+    dev = "cuda"
+    wl = synth.WORKLOADS[args.workload]
+    N, n, b, K = wl.n_req, wl.n_inst, wl.bucket, wl.n_buckets
+    cur_h, rem_h, inst_h = variance_inputs(wl)
+    beta_h = synth.bucket_weights(K)
+    cur = torch.from_numpy(cur_h).to(dev)
+    rem = torch.from_numpy(rem_h).to(dev)
+    inst = torch.from_numpy(inst_h).to(dev)
+    beta = torch.from_numpy(beta_h.view(np.int16)).to(dev)
+    load = torch.empty((n, K), dtype=torch.int64, device=dev)
+    gain = torch.empty((N, n, 2), dtype=torch.int64, device=dev)
+    best_t = torch.empty(N, dtype=torch.int32, device=dev)
+    best_g = torch.empty((N, 2), dtype=torch.int64, device=dev)
+    move = torch.empty(star.MOVE_FIELDS, dtype=torch.int32, device=dev)
+    lp = star.load_params(N, n, b, K)
+    ws_l = star.Workspace(star.project_load_workspace_size(lp))
+    ws_v = star.Workspace(star.score_variance_workspace_size(lp))
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+
+    def project(slot):
+        star.project_load(lp, cur[slot], rem[slot], inst, load, ws_l, stream)
+
+    def score(slot):
+        star.score_variance(lp, cur[slot], rem[slot], inst, load, beta, gain, best_t, best_g, move,
+                            ws_v, stream)
+
+    for i in range(args.warmup):
+        project(i % VAR_STEPS)
+        score(i % VAR_STEPS)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        project(i % VAR_STEPS)
+        score(i % VAR_STEPS)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+
+    # star_score_variance (prefix tables + scoring) timed with HIP events on
+    # its stream, one pair per call
+    he = HipEvents()
+    evs = he.create(2 * args.steps)
+    hs = ctypes.c_void_p(stream.cuda_stream)
+    he.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    for i in range(args.steps):
+        project(i % VAR_STEPS)
+        he.hip.hipEventRecord(evs[2 * i], hs)
+        score(i % VAR_STEPS)
+        he.hip.hipEventRecord(evs[2 * i + 1], hs)
+    torch.cuda.synchronize()
+    call_s = float(np.mean([he.elapsed_ms(evs[2 * i], evs[2 * i + 1])
+                            for i in range(args.steps)])) * 1e-3
+    he.destroy(evs)
+    # algorithmic bytes of one call: request arrays, curves and weights in;
+    # gains, best targets and gains, and the move out
+    nbytes = 12 * N + 8 * n * K + 2 * K + 16 * N * n + 20 * N + 32
+    achieved = nbytes / call_s / 1e9
+
+    out = {
+        "metric": "requests scored/sec by exact time-weighted variance gain "
+                  "(projection + all N x n migrations + best feasible move)",
+        "value": N / (ms_step * 1e-3),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int128",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {N} requests on {n} instances, true remaining "
+                               f"lengths {wl.true_len or 'uniform'}, horizon {wl.horizon} in "
+                               f"{b}-step buckets, weights halving every K/8 buckets, "
+                               f"{N}x{n} migrations, {VAR_STEPS} staged decode steps",
+                   "n_req": N, "n_inst": n, "horizon": wl.horizon, "bucket": b},
+        "roofline": {"kernel": "star_score_variance (var_prep_kernel + var_score_kernel)",
+                     "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "avg_call_us": call_s * 1e6, "algorithmic_bytes": nbytes},
+    }
+    if args.cpu_rounds > 0:
+        out["cpu_baseline"] = variance_cpu_baseline(wl, cur_h[0], rem_h[0], inst_h, beta_h,
+                                                    min(N, 8192))
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = _parse()
     if args.copy_calibration:
@@ -142,6 +288,9 @@ def main():
         print("bench.py: this hot path runs on one GPU (decode instances are data, not devices); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
+    if args.path == "variance":
+        bench_variance(args)
+        return
 
     import torch
     from paper_2510_13668_amd import star, synth

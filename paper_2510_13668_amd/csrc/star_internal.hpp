@@ -51,10 +51,10 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
                         int32_t* err_word, hipStream_t stream);
 
 struct VarPlan {
-    int lpr_log2 = 0;     // lanes per request (log2)
-    int groups = 0;       // request groups (one wave each)
+    int lg = 0;           // lanes per request = 2^lg (<= 16)
     int blocks = 0;       // scoring workgroups
-    size_t qa_off = 0, qb_off = 0, bs_off = 0, part_off = 0, total = 0;
+    bool ticketed = false;  // best move found inside the scoring kernel
+    size_t qt_off = 0, lt_off = 0, bs_off = 0, part_off = 0, total = 0;
 };
 VarPlan plan_variance(const star_load_params& p);
 hipError_t launch_variance(const star_load_params& p, const VarPlan& pl, const int32_t* cur,

@@ -28,14 +28,17 @@
 // smallest key (G, r n + t) with G < 0.
 //
 // Kernels:
-//  * var_prep_kernel: one workgroup per instance row (QA, QB) plus one for
-//    the weight sums (B0, B1, B2); a chunked block scan in LDS.
-//  * var_score_kernel: each wave takes requests in groups of 64 / P lanes,
-//    P = the power of two >= n (capped at 64; larger n loops over targets).
-//    A lane scores one candidate, writes its gain, and the group's best
-//    target comes from a butterfly of lane shuffles.  Negative best keys are
-//    reduced per workgroup; the last workgroup to finish (atomic ticket)
-//    reduces the workgroups' partials and writes the best feasible move.
+//  * var_prep_kernel: one workgroup per instance (QA, QB) plus one for the
+//    weight sums (B0, B1, B2); a chunked block scan in LDS.  The
+//    per-instance tables are stored bucket-major, [k][t] (and a bucket-major
+//    copy of the curves), so that the lanes scoring one request's targets
+//    read one contiguous run.
+//  * var_score_kernel: up to 16 lanes per request; a lane walks every 16th
+//    target (reads and writes stay contiguous across the request's lanes)
+//    and keeps its best key in registers, and a short DPP scan combines the
+//    lanes.  Negative best keys are reduced per workgroup.  In small grids the last workgroup to finish
+//    (atomic ticket) reduces the workgroups' partials and writes the best
+//    feasible move; larger grids leave that to var_final_kernel.
 #include "star_common.hpp"
 #include "star_internal.hpp"
 
@@ -47,11 +50,33 @@ typedef __int128 s128;
 constexpr int VP_THREADS = 256;
 constexpr int VS_THREADS = 256;
 constexpr int VS_WAVES = VS_THREADS / kWave;
-constexpr int VS_MAX_BLOCKS = 1024;
 
 constexpr size_t kHdrVarTicket = 64;   // workspace header: finished-workgroup ticket
+// Grids up to this many workgroups find the best move in the scoring kernel
+// (the last workgroup to finish reduces the partials); larger ones hand the
+// partials to a one-workgroup kernel, because every workgroup's release
+// fence would write back its XCD's L2, full of freshly written gains.
+constexpr int VS_TICKET_BLOCKS = 64;
+constexpr int VS_MAX_LG = 4;             // at most 16 lanes per request
 
 __device__ inline u128 wide(int64_t v) { return (u128)(s128)v; }
+
+// a * x modulo 2^128 for a 128-bit a and a non-negative 64-bit x: one full
+// 64 x 64 product and one low half
+__device__ inline u128 mul_u64(u128 a, uint64_t x) {
+    return (u128)(uint64_t)a * x + ((u128)((uint64_t)(a >> 64) * x) << 64);
+}
+// a * x modulo 2^128 for a signed 64-bit x (x sign-extended to 128 bits)
+__device__ inline u128 mul_s64(u128 a, int64_t x) {
+    u128 r = mul_u64(a, (uint64_t)x);
+    if (x < 0) r -= a << 64;
+    return r;
+}
+
+// one bucket-major table entry: QA_t[k], QB_t[k]
+struct QEntry {
+    u128 qa, qb;
+};
 
 // ---------------------------------------------------------------------------
 // prefix tables
@@ -60,11 +85,27 @@ __device__ inline u128 wide(int64_t v) { return (u128)(s128)v; }
 // Thread j of the workgroup owns the buckets [j*per, (j+1)*per); its sums
 // are scanned across the workgroup in LDS (inclusive Hillis-Steele; the
 // exclusive prefix is the inclusive one minus the thread's own sum, which
-// modular arithmetic allows), then each thread writes its run.
+// modular arithmetic allows), then each thread writes its run.  Up to
+// VP_REG buckets per thread stay in registers between the two passes, so
+// that no load waits behind the table stores (loads and stores share one
+// counter on gfx9).
+constexpr int VP_REG = 8;
+
+__device__ inline void prep_load(const uint16_t* beta, const int64_t* L, bool wrow, int c0,
+                                 int last, uint32_t* wv, int64_t* lv) {
+#pragma unroll
+    for (int i = 0; i < VP_REG; ++i) {
+        const int j = c0 + i < last ? c0 + i : last;   // clamped: no branch per slot
+        wv[i] = beta[j];
+        lv[i] = wrow ? 0 : L[j];
+    }
+}
+
 __global__ __launch_bounds__(VP_THREADS) void var_prep_kernel(const int64_t* __restrict__ load,
                                                               const uint16_t* __restrict__ beta,
-                                                              int n, int K, u128* __restrict__ qa,
-                                                              u128* __restrict__ qb,
+                                                              int n, int K,
+                                                              QEntry* __restrict__ qt,
+                                                              int64_t* __restrict__ lt,
                                                               u128* __restrict__ bs,
                                                               uint32_t* __restrict__ ticket) {
     __shared__ u128 sx[3][VP_THREADS];
@@ -77,17 +118,24 @@ __global__ __launch_bounds__(VP_THREADS) void var_prep_kernel(const int64_t* __r
 
     if (row == 0 && tid == 0) *ticket = 0u;   // the scoring kernel runs after this one
 
+    uint32_t wv[VP_REG];
+    int64_t lv[VP_REG];
     u128 x0 = 0, x1 = 0, x2 = 0;
-    for (int j = j0; j < j1; ++j) {
-        const u128 w = beta[j], uj = (u128)j;
-        if (wrow) {
-            x0 += w;
-            x1 += w * uj;
-            x2 += w * uj * uj;
-        } else {
-            const u128 wl = w * wide(L[j]);
-            x0 += wl;
-            x1 += wl * uj;
+    for (int c0 = j0; c0 < j1; c0 += VP_REG) {
+        prep_load(beta, L, wrow, c0, j1 - 1, wv, lv);
+#pragma unroll
+        for (int i = 0; i < VP_REG; ++i) {
+            const bool in = c0 + i < j1;
+            const u128 w = in ? (u128)wv[i] : (u128)0, uj = (u128)(c0 + i);
+            if (wrow) {
+                x0 += w;
+                x1 += w * uj;
+                x2 += w * uj * uj;
+            } else {
+                const u128 wl = mul_s64(w, lv[i]);
+                x0 += wl;
+                x1 += wl * uj;
+            }
         }
     }
     sx[0][tid] = x0;
@@ -108,28 +156,37 @@ __global__ __launch_bounds__(VP_THREADS) void var_prep_kernel(const int64_t* __r
         __syncthreads();
     }
     u128 p0 = sx[0][tid] - x0, p1 = sx[1][tid] - x1, p2 = sx[2][tid] - x2;
-    u128* o0 = wrow ? bs : qa + (size_t)row * K1;
-    u128* o1 = wrow ? bs + K1 : qb + (size_t)row * K1;
-    u128* o2 = bs + 2 * (size_t)K1;
-    for (int j = j0; j < j1; ++j) {
-        o0[j] = p0;
-        o1[j] = p1;
-        if (wrow) o2[j] = p2;
-        const u128 w = beta[j], uj = (u128)j;
-        if (wrow) {
-            p0 += w;
-            p1 += w * uj;
-            p2 += w * uj * uj;
-        } else {
-            const u128 wl = w * wide(L[j]);
-            p0 += wl;
-            p1 += wl * uj;
+    for (int c0 = j0; c0 < j1; c0 += VP_REG) {
+        if (per > VP_REG) prep_load(beta, L, wrow, c0, j1 - 1, wv, lv);
+#pragma unroll
+        for (int i = 0; i < VP_REG; ++i) {
+            const int j = c0 + i;
+            if (j >= j1) break;
+            const u128 w = wv[i], uj = (u128)j;
+            if (wrow) {
+                bs[j] = p0;
+                bs[K1 + j] = p1;
+                bs[2 * (size_t)K1 + j] = p2;
+                p0 += w;
+                p1 += w * uj;
+                p2 += w * uj * uj;
+            } else {
+                qt[(size_t)j * n + row] = QEntry{p0, p1};
+                lt[(size_t)j * n + row] = lv[i];
+                const u128 wl = mul_s64(w, lv[i]);
+                p0 += wl;
+                p1 += wl * uj;
+            }
         }
     }
     if (tid == VP_THREADS - 1) {
-        o0[K] = sx[0][tid];
-        o1[K] = sx[1][tid];
-        if (wrow) o2[K] = sx[2][tid];
+        if (wrow) {
+            bs[K] = sx[0][tid];
+            bs[K1 + K] = sx[1][tid];
+            bs[2 * (size_t)K1 + K] = sx[2][tid];
+        } else {
+            qt[(size_t)K * n + row] = QEntry{sx[0][tid], sx[1][tid]};
+        }
     }
 }
 
@@ -147,21 +204,56 @@ __device__ inline bool vless(const VKey& a, const VKey& b) {
 }
 __device__ inline VKey vmin(const VKey& a, const VKey& b) { return vless(b, a) ? b : a; }
 
-__device__ inline VKey shfl_xor_key(const VKey& k, int m) {
+// DPP move of a whole key; a lane whose source lies outside its row, or in
+// a row that kRowMask leaves out, receives the no-key sentinel
+template <int kCtrl, int kRowMask>
+__device__ inline VKey dpp_key(const VKey& k) {
     const u128 u = (u128)k.g;
-    const uint32_t w0 = (uint32_t)__shfl_xor((int)(uint32_t)u, m, kWave);
-    const uint32_t w1 = (uint32_t)__shfl_xor((int)(uint32_t)(u >> 32), m, kWave);
-    const uint32_t w2 = (uint32_t)__shfl_xor((int)(uint32_t)(u >> 64), m, kWave);
-    const uint32_t w3 = (uint32_t)__shfl_xor((int)(uint32_t)(u >> 96), m, kWave);
+    const u128 inf = ~(u128)0 >> 1;
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        w[i] = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(inf >> (32 * i)),
+                                                    (int)(uint32_t)(u >> (32 * i)), kCtrl,
+                                                    kRowMask, 0xF, false);
     VKey o;
-    o.g = (s128)(((u128)w3 << 96) | ((u128)w2 << 64) | ((u128)w1 << 32) | (u128)w0);
-    o.idx = (uint32_t)__shfl_xor((int)k.idx, m, kWave);
+    o.g = (s128)(((u128)w[3] << 96) | ((u128)w[2] << 64) | ((u128)w[1] << 32) | (u128)w[0]);
+    o.idx = (uint32_t)__builtin_amdgcn_update_dpp((int)kNoIdx, (int)k.idx, kCtrl, kRowMask, 0xF,
+                                                  false);
     return o;
 }
 
-// min over lanes whose indexes differ only in the bits of [lo, hi)
-__device__ inline VKey butterfly_min(VKey k, int lo, int hi) {
-    for (int m = lo; m < hi; m <<= 1) k = vmin(k, shfl_xor_key(k, m));
+// Minimum over each aligned group of 2^lg lanes (lg <= 6), valid in the
+// group's last lane: an inclusive min-scan by DPP row shifts, where a lane
+// ignores a source in the previous group (tl = lane index in its group),
+// then the row broadcasts for groups of 32 and 64 lanes.  Every lane of the
+// wave must be active.
+__device__ inline VKey group_min(VKey k, int lg, int tl) {
+    VKey o;
+    if (lg >= 1) {
+        o = dpp_key<kDppRowShr1, 0xF>(k);
+        if (tl >= 1 && vless(o, k)) k = o;
+    }
+    if (lg >= 2) {
+        o = dpp_key<kDppRowShr2, 0xF>(k);
+        if (tl >= 2 && vless(o, k)) k = o;
+    }
+    if (lg >= 3) {
+        o = dpp_key<kDppRowShr4, 0xF>(k);
+        if (tl >= 4 && vless(o, k)) k = o;
+    }
+    if (lg >= 4) {
+        o = dpp_key<kDppRowShr8, 0xF>(k);
+        if (tl >= 8 && vless(o, k)) k = o;
+    }
+    if (lg >= 5) {
+        o = dpp_key<kDppRowBcast15, 0xA>(k);
+        if (vless(o, k)) k = o;
+    }
+    if (lg >= 6) {
+        o = dpp_key<kDppRowBcast31, 0xC>(k);
+        if (vless(o, k)) k = o;
+    }
     return k;
 }
 
@@ -184,112 +276,34 @@ __device__ inline VKey load_part(VPart* p) {
     return VKey{(s128)(((u128)hi << 64) | (u128)lo), (uint32_t)ix};
 }
 
-struct VarArgs {
-    const int32_t* cur;
-    const int32_t* rem;
-    const int32_t* inst;
-    const int64_t* load;
-    const uint16_t* beta;
-    const u128* qa;
-    const u128* qb;
-    const u128* bs;
-    u128* gain;              // [N, n] or null
-    int32_t* best_target;    // [N] or null
-    u128* best_gain;         // [N] or null
-    star_move* move;         // one, or null
-    VPart* part;             // [gridDim.x] when move != null
-    uint32_t* ticket;
-    int32_t* err;
-    int N, n, b, K;
-    int lpr_log2;            // lanes per request = 1 << lpr_log2 (<= 64)
-    int groups;              // request groups of 64 >> lpr_log2 requests
-    int64_t H;
-};
-
-__global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
-    __shared__ VKey wbest[VS_WAVES];
-    __shared__ bool last;
-    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
-    const int lpr = 1 << a.lpr_log2, rpw = kWave >> a.lpr_log2;
-    const int sub = lane >> a.lpr_log2, tl = lane & (lpr - 1);
-    const int n = a.n, K = a.K, K1 = K + 1;
-    const u128 bb = (u128)a.b * (u128)a.b;
-    VKey feas = no_key();   // this lane's view of the wave's best negative key
-
-    for (int grp = blockIdx.x * VS_WAVES + wid; grp < a.groups; grp += gridDim.x * VS_WAVES) {
-        const int r = grp * rpw + sub;
-        const bool live = r < a.N;
-        ReqTerms q{};
-        if (live) q = request_terms(a.inst[r], a.cur[r], a.rem[r], n, a.b, a.H);
-        const bool valid = live && q.bad == 0;
-        if (live && tl == 0) report_error(a.err, q.bad);
-
-        // the request's part of G, independent of the target
-        u128 base = 0, bp = 0, al = 0;
-        const int ke = q.ke;
-        const bool part = valid && ke < K;
-        if (valid) {
-            al = wide(q.alpha);
-            const u128 b0 = a.bs[ke], b1 = a.bs[K1 + ke], b2 = a.bs[2 * K1 + ke];
-            const size_t so = (size_t)q.s * K1 + ke;
-            base = al * al * b0 + (u128)2 * al * bb * b1 + bb * bb * b2 - al * a.qa[so] -
-                   bb * a.qb[so];
-            if (part) {
-                bp = (u128)a.beta[ke] * wide(q.p);
-                base += bp * (wide(q.p) - wide(a.load[(size_t)q.s * K + ke]));
-            }
-        }
-        VKey best = no_key();
-        for (int t = tl; t < n; t += lpr) {
-            if (!live) break;
-            u128 g = 0;
-            if (valid && t != q.s) {
-                const size_t to = (size_t)t * K1 + ke;
-                g = base + al * a.qa[to] + bb * a.qb[to];
-                if (part) g += bp * wide(a.load[(size_t)t * K + ke]);
-                best = vmin(best, VKey{(s128)g, (uint32_t)r * (uint32_t)n + (uint32_t)t});
-            }
-            if (a.gain) a.gain[(size_t)r * n + t] = g;
-        }
-        best = butterfly_min(best, 1, lpr);
-        if (live && tl == 0) {
-            const bool has = best.idx != kNoIdx;
-            if (a.best_target)
-                a.best_target[r] = has ? (int32_t)(best.idx - (uint32_t)r * (uint32_t)n) : -1;
-            if (a.best_gain) a.best_gain[r] = has ? (u128)best.g : (u128)0;
-        }
-        if (best.g < 0) feas = vmin(feas, best);
-    }
-    if (!a.move) return;
-
-    // best negative key of the workgroup, then of the grid
-    feas = butterfly_min(feas, 1, kWave);
-    if (lane == 0) wbest[wid] = feas;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        VKey k = wbest[0];
-        for (int w = 1; w < VS_WAVES; ++w) k = vmin(k, wbest[w]);
-        store_part(&a.part[blockIdx.x], k);
-        __threadfence();
-        const uint32_t done = atomicAdd(a.ticket, 1u);
-        last = done == gridDim.x - 1;
-    }
-    __syncthreads();
-    if (!last) return;
-    __threadfence();
+// One workgroup: the smallest of `parts` partial keys, written as the move
+// (or the no-move record when none is negative).
+template <bool kAtomic>
+__device__ void reduce_parts(VPart* part, int parts, const int32_t* inst, int n, star_move* move,
+                             VKey* wbest) {
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
     VKey k = no_key();
-    for (int g = threadIdx.x; g < (int)gridDim.x; g += VS_THREADS) k = vmin(k, load_part(&a.part[g]));
-    k = butterfly_min(k, 1, kWave);
-    if (lane == 0) wbest[wid] = k;
+    for (int g = tid; g < parts; g += VS_THREADS) {
+        VKey p;
+        if (kAtomic) {
+            p = load_part(&part[g]);
+        } else {
+            const VPart v = part[g];
+            p = VKey{(s128)(((u128)v.w[1] << 64) | (u128)v.w[0]), (uint32_t)v.w[2]};
+        }
+        k = vmin(k, p);
+    }
+    k = group_min(k, 6, lane);
+    if (lane == kWave - 1) wbest[wid] = k;
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
         VKey m = wbest[0];
         for (int w = 1; w < VS_WAVES; ++w) m = vmin(m, wbest[w]);
         star_move mv;
         if (m.idx != kNoIdx) {
             const int r = (int)(m.idx / (uint32_t)n);
             mv.req = r;
-            mv.src = a.inst[r];
+            mv.src = inst[r];
             mv.tgt = (int)(m.idx - (uint32_t)r * (uint32_t)n);
             mv.gain.lo = (uint64_t)(u128)m.g;
             mv.gain.hi = (int64_t)(m.g >> 64);
@@ -299,9 +313,203 @@ __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
             mv.gain.hi = 0;
         }
         mv.reserved = 0;
-        *a.move = mv;
-        *a.ticket = 0u;
+        *move = mv;
     }
+}
+
+// A request's target-independent part of G, staged in LDS.
+struct ReqStash {
+    u128 base, bp;
+    uint64_t al;
+    int32_t ke;
+    int32_t s;        // source instance; -2: invalid request, -1: past the end
+    int32_t pad[2];
+};
+
+struct VarArgs {
+    const int32_t* cur;
+    const int32_t* rem;
+    const int32_t* inst;
+    const uint16_t* beta;
+    const QEntry* qt;        // [K + 1][n]
+    const int64_t* lt;       // [K][n]
+    const u128* bs;          // [3][K + 1]
+    u128* gain;              // [N, n] or null
+    int32_t* best_target;    // [N] or null
+    u128* best_gain;         // [N] or null
+    star_move* move;         // one, or null
+    VPart* part;             // [gridDim.x] when move != null
+    uint32_t* ticket;
+    int32_t* err;
+    int N, n, b, K;
+    int ticketed;            // 1: the last workgroup reduces the partials
+    int64_t H;
+};
+
+constexpr int VS_M = 4;      // targets per lane per chunk
+
+// (g, t) keys of one request: smaller gain, then smaller target
+__device__ inline bool gt_less(s128 ga, int ta, s128 gb, int tb) {
+    return ga < gb || (ga == gb && (uint32_t)ta < (uint32_t)tb);
+}
+
+// One DPP step of the per-request reduction: the key of lane - S (row
+// shift) replaces this lane's if smaller; lanes whose source lies in the
+// previous request's group (or row) keep theirs.
+template <int kCtrl, int S>
+__device__ inline void dpp_step(s128& g, int& t, int tl) {
+    const u128 u = (u128)g;
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int x = (int)(uint32_t)(u >> (32 * i));
+        w[i] = (uint32_t)__builtin_amdgcn_update_dpp(x, x, kCtrl, 0xF, 0xF, false);
+    }
+    const int to = __builtin_amdgcn_update_dpp(t, t, kCtrl, 0xF, 0xF, false);
+    const s128 go =
+        (s128)(((u128)w[3] << 96) | ((u128)w[2] << 64) | ((u128)w[1] << 32) | (u128)w[0]);
+    if (tl >= S && gt_less(go, to, g, t)) {
+        g = go;
+        t = to;
+    }
+}
+
+// A workgroup takes VS_WAVES * 64 / P requests (P = 2^LG <= 16 lanes per
+// request).  Phase A: thread j stages request j's target-independent terms
+// in LDS (coalesced reads, one gather of the weight sums and of its
+// source's entry).  Phase B: each wave takes 64 / P requests at once; lane
+// l of a request's group walks the targets l, l + P, ... in chunks of
+// VS_M, loading a chunk's table entries (contiguous across the group)
+// before storing its gains and keeping its best key in registers; then an
+// LG-step DPP row-shift scan leaves the request's best key in the group's
+// last lane.  One pass per wave: on gfx9 loads and stores share one
+// counter, so a second pass's loads would wait for the first pass's stores.
+template <int LG>
+__global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
+    constexpr int P = 1 << LG, RPW = kWave / P, TILE = VS_WAVES * RPW;
+    __shared__ ReqStash st[TILE];
+    __shared__ VKey wbest[VS_WAVES];
+    __shared__ bool last;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int sub = lane >> LG, tl = lane & (P - 1);
+    const int n = a.n, K = a.K, K1 = K + 1;
+    const uint64_t bb = (uint64_t)a.b * (uint64_t)a.b;
+    const int r0 = blockIdx.x * TILE;
+    const QEntry* __restrict__ qt = a.qt;
+    const int64_t* __restrict__ lt = a.lt;
+    u128* __restrict__ gain = a.gain;
+
+    if (tid < TILE) {
+        const int r = r0 + tid;
+        ReqStash e;
+        e.base = 0;
+        e.bp = 0;
+        e.al = 0;
+        e.ke = 0;
+        e.s = -1;
+        if (r < a.N) {
+            const ReqTerms q = request_terms(a.inst[r], a.cur[r], a.rem[r], n, a.b, a.H);
+            report_error(a.err, q.bad);
+            e.s = q.bad ? -2 : q.s;
+            if (!q.bad) {
+                // alpha, b^2 and p are non-negative and below 2^62
+                const uint64_t al = (uint64_t)q.alpha;
+                const int ke = q.ke;
+                const u128 b0 = a.bs[ke], b1 = a.bs[K1 + ke], b2 = a.bs[2 * K1 + ke];
+                const QEntry qs = qt[(size_t)ke * n + q.s];
+                u128 base = mul_u64(mul_u64(b0, al), al) + mul_u64(mul_u64(b1, al), 2 * bb) +
+                            mul_u64(mul_u64(b2, bb), bb) - mul_u64(qs.qa, al) -
+                            mul_u64(qs.qb, bb);
+                u128 bp = 0;
+                if (ke < K) {
+                    bp = (u128)a.beta[ke] * (u128)(uint64_t)q.p;
+                    base += mul_s64(bp, q.p - lt[(size_t)ke * n + q.s]);
+                }
+                e.base = base;
+                e.bp = bp;
+                e.al = al;
+                e.ke = ke;
+            }
+        }
+        st[tid] = e;
+    }
+    __syncthreads();
+
+    const int j = wid * RPW + sub;
+    const int r = r0 + j;
+    const u128 base = st[j].base, bp = st[j].bp;
+    const uint64_t al = st[j].al;
+    const int ke = st[j].ke, src = st[j].s;
+    const bool live = src != -1, valid = src >= 0;
+    const size_t row = valid ? (size_t)ke * n : 0;   // others read entry 0, unused
+    s128 bg = ~(u128)0 >> 1;
+    int bt = -1;
+    for (int c0 = 0; c0 < n; c0 += P * VS_M) {
+        QEntry qe[VS_M];
+        int64_t le[VS_M];
+#pragma unroll
+        for (int i = 0; i < VS_M; ++i) {
+            const int t = c0 + tl + P * i;
+            const size_t o = row + (t < n ? t : 0);
+            qe[i] = qt[o];
+            le[i] = lt[o];
+        }
+#pragma unroll
+        for (int i = 0; i < VS_M; ++i) {
+            const int t = c0 + tl + P * i;
+            u128 g = base + mul_u64(qe[i].qa, al) + mul_u64(qe[i].qb, bb);
+            if (ke < K) g += mul_s64(bp, le[i]);
+            const bool mig = valid && t < n && t != src;
+            if (!mig) g = 0;
+            if (mig && (s128)g < bg) {   // targets ascend within a lane
+                bg = (s128)g;
+                bt = t;
+            }
+            if (gain && live && t < n) gain[(size_t)r * n + t] = g;
+        }
+    }
+    if (LG >= 1) dpp_step<kDppRowShr1, 1>(bg, bt, tl);
+    if (LG >= 2) dpp_step<kDppRowShr2, 2>(bg, bt, tl);
+    if (LG >= 3) dpp_step<kDppRowShr4, 4>(bg, bt, tl);
+    if (LG >= 4) dpp_step<kDppRowShr8, 8>(bg, bt, tl);
+
+    VKey feas = no_key();   // the request's best key if it lowers the objective
+    if (live && tl == P - 1) {
+        if (a.best_target) a.best_target[r] = bt;
+        if (a.best_gain) a.best_gain[r] = bt >= 0 ? (u128)bg : (u128)0;
+        if (bt >= 0 && bg < 0) feas = VKey{bg, (uint32_t)r * (uint32_t)n + (uint32_t)bt};
+    }
+    if (!a.move) return;
+
+    // best negative key of the workgroup, then (small grids) of the grid
+    feas = group_min(feas, 6, lane);
+    if (lane == kWave - 1) wbest[wid] = feas;
+    __syncthreads();
+    if (tid == 0) {
+        VKey k = wbest[0];
+        for (int w = 1; w < VS_WAVES; ++w) k = vmin(k, wbest[w]);
+        store_part(&a.part[blockIdx.x], k);
+        if (a.ticketed) {
+            // small grids only: this release fence writes back the XCD's L2
+            __threadfence();
+            last = atomicAdd(a.ticket, 1u) == gridDim.x - 1;
+        }
+    }
+    if (!a.ticketed) return;
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    reduce_parts<true>(a.part, gridDim.x, a.inst, n, a.move, wbest);
+    if (tid == 0) *a.ticket = 0u;
+}
+
+// The best feasible move from the scoring workgroups' partials (large grids,
+// after the scoring kernel has finished).
+__global__ __launch_bounds__(VS_THREADS) void var_final_kernel(VPart* part, int parts,
+                                                               const int32_t* inst, int n,
+                                                               star_move* move) {
+    __shared__ VKey wbest[VS_WAVES];
+    reduce_parts<false>(part, parts, inst, n, move, wbest);
 }
 
 // ---------------------------------------------------------------------------
@@ -312,17 +520,16 @@ VarPlan plan_variance(const star_load_params& p) {
     const int n = p.n_inst, N = p.n_req;
     const size_t K1 = (size_t)p.n_buckets + 1;
     int lg = 0;
-    while ((1 << lg) < n && lg < 6) ++lg;
-    pl.lpr_log2 = lg;
-    const int rpw = kWave >> lg;
-    pl.groups = (int)ceil_div(N, rpw);
-    const int64_t blocks = ceil_div(pl.groups, VS_WAVES);
-    pl.blocks = (int)(blocks < 1 ? 1 : blocks > VS_MAX_BLOCKS ? VS_MAX_BLOCKS : blocks);
+    while ((1 << lg) < n && lg < VS_MAX_LG) ++lg;
+    pl.lg = lg;
+    const int64_t blocks = ceil_div(N, (int64_t)VS_WAVES * (kWave >> lg));
+    pl.blocks = (int)(blocks < 1 ? 1 : blocks);
+    pl.ticketed = pl.blocks <= VS_TICKET_BLOCKS;
     size_t off = STAR_WS_HEADER_BYTES;
-    pl.qa_off = off;
-    off += align_up((size_t)n * K1 * sizeof(u128), 256);
-    pl.qb_off = off;
-    off += align_up((size_t)n * K1 * sizeof(u128), 256);
+    pl.qt_off = off;
+    off += align_up((size_t)n * K1 * sizeof(QEntry), 256);
+    pl.lt_off = off;
+    off += align_up((size_t)n * K1 * sizeof(int64_t), 256);
     pl.bs_off = off;
     off += align_up(3 * K1 * sizeof(u128), 256);
     pl.part_off = off;
@@ -338,20 +545,19 @@ hipError_t launch_variance(const star_load_params& p, const VarPlan& pl, const i
                            hipStream_t stream) {
     static_assert(sizeof(star_i128) == sizeof(u128), "star_i128 is one 128-bit integer");
     const int n = p.n_inst, K = p.n_buckets;
-    u128* qa = (u128*)(ws + pl.qa_off);
-    u128* qb = (u128*)(ws + pl.qb_off);
+    QEntry* qt = (QEntry*)(ws + pl.qt_off);
+    int64_t* lt = (int64_t*)(ws + pl.lt_off);
     u128* bs = (u128*)(ws + pl.bs_off);
     uint32_t* ticket = (uint32_t*)(ws + kHdrVarTicket);
     hipLaunchKernelGGL(var_prep_kernel, dim3(n + 1), dim3(VP_THREADS), 0, stream, load, beta, n,
-                       K, qa, qb, bs, ticket);
+                       K, qt, lt, bs, ticket);
     VarArgs a;
     a.cur = cur;
     a.rem = rem;
     a.inst = inst;
-    a.load = load;
     a.beta = beta;
-    a.qa = qa;
-    a.qb = qb;
+    a.qt = qt;
+    a.lt = lt;
     a.bs = bs;
     a.gain = (u128*)gain;
     a.best_target = best_target;
@@ -364,10 +570,28 @@ hipError_t launch_variance(const star_load_params& p, const VarPlan& pl, const i
     a.n = n;
     a.b = p.bucket;
     a.K = K;
-    a.lpr_log2 = pl.lpr_log2;
-    a.groups = pl.groups;
+    a.ticketed = pl.ticketed;
     a.H = (int64_t)p.bucket * K;
-    hipLaunchKernelGGL(var_score_kernel, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
+    switch (pl.lg) {
+        case 0:
+            hipLaunchKernelGGL(var_score_kernel<0>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
+            break;
+        case 1:
+            hipLaunchKernelGGL(var_score_kernel<1>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
+            break;
+        case 2:
+            hipLaunchKernelGGL(var_score_kernel<2>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
+            break;
+        case 3:
+            hipLaunchKernelGGL(var_score_kernel<3>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
+            break;
+        default:
+            hipLaunchKernelGGL(var_score_kernel<4>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
+            break;
+    }
+    if (move && !pl.ticketed)
+        hipLaunchKernelGGL(var_final_kernel, dim3(1), dim3(VS_THREADS), 0, stream, a.part,
+                           pl.blocks, inst, n, move);
     return hipGetLastError();
 }
 
