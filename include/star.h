@@ -206,6 +206,57 @@ star_status star_score_variance(const star_load_params* p, const int32_t* cur_le
                                 star_move* best_move, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * (f2) Algorithm 1 end to end, repeated: a migration plan.
+ *
+ * One pass is one scheduler interval of Algorithm 1 with the variance gain
+ * of (f1) as the figure of merit and no decode progress in between:
+ *   classification: w_i = sum_k beta_k load[i, k]; mean w = (1/n) sum_i w_i;
+ *     O = {i : w_i > (1 + theta) mean w};
+ *     U = {i : N_i < (1 + theta) mean w}    (u_rule 0, as printed), or
+ *         {i : w_i < (1 - theta) mean w}    (u_rule 1),
+ *     N_i = sum of cur_len over the valid requests on i (current load);
+ *   enumeration: (r, s, t) with s = inst_of[r] in O, t in U, t != s,
+ *     rem_len[r] > min_rem (the remaining-length-versus-migration-cost
+ *     filter), and N_t + rem_len[r] <= mem_cap (mem_rule 0, as printed) or
+ *     N_t + cur_len[r] + rem_len[r] <= mem_cap (mem_rule 1);
+ *   selection: the smallest key (gain, r, t) with gain < 0;
+ *   execution: inst_of[r] = t and r's curve moves from load[s] to load[t].
+ * Passes repeat until max_moves migrations are made, O is empty, or no
+ * candidate lowers the objective.  theta = theta_num / theta_den; all
+ * comparisons are exact (cross-multiplied, 128-bit).
+ *   inst_of: int32 [n_req] device, IN/OUT (the placement after the plan).
+ *   load: int64 [n_inst, n_buckets] device, IN/OUT: on entry the curves of
+ *         exactly these requests (star_project_load), on exit the curves
+ *         after the plan.
+ *   beta: uint16 [n_buckets] device (as in star_score_variance).
+ *   moves: star_move [max_moves] device; moves[q] = q-th migration
+ *         (req, src, tgt, gain) in execution order.  n_moves: int32 [1]
+ *         device, the number made.
+ * Cost: one classification-and-scoring pass over all N x n candidates and
+ * one small update per allowed move (2 launches each; once the plan stops,
+ * the remaining launches exit at once).
+ * ---------------------------------------------------------------------- */
+#define STAR_MAX_MOVES 4096
+
+typedef struct {
+    star_load_params load;
+    int32_t max_moves;          /* 0 .. STAR_MAX_MOVES */
+    int32_t theta_num;          /* 0 .. 2^20 */
+    int32_t theta_den;          /* 1 .. 2^20 */
+    int32_t u_rule;             /* 0 or 1, see above */
+    int32_t mem_rule;           /* 0 or 1, see above */
+    int32_t min_rem;            /* candidates need rem_len > min_rem */
+    int64_t mem_cap;            /* >= 0, tokens */
+} star_plan_params;
+
+size_t star_plan_workspace_size(const star_plan_params* p);
+
+star_status star_plan_migrations(const star_plan_params* p, const int32_t* cur_len,
+                                 const int32_t* rem_len, int32_t* inst_of, int64_t* load,
+                                 const uint16_t* beta, star_move* moves, int32_t* n_moves,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Housekeeping.
  * ---------------------------------------------------------------------- */
 /* Zero the whole workspace on `stream` (a fill kernel, no memset node).

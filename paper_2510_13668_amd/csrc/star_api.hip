@@ -221,6 +221,55 @@ STAR_API star_status star_score_variance(const star_load_params* p, const int32_
 }
 
 // ---------------------------------------------------------------------------
+// migration plans
+// ---------------------------------------------------------------------------
+static star_status check_plan_params(const star_plan_params* p) {
+    if (!p) return STAR_ERR_INVALID_ARG;
+    star_status st = check_variance_params(&p->load);
+    if (st != STAR_OK) return st;
+    if (p->max_moves < 0 || p->max_moves > STAR_MAX_MOVES) return STAR_ERR_INVALID_ARG;
+    if (p->theta_num < 0 || p->theta_num > (1 << 20) || p->theta_den < 1 ||
+        p->theta_den > (1 << 20))
+        return STAR_ERR_INVALID_ARG;
+    if ((p->u_rule != 0 && p->u_rule != 1) || (p->mem_rule != 0 && p->mem_rule != 1))
+        return STAR_ERR_INVALID_ARG;
+    if (p->mem_cap < 0) return STAR_ERR_INVALID_ARG;
+    if (p->load.n_inst > 1024) return STAR_ERR_UNSUPPORTED;
+    // n (theta_den + theta_num) w_i with w_i <= 65535 * sum of every load
+    const long double H = (long double)p->load.bucket * p->load.n_buckets;
+    const long double w = 65535.0L * ((long double)p->load.n_req + 1.0L) * H *
+                          (2147483648.0L + H);
+    const long double bound = (long double)p->load.n_inst * (2.0L * 1048576.0L) * w;
+    if (!(bound < ldexpl(1.0L, 126))) return STAR_ERR_OVERFLOW;
+    return STAR_OK;
+}
+
+STAR_API size_t star_plan_workspace_size(const star_plan_params* p) {
+    if (check_plan_params(p) != STAR_OK) return 0;
+    return plan_plan(*p).total;
+}
+
+STAR_API star_status star_plan_migrations(const star_plan_params* p, const int32_t* cur_len,
+                                          const int32_t* rem_len, int32_t* inst_of,
+                                          int64_t* load, const uint16_t* beta, star_move* moves,
+                                          int32_t* n_moves, void* ws, size_t ws_bytes,
+                                          void* stream) {
+    star_status st = check_plan_params(p);
+    if (st != STAR_OK) return st;
+    if (!load || !beta || !n_moves) return STAR_ERR_INVALID_ARG;
+    if (p->max_moves > 0 && !moves) return STAR_ERR_INVALID_ARG;
+    if (p->load.n_req > 0 && (!cur_len || !rem_len || !inst_of)) return STAR_ERR_INVALID_ARG;
+    if (!aligned(moves, 16)) return STAR_ERR_UNSUPPORTED;
+    const PlanPlan pl = plan_plan(*p);
+    st = check_ws(ws, ws_bytes, pl.total);
+    if (st != STAR_OK) return st;
+    int32_t* err = (int32_t*)((char*)ws + kHdrErrorWord);
+    hipError_t e = launch_plan(*p, pl, cur_len, rem_len, inst_of, load, beta, moves, n_moves,
+                               (char*)ws, err, (hipStream_t)stream);
+    return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
 // housekeeping
 // ---------------------------------------------------------------------------
 STAR_API star_status star_workspace_init(void* ws, size_t ws_bytes, void* stream) {

@@ -63,6 +63,16 @@ hipError_t launch_variance(const star_load_params& p, const VarPlan& pl, const i
                            star_i128* best_gain, star_move* move, char* ws, int32_t* err,
                            hipStream_t stream);
 
+struct PlanPlan {
+    VarPlan v;
+    size_t now_off = 0, total = 0;
+};
+PlanPlan plan_plan(const star_plan_params& p);
+hipError_t launch_plan(const star_plan_params& p, const PlanPlan& pl, const int32_t* cur,
+                       const int32_t* rem, int32_t* inst, int64_t* load, const uint16_t* beta,
+                       star_move* moves, int32_t* n_moves, char* ws, int32_t* err,
+                       hipStream_t stream);
+
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 
 }  // namespace star

@@ -58,6 +58,10 @@ constexpr size_t kHdrVarTicket = 64;   // workspace header: finished-workgroup t
 // fence would write back its XCD's L2, full of freshly written gains.
 constexpr int VS_TICKET_BLOCKS = 64;
 constexpr int VS_MAX_LG = 4;             // at most 16 lanes per request
+constexpr int PLAN_MAX_INST = 1024;      // instances a plan classifies in LDS
+
+constexpr size_t kHdrPlanDone = 72;      // workspace header: the plan has stopped
+constexpr size_t kHdrPlanCount = 76;     // workspace header: moves made
 
 __device__ inline u128 wide(int64_t v) { return (u128)(s128)v; }
 
@@ -101,22 +105,18 @@ __device__ inline void prep_load(const uint16_t* beta, const int64_t* L, bool wr
     }
 }
 
-__global__ __launch_bounds__(VP_THREADS) void var_prep_kernel(const int64_t* __restrict__ load,
-                                                              const uint16_t* __restrict__ beta,
-                                                              int n, int K,
-                                                              QEntry* __restrict__ qt,
-                                                              int64_t* __restrict__ lt,
-                                                              u128* __restrict__ bs,
-                                                              uint32_t* __restrict__ ticket) {
-    __shared__ u128 sx[3][VP_THREADS];
-    const int row = blockIdx.x, tid = threadIdx.x;
+// The tables of one row, computed by the whole workgroup (sx: LDS of
+// 3 x VP_THREADS entries).  L is the instance's curve (row < n) or unused
+// (the weights' row, wrow).  A thread reads back only buckets it owns, so
+// a caller may have just written them itself.
+__device__ void prep_row(const int64_t* __restrict__ L, const uint16_t* __restrict__ beta, int n,
+                         int K, int row, bool wrow, QEntry* __restrict__ qt,
+                         int64_t* __restrict__ lt, u128* __restrict__ bs, u128 (*sx)[VP_THREADS]) {
+    const int tid = threadIdx.x;
     const int K1 = K + 1;
-    const bool wrow = row == n;
     const int per = (K + VP_THREADS - 1) / VP_THREADS;
     const int j0 = min(tid * per, K), j1 = min(j0 + per, K);
-    const int64_t* L = load + (size_t)(wrow ? 0 : row) * K;
-
-    if (row == 0 && tid == 0) *ticket = 0u;   // the scoring kernel runs after this one
+    __syncthreads();   // sx may still be read by a previous row
 
     uint32_t wv[VP_REG];
     int64_t lv[VP_REG];
@@ -188,6 +188,19 @@ __global__ __launch_bounds__(VP_THREADS) void var_prep_kernel(const int64_t* __r
             qt[(size_t)K * n + row] = QEntry{sx[0][tid], sx[1][tid]};
         }
     }
+}
+
+__global__ __launch_bounds__(VP_THREADS) void var_prep_kernel(const int64_t* __restrict__ load,
+                                                              const uint16_t* __restrict__ beta,
+                                                              int n, int K,
+                                                              QEntry* __restrict__ qt,
+                                                              int64_t* __restrict__ lt,
+                                                              u128* __restrict__ bs,
+                                                              uint32_t* __restrict__ ticket) {
+    __shared__ u128 sx[3][VP_THREADS];
+    const int row = blockIdx.x;
+    if (row == 0 && threadIdx.x == 0) *ticket = 0u;   // the scoring kernel runs after this one
+    prep_row(load + (size_t)(row == n ? 0 : row) * K, beta, n, K, row, row == n, qt, lt, bs, sx);
 }
 
 // ---------------------------------------------------------------------------
@@ -278,9 +291,10 @@ __device__ inline VKey load_part(VPart* p) {
 
 // One workgroup: the smallest of `parts` partial keys, written as the move
 // (or the no-move record when none is negative).
+// One workgroup: the smallest of `parts` partial keys, returned to every
+// thread.
 template <bool kAtomic>
-__device__ void reduce_parts(VPart* part, int parts, const int32_t* inst, int n, star_move* move,
-                             VKey* wbest) {
+__device__ VKey reduce_keys(VPart* part, int parts, VKey* wbest) {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
     VKey k = no_key();
     for (int g = tid; g < parts; g += VS_THREADS) {
@@ -296,25 +310,36 @@ __device__ void reduce_parts(VPart* part, int parts, const int32_t* inst, int n,
     k = group_min(k, 6, lane);
     if (lane == kWave - 1) wbest[wid] = k;
     __syncthreads();
-    if (tid == 0) {
-        VKey m = wbest[0];
-        for (int w = 1; w < VS_WAVES; ++w) m = vmin(m, wbest[w]);
-        star_move mv;
-        if (m.idx != kNoIdx) {
-            const int r = (int)(m.idx / (uint32_t)n);
-            mv.req = r;
-            mv.src = inst[r];
-            mv.tgt = (int)(m.idx - (uint32_t)r * (uint32_t)n);
-            mv.gain.lo = (uint64_t)(u128)m.g;
-            mv.gain.hi = (int64_t)(m.g >> 64);
-        } else {
-            mv.req = mv.src = mv.tgt = -1;
-            mv.gain.lo = 0;
-            mv.gain.hi = 0;
-        }
-        mv.reserved = 0;
-        *move = mv;
+    VKey m = wbest[0];
+    for (int w = 1; w < VS_WAVES; ++w) m = vmin(m, wbest[w]);
+    __syncthreads();
+    return m;
+}
+
+// The move record of key m (or the no-move record).
+__device__ inline star_move move_of(const VKey& m, const int32_t* inst, int n) {
+    star_move mv;
+    if (m.idx != kNoIdx) {
+        const int r = (int)(m.idx / (uint32_t)n);
+        mv.req = r;
+        mv.src = inst[r];
+        mv.tgt = (int)(m.idx - (uint32_t)r * (uint32_t)n);
+        mv.gain.lo = (uint64_t)(u128)m.g;
+        mv.gain.hi = (int64_t)(m.g >> 64);
+    } else {
+        mv.req = mv.src = mv.tgt = -1;
+        mv.gain.lo = 0;
+        mv.gain.hi = 0;
     }
+    mv.reserved = 0;
+    return mv;
+}
+
+template <bool kAtomic>
+__device__ void reduce_parts(VPart* part, int parts, const int32_t* inst, int n, star_move* move,
+                             VKey* wbest) {
+    const VKey m = reduce_keys<kAtomic>(part, parts, wbest);
+    if (threadIdx.x == 0) *move = move_of(m, inst, n);
 }
 
 // A request's target-independent part of G, staged in LDS.
@@ -322,8 +347,9 @@ struct ReqStash {
     u128 base, bp;
     uint64_t al;
     int32_t ke;
-    int32_t s;        // source instance; -2: invalid request, -1: past the end
-    int32_t pad[2];
+    int32_t s;        // source instance; -2: no candidates (invalid request, or a
+                      // source Algorithm 1 does not move from); -1: past the end
+    int64_t need;     // memory the request takes on a target (plans)
 };
 
 struct VarArgs {
@@ -344,6 +370,11 @@ struct VarArgs {
     int N, n, b, K;
     int ticketed;            // 1: the last workgroup reduces the partials
     int64_t H;
+    // plans (Algorithm 1's classification and candidate filters)
+    const int64_t* now;      // [n] current loads N_i
+    const int32_t* done;     // nonzero: the plan has stopped
+    int theta_num, theta_den, u_rule, mem_rule, min_rem;
+    int64_t mem_cap;
 };
 
 constexpr int VS_M = 4;      // targets per lane per chunk
@@ -384,12 +415,23 @@ __device__ inline void dpp_step(s128& g, int& t, int tl) {
 // LG-step DPP row-shift scan leaves the request's best key in the group's
 // last lane.  One pass per wave: on gfx9 loads and stores share one
 // counter, so a second pass's loads would wait for the first pass's stores.
-template <int LG>
+//
+// Plans (kPlan): Algorithm 1's classification runs first in every
+// workgroup.  w_i = QA_i[K] comes straight from the tables; O = {w_i > (1 +
+// theta) mean w}; U by the chosen rule; for each target the memory room
+// C_mem - N_t (or -1 outside U).  Only requests on an instance of O with
+// rem_len > min_rem are staged as sources, a candidate must fit the room,
+// and only the workgroup's best negative key is written.
+template <int LG, bool kPlan>
 __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
     constexpr int P = 1 << LG, RPW = kWave / P, TILE = VS_WAVES * RPW;
+    constexpr int NM = kPlan ? PLAN_MAX_INST : 1;
     __shared__ ReqStash st[TILE];
     __shared__ VKey wbest[VS_WAVES];
     __shared__ bool last;
+    __shared__ uint8_t over_m[NM];
+    __shared__ int64_t room_m[NM];
+    __shared__ u128 wred[kPlan ? VS_THREADS : 1];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
     const int sub = lane >> LG, tl = lane & (P - 1);
     const int n = a.n, K = a.K, K1 = K + 1;
@@ -399,6 +441,30 @@ __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
     const int64_t* __restrict__ lt = a.lt;
     u128* __restrict__ gain = a.gain;
 
+    if (kPlan) {
+        if (*a.done) return;
+        // classification: sum of w, then O and the targets' room
+        u128 acc = 0;
+        for (int i = tid; i < n; i += VS_THREADS) acc += qt[(size_t)K * n + i].qa;
+        wred[tid] = acc;
+        __syncthreads();
+        for (int o = VS_THREADS / 2; o > 0; o >>= 1) {
+            if (tid < o) wred[tid] += wred[tid + o];
+            __syncthreads();
+        }
+        const s128 wsum = (s128)wred[0];
+        const s128 den = a.theta_den, num = a.theta_num;
+        const s128 hi = (den + num) * wsum, lo = (den - num) * wsum;   // n den (1 +- theta) mean w
+        for (int i = tid; i < n; i += VS_THREADS) {
+            const s128 nw = (s128)n * den * (s128)qt[(size_t)K * n + i].qa;
+            const int64_t now = a.now[i];
+            over_m[i] = nw > hi;
+            const bool under = a.u_rule == 0 ? (s128)n * den * (s128)now < hi : nw < lo;
+            room_m[i] = under ? a.mem_cap - now : -1;
+        }
+        __syncthreads();
+    }
+
     if (tid < TILE) {
         const int r = r0 + tid;
         ReqStash e;
@@ -407,11 +473,17 @@ __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
         e.al = 0;
         e.ke = 0;
         e.s = -1;
+        e.need = 0;
         if (r < a.N) {
             const ReqTerms q = request_terms(a.inst[r], a.cur[r], a.rem[r], n, a.b, a.H);
-            report_error(a.err, q.bad);
-            e.s = q.bad ? -2 : q.s;
-            if (!q.bad) {
+            if (!kPlan) report_error(a.err, q.bad);
+            bool src_ok = !q.bad;
+            if (kPlan && src_ok) {
+                src_ok = over_m[q.s] && a.rem[r] > a.min_rem;
+                e.need = a.rem[r] + (a.mem_rule ? a.cur[r] : 0);
+            }
+            e.s = src_ok ? q.s : -2;
+            if (src_ok) {
                 // alpha, b^2 and p are non-negative and below 2^62
                 const uint64_t al = (uint64_t)q.alpha;
                 const int ke = q.ke;
@@ -440,6 +512,7 @@ __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
     const u128 base = st[j].base, bp = st[j].bp;
     const uint64_t al = st[j].al;
     const int ke = st[j].ke, src = st[j].s;
+    const int64_t need = st[j].need;
     const bool live = src != -1, valid = src >= 0;
     const size_t row = valid ? (size_t)ke * n : 0;   // others read entry 0, unused
     s128 bg = ~(u128)0 >> 1;
@@ -459,13 +532,14 @@ __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
             const int t = c0 + tl + P * i;
             u128 g = base + mul_u64(qe[i].qa, al) + mul_u64(qe[i].qb, bb);
             if (ke < K) g += mul_s64(bp, le[i]);
-            const bool mig = valid && t < n && t != src;
+            bool mig = valid && t < n && t != src;
+            if (kPlan) mig = mig && need <= room_m[t < n ? t : 0];
             if (!mig) g = 0;
             if (mig && (s128)g < bg) {   // targets ascend within a lane
                 bg = (s128)g;
                 bt = t;
             }
-            if (gain && live && t < n) gain[(size_t)r * n + t] = g;
+            if (!kPlan && gain && live && t < n) gain[(size_t)r * n + t] = g;
         }
     }
     if (LG >= 1) dpp_step<kDppRowShr1, 1>(bg, bt, tl);
@@ -475,11 +549,11 @@ __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
 
     VKey feas = no_key();   // the request's best key if it lowers the objective
     if (live && tl == P - 1) {
-        if (a.best_target) a.best_target[r] = bt;
-        if (a.best_gain) a.best_gain[r] = bt >= 0 ? (u128)bg : (u128)0;
+        if (!kPlan && a.best_target) a.best_target[r] = bt;
+        if (!kPlan && a.best_gain) a.best_gain[r] = bt >= 0 ? (u128)bg : (u128)0;
         if (bt >= 0 && bg < 0) feas = VKey{bg, (uint32_t)r * (uint32_t)n + (uint32_t)bt};
     }
-    if (!a.move) return;
+    if (!kPlan && !a.move) return;
 
     // best negative key of the workgroup, then (small grids) of the grid
     feas = group_min(feas, 6, lane);
@@ -489,13 +563,13 @@ __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
         VKey k = wbest[0];
         for (int w = 1; w < VS_WAVES; ++w) k = vmin(k, wbest[w]);
         store_part(&a.part[blockIdx.x], k);
-        if (a.ticketed) {
+        if (!kPlan && a.ticketed) {
             // small grids only: this release fence writes back the XCD's L2
             __threadfence();
             last = atomicAdd(a.ticket, 1u) == gridDim.x - 1;
         }
     }
-    if (!a.ticketed) return;
+    if (kPlan || !a.ticketed) return;
     __syncthreads();
     if (!last) return;
     __threadfence();
@@ -513,8 +587,148 @@ __global__ __launch_bounds__(VS_THREADS) void var_final_kernel(VPart* part, int 
 }
 
 // ---------------------------------------------------------------------------
+// (f2) Algorithm 1 end to end: one migration per pass, repeated
+// ---------------------------------------------------------------------------
+struct PlanArgs {
+    const int32_t* cur;
+    const int32_t* rem;
+    int32_t* inst;           // updated in place
+    int64_t* load;           // [n, K], updated in place
+    const uint16_t* beta;
+    QEntry* qt;
+    int64_t* lt;
+    u128* bs;
+    VPart* part;
+    int parts;
+    int64_t* now;            // [n] current loads N_i
+    int32_t* done;
+    int32_t* count;
+    int32_t* n_moves;        // caller's move count
+    star_move* moves;        // caller's [max_moves]
+    int32_t* err;
+    int N, n, b, K;
+    int64_t H;
+};
+
+// Tables of every row (as var_prep_kernel), the current load N_i of every
+// instance (each row's workgroup sums its valid requests' cur_len), and the
+// plan's state reset; the weights' workgroup reports invalid requests.
+__global__ __launch_bounds__(VP_THREADS) void plan_prep_kernel(PlanArgs a) {
+    __shared__ u128 sx[3][VP_THREADS];
+    __shared__ int64_t red[VP_THREADS];
+    const int row = blockIdx.x, tid = threadIdx.x, n = a.n;
+    if (row < n) {
+        int64_t acc = 0;
+        for (int r = tid; r < a.N; r += VP_THREADS) {
+            const int c = a.cur[r];
+            if (a.inst[r] == row && c >= 1 && a.rem[r] >= 1) acc += c;
+        }
+        red[tid] = acc;
+        __syncthreads();
+        for (int o = VP_THREADS / 2; o > 0; o >>= 1) {
+            if (tid < o) red[tid] += red[tid + o];
+            __syncthreads();
+        }
+        if (tid == 0) a.now[row] = red[0];
+    } else {
+        int32_t bad = 0;
+        for (int r = tid; r < a.N; r += VP_THREADS) {
+            const int s = a.inst[r];
+            if (s < 0 || s >= n) bad |= STAR_DEV_BAD_INST;
+            if (a.cur[r] < 1) bad |= STAR_DEV_BAD_CUR;
+            if (a.rem[r] < 1) bad |= STAR_DEV_BAD_REM;
+        }
+        report_error(a.err, bad);
+        if (tid == 0) {
+            *a.done = 0;
+            *a.count = 0;
+            *a.n_moves = 0;
+        }
+    }
+    prep_row(a.load + (size_t)(row == n ? 0 : row) * a.K, a.beta, n, a.K, row, row == n, a.qt,
+             a.lt, a.bs, sx);
+}
+
+// One workgroup after each scoring pass: the best feasible key of the
+// pass; none stops the plan.  Otherwise the move is recorded and executed:
+// inst_of[r] = t, N_s and N_t adjusted, r's own curve taken from row s and
+// added to row t of the curves, and those two rows' tables recomputed.
+__global__ __launch_bounds__(VP_THREADS) void plan_apply_kernel(PlanArgs a) {
+    __shared__ u128 sx[3][VP_THREADS];
+    __shared__ VKey wbest[VS_WAVES];
+    if (*a.done) return;
+    const int tid = threadIdx.x, n = a.n, K = a.K;
+    const VKey m = reduce_keys<false>(a.part, a.parts, wbest);
+    if (m.idx == kNoIdx) {
+        if (tid == 0) *a.done = 1;
+        return;
+    }
+    const int r = (int)(m.idx / (uint32_t)n);
+    const int t = (int)(m.idx - (uint32_t)r * (uint32_t)n);
+    const int s = a.inst[r];
+    const int c = a.cur[r];
+    __syncthreads();   // every thread has read inst[r] before it changes
+    if (tid == 0) {
+        const int q = *a.count;
+        star_move mv;
+        mv.req = r;
+        mv.src = s;
+        mv.tgt = t;
+        mv.reserved = 0;
+        mv.gain.lo = (uint64_t)(u128)m.g;
+        mv.gain.hi = (int64_t)(m.g >> 64);
+        a.moves[q] = mv;
+        *a.count = q + 1;
+        *a.n_moves = q + 1;
+        a.inst[r] = t;
+        a.now[s] -= c;
+        a.now[t] += c;
+    }
+    // the same bucket ranges as prep_row: each thread rereads only its own writes
+    const ReqTerms rq = request_terms(t, c, a.rem[r], n, a.b, a.H);
+    const int64_t bb = (int64_t)a.b * a.b;
+    const int per = (K + VP_THREADS - 1) / VP_THREADS;
+    const int j0 = min(tid * per, K), j1 = min(j0 + per, K);
+    int64_t* Ls = a.load + (size_t)s * K;
+    int64_t* Lt = a.load + (size_t)t * K;
+    for (int j = j0; j < j1 && j <= rq.ke; ++j) {
+        const int64_t R = j < rq.ke ? rq.alpha + bb * j : rq.p;
+        Ls[j] -= R;
+        Lt[j] += R;
+    }
+    prep_row(Ls, a.beta, n, K, s, false, a.qt, a.lt, a.bs, sx);
+    prep_row(Lt, a.beta, n, K, t, false, a.qt, a.lt, a.bs, sx);
+}
+
+// ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
+template <bool kPlan>
+static void launch_score_lg(int lg, int blocks, const VarArgs& a, hipStream_t stream) {
+    switch (lg) {
+        case 0:
+            hipLaunchKernelGGL((var_score_kernel<0, kPlan>), dim3(blocks), dim3(VS_THREADS), 0,
+                               stream, a);
+            break;
+        case 1:
+            hipLaunchKernelGGL((var_score_kernel<1, kPlan>), dim3(blocks), dim3(VS_THREADS), 0,
+                               stream, a);
+            break;
+        case 2:
+            hipLaunchKernelGGL((var_score_kernel<2, kPlan>), dim3(blocks), dim3(VS_THREADS), 0,
+                               stream, a);
+            break;
+        case 3:
+            hipLaunchKernelGGL((var_score_kernel<3, kPlan>), dim3(blocks), dim3(VS_THREADS), 0,
+                               stream, a);
+            break;
+        default:
+            hipLaunchKernelGGL((var_score_kernel<4, kPlan>), dim3(blocks), dim3(VS_THREADS), 0,
+                               stream, a);
+            break;
+    }
+}
+
 VarPlan plan_variance(const star_load_params& p) {
     VarPlan pl;
     const int n = p.n_inst, N = p.n_req;
@@ -572,26 +786,85 @@ hipError_t launch_variance(const star_load_params& p, const VarPlan& pl, const i
     a.K = K;
     a.ticketed = pl.ticketed;
     a.H = (int64_t)p.bucket * K;
-    switch (pl.lg) {
-        case 0:
-            hipLaunchKernelGGL(var_score_kernel<0>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
-            break;
-        case 1:
-            hipLaunchKernelGGL(var_score_kernel<1>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
-            break;
-        case 2:
-            hipLaunchKernelGGL(var_score_kernel<2>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
-            break;
-        case 3:
-            hipLaunchKernelGGL(var_score_kernel<3>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
-            break;
-        default:
-            hipLaunchKernelGGL(var_score_kernel<4>, dim3(pl.blocks), dim3(VS_THREADS), 0, stream, a);
-            break;
-    }
+    launch_score_lg<false>(pl.lg, pl.blocks, a, stream);
     if (move && !pl.ticketed)
         hipLaunchKernelGGL(var_final_kernel, dim3(1), dim3(VS_THREADS), 0, stream, a.part,
                            pl.blocks, inst, n, move);
+    return hipGetLastError();
+}
+
+PlanPlan plan_plan(const star_plan_params& p) {
+    PlanPlan pl;
+    pl.v = plan_variance(p.load);
+    size_t off = pl.v.total;
+    pl.now_off = off;
+    off += align_up((size_t)p.load.n_inst * sizeof(int64_t), 256);
+    pl.total = off;
+    return pl;
+}
+
+hipError_t launch_plan(const star_plan_params& p, const PlanPlan& pl, const int32_t* cur,
+                       const int32_t* rem, int32_t* inst, int64_t* load, const uint16_t* beta,
+                       star_move* moves, int32_t* n_moves, char* ws, int32_t* err,
+                       hipStream_t stream) {
+    const int n = p.load.n_inst, K = p.load.n_buckets;
+    PlanArgs a;
+    a.cur = cur;
+    a.rem = rem;
+    a.inst = inst;
+    a.load = load;
+    a.beta = beta;
+    a.qt = (QEntry*)(ws + pl.v.qt_off);
+    a.lt = (int64_t*)(ws + pl.v.lt_off);
+    a.bs = (u128*)(ws + pl.v.bs_off);
+    a.part = (VPart*)(ws + pl.v.part_off);
+    a.parts = pl.v.blocks;
+    a.now = (int64_t*)(ws + pl.now_off);
+    a.done = (int32_t*)(ws + kHdrPlanDone);
+    a.count = (int32_t*)(ws + kHdrPlanCount);
+    a.n_moves = n_moves;
+    a.moves = moves;
+    a.err = err;
+    a.N = p.load.n_req;
+    a.n = n;
+    a.b = p.load.bucket;
+    a.K = K;
+    a.H = (int64_t)p.load.bucket * K;
+    hipLaunchKernelGGL(plan_prep_kernel, dim3(n + 1), dim3(VP_THREADS), 0, stream, a);
+
+    VarArgs v;
+    v.cur = cur;
+    v.rem = rem;
+    v.inst = inst;
+    v.beta = beta;
+    v.qt = a.qt;
+    v.lt = a.lt;
+    v.bs = a.bs;
+    v.gain = nullptr;
+    v.best_target = nullptr;
+    v.best_gain = nullptr;
+    v.move = nullptr;
+    v.part = a.part;
+    v.ticket = nullptr;
+    v.err = err;
+    v.N = a.N;
+    v.n = n;
+    v.b = a.b;
+    v.K = K;
+    v.ticketed = 0;
+    v.H = a.H;
+    v.now = a.now;
+    v.done = a.done;
+    v.theta_num = p.theta_num;
+    v.theta_den = p.theta_den;
+    v.u_rule = p.u_rule;
+    v.mem_rule = p.mem_rule;
+    v.min_rem = p.min_rem;
+    v.mem_cap = p.mem_cap;
+    for (int m = 0; m < p.max_moves; ++m) {
+        launch_score_lg<true>(pl.v.lg, pl.v.blocks, v, stream);
+        hipLaunchKernelGGL(plan_apply_kernel, dim3(1), dim3(VP_THREADS), 0, stream, a);
+    }
     return hipGetLastError();
 }
 

@@ -41,6 +41,12 @@ class ScoreParams(ctypes.Structure):
     _fields_ = [("load", LoadParams), ("top_k", _i32)]
 
 
+class PlanParams(ctypes.Structure):
+    _fields_ = [("load", LoadParams), ("max_moves", _i32), ("theta_num", _i32),
+                ("theta_den", _i32), ("u_rule", _i32), ("mem_rule", _i32), ("min_rem", _i32),
+                ("mem_cap", ctypes.c_int64)]
+
+
 class StarError(RuntimeError):
     def __init__(self, fn: str, status: int, msg: str):
         super().__init__(f"{fn}: {msg} ({status})")
@@ -83,6 +89,11 @@ def lib():
         L.star_score_variance.restype = ctypes.c_int
         L.star_score_variance.argtypes = ([ctypes.POINTER(LoadParams)] + [_P] * 10 +
                                           [ctypes.c_size_t, _P])
+        L.star_plan_workspace_size.restype = ctypes.c_size_t
+        L.star_plan_workspace_size.argtypes = [ctypes.POINTER(PlanParams)]
+        L.star_plan_migrations.restype = ctypes.c_int
+        L.star_plan_migrations.argtypes = ([ctypes.POINTER(PlanParams)] + [_P] * 8 +
+                                           [ctypes.c_size_t, _P])
         L.star_workspace_init.restype = ctypes.c_int
         L.star_workspace_init.argtypes = [_P, ctypes.c_size_t, _P]
         L.star_read_device_error.restype = ctypes.c_int
@@ -225,3 +236,26 @@ def score_variance(p: LoadParams, cur_len, rem_len, inst_of, load, beta, gain, b
 def i128_to_int(lo: int, hi: int) -> int:
     """One (low, high) int64 pair of a 128-bit two's complement value."""
     return (int(hi) << 64) + (int(lo) & ((1 << 64) - 1))
+
+
+# ---------------------------------------------------------------------------
+# migration plans (Algorithm 1 end to end)
+# ---------------------------------------------------------------------------
+def plan_params(n_req, n_inst, bucket, n_buckets, max_moves, theta=(0, 1), u_rule=0,
+                mem_rule=0, min_rem=0, mem_cap=(1 << 62)) -> PlanParams:
+    return PlanParams(load_params(n_req, n_inst, bucket, n_buckets), max_moves, theta[0],
+                      theta[1], u_rule, mem_rule, min_rem, mem_cap)
+
+
+def plan_workspace_size(p: PlanParams) -> int:
+    return int(lib().star_plan_workspace_size(ctypes.byref(p)))
+
+
+def plan_migrations(p: PlanParams, cur_len, rem_len, inst_of, load, beta, moves, n_moves,
+                    ws: Workspace, stream=None):
+    """star_plan_migrations: inst_of and load are updated in place; moves is
+    an int32 tensor of max_moves * MOVE_FIELDS words, n_moves int32 [1]."""
+    _dev(cur_len, rem_len, inst_of, load, beta, moves, n_moves)
+    _check("star_plan_migrations", lib().star_plan_migrations(
+        ctypes.byref(p), _ptr(cur_len), _ptr(rem_len), _ptr(inst_of), _ptr(load), _ptr(beta),
+        _ptr(moves), _ptr(n_moves), ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))

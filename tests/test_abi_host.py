@@ -144,6 +144,28 @@ def test_score_variance_validation(L):
     assert star.score_variance_workspace_size(star.load_params(32768, 64, 64, 1024)) > 0
 
 
+def test_plan_validation(L):
+    f = FAKE
+    pp = star.plan_params(1024, 8, 64, 256, 16)
+    need = star.plan_workspace_size(pp)
+    assert need >= star.score_variance_workspace_size(star.load_params(1024, 8, 64, 256)) + 64
+    args = [f] * 7            # cur, rem, inst, load, beta, moves, n_moves
+    assert L.star_plan_migrations(ctypes.byref(pp), *args, f, need - 1, None) == -4
+    assert L.star_plan_migrations(ctypes.byref(pp), *args[:4], None, *args[5:], f, need, None) == -1
+    assert L.star_plan_migrations(ctypes.byref(pp), *args[:6], None, f, need, None) == -1
+    assert L.star_plan_migrations(ctypes.byref(pp), *args[:5], None, f, f, need, None) == -1
+    for bad in (dict(max_moves=-1), dict(max_moves=5000), dict(theta=(0, 0)),
+                dict(theta=(-1, 1)), dict(theta=(1 << 21, 1)), dict(u_rule=2), dict(mem_rule=-1),
+                dict(mem_cap=-5)):
+        kw = dict(max_moves=4)
+        kw.update(bad)
+        bp = star.plan_params(100, 4, 8, 16, **kw)
+        assert L.star_plan_migrations(ctypes.byref(bp), *args, f, 1 << 30, None) == -1, bad
+    # more instances than a workgroup classifies in LDS
+    assert star.plan_workspace_size(star.plan_params(100, 1025, 1, 4, 1)) == 0
+    assert star.plan_workspace_size(star.plan_params(1 << 18, 8, 1 << 10, 1 << 20, 1)) == 0
+
+
 def test_read_device_error_rejects_bad_args(L):
     code = ctypes.c_int32(0)
     assert L.star_read_device_error(FAKE, None, None) == -1
