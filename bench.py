@@ -13,6 +13,11 @@ microseconds per round.
 Prints ONE JSON line.  Usage:
     python bench.py [--gpus 1] [--steps 200] [--warmup 10] [--mode graph|eager]
 
+``--path plan [--workload NAME] [--moves M]`` measures Algorithm 1 end to
+end: per step, the placement is restored (a quarter of the requests crowded
+onto one instance), then star_project_load -> star_plan_migrations with up
+to M migrations (theta = 1/10, rem_len > 64).
+
 ``--path variance [--workload NAME]`` measures the time-weighted variance
 objective instead: per step, star_project_load -> star_score_variance (every
 migration's exact gain, each request's best target, the best feasible
@@ -45,9 +50,10 @@ def _parse():
                     help="which timing gives `value` (the other is reported beside it)")
     ap.add_argument("--cpu-rounds", type=int, default=20,
                     help="rounds of the CPU oracle timed for the baseline (0 = skip)")
-    ap.add_argument("--path", choices=("round", "variance"), default="round",
+    ap.add_argument("--path", choices=("round", "variance", "plan"), default="round",
                     help="round: the full rescheduling round; variance: projection + "
-                         "variance-gain scoring")
+                         "variance-gain scoring; plan: Algorithm 1 repeated")
+    ap.add_argument("--moves", type=int, default=16, help="max_moves of --path plan")
     ap.add_argument("--workload", default="rebalance_scan",
                     help="workload of --path variance")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -278,6 +284,149 @@ def bench_variance(args):
     print(json.dumps(out), flush=True)
 
 
+def plan_cpu_baseline(wl, cur, rem, inst, beta, moves: int):
+    """The oracle's Algorithm 1 on the same start.  Small workloads run the
+    whole plan; large ones time one pass's dominant cost (the full weighted
+    variance of the moved curves for every filtered candidate) on a sample
+    of the source requests and scale it to all of them."""
+    import oracle
+    if wl.n_req <= 8192:
+        t0 = time.perf_counter()
+        out = oracle.plan(cur, rem, inst, beta, n_inst=wl.n_inst, bucket=wl.bucket,
+                          n_buckets=wl.n_buckets, theta=(1, 10), min_rem=64, max_moves=moves)
+        dt = time.perf_counter() - t0
+        made = max(len(out["moves"]), 1)
+        return {"value": made / dt, "unit": "moves/s", "cores": oracle.threads(),
+                "kind": "oracle",
+                "sample": f"{len(out['moves'])} moves of the same plan from the same start "
+                          f"(classification, filtered candidates scored by the full weighted "
+                          f"variance of the moved curves, per-step curve rebuild); {dt:.2f} s"}
+    t0 = time.perf_counter()
+    load, _ = oracle.project_load(cur, rem, inst, n_inst=wl.n_inst, bucket=wl.bucket,
+                                  n_buckets=wl.n_buckets)
+    t_proj = time.perf_counter() - t0
+    w = load.astype(object).dot(beta.astype(object))
+    wsum = sum(w)
+    over = [10 * wl.n_inst * wi > 11 * wsum for wi in w]
+    srcs = np.array([r for r in range(wl.n_req) if over[inst[r]] and rem[r] > 64], np.int64)
+    sample = srcs[np.linspace(0, len(srcs) - 1, min(len(srcs), 4096)).astype(np.int64)]
+    t0 = time.perf_counter()
+    oracle.score_variance(cur[sample], rem[sample], inst[sample], load, beta, bucket=wl.bucket)
+    t_score = time.perf_counter() - t0
+    per_move = t_proj + t_score * len(srcs) / max(len(sample), 1)
+    return {"value": 1.0 / per_move, "unit": "moves/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"one pass of the plan from the same start: projection ({t_proj:.2f} s) and "
+                      f"the variance gains of {len(sample)} of the {len(srcs)} source requests on "
+                      f"overloaded instances ({t_score:.2f} s), scaled to all of them"}
+
+
+def bench_plan(args):
+    import torch
+    from paper_2510_13668_amd import star, synth
+
+    dev = "cuda"
+    wl = synth.WORKLOADS[args.workload]
+    N, n, b, K = wl.n_req, wl.n_inst, wl.bucket, wl.n_buckets
+    M = args.moves
+    x = synth.make_inputs(wl, steps=1, n_req=1)
+    rem_h = x.true_len
+    if rem_h is None:
+        rem_h = np.random.default_rng(0).integers(1, wl.horizon, size=N,
+                                                  endpoint=True).astype(np.int32)
+    inst_h = x.inst_of.copy()
+    inst_h[: N // 4] = 3 % n
+    beta_h = synth.bucket_weights(K)
+    cur = torch.from_numpy(x.cur_len).to(dev)
+    rem = torch.from_numpy(rem_h).to(dev)
+    inst0 = torch.from_numpy(inst_h).to(dev)
+    inst = inst0.clone()
+    beta = torch.from_numpy(beta_h.view(np.int16)).to(dev)
+    load = torch.empty((n, K), dtype=torch.int64, device=dev)
+    moves = torch.empty(max(M, 1) * star.MOVE_FIELDS, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    lp = star.load_params(N, n, b, K)
+    pp = star.plan_params(N, n, b, K, M, theta=(1, 10), min_rem=64)
+    ws_l = star.Workspace(star.project_load_workspace_size(lp))
+    ws_p = star.Workspace(star.plan_workspace_size(pp))
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+
+    def step():
+        with torch.cuda.stream(stream):
+            inst.copy_(inst0)
+        star.project_load(lp, cur, rem, inst, load, ws_l, stream)
+        star.plan_migrations(pp, cur, rem, inst, load, beta, moves, cnt, ws_p, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    made = int(cnt.cpu()[0])
+
+    # star_plan_migrations alone, HIP events on its stream
+    he = HipEvents()
+    evs = he.create(2 * args.steps)
+    hs = ctypes.c_void_p(stream.cuda_stream)
+    he.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    for i in range(args.steps):
+        with torch.cuda.stream(stream):
+            inst.copy_(inst0)
+        star.project_load(lp, cur, rem, inst, load, ws_l, stream)
+        he.hip.hipEventRecord(evs[2 * i], hs)
+        star.plan_migrations(pp, cur, rem, inst, load, beta, moves, cnt, ws_p, stream)
+        he.hip.hipEventRecord(evs[2 * i + 1], hs)
+    torch.cuda.synchronize()
+    call_s = float(np.mean([he.elapsed_ms(evs[2 * i], evs[2 * i + 1])
+                            for i in range(args.steps)])) * 1e-3
+    he.destroy(evs)
+    # algorithmic bytes: per pass the request arrays and the tables' target
+    # rows are read once (12 B per request, 40 B per bucket and instance);
+    # per move two curve rows are rewritten (16 B per bucket)
+    passes = min(made + 1, M) if M else 0
+    nbytes = passes * (12 * N + 40 * n * (K + 1)) + made * 16 * K + 40 * (n + 1) * (K + 1)
+    achieved = nbytes / call_s / 1e9
+
+    out = {
+        "metric": "migration plans/sec (Algorithm 1: classification, filtered candidates, "
+                  "best feasible move by exact variance gain, repeated)",
+        "value": 1.0 / (ms_step * 1e-3),
+        "unit": "plans/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int128",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {N} requests on {n} instances, a quarter crowded onto "
+                               f"one, true remaining lengths {wl.true_len or 'uniform'}, horizon "
+                               f"{wl.horizon} in {b}-step buckets, up to {M} migrations per plan, "
+                               f"theta 1/10, rem_len > 64",
+                   "n_req": N, "n_inst": n, "horizon": wl.horizon, "bucket": b, "max_moves": M,
+                   "moves_made": made},
+        "roofline": {"kernel": "star_plan_migrations (prep, then per move a masked scoring pass "
+                               "and a one-workgroup update)",
+                     "bound": "latency", "achieved": achieved, "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "avg_call_us": call_s * 1e6, "us_per_move": call_s * 1e6 / max(made, 1),
+                     "algorithmic_bytes": nbytes},
+    }
+    if args.cpu_rounds > 0:
+        out["cpu_baseline"] = plan_cpu_baseline(wl, x.cur_len, rem_h, inst_h, beta_h,
+                                                min(M, 4 if N > 8192 else M))
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = _parse()
     if args.copy_calibration:
@@ -290,6 +439,9 @@ def main():
         sys.exit(2)
     if args.path == "variance":
         bench_variance(args)
+        return
+    if args.path == "plan":
+        bench_plan(args)
         return
 
     import torch

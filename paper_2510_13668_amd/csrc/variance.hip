@@ -59,6 +59,8 @@ constexpr size_t kHdrVarTicket = 64;   // workspace header: finished-workgroup t
 constexpr int VS_TICKET_BLOCKS = 64;
 constexpr int VS_MAX_LG = 4;             // at most 16 lanes per request
 constexpr int PLAN_MAX_INST = 1024;      // instances a plan classifies in LDS
+constexpr int PA_THREADS = 256;          // the plan's update workgroup
+constexpr int PLAN_MAX_BLOCKS = 1 << 20; // scoring workgroups of a plan pass (one tile each)
 
 constexpr size_t kHdrPlanDone = 72;      // workspace header: the plan has stopped
 constexpr size_t kHdrPlanCount = 76;     // workspace header: moves made
@@ -293,25 +295,32 @@ __device__ inline VKey load_part(VPart* p) {
 // (or the no-move record when none is negative).
 // One workgroup: the smallest of `parts` partial keys, returned to every
 // thread.
-template <bool kAtomic>
+template <bool kAtomic, int kThreads = VS_THREADS>
 __device__ VKey reduce_keys(VPart* part, int parts, VKey* wbest) {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    constexpr int kBatch = 8;   // partials in flight per thread
     VKey k = no_key();
-    for (int g = tid; g < parts; g += VS_THREADS) {
-        VKey p;
-        if (kAtomic) {
-            p = load_part(&part[g]);
-        } else {
-            const VPart v = part[g];
-            p = VKey{(s128)(((u128)v.w[1] << 64) | (u128)v.w[0]), (uint32_t)v.w[2]};
+    for (int g0 = tid; g0 < parts; g0 += kThreads * kBatch) {
+        VKey p[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            const int g = g0 + i * kThreads;
+            VPart* src = &part[g < parts ? g : parts - 1];
+            if (kAtomic) {
+                p[i] = load_part(src);
+            } else {
+                const VPart v = *src;
+                p[i] = VKey{(s128)(((u128)v.w[1] << 64) | (u128)v.w[0]), (uint32_t)v.w[2]};
+            }
         }
-        k = vmin(k, p);
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) k = vmin(k, p[i]);   // repeats are harmless
     }
     k = group_min(k, 6, lane);
     if (lane == kWave - 1) wbest[wid] = k;
     __syncthreads();
     VKey m = wbest[0];
-    for (int w = 1; w < VS_WAVES; ++w) m = vmin(m, wbest[w]);
+    for (int w = 1; w < kThreads / kWave; ++w) m = vmin(m, wbest[w]);
     __syncthreads();
     return m;
 }
@@ -369,6 +378,7 @@ struct VarArgs {
     int32_t* err;
     int N, n, b, K;
     int ticketed;            // 1: the last workgroup reduces the partials
+    int tiles;               // request tiles (workgroups loop over them in plans)
     int64_t H;
     // plans (Algorithm 1's classification and candidate filters)
     const int64_t* now;      // [n] current loads N_i
@@ -436,7 +446,6 @@ __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
     const int sub = lane >> LG, tl = lane & (P - 1);
     const int n = a.n, K = a.K, K1 = K + 1;
     const uint64_t bb = (uint64_t)a.b * (uint64_t)a.b;
-    const int r0 = blockIdx.x * TILE;
     const QEntry* __restrict__ qt = a.qt;
     const int64_t* __restrict__ lt = a.lt;
     u128* __restrict__ gain = a.gain;
@@ -465,93 +474,101 @@ __global__ __launch_bounds__(VS_THREADS) void var_score_kernel(VarArgs a) {
         __syncthreads();
     }
 
-    if (tid < TILE) {
-        const int r = r0 + tid;
-        ReqStash e;
-        e.base = 0;
-        e.bp = 0;
-        e.al = 0;
-        e.ke = 0;
-        e.s = -1;
-        e.need = 0;
-        if (r < a.N) {
-            const ReqTerms q = request_terms(a.inst[r], a.cur[r], a.rem[r], n, a.b, a.H);
-            if (!kPlan) report_error(a.err, q.bad);
-            bool src_ok = !q.bad;
-            if (kPlan && src_ok) {
-                src_ok = over_m[q.s] && a.rem[r] > a.min_rem;
-                e.need = a.rem[r] + (a.mem_rule ? a.cur[r] : 0);
-            }
-            e.s = src_ok ? q.s : -2;
-            if (src_ok) {
-                // alpha, b^2 and p are non-negative and below 2^62
-                const uint64_t al = (uint64_t)q.alpha;
-                const int ke = q.ke;
-                const u128 b0 = a.bs[ke], b1 = a.bs[K1 + ke], b2 = a.bs[2 * K1 + ke];
-                const QEntry qs = qt[(size_t)ke * n + q.s];
-                u128 base = mul_u64(mul_u64(b0, al), al) + mul_u64(mul_u64(b1, al), 2 * bb) +
-                            mul_u64(mul_u64(b2, bb), bb) - mul_u64(qs.qa, al) -
-                            mul_u64(qs.qb, bb);
-                u128 bp = 0;
-                if (ke < K) {
-                    bp = (u128)a.beta[ke] * (u128)(uint64_t)q.p;
-                    base += mul_s64(bp, q.p - lt[(size_t)ke * n + q.s]);
+    VKey feas = no_key();   // best key of this lane's requests that lowers the objective
+    for (int tile = blockIdx.x; tile < a.tiles; tile += gridDim.x) {
+        const int r0 = tile * TILE;
+        __syncthreads();   // the previous tile's stash has been read
+        if (tid < TILE) {
+            const int r = r0 + tid;
+            ReqStash e;
+            e.base = 0;
+            e.bp = 0;
+            e.al = 0;
+            e.ke = 0;
+            e.s = -1;
+            e.need = 0;
+            if (r < a.N) {
+                const ReqTerms q = request_terms(a.inst[r], a.cur[r], a.rem[r], n, a.b, a.H);
+                if (!kPlan) report_error(a.err, q.bad);
+                bool src_ok = !q.bad;
+                if (kPlan && src_ok) {
+                    src_ok = over_m[q.s] && a.rem[r] > a.min_rem;
+                    e.need = a.rem[r] + (a.mem_rule ? a.cur[r] : 0);
                 }
-                e.base = base;
-                e.bp = bp;
-                e.al = al;
-                e.ke = ke;
+                e.s = src_ok ? q.s : -2;
+                if (src_ok) {
+                    // alpha, b^2 and p are non-negative and below 2^62
+                    const uint64_t al = (uint64_t)q.alpha;
+                    const int ke = q.ke;
+                    const u128 b0 = a.bs[ke], b1 = a.bs[K1 + ke], b2 = a.bs[2 * K1 + ke];
+                    const QEntry qs = qt[(size_t)ke * n + q.s];
+                    u128 base = mul_u64(mul_u64(b0, al), al) + mul_u64(mul_u64(b1, al), 2 * bb) +
+                                mul_u64(mul_u64(b2, bb), bb) - mul_u64(qs.qa, al) -
+                                mul_u64(qs.qb, bb);
+                    u128 bp = 0;
+                    if (ke < K) {
+                        bp = (u128)a.beta[ke] * (u128)(uint64_t)q.p;
+                        base += mul_s64(bp, q.p - lt[(size_t)ke * n + q.s]);
+                    }
+                    e.base = base;
+                    e.bp = bp;
+                    e.al = al;
+                    e.ke = ke;
+                }
+            }
+            st[tid] = e;
+        }
+        __syncthreads();
+
+        const int j = wid * RPW + sub;
+        const int r = r0 + j;
+        const u128 base = st[j].base, bp = st[j].bp;
+        const uint64_t al = st[j].al;
+        const int ke = st[j].ke, src = st[j].s;
+        const int64_t need = st[j].need;
+        const bool live = src != -1, valid = src >= 0;
+        const size_t row = valid ? (size_t)ke * n : 0;   // others read entry 0, unused
+        s128 bg = ~(u128)0 >> 1;
+        int bt = -1;
+        for (int c0 = 0; c0 < n; c0 += P * VS_M) {
+            QEntry qe[VS_M];
+            int64_t le[VS_M];
+#pragma unroll
+            for (int i = 0; i < VS_M; ++i) {
+                const int t = c0 + tl + P * i;
+                const size_t o = row + (t < n ? t : 0);
+                qe[i] = qt[o];
+                le[i] = lt[o];
+            }
+#pragma unroll
+            for (int i = 0; i < VS_M; ++i) {
+                const int t = c0 + tl + P * i;
+                u128 g = 0;
+                if (valid) {   // whole waves without a source skip the arithmetic
+                    g = base + mul_u64(qe[i].qa, al) + mul_u64(qe[i].qb, bb);
+                    if (ke < K) g += mul_s64(bp, le[i]);
+                }
+                bool mig = valid && t < n && t != src;
+                if (kPlan) mig = mig && need <= room_m[t < n ? t : 0];
+                if (!mig) g = 0;
+                if (mig && (s128)g < bg) {   // targets ascend within a lane
+                    bg = (s128)g;
+                    bt = t;
+                }
+                if (!kPlan && gain && live && t < n) gain[(size_t)r * n + t] = g;
             }
         }
-        st[tid] = e;
-    }
-    __syncthreads();
+        if (LG >= 1) dpp_step<kDppRowShr1, 1>(bg, bt, tl);
+        if (LG >= 2) dpp_step<kDppRowShr2, 2>(bg, bt, tl);
+        if (LG >= 3) dpp_step<kDppRowShr4, 4>(bg, bt, tl);
+        if (LG >= 4) dpp_step<kDppRowShr8, 8>(bg, bt, tl);
 
-    const int j = wid * RPW + sub;
-    const int r = r0 + j;
-    const u128 base = st[j].base, bp = st[j].bp;
-    const uint64_t al = st[j].al;
-    const int ke = st[j].ke, src = st[j].s;
-    const int64_t need = st[j].need;
-    const bool live = src != -1, valid = src >= 0;
-    const size_t row = valid ? (size_t)ke * n : 0;   // others read entry 0, unused
-    s128 bg = ~(u128)0 >> 1;
-    int bt = -1;
-    for (int c0 = 0; c0 < n; c0 += P * VS_M) {
-        QEntry qe[VS_M];
-        int64_t le[VS_M];
-#pragma unroll
-        for (int i = 0; i < VS_M; ++i) {
-            const int t = c0 + tl + P * i;
-            const size_t o = row + (t < n ? t : 0);
-            qe[i] = qt[o];
-            le[i] = lt[o];
+        if (live && tl == P - 1) {
+            if (!kPlan && a.best_target) a.best_target[r] = bt;
+            if (!kPlan && a.best_gain) a.best_gain[r] = bt >= 0 ? (u128)bg : (u128)0;
+            if (bt >= 0 && bg < 0)
+                feas = vmin(feas, VKey{bg, (uint32_t)r * (uint32_t)n + (uint32_t)bt});
         }
-#pragma unroll
-        for (int i = 0; i < VS_M; ++i) {
-            const int t = c0 + tl + P * i;
-            u128 g = base + mul_u64(qe[i].qa, al) + mul_u64(qe[i].qb, bb);
-            if (ke < K) g += mul_s64(bp, le[i]);
-            bool mig = valid && t < n && t != src;
-            if (kPlan) mig = mig && need <= room_m[t < n ? t : 0];
-            if (!mig) g = 0;
-            if (mig && (s128)g < bg) {   // targets ascend within a lane
-                bg = (s128)g;
-                bt = t;
-            }
-            if (!kPlan && gain && live && t < n) gain[(size_t)r * n + t] = g;
-        }
-    }
-    if (LG >= 1) dpp_step<kDppRowShr1, 1>(bg, bt, tl);
-    if (LG >= 2) dpp_step<kDppRowShr2, 2>(bg, bt, tl);
-    if (LG >= 3) dpp_step<kDppRowShr4, 4>(bg, bt, tl);
-    if (LG >= 4) dpp_step<kDppRowShr8, 8>(bg, bt, tl);
-
-    VKey feas = no_key();   // the request's best key if it lowers the objective
-    if (live && tl == P - 1) {
-        if (!kPlan && a.best_target) a.best_target[r] = bt;
-        if (!kPlan && a.best_gain) a.best_gain[r] = bt >= 0 ? (u128)bg : (u128)0;
-        if (bt >= 0 && bg < 0) feas = VKey{bg, (uint32_t)r * (uint32_t)n + (uint32_t)bt};
     }
     if (!kPlan && !a.move) return;
 
@@ -610,55 +627,67 @@ struct PlanArgs {
     int64_t H;
 };
 
-// Tables of every row (as var_prep_kernel), the current load N_i of every
-// instance (each row's workgroup sums its valid requests' cur_len), and the
-// plan's state reset; the weights' workgroup reports invalid requests.
+// The plan's state: current loads (accumulated by plan_prep_kernel), stop
+// flag and move counts.
+__global__ void plan_zero_kernel(int64_t* now, int n, int32_t* done, int32_t* count,
+                                 int32_t* n_moves) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) now[i] = 0;
+    if (threadIdx.x == 0) {
+        *done = 0;
+        *count = 0;
+        *n_moves = 0;
+    }
+}
+
+constexpr int PLAN_REQ_CHUNK = 4096;     // requests per current-load workgroup
+
+// Workgroups 0..n: the tables of every row (as var_prep_kernel).  The
+// others: each sums cur_len per instance over a chunk of valid requests in
+// LDS and adds the sums to N_i (int64 atomics: exact, any order), and
+// reports invalid requests.
 __global__ __launch_bounds__(VP_THREADS) void plan_prep_kernel(PlanArgs a) {
     __shared__ u128 sx[3][VP_THREADS];
-    __shared__ int64_t red[VP_THREADS];
+    __shared__ unsigned long long hist[PLAN_MAX_INST];
     const int row = blockIdx.x, tid = threadIdx.x, n = a.n;
-    if (row < n) {
-        int64_t acc = 0;
-        for (int r = tid; r < a.N; r += VP_THREADS) {
-            const int c = a.cur[r];
-            if (a.inst[r] == row && c >= 1 && a.rem[r] >= 1) acc += c;
-        }
-        red[tid] = acc;
-        __syncthreads();
-        for (int o = VP_THREADS / 2; o > 0; o >>= 1) {
-            if (tid < o) red[tid] += red[tid + o];
-            __syncthreads();
-        }
-        if (tid == 0) a.now[row] = red[0];
-    } else {
-        int32_t bad = 0;
-        for (int r = tid; r < a.N; r += VP_THREADS) {
-            const int s = a.inst[r];
-            if (s < 0 || s >= n) bad |= STAR_DEV_BAD_INST;
-            if (a.cur[r] < 1) bad |= STAR_DEV_BAD_CUR;
-            if (a.rem[r] < 1) bad |= STAR_DEV_BAD_REM;
-        }
-        report_error(a.err, bad);
-        if (tid == 0) {
-            *a.done = 0;
-            *a.count = 0;
-            *a.n_moves = 0;
-        }
+    if (row <= n) {
+        prep_row(a.load + (size_t)(row == n ? 0 : row) * a.K, a.beta, n, a.K, row, row == n,
+                 a.qt, a.lt, a.bs, sx);
+        return;
     }
-    prep_row(a.load + (size_t)(row == n ? 0 : row) * a.K, a.beta, n, a.K, row, row == n, a.qt,
-             a.lt, a.bs, sx);
+    for (int i = tid; i < n; i += VP_THREADS) hist[i] = 0;
+    __syncthreads();
+    const int r0 = (row - n - 1) * PLAN_REQ_CHUNK;
+    const int r1 = min(a.N, r0 + PLAN_REQ_CHUNK);
+    int32_t bad = 0;
+    for (int r = r0 + tid; r < r1; r += VP_THREADS) {
+        const int s = a.inst[r], c = a.cur[r], l = a.rem[r];
+        int32_t f = 0;
+        if (s < 0 || s >= n) f |= STAR_DEV_BAD_INST;
+        if (c < 1) f |= STAR_DEV_BAD_CUR;
+        if (l < 1) f |= STAR_DEV_BAD_REM;
+        if (!f) atomicAdd(&hist[s], (unsigned long long)c);
+        bad |= f;
+    }
+    report_error(a.err, bad);
+    __syncthreads();
+    for (int i = tid; i < n; i += VP_THREADS)
+        if (hist[i]) atomicAdd((unsigned long long*)&a.now[i], hist[i]);
 }
 
 // One workgroup after each scoring pass: the best feasible key of the
 // pass; none stops the plan.  Otherwise the move is recorded and executed:
-// inst_of[r] = t, N_s and N_t adjusted, r's own curve taken from row s and
-// added to row t of the curves, and those two rows' tables recomputed.
-__global__ __launch_bounds__(VP_THREADS) void plan_apply_kernel(PlanArgs a) {
-    __shared__ u128 sx[3][VP_THREADS];
-    __shared__ VKey wbest[VS_WAVES];
+// inst_of[r] = t, N_s and N_t adjusted, r's own curve R taken from row s
+// and added to row t of the curves.  The tables change by closed forms, so
+// no scan is needed: with F_A(k) = sum_{j<k} beta_j R_j and
+// F_B(k) = sum_{j<k} beta_j j R_j,
+//     F_A(k) = alpha B0[k] + b^2 B1[k],  F_B(k) = alpha B1[k] + b^2 B2[k]
+// for k <= k_e, and for k > k_e the value at k_e plus beta_{k_e} p (times
+// k_e for F_B); QA and QB of row s fall by F, those of row t rise by F.
+__global__ __launch_bounds__(PA_THREADS) void plan_apply_kernel(PlanArgs a) {
+    __shared__ VKey wbest[PA_THREADS / kWave];
     if (*a.done) return;
-    const int tid = threadIdx.x, n = a.n, K = a.K;
-    const VKey m = reduce_keys<false>(a.part, a.parts, wbest);
+    const int tid = threadIdx.x, n = a.n, K = a.K, K1 = K + 1;
+    const VKey m = reduce_keys<false, PA_THREADS>(a.part, a.parts, wbest);
     if (m.idx == kNoIdx) {
         if (tid == 0) *a.done = 1;
         return;
@@ -684,20 +713,32 @@ __global__ __launch_bounds__(VP_THREADS) void plan_apply_kernel(PlanArgs a) {
         a.now[s] -= c;
         a.now[t] += c;
     }
-    // the same bucket ranges as prep_row: each thread rereads only its own writes
     const ReqTerms rq = request_terms(t, c, a.rem[r], n, a.b, a.H);
-    const int64_t bb = (int64_t)a.b * a.b;
-    const int per = (K + VP_THREADS - 1) / VP_THREADS;
-    const int j0 = min(tid * per, K), j1 = min(j0 + per, K);
-    int64_t* Ls = a.load + (size_t)s * K;
-    int64_t* Lt = a.load + (size_t)t * K;
-    for (int j = j0; j < j1 && j <= rq.ke; ++j) {
-        const int64_t R = j < rq.ke ? rq.alpha + bb * j : rq.p;
-        Ls[j] -= R;
-        Lt[j] += R;
+    const int ke = rq.ke;
+    const uint64_t al = (uint64_t)rq.alpha;
+    const uint64_t bb = (uint64_t)a.b * (uint64_t)a.b;
+    const u128 tail = ke < K ? (u128)a.beta[ke] * (u128)(uint64_t)rq.p : (u128)0;
+    for (int k = tid; k <= K; k += PA_THREADS) {
+        const int kk = k <= ke ? k : ke;
+        u128 fa = mul_u64(a.bs[kk], al) + mul_u64(a.bs[K1 + kk], bb);
+        u128 fb = mul_u64(a.bs[K1 + kk], al) + mul_u64(a.bs[2 * (size_t)K1 + kk], bb);
+        if (k > ke) {
+            fa += tail;
+            fb += mul_u64(tail, (uint64_t)ke);
+        }
+        QEntry* es = &a.qt[(size_t)k * n + s];
+        QEntry* et = &a.qt[(size_t)k * n + t];
+        const QEntry vs = *es, vt = *et;
+        *es = QEntry{vs.qa - fa, vs.qb - fb};
+        *et = QEntry{vt.qa + fa, vt.qb + fb};
+        if (k < K && k <= ke) {
+            const int64_t R = k < ke ? rq.alpha + (int64_t)bb * k : rq.p;
+            a.lt[(size_t)k * n + s] -= R;
+            a.lt[(size_t)k * n + t] += R;
+            a.load[(size_t)s * K + k] -= R;
+            a.load[(size_t)t * K + k] += R;
+        }
     }
-    prep_row(Ls, a.beta, n, K, s, false, a.qt, a.lt, a.bs, sx);
-    prep_row(Lt, a.beta, n, K, t, false, a.qt, a.lt, a.bs, sx);
 }
 
 // ---------------------------------------------------------------------------
@@ -785,6 +826,7 @@ hipError_t launch_variance(const star_load_params& p, const VarPlan& pl, const i
     a.b = p.bucket;
     a.K = K;
     a.ticketed = pl.ticketed;
+    a.tiles = pl.blocks;
     a.H = (int64_t)p.bucket * K;
     launch_score_lg<false>(pl.lg, pl.blocks, a, stream);
     if (move && !pl.ticketed)
@@ -818,7 +860,8 @@ hipError_t launch_plan(const star_plan_params& p, const PlanPlan& pl, const int3
     a.lt = (int64_t*)(ws + pl.v.lt_off);
     a.bs = (u128*)(ws + pl.v.bs_off);
     a.part = (VPart*)(ws + pl.v.part_off);
-    a.parts = pl.v.blocks;
+    const int grid = pl.v.blocks < PLAN_MAX_BLOCKS ? pl.v.blocks : PLAN_MAX_BLOCKS;
+    a.parts = grid;
     a.now = (int64_t*)(ws + pl.now_off);
     a.done = (int32_t*)(ws + kHdrPlanDone);
     a.count = (int32_t*)(ws + kHdrPlanCount);
@@ -830,7 +873,10 @@ hipError_t launch_plan(const star_plan_params& p, const PlanPlan& pl, const int3
     a.b = p.load.bucket;
     a.K = K;
     a.H = (int64_t)p.load.bucket * K;
-    hipLaunchKernelGGL(plan_prep_kernel, dim3(n + 1), dim3(VP_THREADS), 0, stream, a);
+    hipLaunchKernelGGL(plan_zero_kernel, dim3(1), dim3(256), 0, stream, a.now, n, a.done, a.count,
+                       n_moves);
+    const int chunks = (int)ceil_div(a.N, PLAN_REQ_CHUNK);
+    hipLaunchKernelGGL(plan_prep_kernel, dim3(n + 1 + chunks), dim3(VP_THREADS), 0, stream, a);
 
     VarArgs v;
     v.cur = cur;
@@ -852,6 +898,7 @@ hipError_t launch_plan(const star_plan_params& p, const PlanPlan& pl, const int3
     v.b = a.b;
     v.K = K;
     v.ticketed = 0;
+    v.tiles = pl.v.blocks;
     v.H = a.H;
     v.now = a.now;
     v.done = a.done;
@@ -862,8 +909,8 @@ hipError_t launch_plan(const star_plan_params& p, const PlanPlan& pl, const int3
     v.min_rem = p.min_rem;
     v.mem_cap = p.mem_cap;
     for (int m = 0; m < p.max_moves; ++m) {
-        launch_score_lg<true>(pl.v.lg, pl.v.blocks, v, stream);
-        hipLaunchKernelGGL(plan_apply_kernel, dim3(1), dim3(VP_THREADS), 0, stream, a);
+        launch_score_lg<true>(pl.v.lg, grid, v, stream);
+        hipLaunchKernelGGL(plan_apply_kernel, dim3(1), dim3(PA_THREADS), 0, stream, a);
     }
     return hipGetLastError();
 }
