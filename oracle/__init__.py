@@ -42,7 +42,12 @@ def _load():
         lib.star_oracle_select_variance.argtypes = [_I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P]
         lib.star_oracle_plan.argtypes = [_I64, _I64, _I64, _I64, _P, _P, _P, _P, _P, _I64, _I64,
                                          ctypes.c_int, _I64, _I64, ctypes.c_int, _I64, _P, _P, _P]
-        for f in ("star_oracle_predict", "star_oracle_project_load", "star_oracle_score",
+        lib.star_oracle_predict_mlp4.argtypes = [_I64, _I64, _I64, _I64, _I64, ctypes.c_int,
+                                                 _P, _P, _P, _P, _P, _P, _P, _P,
+                                                 ctypes.c_double, _P, _I64, ctypes.c_double,
+                                                 ctypes.c_int, _P, _I64, _P, _P, _P]
+        for f in ("star_oracle_predict_mlp4", "star_oracle_predict", "star_oracle_project_load",
+                  "star_oracle_score",
                   "star_oracle_rank", "star_oracle_score_variance",
                   "star_oracle_select_variance", "star_oracle_plan"):
             getattr(lib, f).restype = ctypes.c_int
@@ -102,6 +107,39 @@ def predict(hidden, w1, w2, bin_values, *, dtype: int, act: int, b1=None, b2=Non
         out["z1"] = z1
         out["z2"] = z2
     return out
+
+
+def predict_mlp4(hidden, w1, w2, w3, w4, *, dtype: int, b1=None, b2=None, b3=None, b4=0.0,
+                 rows=None, ema_alpha: float = 0.0, ema_init: bool = False,
+                 ema_state: Optional[np.ndarray] = None, len_max: int = 1 << 30):
+    """fp64 4-layer ReLU regression head on the listed rows (all if None).
+
+    Returns dict(expected, rem_len, scale) indexed like `rows`.  ``ema_state``
+    (fp64, one per listed row) is updated in place when ``ema_alpha > 0``.
+    """
+    et = np.uint16 if dtype == BF16 else np.float32
+    hidden, w1, w2, w3 = (_c(a, et) for a in (hidden, w1, w2, w3))
+    B, d = hidden.shape
+    m1, m2, m3 = w1.shape[0], w2.shape[0], w3.shape[0]
+    assert w1.shape == (m1, d) and w2.shape == (m2, m1) and w3.shape == (m3, m2)
+    w4 = _c(w4, np.float32)
+    assert w4.shape == (m3,)
+    b1, b2, b3 = (_c(b, np.float32) for b in (b1, b2, b3))
+    rows = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    R = B if rows is None else rows.shape[0]
+    if ema_alpha > 0.0:
+        assert ema_state is not None and ema_state.dtype == np.float64 and ema_state.shape == (R,)
+    expected = np.empty(R, np.float64)
+    rem = np.empty(R, np.int32)
+    scale = np.empty(R, np.float64)
+    rc = _load().star_oracle_predict_mlp4(B, d, m1, m2, m3, dtype, _ptr(hidden), _ptr(w1),
+                                          _ptr(b1), _ptr(w2), _ptr(b2), _ptr(w3), _ptr(b3),
+                                          _ptr(w4), float(b4), _ptr(rows), R, float(ema_alpha),
+                                          int(bool(ema_init)), _ptr(ema_state), int(len_max),
+                                          _ptr(expected), _ptr(rem), _ptr(scale))
+    if rc != 0:
+        raise ValueError("star_oracle_predict_mlp4: malformed arguments")
+    return {"expected": expected, "rem_len": rem, "scale": scale}
 
 
 def project_load(cur_len, rem_len, inst_of, *, n_inst: int, bucket: int, n_buckets: int):

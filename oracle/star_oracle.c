@@ -137,6 +137,70 @@ static int request_flags(int64_t r, int64_t n, const int32_t* cur, const int32_t
 }
 
 /* ---------------------------------------------------------------------- */
+/* (f3) the paper's regression head: a 4-layer ReLU MLP with scalar output */
+/* ---------------------------------------------------------------------- */
+/* y^ = w4 . phi(W3 phi(W2 phi(W1 h + b1) + b2) + b3) + b4 (Section 4.2,
+ * Eq. 2, biases optional), phi = ReLU; then the same EMA and integerisation
+ * as the binned head.  Only the rows listed in `rows` (or all when rows is
+ * NULL) are computed; outputs are indexed like the rows list.  scale_out
+ * (or NULL) receives sum_j |w4_j a3_j| + |b4| per row, the magnitude the
+ * result's rounding error is relative to. */
+int star_oracle_predict_mlp4(int64_t B, int64_t d, int64_t m1, int64_t m2, int64_t m3,
+                             int dtype, const void* hidden, const void* w1, const float* b1,
+                             const void* w2, const float* b2, const void* w3, const float* b3,
+                             const float* w4, double b4, const int64_t* rows, int64_t n_rows,
+                             double ema_alpha, int ema_init, double* ema_state, int64_t len_max,
+                             double* expected, int32_t* rem_len, double* scale_out) {
+    if (B < 0 || d < 1 || m1 < 1 || m2 < 1 || m3 < 1 || len_max < 1) return -1;
+    const int64_t R = rows ? n_rows : B;
+    int bad = 0;
+    #pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (int64_t q = 0; q < R; ++q) {
+        const int64_t b = rows ? rows[q] : q;
+        if (b < 0 || b >= B) { bad = 1; continue; }
+        double* a1 = (double*)malloc(sizeof(double) * (size_t)m1);
+        double* a2 = (double*)malloc(sizeof(double) * (size_t)m2);
+        double* a3 = (double*)malloc(sizeof(double) * (size_t)m3);
+        for (int64_t j = 0; j < m1; ++j) {
+            double z = b1 ? (double)b1[j] : 0.0;
+            for (int64_t k = 0; k < d; ++k)
+                z += widen(hidden, b * d + k, dtype) * widen(w1, j * d + k, dtype);
+            a1[j] = activation(z, STAR_ORACLE_RELU);
+        }
+        for (int64_t j = 0; j < m2; ++j) {
+            double z = b2 ? (double)b2[j] : 0.0;
+            for (int64_t k = 0; k < m1; ++k) z += a1[k] * widen(w2, j * m1 + k, dtype);
+            a2[j] = activation(z, STAR_ORACLE_RELU);
+        }
+        double y = b4, scale = fabs(b4);
+        for (int64_t j = 0; j < m3; ++j) {
+            double z = b3 ? (double)b3[j] : 0.0;
+            for (int64_t k = 0; k < m2; ++k) z += a2[k] * widen(w3, j * m2 + k, dtype);
+            a3[j] = activation(z, STAR_ORACLE_RELU);
+            y += (double)w4[j] * a3[j];
+            scale += fabs((double)w4[j] * a3[j]);
+        }
+        expected[q] = y;
+        if (scale_out) scale_out[q] = scale;
+        double yv = y;
+        if (ema_alpha > 0.0) {
+            yv = ema_init ? y : ema_alpha * y + (1.0 - ema_alpha) * ema_state[q];
+            ema_state[q] = yv;
+        }
+        if (rem_len) {
+            double r = nearbyint(yv);
+            if (!(r >= 1.0)) r = 1.0;
+            if (r > (double)len_max) r = (double)len_max;
+            rem_len[q] = (int32_t)r;
+        }
+        free(a1);
+        free(a2);
+        free(a3);
+    }
+    return bad ? -1 : 0;
+}
+
+/* ---------------------------------------------------------------------- */
 /* (b) predicted per-instance load curve, by per-step summation            */
 /* ---------------------------------------------------------------------- */
 int star_oracle_project_load(int64_t N, int64_t n, int64_t b, int64_t K,

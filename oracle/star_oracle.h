@@ -35,6 +35,20 @@ int star_oracle_predict(int64_t B, int64_t d, int64_t m, int64_t nb, int dtype, 
                         int64_t len_max, double* expected, int32_t* rem_len,
                         double* z1_out, double* z2_out);
 
+/* The paper's regression head (Section 4.2, Eq. 2): a 4-layer ReLU MLP
+ * d -> m1 -> m2 -> m3 -> 1 with optional biases b1..b3 (fp32 or NULL) and
+ * output weights w4 [m3] fp32, scalar bias b4; W1 [m1,d], W2 [m2,m1],
+ * W3 [m3,m2] in `dtype`.  Computes the rows listed in `rows` (n_rows of
+ * them; NULL = all B rows); expected [q] <- y^ of rows[q]; EMA and
+ * integerisation as star_oracle_predict (ema_state indexed like the rows
+ * list); scale_out [q] (or NULL) <- sum_j |w4_j a3_j| + |b4|. */
+int star_oracle_predict_mlp4(int64_t B, int64_t d, int64_t m1, int64_t m2, int64_t m3,
+                             int dtype, const void* hidden, const void* w1, const float* b1,
+                             const void* w2, const float* b2, const void* w3, const float* b3,
+                             const float* w4, double b4, const int64_t* rows, int64_t n_rows,
+                             double ema_alpha, int ema_init, double* ema_state, int64_t len_max,
+                             double* expected, int32_t* rem_len, double* scale_out);
+
 /* Load curves (Section 5.2, Eq. 4 and the worker-side summary of the
  * complexity analysis).  load [n,K]: load[i,k] = sum over decode steps
  * t in [k b, (k+1) b) of sum_{r in B_i, t < rem_r} (cur_r + t).

@@ -239,6 +239,60 @@ def make_inputs(wl: Workload, seed: int = 0, *, with_bias: bool = False,
                   cur, true, inst)
 
 
+@dataclasses.dataclass
+class Mlp4Inputs:
+    hidden: np.ndarray             # [B, d] or [S, B, d]; uint16 bits (bf16) or float32
+    w1: np.ndarray                 # [m1, d]
+    w2: np.ndarray                 # [m2, m1]
+    w3: np.ndarray                 # [m3, m2]
+    w4: np.ndarray                 # [m3] float32
+    b1: Optional[np.ndarray]
+    b2: Optional[np.ndarray]
+    b3: Optional[np.ndarray]
+    b4: float
+
+
+MLP4_DIMS = (3584, 2048, 512, 64)   # d and the three widths of the paper's head (Section 4.2)
+
+
+def make_mlp4(n_req: int, dims=MLP4_DIMS, *, dtype: int = BF16, seed: int = 0, steps: int = 1,
+              ar_rho: float = 0.95, with_bias: bool = False, y_mean: float = 1100.0,
+              y_spread: float = 400.0) -> Mlp4Inputs:
+    """Random-initialised regression head of the paper's shape and hidden
+    states for it.  W1..W3 ~ N(0, 2/fan_in) (ReLU-preserving scale); w4 ~
+    N(0, (y_spread)^2 / m3) and b4 = y_mean put the outputs at realistic
+    remaining lengths.  Hidden states: N(0,1), an AR(1) chain over `steps`
+    decode steps (as the continuous workload)."""
+    d, m1, m2, m3 = dims
+    children = np.random.SeedSequence(seed).spawn(9)
+    rs = [np.random.default_rng(c) for c in children]
+
+    def mat(rng, shape, fan_in):
+        w = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(np.sqrt(2.0 / fan_in))
+        return f32_to_bf16_bits(w) if dtype == BF16 else w
+
+    if steps > 1:
+        hidden = np.empty((steps, n_req, d), dtype=np.uint16 if dtype == BF16 else np.float32)
+        state = rs[0].standard_normal(size=(n_req, d), dtype=np.float32)
+        sig = np.float32(np.sqrt(1.0 - ar_rho ** 2))
+        for t in range(steps):
+            if t > 0:
+                state = np.float32(ar_rho) * state + sig * rs[1].standard_normal(
+                    size=(n_req, d), dtype=np.float32)
+            hidden[t] = f32_to_bf16_bits(state) if dtype == BF16 else state
+    else:
+        h = rs[0].standard_normal(size=(n_req, d), dtype=np.float32)
+        hidden = f32_to_bf16_bits(h) if dtype == BF16 else h
+    w1, w2, w3 = mat(rs[2], (m1, d), d), mat(rs[3], (m2, m1), m1), mat(rs[4], (m3, m2), m2)
+    w4 = (rs[5].standard_normal(size=m3) * (y_spread / np.sqrt(m3))).astype(np.float32)
+    b1 = b2 = b3 = None
+    if with_bias:
+        b1 = (rs[6].standard_normal(size=m1) * 0.1).astype(np.float32)
+        b2 = (rs[7].standard_normal(size=m2) * 0.1).astype(np.float32)
+        b3 = (rs[8].standard_normal(size=m3) * 0.1).astype(np.float32)
+    return Mlp4Inputs(hidden, w1, w2, w3, w4, b1, b2, b3, float(y_mean))
+
+
 def random_requests(rng: np.random.Generator, n_req: int, n_inst: int, *, cur_hi: int,
                     len_hi: int, contiguous: bool = False, empty_inst: int = 0):
     """Small random (cur_len, rem_len, inst_of) triples for parity and pin tests.
