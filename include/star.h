@@ -106,6 +106,44 @@ star_status star_predict(const star_predict_params* p, const void* hidden, const
                          int32_t* rem_len, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * (f3) The paper's regression head.
+ *
+ * Section 4.2 (Eq. 2) predicts the remaining length directly with a 4-layer
+ * MLP on the same last-layer, last-token hidden state h:
+ *     y^ = w4 . relu(W3 relu(W2 relu(W1 h + b1) + b2) + b3) + b4
+ * W1 [m1, d], W2 [m2, m1], W3 [m3, m2] (dtype of hidden), w4 [m3] fp32;
+ * b1 [m1], b2 [m2], b3 [m3] fp32 or NULL (Eq. 2 has none); b4 in the params.
+ * The paper's sizes: d = 3584, m1 = 2048, m2 = 512, m3 = 64 (8.4 M weights).
+ * expected_len [B] <- y^; the EMA and rem_len follow as in (a).
+ * Precision: bf16 (or fp32) operands, fp32 accumulation; the first layer's
+ * output is rounded to the operand type before the second product; the
+ * second layer's output enters the third as a bf16 hi/lo pair (bf16) or
+ * fp32; fp32 for the rest.
+ * Workspace: split-K partials of the first two layers and the first layer's
+ * output.  Limits: d, m1, m2 multiples of 8 (bf16) or 4 (fp32); m2 <= 2048;
+ * m3 <= 256.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    int32_t n_req;      /* B >= 0 */
+    int32_t d_model;    /* d >= 1 */
+    int32_t m1, m2, m3; /* hidden widths */
+    int32_t dtype;      /* star_dtype of hidden, w1, w2, w3 */
+    float   ema_alpha;  /* 0 disables smoothing; else in (0, 1] */
+    int32_t ema_init;
+    int32_t len_max;    /* >= 1 */
+    float   b4;         /* output bias */
+    void*   timing_events; /* NULL, or two hipEvent_t around the first layer's GEMM */
+} star_mlp4_params;
+
+size_t star_predict_mlp4_workspace_size(const star_mlp4_params* p);
+
+star_status star_predict_mlp4(const star_mlp4_params* p, const void* hidden, const void* w1,
+                              const float* b1, const void* w2, const float* b2, const void* w3,
+                              const float* b3, const float* w4, float* ema_state,
+                              float* expected_len, int32_t* rem_len, void* ws, size_t ws_bytes,
+                              void* stream);
+
+/* ------------------------------------------------------------------------
  * (b) Per-instance predicted load curves.
  *
  * Worker-side future-load simulation of Section 5.2's complexity analysis,

@@ -273,12 +273,15 @@ __device__ inline float apply_act(float x, int act) {
 
 // kS = number of split-K partial planes (compile time, so that all of a
 // thread's partial loads are issued before the first is consumed).
-template <bool kBF16, int kS>
+// kReg: the regression head's last two layers instead of the binned one
+// (the nb "bin logits" are the third layer's outputs, `bins` holds w4 and
+// phase 3 computes relu(z) . w4 + b4 in place of the softmax mean).
+template <bool kBF16, int kS, bool kReg = false>
 __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     const float* __restrict__ P, int B, int m, int nb, const float* __restrict__ b1,
     const void* __restrict__ w2, const float* __restrict__ b2, const float* __restrict__ bins,
     int act, float ema_alpha, int ema_init, float* __restrict__ ema_state,
-    float* __restrict__ expected, int32_t* __restrict__ rem_len, int len_max) {
+    float* __restrict__ expected, int32_t* __restrict__ rem_len, int len_max, float b4 = 0.0f) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -446,23 +449,33 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     for (int r = wid; r < HD_RB; r += HD_THREADS / 64) {
         const int gr = row0 + r;
         if (gr >= B) continue;
-        float zmax = -INFINITY;
-        for (int j = lane; j < nb; j += 64) zmax = fmaxf(zmax, z[r * nbpad + j]);
-        zmax = wave_max_f32(zmax);
-        float den = 0.0f, num = 0.0f;
+        float den = 1.0f, num = 0.0f;
+        if constexpr (kReg) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int j = lane + 64 * i;
-            if (j < nb) {
-                const float e = expf(z[r * nbpad + j] - zmax);
-                den += e;
-                num += e * binv[i];
+            for (int i = 0; i < 4; ++i) {
+                const int j = lane + 64 * i;
+                if (j < nb) num += fmaxf(z[r * nbpad + j], 0.0f) * binv[i];
             }
+            num = wave_sum_f32(num) + b4;
+        } else {
+            float zmax = -INFINITY;
+            for (int j = lane; j < nb; j += 64) zmax = fmaxf(zmax, z[r * nbpad + j]);
+            zmax = wave_max_f32(zmax);
+            den = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int j = lane + 64 * i;
+                if (j < nb) {
+                    const float e = expf(z[r * nbpad + j] - zmax);
+                    den += e;
+                    num += e * binv[i];
+                }
+            }
+            den = wave_sum_f32(den);
+            num = wave_sum_f32(num);
         }
-        den = wave_sum_f32(den);
-        num = wave_sum_f32(num);
         if (lane == 0) {
-            const float E = num / den;
+            const float E = kReg ? num : num / den;
             expected[gr] = E;
             float y = E;
             if (ema_alpha > 0.0f) {
@@ -483,23 +496,83 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// (f3) between the regression head's first two layers: fixed-order split-K
+// reduction, bias, ReLU, and the operand of the next product (bf16, round
+// to nearest even, or fp32)
+// ---------------------------------------------------------------------------
+constexpr int ACT_THREADS = 256;
+constexpr int ACT_BATCH = 4;      // float4 items per thread in flight
+
+template <int kS, bool kBF16>
+__global__ __launch_bounds__(ACT_THREADS) void act_kernel(const float* __restrict__ P,
+                                                          int64_t items, int m4,
+                                                          const float* __restrict__ bias,
+                                                          void* __restrict__ out) {
+    const float4* P4 = (const float4*)P;
+    for (int64_t base = (int64_t)blockIdx.x * ACT_THREADS * ACT_BATCH; base < items;
+         base += (int64_t)gridDim.x * ACT_THREADS * ACT_BATCH) {
+        float4 v[ACT_BATCH][kS];
+#pragma unroll
+        for (int i = 0; i < ACT_BATCH; ++i) {
+            const int64_t e = base + i * ACT_THREADS + threadIdx.x;
+            const int64_t o = e < items ? e : 0;
+#pragma unroll
+            for (int q = 0; q < kS; ++q) v[i][q] = P4[q * items + o];
+        }
+#pragma unroll
+        for (int i = 0; i < ACT_BATCH; ++i) {
+            const int64_t e = base + i * ACT_THREADS + threadIdx.x;
+            if (e >= items) break;
+            float4 sum = v[i][0];
+#pragma unroll
+            for (int q = 1; q < kS; ++q) {
+                sum.x += v[i][q].x; sum.y += v[i][q].y; sum.z += v[i][q].z; sum.w += v[i][q].w;
+            }
+            const int c = (int)(e % m4) * 4;
+            const float4 bv = bias ? *(const float4*)(bias + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float a0 = fmaxf(sum.x + bv.x, 0.0f), a1 = fmaxf(sum.y + bv.y, 0.0f);
+            const float a2 = fmaxf(sum.z + bv.z, 0.0f), a3 = fmaxf(sum.w + bv.w, 0.0f);
+            if constexpr (kBF16) {
+                ((uint2*)out)[e] = make_uint2(
+                    f32_to_bf16_rne(a0) | ((uint32_t)f32_to_bf16_rne(a1) << 16),
+                    f32_to_bf16_rne(a2) | ((uint32_t)f32_to_bf16_rne(a3) << 16));
+            } else {
+                ((float4*)out)[e] = make_float4(a0, a1, a2, a3);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-PredictPlan plan_predict(const star_predict_params& p) {
-    PredictPlan pl;
-    const int elem = p.dtype == STAR_BF16 ? 2 : 4;
+// Tiles and split-K factor of one product [M, K] x [N, K]^T: the split is a
+// power of two in [1, 16] that brings the workgroups near one per CU.
+GemmPlan plan_gemm(int M, int N, int K, int elem) {
+    GemmPlan g;
     const int bk = G1_KBYTES / elem;
-    pl.tiles_m = (int)ceil_div(p.n_req, G1_BM);
-    pl.tiles_n = (int)ceil_div(p.d_hidden, G1_BN);
-    pl.ktiles = (int)ceil_div(p.d_model, bk);
-    const int tiles = pl.tiles_m * pl.tiles_n;
+    g.tiles_m = (int)ceil_div(M, G1_BM);
+    g.tiles_n = (int)ceil_div(N, G1_BN);
+    g.ktiles = (int)ceil_div(K, bk);
+    const int tiles = g.tiles_m * g.tiles_n;
     int s = 1;
     if (tiles > 0 && tiles < 192) {
         int want = 256 / tiles;
         if (want > 16) want = 16;
-        if (want > pl.ktiles / 2) want = pl.ktiles / 2;
-        while (s * 2 <= want) s *= 2;          // a power of two in [1, 16]
+        if (want > g.ktiles / 2) want = g.ktiles / 2;
+        while (s * 2 <= want) s *= 2;
     }
+    g.splits = s;
+    return g;
+}
+
+PredictPlan plan_predict(const star_predict_params& p) {
+    PredictPlan pl;
+    const GemmPlan g = plan_gemm(p.n_req, p.d_hidden, p.d_model, p.dtype == STAR_BF16 ? 2 : 4);
+    pl.tiles_m = g.tiles_m;
+    pl.tiles_n = g.tiles_n;
+    pl.ktiles = g.ktiles;
+    const int s = g.splits;
     pl.splits = s;
     pl.partial_bytes = (size_t)s * (size_t)p.n_req * (size_t)p.d_hidden * sizeof(float);
     const int mpad = (p.d_hidden + 31) & ~31;
@@ -511,34 +584,35 @@ PredictPlan plan_predict(const star_predict_params& p) {
     return pl;
 }
 
-template <bool kBF16, int kS>
+template <bool kBF16, int kS, bool kReg>
 static hipError_t launch_head_s(const star_predict_params& p, const PredictPlan& pl, dim3 grid,
                                 const float* partials, const float* b1, const void* w2,
                                 const float* b2, const float* bins, float* ema_state,
-                                float* expected, int32_t* rem_len, hipStream_t stream) {
+                                float* expected, int32_t* rem_len, float b4, hipStream_t stream) {
     if (pl.head_lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)head_kernel<kBF16, kS>,
+        hipError_t e = hipFuncSetAttribute((const void*)head_kernel<kBF16, kS, kReg>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)pl.head_lds);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((head_kernel<kBF16, kS>), grid, dim3(HD_THREADS), pl.head_lds, stream,
-                       partials, p.n_req, p.d_hidden, p.n_bins, b1, w2, b2, bins, p.act,
-                       p.ema_alpha, p.ema_init, ema_state, expected, rem_len, p.len_max);
+    hipLaunchKernelGGL((head_kernel<kBF16, kS, kReg>), grid, dim3(HD_THREADS), pl.head_lds,
+                       stream, partials, p.n_req, p.d_hidden, p.n_bins, b1, w2, b2, bins, p.act,
+                       p.ema_alpha, p.ema_init, ema_state, expected, rem_len, p.len_max, b4);
     return hipGetLastError();
 }
 
-template <bool kBF16>
+template <bool kBF16, bool kReg = false>
 static hipError_t launch_head(const star_predict_params& p, const PredictPlan& pl, dim3 grid,
                               const float* partials, const float* b1, const void* w2,
                               const float* b2, const float* bins, float* ema_state,
-                              float* expected, int32_t* rem_len, hipStream_t stream) {
+                              float* expected, int32_t* rem_len, hipStream_t stream,
+                              float b4 = 0.0f) {
     switch (pl.splits) {
-        case 1: return launch_head_s<kBF16, 1>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
-        case 2: return launch_head_s<kBF16, 2>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
-        case 4: return launch_head_s<kBF16, 4>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
-        case 8: return launch_head_s<kBF16, 8>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
-        case 16: return launch_head_s<kBF16, 16>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
+        case 1: return launch_head_s<kBF16, 1, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
+        case 2: return launch_head_s<kBF16, 2, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
+        case 4: return launch_head_s<kBF16, 4, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
+        case 8: return launch_head_s<kBF16, 8, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
+        case 16: return launch_head_s<kBF16, 16, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -574,6 +648,104 @@ hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, c
                                                     ema_state, expected, rem_len, stream)
                                 : launch_head<false>(p, pl, g2, partials, b1, w2, b2, bins,
                                                      ema_state, expected, rem_len, stream);
+}
+
+// ---------------------------------------------------------------------------
+// (f3) the regression head: GEMM (layer 1) -> act -> GEMM (layer 2) -> head
+// (layers 3 and 4, EMA, integerisation)
+// ---------------------------------------------------------------------------
+// The head kernel's view of the last two layers: a "binned head" whose
+// input width is m2, whose nb = m3 outputs get ReLU and are dotted with w4.
+static star_predict_params head_view(const star_mlp4_params& p) {
+    star_predict_params h;
+    h.n_req = p.n_req;
+    h.d_model = p.m1;
+    h.d_hidden = p.m2;
+    h.n_bins = p.m3;
+    h.dtype = p.dtype;
+    h.act = STAR_ACT_RELU;
+    h.ema_alpha = p.ema_alpha;
+    h.ema_init = p.ema_init;
+    h.len_max = p.len_max;
+    h.timing_events = nullptr;
+    return h;
+}
+
+Mlp4Plan plan_mlp4(const star_mlp4_params& p) {
+    Mlp4Plan pl;
+    const int elem = p.dtype == STAR_BF16 ? 2 : 4;
+    pl.g1 = plan_gemm(p.n_req, p.m1, p.d_model, elem);
+    pl.head = plan_predict(head_view(p));          // layer 2 and the head
+    size_t off = 0;
+    pl.p1_off = off;
+    off += align_up((size_t)pl.g1.splits * p.n_req * p.m1 * sizeof(float), 256);
+    pl.a1_off = off;
+    off += align_up((size_t)p.n_req * p.m1 * elem, 256);
+    pl.p2_off = off;
+    off += align_up(pl.head.partial_bytes, 256);
+    pl.total = off;
+    return pl;
+}
+
+template <bool kBF16>
+static hipError_t launch_act(int splits, dim3 grid, const float* P, int64_t items, int m4,
+                             const float* bias, void* out, hipStream_t stream) {
+    switch (splits) {
+        case 1: hipLaunchKernelGGL((act_kernel<1, kBF16>), grid, dim3(ACT_THREADS), 0, stream, P, items, m4, bias, out); break;
+        case 2: hipLaunchKernelGGL((act_kernel<2, kBF16>), grid, dim3(ACT_THREADS), 0, stream, P, items, m4, bias, out); break;
+        case 4: hipLaunchKernelGGL((act_kernel<4, kBF16>), grid, dim3(ACT_THREADS), 0, stream, P, items, m4, bias, out); break;
+        case 8: hipLaunchKernelGGL((act_kernel<8, kBF16>), grid, dim3(ACT_THREADS), 0, stream, P, items, m4, bias, out); break;
+        case 16: hipLaunchKernelGGL((act_kernel<16, kBF16>), grid, dim3(ACT_THREADS), 0, stream, P, items, m4, bias, out); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_mlp4(const star_mlp4_params& p, const Mlp4Plan& pl, const void* hidden,
+                       const void* w1, const float* b1, const void* w2, const float* b2,
+                       const void* w3, const float* b3, const float* w4, float* ema_state,
+                       float* expected, int32_t* rem_len, char* ws, hipStream_t stream) {
+    if (p.n_req == 0) return hipSuccess;
+    const bool bf = p.dtype == STAR_BF16;
+    float* P1 = (float*)(ws + pl.p1_off);
+    void* A1 = ws + pl.a1_off;
+    float* P2 = (float*)(ws + pl.p2_off);
+    hipEvent_t* ev = (hipEvent_t*)p.timing_events;
+    hipError_t e;
+    if (ev && (e = hipEventRecord(ev[0], stream)) != hipSuccess) return e;
+    const dim3 g1(pl.g1.tiles_m * pl.g1.tiles_n * pl.g1.splits);
+    if (bf)
+        hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES>), g1, dim3(G1_THREADS), 0, stream,
+                           (const char*)hidden, (const char*)w1, P1, p.n_req, p.m1, p.d_model,
+                           pl.g1.splits, pl.g1.tiles_n, pl.g1.ktiles);
+    else
+        hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES>), g1, dim3(G1_THREADS), 0, stream,
+                           (const char*)hidden, (const char*)w1, P1, p.n_req, p.m1, p.d_model,
+                           pl.g1.splits, pl.g1.tiles_n, pl.g1.ktiles);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ev && (e = hipEventRecord(ev[1], stream)) != hipSuccess) return e;
+    const int64_t items = (int64_t)p.n_req * p.m1 / 4;
+    int64_t ab = ceil_div(items, (int64_t)ACT_THREADS * ACT_BATCH);
+    const dim3 ga((unsigned)(ab > 2048 ? 2048 : ab));
+    e = bf ? launch_act<true>(pl.g1.splits, ga, P1, items, p.m1 / 4, b1, A1, stream)
+           : launch_act<false>(pl.g1.splits, ga, P1, items, p.m1 / 4, b1, A1, stream);
+    if (e != hipSuccess) return e;
+    const star_predict_params h = head_view(p);
+    const dim3 g2(pl.head.tiles_m * pl.head.tiles_n * pl.head.splits);
+    if (bf)
+        hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES>), g2, dim3(G1_THREADS), 0, stream,
+                           (const char*)A1, (const char*)w2, P2, p.n_req, p.m2, p.m1,
+                           pl.head.splits, pl.head.tiles_n, pl.head.ktiles);
+    else
+        hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES>), g2, dim3(G1_THREADS), 0, stream,
+                           (const char*)A1, (const char*)w2, P2, p.n_req, p.m2, p.m1,
+                           pl.head.splits, pl.head.tiles_n, pl.head.ktiles);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const dim3 gh((unsigned)ceil_div(p.n_req, HD_RB));
+    return bf ? launch_head<true, true>(h, pl.head, gh, P2, b2, w3, b3, w4, ema_state, expected,
+                                        rem_len, stream, p.b4)
+              : launch_head<false, true>(h, pl.head, gh, P2, b2, w3, b3, w4, ema_state, expected,
+                                         rem_len, stream, p.b4);
 }
 
 }  // namespace star

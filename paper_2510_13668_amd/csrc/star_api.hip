@@ -111,6 +111,52 @@ STAR_API star_status star_predict(const star_predict_params* p, const void* hidd
 }
 
 // ---------------------------------------------------------------------------
+// regression head
+// ---------------------------------------------------------------------------
+static star_status check_mlp4_params(const star_mlp4_params* p) {
+    if (!p) return STAR_ERR_INVALID_ARG;
+    if (p->n_req < 0 || p->d_model < 1 || p->m1 < 1 || p->m2 < 1 || p->m3 < 1 || p->len_max < 1)
+        return STAR_ERR_INVALID_ARG;
+    if (p->dtype != STAR_F32 && p->dtype != STAR_BF16) return STAR_ERR_INVALID_ARG;
+    if (!(p->ema_alpha >= 0.0f && p->ema_alpha <= 1.0f)) return STAR_ERR_INVALID_ARG;
+    if (p->ema_init != 0 && p->ema_init != 1) return STAR_ERR_INVALID_ARG;
+    if (!(p->b4 == p->b4) || p->b4 > 3.0e38f || p->b4 < -3.0e38f) return STAR_ERR_INVALID_ARG;
+    const int vec = p->dtype == STAR_BF16 ? 8 : 4;
+    if (p->d_model % vec || p->m1 % vec || p->m2 % vec) return STAR_ERR_UNSUPPORTED;
+    if (p->m2 > 2048 || p->m3 > 256) return STAR_ERR_UNSUPPORTED;
+    return STAR_OK;
+}
+
+STAR_API size_t star_predict_mlp4_workspace_size(const star_mlp4_params* p) {
+    if (check_mlp4_params(p) != STAR_OK) return 0;
+    return STAR_WS_HEADER_BYTES + plan_mlp4(*p).total;
+}
+
+STAR_API star_status star_predict_mlp4(const star_mlp4_params* p, const void* hidden,
+                                       const void* w1, const float* b1, const void* w2,
+                                       const float* b2, const void* w3, const float* b3,
+                                       const float* w4, float* ema_state, float* expected_len,
+                                       int32_t* rem_len, void* ws, size_t ws_bytes,
+                                       void* stream) {
+    star_status st = check_mlp4_params(p);
+    if (st != STAR_OK) return st;
+    if (p->n_req > 0) {
+        if (!hidden || !w1 || !w2 || !w3 || !w4 || !expected_len) return STAR_ERR_INVALID_ARG;
+        if (p->ema_alpha > 0.0f && !ema_state) return STAR_ERR_INVALID_ARG;
+        if (!aligned(hidden, 16) || !aligned(w1, 16) || !aligned(w2, 16) || !aligned(w3, 16) ||
+            !aligned(b1, 16))
+            return STAR_ERR_UNSUPPORTED;
+    }
+    const Mlp4Plan pl = plan_mlp4(*p);
+    st = check_ws(ws, ws_bytes, STAR_WS_HEADER_BYTES + pl.total);
+    if (st != STAR_OK) return st;
+    hipError_t e = launch_mlp4(*p, pl, hidden, w1, b1, w2, b2, w3, b3, w4, ema_state,
+                               expected_len, rem_len, (char*)ws + STAR_WS_HEADER_BYTES,
+                               (hipStream_t)stream);
+    return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
 // load projection
 // ---------------------------------------------------------------------------
 STAR_API size_t star_project_load_workspace_size(const star_load_params* p) {

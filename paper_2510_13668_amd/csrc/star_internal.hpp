@@ -20,6 +20,22 @@ hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, c
                           const float* bins, float* ema_state, float* expected, int32_t* rem_len,
                           float* partials, hipStream_t stream);
 
+struct GemmPlan {
+    int tiles_m = 0, tiles_n = 0, ktiles = 0, splits = 1;
+};
+GemmPlan plan_gemm(int M, int N, int K, int elem);
+
+struct Mlp4Plan {
+    GemmPlan g1;          // layer 1
+    PredictPlan head;     // layer 2 (its split-K partials) and the last two layers
+    size_t p1_off = 0, a1_off = 0, p2_off = 0, total = 0;
+};
+Mlp4Plan plan_mlp4(const star_mlp4_params& p);
+hipError_t launch_mlp4(const star_mlp4_params& p, const Mlp4Plan& pl, const void* hidden,
+                       const void* w1, const float* b1, const void* w2, const float* b2,
+                       const void* w3, const float* b3, const float* w4, float* ema_state,
+                       float* expected, int32_t* rem_len, char* ws, hipStream_t stream);
+
 struct LoadPlan {
     int chunk = 0;       // buckets per workgroup
     int n_chunks = 0;

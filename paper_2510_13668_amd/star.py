@@ -33,6 +33,12 @@ class PredictParams(ctypes.Structure):
                 ("ema_init", _i32), ("len_max", _i32), ("timing_events", _P)]
 
 
+class Mlp4Params(ctypes.Structure):
+    _fields_ = [("n_req", _i32), ("d_model", _i32), ("m1", _i32), ("m2", _i32), ("m3", _i32),
+                ("dtype", _i32), ("ema_alpha", ctypes.c_float), ("ema_init", _i32),
+                ("len_max", _i32), ("b4", ctypes.c_float), ("timing_events", _P)]
+
+
 class LoadParams(ctypes.Structure):
     _fields_ = [("n_req", _i32), ("n_inst", _i32), ("bucket", _i32), ("n_buckets", _i32)]
 
@@ -94,6 +100,11 @@ def lib():
         L.star_plan_migrations.restype = ctypes.c_int
         L.star_plan_migrations.argtypes = ([ctypes.POINTER(PlanParams)] + [_P] * 8 +
                                            [ctypes.c_size_t, _P])
+        L.star_predict_mlp4_workspace_size.restype = ctypes.c_size_t
+        L.star_predict_mlp4_workspace_size.argtypes = [ctypes.POINTER(Mlp4Params)]
+        L.star_predict_mlp4.restype = ctypes.c_int
+        L.star_predict_mlp4.argtypes = ([ctypes.POINTER(Mlp4Params)] + [_P] * 12 +
+                                        [ctypes.c_size_t, _P])
         L.star_workspace_init.restype = ctypes.c_int
         L.star_workspace_init.argtypes = [_P, ctypes.c_size_t, _P]
         L.star_read_device_error.restype = ctypes.c_int
@@ -259,3 +270,25 @@ def plan_migrations(p: PlanParams, cur_len, rem_len, inst_of, load, beta, moves,
     _check("star_plan_migrations", lib().star_plan_migrations(
         ctypes.byref(p), _ptr(cur_len), _ptr(rem_len), _ptr(inst_of), _ptr(load), _ptr(beta),
         _ptr(moves), _ptr(n_moves), ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# the paper's regression head
+# ---------------------------------------------------------------------------
+def mlp4_params(n_req, d_model, m1, m2, m3, dtype, ema_alpha=0.0, ema_init=False,
+                len_max=1 << 30, b4=0.0, timing_events=None) -> Mlp4Params:
+    return Mlp4Params(n_req, d_model, m1, m2, m3, dtype, ema_alpha, int(bool(ema_init)), len_max,
+                      b4, timing_events)
+
+
+def predict_mlp4_workspace_size(p: Mlp4Params) -> int:
+    return int(lib().star_predict_mlp4_workspace_size(ctypes.byref(p)))
+
+
+def predict_mlp4(p: Mlp4Params, hidden, w1, b1, w2, b2, w3, b3, w4, ema_state, expected_len,
+                 rem_len, ws: Workspace, stream=None):
+    _dev(hidden, w1, b1, w2, b2, w3, b3, w4, ema_state, expected_len, rem_len)
+    _check("star_predict_mlp4", lib().star_predict_mlp4(
+        ctypes.byref(p), _ptr(hidden), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(w3), _ptr(b3),
+        _ptr(w4), _ptr(ema_state), _ptr(expected_len), _ptr(rem_len), ctypes.c_void_p(ws.ptr),
+        ws.nbytes, _stream(stream)))

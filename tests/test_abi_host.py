@@ -166,6 +166,34 @@ def test_plan_validation(L):
     assert star.plan_workspace_size(star.plan_params(1 << 18, 8, 1 << 10, 1 << 20, 1)) == 0
 
 
+def test_mlp4_validation(L):
+    f = FAKE
+    mp = star.mlp4_params(1024, 3584, 2048, 512, 64, star.BF16)
+    need = star.predict_mlp4_workspace_size(mp)
+    # split-K partials of both layers plus the first layer's bf16 output
+    assert need >= 256 + 1024 * 2048 * (4 + 2) + 1024 * 512 * 4
+    args = [f] * 11           # hidden, w1, b1, w2, b2, w3, b3, w4, ema, expected, rem
+    args[2] = args[4] = args[6] = None
+    assert L.star_predict_mlp4(ctypes.byref(mp), *args, f, need - 1, None) == -4
+    bad = list(args)
+    bad[7] = None             # w4
+    assert L.star_predict_mlp4(ctypes.byref(mp), *bad, f, need, None) == -1
+    for kw in (dict(m2=4096), dict(m3=300), dict(d_model=3583)):
+        base = dict(n_req=8, d_model=3584, m1=2048, m2=512, m3=64, dtype=star.BF16)
+        base.update(kw)
+        assert L.star_predict_mlp4(ctypes.byref(star.mlp4_params(**base)), *args, f, 1 << 30,
+                                   None) == -2, kw
+    assert L.star_predict_mlp4(ctypes.byref(star.mlp4_params(8, 64, 64, 64, 8, 7)), *args, f,
+                               1 << 30, None) == -1
+    assert L.star_predict_mlp4(ctypes.byref(star.mlp4_params(8, 64, 64, 64, 8, star.BF16,
+                                                             ema_alpha=1.5)), *args, f,
+                               1 << 30, None) == -1
+    odd = ctypes.c_void_p((1 << 20) + 4)
+    bad = list(args)
+    bad[2] = odd              # b1 not 16-byte aligned
+    assert L.star_predict_mlp4(ctypes.byref(mp), *bad, f, need, None) == -2
+
+
 def test_read_device_error_rejects_bad_args(L):
     code = ctypes.c_int32(0)
     assert L.star_read_device_error(FAKE, None, None) == -1
