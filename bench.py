@@ -13,6 +13,12 @@ microseconds per round.
 Prints ONE JSON line.  Usage:
     python bench.py [--gpus 1] [--steps 200] [--warmup 10] [--mode graph|eager]
 
+``--path mlp4`` measures the paper's own predictor, the 4-layer ReLU
+regression head 3584 -> 2048 -> 512 -> 64 -> 1 (random-initialised weights of
+that shape): per step one star_predict_mlp4 call on a 1024-request batch of
+bf16 hidden states (AR(1) over 16 staged decode steps, EMA 0.2), plus the
+latency of one call at batch 1 and 10.
+
 ``--path plan [--workload NAME] [--moves M]`` measures Algorithm 1 end to
 end: per step, the placement is restored (a quarter of the requests crowded
 onto one instance), then star_project_load -> star_plan_migrations with up
@@ -50,9 +56,10 @@ def _parse():
                     help="which timing gives `value` (the other is reported beside it)")
     ap.add_argument("--cpu-rounds", type=int, default=20,
                     help="rounds of the CPU oracle timed for the baseline (0 = skip)")
-    ap.add_argument("--path", choices=("round", "variance", "plan"), default="round",
+    ap.add_argument("--path", choices=("round", "variance", "plan", "mlp4"), default="round",
                     help="round: the full rescheduling round; variance: projection + "
-                         "variance-gain scoring; plan: Algorithm 1 repeated")
+                         "variance-gain scoring; plan: Algorithm 1 repeated; mlp4: the paper's "
+                         "4-layer regression head")
     ap.add_argument("--moves", type=int, default=16, help="max_moves of --path plan")
     ap.add_argument("--workload", default="rebalance_scan",
                     help="workload of --path variance")
@@ -427,6 +434,111 @@ def bench_plan(args):
     print(json.dumps(out), flush=True)
 
 
+def bench_mlp4(args):
+    import torch
+    from paper_2510_13668_amd import star, synth
+    import oracle
+
+    dev = "cuda"
+    B, S = 1024, 16
+    d, m1, m2, m3 = synth.MLP4_DIMS
+    x = synth.make_mlp4(B, dtype=synth.BF16, seed=0, steps=S)
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    hid = bf(x.hidden)
+    w1, w2, w3 = bf(x.w1), bf(x.w2), bf(x.w3)
+    w4 = torch.from_numpy(x.w4).to(dev)
+    ema = torch.zeros(B, dtype=torch.float32, device=dev)
+    y = torch.empty(B, dtype=torch.float32, device=dev)
+    rem = torch.empty(B, dtype=torch.int32, device=dev)
+    stream = torch.cuda.Stream()
+
+    def params(n, init=False, ev=None):
+        return star.mlp4_params(n, d, m1, m2, m3, synth.BF16, 0.2, init, 32768, x.b4, ev)
+
+    ws = star.Workspace(star.predict_mlp4_workspace_size(params(B)))
+    star.predict_mlp4(params(B, True), hid[0], w1, None, w2, None, w3, None, w4, ema, y, rem, ws,
+                      stream)
+    torch.cuda.synchronize()
+
+    def timed(fn, steps):
+        for i in range(args.warmup):
+            fn(i)
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for i in range(steps):
+            fn(args.warmup + i)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / steps
+
+    pp = params(B)
+    ms_step = timed(lambda i: star.predict_mlp4(pp, hid[i % S], w1, None, w2, None, w3, None, w4,
+                                                ema, y, rem, ws, stream), args.steps)
+    lat = {}
+    for nb in (1, 10):
+        p_small = params(nb)
+        lat[nb] = timed(lambda i: star.predict_mlp4(p_small, hid[i % S, :nb], w1, None, w2, None,
+                                                    w3, None, w4, ema[:nb], y[:nb], rem[:nb], ws,
+                                                    stream), args.steps) * 1e3
+
+    # the first layer's GEMM, HIP events recorded by the library around it
+    he = HipEvents()
+    evs = he.create(2 * args.steps)
+    arrs = [(ctypes.c_void_p * 2)(evs[2 * i].value, evs[2 * i + 1].value)
+            for i in range(args.steps)]
+    pps = [params(B, False, ctypes.cast(a, ctypes.c_void_p)) for a in arrs]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        star.predict_mlp4(pps[i], hid[i % S], w1, None, w2, None, w3, None, w4, ema, y, rem, ws,
+                          stream)
+    torch.cuda.synchronize()
+    g_s = float(np.mean([he.elapsed_ms(evs[2 * i], evs[2 * i + 1])
+                         for i in range(args.steps)])) * 1e-3
+    he.destroy(evs)
+    flops = 2.0 * B * d * m1
+    achieved = flops / g_s / 1e12
+
+    out = {
+        "metric": "requests predicted/sec by the paper's 4-layer regression head "
+                  "(3584->2048->512->64->1, bf16) at a 1024-request batch",
+        "value": B / (ms_step * 1e-3),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "regression head of the paper's shape, random-initialised weights, "
+                               "1024 requests, bf16 hidden [1024,3584] AR(1) over 16 staged steps, "
+                               "EMA 0.2",
+                   "n_req": B, "dims": [d, m1, m2, m3]},
+        "latency_us": {"batch_1": lat[1], "batch_10": lat[10]},
+        "roofline": {"kernel": "gemm1_splitk_kernel (layer 1, H[1024,3584] x W1[2048,3584]^T)",
+                     "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "avg_kernel_us": g_s * 1e6, "algorithmic_flop": flops},
+    }
+    if args.cpu_rounds > 0:
+        steps = 8
+        st = np.zeros(B, np.float64)
+        t0 = time.perf_counter()
+        for t in range(steps):
+            oracle.predict_mlp4(x.hidden[t], x.w1, x.w2, x.w3, x.w4, dtype=synth.BF16, b4=x.b4,
+                                ema_alpha=0.2, ema_init=(t == 0), ema_state=st, len_max=32768)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": B * steps / dt, "unit": "requests/s",
+                               "cores": oracle.threads(), "kind": "oracle",
+                               "sample": f"all {B} rows of the first {steps} decode steps, fp64 "
+                                         f"triple loops; {dt:.2f} s"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = _parse()
     if args.copy_calibration:
@@ -442,6 +554,9 @@ def main():
         return
     if args.path == "plan":
         bench_plan(args)
+        return
+    if args.path == "mlp4":
+        bench_mlp4(args)
         return
 
     import torch
