@@ -11,7 +11,7 @@ requests predicted + scored per second (= 1024 / seconds per round) and
 microseconds per round.
 
 Prints ONE JSON line.  Usage:
-    python bench.py [--gpus 1] [--steps 200] [--warmup 10] [--mode graph|eager]
+    python bench.py [--gpus 1] [--steps 200] [--warmup 40] [--mode graph_pipelined|...]
 
 ``--path mlp4`` measures the paper's own predictor, the 4-layer ReLU
 regression head 3584 -> 2048 -> 512 -> 64 -> 1 (random-initialised weights of
@@ -56,9 +56,15 @@ def _parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--mode", choices=("graph", "eager"), default="eager",
-                    help="which timing gives `value` (the other is reported beside it)")
+    ap.add_argument("--warmup", type=int, default=40)
+    ap.add_argument("--mode", choices=("graph_pipelined", "pipelined", "eager", "graph"),
+                    default="graph_pipelined",
+                    help="which timing gives `value` (the others are reported beside it): "
+                         "pipelined = prediction of the next round on one stream while the "
+                         "current round is projected and scored on a second (eagerly "
+                         "launched); graph_pipelined = the same, 40 rounds per captured HIP "
+                         "graph; eager = one stream, round after round; graph = one captured "
+                         "graph per round")
     ap.add_argument("--cpu-rounds", type=int, default=20,
                     help="rounds of the CPU oracle timed for the baseline (0 = skip)")
     ap.add_argument("--path", choices=("round", "variance", "plan", "mlp4", "sim"),
@@ -704,7 +710,109 @@ def main():
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) / args.steps
 
+    # Pipelined rounds: round i's prediction needs only round i-1's EMA state,
+    # so it runs on `stream` while round i-1 is projected and scored on
+    # `sched`.  Per-round outputs are double-buffered; an event keeps a
+    # buffer from being overwritten before its scheduling has finished.
+    sched = torch.cuda.Stream()
+    NSLOT = 2
+    slot_buf = []
+    for _ in range(NSLOT):
+        slot_buf.append(dict(
+            expected=torch.empty(N, dtype=torch.float32, device=dev),
+            rem=torch.empty(N, dtype=torch.int32, device=dev),
+            load=torch.empty((n, K), dtype=torch.int64, device=dev),
+            scores=torch.empty((N, n), dtype=torch.int64, device=dev),
+            best_t=torch.empty(N, dtype=torch.int32, device=dev),
+            best_s=torch.empty(N, dtype=torch.int64, device=dev),
+            tr=torch.empty(top_k, dtype=torch.int32, device=dev),
+            tt=torch.empty(top_k, dtype=torch.int32, device=dev),
+            ts=torch.empty(top_k, dtype=torch.int64, device=dev)))
+    ev_pred = [torch.cuda.Event() for _ in range(NSLOT)]
+    ev_done = [torch.cuda.Event() for _ in range(NSLOT)]
+    used = [False] * NSLOT
+
+    def pipelined_round(i):
+        step = (i + 1) % S
+        k = i % NSLOT
+        sb = slot_buf[k]
+        if used[k]:
+            stream.wait_event(ev_done[k])
+        star.predict(pp, hid[step], w1, None, w2, None, bins, ema, sb["expected"], sb["rem"],
+                     ws_p, stream)
+        ev_pred[k].record(stream)
+        sched.wait_event(ev_pred[k])
+        star.project_load(lp, cur_steps[step], sb["rem"], inst, sb["load"], ws_l, sched)
+        star.score_migrations(sp, cur_steps[step], sb["rem"], inst, sb["load"], sb["scores"],
+                              sb["best_t"], sb["best_s"], sb["tr"], sb["tt"], sb["ts"], ws_s,
+                              sched)
+        ev_done[k].record(sched)
+        used[k] = True
+
+    def timed_pipelined():
+        for i in range(args.warmup):
+            pipelined_round(i)
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for i in range(args.steps):
+            pipelined_round(args.warmup + i)
+        for k in range(NSLOT):
+            stream.wait_event(ev_done[k])
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / args.steps
+
+    # The same pipeline captured in HIP graphs of CHUNK rounds each (the two
+    # streams fork and join inside the capture), so that the host launches
+    # one graph per CHUNK rounds instead of five kernels and four event
+    # operations per round.
+    CHUNK = 40
+    chunk_graphs = []
+    torch.cuda.synchronize()
+    for c0 in range(0, S, CHUNK):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            sched.wait_stream(stream)
+            for j in range(CHUNK):
+                step = (c0 + j) % S
+                k = j % NSLOT
+                sb = slot_buf[k]
+                if j >= NSLOT:
+                    stream.wait_event(ev_done[k])
+                star.predict(pp, hid[step], w1, None, w2, None, bins, ema, sb["expected"],
+                             sb["rem"], ws_p, stream)
+                ev_pred[k].record(stream)
+                sched.wait_event(ev_pred[k])
+                star.project_load(lp, cur_steps[step], sb["rem"], inst, sb["load"], ws_l, sched)
+                star.score_migrations(sp, cur_steps[step], sb["rem"], inst, sb["load"],
+                                      sb["scores"], sb["best_t"], sb["best_s"], sb["tr"],
+                                      sb["tt"], sb["ts"], ws_s, sched)
+                ev_done[k].record(sched)
+            stream.wait_stream(sched)
+        chunk_graphs.append(g)
+    torch.cuda.synchronize()
+
+    def timed_graph_pipelined():
+        reps = max(1, args.steps // CHUNK)
+        for i in range(max(1, args.warmup // CHUNK)):
+            with torch.cuda.stream(stream):
+                chunk_graphs[i % len(chunk_graphs)].replay()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        with torch.cuda.stream(stream):
+            for i in range(reps):
+                chunk_graphs[i % len(chunk_graphs)].replay()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / (reps * CHUNK)
+
     ms_mode = {m: timed(m) for m in ("eager", "graph")}
+    ms_mode["pipelined"] = timed_pipelined()
+    ms_mode["graph_pipelined"] = timed_graph_pipelined()
     ms_step = ms_mode[args.mode]
 
     # Dominant kernel (first-layer GEMM) timed with HIP events recorded by the
@@ -744,7 +852,9 @@ def main():
                                "top-256",
                    "n_req": N, "d_model": d, "d_hidden": m, "n_bins": nb, "n_inst": n,
                    "horizon": wl.horizon, "bucket": b, "top_k": top_k,
-                   "mode": args.mode + " (one stream, inputs resident in HBM)"},
+                   "mode": args.mode + " (inputs resident in HBM)"},
+        "us_per_round_pipelined": ms_mode["pipelined"] * 1e3,
+        "us_per_round_graph_pipelined": ms_mode["graph_pipelined"] * 1e3,
         "us_per_round_eager": ms_mode["eager"] * 1e3,
         "us_per_round_graph": ms_mode["graph"] * 1e3,
         "roofline": {"kernel": "gemm1_splitk_kernel (bf16 MFMA, H[1024,4096] x W1[512,4096]^T)",

@@ -254,3 +254,76 @@ def test_graph_replay_matches_eager():
         assert_round_equal(got, want)
         np.testing.assert_array_equal(pr.ema.cpu().numpy(), want_ema)
         _ = torch.ones(1000, device="cuda").sum().item()    # unrelated eager work between replays
+
+
+def test_pipelined_graph_rounds_match_eager():
+    """Rounds pipelined on two streams: round i is predicted on one stream
+    while round i-1 is projected and scored on a second.  The per-round
+    outputs alternate between two buffers, and events order the rounds.
+    The whole chunk is captured as one HIP graph, as the benchmark runs it.
+    Every replay (with eager work and synchronisations between replays)
+    must leave the last two rounds' outputs and the EMA state equal to six
+    eager rounds run one after another."""
+    wl = synth.WORKLOADS["continuous"]
+    R = 6
+    x = synth.make_inputs(wl, steps=R + 1)
+    hid = to_dev(x.hidden, True)
+    N = wl.n_req
+    pr = Predictor(x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act, n_req=N,
+                   len_max=wl.len_max, ema_alpha=wl.ema_alpha)
+    inst = to_dev(x.inst_of)
+    curs = [to_dev((x.cur_len + s).astype(np.int32)) for s in range(R + 1)]
+
+    # eager reference: step 0 initialises the EMA, then rounds on steps 1..R
+    pr.run(hid[0], ema_init=True)
+    ema0 = pr.ema.clone()
+    ref = Rescheduler(N, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k)
+    want = []
+    for j in range(R):
+        pr.run(hid[j + 1])
+        ref.run(curs[j + 1], pr.rem, inst)
+        want.append(ref.result())
+    want_ema = pr.ema.cpu().numpy().copy()
+
+    P, S2 = torch.cuda.Stream(), torch.cuda.Stream()
+    slots = [Rescheduler(N, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k) for _ in range(2)]
+    rems = [torch.empty(N, dtype=torch.int32, device="cuda") for _ in range(2)]
+    exps = [torch.empty(N, dtype=torch.float32, device="cuda") for _ in range(2)]
+    ev_pred = [torch.cuda.Event() for _ in range(2)]
+    ev_done = [torch.cuda.Event() for _ in range(2)]
+    pp = pr.params(False)
+
+    def chunk():
+        S2.wait_stream(P)
+        for j in range(R):
+            k = j % 2
+            if j >= 2:
+                P.wait_event(ev_done[k])
+            star.predict(pp, hid[j + 1], pr.w1, pr.b1, pr.w2, pr.b2, pr.bins, pr.ema, exps[k],
+                         rems[k], pr.ws, P)
+            ev_pred[k].record(P)
+            S2.wait_event(ev_pred[k])
+            slots[k].run(curs[j + 1], rems[k], inst, stream=S2)
+            ev_done[k].record(S2)
+        P.wait_stream(S2)
+
+    torch.cuda.synchronize()
+    with torch.cuda.stream(P):
+        pr.ema.copy_(ema0)
+    chunk()                      # warm-up, eager, on the capture streams
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=P):
+        chunk()
+    for rep in range(3):
+        pr.ema.copy_(ema0)
+        for sl in slots:
+            sl.load.fill_(-7)
+            sl.best_target.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for j in (R - 2, R - 1):
+            assert_round_equal(slots[j % 2].result(), want[j])
+        np.testing.assert_array_equal(pr.ema.cpu().numpy(), want_ema)
+        _ = torch.ones(1000, device="cuda").sum().item()    # unrelated eager work between replays
