@@ -24,16 +24,9 @@ namespace star {
 // ---------------------------------------------------------------------------
 // GEMM1
 // ---------------------------------------------------------------------------
-constexpr int G1_BM = 128;
-constexpr int G1_BN = 128;
 constexpr int G1_KBYTES = 128;                 // bytes of K per LDS row
 constexpr int G1_ROW = G1_KBYTES + 16;         // padded LDS row (bytes)
-constexpr int G1_TILE = G1_BM * G1_ROW;        // one operand tile (bytes)
-constexpr int G1_THREADS = 256;
 constexpr int G1_STAGES = 3;                   // K-tiles of loads in flight ahead of the multiply
-constexpr int G1_OUT_ROW = G1_BN + 8;          // floats per LDS row of the output tile
-constexpr int G1_CHUNKS = G1_BM * G1_KBYTES / 16 / G1_THREADS;   // 16-byte chunks per thread per operand
-
 
 template <int kElemBytes> struct G1Elem;
 template <> struct G1Elem<2> { static constexpr int BK = 64; };   // bf16
@@ -48,18 +41,34 @@ __device__ inline int xcd_logical_block(int bid, int nblk) {
     return x * q + (x < r ? x : r) + bid / 8;
 }
 
-// One K-tile of both operands staged in registers: 4 x 16 bytes per thread
-// per operand (plain members, so the stages stay in VGPRs).
-struct G1Stage {
-    uint4 a0, a1, a2, a3, b0, b1, b2, b3;
+// Tile shape of the split-K product: BM x BN outputs per workgroup, WM x WN
+// waves, each wave a (BM/WM) x (BN/WN) slab of 32 x 32 matrix-core blocks.
+template <int kBM, int kBN, int kWM, int kWN>
+struct G1Shape {
+    static constexpr int BM = kBM, BN = kBN, WM = kWM, WN = kWN;
+    static constexpr int THREADS = 64 * WM * WN;
+    static constexpr int MI = BM / WM / 32, NJ = BN / WN / 32;
+    static constexpr int CA = BM * G1_KBYTES / 16 / THREADS;   // 16-byte chunks per thread, A
+    static constexpr int CB = BN * G1_KBYTES / 16 / THREADS;   // ... and W
+    static constexpr int LDS_A = BM * G1_ROW, LDS_B = BN * G1_ROW;
+    static constexpr int OUT_ROW = BN + 8;     // floats per LDS row of the output tile
+    static_assert(MI >= 1 && NJ >= 1 && CA >= 1 && CB >= 1, "shape");
+    static_assert(BM * OUT_ROW * 4 <= 2 * (LDS_A + LDS_B), "output tile fits the operand buffers");
 };
-static_assert(G1_CHUNKS == 4, "G1Stage holds four 16-byte chunks per operand");
-static_assert(G1_BM * G1_OUT_ROW * 4 <= 2 * 2 * G1_TILE, "output tile fits the operand buffers");
+using G1Big = G1Shape<128, 128, 4, 2>;     // 8 waves, 32 x 64 slabs
+using G1Small = G1Shape<64, 64, 2, 2>;     // 4 waves, 32 x 32 slabs
+
+// One K-tile of both operands staged in registers (constant indices only,
+// so the stages stay in VGPRs).
+template <class SH>
+struct G1Stage {
+    uint4 a[SH::CA], b[SH::CB];
+};
 
 struct G1Ctx {
     const char* A;
     const char* W;
-    int M, N, tm, tn, tid;
+    int M, N, tm, tn, tid, threads, bm, bn;
     int64_t row_bytes;
 };
 
@@ -68,52 +77,50 @@ struct G1Ctx {
 // out-of-range values are zeroed when they are written to LDS.
 __device__ __forceinline__ uint4 g1_load(const G1Ctx& c, const char* base, int rows, int row0,
                                          int p, int64_t kb) {
-    const int ch = c.tid + p * G1_THREADS;
+    const int ch = c.tid + p * c.threads;
     const int row = row0 + (ch >> 3);
     const int64_t off = kb + (ch & 7) * 16;
     const int64_t ko = off < c.row_bytes ? off : 0;
     return *(const uint4*)(base + (int64_t)(row < rows ? row : rows - 1) * c.row_bytes + ko);
 }
 
-__device__ __forceinline__ void g1_load_stage(const G1Ctx& c, int kt, G1Stage& s) {
+template <class SH>
+__device__ __forceinline__ void g1_load_stage(const G1Ctx& c, int kt, G1Stage<SH>& s) {
     const int64_t kb = (int64_t)kt * G1_KBYTES;
-    const int ra = c.tm * G1_BM, rb = c.tn * G1_BN;
-    s.a0 = g1_load(c, c.A, c.M, ra, 0, kb);
-    s.b0 = g1_load(c, c.W, c.N, rb, 0, kb);
-    s.a1 = g1_load(c, c.A, c.M, ra, 1, kb);
-    s.b1 = g1_load(c, c.W, c.N, rb, 1, kb);
-    s.a2 = g1_load(c, c.A, c.M, ra, 2, kb);
-    s.b2 = g1_load(c, c.W, c.N, rb, 2, kb);
-    s.a3 = g1_load(c, c.A, c.M, ra, 3, kb);
-    s.b3 = g1_load(c, c.W, c.N, rb, 3, kb);
+    const int ra = c.tm * SH::BM, rb = c.tn * SH::BN;
+#pragma unroll
+    for (int p = 0; p < SH::CA; ++p) s.a[p] = g1_load(c, c.A, c.M, ra, p, kb);
+#pragma unroll
+    for (int p = 0; p < SH::CB; ++p) s.b[p] = g1_load(c, c.W, c.N, rb, p, kb);
 }
 
-__device__ __forceinline__ void g1_store_chunk(const G1Ctx& c, char* la, char* lb, int p,
-                                               int64_t kb, uint4 va, uint4 vb) {
-    const int ch = c.tid + p * G1_THREADS;
+__device__ __forceinline__ void g1_store_chunk(const G1Ctx& c, char* l, int p, int64_t kb,
+                                               int row0, int rows, uint4 v) {
+    const int ch = c.tid + p * c.threads;
     const int row = ch >> 3;
     const int cb = (ch & 7) * 16;
-    const bool kin = kb + cb < c.row_bytes;
     // bitwise masks, not a select of uint4 structs (which would go through memory)
-    const uint32_t ma = (kin && c.tm * G1_BM + row < c.M) ? 0xFFFFFFFFu : 0u;
-    const uint32_t mb = (kin && c.tn * G1_BN + row < c.N) ? 0xFFFFFFFFu : 0u;
-    *(uint4*)(la + row * G1_ROW + cb) = make_uint4(va.x & ma, va.y & ma, va.z & ma, va.w & ma);
-    *(uint4*)(lb + row * G1_ROW + cb) = make_uint4(vb.x & mb, vb.y & mb, vb.z & mb, vb.w & mb);
+    const uint32_t m = (kb + cb < c.row_bytes && row0 + row < rows) ? 0xFFFFFFFFu : 0u;
+    *(uint4*)(l + row * G1_ROW + cb) = make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
 }
 
+template <class SH>
 __device__ __forceinline__ void g1_store_stage(const G1Ctx& c, char* la, char* lb, int kt,
-                                               const G1Stage& s) {
+                                               const G1Stage<SH>& s) {
     const int64_t kb = (int64_t)kt * G1_KBYTES;
-    g1_store_chunk(c, la, lb, 0, kb, s.a0, s.b0);
-    g1_store_chunk(c, la, lb, 1, kb, s.a1, s.b1);
-    g1_store_chunk(c, la, lb, 2, kb, s.a2, s.b2);
-    g1_store_chunk(c, la, lb, 3, kb, s.a3, s.b3);
+#pragma unroll
+    for (int p = 0; p < SH::CA; ++p) g1_store_chunk(c, la, p, kb, c.tm * SH::BM, c.M, s.a[p]);
+#pragma unroll
+    for (int p = 0; p < SH::CB; ++p) g1_store_chunk(c, lb, p, kb, c.tn * SH::BN, c.N, s.b[p]);
 }
 
-template <int kElemBytes>
+// A wave multiplies its (32 MI) x (32 NJ) slab: rows wm * 32 MI..,
+// columns wn * 32 NJ..
+template <int kElemBytes, class SH>
 __device__ __forceinline__ void g1_compute(const char* la, const char* lb, int wm, int wn,
-                                           int lane, f32x16 (&acc)[2][2]) {
+                                           int lane, f32x16 (&acc)[SH::MI][SH::NJ]) {
     constexpr int BK = G1Elem<kElemBytes>::BK;
+    constexpr int MI = SH::MI, NJ = SH::NJ;
     const int r32 = lane & 31;
     const int khalf = lane >> 5;   // which half of the MFMA's K slice this lane feeds
     if constexpr (kElemBytes == 2) {
@@ -121,17 +128,17 @@ __device__ __forceinline__ void g1_compute(const char* la, const char* lb, int w
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
             const int koff = (kk * 16 + khalf * 8) * 2;
-            bf16x8_t a[2], b[2];
+            bf16x8_t a[MI], b[NJ];
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-                a[i] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(la + (wm * 64 + i * 32 + r32) * G1_ROW + koff));
+            for (int i = 0; i < MI; ++i)
+                a[i] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(la + (wm * 32 * MI + i * 32 + r32) * G1_ROW + koff));
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-                b[j] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(lb + (wn * 64 + j * 32 + r32) * G1_ROW + koff));
+            for (int j = 0; j < NJ; ++j)
+                b[j] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(lb + (wn * 32 * NJ + j * 32 + r32) * G1_ROW + koff));
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < MI; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < NJ; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
     } else {
@@ -139,15 +146,15 @@ __device__ __forceinline__ void g1_compute(const char* la, const char* lb, int w
 #pragma unroll
         for (int kk = 0; kk < BK / 2; ++kk) {
             const int koff = (kk * 2 + khalf) * 4;
-            float a[2], b[2];
+            float a[MI], b[NJ];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) a[i] = *(const float*)(la + (wm * 64 + i * 32 + r32) * G1_ROW + koff);
+            for (int i = 0; i < MI; ++i) a[i] = *(const float*)(la + (wm * 32 * MI + i * 32 + r32) * G1_ROW + koff);
 #pragma unroll
-            for (int j = 0; j < 2; ++j) b[j] = *(const float*)(lb + (wn * 64 + j * 32 + r32) * G1_ROW + koff);
+            for (int j = 0; j < NJ; ++j) b[j] = *(const float*)(lb + (wn * 32 * NJ + j * 32 + r32) * G1_ROW + koff);
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < MI; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < NJ; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
         }
     }
@@ -159,34 +166,36 @@ __device__ __forceinline__ void g1_compute(const char* la, const char* lb, int w
 // multiply buffer i % 2.  A buffer is rewritten two steps after its last
 // use, and every thread has passed the intervening barrier only after
 // finishing that use.
-template <int kElemBytes, int NS>
-__device__ __forceinline__ void g1_step(const G1Ctx& c, char (*lds)[2][G1_TILE], int kt0, int nk,
-                                        int i, G1Stage& s, int wm, int wn, int lane,
-                                        f32x16 (&acc)[2][2]) {
+template <int kElemBytes, int NS, class SH>
+__device__ __forceinline__ void g1_step(const G1Ctx& c, char (*lds)[SH::LDS_A + SH::LDS_B],
+                                        int kt0, int nk, int i, G1Stage<SH>& s, int wm, int wn,
+                                        int lane, f32x16 (&acc)[SH::MI][SH::NJ]) {
     const int buf = i & 1;
     // scheduling fences keep each phase in place: otherwise the compiler
     // hoists the next stage's masking into the multiply, which then waits
     // for loads issued only one step earlier
     __builtin_amdgcn_sched_barrier(0);
-    g1_store_stage(c, lds[buf][0], lds[buf][1], kt0 + i, s);
+    g1_store_stage<SH>(c, lds[buf], lds[buf] + SH::LDS_A, kt0 + i, s);
     __syncthreads();
-    g1_load_stage(c, kt0 + (i + NS < nk ? i + NS : i), s);
+    g1_load_stage<SH>(c, kt0 + (i + NS < nk ? i + NS : i), s);
     __builtin_amdgcn_sched_barrier(0);
-    g1_compute<kElemBytes>(lds[buf][0], lds[buf][1], wm, wn, lane, acc);
+    g1_compute<kElemBytes, SH>(lds[buf], lds[buf] + SH::LDS_A, wm, wn, lane, acc);
 }
 
+// Split-K product P[split] = A[:, Ks] W[:, Ks]^T over one BM x BN tile:
 // NS K-tiles of global loads are in flight ahead of the tile being
 // multiplied (register staging, two LDS buffers, one barrier per K-tile).
-template <int kElemBytes, int NS>
-__global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
+template <int kElemBytes, int NS, class SH>
+__global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
     const char* __restrict__ A, const char* __restrict__ W, float* __restrict__ P,
     int M, int N, int Kd, int splits, int tiles_n, int ktiles) {
-    __shared__ __attribute__((aligned(16))) char lds[2][2][G1_TILE];
+    constexpr int MI = SH::MI, NJ = SH::NJ;
+    __shared__ __attribute__((aligned(16))) char lds[2][SH::LDS_A + SH::LDS_B];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
-    const int wm = wid >> 1, wn = wid & 1;
+    const int wm = wid / SH::WN, wn = wid % SH::WN;
 
     const int logical = xcd_logical_block(blockIdx.x, gridDim.x);
     const int tiles = gridDim.x / splits;
@@ -199,13 +208,14 @@ __global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
 
     G1Ctx c;
     c.A = A; c.W = W; c.M = M; c.N = N; c.tm = tm; c.tn = tn; c.tid = tid;
+    c.threads = SH::THREADS; c.bm = SH::BM; c.bn = SH::BN;
     c.row_bytes = (int64_t)Kd * kElemBytes;
 
-    f32x16 acc[2][2];
+    f32x16 acc[MI][NJ];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
@@ -213,49 +223,75 @@ __global__ __launch_bounds__(G1_THREADS) void gemm1_splitk_kernel(
     const int khalf = lane >> 5;
 
     if (nk > 0) {
-        G1Stage st[NS];
+        G1Stage<SH> st[NS];
 #pragma unroll
-        for (int u = 0; u < NS; ++u) g1_load_stage(c, kt0 + (u < nk ? u : 0), st[u]);
+        for (int u = 0; u < NS; ++u) g1_load_stage<SH>(c, kt0 + (u < nk ? u : 0), st[u]);
         int i = 0;
         for (; i + NS <= nk; i += NS) {
 #pragma unroll
             for (int u = 0; u < NS; ++u)
-                g1_step<kElemBytes, NS>(c, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
+                g1_step<kElemBytes, NS, SH>(c, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
         }
 #pragma unroll
         for (int u = 0; u < NS - 1; ++u)
-            if (i + u < nk) g1_step<kElemBytes, NS>(c, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
+            if (i + u < nk) g1_step<kElemBytes, NS, SH>(c, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
     }
 
     // epilogue: the 32x32 accumulator layout (element v of lane l is row
     // 8*(v/4) + 4*(l/32) + v%4, column l%32 of its block) goes through LDS
     // (the operand buffers, free now) so that global stores are whole
-    // 16-byte row chunks.  LDS rows hold G1_OUT_ROW floats (the padding puts
+    // 16-byte row chunks.  LDS rows hold OUT_ROW floats (the padding puts
     // the two 4-row halves of a store on disjoint banks).
     __syncthreads();
-    float* otile = (float*)&lds[0][0][0];
+    float* otile = (float*)&lds[0][0];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int col = wn * 64 + j * 32 + r32;
+        for (int j = 0; j < NJ; ++j) {
+            const int col = wn * 32 * NJ + j * 32 + r32;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int row = wm * 64 + i * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
-                otile[row * G1_OUT_ROW + col] = acc[i][j][v];
+                const int row = wm * 32 * MI + i * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
+                otile[row * SH::OUT_ROW + col] = acc[i][j][v];
             }
         }
     __syncthreads();
     float* out = P + (int64_t)split * M * N;
-    constexpr int CH = G1_BM * G1_BN / 4;             // float4 chunks in the tile
+    constexpr int CH = SH::BM * SH::BN / 4;           // float4 chunks in the tile
 #pragma unroll
-    for (int it = 0; it < CH / G1_THREADS; ++it) {
-        const int ch = it * G1_THREADS + tid;
-        const int row = ch / (G1_BN / 4), c4 = ch % (G1_BN / 4);
-        const int grow = tm * G1_BM + row, gcol = tn * G1_BN + c4 * 4;
+    for (int it = 0; it < CH / SH::THREADS; ++it) {
+        const int ch = it * SH::THREADS + tid;
+        const int row = ch / (SH::BN / 4), c4 = ch % (SH::BN / 4);
+        const int grow = tm * SH::BM + row, gcol = tn * SH::BN + c4 * 4;
         if (grow < M && gcol < N)                     // N % 4 == 0: chunks never straddle N
-            *(float4*)&out[(int64_t)grow * N + gcol] = *(const float4*)&otile[row * G1_OUT_ROW + c4 * 4];
+            *(float4*)&out[(int64_t)grow * N + gcol] = *(const float4*)&otile[row * SH::OUT_ROW + c4 * 4];
     }
+}
+
+// Launch of the split-K product with the plan's tile shape.
+static hipError_t launch_gemm(const GemmPlan& g, bool bf16, const void* A, const void* W,
+                              float* P, int M, int N, int K, hipStream_t stream) {
+    const dim3 grid(g.tiles_m * g.tiles_n * g.splits);
+    if (g.big) {
+        if (bf16)
+            hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES, G1Big>), grid,
+                               dim3(G1Big::THREADS), 0, stream, (const char*)A, (const char*)W, P,
+                               M, N, K, g.splits, g.tiles_n, g.ktiles);
+        else
+            hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES, G1Big>), grid,
+                               dim3(G1Big::THREADS), 0, stream, (const char*)A, (const char*)W, P,
+                               M, N, K, g.splits, g.tiles_n, g.ktiles);
+    } else {
+        if (bf16)
+            hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES, G1Small>), grid,
+                               dim3(G1Small::THREADS), 0, stream, (const char*)A, (const char*)W, P,
+                               M, N, K, g.splits, g.tiles_n, g.ktiles);
+        else
+            hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES, G1Small>), grid,
+                               dim3(G1Small::THREADS), 0, stream, (const char*)A, (const char*)W, P,
+                               M, N, K, g.splits, g.tiles_n, g.ktiles);
+    }
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -546,29 +582,48 @@ __global__ __launch_bounds__(ACT_THREADS) void act_kernel(const float* __restric
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-// Tiles and split-K factor of one product [M, K] x [N, K]^T: the split is a
-// power of two in [1, 16] that brings the workgroups near one per CU.
+// Tiles and split-K factor of one product [M, K] x [N, K]^T.  For each tile
+// shape the split is a power of two in [1, 16] that brings the workgroups
+// near one per CU.  The shape is chosen by a cost model of its two data
+// streams: operand rows read into the CUs (every A row once per column of
+// tiles, every W row once per row of tiles) at the L2's aggregate ~17 TB/s,
+// and the fp32 split-K partials written, flushed out of L2 at the end of
+// the kernel and read back at ~2.4 TB/s (both rates measured on MI355X).
 GemmPlan plan_gemm(int M, int N, int K, int elem) {
-    GemmPlan g;
+    GemmPlan best;
+    double best_cost = 0.0;
     const int bk = G1_KBYTES / elem;
-    g.tiles_m = (int)ceil_div(M, G1_BM);
-    g.tiles_n = (int)ceil_div(N, G1_BN);
-    g.ktiles = (int)ceil_div(K, bk);
-    const int tiles = g.tiles_m * g.tiles_n;
-    int s = 1;
-    if (tiles > 0 && tiles < 192) {
-        int want = 256 / tiles;
-        if (want > 16) want = 16;
-        if (want > g.ktiles / 2) want = g.ktiles / 2;
-        while (s * 2 <= want) s *= 2;
+    for (int big = 1; big >= 0; --big) {
+        GemmPlan g;
+        g.big = big;
+        const int bm = big ? G1Big::BM : G1Small::BM, bn = big ? G1Big::BN : G1Small::BN;
+        g.tiles_m = (int)ceil_div(M, bm);
+        g.tiles_n = (int)ceil_div(N, bn);
+        g.ktiles = (int)ceil_div(K, bk);
+        const int tiles = g.tiles_m * g.tiles_n;
+        int s = 1;
+        if (tiles > 0 && tiles < 192) {
+            int want = 256 / tiles;
+            if (want > 16) want = 16;
+            if (want > g.ktiles / 2) want = g.ktiles / 2;
+            while (s * 2 <= want) s *= 2;
+        }
+        g.splits = s;
+        const double operands = ((double)g.tiles_n * M + (double)g.tiles_m * N) * K * elem;
+        const double partials = (double)s * M * N * 4.0;
+        const double cost = operands / 17e12 + 2.0 * partials / 2.4e12;
+        if (big || cost < best_cost) {
+            best = g;
+            best_cost = cost;
+        }
     }
-    g.splits = s;
-    return g;
+    return best;
 }
 
 PredictPlan plan_predict(const star_predict_params& p) {
     PredictPlan pl;
     const GemmPlan g = plan_gemm(p.n_req, p.d_hidden, p.d_model, p.dtype == STAR_BF16 ? 2 : 4);
+    pl.gemm = g;
     pl.tiles_m = g.tiles_m;
     pl.tiles_n = g.tiles_n;
     pl.ktiles = g.ktiles;
@@ -628,17 +683,8 @@ hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, c
         e = hipEventRecord(ev[0], stream);
         if (e != hipSuccess) return e;
     }
-    const dim3 g1(pl.tiles_m * pl.tiles_n * pl.splits);
-    if (p.dtype == STAR_BF16)
-        hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES>), g1, dim3(G1_THREADS), 0, stream,
-                           (const char*)hidden, (const char*)w1, partials, p.n_req, p.d_hidden,
-                           p.d_model, pl.splits, pl.tiles_n, pl.ktiles);
-    else
-        hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES>), g1, dim3(G1_THREADS), 0, stream,
-                           (const char*)hidden, (const char*)w1, partials, p.n_req, p.d_hidden,
-                           p.d_model, pl.splits, pl.tiles_n, pl.ktiles);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    e = launch_gemm(pl.gemm, p.dtype == STAR_BF16, hidden, w1, partials, p.n_req, p.d_hidden,
+                    p.d_model, stream);
     if (ev) {
         e = hipEventRecord(ev[1], stream);
         if (e != hipSuccess) return e;
@@ -713,16 +759,9 @@ hipError_t launch_mlp4(const star_mlp4_params& p, const Mlp4Plan& pl, const void
     hipEvent_t* ev = (hipEvent_t*)p.timing_events;
     hipError_t e;
     if (ev && (e = hipEventRecord(ev[0], stream)) != hipSuccess) return e;
-    const dim3 g1(pl.g1.tiles_m * pl.g1.tiles_n * pl.g1.splits);
-    if (bf)
-        hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES>), g1, dim3(G1_THREADS), 0, stream,
-                           (const char*)hidden, (const char*)w1, P1, p.n_req, p.m1, p.d_model,
-                           pl.g1.splits, pl.g1.tiles_n, pl.g1.ktiles);
-    else
-        hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES>), g1, dim3(G1_THREADS), 0, stream,
-                           (const char*)hidden, (const char*)w1, P1, p.n_req, p.m1, p.d_model,
-                           pl.g1.splits, pl.g1.tiles_n, pl.g1.ktiles);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_gemm(pl.g1, bf, hidden, w1, P1, p.n_req, p.m1, p.d_model, stream)) !=
+        hipSuccess)
+        return e;
     if (ev && (e = hipEventRecord(ev[1], stream)) != hipSuccess) return e;
     const int64_t items = (int64_t)p.n_req * p.m1 / 4;
     int64_t ab = ceil_div(items, (int64_t)ACT_THREADS * ACT_BATCH);
@@ -731,16 +770,9 @@ hipError_t launch_mlp4(const star_mlp4_params& p, const Mlp4Plan& pl, const void
            : launch_act<false>(pl.g1.splits, ga, P1, items, p.m1 / 4, b1, A1, stream);
     if (e != hipSuccess) return e;
     const star_predict_params h = head_view(p);
-    const dim3 g2(pl.head.tiles_m * pl.head.tiles_n * pl.head.splits);
-    if (bf)
-        hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES>), g2, dim3(G1_THREADS), 0, stream,
-                           (const char*)A1, (const char*)w2, P2, p.n_req, p.m2, p.m1,
-                           pl.head.splits, pl.head.tiles_n, pl.head.ktiles);
-    else
-        hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES>), g2, dim3(G1_THREADS), 0, stream,
-                           (const char*)A1, (const char*)w2, P2, p.n_req, p.m2, p.m1,
-                           pl.head.splits, pl.head.tiles_n, pl.head.ktiles);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_gemm(pl.head.gemm, bf, A1, w2, P2, p.n_req, p.m2, p.m1, stream)) !=
+        hipSuccess)
+        return e;
     const dim3 gh((unsigned)ceil_div(p.n_req, HD_RB));
     return bf ? launch_head<true, true>(h, pl.head, gh, P2, b2, w3, b3, w4, ema_state, expected,
                                         rem_len, stream, p.b4)

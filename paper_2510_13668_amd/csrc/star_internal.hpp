@@ -9,7 +9,14 @@
 
 namespace star {
 
+struct GemmPlan {
+    int tiles_m = 0, tiles_n = 0, ktiles = 0, splits = 1;
+    int big = 1;          // 128 x 128 tiles (else 64 x 64)
+};
+GemmPlan plan_gemm(int M, int N, int K, int elem);
+
 struct PredictPlan {
+    GemmPlan gemm;
     int tiles_m = 0, tiles_n = 0, ktiles = 0, splits = 1;
     size_t partial_bytes = 0;   // fp32 split-K partials [splits, B, m]
     size_t head_lds = 0;        // dynamic LDS of the head kernel
@@ -19,11 +26,6 @@ hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, c
                           const void* w1, const float* b1, const void* w2, const float* b2,
                           const float* bins, float* ema_state, float* expected, int32_t* rem_len,
                           float* partials, hipStream_t stream);
-
-struct GemmPlan {
-    int tiles_m = 0, tiles_n = 0, ktiles = 0, splits = 1;
-};
-GemmPlan plan_gemm(int M, int N, int K, int elem);
 
 struct Mlp4Plan {
     GemmPlan g1;          // layer 1
