@@ -26,7 +26,12 @@ namespace star {
 // ---------------------------------------------------------------------------
 constexpr int G1_KBYTES = 128;                 // bytes of K per LDS row
 constexpr int G1_ROW = G1_KBYTES + 16;         // padded LDS row (bytes)
-constexpr int G1_STAGES = 3;                   // K-tiles of loads in flight ahead of the multiply
+// K-tiles of global loads in flight ahead of the multiply: three for the
+// 128 x 128 shape (one 8-wave workgroup per CU), two for the 64 x 64 one,
+// which runs two workgroups per CU that share the CU's load path (measured:
+// deeper register staging only lengthens each workgroup there).
+constexpr int G1_STAGES_BIG = 3;
+constexpr int G1_STAGES_SMALL = 2;
 
 template <int kElemBytes> struct G1Elem;
 template <> struct G1Elem<2> { static constexpr int BK = 64; };   // bf16
@@ -274,20 +279,20 @@ static hipError_t launch_gemm(const GemmPlan& g, bool bf16, const void* A, const
     const dim3 grid(g.tiles_m * g.tiles_n * g.splits);
     if (g.big) {
         if (bf16)
-            hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES, G1Big>), grid,
+            hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES_BIG, G1Big>), grid,
                                dim3(G1Big::THREADS), 0, stream, (const char*)A, (const char*)W, P,
                                M, N, K, g.splits, g.tiles_n, g.ktiles);
         else
-            hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES, G1Big>), grid,
+            hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES_BIG, G1Big>), grid,
                                dim3(G1Big::THREADS), 0, stream, (const char*)A, (const char*)W, P,
                                M, N, K, g.splits, g.tiles_n, g.ktiles);
     } else {
         if (bf16)
-            hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES, G1Small>), grid,
+            hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES_SMALL, G1Small>), grid,
                                dim3(G1Small::THREADS), 0, stream, (const char*)A, (const char*)W, P,
                                M, N, K, g.splits, g.tiles_n, g.ktiles);
         else
-            hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES, G1Small>), grid,
+            hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES_SMALL, G1Small>), grid,
                                dim3(G1Small::THREADS), 0, stream, (const char*)A, (const char*)W, P,
                                M, N, K, g.splits, g.tiles_n, g.ktiles);
     }
@@ -584,7 +589,8 @@ __global__ __launch_bounds__(ACT_THREADS) void act_kernel(const float* __restric
 // ---------------------------------------------------------------------------
 // Tiles and split-K factor of one product [M, K] x [N, K]^T.  For each tile
 // shape the split is a power of two in [1, 16] that brings the workgroups
-// near one per CU.  The shape is chosen by a cost model of its two data
+// near one per CU (128 x 128) or two per CU (64 x 64).  The shape is chosen
+// by a cost model of its two data
 // streams: operand rows read into the CUs (every A row once per column of
 // tiles, every W row once per row of tiles) at the L2's aggregate ~17 TB/s,
 // and the fp32 split-K partials written, flushed out of L2 at the end of
@@ -602,8 +608,9 @@ GemmPlan plan_gemm(int M, int N, int K, int elem) {
         g.ktiles = (int)ceil_div(K, bk);
         const int tiles = g.tiles_m * g.tiles_n;
         int s = 1;
-        if (tiles > 0 && tiles < 192) {
-            int want = 256 / tiles;
+        const int slots = big ? 256 : 512;
+        if (tiles > 0 && tiles < 3 * slots / 4) {
+            int want = slots / tiles;
             if (want > 16) want = 16;
             if (want > g.ktiles / 2) want = g.ktiles / 2;
             while (s * 2 <= want) s *= 2;

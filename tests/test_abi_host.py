@@ -79,9 +79,9 @@ def test_predict_rejects_null_pointers_and_workspace(L):
     assert _predict(L, _pp(), hidden=ctypes.c_void_p((1 << 20) + 2)) == -2   # misaligned
     p = _pp()
     need = star.predict_workspace_size(p)
-    # 64 x 64 tiles: 16 x 8 of them, 2 K-splits of a [1024, 512] fp32
+    # 64 x 64 tiles: 16 x 8 of them, 4 K-splits of a [1024, 512] fp32
     # partial product, plus the header
-    assert need == 256 + 2 * 1024 * 512 * 4
+    assert need == 256 + 4 * 1024 * 512 * 4
     assert _predict(L, p, ws_bytes=need - 1) == -4
     assert _predict(L, p, ws=None) == -4
     assert _predict(L, p, ws=ctypes.c_void_p((1 << 20) + 64)) == -4   # not 256-aligned
