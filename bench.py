@@ -5,7 +5,8 @@ continuous-mode workload (1024 concurrent requests on 8 decode instances,
 bf16 hidden states [1024, 4096] from an AR(1) process, head 4096 -> 512
 (GELU) -> 64 length bins with EMA alpha 0.2, horizon 16384 steps in 64-step
 buckets, all 1024 x 8 candidates scored, top-256 ranked):
-    star_predict -> star_project_load -> star_score_migrations.
+    star_predict -> star_project_and_score (the load projection and the
+    migration scoring and ranking in one call).
 Inputs for 200 decode steps are staged in HBM before timing.  The metric is
 requests predicted + scored per second (= 1024 / seconds per round) and
 microseconds per round.
@@ -664,20 +665,19 @@ def main():
 
     pp = star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, False, wl.len_max)
     pp_init = star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, True, wl.len_max)
-    lp = star.load_params(N, n, b, K)
     sp = star.score_params(N, n, b, K, top_k)
     ws_p = star.Workspace(star.predict_workspace_size(pp))
-    ws_l = star.Workspace(star.project_load_workspace_size(lp))
-    ws_s = star.Workspace(star.score_workspace_size(sp))
+    ws_s = star.Workspace(star.project_and_score_workspace_size(sp))
 
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()
 
+    # One round: the predictor head, then the load projection and the
+    # migration scoring in one call (one kernel launch at this size).
     def round_(slot, params=pp):
         star.predict(params, hid[slot], w1, None, w2, None, bins, ema, expected, rem, ws_p, stream)
-        star.project_load(lp, cur_steps[slot], rem, inst, load, ws_l, stream)
-        star.score_migrations(sp, cur_steps[slot], rem, inst, load, scores, best_t, best_s,
-                              tr, tt, ts, ws_s, stream)
+        star.project_and_score(sp, cur_steps[slot], rem, inst, load, scores, best_t, best_s,
+                               tr, tt, ts, ws_s, stream)
 
     with torch.cuda.stream(stream):
         round_(0, pp_init)                          # first decode step initialises the EMA
@@ -714,6 +714,8 @@ def main():
     # so it runs on `stream` while round i-1 is projected and scored on
     # `sched`.  Per-round outputs are double-buffered; an event keeps a
     # buffer from being overwritten before its scheduling has finished.
+    # (Measured: giving each round of a captured chunk its own buffers, which
+    # drops these events, makes the replayed graph slower.)
     sched = torch.cuda.Stream()
     NSLOT = 2
     slot_buf = []
@@ -742,10 +744,9 @@ def main():
                      ws_p, stream)
         ev_pred[k].record(stream)
         sched.wait_event(ev_pred[k])
-        star.project_load(lp, cur_steps[step], sb["rem"], inst, sb["load"], ws_l, sched)
-        star.score_migrations(sp, cur_steps[step], sb["rem"], inst, sb["load"], sb["scores"],
-                              sb["best_t"], sb["best_s"], sb["tr"], sb["tt"], sb["ts"], ws_s,
-                              sched)
+        star.project_and_score(sp, cur_steps[step], sb["rem"], inst, sb["load"], sb["scores"],
+                               sb["best_t"], sb["best_s"], sb["tr"], sb["tt"], sb["ts"], ws_s,
+                               sched)
         ev_done[k].record(sched)
         used[k] = True
 
@@ -766,8 +767,8 @@ def main():
 
     # The same pipeline captured in HIP graphs of CHUNK rounds each (the two
     # streams fork and join inside the capture), so that the host launches
-    # one graph per CHUNK rounds instead of five kernels and four event
-    # operations per round.
+    # one graph per CHUNK rounds instead of the kernels and event operations
+    # of every round.
     CHUNK = 40
     chunk_graphs = []
     torch.cuda.synchronize()
@@ -785,10 +786,9 @@ def main():
                              sb["rem"], ws_p, stream)
                 ev_pred[k].record(stream)
                 sched.wait_event(ev_pred[k])
-                star.project_load(lp, cur_steps[step], sb["rem"], inst, sb["load"], ws_l, sched)
-                star.score_migrations(sp, cur_steps[step], sb["rem"], inst, sb["load"],
-                                      sb["scores"], sb["best_t"], sb["best_s"], sb["tr"],
-                                      sb["tt"], sb["ts"], ws_s, sched)
+                star.project_and_score(sp, cur_steps[step], sb["rem"], inst, sb["load"],
+                                       sb["scores"], sb["best_t"], sb["best_s"], sb["tr"],
+                                       sb["tt"], sb["ts"], ws_s, sched)
                 ev_done[k].record(sched)
             stream.wait_stream(sched)
         chunk_graphs.append(g)

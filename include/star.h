@@ -20,9 +20,13 @@
  *     return.  Results are valid once the stream has reached that point.
  *   - `ws` is a caller-owned device workspace of at least the size reported
  *     by the matching *_workspace_size() call, 256-byte aligned, zeroed once
- *     before first use (star_workspace_init).  Its first 256 bytes hold a
- *     sticky device-error word; the rest is scratch.  Calls sharing a workspace must be ordered (same
- *     stream, or synchronised); concurrent calls need distinct workspaces.
+ *     before first use (star_workspace_init).  Its first STAR_WS_HEADER_BYTES
+ *     bytes are the library's state between calls (a sticky device-error
+ *     word; counters and a histogram that every call leaves at zero); the
+ *     rest is scratch that any call may overwrite, so one workspace can
+ *     serve every entry point.  Calls sharing a workspace must be ordered
+ *     (same stream, or synchronised); concurrent calls need distinct
+ *     workspaces.
  *   - Array CONTENTS that break a documented precondition (instance index
  *     out of range, cur_len < 1, rem_len < 1) are detected on the device:
  *     the offending request is left out of every curve, score and ranking,
@@ -41,7 +45,7 @@ extern "C" {
 #endif
 
 #define STAR_ABI_VERSION 1
-#define STAR_WS_HEADER_BYTES 256
+#define STAR_WS_HEADER_BYTES 8192
 #define STAR_MAX_TOP_K 1024
 
 typedef enum {
@@ -197,6 +201,25 @@ star_status star_score_migrations(const star_score_params* p, const int32_t* cur
                                   const int64_t* load, int64_t* scores, int32_t* best_target,
                                   int64_t* best_score, int32_t* topk_req, int32_t* topk_tgt,
                                   int64_t* topk_score, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * (b) + (c) in one call: the load projection of the requests followed by
+ * the scoring and ranking of their migrations (Section 5.2, Eq. 4;
+ * Algorithm 1), with the same arguments and results as star_project_load
+ * then star_score_migrations on that load, except that `load` (int64
+ * [n_inst, n_buckets], fully overwritten) is an output here and the two
+ * share one workspace of star_project_and_score_workspace_size() bytes.
+ * Rounds whose curves fit on-chip (and with at most 8192 requests) skip
+ * the projection kernel: every scoring workgroup builds the curves itself
+ * and one of them writes `load`; other sizes run the projection first.
+ * ---------------------------------------------------------------------- */
+size_t star_project_and_score_workspace_size(const star_score_params* p);
+
+star_status star_project_and_score(const star_score_params* p, const int32_t* cur_len,
+                                   const int32_t* rem_len, const int32_t* inst_of, int64_t* load,
+                                   int64_t* scores, int32_t* best_target, int64_t* best_score,
+                                   int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score,
+                                   void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * (f1) Migration candidates scored by the change of the time-weighted load

@@ -46,6 +46,8 @@ constexpr int SC_THREADS = 256;
 constexpr int SC_CAND = 256;                 // target candidates per scoring workgroup
 constexpr int SC_FUSED_ENTRIES = 2600;       // n*(K+1) up to which PM/SM live in LDS
 constexpr int SC_LBATCH = (SC_FUSED_ENTRIES + SC_THREADS - 1) / SC_THREADS;  // curve reads per thread
+constexpr int SC_PBATCH = 4;                 // requests per thread in flight (in-kernel projection)
+constexpr int SC_PROJECT_MAX_REQ = 8192;     // requests up to which every group projects for itself
 
 constexpr int SEL_DIGIT = 12;                // radix-select digit width
 constexpr int SEL_BINS = 1 << SEL_DIGIT;
@@ -208,6 +210,93 @@ __device__ inline void build_pm_sm(const int64_t* lL, int64_t* lPM, int64_t* lSM
     }
 }
 
+// Inclusive prefix sum over the 32 lanes of each half wave (lane order),
+// DPP as in half_incl_max_i64; lanes without a source add 0.
+template <int kCtrl, int kRowMask>
+__device__ inline int64_t dpp_add_step_i64(int64_t v) {
+    const int lo = dpp_i32<kCtrl, kRowMask>((int)(uint32_t)v, 0);
+    const int hi = dpp_i32<kCtrl, kRowMask>((int)(v >> 32), 0);
+    return v + (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+__device__ inline int64_t half_incl_add_i64(int64_t v) {
+    v = dpp_add_step_i64<kDppRowShr1, 0xF>(v);
+    v = dpp_add_step_i64<kDppRowShr2, 0xF>(v);
+    v = dpp_add_step_i64<kDppRowShr4, 0xF>(v);
+    v = dpp_add_step_i64<kDppRowShr8, 0xF>(v);
+    v = dpp_add_step_i64<kDppRowBcast15, 0xA>(v);
+    return v;
+}
+
+// Section 5.2's curves of every instance from its requests, in LDS (rows of
+// stride K+1): hA / hN hold alpha_r and the request count by k_e (1..K), hP
+// the partial-bucket terms by k_e (0..K-1).  With S_A(k), S_n(k) the sums of
+// hA, hN over k_e > k, L[k] = S_A(k) + b^2 k S_n(k) + hP[k] is written over
+// hP, and entry K of each row becomes -inf (padding read by the scoring).
+// Each instance is taken by half a wave; lane l owns a run of S (odd)
+// buckets counted from the end, as in build_pm_sm: a sum over its run, one
+// DPP scan across the 32 runs, then a pass that writes.
+template <int kT>
+__device__ inline void build_curves(const int64_t* hA, const int64_t* hN, int64_t* hPL, int n,
+                                    int K, int64_t bb) {
+    const int l = threadIdx.x & 31;
+    const int K1 = K + 1;
+    const int S = ((K + 31) >> 5) | 1;
+    for (int t0 = 0; t0 < n; t0 += kT / 32) {
+        const int t = t0 + (int)(threadIdx.x >> 5);
+        const bool live = t < n;
+        const int tc = live ? t : 0;
+        const int64_t* A = hA + tc * K1;
+        const int64_t* C = hN + tc * K1;
+        int64_t* L = hPL + tc * K1;
+        const int j0 = l * S;
+        const int j1 = j0 + S < K ? j0 + S : K;
+        const int q0 = K - 1 - j0, q1 = K - j1;      // buckets [q1, q0], walked downwards
+        int64_t sa = 0, sn = 0;
+        for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {
+            int64_t xa[PMSM_BATCH], xn[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u >= q1 ? jb - u : q0;
+                xa[u] = A[q + 1];
+                xn[u] = C[q + 1];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u)
+                if (jb - u >= q1) {
+                    sa += xa[u];
+                    sn += xn[u];
+                }
+        }
+        // the lane shifts run on every lane (a DPP move inside one arm of a
+        // branch would read disabled lanes), then each half's first lane
+        // takes 0
+        const int64_t ia = half_incl_add_i64(sa), in = half_incl_add_i64(sn);
+        const int64_t ea = wave_shr1_i64(ia, 0), en = wave_shr1_i64(in, 0);
+        int64_t ra = l == 0 ? 0 : ea;
+        int64_t rn = l == 0 ? 0 : en;
+        for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {
+            int64_t xa[PMSM_BATCH], xn[PMSM_BATCH], xp[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u >= q1 ? jb - u : q0;
+                xa[u] = A[q + 1];
+                xn[u] = C[q + 1];
+                xp[u] = L[q];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u;
+                if (q >= q1) {
+                    ra += xa[u];
+                    rn += xn[u];
+                    if (live) L[q] = ra + bb * q * rn + xp[u];
+                }
+            }
+        }
+        if (live && l == 0) L[K] = INT64_MIN;
+    }
+}
+
 // Minimum of a 64-bit value over aligned groups of g lanes (g a power of
 // two, 2..64); every lane of a group gets it.  DPP quad permutes for lane
 // distances 1 and 2, row shifts under bank masks for 4 and 8, and
@@ -309,6 +398,7 @@ struct ScoreArgs {
     int32_t* best_target;         // caller's array or workspace copy
     int64_t* best_score;
     int32_t* err_word;
+    int64_t* load_out;            // curves built by the scoring kernel itself (group 0 writes)
     int N, n, b, K, rpb, cand;
     uint32_t magic_K, magic_n;
 };
@@ -1007,150 +1097,6 @@ struct RankArgs {
     int32_t* offs;                // [groups, RK_CODES + 1] exclusive code offsets per group
 };
 
-// Fused scoring (all curves in LDS) plus each group's migration keys sorted
-// by code (a counting sort in LDS), its code offsets and the global code
-// histogram.
-__global__ __launch_bounds__(SC_THREADS) void score_rank_kernel(ScoreArgs a, RankArgs rk) {
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    __shared__ int lhist[RK_CODES];
-    __shared__ int wtot[SC_THREADS / 64];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int n = a.n, K = a.K, b = a.b;
-    const int K1 = K + 1;
-    const int cand = a.cand;                       // rpb * n <= SC_THREADS: one per thread
-    const int rpb = a.rpb;
-
-    int64_t* lL = (int64_t*)smem;
-    int64_t* lPM = lL + n * K1;
-    int64_t* lSM = lPM + n * K1;
-    int64_t* ks = lSM + n * K1;
-    int64_t* r_alpha = ks + cand;
-    int64_t* r_p = r_alpha + rpb;
-    uint32_t* ki = (uint32_t*)(r_p + rpb);
-    int32_t* r_ke = (int32_t*)(ki + cand);
-    int32_t* r_s = r_ke + rpb;
-
-    const int g = blockIdx.x;
-    const int row0 = g * rpb;
-    const int64_t H = (int64_t)b * K;
-    const int64_t bb = (int64_t)b * b;
-
-    // 0) curves and per-request terms (all reads issued first)
-    const int nK = n * K;
-    int64_t lv[SC_LBATCH];
-#pragma unroll
-    for (int j = 0; j < SC_LBATCH; ++j) {
-        const int e = j * SC_THREADS + tid;
-        lv[j] = a.load[e < nK ? e : nK - 1];
-    }
-    int32_t bad = 0;
-    {
-        const int q = tid;                           // rpb <= SC_THREADS
-        int r = row0 + q;
-        r = r < a.N ? r : a.N - 1;
-        const int sv = a.inst[r], cv = a.cur[r], rv = a.rem[r];
-        if (q < rpb) {
-            const bool live = row0 + q < a.N;
-            const ReqTerms rt = request_terms(sv, cv, rv, n, b, H);
-            bad = live ? rt.bad : 0;
-            r_s[q] = live ? rt.s : -1;
-            r_ke[q] = rt.ke;
-            r_alpha[q] = rt.alpha;
-            r_p[q] = rt.p;
-        }
-    }
-    bad = wave_or_i32(bad);
-    if (lane == 0) report_error(a.err_word, bad);
-#pragma unroll
-    for (int j = 0; j < SC_LBATCH; ++j) {
-        const int e = j * SC_THREADS + tid;
-        if (e < nK) {
-            const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
-            lL[t * K1 + (e - t * K)] = lv[j];
-        }
-    }
-    for (int t = tid; t < n; t += SC_THREADS) lL[t * K1 + K] = INT64_MIN;
-    for (int c = tid; c < RK_CODES; c += SC_THREADS) lhist[c] = 0;
-    __syncthreads();
-    build_pm_sm<SC_THREADS>(lL, lPM, lSM, n, K, bb);
-    __syncthreads();
-
-    // 1) this thread's candidate e = q n + t
-    int64_t base = INT64_MAX;                         // smallest target peak
-    for (int t = 0; t < n; ++t) {
-        const int64_t v = lSM[t * K1];
-        base = v < base ? v : base;
-    }
-    const int e = tid;
-    const uint32_t ec = (uint32_t)(e < cand ? e : cand - 1);
-    const int q = (int)fast_div(ec, (uint32_t)n, a.magic_n);
-    const int t = (int)ec - q * n;
-    const int r = row0 + q;
-    const bool live = e < cand && r < a.N;
-    const int s = r_s[q], ke = r_ke[q];
-    const int64_t* pm_t = lPM + t * K1;
-    const int64_t* sm_t = lSM + t * K1;
-    const int64_t mv = move_score(pm_t, sm_t, lL[t * K1 + ke], ke, K, r_alpha[q], r_p[q]);
-    const int64_t sc = s < 0 ? -1 : (t == s ? sm_t[0] : mv);
-    const bool mig = live && s >= 0 && t != s;
-    if (live && a.scores) a.scores[(int64_t)r * n + t] = sc;
-    if (e < cand) {
-        ks[e] = mig ? sc : kInfS;
-        ki[e] = mig ? (uint32_t)((int64_t)r * n + t) : kInfI;
-    }
-    // code and rank of this key among the group's keys of equal code
-    const uint32_t code = mig ? key_code((uint64_t)(sc - base)) : 0;
-    const int lrank = mig ? atomicAdd(&lhist[code], 1) : 0;
-    __syncthreads();
-
-    // 2) best migration per request: smallest (score, t) over t != s
-    for (int qq = tid; qq < rpb; qq += SC_THREADS) {
-        const int rr = row0 + qq;
-        if (rr >= a.N) continue;
-        int64_t bs = kInfS;
-        uint32_t bi = kInfI;
-        for (int tt = 0; tt < n; ++tt) {
-            const int ee = qq * n + tt;
-            if (key_less(ks[ee], ki[ee], bs, bi)) { bs = ks[ee]; bi = ki[ee]; }
-        }
-        const bool none = bi == kInfI;
-        if (a.best_target) a.best_target[rr] = none ? -1 : (int32_t)(bi - (uint32_t)((int64_t)rr * n));
-        if (a.best_score) a.best_score[rr] = none ? -1 : bs;
-    }
-
-    // 3) code histogram -> exclusive offsets (4 codes per thread), global counts
-    constexpr int PER = RK_CODES / SC_THREADS;
-    int c4[PER], own = 0;
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-        c4[u] = lhist[tid * PER + u];
-        own += c4[u];
-    }
-    const int inc = wave_incl_add_i32(own);
-    if (lane == 63) wtot[tid >> 6] = inc;
-    __syncthreads();
-    int before = inc - own;
-    for (int w = 0; w < (tid >> 6); ++w) before += wtot[w];
-    int32_t* go = rk.offs + (int64_t)g * (RK_CODES + 1);
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-        const int c = tid * PER + u;
-        go[c] = before;
-        if (c4[u]) atomicAdd(&rk.ghist[c], (uint32_t)c4[u]);
-        lhist[c] = before;                            // now the offset
-        before += c4[u];
-    }
-    if (tid == SC_THREADS - 1) go[RK_CODES] = before;  // this group's migration count
-    if (g == 0 && tid == 0) *rk.base = base;
-    __syncthreads();
-    if (mig) {
-        const int64_t at = (int64_t)g * cand + lhist[code] + lrank;
-        rk.keys_s[at] = sc;
-        rk.keys_i[at] = (uint32_t)((int64_t)r * n + t);
-    }
-}
-
 struct FinalArgs {
     uint32_t* ghist;              // zeroed here after use
     const int32_t* offs;
@@ -1204,15 +1150,29 @@ __device__ inline int find_part(const int32_t* pre, int G, int p) {
     return lo;
 }
 
-__global__ __launch_bounds__(RK_THREADS) void rank_final_kernel(FinalArgs a) {
-    __shared__ SelShared<RK_THREADS> sh;
-    __shared__ int64_t ws_s[STAR_MAX_TOP_K];
-    __shared__ uint32_t ws_i[STAR_MAX_TOP_K];
-    __shared__ uint64_t sv[STAR_MAX_TOP_K];
-    __shared__ int32_t lo_w[RK_MAX_GROUPS], hi_w[RK_MAX_GROUPS];
-    __shared__ int32_t pre_a[RK_MAX_GROUPS], pre_b[RK_MAX_GROUPS];
-    __shared__ int64_t bs_s[RK_BCAP];
-    __shared__ uint32_t bs_i[RK_BCAP];
+// LDS of the final ranking workgroup.
+struct FinalLds {
+    SelShared<RK_THREADS> sh;
+    int64_t ws_s[STAR_MAX_TOP_K];
+    uint32_t ws_i[STAR_MAX_TOP_K];
+    uint64_t sv[STAR_MAX_TOP_K];
+    int32_t lo_w[RK_MAX_GROUPS], hi_w[RK_MAX_GROUPS];
+    int32_t pre_a[RK_MAX_GROUPS], pre_b[RK_MAX_GROUPS];
+    int64_t bs_s[RK_BCAP];
+    uint32_t bs_i[RK_BCAP];
+};
+
+__device__ __forceinline__ void rank_final_body(const FinalArgs& a, FinalLds& F) {
+    SelShared<RK_THREADS>& sh = F.sh;
+    int64_t* ws_s = F.ws_s;
+    uint32_t* ws_i = F.ws_i;
+    uint64_t* sv = F.sv;
+    int32_t* lo_w = F.lo_w;
+    int32_t* hi_w = F.hi_w;
+    int32_t* pre_a = F.pre_a;
+    int32_t* pre_b = F.pre_b;
+    int64_t* bs_s = F.bs_s;
+    uint32_t* bs_i = F.bs_i;
     const int tid = threadIdx.x;
     const int G = a.groups;
 
@@ -1343,6 +1303,204 @@ __global__ __launch_bounds__(RK_THREADS) void rank_final_kernel(FinalArgs a) {
     order_and_write<RK_THREADS>(ws_s, ws_i, nw, wmin, wmax, a.ibits, a.n, a.magic_n, a.topk_req,
                                 a.topk_tgt, a.topk_score, a.top_k, sh, sv);
 }
+
+__global__ __launch_bounds__(RK_THREADS) void rank_final_kernel(FinalArgs a) {
+    __shared__ FinalLds F;
+    rank_final_body(a, F);
+}
+
+// Fused scoring (all curves in LDS) plus each group's migration keys sorted
+// by code (a counting sort in LDS), its code offsets and the global code
+// histogram.
+// kProject: every group builds the curves itself from all N requests (the
+//   load projection, redundantly per group: N is small on this path) and
+//   group 0 writes them to a.load_out, so no projection kernel runs first.
+//   (Measured on MI355X: one launch fewer per round is worth more than the
+//   repeated reads of the requests.  Handing the final ranking to the last
+//   group to finish was not: its device-scope fences and the ranking's LDS
+//   in every group cost more than the ranking kernel's launch.)
+template <bool kProject>
+__global__ __launch_bounds__(SC_THREADS) void score_rank_kernel(ScoreArgs a, RankArgs rk) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ int lhist[RK_CODES];
+    __shared__ int wtot[SC_THREADS / 64];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int n = a.n, K = a.K, b = a.b;
+    const int K1 = K + 1;
+    const int cand = a.cand;                       // rpb * n <= SC_THREADS: one per thread
+    const int rpb = a.rpb;
+
+    int64_t* lL = (int64_t*)smem;
+    int64_t* lPM = lL + n * K1;
+    int64_t* lSM = lPM + n * K1;
+    int64_t* ks = lSM + n * K1;
+    int64_t* r_alpha = ks + cand;
+    int64_t* r_p = r_alpha + rpb;
+    uint32_t* ki = (uint32_t*)(r_p + rpb);
+    int32_t* r_ke = (int32_t*)(ki + cand);
+    int32_t* r_s = r_ke + rpb;
+
+    const int g = blockIdx.x;
+    const int row0 = g * rpb;
+    const int64_t H = (int64_t)b * K;
+    const int64_t bb = (int64_t)b * b;
+
+    // 0) curves and per-request terms (all reads issued first)
+    const int nK = n * K;
+    int64_t lv[kProject ? 1 : SC_LBATCH];
+    if constexpr (!kProject) {
+#pragma unroll
+        for (int j = 0; j < SC_LBATCH; ++j) {
+            const int e = j * SC_THREADS + tid;
+            lv[j] = a.load[e < nK ? e : nK - 1];
+        }
+    }
+    int32_t bad = 0;
+    {
+        const int q = tid;                           // rpb <= SC_THREADS
+        int r = row0 + q;
+        r = r < a.N ? r : a.N - 1;
+        const int sv = a.inst[r], cv = a.cur[r], rv = a.rem[r];
+        if (q < rpb) {
+            const bool live = row0 + q < a.N;
+            const ReqTerms rt = request_terms(sv, cv, rv, n, b, H);
+            bad = live ? rt.bad : 0;
+            r_s[q] = live ? rt.s : -1;
+            r_ke[q] = rt.ke;
+            r_alpha[q] = rt.alpha;
+            r_p[q] = rt.p;
+        }
+    }
+    bad = wave_or_i32(bad);
+    if (lane == 0) report_error(a.err_word, bad);
+    if constexpr (kProject) {
+        // histograms by k_e: hA in PM's rows, hN in SM's, hP in L's (the
+        // three are contiguous); invalid requests add nothing
+        for (int e = tid; e < 3 * n * K1; e += SC_THREADS) lL[e] = 0;
+        __syncthreads();
+        for (int base = 0; base < a.N; base += SC_THREADS * SC_PBATCH) {
+            int sv[SC_PBATCH], cv[SC_PBATCH], rv[SC_PBATCH];
+#pragma unroll
+            for (int j = 0; j < SC_PBATCH; ++j) {
+                const int r = base + j * SC_THREADS + tid;
+                const int rc = r < a.N ? r : a.N - 1;
+                sv[j] = a.inst[rc];
+                cv[j] = a.cur[rc];
+                rv[j] = a.rem[rc];
+            }
+#pragma unroll
+            for (int j = 0; j < SC_PBATCH; ++j) {
+                if (base + j * SC_THREADS + tid >= a.N) continue;
+                const ReqTerms rt = request_terms(sv[j], cv[j], rv[j], n, b, H);
+                if (rt.s < 0) continue;
+                const int row = rt.s * K1;
+                if (rt.ke > 0) {
+                    atomicAdd((unsigned long long*)&lPM[row + rt.ke], (unsigned long long)rt.alpha);
+                    atomicAdd((unsigned long long*)&lSM[row + rt.ke], 1ull);
+                }
+                if (rt.p != 0) atomicAdd((unsigned long long*)&lL[row + rt.ke], (unsigned long long)rt.p);
+            }
+        }
+        __syncthreads();
+        build_curves<SC_THREADS>(lPM, lSM, lL, n, K, bb);
+        __syncthreads();
+        if (g == 0)
+            for (int e = tid; e < nK; e += SC_THREADS) {
+                const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
+                a.load_out[e] = lL[t * K1 + (e - t * K)];
+            }
+    } else {
+#pragma unroll
+        for (int j = 0; j < SC_LBATCH; ++j) {
+            const int e = j * SC_THREADS + tid;
+            if (e < nK) {
+                const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
+                lL[t * K1 + (e - t * K)] = lv[j];
+            }
+        }
+        for (int t = tid; t < n; t += SC_THREADS) lL[t * K1 + K] = INT64_MIN;
+    }
+    for (int c = tid; c < RK_CODES; c += SC_THREADS) lhist[c] = 0;
+    __syncthreads();
+    build_pm_sm<SC_THREADS>(lL, lPM, lSM, n, K, bb);
+    __syncthreads();
+
+    // 1) this thread's candidate e = q n + t
+    int64_t base = INT64_MAX;                         // smallest target peak
+    for (int t = 0; t < n; ++t) {
+        const int64_t v = lSM[t * K1];
+        base = v < base ? v : base;
+    }
+    const int e = tid;
+    const uint32_t ec = (uint32_t)(e < cand ? e : cand - 1);
+    const int q = (int)fast_div(ec, (uint32_t)n, a.magic_n);
+    const int t = (int)ec - q * n;
+    const int r = row0 + q;
+    const bool live = e < cand && r < a.N;
+    const int s = r_s[q], ke = r_ke[q];
+    const int64_t* pm_t = lPM + t * K1;
+    const int64_t* sm_t = lSM + t * K1;
+    const int64_t mv = move_score(pm_t, sm_t, lL[t * K1 + ke], ke, K, r_alpha[q], r_p[q]);
+    const int64_t sc = s < 0 ? -1 : (t == s ? sm_t[0] : mv);
+    const bool mig = live && s >= 0 && t != s;
+    if (live && a.scores) a.scores[(int64_t)r * n + t] = sc;
+    if (e < cand) {
+        ks[e] = mig ? sc : kInfS;
+        ki[e] = mig ? (uint32_t)((int64_t)r * n + t) : kInfI;
+    }
+    // code and rank of this key among the group's keys of equal code
+    const uint32_t code = mig ? key_code((uint64_t)(sc - base)) : 0;
+    const int lrank = mig ? atomicAdd(&lhist[code], 1) : 0;
+    __syncthreads();
+
+    // 2) best migration per request: smallest (score, t) over t != s
+    for (int qq = tid; qq < rpb; qq += SC_THREADS) {
+        const int rr = row0 + qq;
+        if (rr >= a.N) continue;
+        int64_t bs = kInfS;
+        uint32_t bi = kInfI;
+        for (int tt = 0; tt < n; ++tt) {
+            const int ee = qq * n + tt;
+            if (key_less(ks[ee], ki[ee], bs, bi)) { bs = ks[ee]; bi = ki[ee]; }
+        }
+        const bool none = bi == kInfI;
+        if (a.best_target) a.best_target[rr] = none ? -1 : (int32_t)(bi - (uint32_t)((int64_t)rr * n));
+        if (a.best_score) a.best_score[rr] = none ? -1 : bs;
+    }
+
+    // 3) code histogram -> exclusive offsets (4 codes per thread), global counts
+    constexpr int PER = RK_CODES / SC_THREADS;
+    int c4[PER], own = 0;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        c4[u] = lhist[tid * PER + u];
+        own += c4[u];
+    }
+    const int inc = wave_incl_add_i32(own);
+    if (lane == 63) wtot[tid >> 6] = inc;
+    __syncthreads();
+    int before = inc - own;
+    for (int w = 0; w < (tid >> 6); ++w) before += wtot[w];
+    int32_t* go = rk.offs + (int64_t)g * (RK_CODES + 1);
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int c = tid * PER + u;
+        go[c] = before;
+        if (c4[u]) atomicAdd(&rk.ghist[c], (uint32_t)c4[u]);
+        lhist[c] = before;                            // now the offset
+        before += c4[u];
+    }
+    if (tid == SC_THREADS - 1) go[RK_CODES] = before;  // this group's migration count
+    if (g == 0 && tid == 0) *rk.base = base;
+    __syncthreads();
+    if (mig) {
+        const int64_t at = (int64_t)g * cand + lhist[code] + lrank;
+        rk.keys_s[at] = sc;
+        rk.keys_i[at] = (uint32_t)((int64_t)r * n + t);
+    }
+}
+
 
 // ---------------------------------------------------------------------------
 // small rounds: one workgroup scores and ranks
@@ -1559,7 +1717,7 @@ __global__ void fill_i32_kernel(int32_t* p, int count, int32_t v) {
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-ScorePlan plan_score(const star_score_params& p) {
+ScorePlan plan_score(const star_score_params& p, bool project) {
     ScorePlan pl;
     const int n = p.load.n_inst;
     const int N = p.load.n_req;
@@ -1582,8 +1740,9 @@ ScorePlan plan_score(const star_score_params& p) {
     pl.rank2 = pl.fused && p.top_k > 0 && pl.groups <= RK_MAX_GROUPS && pl.cand <= SC_THREADS;
     if (pl.rank2) {
         pl.small = false;
-        pl.ghist_off = off;
-        off = align_up(off + RK_CODES * 4, 256);
+        pl.project_in = project && N > 0 && N <= SC_PROJECT_MAX_REQ;
+        static_assert(RK_CODES == 1024, "the header's histogram has 1024 codes");
+        pl.ghist_off = kHdrScoreHist;             // in the header: zero between calls
         pl.base_off = off;
         off = align_up(off + 8, 256);
         pl.keys_s_off = off;
@@ -1646,7 +1805,7 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
                         const int32_t* rem, const int32_t* inst, const int64_t* load,
                         int64_t* scores, int32_t* best_target, int64_t* best_score,
                         int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score, char* ws,
-                        int32_t* err_word, hipStream_t stream) {
+                        int32_t* err_word, hipStream_t stream, int64_t* load_out) {
     const star_load_params& lp = p.load;
     if (lp.n_req == 0) {
         if (p.top_k > 0) {                       // no candidates: top-k is all -1
@@ -1672,9 +1831,12 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
         rk.keys_s = (int64_t*)(ws + pl.keys_s_off);
         rk.keys_i = (uint32_t*)(ws + pl.keys_i_off);
         rk.offs = (int32_t*)(ws + pl.offs_off);
-        hipError_t e = set_lds((const void*)score_rank_kernel, pl.lds, RK_CODES * 4 + 64);
+        a.load_out = load_out;
+        using Kern = void (*)(ScoreArgs, RankArgs);
+        const Kern kern = pl.project_in ? score_rank_kernel<true> : score_rank_kernel<false>;
+        hipError_t e = set_lds((const void*)kern, pl.lds, RK_CODES * 4 + 64);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(score_rank_kernel, dim3(pl.groups), dim3(SC_THREADS), pl.lds, stream, a, rk);
+        hipLaunchKernelGGL(kern, dim3(pl.groups), dim3(SC_THREADS), pl.lds, stream, a, rk);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         FinalArgs f = {};

@@ -222,6 +222,39 @@ STAR_API star_status star_score_migrations(const star_score_params* p, const int
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
 }
 
+STAR_API size_t star_project_and_score_workspace_size(const star_score_params* p) {
+    if (check_score_params(p) != STAR_OK) return 0;
+    return plan_score(*p, true).total;
+}
+
+STAR_API star_status star_project_and_score(const star_score_params* p, const int32_t* cur_len,
+                                            const int32_t* rem_len, const int32_t* inst_of,
+                                            int64_t* load, int64_t* scores, int32_t* best_target,
+                                            int64_t* best_score, int32_t* topk_req,
+                                            int32_t* topk_tgt, int64_t* topk_score, void* ws,
+                                            size_t ws_bytes, void* stream) {
+    star_status st = check_score_params(p);
+    if (st != STAR_OK) return st;
+    if (!load) return STAR_ERR_INVALID_ARG;
+    if (p->load.n_req > 0 && (!cur_len || !rem_len || !inst_of)) return STAR_ERR_INVALID_ARG;
+    const bool any_topk = topk_req || topk_tgt || topk_score;
+    const bool all_topk = topk_req && topk_tgt && topk_score;
+    if (p->top_k > 0 ? !all_topk : any_topk) return STAR_ERR_INVALID_ARG;
+    const ScorePlan pl = plan_score(*p, true);
+    st = check_ws(ws, ws_bytes, pl.total);
+    if (st != STAR_OK) return st;
+    int32_t* err = (int32_t*)((char*)ws + kHdrErrorWord);
+    hipError_t e = hipSuccess;
+    if (!pl.project_in)
+        e = launch_project_load(p->load, plan_load(p->load), cur_len, rem_len, inst_of, load, err,
+                                (hipStream_t)stream);
+    if (e == hipSuccess)
+        e = launch_score(*p, pl, cur_len, rem_len, inst_of, load, scores, best_target, best_score,
+                         topk_req, topk_tgt, topk_score, (char*)ws, err, (hipStream_t)stream,
+                         pl.project_in ? load : nullptr);
+    return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
+}
+
 // ---------------------------------------------------------------------------
 // time-weighted variance gains
 // ---------------------------------------------------------------------------

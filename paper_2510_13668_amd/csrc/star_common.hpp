@@ -11,8 +11,14 @@ namespace star {
 constexpr int kWave = 64;
 
 // Workspace header layout (STAR_WS_HEADER_BYTES bytes at the start of every
-// workspace).
-constexpr size_t kHdrErrorWord = 0;   // int32: sticky OR of STAR_DEV_* bits
+// workspace, never used as scratch: whatever must hold between calls lives
+// here, and the calls that use a counter or the histogram leave it at zero).
+constexpr size_t kHdrErrorWord = 0;     // int32: sticky OR of STAR_DEV_* bits
+constexpr size_t kHdrVarTicket = 64;    // uint32: finished variance-scoring workgroups
+constexpr size_t kHdrPlanDone = 72;     // int32: the migration plan has stopped
+constexpr size_t kHdrPlanCount = 76;    // int32: moves made by the plan
+constexpr size_t kHdrScoreHist = 256;   // uint32[1024]: key-code histogram of the ranking
+static_assert(kHdrScoreHist + 1024 * 4 <= STAR_WS_HEADER_BYTES, "header holds the histogram");
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }

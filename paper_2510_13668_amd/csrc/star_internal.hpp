@@ -51,6 +51,8 @@ struct ScorePlan {
     bool fused = false;   // PM/SM built in LDS by the scoring kernel
     bool small = false;   // one workgroup scores and ranks everything
     bool rank2 = false;   // fused scoring that code-sorts its keys, then one ranking workgroup
+    bool project_in = false; // rank2: the scoring workgroups project the curves themselves
+                             // (star_project_and_score only)
     size_t ghist_off = 0, base_off = 0, keys_s_off = 0, keys_i_off = 0, offs_off = 0;
     int rpb = 0;          // requests per scoring workgroup
     int cand = 0;         // candidates per scoring workgroup (rpb * n)
@@ -61,12 +63,12 @@ struct ScorePlan {
     size_t pm_off = 0, sm_off = 0, scores_off = 0, bscore_off = 0, btarget_off = 0, total = 0;
     size_t lds = 0;       // dynamic LDS of the scoring kernel (or of the small path's one)
 };
-ScorePlan plan_score(const star_score_params& p);
+ScorePlan plan_score(const star_score_params& p, bool project = false);
 hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const int32_t* cur,
                         const int32_t* rem, const int32_t* inst, const int64_t* load,
                         int64_t* scores, int32_t* best_target, int64_t* best_score,
                         int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score, char* ws,
-                        int32_t* err_word, hipStream_t stream);
+                        int32_t* err_word, hipStream_t stream, int64_t* load_out = nullptr);
 
 struct VarPlan {
     int lg = 0;           // lanes per request = 2^lg (<= 16)

@@ -51,7 +51,6 @@ constexpr int VP_THREADS = 256;
 constexpr int VS_THREADS = 256;
 constexpr int VS_WAVES = VS_THREADS / kWave;
 
-constexpr size_t kHdrVarTicket = 64;   // workspace header: finished-workgroup ticket
 // Grids up to this many workgroups find the best move in the scoring kernel
 // (the last workgroup to finish reduces the partials); larger ones hand the
 // partials to a one-workgroup kernel, because every workgroup's release
@@ -62,8 +61,6 @@ constexpr int PLAN_MAX_INST = 1024;      // instances a plan classifies in LDS
 constexpr int PA_THREADS = 256;          // the plan's update workgroup
 constexpr int PLAN_MAX_BLOCKS = 1 << 20; // scoring workgroups of a plan pass (one tile each)
 
-constexpr size_t kHdrPlanDone = 72;      // workspace header: the plan has stopped
-constexpr size_t kHdrPlanCount = 76;     // workspace header: moves made
 
 __device__ inline u128 wide(int64_t v) { return (u128)(s128)v; }
 

@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libstar.so")
 
 STAR_OK = 0
-STAR_WS_HEADER_BYTES = 256
+STAR_WS_HEADER_BYTES = 8192
 STAR_MAX_TOP_K = 1024
 F32, BF16 = 0, 1
 ACT_RELU, ACT_GELU = 0, 1
@@ -90,6 +90,11 @@ def lib():
         L.star_score_migrations.restype = ctypes.c_int
         L.star_score_migrations.argtypes = ([ctypes.POINTER(ScoreParams)] + [_P] * 11 +
                                             [ctypes.c_size_t, _P])
+        L.star_project_and_score_workspace_size.restype = ctypes.c_size_t
+        L.star_project_and_score_workspace_size.argtypes = [ctypes.POINTER(ScoreParams)]
+        L.star_project_and_score.restype = ctypes.c_int
+        L.star_project_and_score.argtypes = ([ctypes.POINTER(ScoreParams)] + [_P] * 11 +
+                                             [ctypes.c_size_t, _P])
         L.star_score_variance_workspace_size.restype = ctypes.c_size_t
         L.star_score_variance_workspace_size.argtypes = [ctypes.POINTER(LoadParams)]
         L.star_score_variance.restype = ctypes.c_int
@@ -216,6 +221,22 @@ def score_migrations(p: ScoreParams, cur_len, rem_len, inst_of, load, scores, be
     _dev(cur_len, rem_len, inst_of, load, scores, best_target, best_score, topk_req, topk_tgt,
          topk_score)
     _check("star_score_migrations", lib().star_score_migrations(
+        ctypes.byref(p), _ptr(cur_len), _ptr(rem_len), _ptr(inst_of), _ptr(load), _ptr(scores),
+        _ptr(best_target), _ptr(best_score), _ptr(topk_req), _ptr(topk_tgt), _ptr(topk_score),
+        ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))
+
+
+def project_and_score_workspace_size(p: ScoreParams) -> int:
+    return lib().star_project_and_score_workspace_size(ctypes.byref(p))
+
+
+def project_and_score(p: ScoreParams, cur_len, rem_len, inst_of, load, scores, best_target,
+                      best_score, topk_req, topk_tgt, topk_score, ws: Workspace, stream=None):
+    """star_project_and_score: load projection and migration scoring in one
+    call (`load` is an output)."""
+    _dev(cur_len, rem_len, inst_of, load, scores, best_target, best_score, topk_req, topk_tgt,
+         topk_score)
+    _check("star_project_and_score", lib().star_project_and_score(
         ctypes.byref(p), _ptr(cur_len), _ptr(rem_len), _ptr(inst_of), _ptr(load), _ptr(scores),
         _ptr(best_target), _ptr(best_score), _ptr(topk_req), _ptr(topk_tgt), _ptr(topk_score),
         ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))

@@ -53,13 +53,20 @@ class Predictor:
 
 
 class Rescheduler:
-    """Buffers and workspaces for (b) and (c) at fixed sizes."""
+    """Buffers and workspaces for (b) and (c) at fixed sizes.  fused: one
+    star_project_and_score call per round (one workspace) instead of
+    star_project_load then star_score_migrations."""
 
-    def __init__(self, n_req, n_inst, bucket, n_buckets, top_k, want_scores=True):
+    def __init__(self, n_req, n_inst, bucket, n_buckets, top_k, want_scores=True, fused=False):
         self.lp = star.load_params(n_req, n_inst, bucket, n_buckets)
         self.sp = star.score_params(n_req, n_inst, bucket, n_buckets, top_k)
-        self.ws_load = star.Workspace(star.project_load_workspace_size(self.lp))
-        self.ws_score = star.Workspace(star.score_workspace_size(self.sp))
+        self.fused = fused
+        if fused:
+            self.ws_load = self.ws_score = star.Workspace(
+                star.project_and_score_workspace_size(self.sp))
+        else:
+            self.ws_load = star.Workspace(star.project_load_workspace_size(self.lp))
+            self.ws_score = star.Workspace(star.score_workspace_size(self.sp))
         self.load = torch.empty((n_inst, n_buckets), dtype=torch.int64, device=DEV)
         self.scores = (torch.empty((n_req, n_inst), dtype=torch.int64, device=DEV)
                        if want_scores else None)
@@ -72,6 +79,11 @@ class Rescheduler:
         self.ts = torch.empty(k, dtype=torch.int64, device=DEV) if top_k else None
 
     def run(self, cur, rem, inst, stream=None):
+        if self.fused:
+            star.project_and_score(self.sp, cur, rem, inst, self.load, self.scores,
+                                   self.best_target, self.best_score, self.tr, self.tt, self.ts,
+                                   self.ws_score, stream)
+            return
         star.project_load(self.lp, cur, rem, inst, self.load, self.ws_load, stream)
         star.score_migrations(self.sp, cur, rem, inst, self.load, self.scores, self.best_target,
                               self.best_score, self.tr, self.tt, self.ts, self.ws_score, stream)

@@ -81,7 +81,7 @@ def test_predict_rejects_null_pointers_and_workspace(L):
     need = star.predict_workspace_size(p)
     # 64 x 64 tiles: 16 x 8 of them, 4 K-splits of a [1024, 512] fp32
     # partial product, plus the header
-    assert need == 256 + 4 * 1024 * 512 * 4
+    assert need == star.STAR_WS_HEADER_BYTES + 4 * 1024 * 512 * 4
     assert _predict(L, p, ws_bytes=need - 1) == -4
     assert _predict(L, p, ws=None) == -4
     assert _predict(L, p, ws=ctypes.c_void_p((1 << 20) + 64)) == -4   # not 256-aligned
@@ -89,7 +89,7 @@ def test_predict_rejects_null_pointers_and_workspace(L):
 
 def test_load_and_score_validation(L):
     lp = star.load_params(1024, 8, 64, 256)
-    assert star.project_load_workspace_size(lp) == 256
+    assert star.project_load_workspace_size(lp) == star.STAR_WS_HEADER_BYTES
     f = FAKE
     assert L.star_project_load(ctypes.byref(star.load_params(1, 0, 1, 1)), f, f, f, f, f, 256, None) == -1
     assert L.star_project_load(ctypes.byref(star.load_params(1, 1, 0, 1)), f, f, f, f, f, 256, None) == -1
@@ -106,11 +106,12 @@ def test_load_and_score_validation(L):
     # ranking keeps per-workgroup sorted keys (or scores and best moves, and
     # PM/SM for large curve sets) in the workspace; without a top-k and with
     # the curves in LDS only the header is needed
-    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 0)) >= 256
-    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 256)) > 256
+    H = star.STAR_WS_HEADER_BYTES
+    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 0)) >= H
+    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 256)) > H
     sp = star.score_params(4096, 16, 64, 512, 256)
     need = star.score_workspace_size(sp)
-    assert need > 256
+    assert need > H
     args = [f] * 10
     assert L.star_score_migrations(ctypes.byref(sp), *args, f, need - 1, None) == -4
     nk = star.score_params(1024, 8, 64, 256, 0)
@@ -123,12 +124,34 @@ def test_load_and_score_validation(L):
                                    1 << 30, None) == -2
 
 
+def test_project_and_score_validation(L):
+    f = FAKE
+    sp = star.score_params(1024, 8, 64, 256, 256)
+    need = star.project_and_score_workspace_size(sp)
+    # the same workspace layout as scoring alone (its ticket sits in the header)
+    assert need == star.score_workspace_size(sp)
+    args = [f] * 10
+    assert L.star_project_and_score(None, *args, f, need, None) == -1
+    assert L.star_project_and_score(ctypes.byref(sp), *args, f, need - 1, None) == -4
+    assert L.star_project_and_score(ctypes.byref(sp), *args, None, need, None) == -4
+    # load is an output here and may not be NULL
+    assert L.star_project_and_score(ctypes.byref(sp), f, f, f, None, *args[4:], f, need,
+                                    None) == -1
+    # top-k outputs must be NULL iff top_k == 0
+    nk = star.score_params(1024, 8, 64, 256, 0)
+    assert L.star_project_and_score(ctypes.byref(nk), *args, f, 1 << 30, None) == -1
+    assert L.star_project_and_score(ctypes.byref(sp), *args[:7], None, f, f, f, 1 << 30,
+                                    None) == -1
+    assert L.star_project_and_score(ctypes.byref(star.score_params(4, 5000, 1, 1, 1)), *args, f,
+                                    1 << 30, None) == -2
+
+
 def test_score_variance_validation(L):
     f = FAKE
     lp = star.load_params(1024, 8, 64, 256)
     need = star.score_variance_workspace_size(lp)
     # 128-bit prefix tables: two per instance and one for the weights, K + 1 each
-    assert need >= 256 + (2 * 8 + 3) * 257 * 16
+    assert need >= star.STAR_WS_HEADER_BYTES + (2 * 8 + 3) * 257 * 16
     args = [f] * 9            # cur, rem, inst, load, beta, gain, best_target, best_gain, move
     assert L.star_score_variance(ctypes.byref(lp), *args, f, need - 1, None) == -4
     assert L.star_score_variance(ctypes.byref(lp), *args[:4], None, *args[5:], f, need, None) == -1
@@ -172,7 +195,7 @@ def test_mlp4_validation(L):
     mp = star.mlp4_params(1024, 3584, 2048, 512, 64, star.BF16)
     need = star.predict_mlp4_workspace_size(mp)
     # split-K partials of both layers plus the first layer's bf16 output
-    assert need >= 256 + 1024 * 2048 * (4 + 2) + 1024 * 512 * 4
+    assert need >= star.STAR_WS_HEADER_BYTES + 1024 * 2048 * (4 + 2) + 1024 * 512 * 4
     args = [f] * 11           # hidden, w1, b1, w2, b2, w3, b3, w4, ema, expected, rem
     args[2] = args[4] = args[6] = None
     assert L.star_predict_mlp4(ctypes.byref(mp), *args, f, need - 1, None) == -4

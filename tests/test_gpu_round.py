@@ -1,7 +1,8 @@
 """GPU parity of (b) load projection and (c) scoring/ranking against the
 oracle: bit-exact load curves, scores, best targets and top-k triples, at the
 five workloads' full sizes and on adversarial inputs; plus the chained round
-(a) -> (b) -> (c), device-error reporting and HIP-graph replay."""
+(a) -> (b) -> (c), device-error reporting and HIP-graph replay.  Cases marked
+`fused` run (b) and (c) as one star_project_and_score call."""
 import zlib
 
 import numpy as np
@@ -15,29 +16,31 @@ from gpu_util import Predictor, Rescheduler, assert_round_equal, to_dev
 pytestmark = pytest.mark.gpu
 
 
-def _gpu_round(cur, rem, inst, n, b, K, top_k, want_scores=True):
-    rs = Rescheduler(len(cur), n, b, K, top_k, want_scores)
+def _gpu_round(cur, rem, inst, n, b, K, top_k, want_scores=True, fused=False):
+    rs = Rescheduler(len(cur), n, b, K, top_k, want_scores, fused)
     rs.run(to_dev(cur), to_dev(rem), to_dev(inst))
     out = rs.result()
     out["error"] = rs.ws_load.read_device_error() | rs.ws_score.read_device_error()
     return out
 
 
-def _check(cur, rem, inst, n, b, K, top_k, want_scores=True):
-    print(f"round N={len(cur)} n={n} b={b} K={K} top_k={top_k}", flush=True)
-    gpu = _gpu_round(cur, rem, inst, n, b, K, top_k, want_scores)
+def _check(cur, rem, inst, n, b, K, top_k, want_scores=True, fused=False):
+    print(f"round N={len(cur)} n={n} b={b} K={K} top_k={top_k} fused={fused}", flush=True)
+    gpu = _gpu_round(cur, rem, inst, n, b, K, top_k, want_scores, fused)
     ref = oracle.round_(cur, rem, inst, n_inst=n, bucket=b, n_buckets=K, top_k=top_k)
     assert_round_equal(gpu, ref)
     assert gpu["error"] == ref["flags"]
     return gpu, ref
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
 @pytest.mark.parametrize("name", ["8b_batch", "32b_long_mix", "continuous", "rebalance_scan"])
-def test_workload_true_lengths(name):
+def test_workload_true_lengths(name, fused):
     """Oracle-predictor mode: the workload's true remaining lengths."""
     wl = synth.WORKLOADS[name]
     x = synth.make_inputs(wl, steps=1, n_req=1)
-    _check(x.cur_len, x.true_len, x.inst_of, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k)
+    _check(x.cur_len, x.true_len, x.inst_of, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k,
+           fused=fused)
 
 
 def test_long_output_stress_mix():
@@ -107,8 +110,9 @@ ADVERSARIAL = [
 ]
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
 @pytest.mark.parametrize("case", ADVERSARIAL, ids=[c[0] for c in ADVERSARIAL])
-def test_adversarial(case):
+def test_adversarial(case, fused):
     label, N, n, b, K, top_k, cur_hi, len_hi, contiguous, empty = case
     rng = np.random.default_rng(zlib.crc32(label.encode()))
     cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=cur_hi, len_hi=len_hi,
@@ -118,11 +122,12 @@ def test_adversarial(case):
     special = np.array([1, b, 2 * b, H - 1, H, H + 1, 3 * H], np.int64)
     m = min(len(special), N)
     rem[:m] = np.clip(special[:m], 1, 2 ** 31 - 1).astype(np.int32)
-    _check(cur, rem, inst, n, b, K, top_k)
+    _check(cur, rem, inst, n, b, K, top_k, fused=fused)
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
 @pytest.mark.parametrize("N", [256, 6000])
-def test_ties_from_duplicated_requests(N):
+def test_ties_from_duplicated_requests(N, fused):
     """Many equal scores; N = 6000 takes the two-stage (pruned) ranking."""
     rng = np.random.default_rng(3)
     n = 8
@@ -131,7 +136,7 @@ def test_ties_from_duplicated_requests(N):
     inst = rng.integers(0, n, N).astype(np.int32)
     cur[::3] = 5
     rem[::5] = 64
-    _check(cur, rem, inst, n, 64, 32, 300)
+    _check(cur, rem, inst, n, 64, 32, 300, fused=fused)
 
 
 def _key_bits(ref, inst, n):
@@ -176,7 +181,8 @@ def test_wide_keys_many_instances():
     assert int(v.max() - v.min()).bit_length() + int(n - 1).bit_length() > 64
 
 
-def test_invalid_requests_are_skipped_and_reported():
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_invalid_requests_are_skipped_and_reported(fused):
     rng = np.random.default_rng(4)
     N, n = 500, 6
     cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=3000, len_hi=3000)
@@ -185,16 +191,53 @@ def test_invalid_requests_are_skipped_and_reported():
     cur[20] = 0
     rem[30] = 0
     rem[31] = -5
-    gpu, ref = _check(cur, rem, inst, n, 64, 64, 128)
+    gpu, ref = _check(cur, rem, inst, n, 64, 64, 128, fused=fused)
     assert gpu["error"] == star.DEV_BAD_INST | star.DEV_BAD_CUR | star.DEV_BAD_REM
     assert (gpu["best_target"][[10, 11, 20, 30, 31]] == -1).all()
 
 
-def test_empty_request_set():
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_empty_request_set(fused):
     gpu = _gpu_round(np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32),
-                     4, 8, 16, 10)
+                     4, 8, 16, 10, fused=fused)
     assert (gpu["load"] == 0).all()
     assert (gpu["topk_req"] == -1).all()
+
+
+# (N, n, b, K, top_k): curves projected in every scoring group, at 32, 35
+# and 188 groups; too many requests to project per group (the projection
+# kernel runs first); no top-k; curves too large for LDS
+FUSED_PATHS = [(1024, 8, 64, 256, 256), (700, 5, 16, 100, 64), (6000, 8, 64, 32, 300),
+               (10000, 8, 16, 40, 512), (900, 6, 32, 50, 0), (300, 64, 8, 80, 100)]
+
+
+def test_calls_of_every_path_share_a_workspace():
+    """Rounds of every path, one after another on one workspace sized for
+    the largest, with a predictor call on the same workspace before each
+    (its split-K partials fill the scratch area): the ranking's code
+    histogram lives in the workspace header, which no call uses as scratch,
+    and every call must equal the oracle."""
+    rng = np.random.default_rng(21)
+    B, d, m, nb = 64, 512, 128, 32
+    w1 = synth.f32_to_bf16_bits((rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32))
+    w2 = synth.f32_to_bf16_bits((rng.standard_normal((nb, m)) / np.sqrt(m)).astype(np.float32))
+    hid = to_dev(synth.f32_to_bf16_bits(rng.standard_normal((B, d)).astype(np.float32)), True)
+    pr = Predictor(w1, w2, synth.bin_values(nb, 1.0, 4096.0), dtype=synth.BF16,
+                   act=synth.ACT_GELU, n_req=B, len_max=4096)
+    ws = star.Workspace(max([star.project_and_score_workspace_size(star.score_params(*c))
+                             for c in FUSED_PATHS] + [star.predict_workspace_size(pr.params(False))]))
+    pr.ws = ws
+    for rep in range(2):
+        for N, n, b, K, top_k in FUSED_PATHS:
+            print(f"fused rep={rep} N={N} n={n} b={b} K={K} top_k={top_k}", flush=True)
+            pr.run(hid)
+            cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=4000, len_hi=b * K + 50)
+            rs = Rescheduler(N, n, b, K, top_k, fused=True)
+            rs.ws_load = rs.ws_score = ws
+            rs.run(to_dev(cur), to_dev(rem), to_dev(inst))
+            ref = oracle.round_(cur, rem, inst, n_inst=n, bucket=b, n_buckets=K, top_k=top_k)
+            assert_round_equal(rs.result(), ref)
+            assert ws.read_device_error() == ref["flags"]
 
 
 def test_error_word_clears_after_read():
@@ -263,7 +306,8 @@ def test_pipelined_graph_rounds_match_eager():
     The whole chunk is captured as one HIP graph, as the benchmark runs it.
     Every replay (with eager work and synchronisations between replays)
     must leave the last two rounds' outputs and the EMA state equal to six
-    eager rounds run one after another."""
+    eager rounds run one after another.  The pipelined rounds use the fused
+    projection-and-scoring call, the eager ones the two separate calls."""
     wl = synth.WORKLOADS["continuous"]
     R = 6
     x = synth.make_inputs(wl, steps=R + 1)
@@ -286,7 +330,8 @@ def test_pipelined_graph_rounds_match_eager():
     want_ema = pr.ema.cpu().numpy().copy()
 
     P, S2 = torch.cuda.Stream(), torch.cuda.Stream()
-    slots = [Rescheduler(N, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k) for _ in range(2)]
+    slots = [Rescheduler(N, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k, fused=True)
+             for _ in range(2)]
     rems = [torch.empty(N, dtype=torch.int32, device="cuda") for _ in range(2)]
     exps = [torch.empty(N, dtype=torch.float32, device="cuda") for _ in range(2)]
     ev_pred = [torch.cuda.Event() for _ in range(2)]
