@@ -66,7 +66,7 @@ def _parse():
                          "launched); graph_pipelined = the same, 40 rounds per captured HIP "
                          "graph; eager = one stream, round after round; graph = one captured "
                          "graph per round")
-    ap.add_argument("--cpu-rounds", type=int, default=20,
+    ap.add_argument("--cpu-rounds", type=int, default=200,
                     help="rounds of the CPU oracle timed for the baseline (0 = skip)")
     ap.add_argument("--path", choices=("round", "variance", "plan", "mlp4", "sim"),
                     default="round",
