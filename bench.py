@@ -50,6 +50,7 @@ import numpy as np
 METRIC = "requests predicted+scored/sec at B=1024,d=4096; µs per reschedule round"
 WORKLOAD = "continuous"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 MFMA
 PEAK_HBM_GBS = 8000.0
 
 
@@ -68,11 +69,12 @@ def _parse():
                          "graph per round")
     ap.add_argument("--cpu-rounds", type=int, default=200,
                     help="rounds of the CPU oracle timed for the baseline (0 = skip)")
-    ap.add_argument("--path", choices=("round", "variance", "plan", "mlp4", "sim"),
+    ap.add_argument("--path", choices=("round", "variance", "plan", "mlp4", "sim", "configs"),
                     default="round",
                     help="round: the full rescheduling round; variance: projection + "
                          "variance-gain scoring; plan: Algorithm 1 repeated; mlp4: the paper's "
-                         "4-layer regression head")
+                         "4-layer regression head; sim: the event-driven simulation; configs: "
+                         "per-call times at every workload's shape")
     ap.add_argument("--moves", type=int, default=16, help="max_moves of --path plan")
     ap.add_argument("--workload", default="rebalance_scan",
                     help="workload of --path variance")
@@ -552,6 +554,121 @@ def bench_mlp4(args):
     print(json.dumps(out), flush=True)
 
 
+def bench_configs(args):
+    """Per-call times of the round's two calls at each workload's own shape,
+    with the first-layer GEMM's MFMA fraction and the projection-and-scoring
+    call's compulsory bytes over its time (an HBM fraction)."""
+    import torch
+    from paper_2510_13668_amd import star, synth
+
+    dev = "cuda"
+    stream = torch.cuda.Stream()
+    he = HipEvents()
+    rows = []
+    for name in synth.WORKLOAD_ORDER:
+        wl = synth.WORKLOADS[name]
+        x = synth.make_inputs(wl, steps=1)
+        N, d, m, nb = wl.n_req, wl.d_model, wl.d_hidden, wl.n_bins
+        n, b, K, top_k = wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k
+        bf16 = wl.dtype == synth.BF16
+
+        def up(a, as_bf16=False):
+            t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16) if as_bf16 else a).to(dev)
+            return t.view(torch.bfloat16) if as_bf16 else t
+        hid, w1, w2 = up(x.hidden, bf16), up(x.w1, bf16), up(x.w2, bf16)
+        bins, cur, inst = up(x.bin_values), up(x.cur_len), up(x.inst_of)
+        ema = torch.zeros(N, dtype=torch.float32, device=dev) if wl.ema_alpha > 0 else None
+        expected = torch.empty(N, dtype=torch.float32, device=dev)
+        rem = torch.empty(N, dtype=torch.int32, device=dev)
+        load = torch.empty((n, K), dtype=torch.int64, device=dev)
+        scores = torch.empty((N, n), dtype=torch.int64, device=dev)
+        best_t = torch.empty(N, dtype=torch.int32, device=dev)
+        best_s = torch.empty(N, dtype=torch.int64, device=dev)
+        tr = torch.empty(top_k, dtype=torch.int32, device=dev)
+        tt = torch.empty(top_k, dtype=torch.int32, device=dev)
+        ts = torch.empty(top_k, dtype=torch.int64, device=dev)
+        pp = star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, False, wl.len_max)
+        sp = star.score_params(N, n, b, K, top_k)
+        ws_p = star.Workspace(star.predict_workspace_size(pp))
+        ws_s = star.Workspace(star.project_and_score_workspace_size(sp))
+        # oracle-predictor mode where the workload has true remaining lengths
+        rem_in = up(x.true_len) if x.true_len is not None else rem
+
+        def predict(p=pp):
+            star.predict(p, hid, w1, None, w2, None, bins, ema, expected, rem, ws_p, stream)
+
+        def project_score():
+            star.project_and_score(sp, cur, rem_in, inst, load, scores, best_t, best_s, tr, tt,
+                                   ts, ws_s, stream)
+
+        reps = 20 if N * d >= (1 << 27) else args.steps
+
+        def timed(fn):
+            for _ in range(5):
+                fn()
+            torch.cuda.synchronize()
+            t0 = torch.cuda.Event(enable_timing=True)
+            t1 = torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            for _ in range(reps):
+                fn()
+            t1.record(stream)
+            torch.cuda.synchronize()
+            return t0.elapsed_time(t1) * 1e3 / reps
+
+        predict_us = timed(predict)
+        ps_us = timed(project_score)
+        round_us = timed(lambda: (predict(), project_score()))
+        evs = he.create(2 * reps)
+        arrs = [(ctypes.c_void_p * 2)(evs[2 * i].value, evs[2 * i + 1].value) for i in range(reps)]
+        pps = [star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, False, wl.len_max,
+                                   ctypes.cast(a, ctypes.c_void_p)) for a in arrs]
+        torch.cuda.synchronize()
+        for i in range(reps):
+            predict(pps[i])
+        torch.cuda.synchronize()
+        g_us = float(np.mean([he.elapsed_ms(evs[2 * i], evs[2 * i + 1]) for i in range(reps)])) * 1e3
+        he.destroy(evs)
+        flops = 2.0 * N * d * m
+        peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+        ps_bytes = 12 * N + 8 * n * K + 8 * N * n + 12 * N + 16 * top_k
+        rows.append({
+            "workload": name, "n_req": N, "d_model": d, "d_hidden": m, "n_bins": nb,
+            "n_inst": n, "n_buckets": K, "top_k": top_k, "dtype": "bf16" if bf16 else "f32",
+            "rem_len": "true lengths" if x.true_len is not None else "predicted",
+            "predict_us": predict_us, "project_and_score_us": ps_us, "round_us": round_us,
+            "gemm1_us": g_us, "gemm1_tflops": flops / (g_us * 1e-6) / 1e12,
+            "gemm1_frac": flops / (g_us * 1e-6) / 1e12 / peak, "gemm1_peak_tflops": peak,
+            "project_and_score_bytes": ps_bytes,
+            "project_and_score_gbs": ps_bytes / (ps_us * 1e-6) / 1e9,
+            "project_and_score_hbm_frac": ps_bytes / (ps_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+            "reps": reps})
+        print(f"{name}: predict {predict_us:.1f} us (GEMM1 {g_us:.1f} us, "
+              f"{rows[-1]['gemm1_frac'] * 100:.1f}% of peak), project+score {ps_us:.1f} us",
+              file=sys.stderr, flush=True)
+        del hid, w1, w2, ws_p, ws_s, scores
+        torch.cuda.empty_cache()
+
+    out = {
+        "metric": "per-call microseconds of star_predict and star_project_and_score at each "
+                  "workload's shape",
+        "value": rows[-1]["round_us"],
+        "unit": "us per round at the largest workload",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": 5,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 (tiny: f32)",
+        "data": "synthetic",
+        "config": {"workload": "the five workloads, one decode step each; (b)(c) on the "
+                               "workload's true remaining lengths where it has them"},
+        "configs": rows,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def bench_sim(args):
     import dataclasses
     from paper_2510_13668_amd import sim
@@ -634,6 +751,9 @@ def main():
         return
     if args.path == "sim":
         bench_sim(args)
+        return
+    if args.path == "configs":
+        bench_configs(args)
         return
 
     import torch
@@ -810,7 +930,23 @@ def main():
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) / (reps * CHUNK)
 
+    def eager_percentiles():
+        """Each eager round bracketed by its own events: p50 / p99 in us."""
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for i in range(args.warmup):
+            round_((i + 1) % S)
+        torch.cuda.synchronize()
+        for i, (a, b_) in enumerate(evs):
+            a.record(stream)
+            round_((args.warmup + i + 1) % S)
+            b_.record(stream)
+        torch.cuda.synchronize()
+        t = np.array([a.elapsed_time(b_) * 1e3 for a, b_ in evs])
+        return float(np.percentile(t, 50)), float(np.percentile(t, 99))
+
     ms_mode = {m: timed(m) for m in ("eager", "graph")}
+    p50, p99 = eager_percentiles()
     ms_mode["pipelined"] = timed_pipelined()
     ms_mode["graph_pipelined"] = timed_graph_pipelined()
     ms_step = ms_mode[args.mode]
@@ -856,6 +992,8 @@ def main():
         "us_per_round_pipelined": ms_mode["pipelined"] * 1e3,
         "us_per_round_graph_pipelined": ms_mode["graph_pipelined"] * 1e3,
         "us_per_round_eager": ms_mode["eager"] * 1e3,
+        "us_per_round_eager_p50": p50,
+        "us_per_round_eager_p99": p99,
         "us_per_round_graph": ms_mode["graph"] * 1e3,
         "roofline": {"kernel": "gemm1_splitk_kernel (bf16 MFMA, H[1024,4096] x W1[512,4096]^T)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,

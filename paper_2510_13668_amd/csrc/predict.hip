@@ -12,7 +12,8 @@
 //   batches still launch ~256 workgroups.  Partials are fp32, reduced later
 //   in a fixed order (deterministic results).
 // Kernel 2 (head): 4 rows per workgroup (many workgroups, so the split-K
-//   partial reads have plenty of loads in flight): fixed-order split-K
+//   partial reads have plenty of loads in flight), 16 for large batches:
+//   fixed-order split-K
 //   reduction, bias, activation, the bin GEMM (bf16 MFMA 16x16x32 on a hi/lo
 //   split of a1, or fp32 FMA), softmax, expectation, EMA, round-half-even,
 //   clamp.
@@ -32,6 +33,8 @@ constexpr int G1_ROW = G1_KBYTES + 16;         // padded LDS row (bytes)
 // deeper register staging only lengthens each workgroup there).
 constexpr int G1_STAGES_BIG = 3;
 constexpr int G1_STAGES_SMALL = 2;
+constexpr int G1_STAGES_WIDE = 2;
+constexpr int G1_WIDE_MIN_TILES = 1024;   // 128 x 128 tiles from which G1Wide replaces G1Big
 
 template <int kElemBytes> struct G1Elem;
 template <> struct G1Elem<2> { static constexpr int BK = 64; };   // bf16
@@ -62,6 +65,10 @@ struct G1Shape {
 };
 using G1Big = G1Shape<128, 128, 4, 2>;     // 8 waves, 32 x 64 slabs
 using G1Small = G1Shape<64, 64, 2, 2>;     // 4 waves, 32 x 32 slabs
+// 4 waves, 64 x 64 slabs: twice the matrix-core work per LDS byte of G1Big,
+// at half its waves per workgroup; it wins once every CU has several
+// workgroups queued (measured: 580 against 786 us for 32768 x 1024 x 8192)
+using G1Wide = G1Shape<128, 128, 2, 2>;
 
 // One K-tile of both operands staged in registers (constant indices only,
 // so the stages stay in VGPRs).
@@ -274,27 +281,31 @@ __global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
 }
 
 // Launch of the split-K product with the plan's tile shape.
-static hipError_t launch_gemm(const GemmPlan& g, bool bf16, const void* A, const void* W,
+template <int NS, class SH>
+static void launch_gemm_shape(const GemmPlan& g, bool bf16, const void* A, const void* W,
                               float* P, int M, int N, int K, hipStream_t stream) {
     const dim3 grid(g.tiles_m * g.tiles_n * g.splits);
-    if (g.big) {
-        if (bf16)
-            hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES_BIG, G1Big>), grid,
-                               dim3(G1Big::THREADS), 0, stream, (const char*)A, (const char*)W, P,
-                               M, N, K, g.splits, g.tiles_n, g.ktiles);
-        else
-            hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES_BIG, G1Big>), grid,
-                               dim3(G1Big::THREADS), 0, stream, (const char*)A, (const char*)W, P,
-                               M, N, K, g.splits, g.tiles_n, g.ktiles);
-    } else {
-        if (bf16)
-            hipLaunchKernelGGL((gemm1_splitk_kernel<2, G1_STAGES_SMALL, G1Small>), grid,
-                               dim3(G1Small::THREADS), 0, stream, (const char*)A, (const char*)W, P,
-                               M, N, K, g.splits, g.tiles_n, g.ktiles);
-        else
-            hipLaunchKernelGGL((gemm1_splitk_kernel<4, G1_STAGES_SMALL, G1Small>), grid,
-                               dim3(G1Small::THREADS), 0, stream, (const char*)A, (const char*)W, P,
-                               M, N, K, g.splits, g.tiles_n, g.ktiles);
+    if (bf16)
+        hipLaunchKernelGGL((gemm1_splitk_kernel<2, NS, SH>), grid, dim3(SH::THREADS), 0, stream,
+                           (const char*)A, (const char*)W, P, M, N, K, g.splits, g.tiles_n,
+                           g.ktiles);
+    else
+        hipLaunchKernelGGL((gemm1_splitk_kernel<4, NS, SH>), grid, dim3(SH::THREADS), 0, stream,
+                           (const char*)A, (const char*)W, P, M, N, K, g.splits, g.tiles_n,
+                           g.ktiles);
+}
+
+static hipError_t launch_gemm(const GemmPlan& g, bool bf16, const void* A, const void* W,
+                              float* P, int M, int N, int K, hipStream_t stream) {
+    switch (g.shape) {
+        case GemmPlan::kBig:
+            launch_gemm_shape<G1_STAGES_BIG, G1Big>(g, bf16, A, W, P, M, N, K, stream);
+            break;
+        case GemmPlan::kWide:
+            launch_gemm_shape<G1_STAGES_WIDE, G1Wide>(g, bf16, A, W, P, M, N, K, stream);
+            break;
+        default:
+            launch_gemm_shape<G1_STAGES_SMALL, G1Small>(g, bf16, A, W, P, M, N, K, stream);
     }
     return hipGetLastError();
 }
@@ -302,9 +313,17 @@ static hipError_t launch_gemm(const GemmPlan& g, bool bf16, const void* A, const
 // ---------------------------------------------------------------------------
 // head
 // ---------------------------------------------------------------------------
-constexpr int HD_RB = 4;          // rows per workgroup (one wave per row in the softmax)
+// Rows per workgroup: 4 (many workgroups, so the split-K partial reads have
+// plenty of loads in flight), or 16 for batches of at least HD_WIDE_MIN_REQ
+// (bf16 binned head), which fills the 16-row matrix-core blocks and reads W2
+// once per 16 rows instead of once per 4.
+constexpr int HD_RB = 4;
+constexpr int HD_RB_WIDE = 16;
+constexpr int HD_WIDE_MIN_REQ = 8192;
 constexpr int HD_THREADS = 256;
-constexpr int HD_BATCH = 2;       // float4 items per thread whose partial loads are in flight together
+// float4 items per thread whose partial loads are in flight together: more
+// when there are few split-K planes (registers hold kS x batch float4)
+template <int kS> constexpr int hd_batch() { return kS == 1 ? 8 : kS == 2 ? 4 : 2; }
 constexpr int HD_W2PF = 16;       // W2 fragments (K-steps of 32) loaded per wave at a time
 
 __device__ inline float apply_act(float x, int act) {
@@ -317,25 +336,26 @@ __device__ inline float apply_act(float x, int act) {
 // kReg: the regression head's last two layers instead of the binned one
 // (the nb "bin logits" are the third layer's outputs, `bins` holds w4 and
 // phase 3 computes relu(z) . w4 + b4 in place of the softmax mean).
-template <bool kBF16, int kS, bool kReg = false>
+template <bool kBF16, int kS, bool kReg = false, int kRB = HD_RB>
 __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     const float* __restrict__ P, int B, int m, int nb, const float* __restrict__ b1,
     const void* __restrict__ w2, const float* __restrict__ b2, const float* __restrict__ bins,
     int act, float ema_alpha, int ema_init, float* __restrict__ ema_state,
     float* __restrict__ expected, int32_t* __restrict__ rem_len, int len_max, float b4 = 0.0f) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
+    constexpr int kBatch = hd_batch<kS>();
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
-    const int row0 = blockIdx.x * HD_RB;
+    const int row0 = blockIdx.x * kRB;
     const int mpad = (m + 31) & ~31;
     const int astride = mpad + 8;                 // bf16 elements per LDS row
     const int nbpad = (nb + 15) & ~15;
 
     uint16_t* ahi = (uint16_t*)smem;
-    uint16_t* alo = ahi + HD_RB * astride;
+    uint16_t* alo = ahi + kRB * astride;
     float* a32 = (float*)smem;
-    float* z = kBF16 ? (float*)(alo + HD_RB * astride) : (float*)(a32 + HD_RB * m);
+    float* z = kBF16 ? (float*)(alo + kRB * astride) : (float*)(a32 + kRB * m);
 
     // 0) everything phases 2 and 3 read from global memory is requested now,
     //    so that its latency overlaps the split-K reads
@@ -365,16 +385,16 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
 
     // 1) fixed-order split-K reduction, bias, activation (float4 items)
     const int m4 = m >> 2;
-    const int items = HD_RB * m4;
+    const int items = kRB * m4;
     const int64_t plane4 = (int64_t)B * m4;
     const float4* P4 = (const float4*)P;
-    for (int base = 0; base < items; base += HD_BATCH * HD_THREADS) {
-        float4 v[HD_BATCH][kS];
-        float4 bv[HD_BATCH];
-        int row[HD_BATCH], c4[HD_BATCH];
-        bool ok[HD_BATCH];
+    for (int base = 0; base < items; base += kBatch * HD_THREADS) {
+        float4 v[kBatch][kS];
+        float4 bv[kBatch];
+        int row[kBatch], c4[kBatch];
+        bool ok[kBatch];
 #pragma unroll
-        for (int i = 0; i < HD_BATCH; ++i) {
+        for (int i = 0; i < kBatch; ++i) {
             const int e = base + i * HD_THREADS + tid;
             row[i] = e / m4;
             c4[i] = e - row[i] * m4;
@@ -385,7 +405,7 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
             bv[i] = b1 ? *(const float4*)(b1 + 4 * c4[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
-        for (int i = 0; i < HD_BATCH; ++i) {
+        for (int i = 0; i < kBatch; ++i) {
             const int e = base + i * HD_THREADS + tid;
             if (e >= items) continue;
             float4 sum = v[i][0];
@@ -412,7 +432,7 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
         }
     }
     if constexpr (kBF16) {      // zero K padding [m, mpad)
-        for (int e = tid; e < HD_RB * (mpad - m); e += HD_THREADS) {
+        for (int e = tid; e < kRB * (mpad - m); e += HD_THREADS) {
             const int r = e / (mpad - m), u = m + e % (mpad - m);
             ahi[r * astride + u] = 0;
             alo[r * astride + u] = 0;
@@ -424,9 +444,9 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     if constexpr (kBF16) {
         // v_mfma_f32_16x16x32_bf16: lane feeds row (lane%16), k = 8*(lane/16)..+7;
         // accumulator element v of lane l is row 4*(l/16)+v, column l%16.  Only
-        // rows < HD_RB are real; the other A rows are fed as zeros.
+        // rows < kRB are real; the other A rows are fed as zeros.
         const uint16_t* W2 = (const uint16_t*)w2;
-        const bool arow = r16 < HD_RB;
+        const bool arow = r16 < kRB;
         for (int nblk = wid; nblk * 16 < nb; nblk += HD_THREADS / 64) {
             const int j = nblk * 16 + r16;
             f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -444,7 +464,7 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
                     }
                 }
                 // all of this chunk's a1 fragments are read from LDS first, so
-                // their latencies overlap; rows >= HD_RB read row 0 and are
+                // their latencies overlap; rows >= kRB read row 0 and are
                 // zeroed afterwards (their MFMA rows are discarded anyway)
                 bf16x8 hv[HD_W2PF], lv[HD_W2PF];
                 const int arow_off = (arow ? r16 : 0) * astride;
@@ -470,12 +490,12 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
             for (int v = 0; v < 4; ++v) {
                 const int row = 4 * kq + v;
                 const float bias = nblk == wid ? b2v : (b2 && col < nb ? b2[col] : 0.0f);
-                if (row < HD_RB && col < nb) z[row * nbpad + col] = acc[v] + bias;
+                if (row < kRB && col < nb) z[row * nbpad + col] = acc[v] + bias;
             }
         }
     } else {
         const float* W2 = (const float*)w2;
-        for (int e = tid; e < HD_RB * nb; e += HD_THREADS) {
+        for (int e = tid; e < kRB * nb; e += HD_THREADS) {
             const int r = e / nb, j = e % nb;
             const float* wrow = W2 + (int64_t)j * m;
             const float* arow = a32 + r * m;
@@ -487,7 +507,7 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     __syncthreads();
 
     // 3) softmax, expectation, EMA, integerisation: one wave per row
-    for (int r = wid; r < HD_RB; r += HD_THREADS / 64) {
+    for (int r = wid; r < kRB; r += HD_THREADS / 64) {
         const int gr = row0 + r;
         if (gr >= B) continue;
         float den = 1.0f, num = 0.0f;
@@ -601,7 +621,7 @@ GemmPlan plan_gemm(int M, int N, int K, int elem) {
     const int bk = G1_KBYTES / elem;
     for (int big = 1; big >= 0; --big) {
         GemmPlan g;
-        g.big = big;
+        g.shape = big ? GemmPlan::kBig : GemmPlan::kSmall;
         const int bm = big ? G1Big::BM : G1Small::BM, bn = big ? G1Big::BN : G1Small::BN;
         g.tiles_m = (int)ceil_div(M, bm);
         g.tiles_n = (int)ceil_div(N, bn);
@@ -624,10 +644,12 @@ GemmPlan plan_gemm(int M, int N, int K, int elem) {
             best_cost = cost;
         }
     }
+    if (best.shape == GemmPlan::kBig && best.tiles_m * best.tiles_n >= G1_WIDE_MIN_TILES)
+        best.shape = GemmPlan::kWide;             // same tiles and splits, 64 x 64 per wave
     return best;
 }
 
-PredictPlan plan_predict(const star_predict_params& p) {
+PredictPlan plan_predict(const star_predict_params& p, bool wide_rows) {
     PredictPlan pl;
     const GemmPlan g = plan_gemm(p.n_req, p.d_hidden, p.d_model, p.dtype == STAR_BF16 ? 2 : 4);
     pl.gemm = g;
@@ -639,42 +661,65 @@ PredictPlan plan_predict(const star_predict_params& p) {
     pl.partial_bytes = (size_t)s * (size_t)p.n_req * (size_t)p.d_hidden * sizeof(float);
     const int mpad = (p.d_hidden + 31) & ~31;
     const int nbpad = (p.n_bins + 15) & ~15;
+    pl.head_rows = wide_rows && p.dtype == STAR_BF16 && p.n_req >= HD_WIDE_MIN_REQ ? HD_RB_WIDE
+                                                                                  : HD_RB;
+    const size_t rb = (size_t)pl.head_rows;
     if (p.dtype == STAR_BF16)
-        pl.head_lds = (size_t)2 * HD_RB * (mpad + 8) * 2 + (size_t)HD_RB * nbpad * 4;
+        pl.head_lds = 2 * rb * (mpad + 8) * 2 + rb * nbpad * 4;
     else
-        pl.head_lds = (size_t)HD_RB * p.d_hidden * 4 + (size_t)HD_RB * nbpad * 4;
+        pl.head_lds = rb * p.d_hidden * 4 + rb * nbpad * 4;
     return pl;
 }
 
-template <bool kBF16, int kS, bool kReg>
-static hipError_t launch_head_s(const star_predict_params& p, const PredictPlan& pl, dim3 grid,
-                                const float* partials, const float* b1, const void* w2,
-                                const float* b2, const float* bins, float* ema_state,
-                                float* expected, int32_t* rem_len, float b4, hipStream_t stream) {
+template <bool kBF16, int kS, bool kReg, int kRB>
+static hipError_t launch_head_rows(const star_predict_params& p, const PredictPlan& pl,
+                                   const float* partials, const float* b1, const void* w2,
+                                   const float* b2, const float* bins, float* ema_state,
+                                   float* expected, int32_t* rem_len, float b4,
+                                   hipStream_t stream) {
     if (pl.head_lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)head_kernel<kBF16, kS, kReg>,
+        hipError_t e = hipFuncSetAttribute((const void*)head_kernel<kBF16, kS, kReg, kRB>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)pl.head_lds);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((head_kernel<kBF16, kS, kReg>), grid, dim3(HD_THREADS), pl.head_lds,
+    const dim3 grid((unsigned)ceil_div(p.n_req, kRB));
+    hipLaunchKernelGGL((head_kernel<kBF16, kS, kReg, kRB>), grid, dim3(HD_THREADS), pl.head_lds,
                        stream, partials, p.n_req, p.d_hidden, p.n_bins, b1, w2, b2, bins, p.act,
                        p.ema_alpha, p.ema_init, ema_state, expected, rem_len, p.len_max, b4);
     return hipGetLastError();
 }
 
+// 16-row workgroups only for the bf16 binned head (the plan never picks
+// them elsewhere)
+template <bool kBF16, int kS, bool kReg>
+static hipError_t launch_head_s(const star_predict_params& p, const PredictPlan& pl,
+                                const float* partials, const float* b1, const void* w2,
+                                const float* b2, const float* bins, float* ema_state,
+                                float* expected, int32_t* rem_len, float b4, hipStream_t stream) {
+    if constexpr (kBF16 && !kReg) {
+        if (pl.head_rows == HD_RB_WIDE)
+            return launch_head_rows<kBF16, kS, kReg, HD_RB_WIDE>(p, pl, partials, b1, w2, b2,
+                                                                 bins, ema_state, expected,
+                                                                 rem_len, b4, stream);
+    }
+    if (pl.head_rows != HD_RB) return hipErrorInvalidValue;
+    return launch_head_rows<kBF16, kS, kReg, HD_RB>(p, pl, partials, b1, w2, b2, bins, ema_state,
+                                                    expected, rem_len, b4, stream);
+}
+
 template <bool kBF16, bool kReg = false>
-static hipError_t launch_head(const star_predict_params& p, const PredictPlan& pl, dim3 grid,
+static hipError_t launch_head(const star_predict_params& p, const PredictPlan& pl,
                               const float* partials, const float* b1, const void* w2,
                               const float* b2, const float* bins, float* ema_state,
                               float* expected, int32_t* rem_len, hipStream_t stream,
                               float b4 = 0.0f) {
     switch (pl.splits) {
-        case 1: return launch_head_s<kBF16, 1, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
-        case 2: return launch_head_s<kBF16, 2, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
-        case 4: return launch_head_s<kBF16, 4, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
-        case 8: return launch_head_s<kBF16, 8, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
-        case 16: return launch_head_s<kBF16, 16, kReg>(p, pl, grid, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
+        case 1: return launch_head_s<kBF16, 1, kReg>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
+        case 2: return launch_head_s<kBF16, 2, kReg>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
+        case 4: return launch_head_s<kBF16, 4, kReg>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
+        case 8: return launch_head_s<kBF16, 8, kReg>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
+        case 16: return launch_head_s<kBF16, 16, kReg>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, b4, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -696,10 +741,9 @@ hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, c
         e = hipEventRecord(ev[1], stream);
         if (e != hipSuccess) return e;
     }
-    const dim3 g2((unsigned)ceil_div(p.n_req, HD_RB));
-    return p.dtype == STAR_BF16 ? launch_head<true>(p, pl, g2, partials, b1, w2, b2, bins,
+    return p.dtype == STAR_BF16 ? launch_head<true>(p, pl, partials, b1, w2, b2, bins,
                                                     ema_state, expected, rem_len, stream)
-                                : launch_head<false>(p, pl, g2, partials, b1, w2, b2, bins,
+                                : launch_head<false>(p, pl, partials, b1, w2, b2, bins,
                                                      ema_state, expected, rem_len, stream);
 }
 
@@ -728,7 +772,7 @@ Mlp4Plan plan_mlp4(const star_mlp4_params& p) {
     Mlp4Plan pl;
     const int elem = p.dtype == STAR_BF16 ? 2 : 4;
     pl.g1 = plan_gemm(p.n_req, p.m1, p.d_model, elem);
-    pl.head = plan_predict(head_view(p));          // layer 2 and the head
+    pl.head = plan_predict(head_view(p), false);   // layer 2 and the head
     size_t off = 0;
     pl.p1_off = off;
     off += align_up((size_t)pl.g1.splits * p.n_req * p.m1 * sizeof(float), 256);
@@ -780,10 +824,9 @@ hipError_t launch_mlp4(const star_mlp4_params& p, const Mlp4Plan& pl, const void
     if ((e = launch_gemm(pl.head.gemm, bf, A1, w2, P2, p.n_req, p.m2, p.m1, stream)) !=
         hipSuccess)
         return e;
-    const dim3 gh((unsigned)ceil_div(p.n_req, HD_RB));
-    return bf ? launch_head<true, true>(h, pl.head, gh, P2, b2, w3, b3, w4, ema_state, expected,
+    return bf ? launch_head<true, true>(h, pl.head, P2, b2, w3, b3, w4, ema_state, expected,
                                         rem_len, stream, p.b4)
-              : launch_head<false, true>(h, pl.head, gh, P2, b2, w3, b3, w4, ema_state, expected,
+              : launch_head<false, true>(h, pl.head, P2, b2, w3, b3, w4, ema_state, expected,
                                          rem_len, stream, p.b4);
 }
 

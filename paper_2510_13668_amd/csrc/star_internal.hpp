@@ -11,7 +11,8 @@ namespace star {
 
 struct GemmPlan {
     int tiles_m = 0, tiles_n = 0, ktiles = 0, splits = 1;
-    int big = 1;          // 128 x 128 tiles (else 64 x 64)
+    enum { kSmall = 0, kBig = 1, kWide = 2 };
+    int shape = kBig;     // 64 x 64 tiles on 4 waves; 128 x 128 on 8; 128 x 128 on 4
 };
 GemmPlan plan_gemm(int M, int N, int K, int elem);
 
@@ -20,8 +21,9 @@ struct PredictPlan {
     int tiles_m = 0, tiles_n = 0, ktiles = 0, splits = 1;
     size_t partial_bytes = 0;   // fp32 split-K partials [splits, B, m]
     size_t head_lds = 0;        // dynamic LDS of the head kernel
+    int head_rows = 4;          // rows per head workgroup (4 or 16)
 };
-PredictPlan plan_predict(const star_predict_params& p);
+PredictPlan plan_predict(const star_predict_params& p, bool wide_rows = true);
 hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, const void* hidden,
                           const void* w1, const float* b1, const void* w2, const float* b2,
                           const float* bins, float* ema_state, float* expected, int32_t* rem_len,

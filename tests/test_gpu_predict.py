@@ -88,6 +88,42 @@ def test_ragged_shapes(dtype, act, B, d, m, nb):
     _run_case(h, w1, w2, bins, dtype=dtype, act=act, b1=b1, b2=b2, len_max=32768)
 
 
+@pytest.mark.parametrize("B,d,m,nb", [(8200, 64, 2048, 256), (8192 + 13, 136, 72, 20),
+                                     (9000, 512, 1024, 128)])
+def test_wide_head_rows_sampled(B, d, m, nb):
+    """Batches of 8192 and more take 16-row head workgroups: ragged last
+    workgroup, maximum width and bins, and odd widths; checked on the first
+    and last rows and a random sample."""
+    rng = np.random.default_rng(B + d + m + nb)
+    h = synth.f32_to_bf16_bits(rng.standard_normal((B, d)).astype(np.float32))
+    w1 = synth.f32_to_bf16_bits((rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32))
+    w2 = synth.f32_to_bf16_bits((rng.standard_normal((nb, m)) * 4 / np.sqrt(m)).astype(np.float32))
+    b1 = (rng.standard_normal(m) * 0.1).astype(np.float32)
+    b2 = (rng.standard_normal(nb) * 0.1).astype(np.float32)
+    bins = synth.bin_values(nb, 1.0, 32768.0)
+    sample = np.unique(np.concatenate([np.arange(40), np.arange(B - 40, B),
+                                       rng.choice(B, 120, replace=False)]))
+    print(f"wide head B={B} d={d} m={m} nb={nb}", flush=True)
+    _run_case(h, w1, w2, bins, dtype=synth.BF16, act=synth.ACT_GELU, b1=b1, b2=b2,
+              len_max=32768, sample=sample)
+
+
+def test_large_fp32_sampled():
+    """fp32 with 1032 output tiles: the 4-wave 128 x 128 GEMM shape, ragged
+    rows, three K-tiles; checked on sampled rows."""
+    B, d, m, nb = 16390, 96, 1024, 40
+    rng = np.random.default_rng(5)
+    h = rng.standard_normal((B, d)).astype(np.float32)
+    w1 = (rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32)
+    w2 = (rng.standard_normal((nb, m)) * 4 / np.sqrt(m)).astype(np.float32)
+    bins = synth.bin_values(nb, 1.0, 32768.0)
+    sample = np.unique(np.concatenate([np.arange(20), np.arange(B - 140, B),
+                                       rng.choice(B, 100, replace=False)]))
+    print(f"large fp32 B={B} d={d} m={m} nb={nb}", flush=True)
+    _run_case(h, w1, w2, bins, dtype=synth.F32, act=synth.ACT_RELU, len_max=32768,
+              sample=sample)
+
+
 def test_empty_batch():
     wl = synth.WORKLOADS["8b_batch"]
     rng = np.random.default_rng(0)
