@@ -276,7 +276,12 @@ __global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
         const int row = ch / (SH::BN / 4), c4 = ch % (SH::BN / 4);
         const int grow = tm * SH::BM + row, gcol = tn * SH::BN + c4 * 4;
         if (grow < M && gcol < N)                     // N % 4 == 0: chunks never straddle N
-            *(float4*)&out[(int64_t)grow * N + gcol] = *(const float4*)&otile[row * SH::OUT_ROW + c4 * 4];
+            // partials are written once and read once by the next kernel:
+            // non-temporal stores stream them out instead of leaving them
+            // dirty in L2 for the end-of-kernel writeback (measured: 15.8 ->
+            // 12.8 us at 1024 x 512 x 4096 with four splits)
+            __builtin_nontemporal_store(*(const f32x4*)&otile[row * SH::OUT_ROW + c4 * 4],
+                                        (f32x4*)&out[(int64_t)grow * N + gcol]);
     }
 }
 
@@ -401,7 +406,12 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
             ok[i] = e < items && row0 + row[i] < B;
             const int64_t off = ok[i] ? (int64_t)(row0 + row[i]) * m4 + c4[i] : 0;
 #pragma unroll
-            for (int q = 0; q < kS; ++q) v[i][q] = P4[q * plane4 + off];
+            for (int q = 0; q < kS; ++q) {
+                // read once: streamed past L2 (non-temporal), so they do not
+                // evict the operands the next product reads
+                const f32x4 t = __builtin_nontemporal_load((const f32x4*)&P4[q * plane4 + off]);
+                v[i][q] = make_float4(t[0], t[1], t[2], t[3]);
+            }
             bv[i] = b1 ? *(const float4*)(b1 + 4 * c4[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
@@ -578,7 +588,10 @@ __global__ __launch_bounds__(ACT_THREADS) void act_kernel(const float* __restric
             const int64_t e = base + i * ACT_THREADS + threadIdx.x;
             const int64_t o = e < items ? e : 0;
 #pragma unroll
-            for (int q = 0; q < kS; ++q) v[i][q] = P4[q * items + o];
+            for (int q = 0; q < kS; ++q) {
+                const f32x4 t = __builtin_nontemporal_load((const f32x4*)&P4[q * items + o]);
+                v[i][q] = make_float4(t[0], t[1], t[2], t[3]);
+            }
         }
 #pragma unroll
         for (int i = 0; i < ACT_BATCH; ++i) {
