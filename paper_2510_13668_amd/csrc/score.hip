@@ -227,17 +227,40 @@ __device__ inline int64_t half_incl_add_i64(int64_t v) {
     return v;
 }
 
-// Section 5.2's curves of every instance from its requests, in LDS (rows of
-// stride K+1): hA / hN hold alpha_r and the request count by k_e (1..K), hP
-// the partial-bucket terms by k_e (0..K-1).  With S_A(k), S_n(k) the sums of
-// hA, hN over k_e > k, L[k] = S_A(k) + b^2 k S_n(k) + hP[k] is written over
-// hP, and entry K of each row becomes -inf (padding read by the scoring).
-// Each instance is taken by half a wave; lane l owns a run of S (odd)
-// buckets counted from the end, as in build_pm_sm: a sum over its run, one
-// DPP scan across the 32 runs, then a pass that writes.
+// Exclusive maximum over the lanes above this one in its half wave (lanes
+// l+1..31 of the same 32), -inf for lane 31: shuffles down.
+__device__ inline int64_t half_excl_max_above_i64(int64_t v) {
+    const int l = threadIdx.x & 31;
+    int64_t inc = v;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+        const uint32_t lo = (uint32_t)__shfl_down((int)(uint32_t)inc, o, 32);
+        const uint32_t hi = (uint32_t)__shfl_down((int)(inc >> 32), o, 32);
+        const int64_t u = (int64_t)(((uint64_t)hi << 32) | lo);
+        inc = l + o < 32 ? imax(inc, u) : inc;
+    }
+    const uint32_t lo = (uint32_t)__shfl_down((int)(uint32_t)inc, 1, 32);
+    const uint32_t hi = (uint32_t)__shfl_down((int)(inc >> 32), 1, 32);
+    const int64_t ex = (int64_t)(((uint64_t)hi << 32) | lo);
+    return l == 31 ? INT64_MIN : ex;
+}
+
+// Section 5.2's curves of every instance from its requests, with their PM
+// and SM, in LDS (rows of stride K+1).  In: hA / hN hold alpha_r and the
+// request count by k_e (1..K), hP the partial-bucket terms by k_e (0..K-1).
+// With S_A(k), S_n(k) the sums of hA, hN over k_e > k, the curve is
+// L[k] = S_A(k) + b^2 k S_n(k) + hP[k], written over hP.  Each instance is
+// taken by half a wave; lane l owns a run of S (odd) buckets counted from
+// the end (lane 0 the top ones), and makes three passes over it:
+//   1) run sums of hA, hN; exclusive suffix sums across lanes (DPP);
+//   2) L over the run, written, with the run's max of L and of L[j] + b^2 j;
+//   3) SM = suffix max (lanes above in bucket order come first: the same
+//      DPP direction), PM = exclusive prefix max of L[j] + b^2 j (the lanes
+//      holding lower buckets: shuffles down), both written from the run.
+// PM_t[K] is the maximum over every bucket; SM_t[K] and L_t[K] are -inf.
 template <int kT>
-__device__ inline void build_curves(const int64_t* hA, const int64_t* hN, int64_t* hPL, int n,
-                                    int K, int64_t bb) {
+__device__ inline void build_curves_pm_sm(const int64_t* hA, const int64_t* hN, int64_t* hPL,
+                                          int64_t* lPM, int64_t* lSM, int n, int K, int64_t bb) {
     const int l = threadIdx.x & 31;
     const int K1 = K + 1;
     const int S = ((K + 31) >> 5) | 1;
@@ -250,7 +273,8 @@ __device__ inline void build_curves(const int64_t* hA, const int64_t* hN, int64_
         int64_t* L = hPL + tc * K1;
         const int j0 = l * S;
         const int j1 = j0 + S < K ? j0 + S : K;
-        const int q0 = K - 1 - j0, q1 = K - j1;      // buckets [q1, q0], walked downwards
+        const int q0 = K - 1 - j0, q1 = K - j1;      // buckets [q1, q0]
+        // 1) run sums
         int64_t sa = 0, sn = 0;
         for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {
             int64_t xa[PMSM_BATCH], xn[PMSM_BATCH];
@@ -267,13 +291,14 @@ __device__ inline void build_curves(const int64_t* hA, const int64_t* hN, int64_
                     sn += xn[u];
                 }
         }
-        // the lane shifts run on every lane (a DPP move inside one arm of a
-        // branch would read disabled lanes), then each half's first lane
-        // takes 0
+        // every lane runs the lane shifts (a DPP move inside one arm of a
+        // branch would read disabled lanes)
         const int64_t ia = half_incl_add_i64(sa), in = half_incl_add_i64(sn);
         const int64_t ea = wave_shr1_i64(ia, 0), en = wave_shr1_i64(in, 0);
         int64_t ra = l == 0 ? 0 : ea;
         int64_t rn = l == 0 ? 0 : en;
+        // 2) L over the run (downwards) and the run's maxima
+        int64_t smax = INT64_MIN, pmax = INT64_MIN;
         for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {
             int64_t xa[PMSM_BATCH], xn[PMSM_BATCH], xp[PMSM_BATCH];
 #pragma unroll
@@ -289,11 +314,59 @@ __device__ inline void build_curves(const int64_t* hA, const int64_t* hN, int64_
                 if (q >= q1) {
                     ra += xa[u];
                     rn += xn[u];
-                    if (live) L[q] = ra + bb * q * rn + xp[u];
+                    const int64_t v = ra + bb * q * rn + xp[u];
+                    if (live) L[q] = v;
+                    smax = imax(smax, v);
+                    pmax = imax(pmax, v + bb * q);
                 }
             }
         }
-        if (live && l == 0) L[K] = INT64_MIN;
+        // 3) SM: suffix max, lanes below l hold the higher buckets (same
+        //    direction as the sums); PM: prefix max over lower buckets =
+        //    lanes above l
+        const int64_t si = half_incl_max_i64(smax);
+        const int64_t se = wave_shr1_i64(si, INT64_MIN);
+        int64_t srun = l == 0 ? INT64_MIN : se;
+        int64_t prun = half_excl_max_above_i64(pmax);
+        const int64_t ptot = imax(prun, pmax);       // lane 0: max over every bucket
+        // the run's L values are this lane's own writes: no barrier needed
+        for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {         // SM downwards
+            int64_t x[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u >= q1 ? jb - u : q0;
+                x[u] = L[q];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u;
+                if (q >= q1) {
+                    srun = imax(srun, x[u]);
+                    if (live) lSM[tc * K1 + q] = srun;
+                }
+            }
+        }
+        for (int jb = q1; jb <= q0; jb += PMSM_BATCH) {         // PM upwards, exclusive
+            int64_t x[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb + u <= q0 ? jb + u : q1;
+                x[u] = L[q];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb + u;
+                if (q <= q0) {
+                    if (live) lPM[tc * K1 + q] = prun;
+                    prun = imax(prun, x[u] + bb * q);
+                }
+            }
+        }
+        if (live && l == 0) {
+            L[K] = INT64_MIN;
+            lSM[tc * K1 + K] = INT64_MIN;
+            lPM[tc * K1 + K] = ptot;
+        }
     }
 }
 
@@ -1403,7 +1476,11 @@ __global__ __launch_bounds__(SC_THREADS) void score_rank_kernel(ScoreArgs a, Ran
             }
         }
         __syncthreads();
-        build_curves<SC_THREADS>(lPM, lSM, lL, n, K, bb);
+        // the histograms hA / hN sit in PM's / SM's rows: every lane reads
+        // them (its own run and one entry of the next) in the first two
+        // sweeps, which the whole wave finishes before any lane writes PM
+        // or SM in the third; instances use disjoint rows
+        build_curves_pm_sm<SC_THREADS>(lPM, lSM, lL, lPM, lSM, n, K, bb);
         __syncthreads();
         if (g == 0)
             for (int e = tid; e < nK; e += SC_THREADS) {
@@ -1423,8 +1500,10 @@ __global__ __launch_bounds__(SC_THREADS) void score_rank_kernel(ScoreArgs a, Ran
     }
     for (int c = tid; c < RK_CODES; c += SC_THREADS) lhist[c] = 0;
     __syncthreads();
-    build_pm_sm<SC_THREADS>(lL, lPM, lSM, n, K, bb);
-    __syncthreads();
+    if constexpr (!kProject) {
+        build_pm_sm<SC_THREADS>(lL, lPM, lSM, n, K, bb);
+        __syncthreads();
+    }
 
     // 1) this thread's candidate e = q n + t
     int64_t base = INT64_MAX;                         // smallest target peak
