@@ -128,7 +128,7 @@ def test_project_and_score_validation(L):
     f = FAKE
     sp = star.score_params(1024, 8, 64, 256, 256)
     need = star.project_and_score_workspace_size(sp)
-    # the same workspace layout as scoring alone (its ticket sits in the header)
+    # the same workspace layout as scoring alone
     assert need == star.score_workspace_size(sp)
     args = [f] * 10
     assert L.star_project_and_score(None, *args, f, need, None) == -1
