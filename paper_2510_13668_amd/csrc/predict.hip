@@ -5,18 +5,18 @@
 // logits = W2 a1 + b2 over length bins, p = softmax, E = sum p_j v_j, then
 // the continuous-prediction smoothing of Section 4.3 and integerisation.
 //
-// Kernel 1 (gemm1_splitk): Z1 partials = H W1^T over a K-slice, on MFMA.
-//   128x128 output tile per 256-thread workgroup (4 waves, 64x64 each as
-//   2x2 MFMA 32x32 blocks), 128 bytes of K per LDS row (64 bf16 / 32 fp32),
-//   double-buffered LDS fed by 16-byte global loads, split-K so that small
-//   batches still launch ~256 workgroups.  Partials are fp32, reduced later
-//   in a fixed order (deterministic results).
+// Kernel 1 (gemm1_splitk): Z1 partials = H W1^T over a K-slice, on MFMA
+//   (32x32 blocks), 128 bytes of K per LDS row (64 bf16 / 32 fp32),
+//   double-buffered LDS fed by register-staged 16-byte global loads, split-K
+//   so that small batches still fill the CUs.  Tile shapes: 64x64 on 4
+//   waves, 128x128 on 8 or 4 waves, 256x256 on 8 waves; a cost model picks
+//   one per product.  Partials are fp32, reduced later in a fixed order
+//   (deterministic results).
 // Kernel 2 (head): 4 rows per workgroup (many workgroups, so the split-K
 //   partial reads have plenty of loads in flight), 16 for large batches:
-//   fixed-order split-K
-//   reduction, bias, activation, the bin GEMM (bf16 MFMA 16x16x32 on a hi/lo
-//   split of a1, or fp32 FMA), softmax, expectation, EMA, round-half-even,
-//   clamp.
+//   fixed-order split-K reduction, bias, activation, the bin GEMM (bf16 MFMA
+//   16x16x32 on a hi/lo split of a1, or fp32 FMA), softmax, expectation,
+//   EMA, round-half-even, clamp.
 #include "star_common.hpp"
 #include "star_internal.hpp"
 
@@ -35,6 +35,8 @@ constexpr int G1_STAGES_BIG = 3;
 constexpr int G1_STAGES_SMALL = 2;
 constexpr int G1_STAGES_WIDE = 2;
 constexpr int G1_WIDE_MIN_TILES = 1024;   // 128 x 128 tiles from which G1Wide replaces G1Big
+constexpr int G1_STAGES_HUGE = 1;
+constexpr int G1_HUGE_MIN_TILES = 256;    // 256 x 256 tiles (no split) from which G1Huge is used
 
 template <int kElemBytes> struct G1Elem;
 template <> struct G1Elem<2> { static constexpr int BK = 64; };   // bf16
@@ -61,7 +63,9 @@ struct G1Shape {
     static constexpr int LDS_A = BM * G1_ROW, LDS_B = BN * G1_ROW;
     static constexpr int OUT_ROW = BN + 8;     // floats per LDS row of the output tile
     static_assert(MI >= 1 && NJ >= 1 && CA >= 1 && CB >= 1, "shape");
-    static_assert(BM * OUT_ROW * 4 <= 2 * (LDS_A + LDS_B), "output tile fits the operand buffers");
+    // the output tile goes out through LDS when it fits the operand buffers,
+    // else straight from the accumulators
+    static constexpr bool LDS_EPI = BM * OUT_ROW * 4 <= 2 * (LDS_A + LDS_B);
 };
 using G1Big = G1Shape<128, 128, 4, 2>;     // 8 waves, 32 x 64 slabs
 using G1Small = G1Shape<64, 64, 2, 2>;     // 4 waves, 32 x 32 slabs
@@ -69,6 +73,11 @@ using G1Small = G1Shape<64, 64, 2, 2>;     // 4 waves, 32 x 32 slabs
 // at half its waves per workgroup; it wins once every CU has several
 // workgroups queued (measured: 580 against 786 us for 32768 x 1024 x 8192)
 using G1Wide = G1Shape<128, 128, 2, 2>;
+// 8 waves, 64 x 128 slabs of a 256 x 256 tile: four times G1Big's matrix-core
+// work per byte loaded, one workgroup per CU (147 KiB of LDS); one K-tile in
+// flight keeps it within 256 registers.  For products with hundreds of such
+// tiles (measured: 448-483 us, 46-49% of peak, at 32768 x 1024 x 8192).
+using G1Huge = G1Shape<256, 256, 4, 2>;
 
 // One K-tile of both operands staged in registers (constant indices only,
 // so the stages stay in VGPRs).
@@ -253,7 +262,26 @@ __global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
     // 8*(v/4) + 4*(l/32) + v%4, column l%32 of its block) goes through LDS
     // (the operand buffers, free now) so that global stores are whole
     // 16-byte row chunks.  LDS rows hold OUT_ROW floats (the padding puts
-    // the two 4-row halves of a store on disjoint banks).
+    // the two 4-row halves of a store on disjoint banks).  Tiles too large
+    // for that store each accumulator element directly: 32 lanes write 128
+    // contiguous bytes of a row.
+    if constexpr (!SH::LDS_EPI) {
+        float* outd = P + (int64_t)split * M * N;
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const int gcol = tn * SH::BN + wn * 32 * NJ + j * 32 + r32;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int grow = tm * SH::BM + wm * 32 * MI + i * 32 + 8 * (v >> 2) +
+                                     4 * khalf + (v & 3);
+                    if (grow < M && gcol < N)
+                        __builtin_nontemporal_store(acc[i][j][v], &outd[(int64_t)grow * N + gcol]);
+                }
+            }
+        return;
+    }
     __syncthreads();
     float* otile = (float*)&lds[0][0];
 #pragma unroll
@@ -308,6 +336,9 @@ static hipError_t launch_gemm(const GemmPlan& g, bool bf16, const void* A, const
             break;
         case GemmPlan::kWide:
             launch_gemm_shape<G1_STAGES_WIDE, G1Wide>(g, bf16, A, W, P, M, N, K, stream);
+            break;
+        case GemmPlan::kHuge:
+            launch_gemm_shape<G1_STAGES_HUGE, G1Huge>(g, bf16, A, W, P, M, N, K, stream);
             break;
         default:
             launch_gemm_shape<G1_STAGES_SMALL, G1Small>(g, bf16, A, W, P, M, N, K, stream);
@@ -655,6 +686,15 @@ GemmPlan plan_gemm(int M, int N, int K, int elem) {
         if (big || cost < best_cost) {
             best = g;
             best_cost = cost;
+        }
+    }
+    if (best.shape == GemmPlan::kBig && best.splits == 1) {
+        const int hm = (int)ceil_div(M, G1Huge::BM), hn = (int)ceil_div(N, G1Huge::BN);
+        if (hm * hn >= G1_HUGE_MIN_TILES) {       // 256 x 256 tiles, 64 x 128 per wave
+            best.shape = GemmPlan::kHuge;
+            best.tiles_m = hm;
+            best.tiles_n = hn;
+            return best;
         }
     }
     if (best.shape == GemmPlan::kBig && best.tiles_m * best.tiles_n >= G1_WIDE_MIN_TILES)
