@@ -349,22 +349,38 @@ static hipError_t launch_gemm(const GemmPlan& g, bool bf16, const void* A, const
 // ---------------------------------------------------------------------------
 // head
 // ---------------------------------------------------------------------------
-// Rows per workgroup: 4 (many workgroups, so the split-K partial reads have
-// plenty of loads in flight), or 16 for batches of at least HD_WIDE_MIN_REQ
-// (bf16 binned head), which fills the 16-row matrix-core blocks and reads W2
-// once per 16 rows instead of once per 4.
+// Rows per workgroup: 4, so that the split-K partial reads of a batch have
+// plenty of workgroups in flight (large bf16 batches take head_tiled_kernel).
 constexpr int HD_RB = 4;
-constexpr int HD_RB_WIDE = 16;
-constexpr int HD_WIDE_MIN_REQ = 8192;
 constexpr int HD_THREADS = 256;
 // float4 items per thread whose partial loads are in flight together: more
 // when there are few split-K planes (registers hold kS x batch float4)
 template <int kS> constexpr int hd_batch() { return kS == 1 ? 8 : kS == 2 ? 4 : 2; }
 constexpr int HD_W2PF = 16;       // W2 fragments (K-steps of 32) loaded per wave at a time
 
+// GELU in its erf form, x Phi(x) with Phi the standard normal distribution
+// function, without branches: h = Phi(-|x|) = erfc(|x| / sqrt 2) / 2 from the
+// rational-times-Gaussian approximation of erfc in Abramowitz & Stegun 7.1.26
+// (absolute error under 1.5e-7 in erf; in fp32 the result is within 1.5e-7
+// max(1, |x|) of the exact GELU, twenty times below the rounding of the bf16
+// hi/lo pair that carries activations into the next product), and
+// x Phi(x) = x - x h for x >= 0, x h below.
+__device__ inline float gelu_erf(float x) {
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, fabsf(x), 1.0f));
+    // coefficients a5 .. a1 of 7.1.26, halved
+    float q = fmaf(t, 0.5307027145f, -0.7265760135f);
+    q = fmaf(t, q, 0.7107068705f);
+    q = fmaf(t, q, -0.142248368f);
+    q = fmaf(t, q, 0.127414796f);
+    // exp(-x^2 / 2) = 2^(-x^2 / (2 ln 2))
+    const float h = t * q * __builtin_amdgcn_exp2f(x * x * -0.72134752044448170f);
+    const float xh = x * h;
+    return x >= 0.0f ? x - xh : xh;
+}
+
 __device__ inline float apply_act(float x, int act) {
     if (act == STAR_ACT_RELU) return x > 0.0f ? x : 0.0f;
-    return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+    return gelu_erf(x);
 }
 
 // kS = number of split-K partial planes (compile time, so that all of a
@@ -458,15 +474,12 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
 #pragma unroll
             for (int j = 0; j < 4; ++j) a[j] = ok[i] ? apply_act(a[j], act) : 0.0f;
             if constexpr (kBF16) {
-                uint16_t h[4], l[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    h[j] = f32_to_bf16_rne(a[j]);
-                    l[j] = f32_to_bf16_rne(a[j] - bf16_to_f32(h[j]));
-                }
+                uint32_t h0, l0, h1, l1;
+                split_bf16x2(a[0], a[1], h0, l0);
+                split_bf16x2(a[2], a[3], h1, l1);
                 const int o = row[i] * astride + 4 * c4[i];
-                *(uint2*)(ahi + o) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
-                *(uint2*)(alo + o) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+                *(uint2*)(ahi + o) = make_uint2(h0, h1);
+                *(uint2*)(alo + o) = make_uint2(l0, l1);
             } else {
                 *(float4*)(a32 + row[i] * m + 4 * c4[i]) = make_float4(a[0], a[1], a[2], a[3]);
             }
@@ -598,6 +611,266 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// The head for large bf16 batches, K-chunked: 64 rows per workgroup (16 per
+// wave).  For each chunk of 64 a1 columns the workgroup reduces that chunk's
+// partials (fixed order), adds b1, applies the activation and writes the
+// bf16 hi/lo pair to LDS, stages W2's chunk in LDS once for all four waves,
+// and runs the 16x16x32 MFMAs; the next chunk's partials and W2 are loaded
+// into registers meanwhile.  With up to 128 bins there are two LDS stages and
+// one barrier per chunk: the next chunk is activated (VALU) into one stage
+// while the products (MFMA) read the other.  The logits stay in registers
+// for the softmax: a row's bins are spread over 16 lanes, plus registers.
+// W2 is read once per 64 rows (the 4-row head reads it once per 4).
+// ---------------------------------------------------------------------------
+constexpr int HT_ROWS = 64;
+constexpr int HT_KC = 64;                   // a1 columns per chunk
+constexpr int HT_ASTR = HT_KC + 8;          // bf16 per LDS row (padding spreads banks)
+constexpr int HT_MIN_REQ = 8192;            // batches from which the tiled head is used
+constexpr int HT_MAX_SPLITS = 4;            // its partial registers: 4 x splits float4
+
+// bin blocks of 16 the tiled head computes: 4, 8 or 16 (compile time, so that
+// every loop over them has a fixed trip count; blocks past nb carry zeros)
+static int head_tiled_blocks(int nb) { return nb <= 64 ? 4 : nb <= 128 ? 8 : 16; }
+// two LDS stages (the next chunk is written while the products read this
+// one) while two workgroups still fit a CU, i.e. up to 8 bin blocks
+constexpr bool head_tiled_two_stages(int nbb) { return nbb <= 8; }
+static size_t head_tiled_lds(int nb) {
+    const int nbb = head_tiled_blocks(nb);
+    return (size_t)(head_tiled_two_stages(nbb) ? 2 : 1) * (2 * HT_ROWS + nbb * 16) * HT_ASTR * 2;
+}
+
+// One chunk's registers: 4 float4 of partials per plane (64 rows x 16
+// float4 per workgroup), their b1, and up to 8 16-byte pieces of W2.
+template <int kS, int kNBB>
+struct HtRegs {
+    float4 pv[4][kS];
+    float4 bv[4];
+    uint4 wv[kNBB / 2];      // kNBB x 16 bins x 8 pieces over 256 threads
+};
+
+struct HtArgs {
+    const float4* P4;
+    const float* b1;
+    const uint16_t* W2;
+    int64_t plane4;
+    int B, m, m4, nb, row0;
+};
+
+template <int kS, int kNBB>
+__device__ __forceinline__ void ht_load(const HtArgs& a, int c, HtRegs<kS, kNBB>& g) {
+    const int tid = threadIdx.x;
+    const int k0 = c * HT_KC;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int idx = u * HD_THREADS + tid;
+        const int r = idx >> 4, kc = k0 + (idx & 15) * 4;
+        const bool ok = a.row0 + r < a.B && kc < a.m;
+        const int64_t off = ok ? (int64_t)(a.row0 + r) * a.m4 + (kc >> 2) : 0;
+#pragma unroll
+        for (int q = 0; q < kS; ++q) {
+            const f32x4 t = __builtin_nontemporal_load((const f32x4*)&a.P4[q * a.plane4 + off]);
+            g.pv[u][q] = make_float4(t[0], t[1], t[2], t[3]);
+        }
+        g.bv[u] = (a.b1 && kc < a.m) ? *(const float4*)(a.b1 + kc) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < kNBB / 2; ++u) {
+        const int it = u * HD_THREADS + tid;
+        const int j = it >> 3, kk = k0 + (it & 7) * 8;
+        const bool ok = j < a.nb && kk < a.m;      // m % 8 == 0: whole pieces
+        g.wv[u] = *(const uint4*)(a.W2 + (ok ? (int64_t)j * a.m + kk : 0));
+    }
+}
+
+template <int kS, int kNBB, bool kGelu>
+__device__ __forceinline__ void ht_store(const HtArgs& a, int c, const HtRegs<kS, kNBB>& g,
+                                         uint16_t* ahi, uint16_t* alo, uint16_t* wl) {
+    const int tid = threadIdx.x;
+    const int k0 = c * HT_KC;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int idx = u * HD_THREADS + tid;
+        const int r = idx >> 4, c4 = idx & 15, kc = k0 + c4 * 4;
+        const bool ok = a.row0 + r < a.B && kc < a.m;
+        float4 sum = g.pv[u][0];
+#pragma unroll
+        for (int q = 1; q < kS; ++q) {
+            sum.x += g.pv[u][q].x; sum.y += g.pv[u][q].y; sum.z += g.pv[u][q].z; sum.w += g.pv[u][q].w;
+        }
+        const float av[4] = {sum.x + g.bv[u].x, sum.y + g.bv[u].y, sum.z + g.bv[u].z, sum.w + g.bv[u].w};
+        uint32_t hw[2], lw[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const float y0 = av[2 * e], y1 = av[2 * e + 1];
+            const float g0 = kGelu ? gelu_erf(y0) : fmaxf(y0, 0.0f);
+            const float g1 = kGelu ? gelu_erf(y1) : fmaxf(y1, 0.0f);
+            split_bf16x2(ok ? g0 : 0.0f, ok ? g1 : 0.0f, hw[e], lw[e]);
+        }
+        const int o = r * HT_ASTR + c4 * 4;
+        *(uint2*)(ahi + o) = make_uint2(hw[0], hw[1]);
+        *(uint2*)(alo + o) = make_uint2(lw[0], lw[1]);
+    }
+#pragma unroll
+    for (int u = 0; u < kNBB / 2; ++u) {
+        const int it = u * HD_THREADS + tid;       // row j < kNBB x 16 of the W2 chunk
+        const int j = it >> 3, kk = k0 + (it & 7) * 8;
+        const uint32_t z = (j < a.nb && kk < a.m) ? 0xFFFFFFFFu : 0u;
+        *(uint4*)(wl + j * HT_ASTR + (it & 7) * 8) =
+            make_uint4(g.wv[u].x & z, g.wv[u].y & z, g.wv[u].z & z, g.wv[u].w & z);
+    }
+}
+
+template <int kS, int kNBB, bool kGelu>
+__global__ __launch_bounds__(HD_THREADS) void head_tiled_kernel(
+    const float* __restrict__ P, int B, int m, int nb, const float* __restrict__ b1,
+    const uint16_t* __restrict__ W2, const float* __restrict__ b2,
+    const float* __restrict__ bins, float ema_alpha, int ema_init,
+    float* __restrict__ ema_state, float* __restrict__ expected, int32_t* __restrict__ rem_len,
+    int len_max) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    const int row0 = blockIdx.x * HT_ROWS;
+    // a stage: A hi [64][HT_ASTR], A lo [64][HT_ASTR], W2 [kNBB * 16][HT_ASTR]
+    constexpr int kStage = (2 * HT_ROWS + kNBB * 16) * HT_ASTR;
+    constexpr bool kTwo = head_tiled_two_stages(kNBB);
+    uint16_t* const st0 = (uint16_t*)smem;
+    uint16_t* const st1 = st0 + (kTwo ? kStage : 0);
+    HtArgs a;
+    a.P4 = (const float4*)P;
+    a.b1 = b1;
+    a.W2 = W2;
+    a.m = m;
+    a.m4 = m >> 2;
+    a.B = B;
+    a.plane4 = (int64_t)B * a.m4;
+    a.nb = nb;
+    a.row0 = row0;
+    const int nchunk = (m + HT_KC - 1) / HT_KC;
+    // loads past the last chunk read offset 0 (masked), so none is guarded
+    HtRegs<kS, kNBB> g;
+
+    f32x4 acc[kNBB];
+#pragma unroll
+    for (int j = 0; j < kNBB; ++j) acc[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    const int ar = wid * 16 + (lane & 15);          // this lane's A row (MFMA row lane % 16)
+    const int kq = (lane >> 4) * 8;                 // its 8 k values within a 32-wide step
+
+    // the products of one chunk: 16 rows of this wave x kNBB bin blocks
+    auto products = [&](const uint16_t* stage) {
+        const uint16_t* ahi = stage;
+        const uint16_t* alo = stage + HT_ROWS * HT_ASTR;
+        const uint16_t* wl = stage + 2 * HT_ROWS * HT_ASTR;
+#pragma unroll
+        for (int sstep = 0; sstep < HT_KC / 32; ++sstep) {
+            const int ka = sstep * 32 + kq;
+            const bf16x8 h = *(const bf16x8*)(ahi + ar * HT_ASTR + ka);
+            const bf16x8 l = *(const bf16x8*)(alo + ar * HT_ASTR + ka);
+            // per group of up to 8 blocks, the hi products, then the lo ones:
+            // consecutive MFMAs are independent
+            constexpr int kG = kNBB < 8 ? kNBB : 8;
+#pragma unroll
+            for (int j0 = 0; j0 < kNBB; j0 += kG) {
+                bf16x8_t wb[kG];
+#pragma unroll
+                for (int j = 0; j < kG; ++j)
+                    wb[j] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(wl + ((j0 + j) * 16 + (lane & 15)) * HT_ASTR + ka));
+#pragma unroll
+                for (int j = 0; j < kG; ++j)
+                    acc[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, h), wb[j], acc[j0 + j], 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < kG; ++j)
+                    acc[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, l), wb[j], acc[j0 + j], 0, 0, 0);
+            }
+        }
+    };
+    auto store = [&](int c, uint16_t* stage) {
+        ht_store<kS, kNBB, kGelu>(a, c, g, stage, stage + HT_ROWS * HT_ASTR, stage + 2 * HT_ROWS * HT_ASTR);
+    };
+
+    ht_load(a, 0, g);
+    if constexpr (kTwo) {
+        // one barrier per chunk: chunk c + 1 is activated and written to the
+        // other stage (VALU) while chunk c's products run (MFMA); that stage
+        // was last read before the previous barrier
+        store(0, st0);
+        ht_load(a, 1, g);
+        __syncthreads();
+        int c = 0;
+        for (; c + 1 < nchunk; ++c) {
+            products((c & 1) ? st1 : st0);
+            store(c + 1, (c & 1) ? st0 : st1);
+            ht_load(a, c + 2, g);
+            __syncthreads();
+        }
+        products((c & 1) ? st1 : st0);
+    } else {
+        for (int c = 0; c < nchunk; ++c) {
+            store(c, st0);
+            __syncthreads();
+            ht_load(a, c + 1, g);                   // in flight during the products
+            products(st0);
+            __syncthreads();                        // before the next chunk overwrites LDS
+        }
+    }
+
+    // softmax over the bins: element v of acc[j] is row 4 (lane / 16) + v of
+    // the wave's 16, bin 16 j + lane % 16
+    // logits with b2; absent bins (past nb) become -inf
+    // and their bin values 0, so that the loops below need no conditions
+    float bvl[kNBB];
+#pragma unroll
+    for (int j = 0; j < kNBB; ++j) {
+        const int col = j * 16 + (lane & 15);
+        const bool ok = col < nb;
+        const int cc = ok ? col : 0;
+        bvl[j] = ok ? bins[cc] : 0.0f;
+        const float bias = b2 ? b2[cc] : 0.0f;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[j][v] = ok ? acc[j][v] + bias : -INFINITY;
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < kNBB; ++j) mx = fmaxf(mx, acc[j][v]);
+#pragma unroll
+        for (int o = 8; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 16));
+        float den = 0.0f, num = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kNBB; ++j) {
+            const float e = expf(acc[j][v] - mx);      // exp(-inf) = 0 for absent bins
+            den += e;
+            num += e * bvl[j];
+        }
+#pragma unroll
+        for (int o = 8; o > 0; o >>= 1) {
+            den += __shfl_xor(den, o, 16);
+            num += __shfl_xor(num, o, 16);
+        }
+        const int gr = row0 + wid * 16 + 4 * (lane >> 4) + v;
+        if ((lane & 15) == 0 && gr < B) {
+            const float E = num / den;
+            expected[gr] = E;
+            float y = E;
+            if (ema_alpha > 0.0f) {
+                y = ema_init ? E : ema_alpha * E + (1.0f - ema_alpha) * ema_state[gr];
+                ema_state[gr] = y;
+            }
+            if (rem_len) {
+                const float q = rintf(y);
+                int32_t li;
+                if (!(q >= 1.0f)) li = 1;
+                else if (q >= (float)len_max) li = len_max;
+                else li = (int32_t)q;
+                rem_len[gr] = li;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // (f3) between the regression head's first two layers: fixed-order split-K
 // reduction, bias, ReLU, and the operand of the next product (bf16, round
 // to nearest even, or fp32)
@@ -638,9 +911,7 @@ __global__ __launch_bounds__(ACT_THREADS) void act_kernel(const float* __restric
             const float a0 = fmaxf(sum.x + bv.x, 0.0f), a1 = fmaxf(sum.y + bv.y, 0.0f);
             const float a2 = fmaxf(sum.z + bv.z, 0.0f), a3 = fmaxf(sum.w + bv.w, 0.0f);
             if constexpr (kBF16) {
-                ((uint2*)out)[e] = make_uint2(
-                    f32_to_bf16_rne(a0) | ((uint32_t)f32_to_bf16_rne(a1) << 16),
-                    f32_to_bf16_rne(a2) | ((uint32_t)f32_to_bf16_rne(a3) << 16));
+                ((uint2*)out)[e] = make_uint2(pack_bf16x2_rne(a0, a1), pack_bf16x2_rne(a2, a3));
             } else {
                 ((float4*)out)[e] = make_float4(a0, a1, a2, a3);
             }
@@ -702,7 +973,7 @@ GemmPlan plan_gemm(int M, int N, int K, int elem) {
     return best;
 }
 
-PredictPlan plan_predict(const star_predict_params& p, bool wide_rows) {
+PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok) {
     PredictPlan pl;
     const GemmPlan g = plan_gemm(p.n_req, p.d_hidden, p.d_model, p.dtype == STAR_BF16 ? 2 : 4);
     pl.gemm = g;
@@ -714,10 +985,13 @@ PredictPlan plan_predict(const star_predict_params& p, bool wide_rows) {
     pl.partial_bytes = (size_t)s * (size_t)p.n_req * (size_t)p.d_hidden * sizeof(float);
     const int mpad = (p.d_hidden + 31) & ~31;
     const int nbpad = (p.n_bins + 15) & ~15;
-    pl.head_rows = wide_rows && p.dtype == STAR_BF16 && p.n_req >= HD_WIDE_MIN_REQ ? HD_RB_WIDE
-                                                                                  : HD_RB;
+    pl.head_tiled = tiled_ok && p.dtype == STAR_BF16 && p.n_req >= HT_MIN_REQ &&
+                    s <= HT_MAX_SPLITS;
+    pl.head_rows = pl.head_tiled ? HT_ROWS : HD_RB;
     const size_t rb = (size_t)pl.head_rows;
-    if (p.dtype == STAR_BF16)
+    if (pl.head_tiled)
+        pl.head_lds = head_tiled_lds(p.n_bins);
+    else if (p.dtype == STAR_BF16)
         pl.head_lds = 2 * rb * (mpad + 8) * 2 + rb * nbpad * 4;
     else
         pl.head_lds = rb * p.d_hidden * 4 + rb * nbpad * 4;
@@ -743,20 +1017,50 @@ static hipError_t launch_head_rows(const star_predict_params& p, const PredictPl
     return hipGetLastError();
 }
 
-// 16-row workgroups only for the bf16 binned head (the plan never picks
-// them elsewhere)
+template <int kS, int kNBB, bool kGelu>
+static hipError_t launch_head_tiled_act(const star_predict_params& p, const PredictPlan& pl,
+                                    const float* partials, const float* b1, const void* w2,
+                                    const float* b2, const float* bins, float* ema_state,
+                                    float* expected, int32_t* rem_len, hipStream_t stream) {
+    if (pl.head_lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)head_tiled_kernel<kS, kNBB, kGelu>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)pl.head_lds);
+        if (e != hipSuccess) return e;
+    }
+    const dim3 grid((unsigned)ceil_div(p.n_req, HT_ROWS));
+    hipLaunchKernelGGL((head_tiled_kernel<kS, kNBB, kGelu>), grid, dim3(HD_THREADS), pl.head_lds, stream,
+                       partials, p.n_req, p.d_hidden, p.n_bins, b1, (const uint16_t*)w2, b2, bins,
+                       p.ema_alpha, p.ema_init, ema_state, expected, rem_len, p.len_max);
+    return hipGetLastError();
+}
+
+template <int kS, int kNBB>
+static hipError_t launch_head_tiled(const star_predict_params& p, const PredictPlan& pl,
+                                    const float* partials, const float* b1, const void* w2,
+                                    const float* b2, const float* bins, float* ema_state,
+                                    float* expected, int32_t* rem_len, hipStream_t stream) {
+    return p.act == STAR_ACT_GELU_ERF
+        ? launch_head_tiled_act<kS, kNBB, true>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream)
+        : launch_head_tiled_act<kS, kNBB, false>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
+}
+
+// The tiled head only for the bf16 binned head with at most HT_MAX_SPLITS
+// planes (the plan never picks it elsewhere).
 template <bool kBF16, int kS, bool kReg>
 static hipError_t launch_head_s(const star_predict_params& p, const PredictPlan& pl,
                                 const float* partials, const float* b1, const void* w2,
                                 const float* b2, const float* bins, float* ema_state,
                                 float* expected, int32_t* rem_len, float b4, hipStream_t stream) {
-    if constexpr (kBF16 && !kReg) {
-        if (pl.head_rows == HD_RB_WIDE)
-            return launch_head_rows<kBF16, kS, kReg, HD_RB_WIDE>(p, pl, partials, b1, w2, b2,
-                                                                 bins, ema_state, expected,
-                                                                 rem_len, b4, stream);
+    if constexpr (kBF16 && !kReg && kS <= HT_MAX_SPLITS) {
+        if (pl.head_tiled) {
+            const int nbb = head_tiled_blocks(p.n_bins);
+            return nbb == 4 ? launch_head_tiled<kS, 4>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream)
+                 : nbb == 8 ? launch_head_tiled<kS, 8>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream)
+                            : launch_head_tiled<kS, 16>(p, pl, partials, b1, w2, b2, bins, ema_state, expected, rem_len, stream);
+        }
     }
-    if (pl.head_rows != HD_RB) return hipErrorInvalidValue;
+    if (pl.head_tiled || pl.head_rows != HD_RB) return hipErrorInvalidValue;
     return launch_head_rows<kBF16, kS, kReg, HD_RB>(p, pl, partials, b1, w2, b2, bins, ema_state,
                                                     expected, rem_len, b4, stream);
 }

@@ -28,13 +28,19 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));  // MFMA operand ty
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-// fp32 -> bf16 bits, round to nearest even (finite inputs).
-__device__ inline uint16_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+// two fp32 -> packed bf16 bits, a in the low half, round to nearest even (one
+// packed conversion instruction)
+__device__ inline uint32_t pack_bf16x2_rne(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2_t));
 }
-__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+// a (and b) as a bf16 pair hi + lo, hi = bf16(a), lo = bf16(a - hi): packed
+// hi and lo words for two values
+__device__ inline void split_bf16x2(float a, float b, uint32_t& hi, uint32_t& lo) {
+    hi = pack_bf16x2_rne(a, b);
+    lo = pack_bf16x2_rne(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xFFFF0000u));
+}
 
 // ---------------------------------------------------------------------------
 // wavefront reductions (64 lanes)

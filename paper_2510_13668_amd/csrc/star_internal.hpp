@@ -22,9 +22,10 @@ struct PredictPlan {
     int tiles_m = 0, tiles_n = 0, ktiles = 0, splits = 1;
     size_t partial_bytes = 0;   // fp32 split-K partials [splits, B, m]
     size_t head_lds = 0;        // dynamic LDS of the head kernel
-    int head_rows = 4;          // rows per head workgroup (4 or 16)
+    int head_rows = 4;          // rows per head workgroup
+    bool head_tiled = false;    // the K-chunked head (large bf16 batches), 64 rows per workgroup
 };
-PredictPlan plan_predict(const star_predict_params& p, bool wide_rows = true);
+PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok = true);
 hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, const void* hidden,
                           const void* w1, const float* b1, const void* w2, const float* b2,
                           const float* bins, float* ema_state, float* expected, int32_t* rem_len,
