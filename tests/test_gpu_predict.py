@@ -91,9 +91,9 @@ def test_ragged_shapes(dtype, act, B, d, m, nb):
 @pytest.mark.parametrize("B,d,m,nb", [(8200, 64, 2048, 256), (8192 + 13, 136, 72, 20),
                                      (9000, 512, 1024, 128)])
 def test_wide_head_rows_sampled(B, d, m, nb):
-    """Batches of 8192 and more take 16-row head workgroups: ragged last
-    workgroup, maximum width and bins, and odd widths; checked on the first
-    and last rows and a random sample."""
+    """bf16 batches of 8192 and more take the K-chunked 64-row head: ragged
+    last workgroup, maximum width and bins, odd widths and a ragged last
+    chunk; checked on the first and last rows and a random sample."""
     rng = np.random.default_rng(B + d + m + nb)
     h = synth.f32_to_bf16_bits(rng.standard_normal((B, d)).astype(np.float32))
     w1 = synth.f32_to_bf16_bits((rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32))
@@ -106,6 +106,41 @@ def test_wide_head_rows_sampled(B, d, m, nb):
     print(f"wide head B={B} d={d} m={m} nb={nb}", flush=True)
     _run_case(h, w1, w2, bins, dtype=synth.BF16, act=synth.ACT_GELU, b1=b1, b2=b2,
               len_max=32768, sample=sample)
+
+
+def _splits(B, d, m, nb):
+    """Split-K planes the plan takes, from the workspace size (host only)."""
+    from paper_2510_13668_amd import star
+    p = star.predict_params(B, d, m, nb, synth.BF16, synth.ACT_RELU)
+    extra = star.predict_workspace_size(p) - star.STAR_WS_HEADER_BYTES
+    assert extra % (B * m * 4) == 0
+    return extra // (B * m * 4)
+
+
+@pytest.mark.parametrize("B,d,m,nb,act,planes", [
+    (8200, 1024, 64, 60, synth.ACT_RELU, 2),       # 4 bin blocks
+    (8192, 2048, 128, 100, synth.ACT_GELU, 2),     # 8 blocks, two LDS stages
+    (8192, 4096, 128, 64, synth.ACT_RELU, 4),      # 4 blocks, ReLU
+    (8192, 4096, 128, 100, synth.ACT_GELU, 4),     # 8 blocks
+    (8192, 4096, 64, 200, synth.ACT_RELU, 4),      # 16 blocks, one LDS stage
+    (9000, 512, 1024, 128, synth.ACT_RELU, 1),     # one plane, ReLU
+])
+def test_tiled_head_planes_and_activations(B, d, m, nb, act, planes):
+    """The K-chunked head over every number of split-K planes it accepts (1,
+    2, 4), every bin-block count and both activations; sampled rows."""
+    assert _splits(B, d, m, nb) == planes, "the plan no longer takes this many planes here"
+    rng = np.random.default_rng(B * 7 + d + m + nb)
+    h = synth.f32_to_bf16_bits(rng.standard_normal((B, d)).astype(np.float32))
+    w1 = synth.f32_to_bf16_bits((rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32))
+    w2 = synth.f32_to_bf16_bits((rng.standard_normal((nb, m)) * 4 / np.sqrt(m)).astype(np.float32))
+    b1 = (rng.standard_normal(m) * 0.1).astype(np.float32)
+    b2 = (rng.standard_normal(nb) * 0.1).astype(np.float32)
+    bins = synth.bin_values(nb, 1.0, 32768.0)
+    sample = np.unique(np.concatenate([np.arange(70), np.arange(B - 70, B),
+                                       rng.choice(B, 120, replace=False)]))
+    print(f"tiled head B={B} d={d} m={m} nb={nb} act={act} planes={planes}", flush=True)
+    _run_case(h, w1, w2, bins, dtype=synth.BF16, act=act, b1=b1, b2=b2, len_max=32768,
+              sample=sample)
 
 
 def test_large_fp32_sampled():
