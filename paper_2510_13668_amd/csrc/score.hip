@@ -34,7 +34,10 @@
 //    best key is smallest (its key is >= its request's best key, and k
 //    distinct requests have best keys below the k-th smallest migration key
 //    otherwise), so the k requests are selected first and only their k(n-1)
-//    migrations are ranked.
+//    migrations are ranked.  When there are more requests than best keys fit
+//    its registers, the top-k counts the best keys' codes (a monotone summary
+//    of the score) in an LDS histogram and gathers only the best keys up to
+//    the code that holds the k-th.
 #include "star_common.hpp"
 #include "star_internal.hpp"
 
@@ -54,8 +57,10 @@ constexpr int SEL_BINS = 1 << SEL_DIGIT;
 constexpr int SEL_SBATCH = 8;                // reads per thread in flight when streaming keys
 
 constexpr int TK_THREADS = 1024;             // top-k workgroup of the multi-workgroup path
-constexpr int TK_RJ = 8;                     // keys per thread held in registers there
+constexpr int TK_RJ = 16;                    // migration keys per thread held in registers there
 constexpr int TK_REG_KEYS = TK_RJ * TK_THREADS;
+constexpr int TK_RJ1 = 8;                    // best keys per thread in registers (pruned, stage 1)
+constexpr int TK_REG_BEST = TK_RJ1 * TK_THREADS;
 
 constexpr int SS_THREADS = 512;              // the one workgroup of the small path
 constexpr int SS_RJ = 16;                    // candidates per thread
@@ -77,6 +82,18 @@ __device__ inline bool key_less(int64_t s0, uint32_t i0, int64_t s1, uint32_t i1
 }
 
 __device__ inline int bit_length(uint64_t x) { return x ? 64 - __clzll((long long)x) : 0; }
+
+// A key's code is a monotone 10-bit summary of d = score - base (base: the
+// smallest target peak, which no migration score is below): the position of
+// d's leading one and the four bits after it.  Keys with a smaller code are
+// smaller keys, so the k smallest keys are all keys whose code is below some
+// c*, plus the smallest few of those with code c*.
+__device__ inline uint32_t key_code(uint64_t d) {
+    const int e = bit_length(d);                         // 0..63
+    if (e <= 4) return (uint32_t)d;
+    return ((uint32_t)(e - 4) << 4) | (uint32_t)((d >> (e - 5)) & 15);   // < 960
+}
+
 
 // q = x / d for d >= 1 with m = floor((2^32 - 1) / d) + 1 (m = 0 encodes
 // d = 1): the multiply-high estimate is exact or one too large (x + d < 2^32).
@@ -472,6 +489,7 @@ struct ScoreArgs {
     int64_t* best_score;
     int32_t* err_word;
     int64_t* load_out;            // curves built by the scoring kernel itself (group 0 writes)
+    int64_t* bbase;               // code base for the top-k's best keys (group 0 writes), or null
     int N, n, b, K, rpb, cand;
     uint32_t magic_K, magic_n;
 };
@@ -586,6 +604,23 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
         ki[e] = key_i;
     }
     __syncthreads();
+
+    // the code base of the top-k's best keys: the smallest target peak (no
+    // migration scores below it), one read per thread and a block minimum
+    if (a.bbase) {
+        int64_t base = INT64_MAX;
+        __shared__ int64_t wmin[SC_THREADS / 64];
+        for (int t = tid; t < n; t += SC_THREADS) {
+            const int64_t v = gSM[(int64_t)t * K1];
+            base = v < base ? v : base;
+        }
+        base = -readlane_i64(wave_incl_max_i64(-base), 63);
+        if (lane == 0) wmin[tid >> 6] = base;
+        __syncthreads();
+#pragma unroll
+        for (int w = 0; w < SC_THREADS / 64; ++w) base = wmin[w] < base ? wmin[w] : base;
+        if (blockIdx.x == 0 && tid == 0) *a.bbase = base;
+    }
 
     // 2) best migration per request: smallest (score, t) over t != s
     for (int q = tid; q < rpb; q += SC_THREADS) {
@@ -709,6 +744,9 @@ struct TopkArgs {
     int32_t* topk_req;
     int32_t* topk_tgt;
     int64_t* topk_score;
+    const int64_t* bbase;         // code base of the best keys (the smallest target peak)
+    int64_t* gs;                  // [TK_REG_BEST] best keys gathered at or below the k-th code
+    uint32_t* gi;
     int N, n, top_k;
     uint32_t magic_n, magic_n1;   // fast_div multipliers for n and n - 1
 };
@@ -752,12 +790,13 @@ struct PrunedKeys {               // every migration of the requests rk[0..nr), 
 
 // Register loaders of the 1024-thread top-k: every slot is loaded (clamped
 // index) and masked afterwards, so the reads are issued together.
-__device__ inline void load_migrations(RegKeys<TK_RJ>& k, const TopkArgs& a) {
+template <int RJ>
+__device__ inline void load_migrations(RegKeys<RJ>& k, const TopkArgs& a) {
     const int M = a.N * a.n;                               // >= 1
-    int32_t iv[TK_RJ], bv[TK_RJ];
-    uint32_t qv[TK_RJ];
+    int32_t iv[RJ], bv[RJ];
+    uint32_t qv[RJ];
 #pragma unroll
-    for (int j = 0; j < TK_RJ; ++j) {
+    for (int j = 0; j < RJ; ++j) {
         const int e = j * TK_THREADS + (int)threadIdx.x;
         const uint32_t ec = (uint32_t)(e < M ? e : M - 1);
         qv[j] = fast_div(ec, (uint32_t)a.n, a.magic_n);
@@ -766,7 +805,7 @@ __device__ inline void load_migrations(RegKeys<TK_RJ>& k, const TopkArgs& a) {
         bv[j] = a.best_target[qv[j]];
     }
 #pragma unroll
-    for (int j = 0; j < TK_RJ; ++j) {
+    for (int j = 0; j < RJ; ++j) {
         const int e = j * TK_THREADS + (int)threadIdx.x;
         const bool ok = e < M && bv[j] >= 0 && (int)((uint32_t)e - qv[j] * (uint32_t)a.n) != iv[j];
         k.s[j] = ok ? k.s[j] : kInfS;
@@ -774,17 +813,17 @@ __device__ inline void load_migrations(RegKeys<TK_RJ>& k, const TopkArgs& a) {
     }
 }
 
-__device__ inline void load_best(RegKeys<TK_RJ>& k, const TopkArgs& a) {
-    int32_t bt[TK_RJ];
+__device__ inline void load_best(RegKeys<TK_RJ1>& k, const TopkArgs& a) {
+    int32_t bt[TK_RJ1];
 #pragma unroll
-    for (int j = 0; j < TK_RJ; ++j) {
+    for (int j = 0; j < TK_RJ1; ++j) {
         const int r = j * TK_THREADS + (int)threadIdx.x;
         const int rc = r < a.N ? r : a.N - 1;              // N >= 1
         k.s[j] = a.best_score[rc];
         bt[j] = a.best_target[rc];
     }
 #pragma unroll
-    for (int j = 0; j < TK_RJ; ++j) {
+    for (int j = 0; j < TK_RJ1; ++j) {
         const int r = j * TK_THREADS + (int)threadIdx.x;
         const bool ok = r < a.N && bt[j] >= 0;
         k.s[j] = ok ? k.s[j] : kInfS;
@@ -792,21 +831,22 @@ __device__ inline void load_best(RegKeys<TK_RJ>& k, const TopkArgs& a) {
     }
 }
 
-__device__ inline void load_pruned(RegKeys<TK_RJ>& k, const TopkArgs& a, const int32_t* rk,
+template <int RJ>
+__device__ inline void load_pruned(RegKeys<RJ>& k, const TopkArgs& a, const int32_t* rk,
                                    const int32_t* rk_inst, int M) {
 #pragma unroll
-    for (int j = 0; j < TK_RJ; ++j) {
+    for (int j = 0; j < RJ; ++j) {
         k.s[j] = kInfS;
         k.i[j] = kInfI;
     }
     if (M == 0) return;                                    // no request has a migration
 #pragma unroll
-    for (int j = 0; j < TK_RJ; ++j) {
+    for (int j = 0; j < RJ; ++j) {
         const int e = j * TK_THREADS + (int)threadIdx.x;
         pruned_key(a, rk, rk_inst, (uint32_t)(e < M ? e : M - 1), &k.s[j], &k.i[j]);
     }
 #pragma unroll
-    for (int j = 0; j < TK_RJ; ++j) {
+    for (int j = 0; j < RJ; ++j) {
         const int e = j * TK_THREADS + (int)threadIdx.x;
         k.s[j] = e < M ? k.s[j] : kInfS;
         k.i[j] = e < M ? k.i[j] : kInfI;
@@ -1091,13 +1131,14 @@ __device__ int select_top(const Src& src, int k, int ibits, SelShared<kT>& sh, i
 // ---------------------------------------------------------------------------
 // top-k kernels of the multi-workgroup path (one workgroup)
 // ---------------------------------------------------------------------------
-// Every migration held in registers (N n <= TK_REG_KEYS).
+// Every migration held in registers, kRJ per thread (N n <= kRJ TK_THREADS).
+template <int kRJ>
 __global__ __launch_bounds__(TK_THREADS) void topk_direct_kernel(TopkArgs a) {
     __shared__ SelShared<TK_THREADS> sh;
     __shared__ int64_t ws_s[STAR_MAX_TOP_K];
     __shared__ uint32_t ws_i[STAR_MAX_TOP_K];
     __shared__ uint64_t sv[STAR_MAX_TOP_K];
-    RegKeys<TK_RJ> keys;
+    RegKeys<kRJ> keys;
     load_migrations(keys, a);
     const int ibits = bit_length((uint64_t)(a.N * a.n - 1));
     int64_t smin, smax_w;
@@ -1106,9 +1147,105 @@ __global__ __launch_bounds__(TK_THREADS) void topk_direct_kernel(TopkArgs a) {
                                 a.topk_tgt, a.topk_score, a.top_k, sh, sv);
 }
 
+// The k smallest of the g gathered best keys, RJ per thread in registers.
+template <int RJ>
+__device__ int select_gathered(const TopkArgs& a, int g, int ib1, SelShared<TK_THREADS>& sh,
+                               int64_t* ws_s, uint32_t* ws_i, int64_t* smin, int64_t* smax_w) {
+    RegKeys<RJ> keys;
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+        const int e = j * TK_THREADS + (int)threadIdx.x;
+        const int ec = e < g ? e : 0;
+        keys.s[j] = a.gs[ec];
+        keys.i[j] = a.gi[ec];
+    }
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+        const int e = j * TK_THREADS + (int)threadIdx.x;
+        keys.s[j] = e < g ? keys.s[j] : kInfS;
+        keys.i[j] = e < g ? keys.i[j] : kInfI;
+    }
+    return select_top<TK_THREADS>(keys, a.top_k, ib1, sh, ws_s, ws_i, smin, smax_w);
+}
+
+// Best key of request r (s = kInfS: none), loaded in batches of SEL_SBATCH
+// per thread; f(r, s) for each.
+template <class F>
+__device__ inline void visit_best(const TopkArgs& a, F&& f) {
+    for (int r0 = 0; r0 < a.N; r0 += TK_THREADS * SEL_SBATCH) {
+        int64_t bs[SEL_SBATCH];
+        int32_t bt[SEL_SBATCH];
+#pragma unroll
+        for (int u = 0; u < SEL_SBATCH; ++u) {
+            const int r = r0 + u * TK_THREADS + (int)threadIdx.x;
+            const int rc = r < a.N ? r : a.N - 1;
+            bs[u] = a.best_score[rc];
+            bt[u] = a.best_target[rc];
+        }
+#pragma unroll
+        for (int u = 0; u < SEL_SBATCH; ++u) {
+            const int r = r0 + u * TK_THREADS + (int)threadIdx.x;
+            f(r, r < a.N && bt[u] >= 0 ? bs[u] : kInfS);
+        }
+    }
+}
+
+// The k smallest best keys by their codes: one pass counts the codes in an
+// LDS histogram and finds the code c* that holds the k-th key, a second
+// gathers every best key of code <= c* (all of the k smallest, and only keys
+// no larger than the rest of code c*), and those are selected in registers.
+// More than TK_REG_BEST such keys (a crowded code c*) take the streamed
+// selection over all best keys instead.
+__device__ int select_best_by_code(const TopkArgs& a, int ib1, SelShared<TK_THREADS>& sh,
+                                   int64_t* ws_s, uint32_t* ws_i, int64_t* smin,
+                                   int64_t* smax_w, int* gcount) {
+    static_assert(RK_CODES == TK_THREADS && RK_CODES <= SEL_BINS, "one code per thread");
+    const int tid = threadIdx.x;
+    const int64_t base = *a.bbase;
+    sh.hist[tid] = 0;
+    __syncthreads();
+    visit_best(a, [&](int, int64_t s) {
+        if (s != kInfS) atomicAdd(&sh.hist[key_code((uint64_t)(s - base))], 1);
+    });
+    __syncthreads();
+    const int h = sh.hist[tid];
+    int total;
+    const int before = block_excl_i32<TK_THREADS>(h, sh, &total);
+    const bool all = total <= a.top_k;
+    if (all ? tid == RK_CODES - 1 : (before < a.top_k && before + h >= a.top_k)) {
+        sh.bcast[0] = tid;                     // c*
+        sh.bcast[1] = before + h;              // best keys of code <= c*
+    }
+    if (tid == 0) *gcount = 0;
+    __syncthreads();
+    const uint32_t cstar = (uint32_t)sh.bcast[0];
+    const int nle = sh.bcast[1];
+    __syncthreads();
+    if (nle > TK_REG_BEST) {
+        BestKeys bk{a.best_score, a.best_target, a.N};
+        return select_top<TK_THREADS>(bk, a.top_k, ib1, sh, ws_s, ws_i, smin, smax_w);
+    }
+    visit_best(a, [&](int r, int64_t s) {
+        if (s != kInfS && key_code((uint64_t)(s - base)) <= cstar) {
+            const int at = atomicAdd(gcount, 1);
+            if (at < TK_REG_BEST) {
+                a.gs[at] = s;
+                a.gi[at] = (uint32_t)r;
+            }
+        }
+    });
+    __syncthreads();                           // the gathered keys are visible to the workgroup
+    const int g = *gcount < TK_REG_BEST ? *gcount : TK_REG_BEST;
+    return select_gathered<TK_RJ1>(a, g, ib1, sh, ws_s, ws_i, smin, smax_w);
+}
+
+// How the pruned top-k finds the k requests with the smallest best keys: all
+// best keys in registers, or those the code histogram leaves.
+enum : int { kStage1Reg = 0, kStage1Code = 1 };
+
 // First the k requests with the smallest best keys, then the k smallest of
-// their migrations; each stage in registers when it fits, else streamed.
-template <bool kReg1, bool kReg2>
+// their migrations (kRJ2 per thread in registers, or streamed when 0).
+template <int kStage1, int kRJ2>
 __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
     __shared__ SelShared<TK_THREADS> sh;
     __shared__ int64_t ws_s[STAR_MAX_TOP_K];
@@ -1116,16 +1253,16 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
     __shared__ uint64_t sv[STAR_MAX_TOP_K];
     __shared__ int32_t rk[STAR_MAX_TOP_K];
     __shared__ int32_t rk_inst[STAR_MAX_TOP_K];
+    __shared__ int gcount;
     int nr;
     int64_t smin, smax_w;
     const int ib1 = bit_length((uint64_t)(a.N - 1));
-    if constexpr (kReg1) {
-        RegKeys<TK_RJ> keys;
+    if constexpr (kStage1 == kStage1Reg) {
+        RegKeys<TK_RJ1> keys;
         load_best(keys, a);
         nr = select_top<TK_THREADS>(keys, a.top_k, ib1, sh, ws_s, ws_i, &smin, &smax_w);
     } else {
-        BestKeys bk{a.best_score, a.best_target, a.N};
-        nr = select_top<TK_THREADS>(bk, a.top_k, ib1, sh, ws_s, ws_i, &smin, &smax_w);
+        nr = select_best_by_code(a, ib1, sh, ws_s, ws_i, &smin, &smax_w, &gcount);
     }
     for (int q = threadIdx.x; q < nr; q += TK_THREADS) {
         const int r = (int)ws_i[q];
@@ -1136,8 +1273,8 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
     const int M = nr * (a.n - 1);
     const int ib2 = bit_length((uint64_t)((int64_t)a.N * a.n - 1));
     int nw;
-    if constexpr (kReg2) {
-        RegKeys<TK_RJ> keys;
+    if constexpr (kRJ2 > 0) {
+        RegKeys<kRJ2> keys;
         load_pruned(keys, a, rk, rk_inst, M);
         nw = select_top<TK_THREADS>(keys, a.top_k, ib2, sh, ws_s, ws_i, &smin, &smax_w);
     } else {
@@ -1151,17 +1288,6 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
 // ---------------------------------------------------------------------------
 // score + first ranking stage (many workgroups), then one workgroup ranks
 // ---------------------------------------------------------------------------
-// A key's code is a monotone 10-bit summary of d = score - base (base: the
-// smallest target peak, which no migration score is below): the position of
-// d's leading one and the four bits after it.  Keys with a smaller code are
-// smaller keys, so the k smallest keys are all keys whose code is below some
-// c*, plus the smallest few of those with code c*.
-__device__ inline uint32_t key_code(uint64_t d) {
-    const int e = bit_length(d);                         // 0..63
-    if (e <= 4) return (uint32_t)d;
-    return ((uint32_t)(e - 4) << 4) | (uint32_t)((d >> (e - 5)) & 15);   // < 960
-}
-
 struct RankArgs {
     uint32_t* ghist;              // [RK_CODES] counts over all groups (zero on entry)
     int64_t* base;                // the code base, written by group 0
@@ -1809,9 +1935,12 @@ ScorePlan plan_score(const star_score_params& p, bool project) {
     pl.groups = N > 0 ? (int)ceil_div(N, pl.rpb) : 0;
     // top-k: select over all migrations when they fit one workgroup's
     // registers, else over the k requests with the smallest best keys first
-    pl.topk_direct = (int64_t)N * n <= TK_REG_KEYS;
-    pl.topk_reg1 = N <= TK_REG_KEYS;
-    pl.topk_reg2 = (int64_t)p.top_k * (n - 1) <= TK_REG_KEYS;
+    // register slots per thread: 8 when that holds every key, else 16
+    const int64_t nmig = (int64_t)N * n, npr = (int64_t)p.top_k * (n - 1);
+    pl.topk_direct = nmig <= TK_REG_KEYS;
+    pl.topk_rj = nmig <= 8 * TK_THREADS ? 8 : TK_RJ;
+    pl.topk_reg1 = N <= TK_REG_BEST;
+    pl.topk_rj2 = npr <= 8 * TK_THREADS ? 8 : npr <= TK_REG_KEYS ? TK_RJ : 0;
 
     size_t off = STAR_WS_HEADER_BYTES;
     // fused scoring with the two-stage ranking: the scoring workgroups sort
@@ -1849,6 +1978,15 @@ ScorePlan plan_score(const star_score_params& p, bool project) {
     off = align_up(off + (size_t)N * 8, 256);
     pl.btarget_off = off;
     off = align_up(off + (size_t)N * 4, 256);
+    pl.topk_hist = p.top_k > 0 && n > 1 && !pl.topk_direct && !pl.topk_reg1;
+    if (pl.topk_hist) {
+        pl.base_off = off;
+        off = align_up(off + 8, 256);
+        pl.gs_off = off;
+        off = align_up(off + (size_t)TK_REG_BEST * 8, 256);
+        pl.gi_off = off;
+        off = align_up(off + (size_t)TK_REG_BEST * 4, 256);
+    }
     pl.total = off;
     pl.lds = (pl.fused ? (size_t)3 * n * K1 * 8 : 0) + (size_t)pl.cand * 12 + (size_t)pl.rpb * 24;
     return pl;
@@ -1863,7 +2001,7 @@ static hipError_t set_lds(const void* fn, size_t lds, size_t static_lds) {
 
 template <bool kFused>
 static hipError_t launch_score_kernel(const ScorePlan& pl, const ScoreArgs& a, hipStream_t stream) {
-    hipError_t e = set_lds((const void*)score_kernel<kFused>, pl.lds, 0);
+    hipError_t e = set_lds((const void*)score_kernel<kFused>, pl.lds, 64);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(score_kernel<kFused>, dim3(pl.groups), dim3(SC_THREADS), pl.lds, stream, a);
     return hipGetLastError();
@@ -1874,10 +2012,17 @@ static hipError_t fill_i32(int32_t* p, int count, int32_t v, hipStream_t stream)
     return hipGetLastError();
 }
 
-template <bool R1, bool R2>
-static hipError_t launch_topk_pruned(const TopkArgs& a, hipStream_t stream) {
-    hipLaunchKernelGGL((topk_pruned_kernel<R1, R2>), dim3(1), dim3(TK_THREADS), 0, stream, a);
+template <int S1, int RJ2>
+static hipError_t launch_topk_pruned1(const TopkArgs& a, hipStream_t stream) {
+    hipLaunchKernelGGL((topk_pruned_kernel<S1, RJ2>), dim3(1), dim3(TK_THREADS), 0, stream, a);
     return hipGetLastError();
+}
+
+template <int S1>
+static hipError_t launch_topk_pruned(const TopkArgs& a, int rj2, hipStream_t stream) {
+    return rj2 == 8 ? launch_topk_pruned1<S1, 8>(a, stream)
+         : rj2 == TK_RJ ? launch_topk_pruned1<S1, TK_RJ>(a, stream)
+                        : launch_topk_pruned1<S1, 0>(a, stream);
 }
 
 hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const int32_t* cur,
@@ -1958,6 +2103,7 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     a.rpb = pl.rpb; a.cand = pl.cand;
     a.magic_K = div_magic((uint32_t)lp.n_buckets);
     a.magic_n = div_magic((uint32_t)lp.n_inst);
+    if (pl.topk_hist) a.bbase = (int64_t*)(ws + pl.base_off);
     hipError_t e;
     if (pl.fused) {
         e = launch_score_kernel<true>(pl, a, stream);
@@ -1986,13 +2132,17 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     t.magic_n = div_magic((uint32_t)lp.n_inst);
     t.magic_n1 = div_magic((uint32_t)lp.n_inst - 1);
     if (pl.topk_direct) {
-        hipLaunchKernelGGL(topk_direct_kernel, dim3(1), dim3(TK_THREADS), 0, stream, t);
+        if (pl.topk_rj == 8)
+            hipLaunchKernelGGL(topk_direct_kernel<8>, dim3(1), dim3(TK_THREADS), 0, stream, t);
+        else
+            hipLaunchKernelGGL(topk_direct_kernel<TK_RJ>, dim3(1), dim3(TK_THREADS), 0, stream, t);
         return hipGetLastError();
     }
-    if (pl.topk_reg1) return pl.topk_reg2 ? launch_topk_pruned<true, true>(t, stream)
-                                          : launch_topk_pruned<true, false>(t, stream);
-    return pl.topk_reg2 ? launch_topk_pruned<false, true>(t, stream)
-                        : launch_topk_pruned<false, false>(t, stream);
+    if (pl.topk_reg1) return launch_topk_pruned<kStage1Reg>(t, pl.topk_rj2, stream);
+    t.bbase = a.bbase;
+    t.gs = (int64_t*)(ws + pl.gs_off);
+    t.gi = (uint32_t*)(ws + pl.gi_off);
+    return launch_topk_pruned<kStage1Code>(t, pl.topk_rj2, stream);
 }
 
 }  // namespace star

@@ -62,8 +62,13 @@ struct ScorePlan {
     int cand = 0;         // candidates per scoring workgroup (rpb * n)
     int groups = 0;       // scoring workgroups
     bool topk_direct = false;  // top-k over all migrations (else over the k best requests' ones)
+    int topk_rj = 8;           // direct top-k: keys per thread in registers (8 or 16)
     bool topk_reg1 = false;    // pruned top-k: best keys fit registers
-    bool topk_reg2 = false;    // pruned top-k: the k requests' migrations fit registers
+    int topk_rj2 = 0;          // pruned top-k: the k requests' migrations per thread in
+                               // registers (8 or 16), 0: streamed
+    bool topk_hist = false;    // pruned top-k, best keys beyond registers: the top-k counts
+                               // their codes and gathers those up to the k-th
+    size_t gs_off = 0, gi_off = 0;  // topk_hist: gathered best keys (base_off: their code base)
     size_t pm_off = 0, sm_off = 0, scores_off = 0, bscore_off = 0, btarget_off = 0, total = 0;
     size_t lds = 0;       // dynamic LDS of the scoring kernel (or of the small path's one)
 };

@@ -126,17 +126,33 @@ def test_adversarial(case, fused):
 
 
 @pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
-@pytest.mark.parametrize("N", [256, 6000])
+@pytest.mark.parametrize("N", [256, 6000, 20000])
 def test_ties_from_duplicated_requests(N, fused):
-    """Many equal scores; N = 6000 takes the two-stage (pruned) ranking."""
+    """Many equal scores; N = 6000 takes the two-stage (pruned) ranking with
+    every best key in registers, N = 20000 narrows its first stage with the
+    best-key code histogram (16 instances: 1250 scoring workgroups)."""
     rng = np.random.default_rng(3)
-    n = 8
+    n = 8 if N < 20000 else 16
     cur = np.full(N, 1000, np.int32)
     rem = np.full(N, 777, np.int32)
     inst = rng.integers(0, n, N).astype(np.int32)
     cur[::3] = 5
     rem[::5] = 64
     _check(cur, rem, inst, n, 64, 32, 300, fused=fused)
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_crowded_best_code_takes_streamed_stage(fused):
+    """Every request's best move is the same (all go to the one empty
+    instance with equal lengths): the code that holds the k-th best key holds
+    all 20000 of them, more than the top-k can gather, so its first stage
+    selects over the streamed best keys."""
+    rng = np.random.default_rng(8)
+    N, n = 20000, 16
+    cur = np.full(N, 1000, np.int32)
+    rem = np.full(N, 777, np.int32)
+    inst = rng.integers(0, n - 1, N).astype(np.int32)     # instance n - 1 stays empty
+    _check(cur, rem, inst, n, 64, 32, 256, fused=fused)
 
 
 def _key_bits(ref, inst, n):
@@ -208,7 +224,8 @@ def test_empty_request_set(fused):
 # and 188 groups; too many requests to project per group (the projection
 # kernel runs first); no top-k; curves too large for LDS
 FUSED_PATHS = [(1024, 8, 64, 256, 256), (700, 5, 16, 100, 64), (6000, 8, 64, 32, 300),
-               (10000, 8, 16, 40, 512), (900, 6, 32, 50, 0), (300, 64, 8, 80, 100)]
+               (10000, 8, 16, 40, 512), (900, 6, 32, 50, 0), (300, 64, 8, 80, 100),
+               (10000, 64, 8, 40, 256)]
 
 
 def test_calls_of_every_path_share_a_workspace():
@@ -216,7 +233,8 @@ def test_calls_of_every_path_share_a_workspace():
     the largest, with a predictor call on the same workspace before each
     (its split-K partials fill the scratch area): the ranking's code
     histogram lives in the workspace header, which no call uses as scratch,
-    and every call must equal the oracle."""
+    and every call must equal the oracle.  The last case gathers best keys
+    by code in the workspace."""
     rng = np.random.default_rng(21)
     B, d, m, nb = 64, 512, 128, 32
     w1 = synth.f32_to_bf16_bits((rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32))
