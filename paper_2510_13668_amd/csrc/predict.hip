@@ -356,7 +356,15 @@ constexpr int HD_THREADS = 256;
 // float4 items per thread whose partial loads are in flight together: more
 // when there are few split-K planes (registers hold kS x batch float4)
 template <int kS> constexpr int hd_batch() { return kS == 1 ? 8 : kS == 2 ? 4 : 2; }
-constexpr int HD_W2PF = 16;       // W2 fragments (K-steps of 32) loaded per wave at a time
+// W2 fragments (K-steps of 32) a wave loads at a time, the first group at
+// kernel entry so that its latency overlaps the split-K reads.  A deep group
+// costs registers: past two workgroups per CU (more than 512 of them) the
+// shallow one, which keeps every workgroup resident, is faster (measured:
+// 54.9 -> 50.8 us per call at 4096 rows with two planes; at 1024 rows the
+// deep group is 0.2 us and for the regression head 1.2 us faster).
+constexpr int HD_W2PF = 16;
+constexpr int HD_W2PF_LOW = 2;
+constexpr int HD_LOWREG_GROUPS = 512;
 
 // GELU in its erf form, x Phi(x) with Phi the standard normal distribution
 // function, without branches: h = Phi(-|x|) = erfc(|x| / sqrt 2) / 2 from the
@@ -388,7 +396,7 @@ __device__ inline float apply_act(float x, int act) {
 // kReg: the regression head's last two layers instead of the binned one
 // (the nb "bin logits" are the third layer's outputs, `bins` holds w4 and
 // phase 3 computes relu(z) . w4 + b4 in place of the softmax mean).
-template <bool kBF16, int kS, bool kReg = false, int kRB = HD_RB>
+template <bool kBF16, int kS, bool kReg = false, int kPF = HD_W2PF>
 __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     const float* __restrict__ P, int B, int m, int nb, const float* __restrict__ b1,
     const void* __restrict__ w2, const float* __restrict__ b2, const float* __restrict__ bins,
@@ -399,22 +407,22 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
-    const int row0 = blockIdx.x * kRB;
+    const int row0 = blockIdx.x * HD_RB;
     const int mpad = (m + 31) & ~31;
     const int astride = mpad + 8;                 // bf16 elements per LDS row
     const int nbpad = (nb + 15) & ~15;
 
     uint16_t* ahi = (uint16_t*)smem;
-    uint16_t* alo = ahi + kRB * astride;
+    uint16_t* alo = ahi + HD_RB * astride;
     float* a32 = (float*)smem;
-    float* z = kBF16 ? (float*)(alo + kRB * astride) : (float*)(a32 + kRB * m);
+    float* z = kBF16 ? (float*)(alo + HD_RB * astride) : (float*)(a32 + HD_RB * m);
 
     // 0) everything phases 2 and 3 read from global memory is requested now,
     //    so that its latency overlaps the split-K reads
     const int r16 = lane & 15;
     const int kq = lane >> 4;
     const int j0 = wid * 16 + r16;                // this lane's bin in the wave's first block
-    bf16x8 wf0[HD_W2PF];
+    bf16x8 wf0[kPF];
     if constexpr (kBF16) {
         const uint16_t* W2 = (const uint16_t*)w2;
         // Loads are unconditional (clamped indices) so none of them is waited
@@ -422,7 +430,7 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
         // it only ever meets zero K-padding of a1 or lands in a column >= nb,
         // which is discarded.
 #pragma unroll
-        for (int u = 0; u < HD_W2PF; ++u) {
+        for (int u = 0; u < kPF; ++u) {
             const int k = u * 32 + kq * 8;
             const bool in = j0 < nb && k < m;
             wf0[u] = *(const bf16x8*)(W2 + (in ? (int64_t)j0 * m + k : 0));
@@ -437,7 +445,7 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
 
     // 1) fixed-order split-K reduction, bias, activation (float4 items)
     const int m4 = m >> 2;
-    const int items = kRB * m4;
+    const int items = HD_RB * m4;
     const int64_t plane4 = (int64_t)B * m4;
     const float4* P4 = (const float4*)P;
     for (int base = 0; base < items; base += kBatch * HD_THREADS) {
@@ -486,7 +494,7 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
         }
     }
     if constexpr (kBF16) {      // zero K padding [m, mpad)
-        for (int e = tid; e < kRB * (mpad - m); e += HD_THREADS) {
+        for (int e = tid; e < HD_RB * (mpad - m); e += HD_THREADS) {
             const int r = e / (mpad - m), u = m + e % (mpad - m);
             ahi[r * astride + u] = 0;
             alo[r * astride + u] = 0;
@@ -498,39 +506,39 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     if constexpr (kBF16) {
         // v_mfma_f32_16x16x32_bf16: lane feeds row (lane%16), k = 8*(lane/16)..+7;
         // accumulator element v of lane l is row 4*(l/16)+v, column l%16.  Only
-        // rows < kRB are real; the other A rows are fed as zeros.
+        // rows < HD_RB are real; the other A rows are fed as zeros.
         const uint16_t* W2 = (const uint16_t*)w2;
-        const bool arow = r16 < kRB;
+        const bool arow = r16 < HD_RB;
         for (int nblk = wid; nblk * 16 < nb; nblk += HD_THREADS / 64) {
             const int j = nblk * 16 + r16;
             f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-            for (int kb = 0; kb < mpad; kb += 32 * HD_W2PF) {
-                bf16x8 wf[HD_W2PF];
+            for (int kb = 0; kb < mpad; kb += 32 * kPF) {
+                bf16x8 wf[kPF];
                 if (nblk == wid && kb == 0) {
 #pragma unroll
-                    for (int u = 0; u < HD_W2PF; ++u) wf[u] = wf0[u];
+                    for (int u = 0; u < kPF; ++u) wf[u] = wf0[u];
                 } else {
 #pragma unroll
-                    for (int u = 0; u < HD_W2PF; ++u) {
+                    for (int u = 0; u < kPF; ++u) {
                         const int k = kb + u * 32 + kq * 8;
                         wf[u] = (j < nb && k < m) ? *(const bf16x8*)(W2 + (int64_t)j * m + k)
                                                   : bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
                     }
                 }
                 // all of this chunk's a1 fragments are read from LDS first, so
-                // their latencies overlap; rows >= kRB read row 0 and are
+                // their latencies overlap; rows >= HD_RB read row 0 and are
                 // zeroed afterwards (their MFMA rows are discarded anyway)
-                bf16x8 hv[HD_W2PF], lv[HD_W2PF];
+                bf16x8 hv[kPF], lv[kPF];
                 const int arow_off = (arow ? r16 : 0) * astride;
 #pragma unroll
-                for (int u = 0; u < HD_W2PF; ++u) {
+                for (int u = 0; u < kPF; ++u) {
                     const int k = (kb + u * 32 < mpad ? kb + u * 32 : 0) + kq * 8;
                     hv[u] = *(const bf16x8*)(ahi + arow_off + k);
                     lv[u] = *(const bf16x8*)(alo + arow_off + k);
                 }
                 const bf16x8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-                for (int u = 0; u < HD_W2PF; ++u) {
+                for (int u = 0; u < kPF; ++u) {
                     if (kb + u * 32 >= mpad) break;          // uniform: mpad % 32 == 0
                     const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, wf[u]);
                     const bf16x8 h = arow ? hv[u] : zero8;
@@ -544,12 +552,12 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
             for (int v = 0; v < 4; ++v) {
                 const int row = 4 * kq + v;
                 const float bias = nblk == wid ? b2v : (b2 && col < nb ? b2[col] : 0.0f);
-                if (row < kRB && col < nb) z[row * nbpad + col] = acc[v] + bias;
+                if (row < HD_RB && col < nb) z[row * nbpad + col] = acc[v] + bias;
             }
         }
     } else {
         const float* W2 = (const float*)w2;
-        for (int e = tid; e < kRB * nb; e += HD_THREADS) {
+        for (int e = tid; e < HD_RB * nb; e += HD_THREADS) {
             const int r = e / nb, j = e % nb;
             const float* wrow = W2 + (int64_t)j * m;
             const float* arow = a32 + r * m;
@@ -561,7 +569,7 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
     __syncthreads();
 
     // 3) softmax, expectation, EMA, integerisation: one wave per row
-    for (int r = wid; r < kRB; r += HD_THREADS / 64) {
+    for (int r = wid; r < HD_RB; r += HD_THREADS / 64) {
         const int gr = row0 + r;
         if (gr >= B) continue;
         float den = 1.0f, num = 0.0f;
@@ -998,20 +1006,20 @@ PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok) {
     return pl;
 }
 
-template <bool kBF16, int kS, bool kReg, int kRB>
+template <bool kBF16, int kS, bool kReg, int kPF>
 static hipError_t launch_head_rows(const star_predict_params& p, const PredictPlan& pl,
                                    const float* partials, const float* b1, const void* w2,
                                    const float* b2, const float* bins, float* ema_state,
                                    float* expected, int32_t* rem_len, float b4,
                                    hipStream_t stream) {
     if (pl.head_lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)head_kernel<kBF16, kS, kReg, kRB>,
+        hipError_t e = hipFuncSetAttribute((const void*)head_kernel<kBF16, kS, kReg, kPF>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)pl.head_lds);
         if (e != hipSuccess) return e;
     }
-    const dim3 grid((unsigned)ceil_div(p.n_req, kRB));
-    hipLaunchKernelGGL((head_kernel<kBF16, kS, kReg, kRB>), grid, dim3(HD_THREADS), pl.head_lds,
+    const dim3 grid((unsigned)ceil_div(p.n_req, HD_RB));
+    hipLaunchKernelGGL((head_kernel<kBF16, kS, kReg, kPF>), grid, dim3(HD_THREADS), pl.head_lds,
                        stream, partials, p.n_req, p.d_hidden, p.n_bins, b1, w2, b2, bins, p.act,
                        p.ema_alpha, p.ema_init, ema_state, expected, rem_len, p.len_max, b4);
     return hipGetLastError();
@@ -1061,8 +1069,14 @@ static hipError_t launch_head_s(const star_predict_params& p, const PredictPlan&
         }
     }
     if (pl.head_tiled || pl.head_rows != HD_RB) return hipErrorInvalidValue;
-    return launch_head_rows<kBF16, kS, kReg, HD_RB>(p, pl, partials, b1, w2, b2, bins, ema_state,
-                                                    expected, rem_len, b4, stream);
+    if constexpr (kBF16) {
+        if (ceil_div(p.n_req, HD_RB) > HD_LOWREG_GROUPS)
+            return launch_head_rows<kBF16, kS, kReg, HD_W2PF_LOW>(p, pl, partials, b1, w2, b2, bins,
+                                                                 ema_state, expected, rem_len, b4,
+                                                                 stream);
+    }
+    return launch_head_rows<kBF16, kS, kReg, HD_W2PF>(p, pl, partials, b1, w2, b2, bins, ema_state,
+                                                      expected, rem_len, b4, stream);
 }
 
 template <bool kBF16, bool kReg = false>

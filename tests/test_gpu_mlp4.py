@@ -69,7 +69,7 @@ def _rint_clamp(y, len_max):
     return np.where(q >= 1, np.minimum(q, len_max), 1).astype(np.int32)
 
 
-@pytest.mark.parametrize("B", [1024, 10, 1])
+@pytest.mark.parametrize("B", [1024, 10, 1, 2500])
 def test_paper_shape(B):
     x = synth.make_mlp4(B, dtype=synth.BF16, seed=B)
     print(f"mlp4 paper shape B={B}", flush=True)

@@ -73,6 +73,9 @@ def test_peaky_softmax_bf16():
     (synth.BF16, synth.ACT_GELU, 17, 64, 2048, 33),     # max hidden width
     (synth.F32, synth.ACT_RELU, 100, 132, 76, 20),
     (synth.F32, synth.ACT_GELU, 129, 1028, 260, 64),
+    # past 512 head workgroups: W2 loaded two fragments at a time
+    (synth.BF16, synth.ACT_GELU, 3000, 136, 72, 20),
+    (synth.BF16, synth.ACT_RELU, 2049, 264, 2048, 200),
 ])
 def test_ragged_shapes(dtype, act, B, d, m, nb):
     rng = np.random.default_rng(B * 7 + d + m + nb)
