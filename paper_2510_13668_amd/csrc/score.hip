@@ -94,7 +94,6 @@ __device__ inline uint32_t key_code(uint64_t d) {
     return ((uint32_t)(e - 4) << 4) | (uint32_t)((d >> (e - 5)) & 15);   // < 960
 }
 
-
 // q = x / d for d >= 1 with m = floor((2^32 - 1) / d) + 1 (m = 0 encodes
 // d = 1): the multiply-high estimate is exact or one too large (x + d < 2^32).
 __device__ inline uint32_t fast_div(uint32_t x, uint32_t d, uint32_t m) {
