@@ -107,6 +107,9 @@ ADVERSARIAL = [
     ("big_bucket", 64, 4, 1000, 3, 16, 100000, 5000, True, 0),
     # many scoring workgroups with all curves in LDS, top-k over every migration
     ("multi_block_direct", 2000, 4, 16, 64, 256, 5000, 1200, False, 0),
+    # separate scoring workgroups grown to 8 requests each (2049 of them,
+    # the last one ragged); the top-k narrows the best keys by code
+    ("grown_groups", 16390, 64, 16, 64, 256, 5000, 1200, False, 0),
 ]
 
 
