@@ -82,9 +82,10 @@ __global__ __launch_bounds__(PL_THREADS) void project_load_kernel(
             if (lr < 1) f |= STAR_DEV_BAD_REM;
             bad |= f;
             if (f || s != i) continue;
-            const int64_t lp = (int64_t)lr < H ? (int64_t)lr : H;
-            const int64_t ke = lp / b;
-            const int64_t mu = lp - ke * b;
+            // l' < 2^31, 1 <= b < 2^31: 32-bit division is exact and cheap
+            const uint32_t lp = (uint32_t)((int64_t)lr < H ? (int64_t)lr : H);
+            const int64_t ke = (int64_t)(lp / (uint32_t)b);
+            const int64_t mu = (int64_t)lp - ke * b;
             if (ke > k0) {
                 const int jj = (int)((ke < k1 ? ke : k1) - k0);          // 1..len
                 atomicAdd((unsigned long long*)&hA[jj], (unsigned long long)((int64_t)b * cr + alpha0));
