@@ -1153,10 +1153,118 @@ __global__ __launch_bounds__(TK_THREADS) void topk_direct_kernel(TopkArgs a) {
                                 a.topk_tgt, a.topk_score, a.top_k, sh, sv);
 }
 
+// Boundary keys of select_by_code, and its counters.
+constexpr int TK_BCAP = 2048;
+struct CodeLds {
+    int64_t bs_s[TK_BCAP];
+    uint32_t bs_i[TK_BCAP];
+    int na, nb;
+};
+
+// The k smallest of a register source's keys, by their codes relative to
+// base (no key is below it).  An LDS histogram of the codes gives c*, the
+// code that holds the k-th key: every key below c* wins, and the k - na
+// smallest of the nb keys of code c* are ranked directly when nb <=
+// TK_THREADS, radix-selected from LDS when nb <= TK_BCAP, and otherwise (a
+// crowded code) the whole source is radix-selected.  The winners go to
+// (ws_s, ws_i) unordered, with their score range; returns their count.
+template <int RJ>
+__device__ __forceinline__ int select_by_code(const RegKeys<RJ>& keys, int k, int64_t base, int ibits,
+                              SelShared<TK_THREADS>& sh, CodeLds& cl, int64_t* ws_s,
+                              uint32_t* ws_i, int64_t* smin, int64_t* smax_w) {
+    static_assert(RK_CODES == TK_THREADS && RK_CODES <= SEL_BINS, "one code per thread");
+    constexpr uint32_t kNone = 0xFFFFFFFFu;
+    const int tid = threadIdx.x;
+    sh.hist[tid] = 0;
+    if (tid == 0) {
+        cl.na = 0;
+        cl.nb = 0;
+    }
+    __syncthreads();
+    uint32_t code[RJ];
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+        code[j] = keys.s[j] != kInfS ? key_code((uint64_t)(keys.s[j] - base)) : kNone;
+        if (code[j] != kNone) atomicAdd(&sh.hist[code[j]], 1);
+    }
+    __syncthreads();
+    const int h = sh.hist[tid];
+    int total;
+    const int before = block_excl_i32<TK_THREADS>(h, sh, &total);
+    const int kk = k < total ? k : total;
+    if (tid == 0) sh.bcast[0] = RK_CODES;              // every key wins when total <= k
+    __syncthreads();
+    if (kk < total && before < kk && kk <= before + h) {
+        sh.bcast[0] = tid;
+        sh.bcast[1] = h;
+    }
+    __syncthreads();
+    const uint32_t cstar = (uint32_t)sh.bcast[0];
+    const int nbc = cstar < (uint32_t)RK_CODES ? sh.bcast[1] : 0;
+    __syncthreads();
+    if (nbc > TK_BCAP) return select_top<TK_THREADS>(keys, k, ibits, sh, ws_s, ws_i, smin, smax_w);
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+        if (code[j] < cstar) {                            // fewer than kk <= STAR_MAX_TOP_K
+            const int p = atomicAdd(&cl.na, 1);
+            ws_s[p] = keys.s[j];
+            ws_i[p] = keys.i[j];
+        } else if (code[j] == cstar) {                    // nbc <= TK_BCAP of them
+            const int p = atomicAdd(&cl.nb, 1);
+            cl.bs_s[p] = keys.s[j];
+            cl.bs_i[p] = keys.i[j];
+        }
+    }
+    __syncthreads();
+    const int na = cl.na, nb = cl.nb;
+    const int need = kk - na;                             // 0 <= need <= nb
+    int nw = na;
+    if (need > 0) {
+        if (nb <= TK_THREADS) {
+            if (tid < nb) {
+                const int64_t xs = cl.bs_s[tid];
+                const uint32_t xi = cl.bs_i[tid];
+                int rank = 0;
+                for (int q = 0; q < nb; ++q) rank += key_less(cl.bs_s[q], cl.bs_i[q], xs, xi) ? 1 : 0;
+                if (rank < need) {
+                    ws_s[na + rank] = xs;
+                    ws_i[na + rank] = xi;
+                }
+            }
+            nw += need;
+        } else {
+            RegKeys<TK_BCAP / TK_THREADS> bk;
+#pragma unroll
+            for (int j = 0; j < TK_BCAP / TK_THREADS; ++j) {
+                const int p = j * TK_THREADS + tid;
+                bk.s[j] = p < nb ? cl.bs_s[p] : kInfS;
+                bk.i[j] = p < nb ? cl.bs_i[p] : kInfI;
+            }
+            int cnt;
+            int64_t us, mn, mx;
+            uint32_t ui;
+            source_stats<TK_THREADS>(bk, sh, &cnt, &mn, &mx);
+            select_bound<TK_THREADS>(bk, need, ibits, cnt, mn, mx, sh, &us, &ui);
+            nw += block_gather<TK_THREADS>(bk, us, ui, sh, ws_s + na, ws_i + na,
+                                           STAR_MAX_TOP_K - na);
+        }
+    }
+    __syncthreads();
+    int64_t lo = kInfS, hi = -1;
+    for (int p = tid; p < nw; p += TK_THREADS) {
+        lo = ws_s[p] < lo ? ws_s[p] : lo;
+        hi = ws_s[p] > hi ? ws_s[p] : hi;
+    }
+    int cntw;
+    block_stats<TK_THREADS>(0, lo, hi, sh, &cntw, smin, smax_w);
+    return nw;
+}
+
 // The k smallest of the g gathered best keys, RJ per thread in registers.
 template <int RJ>
-__device__ int select_gathered(const TopkArgs& a, int g, int ib1, SelShared<TK_THREADS>& sh,
-                               int64_t* ws_s, uint32_t* ws_i, int64_t* smin, int64_t* smax_w) {
+__device__ __forceinline__ int select_gathered(const TopkArgs& a, int g, int ib1, SelShared<TK_THREADS>& sh,
+                               CodeLds& cl, int64_t base, int64_t* ws_s, uint32_t* ws_i,
+                               int64_t* smin, int64_t* smax_w) {
     RegKeys<RJ> keys;
 #pragma unroll
     for (int j = 0; j < RJ; ++j) {
@@ -1171,7 +1279,7 @@ __device__ int select_gathered(const TopkArgs& a, int g, int ib1, SelShared<TK_T
         keys.s[j] = e < g ? keys.s[j] : kInfS;
         keys.i[j] = e < g ? keys.i[j] : kInfI;
     }
-    return select_top<TK_THREADS>(keys, a.top_k, ib1, sh, ws_s, ws_i, smin, smax_w);
+    return select_by_code<RJ>(keys, a.top_k, base, ib1, sh, cl, ws_s, ws_i, smin, smax_w);
 }
 
 // Best key of request r (s = kInfS: none), loaded in batches of SEL_SBATCH
@@ -1202,8 +1310,8 @@ __device__ inline void visit_best(const TopkArgs& a, F&& f) {
 // no larger than the rest of code c*), and those are selected in registers.
 // More than TK_REG_BEST such keys (a crowded code c*) take the streamed
 // selection over all best keys instead.
-__device__ int select_best_by_code(const TopkArgs& a, int ib1, SelShared<TK_THREADS>& sh,
-                                   int64_t* ws_s, uint32_t* ws_i, int64_t* smin,
+__device__ __forceinline__ int select_best_by_code(const TopkArgs& a, int ib1, SelShared<TK_THREADS>& sh,
+                                   CodeLds& cl, int64_t* ws_s, uint32_t* ws_i, int64_t* smin,
                                    int64_t* smax_w, int* gcount) {
     static_assert(RK_CODES == TK_THREADS && RK_CODES <= SEL_BINS, "one code per thread");
     const int tid = threadIdx.x;
@@ -1242,7 +1350,7 @@ __device__ int select_best_by_code(const TopkArgs& a, int ib1, SelShared<TK_THRE
     });
     __syncthreads();                           // the gathered keys are visible to the workgroup
     const int g = *gcount < TK_REG_BEST ? *gcount : TK_REG_BEST;
-    return select_gathered<TK_RJ1>(a, g, ib1, sh, ws_s, ws_i, smin, smax_w);
+    return select_gathered<TK_RJ1>(a, g, ib1, sh, cl, base, ws_s, ws_i, smin, smax_w);
 }
 
 // How the pruned top-k finds the k requests with the smallest best keys: all
@@ -1260,15 +1368,17 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
     __shared__ int32_t rk[STAR_MAX_TOP_K];
     __shared__ int32_t rk_inst[STAR_MAX_TOP_K];
     __shared__ int gcount;
+    __shared__ CodeLds cl;
     int nr;
     int64_t smin, smax_w;
+    const int64_t base = *a.bbase;
     const int ib1 = bit_length((uint64_t)(a.N - 1));
     if constexpr (kStage1 == kStage1Reg) {
         RegKeys<TK_RJ1> keys;
         load_best(keys, a);
-        nr = select_top<TK_THREADS>(keys, a.top_k, ib1, sh, ws_s, ws_i, &smin, &smax_w);
+        nr = select_by_code<TK_RJ1>(keys, a.top_k, base, ib1, sh, cl, ws_s, ws_i, &smin, &smax_w);
     } else {
-        nr = select_best_by_code(a, ib1, sh, ws_s, ws_i, &smin, &smax_w, &gcount);
+        nr = select_best_by_code(a, ib1, sh, cl, ws_s, ws_i, &smin, &smax_w, &gcount);
     }
     for (int q = threadIdx.x; q < nr; q += TK_THREADS) {
         const int r = (int)ws_i[q];
@@ -1282,7 +1392,7 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
     if constexpr (kRJ2 > 0) {
         RegKeys<kRJ2> keys;
         load_pruned(keys, a, rk, rk_inst, M);
-        nw = select_top<TK_THREADS>(keys, a.top_k, ib2, sh, ws_s, ws_i, &smin, &smax_w);
+        nw = select_by_code<kRJ2>(keys, a.top_k, base, ib2, sh, cl, ws_s, ws_i, &smin, &smax_w);
     } else {
         PrunedKeys pk{&a, rk, rk_inst, M};
         nw = select_top<TK_THREADS>(pk, a.top_k, ib2, sh, ws_s, ws_i, &smin, &smax_w);
@@ -1989,10 +2099,13 @@ ScorePlan plan_score(const star_score_params& p, bool project) {
     off = align_up(off + (size_t)N * 8, 256);
     pl.btarget_off = off;
     off = align_up(off + (size_t)N * 4, 256);
-    pl.topk_hist = p.top_k > 0 && n > 1 && !pl.topk_direct && !pl.topk_reg1;
-    if (pl.topk_hist) {
+    pl.topk_pruned = p.top_k > 0 && n > 1 && !pl.topk_direct;
+    pl.topk_hist = pl.topk_pruned && !pl.topk_reg1;
+    if (pl.topk_pruned) {
         pl.base_off = off;
         off = align_up(off + 8, 256);
+    }
+    if (pl.topk_hist) {
         pl.gs_off = off;
         off = align_up(off + (size_t)TK_REG_BEST * 8, 256);
         pl.gi_off = off;
@@ -2114,7 +2227,7 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     a.rpb = pl.rpb; a.cand = pl.cand;
     a.magic_K = div_magic((uint32_t)lp.n_buckets);
     a.magic_n = div_magic((uint32_t)lp.n_inst);
-    if (pl.topk_hist) a.bbase = (int64_t*)(ws + pl.base_off);
+    if (pl.topk_pruned) a.bbase = (int64_t*)(ws + pl.base_off);
     hipError_t e;
     if (pl.fused) {
         e = launch_score_kernel<true>(pl, a, stream);
@@ -2149,8 +2262,8 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
             hipLaunchKernelGGL(topk_direct_kernel<TK_RJ>, dim3(1), dim3(TK_THREADS), 0, stream, t);
         return hipGetLastError();
     }
-    if (pl.topk_reg1) return launch_topk_pruned<kStage1Reg>(t, pl.topk_rj2, stream);
     t.bbase = a.bbase;
+    if (pl.topk_reg1) return launch_topk_pruned<kStage1Reg>(t, pl.topk_rj2, stream);
     t.gs = (int64_t*)(ws + pl.gs_off);
     t.gi = (uint32_t*)(ws + pl.gi_off);
     return launch_topk_pruned<kStage1Code>(t, pl.topk_rj2, stream);

@@ -66,6 +66,7 @@ struct ScorePlan {
     bool topk_reg1 = false;    // pruned top-k: best keys fit registers
     int topk_rj2 = 0;          // pruned top-k: the k requests' migrations per thread in
                                // registers (8 or 16), 0: streamed
+    bool topk_pruned = false;  // pruned top-k: the scoring kernel writes the key-code base
     bool topk_hist = false;    // pruned top-k, best keys beyond registers: the top-k counts
                                // their codes and gathers those up to the k-th
     size_t gs_off = 0, gi_off = 0;  // topk_hist: gathered best keys (base_off: their code base)
