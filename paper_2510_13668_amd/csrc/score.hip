@@ -100,6 +100,7 @@ __device__ inline uint32_t key_code(uint64_t d) {
     if (e <= 4) return (uint32_t)d;
     return ((uint32_t)(e - 4) << 4) | (uint32_t)((d >> (e - 5)) & 15);   // < 960
 }
+constexpr uint16_t kNoCode = 0xFFFF;                     // a request without a migration
 
 // q = x / d for d >= 1 with m = floor((2^32 - 1) / d) + 1 (m = 0 encodes
 // d = 1): the multiply-high estimate is exact or one too large (x + d < 2^32).
@@ -496,6 +497,7 @@ struct ScoreArgs {
     int32_t* err_word;
     int64_t* load_out;            // curves built by the scoring kernel itself (group 0 writes)
     int64_t* bbase;               // code base for the top-k's best keys (group 0 writes), or null
+    uint16_t* bcode;              // [N] code of each request's best key (kNoCode: none), or null
     int N, n, b, K, rpb, cand;
     uint32_t magic_K, magic_n;
 };
@@ -613,8 +615,8 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
 
     // the code base of the top-k's best keys: the smallest target peak (no
     // migration scores below it), one read per thread and a block minimum
+    int64_t base = INT64_MAX;
     if (a.bbase) {
-        int64_t base = INT64_MAX;
         __shared__ int64_t wmin[SC_THREADS / 64];
         for (int t = tid; t < n; t += SC_THREADS) {
             const int64_t v = gSM[(int64_t)t * K1];
@@ -641,6 +643,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
         const bool none = bi == kInfI;
         if (a.best_target) a.best_target[r] = none ? -1 : (int32_t)(bi - (uint32_t)((int64_t)r * n));
         if (a.best_score) a.best_score[r] = none ? -1 : bs;
+        if (a.bcode) a.bcode[r] = none ? kNoCode : (uint16_t)key_code((uint64_t)(bs - base));
     }
 }
 
@@ -751,6 +754,7 @@ struct TopkArgs {
     int32_t* topk_tgt;
     int64_t* topk_score;
     const int64_t* bbase;         // code base of the best keys (the smallest target peak)
+    const uint16_t* bcode;        // [N] code of each best key (kNoCode: none), code stage only
     int64_t* gs;                  // [TK_REG_BEST] best keys gathered at or below the k-th code
     uint32_t* gi;
     int N, n, top_k;
@@ -1282,34 +1286,32 @@ __device__ __forceinline__ int select_gathered(const TopkArgs& a, int g, int ib1
     return select_by_code<RJ>(keys, a.top_k, base, ib1, sh, cl, ws_s, ws_i, smin, smax_w);
 }
 
-// Best key of request r (s = kInfS: none), loaded in batches of SEL_SBATCH
-// per thread; f(r, s) for each.
+// Best-key code of request r (kNoCode: none), loaded in batches of
+// SEL_SBATCH per thread; f(r, code) for each.
 template <class F>
-__device__ inline void visit_best(const TopkArgs& a, F&& f) {
+__device__ inline void visit_codes(const TopkArgs& a, F&& f) {
     for (int r0 = 0; r0 < a.N; r0 += TK_THREADS * SEL_SBATCH) {
-        int64_t bs[SEL_SBATCH];
-        int32_t bt[SEL_SBATCH];
+        uint16_t cv[SEL_SBATCH];
 #pragma unroll
         for (int u = 0; u < SEL_SBATCH; ++u) {
             const int r = r0 + u * TK_THREADS + (int)threadIdx.x;
-            const int rc = r < a.N ? r : a.N - 1;
-            bs[u] = a.best_score[rc];
-            bt[u] = a.best_target[rc];
+            cv[u] = a.bcode[r < a.N ? r : a.N - 1];
         }
 #pragma unroll
         for (int u = 0; u < SEL_SBATCH; ++u) {
             const int r = r0 + u * TK_THREADS + (int)threadIdx.x;
-            f(r, r < a.N && bt[u] >= 0 ? bs[u] : kInfS);
+            f(r, r < a.N ? cv[u] : kNoCode);
         }
     }
 }
 
-// The k smallest best keys by their codes: one pass counts the codes in an
-// LDS histogram and finds the code c* that holds the k-th key, a second
-// gathers every best key of code <= c* (all of the k smallest, and only keys
-// no larger than the rest of code c*), and those are selected in registers.
-// More than TK_REG_BEST such keys (a crowded code c*) take the streamed
-// selection over all best keys instead.
+// The k smallest best keys by their codes, which the scoring kernel wrote
+// (2 bytes per request): one pass counts them in an LDS histogram and finds
+// the code c* that holds the k-th key, a second gathers every best key of
+// code <= c* (all of the k smallest, and only keys no larger than the rest
+// of code c*), and those are selected in registers.  More than TK_REG_BEST
+// such keys (a crowded code c*) take the streamed selection over all best
+// keys instead.
 __device__ __forceinline__ int select_best_by_code(const TopkArgs& a, int ib1, SelShared<TK_THREADS>& sh,
                                    CodeLds& cl, int64_t* ws_s, uint32_t* ws_i, int64_t* smin,
                                    int64_t* smax_w, int* gcount) {
@@ -1318,8 +1320,8 @@ __device__ __forceinline__ int select_best_by_code(const TopkArgs& a, int ib1, S
     const int64_t base = *a.bbase;
     sh.hist[tid] = 0;
     __syncthreads();
-    visit_best(a, [&](int, int64_t s) {
-        if (s != kInfS) atomicAdd(&sh.hist[key_code((uint64_t)(s - base))], 1);
+    visit_codes(a, [&](int, uint16_t c) {
+        if (c != kNoCode) atomicAdd(&sh.hist[c], 1);
     });
     __syncthreads();
     const int h = sh.hist[tid];
@@ -1339,11 +1341,11 @@ __device__ __forceinline__ int select_best_by_code(const TopkArgs& a, int ib1, S
         BestKeys bk{a.best_score, a.best_target, a.N};
         return select_top<TK_THREADS>(bk, a.top_k, ib1, sh, ws_s, ws_i, smin, smax_w);
     }
-    visit_best(a, [&](int r, int64_t s) {
-        if (s != kInfS && key_code((uint64_t)(s - base)) <= cstar) {
+    visit_codes(a, [&](int r, uint16_t c) {
+        if (c != kNoCode && c <= cstar) {
             const int at = atomicAdd(gcount, 1);
             if (at < TK_REG_BEST) {
-                a.gs[at] = s;
+                a.gs[at] = a.best_score[r];
                 a.gi[at] = (uint32_t)r;
             }
         }
@@ -2106,6 +2108,8 @@ ScorePlan plan_score(const star_score_params& p, bool project) {
         off = align_up(off + 8, 256);
     }
     if (pl.topk_hist) {
+        pl.bcode_off = off;
+        off = align_up(off + (size_t)N * 2, 256);
         pl.gs_off = off;
         off = align_up(off + (size_t)TK_REG_BEST * 8, 256);
         pl.gi_off = off;
@@ -2228,6 +2232,7 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     a.magic_K = div_magic((uint32_t)lp.n_buckets);
     a.magic_n = div_magic((uint32_t)lp.n_inst);
     if (pl.topk_pruned) a.bbase = (int64_t*)(ws + pl.base_off);
+    if (pl.topk_hist) a.bcode = (uint16_t*)(ws + pl.bcode_off);
     hipError_t e;
     if (pl.fused) {
         e = launch_score_kernel<true>(pl, a, stream);
@@ -2263,6 +2268,7 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
         return hipGetLastError();
     }
     t.bbase = a.bbase;
+    t.bcode = a.bcode;
     if (pl.topk_reg1) return launch_topk_pruned<kStage1Reg>(t, pl.topk_rj2, stream);
     t.gs = (int64_t*)(ws + pl.gs_off);
     t.gi = (uint32_t*)(ws + pl.gi_off);

@@ -69,7 +69,7 @@ struct ScorePlan {
     bool topk_pruned = false;  // pruned top-k: the scoring kernel writes the key-code base
     bool topk_hist = false;    // pruned top-k, best keys beyond registers: the top-k counts
                                // their codes and gathers those up to the k-th
-    size_t gs_off = 0, gi_off = 0;  // topk_hist: gathered best keys (base_off: their code base)
+    size_t bcode_off = 0, gs_off = 0, gi_off = 0;  // topk_hist: best-key codes, gathered keys
     size_t pm_off = 0, sm_off = 0, scores_off = 0, bscore_off = 0, btarget_off = 0, total = 0;
     size_t lds = 0;       // dynamic LDS of the scoring kernel (or of the small path's one)
 };
