@@ -393,3 +393,49 @@ def test_pipelined_graph_rounds_match_eager():
             assert_round_equal(slots[j % 2].result(), want[j])
         np.testing.assert_array_equal(pr.ema.cpu().numpy(), want_ema)
         _ = torch.ones(1000, device="cuda").sum().item()    # unrelated eager work between replays
+
+
+def _random_round_case(rng, kind):
+    """Sizes aimed at one ranking regime each, and requests that are either
+    random or drawn from a few distinct (c, l) pairs (crowded key codes and
+    many ties)."""
+    if kind == 0:     # pruned top-k, best keys in registers
+        N, n = int(rng.integers(2100, 8192)), int(rng.integers(3, 20))
+    elif kind == 1:   # best keys narrowed by code, many instances
+        N, n = int(rng.integers(8193, 30000)), int(rng.integers(16, 70))
+    elif kind == 2:   # best keys narrowed by code, few instances
+        N, n = int(rng.integers(8193, 40000)), int(rng.integers(4, 16))
+    elif kind == 3:   # direct top-k, 16 keys per thread
+        n = int(rng.integers(2, 8))
+        N = int(rng.integers(8192 // n + 1, 16384 // n))
+    elif kind == 4:   # the k requests' migrations streamed (k (n - 1) > 16384)
+        N, n = int(rng.integers(9000, 20000)), int(rng.integers(70, 120))
+    else:             # small rounds
+        N, n = int(rng.integers(1, 3000)), int(rng.integers(1, 40))
+    b = int(rng.choice([1, 4, 16, 64]))
+    K = int(rng.integers(1, 300))
+    top_k = int(rng.choice([1, 17, 256, 1000, 1024]))
+    H = b * K
+    if rng.random() < 0.5:
+        d = int(rng.integers(1, 6))
+        cv = rng.integers(1, 5000, size=d)
+        lv = rng.integers(1, H + 10, size=d)
+        pick = rng.integers(0, d, size=N)
+        cur, rem = cv[pick].astype(np.int32), lv[pick].astype(np.int32)
+        live = max(1, n - int(rng.integers(0, 2)))
+        inst = rng.integers(0, live, size=N).astype(np.int32)
+    else:
+        cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=int(rng.integers(1, 20000)),
+                                               len_hi=int(rng.integers(1, 3 * H + 2)))
+    return cur, rem, inst, n, b, K, top_k
+
+
+def test_random_rounds_every_ranking_regime():
+    """30 seeded random rounds over the ranking regimes (register, code-
+    narrowed and streamed stages, direct top-k with 8 or 16 keys per thread,
+    crowded boundary codes), each as two calls and as one; bit-exact."""
+    rng = np.random.default_rng(2510)
+    for c in range(30):
+        cur, rem, inst, n, b, K, top_k = _random_round_case(rng, c % 6)
+        for fused in (False, True):
+            _check(cur, rem, inst, n, b, K, top_k, fused=fused)
