@@ -241,3 +241,37 @@ def test_deterministic_and_resumable():
         pr2.run(hid[s])
     np.testing.assert_array_equal(pr2.ema.cpu().numpy(), outs[0][1])
     np.testing.assert_array_equal(pr2.rem.cpu().numpy(), outs[0][2])
+
+
+def test_random_shapes_every_head_variant():
+    """20 seeded random shapes across the head variants: the 4-row head with
+    deep and shallow W2 prefetch (batches on both sides of 2048 rows), the
+    K-chunked head (8192 rows and more), fp32 and bf16, both activations,
+    with and without biases, any width and bin count; sampled rows."""
+    rng = np.random.default_rng(13668)
+    for c in range(20):
+        kind = c % 4
+        bf = kind != 3 or rng.random() < 0.5
+        dtype = synth.BF16 if bf else synth.F32
+        vec = 8 if bf else 4
+        B = (int(rng.integers(1, 2048)) if kind == 0 else
+             int(rng.integers(2049, 8192)) if kind == 1 else int(rng.integers(8192, 20000)))
+        d = vec * int(rng.integers(1, (4096 if B < 8192 else 1024) // vec))
+        m = vec * int(rng.integers(1, 2048 // vec))
+        nb = int(rng.integers(1, 257))
+        act = synth.ACT_GELU if rng.random() < 0.6 else synth.ACT_RELU
+        bias = rng.random() < 0.5
+        h = rng.standard_normal((B, d)).astype(np.float32)
+        w1 = (rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32)
+        w2 = (rng.standard_normal((nb, m)) * 4 / np.sqrt(m)).astype(np.float32)
+        b1 = (rng.standard_normal(m) * 0.1).astype(np.float32) if bias else None
+        b2 = (rng.standard_normal(nb) * 0.1).astype(np.float32) if bias else None
+        if bf:
+            h, w1, w2 = (synth.f32_to_bf16_bits(h), synth.f32_to_bf16_bits(w1),
+                         synth.f32_to_bf16_bits(w2))
+        sample = np.unique(np.concatenate([np.arange(min(B, 70)), np.arange(max(0, B - 70), B),
+                                           rng.choice(B, min(B, 60), replace=False)]))
+        print(f"random head {c}: B={B} d={d} m={m} nb={nb} bf16={bf} act={act} bias={bias}",
+              flush=True)
+        _run_case(h, w1, w2, synth.bin_values(nb, 1.0, 32768.0), dtype=dtype, act=act, b1=b1,
+                  b2=b2, len_max=32768, sample=sample)
