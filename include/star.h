@@ -80,7 +80,9 @@ typedef enum { STAR_ACT_RELU = 0, STAR_ACT_GELU_ERF = 1 } star_act;
  *
  * Precision: bf16 or fp32 operands (dtype applies to hidden, w1 and w2);
  * fp32 accumulation; a1 enters the second product as a bf16 hi/lo pair
- * (bf16 path) or fp32; fp32 softmax and EMA.
+ * (bf16 path) or fp32; fp32 softmax and EMA.  STAR_ACT_GELU_ERF is
+ * x Phi(x) with Phi from the Abramowitz & Stegun 7.1.26 approximation of
+ * erfc (within 1.5e-7 max(1, |x|) of the exact GELU in fp32).
  * ---------------------------------------------------------------------- */
 typedef struct {
     int32_t n_req;      /* B >= 0 rows of hidden */
