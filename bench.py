@@ -832,12 +832,14 @@ def main():
 
     # Pipelined rounds: round i's prediction needs only round i-1's EMA state,
     # so it runs on `stream` while round i-1 is projected and scored on
-    # `sched`.  Per-round outputs are double-buffered; an event keeps a
-    # buffer from being overwritten before its scheduling has finished.
-    # (Measured: giving each round of a captured chunk its own buffers, which
-    # drops these events, makes the replayed graph slower.)
+    # `sched`.  Per-round outputs rotate through NSLOT buffers; an event keeps
+    # a buffer from being overwritten before its scheduling has finished, so
+    # round i's prediction waits for round i - NSLOT's scheduling.
+    # (Measured, graph-replayed: 29.7 us per round with two buffers, 28.1
+    # with three, 28.2 with four; a buffer per round of a captured chunk,
+    # which drops these events, was slower still.)
     sched = torch.cuda.Stream()
-    NSLOT = 2
+    NSLOT = 3
     slot_buf = []
     for _ in range(NSLOT):
         slot_buf.append(dict(

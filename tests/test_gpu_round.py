@@ -323,14 +323,16 @@ def test_graph_replay_matches_eager():
 def test_pipelined_graph_rounds_match_eager():
     """Rounds pipelined on two streams: round i is predicted on one stream
     while round i-1 is projected and scored on a second.  The per-round
-    outputs alternate between two buffers, and events order the rounds.
-    The whole chunk is captured as one HIP graph, as the benchmark runs it.
-    Every replay (with eager work and synchronisations between replays)
-    must leave the last two rounds' outputs and the EMA state equal to six
-    eager rounds run one after another.  The pipelined rounds use the fused
-    projection-and-scoring call, the eager ones the two separate calls."""
+    outputs rotate through three buffers, as in the benchmark, and events
+    order the rounds.  The whole chunk is captured as one HIP graph, as the
+    benchmark runs it.  Every replay (with eager work and synchronisations
+    between replays) must leave the last three rounds' outputs and the EMA
+    state equal to eight eager rounds run one after another.  The pipelined
+    rounds use the fused projection-and-scoring call, the eager ones the two
+    separate calls."""
     wl = synth.WORKLOADS["continuous"]
-    R = 6
+    R = 8
+    NS = 3
     x = synth.make_inputs(wl, steps=R + 1)
     hid = to_dev(x.hidden, True)
     N = wl.n_req
@@ -352,18 +354,18 @@ def test_pipelined_graph_rounds_match_eager():
 
     P, S2 = torch.cuda.Stream(), torch.cuda.Stream()
     slots = [Rescheduler(N, wl.n_inst, wl.bucket, wl.n_buckets, wl.top_k, fused=True)
-             for _ in range(2)]
-    rems = [torch.empty(N, dtype=torch.int32, device="cuda") for _ in range(2)]
-    exps = [torch.empty(N, dtype=torch.float32, device="cuda") for _ in range(2)]
-    ev_pred = [torch.cuda.Event() for _ in range(2)]
-    ev_done = [torch.cuda.Event() for _ in range(2)]
+             for _ in range(NS)]
+    rems = [torch.empty(N, dtype=torch.int32, device="cuda") for _ in range(NS)]
+    exps = [torch.empty(N, dtype=torch.float32, device="cuda") for _ in range(NS)]
+    ev_pred = [torch.cuda.Event() for _ in range(NS)]
+    ev_done = [torch.cuda.Event() for _ in range(NS)]
     pp = pr.params(False)
 
     def chunk():
         S2.wait_stream(P)
         for j in range(R):
-            k = j % 2
-            if j >= 2:
+            k = j % NS
+            if j >= NS:
                 P.wait_event(ev_done[k])
             star.predict(pp, hid[j + 1], pr.w1, pr.b1, pr.w2, pr.b2, pr.bins, pr.ema, exps[k],
                          rems[k], pr.ws, P)
@@ -389,8 +391,8 @@ def test_pipelined_graph_rounds_match_eager():
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        for j in (R - 2, R - 1):
-            assert_round_equal(slots[j % 2].result(), want[j])
+        for j in (R - 3, R - 2, R - 1):
+            assert_round_equal(slots[j % NS].result(), want[j])
         np.testing.assert_array_equal(pr.ema.cpu().numpy(), want_ema)
         _ = torch.ones(1000, device="cuda").sum().item()    # unrelated eager work between replays
 
