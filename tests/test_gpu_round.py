@@ -441,3 +441,27 @@ def test_random_rounds_every_ranking_regime():
         cur, rem, inst, n, b, K, top_k = _random_round_case(rng, c % 6)
         for fused in (False, True):
             _check(cur, rem, inst, n, b, K, top_k, fused=fused)
+
+
+@pytest.mark.parametrize("N", [3, 4099, 8195])
+def test_projection_of_misaligned_request_arrays(N):
+    """Request arrays that start 4 bytes past a 16-byte boundary take the
+    projection's int32 reads, aligned ones of 8192 requests and more its
+    16-byte reads (with a ragged tail): all equal the oracle."""
+    rng = np.random.default_rng(N)
+    n, b, K = 7, 16, 90
+    cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=3000, len_hi=b * K + 40)
+    ref = oracle.round_(cur, rem, inst, n_inst=n, bucket=b, n_buckets=K, top_k=0)
+    lp = star.load_params(N, n, b, K)
+    ws = star.Workspace(star.project_load_workspace_size(lp))
+    for off in (0, 1):
+        def place(a):
+            t = torch.zeros(N + 4, dtype=torch.int32, device="cuda")
+            t[off:off + N] = torch.from_numpy(a).cuda()
+            return t[off:off + N]
+        c, r, s = place(cur), place(rem), place(inst)
+        assert (c.data_ptr() % 16 == 0) == (off == 0)
+        load = torch.full((n, K), -1, dtype=torch.int64, device="cuda")
+        star.project_load(lp, c, r, s, load, ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(load.cpu().numpy(), ref["load"], err_msg=f"offset {off}")
