@@ -177,11 +177,11 @@ __device__ inline ReqTerms request_terms(int s, int c, int l, int n, int b, int6
     if (s < 0 || s >= n) q.bad |= STAR_DEV_BAD_INST;
     if (c < 1) q.bad |= STAR_DEV_BAD_CUR;
     if (l < 1) q.bad |= STAR_DEV_BAD_REM;
-    // l' = min(l, H) < 2^31 and 1 <= b < 2^31: a 32-bit division gives
-    // k_e and mu exactly, at a fraction of a 64-bit one's instructions
-    const uint32_t lp = (uint32_t)((int64_t)l < H ? (int64_t)l : H);
-    const int64_t ke = (int64_t)(lp / (uint32_t)b);
-    const int64_t mu = (int64_t)lp - ke * b;
+    // (a 32-bit division here, exact since l' < 2^31, cost the variance
+    // scoring kernels an occupancy step and gained nothing measurable)
+    const int64_t lp = (int64_t)l < H ? (int64_t)l : H;
+    const int64_t ke = lp / b;
+    const int64_t mu = lp - ke * b;
     const bool ok = q.bad == 0;
     q.s = ok ? s : -1;
     q.ke = ok ? (int)ke : 0;
