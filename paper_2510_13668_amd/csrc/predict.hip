@@ -33,6 +33,7 @@ constexpr int G1_ROW = G1_KBYTES + 16;         // padded LDS row (bytes)
 // deeper register staging only lengthens each workgroup there).
 constexpr int G1_STAGES_BIG = 3;
 constexpr int G1_STAGES_SMALL = 2;
+constexpr int G1_STAGES_MID = 2;
 constexpr int G1_STAGES_WIDE = 2;
 constexpr int G1_WIDE_MIN_TILES = 1024;   // 128 x 128 tiles from which G1Wide replaces G1Big
 constexpr int G1_STAGES_HUGE = 1;
@@ -69,6 +70,14 @@ struct G1Shape {
 };
 using G1Big = G1Shape<128, 128, 4, 2>;     // 8 waves, 32 x 64 slabs
 using G1Small = G1Shape<64, 64, 2, 2>;     // 4 waves, 32 x 32 slabs
+// 8 waves, 32 x 32 slabs of a 128 x 64 tile, for products of at most 128
+// rows: twice G1Big's tiles along N, so half its K-splits fill the chip, and
+// the partials written and read back halve.  The regression head's first
+// layer (2048 x 3584) went from 22.7 to 20.4 us per call at one row and
+// from 26.4 to 23.3 us at ten.  With several row tiles the cost model would
+// also pick it, but there it measured slower (the regression head's first
+// layer at 1024 rows: 29.3 against 33.9 us), so it is offered only here.
+using G1Mid = G1Shape<128, 64, 4, 2>;
 // 4 waves, 64 x 64 slabs: twice the matrix-core work per LDS byte of G1Big,
 // at half its waves per workgroup; it wins once every CU has several
 // workgroups queued (measured: 580 against 786 us for 32768 x 1024 x 8192)
@@ -339,6 +348,9 @@ static hipError_t launch_gemm(const GemmPlan& g, bool bf16, const void* A, const
             break;
         case GemmPlan::kHuge:
             launch_gemm_shape<G1_STAGES_HUGE, G1Huge>(g, bf16, A, W, P, M, N, K, stream);
+            break;
+        case GemmPlan::kMid:
+            launch_gemm_shape<G1_STAGES_MID, G1Mid>(g, bf16, A, W, P, M, N, K, stream);
             break;
         default:
             launch_gemm_shape<G1_STAGES_SMALL, G1Small>(g, bf16, A, W, P, M, N, K, stream);
@@ -932,26 +944,31 @@ __global__ __launch_bounds__(ACT_THREADS) void act_kernel(const float* __restric
 // ---------------------------------------------------------------------------
 // Tiles and split-K factor of one product [M, K] x [N, K]^T.  For each tile
 // shape the split is a power of two in [1, 16] that brings the workgroups
-// near one per CU (128 x 128) or two per CU (64 x 64).  The shape is chosen
-// by a cost model of its two data
-// streams: operand rows read into the CUs (every A row once per column of
-// tiles, every W row once per row of tiles) at the L2's aggregate ~17 TB/s,
+// near one per CU (128 x 128, 128 x 64) or two per CU (64 x 64).  The shape
+// is chosen by a cost model of its two data streams: operand rows read into
+// the CUs (every A row once per column of tiles, every W row once per row of
+// tiles) at the L2's aggregate ~17 TB/s,
 // and the fp32 split-K partials written, flushed out of L2 at the end of
 // the kernel and read back at ~2.4 TB/s (both rates measured on MI355X).
 GemmPlan plan_gemm(int M, int N, int K, int elem) {
     GemmPlan best;
     double best_cost = 0.0;
     const int bk = G1_KBYTES / elem;
-    for (int big = 1; big >= 0; --big) {
+    struct Cand { int shape, bm, bn, slots; };
+    const Cand cands[3] = {{GemmPlan::kBig, G1Big::BM, G1Big::BN, 256},
+                           {GemmPlan::kSmall, G1Small::BM, G1Small::BN, 512},
+                           {GemmPlan::kMid, G1Mid::BM, G1Mid::BN, 256}};
+    for (int ci = 0; ci < 3; ++ci) {
+        if (cands[ci].shape == GemmPlan::kMid && M > G1Mid::BM) continue;
         GemmPlan g;
-        g.shape = big ? GemmPlan::kBig : GemmPlan::kSmall;
-        const int bm = big ? G1Big::BM : G1Small::BM, bn = big ? G1Big::BN : G1Small::BN;
+        g.shape = cands[ci].shape;
+        const int bm = cands[ci].bm, bn = cands[ci].bn;
         g.tiles_m = (int)ceil_div(M, bm);
         g.tiles_n = (int)ceil_div(N, bn);
         g.ktiles = (int)ceil_div(K, bk);
         const int tiles = g.tiles_m * g.tiles_n;
         int s = 1;
-        const int slots = big ? 256 : 512;
+        const int slots = cands[ci].slots;
         if (tiles > 0 && tiles < 3 * slots / 4) {
             int want = slots / tiles;
             if (want > 16) want = 16;
@@ -962,7 +979,7 @@ GemmPlan plan_gemm(int M, int N, int K, int elem) {
         const double operands = ((double)g.tiles_n * M + (double)g.tiles_m * N) * K * elem;
         const double partials = (double)s * M * N * 4.0;
         const double cost = operands / 17e12 + 2.0 * partials / 2.4e12;
-        if (big || cost < best_cost) {
+        if (ci == 0 || cost < best_cost) {
             best = g;
             best_cost = cost;
         }

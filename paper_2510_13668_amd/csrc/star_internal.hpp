@@ -11,9 +11,9 @@ namespace star {
 
 struct GemmPlan {
     int tiles_m = 0, tiles_n = 0, ktiles = 0, splits = 1;
-    enum { kSmall = 0, kBig = 1, kWide = 2, kHuge = 3 };
+    enum { kSmall = 0, kBig = 1, kWide = 2, kHuge = 3, kMid = 4 };
     int shape = kBig;     // 64 x 64 tiles on 4 waves; 128 x 128 on 8; 128 x 128 on 4;
-                          // 256 x 256 on 8
+                          // 256 x 256 on 8; 128 x 64 on 8
 };
 GemmPlan plan_gemm(int M, int N, int K, int elem);
 

@@ -76,6 +76,9 @@ def test_peaky_softmax_bf16():
     # past 512 head workgroups: W2 loaded two fragments at a time
     (synth.BF16, synth.ACT_GELU, 3000, 136, 72, 20),
     (synth.BF16, synth.ACT_RELU, 2049, 264, 2048, 200),
+    # one row tile: 128 x 64 GEMM tiles, ragged rows and columns
+    (synth.BF16, synth.ACT_GELU, 40, 3584, 1096, 20),
+    (synth.F32, synth.ACT_GELU, 60, 1028, 1100, 20),
 ])
 def test_ragged_shapes(dtype, act, B, d, m, nb):
     rng = np.random.default_rng(B * 7 + d + m + nb)
