@@ -114,6 +114,34 @@ def test_wide_head_rows_sampled(B, d, m, nb):
               len_max=32768, sample=sample)
 
 
+@pytest.mark.gpu
+def test_random_single_row_tile_products():
+    """12 seeded random products of at most 128 rows (one row tile of the
+    first-layer GEMM), where the plan may take 128 x 64 tiles with fewer
+    K-splits (six of these twelve do): ragged rows, width and hidden size,
+    fp32 and bf16, both activations; every row checked."""
+    rng = np.random.default_rng(2510)
+    for c in range(12):
+        bf = c % 3 != 2
+        dtype = synth.BF16 if bf else synth.F32
+        vec = 8 if bf else 4
+        B = int(rng.integers(1, 129))
+        d = vec * int(rng.integers(64 // vec, 4096 // vec))
+        m = vec * int(rng.integers(512 // vec, 2048 // vec))
+        nb = int(rng.integers(1, 257))
+        act = synth.ACT_GELU if c % 2 else synth.ACT_RELU
+        h = rng.standard_normal((B, d)).astype(np.float32)
+        w1 = (rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32)
+        w2 = (rng.standard_normal((nb, m)) * 4 / np.sqrt(m)).astype(np.float32)
+        b1 = (rng.standard_normal(m) * 0.1).astype(np.float32)
+        if bf:
+            h, w1, w2 = (synth.f32_to_bf16_bits(h), synth.f32_to_bf16_bits(w1),
+                         synth.f32_to_bf16_bits(w2))
+        print(f"single row tile {c}: B={B} d={d} m={m} nb={nb} bf16={bf} act={act}", flush=True)
+        _run_case(h, w1, w2, synth.bin_values(nb, 1.0, 32768.0), dtype=dtype, act=act, b1=b1,
+                  len_max=32768)
+
+
 def _splits(B, d, m, nb):
     """Split-K planes the plan takes, from the workspace size (host only)."""
     from paper_2510_13668_amd import star
