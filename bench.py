@@ -87,8 +87,9 @@ def _parse():
 COPY_BYTES = 256 << 20
 COPY_REPS = 8
 TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
-                            "gemm1_continuous_traffic.json")
-GEMM1_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2510_13668_amd",
+                            "predict_continuous_traffic.json")
+CPU_ROUNDS_1T = 8       # decode steps of the oracle's one-thread leg
+PREDICT_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2510_13668_amd",
                             "csrc", "predict.hip")
 
 
@@ -105,17 +106,36 @@ def copy_calibration():
 
 
 def measured_traffic():
-    """HBM bytes per first-layer GEMM launch from the committed counter runs,
-    or None when the kernel source changed since they were taken."""
+    """HBM bytes per launch of the predictor kernel from the committed counter
+    runs, or None when the kernel source changed since they were taken."""
     import hashlib
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
-        with open(GEMM1_SOURCE, "rb") as f:
+        with open(PREDICT_SOURCE, "rb") as f:
             sha = hashlib.sha256(f.read()).hexdigest()
     except (OSError, ValueError):
         return None
     return t["traffic_bytes"] if t.get("source_sha256") == sha else None
+
+
+KERNEL_SPLIT_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                                 "predict_continuous_kernels.json")
+
+
+def committed_kernel_split():
+    """Per-kernel average durations of star_predict at this workload from the
+    committed rocprofv3 summary, or None when the kernel source changed since
+    it was taken."""
+    import hashlib
+    try:
+        with open(KERNEL_SPLIT_FILE) as f:
+            t = json.load(f)
+        with open(PREDICT_SOURCE, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    return t["kernels"] if t.get("source_sha256") == sha else None
 
 
 class HipEvents:
@@ -151,24 +171,79 @@ class HipEvents:
         for e in evs:
             self.hip.hipEventDestroy(e)
 
+    def time_calls(self, fn, n, stream):
+        """Mean seconds of fn(i), i < n, each bracketed by its own pair of
+        events recorded on `stream` (the stream fn launches on)."""
+        import torch
+        evs = self.create(2 * n)
+        hs = ctypes.c_void_p(stream.cuda_stream)
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        torch.cuda.synchronize()
+        for i in range(n):
+            self.hip.hipEventRecord(evs[2 * i], hs)
+            fn(i)
+            self.hip.hipEventRecord(evs[2 * i + 1], hs)
+        torch.cuda.synchronize()
+        t = float(np.mean([self.elapsed_ms(evs[2 * i], evs[2 * i + 1]) for i in range(n)])) * 1e-3
+        self.destroy(evs)
+        return t
 
-def cpu_baseline(x, wl, rounds: int):
-    """The CPU oracle on the first `rounds` decode steps of the same workload."""
+
+def cpu_info():
+    """Host CPU model and this process's CPU affinity."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    aff = sorted(os.sched_getaffinity(0))
+    runs, start = [], None
+    for i, c in enumerate(aff):
+        if start is None:
+            start = c
+        if i + 1 == len(aff) or aff[i + 1] != c + 1:
+            runs.append(f"{start}-{c}" if c > start else f"{c}")
+            start = None
+    return {"cpu_model": model, "affinity": ",".join(runs), "affinity_cpus": len(aff)}
+
+
+def cpu_baseline(x, wl, rounds: int, rounds_1t: int):
+    """The CPU oracle on the first `rounds` decode steps of the same workload
+    with all its OpenMP threads, then on the first `rounds_1t` with one."""
     import oracle
-    state = np.zeros(wl.n_req, np.float64)
-    t0 = time.perf_counter()
-    for s in range(rounds):
-        out = oracle.predict(x.hidden[s], x.w1, x.w2, x.bin_values, dtype=wl.dtype, act=wl.act,
-                             ema_alpha=wl.ema_alpha, ema_init=(s == 0), ema_state=state,
-                             len_max=wl.len_max)
-        oracle.round_((x.cur_len + s).astype(np.int32), out["rem_len"], x.inst_of,
-                      n_inst=wl.n_inst, bucket=wl.bucket, n_buckets=wl.n_buckets, top_k=wl.top_k)
-    dt = time.perf_counter() - t0
-    return {"value": wl.n_req * rounds / dt, "unit": "requests/s", "cores": oracle.threads(),
-            "kind": "oracle",
-            "sample": f"first {rounds} of the 200 decode steps, all {wl.n_req} requests, full "
-                      f"round (fp64 head, per-step int64 curves, direct peak per candidate, "
-                      f"full sort); {dt:.2f} s"}
+
+    def run(n_rounds):
+        state = np.zeros(wl.n_req, np.float64)
+        t0 = time.perf_counter()
+        for s in range(n_rounds):
+            out = oracle.predict(x.hidden[s], x.w1, x.w2, x.bin_values, dtype=wl.dtype,
+                                 act=wl.act, ema_alpha=wl.ema_alpha, ema_init=(s == 0),
+                                 ema_state=state, len_max=wl.len_max)
+            oracle.round_((x.cur_len + s).astype(np.int32), out["rem_len"], x.inst_of,
+                          n_inst=wl.n_inst, bucket=wl.bucket, n_buckets=wl.n_buckets,
+                          top_k=wl.top_k)
+        return time.perf_counter() - t0
+
+    threads = oracle.threads()
+    dt = run(rounds)
+    oracle.set_threads(1)
+    try:
+        dt1 = run(rounds_1t)
+    finally:
+        oracle.set_threads(threads)
+    out = {"value": wl.n_req * rounds / dt, "unit": "requests/s", "cores": threads,
+           "kind": "oracle",
+           "sample": f"first {rounds} of the 200 decode steps, all {wl.n_req} requests, full "
+                     f"round (fp64 head, per-step int64 curves, direct peak per candidate, "
+                     f"full sort); {dt:.2f} s on {threads} threads",
+           "value_1thread": wl.n_req * rounds_1t / dt1,
+           "sample_1thread": f"first {rounds_1t} decode steps on one thread; {dt1:.2f} s"}
+    out.update(cpu_info())
+    return out
 
 
 VAR_STEPS = 16    # staged decode steps of the variance path (cur + s, rem - s)
@@ -467,8 +542,8 @@ def bench_mlp4(args):
     rem = torch.empty(B, dtype=torch.int32, device=dev)
     stream = torch.cuda.Stream()
 
-    def params(n, init=False, ev=None):
-        return star.mlp4_params(n, d, m1, m2, m3, synth.BF16, 0.2, init, 32768, x.b4, ev)
+    def params(n, init=False):
+        return star.mlp4_params(n, d, m1, m2, m3, synth.BF16, 0.2, init, 32768, x.b4)
 
     ws = star.Workspace(star.predict_mlp4_workspace_size(params(B)))
     star.predict_mlp4(params(B, True), hid[0], w1, None, w2, None, w3, None, w4, ema, y, rem, ws,
@@ -498,22 +573,14 @@ def bench_mlp4(args):
                                                     w3, None, w4, ema[:nb], y[:nb], rem[:nb], ws,
                                                     stream), args.steps) * 1e3
 
-    # the first layer's GEMM, HIP events recorded by the library around it
+    # one call (the four layers, five kernels) timed with HIP events on its
+    # stream; the per-kernel split comes from rocprofv3
     he = HipEvents()
-    evs = he.create(2 * args.steps)
-    arrs = [(ctypes.c_void_p * 2)(evs[2 * i].value, evs[2 * i + 1].value)
-            for i in range(args.steps)]
-    pps = [params(B, False, ctypes.cast(a, ctypes.c_void_p)) for a in arrs]
-    torch.cuda.synchronize()
-    for i in range(args.steps):
-        star.predict_mlp4(pps[i], hid[i % S], w1, None, w2, None, w3, None, w4, ema, y, rem, ws,
-                          stream)
-    torch.cuda.synchronize()
-    g_s = float(np.mean([he.elapsed_ms(evs[2 * i], evs[2 * i + 1])
-                         for i in range(args.steps)])) * 1e-3
-    he.destroy(evs)
-    flops = 2.0 * B * d * m1
-    achieved = flops / g_s / 1e12
+    call_s = he.time_calls(lambda i: star.predict_mlp4(pp, hid[i % S], w1, None, w2, None, w3,
+                                                       None, w4, ema, y, rem, ws, stream),
+                           args.steps, stream)
+    flops = 2.0 * B * (d * m1 + m1 * m2 + m2 * m3 + m3)
+    achieved = flops / call_s / 1e12
 
     out = {
         "metric": "requests predicted/sec by the paper's 4-layer regression head "
@@ -534,10 +601,11 @@ def bench_mlp4(args):
                                "EMA 0.2",
                    "n_req": B, "dims": [d, m1, m2, m3]},
         "latency_us": {"batch_1": lat[1], "batch_10": lat[10]},
-        "roofline": {"kernel": "gemm1_splitk_kernel (layer 1, H[1024,3584] x W1[2048,3584]^T)",
+        "roofline": {"kernel": "the whole call (four layers; layer 1, H[1024,3584] x "
+                               "W1[2048,3584]^T, is 86% of its FLOPs)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                     "avg_kernel_us": g_s * 1e6, "algorithmic_flop": flops},
+                     "avg_call_us": call_s * 1e6, "algorithmic_flop": flops},
     }
     if args.cpu_rounds > 0:
         steps = 8
@@ -556,8 +624,9 @@ def bench_mlp4(args):
 
 def bench_configs(args):
     """Per-call times of the round's two calls at each workload's own shape,
-    with the first-layer GEMM's MFMA fraction and the projection-and-scoring
-    call's compulsory bytes over its time (an HBM fraction)."""
+    with the predictor's FLOPs (both products) over the call's time (an MFMA
+    fraction) and the projection-and-scoring call's compulsory bytes over its
+    time (an HBM fraction)."""
     import torch
     from paper_2510_13668_amd import star, synth
 
@@ -619,17 +688,8 @@ def bench_configs(args):
         predict_us = timed(predict)
         ps_us = timed(project_score)
         round_us = timed(lambda: (predict(), project_score()))
-        evs = he.create(2 * reps)
-        arrs = [(ctypes.c_void_p * 2)(evs[2 * i].value, evs[2 * i + 1].value) for i in range(reps)]
-        pps = [star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, False, wl.len_max,
-                                   ctypes.cast(a, ctypes.c_void_p)) for a in arrs]
-        torch.cuda.synchronize()
-        for i in range(reps):
-            predict(pps[i])
-        torch.cuda.synchronize()
-        g_us = float(np.mean([he.elapsed_ms(evs[2 * i], evs[2 * i + 1]) for i in range(reps)])) * 1e3
-        he.destroy(evs)
-        flops = 2.0 * N * d * m
+        g_us = he.time_calls(lambda i: predict(), reps, stream) * 1e6
+        flops = 2.0 * N * d * m + 2.0 * N * m * nb
         peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
         ps_bytes = 12 * N + 8 * n * K + 8 * N * n + 12 * N + 16 * top_k
         rows.append({
@@ -637,14 +697,14 @@ def bench_configs(args):
             "n_inst": n, "n_buckets": K, "top_k": top_k, "dtype": "bf16" if bf16 else "f32",
             "rem_len": "true lengths" if x.true_len is not None else "predicted",
             "predict_us": predict_us, "project_and_score_us": ps_us, "round_us": round_us,
-            "gemm1_us": g_us, "gemm1_tflops": flops / (g_us * 1e-6) / 1e12,
-            "gemm1_frac": flops / (g_us * 1e-6) / 1e12 / peak, "gemm1_peak_tflops": peak,
+            "predict_event_us": g_us, "predict_tflops": flops / (g_us * 1e-6) / 1e12,
+            "predict_frac": flops / (g_us * 1e-6) / 1e12 / peak, "peak_tflops": peak,
             "project_and_score_bytes": ps_bytes,
             "project_and_score_gbs": ps_bytes / (ps_us * 1e-6) / 1e9,
             "project_and_score_hbm_frac": ps_bytes / (ps_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
             "reps": reps})
-        print(f"{name}: predict {predict_us:.1f} us (GEMM1 {g_us:.1f} us, "
-              f"{rows[-1]['gemm1_frac'] * 100:.1f}% of peak), project+score {ps_us:.1f} us",
+        print(f"{name}: predict {predict_us:.1f} us (one call between events {g_us:.1f} us, "
+              f"{rows[-1]['predict_frac'] * 100:.1f}% of peak), project+score {ps_us:.1f} us",
               file=sys.stderr, flush=True)
         del hid, w1, w2, ws_p, ws_s, scores
         torch.cuda.empty_cache()
@@ -887,18 +947,19 @@ def main():
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) / args.steps
 
-    # The same pipeline captured in HIP graphs of CHUNK rounds each (the two
-    # streams fork and join inside the capture), so that the host launches
+    # The same pipeline captured in HIP graphs of up to CHUNK rounds each (the
+    # two streams fork and join inside the capture), so that the host launches
     # one graph per CHUNK rounds instead of the kernels and event operations
-    # of every round.
+    # of every round.  The warm-up and the timed region run exactly
+    # args.warmup and args.steps rounds: a shorter graph takes any remainder.
     CHUNK = 40
-    chunk_graphs = []
-    torch.cuda.synchronize()
-    for c0 in range(0, S, CHUNK):
+    graph_cache = {}
+
+    def capture(c0, length):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
             sched.wait_stream(stream)
-            for j in range(CHUNK):
+            for j in range(length):
                 step = (c0 + j) % S
                 k = j % NSLOT
                 sb = slot_buf[k]
@@ -913,24 +974,37 @@ def main():
                                        sb["tt"], sb["ts"], ws_s, sched)
                 ev_done[k].record(sched)
             stream.wait_stream(sched)
-        chunk_graphs.append(g)
+        return g
+
+    def graphs_for(start, rounds):
+        """Graphs that run `rounds` pipelined rounds from decode step `start`."""
+        out, i = [], 0
+        while i < rounds:
+            key = ((start + i) % S, min(CHUNK, rounds - i))
+            if key not in graph_cache:
+                graph_cache[key] = capture(*key)
+            out.append(graph_cache[key])
+            i += key[1]
+        return out
+
+    warm_graphs = graphs_for(0, args.warmup)
+    timed_graphs = graphs_for(args.warmup, args.steps)
     torch.cuda.synchronize()
 
     def timed_graph_pipelined():
-        reps = max(1, args.steps // CHUNK)
-        for i in range(max(1, args.warmup // CHUNK)):
-            with torch.cuda.stream(stream):
-                chunk_graphs[i % len(chunk_graphs)].replay()
+        with torch.cuda.stream(stream):
+            for g in warm_graphs:
+                g.replay()
         torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record(stream)
         with torch.cuda.stream(stream):
-            for i in range(reps):
-                chunk_graphs[i % len(chunk_graphs)].replay()
+            for g in timed_graphs:
+                g.replay()
         t1.record(stream)
         torch.cuda.synchronize()
-        return t0.elapsed_time(t1) / (reps * CHUNK)
+        return t0.elapsed_time(t1) / args.steps
 
     def eager_percentiles():
         """Each eager round bracketed by its own events: p50 / p99 in us."""
@@ -953,22 +1027,18 @@ def main():
     ms_mode["graph_pipelined"] = timed_graph_pipelined()
     ms_step = ms_mode[args.mode]
 
-    # Dominant kernel (first-layer GEMM) timed with HIP events recorded by the
-    # library around that kernel on the same stream, over `steps` eager rounds.
+    # Dominant work of the round: the predictor, star_predict.  At this size
+    # it is two kernels (the split-K first-layer product, then the head that
+    # reduces the splits and runs the second product, softmax and EMA); one
+    # pair of HIP events brackets each call on the stream it is launched on,
+    # over `steps` calls of the round's own inputs.  The split between the
+    # two kernels comes from the committed rocprofv3 summary.
     he = HipEvents()
-    evs = he.create(2 * args.steps)
-    arrs = [(ctypes.c_void_p * 2)(evs[2 * i].value, evs[2 * i + 1].value) for i in range(args.steps)]
-    pps = [star.predict_params(N, d, m, nb, wl.dtype, wl.act, wl.ema_alpha, False, wl.len_max,
-                               ctypes.cast(a, ctypes.c_void_p)) for a in arrs]
-    torch.cuda.synchronize()
-    for i in range(args.steps):
-        round_((i + 1) % S, pps[i])
-    torch.cuda.synchronize()
-    gemm_ms = [he.elapsed_ms(evs[2 * i], evs[2 * i + 1]) for i in range(args.steps)]
-    he.destroy(evs)
-    gemm_avg_s = float(np.mean(gemm_ms)) * 1e-3
-    flops = 2.0 * N * d * m
-    achieved = flops / gemm_avg_s / 1e12
+    kern_s = he.time_calls(lambda i: star.predict(pp, hid[(i + 1) % S], w1, None, w2, None, bins,
+                                                  ema, expected, rem, ws_p, stream),
+                           args.steps, stream)
+    flops = 2.0 * N * d * m + 2.0 * N * m * nb
+    achieved = flops / kern_s / 1e12
 
     out = {
         "metric": METRIC,
@@ -997,14 +1067,23 @@ def main():
         "us_per_round_eager_p50": p50,
         "us_per_round_eager_p99": p99,
         "us_per_round_graph": ms_mode["graph"] * 1e3,
-        "roofline": {"kernel": "gemm1_splitk_kernel (bf16 MFMA, H[1024,4096] x W1[512,4096]^T)",
+        "timing": {"headline": args.mode, "rounds_timed": args.steps,
+                   "warmup_rounds": args.warmup,
+                   "overlap": "graph_pipelined and pipelined time throughput: round i+1's "
+                              "prediction runs while round i is projected and scored; "
+                              "us_per_round_eager (p50/p99) is one round's latency"},
+        "roofline": {"kernel": "star_predict = gemm1_splitk_kernel (bf16 MFMA, H[1024,4096] x "
+                               "W1[512,4096]^T, 4 K-splits) + head_kernel (split reduction, GELU, "
+                               "x W2[64,512]^T, softmax, EMA)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic(),
-                     "avg_kernel_us": gemm_avg_s * 1e6, "algorithmic_flop": flops},
+                     "avg_call_us": kern_s * 1e6, "algorithmic_flop": flops,
+                     "kernels": committed_kernel_split()},
     }
     if args.cpu_rounds > 0:
-        out["cpu_baseline"] = cpu_baseline(x, wl, min(args.cpu_rounds, S))
+        out["cpu_baseline"] = cpu_baseline(x, wl, min(args.cpu_rounds, S),
+                                           min(args.cpu_rounds, CPU_ROUNDS_1T))
     print(json.dumps(out), flush=True)
 
 

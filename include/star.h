@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define STAR_ABI_VERSION 1
+#define STAR_ABI_VERSION 2
 #define STAR_WS_HEADER_BYTES 8192
 #define STAR_MAX_TOP_K 1024
 
@@ -54,7 +54,9 @@ typedef enum {
     STAR_ERR_UNSUPPORTED = -2,   /* shape or alignment outside what the kernels handle */
     STAR_ERR_OVERFLOW = -3,      /* sizes whose int64 loads could overflow */
     STAR_ERR_WORKSPACE = -4,     /* workspace null, misaligned or too small */
-    STAR_ERR_HIP = -5            /* a HIP runtime call or kernel launch failed */
+    STAR_ERR_HIP = -5,           /* a HIP runtime call or kernel launch failed */
+    STAR_ERR_DEVICE_INPUT = -6   /* star_read_device_error: array contents broke a precondition
+                                    (the device error word was non-zero) */
 } star_status;
 
 /* bits of the device-error word */
@@ -94,15 +96,13 @@ typedef struct {
     float   ema_alpha;  /* 0 disables smoothing; else in (0, 1] */
     int32_t ema_init;   /* 1: y := E this call (first step); 0: blend with ema_state */
     int32_t len_max;    /* >= 1, upper clamp of rem_len */
-    void*   timing_events; /* NULL, or a host array of two hipEvent_t recorded
-                              on `stream` just before and just after the
-                              first-layer GEMM kernel (per-kernel timing) */
 } star_predict_params;
 
 size_t star_predict_workspace_size(const star_predict_params* p);
 
 /* hidden [B, d], w1 [m, d], w2 [nb, m]: row-major, 16-byte aligned.
- * b1 [m], b2 [nb]: fp32 or NULL (zero).  bin_values [nb]: fp32.
+ * b1 [m]: fp32, 16-byte aligned, or NULL (zero).  b2 [nb]: fp32 or NULL.
+ * bin_values [nb]: fp32.
  * ema_state [B]: fp32 in/out, required iff ema_alpha > 0.
  * expected_len [B]: fp32 out, the unsmoothed E.
  * rem_len [B]: int32 out, or NULL. */
@@ -138,7 +138,6 @@ typedef struct {
     int32_t ema_init;
     int32_t len_max;    /* >= 1 */
     float   b4;         /* output bias */
-    void*   timing_events; /* NULL, or two hipEvent_t around the first layer's GEMM */
 } star_mlp4_params;
 
 size_t star_predict_mlp4_workspace_size(const star_mlp4_params* p);
@@ -328,7 +327,9 @@ star_status star_plan_migrations(const star_plan_params* p, const int32_t* cur_l
 star_status star_workspace_init(void* ws, size_t ws_bytes, void* stream);
 
 /* Synchronise `stream`, return the workspace's device-error word (OR of
- * STAR_DEV_* bits since the last read) in *code, and clear it. */
+ * STAR_DEV_* bits since the last read) in *code, and clear it.  Returns
+ * STAR_ERR_DEVICE_INPUT when that word was non-zero (*code names the
+ * broken preconditions), STAR_OK when it was zero. */
 star_status star_read_device_error(void* ws, void* stream, int32_t* code);
 
 const char* star_status_string(star_status s);

@@ -60,6 +60,13 @@ def threads() -> int:
     return int(_load().star_oracle_threads())
 
 
+def set_threads(n: int) -> None:
+    """Threads of later parallel loops (timing only; results do not depend on it)."""
+    lib = _load()
+    lib.star_oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.star_oracle_set_threads(int(n))
+
+
 def _ptr(a: Optional[np.ndarray]):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 

@@ -598,3 +598,13 @@ int star_oracle_threads(void) {
     return 1;
 #endif
 }
+
+/* Threads later parallel regions use (n >= 1); a timing control only, the
+ * results do not depend on it. */
+void star_oracle_set_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}

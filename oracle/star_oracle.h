@@ -114,6 +114,7 @@ int star_oracle_plan(int64_t N, int64_t n, int64_t b, int64_t K, const int32_t* 
 
 int star_oracle_abi_version(void);
 int star_oracle_threads(void);
+void star_oracle_set_threads(int n);
 
 #ifdef __cplusplus
 }

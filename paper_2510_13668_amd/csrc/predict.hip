@@ -153,7 +153,33 @@ __device__ __forceinline__ void g1_compute(const char* la, const char* lb, int w
     constexpr int MI = SH::MI, NJ = SH::NJ;
     const int r32 = lane & 31;
     const int khalf = lane >> 5;   // which half of the MFMA's K slice this lane feeds
-    if constexpr (kElemBytes == 2) {
+    constexpr int KK = BK / 16;
+    if constexpr (kElemBytes == 2 && (MI + NJ) * KK <= 12) {
+        // every fragment of the K-tile is read from LDS first, so the wave
+        // waits for LDS once per K-tile and then issues its MFMAs back to back
+        bf16x8_t a[KK][MI], b[KK][NJ];
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const int koff = (kk * 16 + khalf * 8) * 2;
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+                a[kk][i] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(la + (wm * 32 * MI + i * 32 + r32) * G1_ROW + koff));
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                b[kk][j] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(lb + (wn * 32 * NJ + j * 32 + r32) * G1_ROW + koff));
+        }
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk][i], b[kk][j], acc[i][j], 0, 0, 0);
+        // keep that order: the scheduler would otherwise pair reads with
+        // MFMAs to save registers and wait for LDS once per pair
+        __builtin_amdgcn_sched_group_barrier(0x100, (MI + NJ) * KK, 0);   // LDS reads
+        __builtin_amdgcn_sched_group_barrier(0x008, MI * NJ * KK, 0);     // MFMAs
+    } else if constexpr (kElemBytes == 2) {
         // v_mfma_f32_32x32x16_bf16: lane feeds row (lane%32), k = 8*(lane/32)..+7
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
@@ -212,46 +238,34 @@ __device__ __forceinline__ void g1_step(const G1Ctx& c, char (*lds)[SH::LDS_A + 
     g1_compute<kElemBytes, SH>(lds[buf], lds[buf] + SH::LDS_A, wm, wn, lane, acc);
 }
 
-// Split-K product P[split] = A[:, Ks] W[:, Ks]^T over one BM x BN tile:
-// NS K-tiles of global loads are in flight ahead of the tile being
-// multiplied (register staging, two LDS buffers, one barrier per K-tile).
-template <int kElemBytes, int NS, class SH>
-__global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
-    const char* __restrict__ A, const char* __restrict__ W, float* __restrict__ P,
-    int M, int N, int Kd, int splits, int tiles_n, int ktiles) {
-    constexpr int MI = SH::MI, NJ = SH::NJ;
-    __shared__ __attribute__((aligned(16))) char lds[2][SH::LDS_A + SH::LDS_B];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wid = tid >> 6;
-    const int wm = wid / SH::WN, wn = wid % SH::WN;
-
+// The work of one workgroup of the split-K product: tile (tm, tn), K-tiles
+// [kt0, kt1).  Workgroups are dealt to the XCDs round-robin; the logical
+// order puts one K-slice of neighbouring tiles on each XCD.
+struct G1Work {
+    int split, tile, tm, tn, kt0, nk;
+};
+__device__ inline G1Work g1_work(int splits, int tiles_n, int ktiles) {
+    G1Work w;
     const int logical = xcd_logical_block(blockIdx.x, gridDim.x);
     const int tiles = gridDim.x / splits;
-    const int split = logical / tiles;
-    const int tile = logical % tiles;
-    const int tm = tile / tiles_n, tn = tile % tiles_n;
-    const int kt0 = (int)((int64_t)split * ktiles / splits);
-    const int kt1 = (int)((int64_t)(split + 1) * ktiles / splits);
-    const int nk = kt1 - kt0;
+    w.split = logical / tiles;
+    w.tile = logical % tiles;
+    w.tm = w.tile / tiles_n;
+    w.tn = w.tile % tiles_n;
+    w.kt0 = (int)((int64_t)w.split * ktiles / splits);
+    const int kt1 = (int)((int64_t)(w.split + 1) * ktiles / splits);
+    w.nk = kt1 - w.kt0;
+    return w;
+}
 
-    G1Ctx c;
-    c.A = A; c.W = W; c.M = M; c.N = N; c.tm = tm; c.tn = tn; c.tid = tid;
-    c.threads = SH::THREADS; c.bm = SH::BM; c.bn = SH::BN;
-    c.row_bytes = (int64_t)Kd * kElemBytes;
-
-    f32x16 acc[MI][NJ];
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
-
-    const int r32 = lane & 31;
-    const int khalf = lane >> 5;
-
+// Main loop of one workgroup's product: NS K-tiles of global loads are in
+// flight ahead of the tile being multiplied (register staging, two LDS
+// buffers, one barrier per K-tile).  acc receives this wave's slab.
+template <int kElemBytes, int NS, class SH>
+__device__ __forceinline__ void g1_mainloop_edge(const G1Ctx& c, const G1Work& w,
+                                                 char (*lds)[SH::LDS_A + SH::LDS_B], int wm,
+                                                 int wn, int lane, f32x16 (&acc)[SH::MI][SH::NJ]) {
+    const int nk = w.nk, kt0 = w.kt0;
     if (nk > 0) {
         G1Stage<SH> st[NS];
 #pragma unroll
@@ -266,6 +280,136 @@ __global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
         for (int u = 0; u < NS - 1; ++u)
             if (i + u < nk) g1_step<kElemBytes, NS, SH>(c, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
     }
+}
+
+// The same for a tile wholly inside the product whose K is a whole number
+// of K-tiles: nothing to clamp or mask.  Each thread's row offsets (32-bit,
+// the operands are under 4 GiB) and LDS offsets are computed once; per
+// K-tile only the uniform base pointer moves, so the loads take the
+// scalar-base form and the loop carries no per-element masks.
+template <class SH>
+struct G1Fast {
+    uint32_t ga[SH::CA], gb[SH::CB];          // global byte offsets within a K-tile column
+    uint32_t la[SH::CA], lb[SH::CB];          // LDS byte offsets
+};
+typedef uint32_t g1u4 __attribute__((ext_vector_type(4)));
+template <class SH>
+struct G1FStage {                             // one K-tile of both operands in registers
+    g1u4 a[SH::CA], b[SH::CB];
+};
+
+template <class SH>
+__device__ __forceinline__ void g1f_load(const G1Ctx& c, const G1Fast<SH>& f, int kt,
+                                         G1FStage<SH>& st) {
+    const char* pa = c.A + (int64_t)kt * G1_KBYTES;
+    const char* pb = c.W + (int64_t)kt * G1_KBYTES;
+#pragma unroll
+    for (int p = 0; p < SH::CA; ++p) st.a[p] = *(const g1u4*)(pa + f.ga[p]);
+#pragma unroll
+    for (int p = 0; p < SH::CB; ++p) st.b[p] = *(const g1u4*)(pb + f.gb[p]);
+}
+
+template <int kElemBytes, int NS, class SH>
+__device__ __forceinline__ void g1f_step(const G1Ctx& c, const G1Fast<SH>& f,
+                                         char (*lds)[SH::LDS_A + SH::LDS_B], int kt0, int nk,
+                                         int i, G1FStage<SH>& st, int wm, int wn, int lane,
+                                         f32x16 (&acc)[SH::MI][SH::NJ]) {
+    char* l = lds[i & 1];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int p = 0; p < SH::CA; ++p) *(g1u4*)(l + f.la[p]) = st.a[p];
+#pragma unroll
+    for (int p = 0; p < SH::CB; ++p) *(g1u4*)(l + f.lb[p]) = st.b[p];
+    __syncthreads();
+    g1f_load<SH>(c, f, kt0 + (i + NS < nk ? i + NS : i), st);
+    __builtin_amdgcn_sched_barrier(0);
+    g1_compute<kElemBytes, SH>(l, l + SH::LDS_A, wm, wn, lane, acc);
+}
+
+template <int kElemBytes, int NS, class SH>
+__device__ __forceinline__ void g1_mainloop_interior(const G1Ctx& c, const G1Work& w,
+                                                     char (*lds)[SH::LDS_A + SH::LDS_B], int wm,
+                                                     int wn, int lane,
+                                                     f32x16 (&acc)[SH::MI][SH::NJ]) {
+    G1Fast<SH> f;
+#pragma unroll
+    for (int p = 0; p < SH::CA; ++p) {
+        const int ch = c.tid + p * c.threads;
+        f.ga[p] = (uint32_t)((c.tm * SH::BM + (ch >> 3)) * c.row_bytes + (ch & 7) * 16);
+        f.la[p] = (uint32_t)((ch >> 3) * G1_ROW + (ch & 7) * 16);
+    }
+#pragma unroll
+    for (int p = 0; p < SH::CB; ++p) {
+        const int ch = c.tid + p * c.threads;
+        f.gb[p] = (uint32_t)((c.tn * SH::BN + (ch >> 3)) * c.row_bytes + (ch & 7) * 16);
+        f.lb[p] = (uint32_t)(SH::LDS_A + (ch >> 3) * G1_ROW + (ch & 7) * 16);
+    }
+    const int nk = w.nk, kt0 = w.kt0;
+    if (nk > 0) {
+        G1FStage<SH> st[NS];
+#pragma unroll
+        for (int u = 0; u < NS; ++u) g1f_load<SH>(c, f, kt0 + (u < nk ? u : 0), st[u]);
+        int i = 0;
+        for (; i + NS <= nk; i += NS) {
+#pragma unroll
+            for (int u = 0; u < NS; ++u)
+                g1f_step<kElemBytes, NS, SH>(c, f, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
+        }
+#pragma unroll
+        for (int u = 0; u < NS - 1; ++u)
+            if (i + u < nk)
+                g1f_step<kElemBytes, NS, SH>(c, f, lds, kt0, nk, i + u, st[u], wm, wn, lane, acc);
+    }
+}
+
+template <int kElemBytes, int NS, class SH>
+__device__ __forceinline__ void g1_mainloop(const char* A, const char* W, int M, int N, int Kd,
+                                            const G1Work& w, char (*lds)[SH::LDS_A + SH::LDS_B],
+                                            f32x16 (&acc)[SH::MI][SH::NJ]) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    const int wm = wid / SH::WN, wn = wid % SH::WN;
+    G1Ctx c;
+    c.A = A; c.W = W; c.M = M; c.N = N; c.tm = w.tm; c.tn = w.tn; c.tid = tid;
+    c.threads = SH::THREADS; c.bm = SH::BM; c.bn = SH::BN;
+    c.row_bytes = (int64_t)Kd * kElemBytes;
+#pragma unroll
+    for (int i = 0; i < SH::MI; ++i)
+#pragma unroll
+        for (int j = 0; j < SH::NJ; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+    // uniform over the workgroup: rows and columns in range, K whole tiles,
+    // and both operands addressable with 32-bit offsets
+    const bool interior = (w.tm + 1) * SH::BM <= M && (w.tn + 1) * SH::BN <= N &&
+                          c.row_bytes % G1_KBYTES == 0 &&
+                          (int64_t)M * c.row_bytes < ((int64_t)1 << 32) &&
+                          (int64_t)N * c.row_bytes < ((int64_t)1 << 32);
+    if (interior)
+        g1_mainloop_interior<kElemBytes, NS, SH>(c, w, lds, wm, wn, lane, acc);
+    else
+        g1_mainloop_edge<kElemBytes, NS, SH>(c, w, lds, wm, wn, lane, acc);
+}
+
+// Split-K product P[split] = A[:, Ks] W[:, Ks]^T over one BM x BN tile.
+template <int kElemBytes, int NS, class SH>
+__global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
+    const char* __restrict__ A, const char* __restrict__ W, float* __restrict__ P,
+    int M, int N, int Kd, int splits, int tiles_n, int ktiles) {
+    constexpr int MI = SH::MI, NJ = SH::NJ;
+    __shared__ __attribute__((aligned(16))) char lds[2][SH::LDS_A + SH::LDS_B];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    const int wm = wid / SH::WN, wn = wid % SH::WN;
+    const G1Work w = g1_work(splits, tiles_n, ktiles);
+    const int split = w.split, tm = w.tm, tn = w.tn;
+    f32x16 acc[MI][NJ];
+    g1_mainloop<kElemBytes, NS, SH>(A, W, M, N, Kd, w, lds, acc);
+    const int r32 = lane & 31;
+    const int khalf = lane >> 5;
 
     // epilogue: the 32x32 accumulator layout (element v of lane l is row
     // 8*(v/4) + 4*(l/32) + v%4, column l%32 of its block) goes through LDS
@@ -899,6 +1043,338 @@ __global__ __launch_bounds__(HD_THREADS) void head_tiled_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// The whole binned head in one kernel (bf16), for products that take one
+// K-slice (no split-K): first product, bias, activation, second product,
+// softmax, expectation, EMA and integerisation.
+//
+// Every workgroup computes one BM x BN tile of z1 = H W1^T over all of K,
+// adds b1 and applies the activation.  The second product is linear in a1's
+// columns, so the workgroup then multiplies its BN columns of a1 with the
+// same BN columns of W2: the tile's share of every bin logit of its BM rows.
+// The column tiles of a row block meet through a counter; the last to
+// arrive sums the shares in column order (the same fixed order whatever the
+// arrival order) and finishes its rows: b2, softmax over the bins, mean over
+// the bin values, EMA, round half to even, clamp.  z1 never leaves the chip.
+//
+// No cache maintenance: the shares are stored and loaded with the
+// device-coherent cache policy (sc1), every storer waits for its stores to
+// complete before its counter increment, and the last arriver loads only
+// after its own increment has returned.  So the shares never need an L2
+// write-back (release) or invalidation (acquire), which would also throw out
+// the operands the other workgroups of the XCD are still reading.  The
+// counters live in the workspace header, and every call leaves them at zero.
+//
+// Products that need a K-split take the two-kernel path instead (split-K
+// product, then the head kernel): meeting the K-slices in this kernel as
+// well put two exchanges and the whole head of the last tile on one
+// workgroup's critical path, which measured slower than the kernel boundary.
+// ---------------------------------------------------------------------------
+constexpr int FU_NB_MAX = 128;            // bins of the fused head (its logits fit the LDS)
+constexpr int FU_NBP = FU_NB_MAX + 4;     // fp32 per LDS row of logits (banks spread by rows)
+constexpr int FU_MAX_TICKETS = (int)((STAR_WS_HEADER_BYTES - kHdrFusedTickets) / 4);
+constexpr int kCpolCoherent = 16;         // buffer cache policy bits: sc1 (device scope)
+constexpr uint32_t kFuOob = 0x7FFFFFF0u;  // a buffer offset past every share: reads 0
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ inline __amdgpu_buffer_rsrc_t fu_rsrc(const void* base, uint32_t bytes) {
+    // raw buffer (stride 0); out-of-range accesses read 0 and drop writes
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+__device__ inline void fu_store(f32x4 v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)off, 0,
+                                           kCpolCoherent);
+}
+__device__ inline f32x4 fu_load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0,
+                                                                           kCpolCoherent));
+}
+// every store this thread issued has completed (is visible device-wide)
+__device__ inline void fu_wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// One workgroup's arrival at a counter that `expect` workgroups reach: true
+// for the last to arrive, which also resets the counter.  Call after the
+// workgroup's coherent stores have completed (fu_wait_stores in every thread).
+__device__ inline bool fu_last_arrival(uint32_t* counter, uint32_t expect, uint32_t* s_ticket) {
+    __syncthreads();
+    if (threadIdx.x == 0)
+        *s_ticket = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const bool last = *s_ticket == expect - 1;
+    if (last && threadIdx.x == 0)
+        __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return last;
+}
+
+__device__ inline f32x4 fu_chunk(const f32x16& a, int q) {
+    return f32x4{a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]};
+}
+
+struct FusedArgs {
+    const char* A;            // hidden [M, Kd] bf16
+    const char* W;            // w1 [N, Kd] bf16
+    const float* b1;          // [N] or null
+    const uint16_t* W2;       // [nb, N] bf16
+    const float* b2;          // [nb] or null
+    const float* bins;        // [nb]
+    float* lpart;             // logit shares: [tiles_m][tiles_n][blocks][1024] (tiles_n > 1)
+    uint32_t* tix_row;        // [tiles_m]
+    float* ema_state;
+    float* expected;
+    int32_t* rem_len;
+    int M, N, Kd, nb, tiles_n, ktiles, act, ema_init, len_max;
+    float ema_alpha;
+};
+
+template <int NS, class SH>
+__global__ __launch_bounds__(SH::THREADS) void predict_fused_kernel(FusedArgs a) {
+    constexpr int MI = SH::MI, NJ = SH::NJ, T = SH::THREADS, NW = T / 64;
+    constexpr int BM = SH::BM, BN = SH::BN;
+    constexpr int ZST = BN * 4 + 16;             // bytes per LDS row of the z1 / a1 tile
+    constexpr int C8 = BN / 8;                   // 8-column chunks per row
+    static_assert(T % C8 == 0, "a thread keeps its chunk column");
+    constexpr int NBI = BM / 32;                 // row blocks of the logit product
+    constexpr int MAXB = (NBI * (FU_NB_MAX / 32) + NW - 1) / NW;   // logit blocks per wave
+    constexpr int LPR = T / BM;                  // lanes per row in the softmax
+    static_assert(LPR >= 1 && (LPR & (LPR - 1)) == 0 && LPR <= 64, "lanes per row");
+    // the operand buffers of the main loop, reused for the z1 / a1 tile and
+    // then the logits
+    constexpr int kMainBytes = 2 * (SH::LDS_A + SH::LDS_B);
+    constexpr int kLogitBytes = (BM * FU_NBP + 2 * FU_NB_MAX) * 4;   // logits, bin values, b2
+    constexpr int kTileBytes = BM * ZST;
+    constexpr int kEpiBytes = kLogitBytes > kTileBytes ? kLogitBytes : kTileBytes;
+    __shared__ __attribute__((aligned(16))) char lds_raw[kMainBytes > kEpiBytes ? kMainBytes : kEpiBytes];
+    auto lds = reinterpret_cast<char (*)[SH::LDS_A + SH::LDS_B]>(lds_raw);
+    __shared__ uint32_t s_ticket;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    const int wm = wid / SH::WN, wn = wid % SH::WN;
+    const int r32 = lane & 31;
+    const int khalf = lane >> 5;
+    const G1Work w = g1_work(1, a.tiles_n, a.ktiles);
+    f32x16 acc[MI][NJ];
+    g1_mainloop<2, NS, SH>(a.A, a.W, a.M, a.N, a.Kd, w, lds, acc);
+
+    // The head's global reads (W2 fragments, b1, b2, bin values, EMA state)
+    // are all requested at once: one memory latency instead of one per use.
+    const int nbj = (a.nb + 31) >> 5;
+    const int nblk = NBI * nbj;
+    bf16x8 wf[MAXB][BN / 16];
+    f32x4 b1v[2];                                 // b1 of this thread's 8-column chunk
+    float binv, b2v, ema_prev;
+    const int c8 = tid % C8;
+    const int r = tid / LPR, sub = tid % LPR;     // the row this thread finishes in 5)
+    const int gr = w.tm * BM + r;
+    auto prefetch = [&]() {
+#pragma unroll
+        for (int u = 0; u < MAXB; ++u) {
+            const int blk = wid + u * NW;
+            const int jrow = (blk / NBI) * 32 + r32;
+#pragma unroll
+            for (int ks = 0; ks < BN / 16; ++ks) {
+                // clamped, unconditional; m % 8 == 0, so a chunk is wholly in or out
+                const int c = w.tn * BN + ks * 16 + 8 * khalf;
+                const bool ok = blk < nblk && jrow < a.nb && c < a.N;
+                const bf16x8 t = *(const bf16x8*)(a.W2 + (ok ? (int64_t)jrow * a.N + c : 0));
+                wf[u][ks] = t & (ok ? (short)-1 : (short)0);
+            }
+        }
+        {
+            // m % 8 == 0: the chunk is wholly in or out; b1 is 16-byte aligned
+            const int gcol = w.tn * BN + c8 * 8;
+            b1v[0] = b1v[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            if (a.b1 && gcol < a.N) {
+                b1v[0] = *(const f32x4*)(a.b1 + gcol);
+                b1v[1] = *(const f32x4*)(a.b1 + gcol + 4);
+            }
+        }
+        const int jb = tid < a.nb ? tid : 0;
+        binv = tid < a.nb ? a.bins[jb] : 0.0f;
+        b2v = (a.b2 && tid < a.nb) ? a.b2[jb] : 0.0f;
+        ema_prev = (a.ema_alpha > 0.0f && !a.ema_init) ? a.ema_state[gr < a.M ? gr : a.M - 1] : 0.0f;
+    };
+
+    prefetch();
+    __syncthreads();                         // the last products have read the LDS
+
+    // 1) z1 into LDS rows [BM][ZST bytes] (fp32); then, a chunk of 8 columns
+    //    at a time, bias and activation, written back in place as the bf16
+    //    pair [hi x 8 | lo x 8].  Element v of lane l of a 32 x 32 block is
+    //    row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32.
+    char* zt = lds_raw;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int col = wn * 32 * NJ + j * 32 + r32;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int row = wm * 32 * MI + i * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
+                *(float*)(zt + row * ZST + col * 4) = acc[i][j][v];
+            }
+        }
+    __syncthreads();
+    {
+        const bool cok = w.tn * BN + c8 * 8 < a.N;
+#pragma unroll 1
+        for (int e = tid; e < BM * C8; e += T) {
+            char* pz = zt + (e / C8) * ZST + c8 * 32;
+            const f32x4 z0 = *(const f32x4*)pz, z1 = *(const f32x4*)(pz + 16);
+            float x[8];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                x[k] = cok ? apply_act(z0[k] + b1v[0][k], a.act) : 0.0f;
+                x[k + 4] = cok ? apply_act(z1[k] + b1v[1][k], a.act) : 0.0f;
+            }
+            uint32_t hi[4], lo[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) split_bf16x2(x[2 * k], x[2 * k + 1], hi[k], lo[k]);
+            *(uint4*)pz = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+            *(uint4*)(pz + 16) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+        }
+    }
+    __syncthreads();
+
+    // 2) this tile's share of the bin logits, [BM rows] x [bins] over its BN
+    //    columns: v_mfma_f32_32x32x16_bf16 with A = a1 rows (hi, then lo) and
+    //    B = W2 rows.  Wave wid takes the blocks wid, wid + NW, ...
+    f32x16 lg[MAXB];
+#pragma unroll
+    for (int u = 0; u < MAXB; ++u) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) lg[u][e] = 0.0f;
+        const int blk = wid + u * NW;
+        if (blk < nblk) {
+            const int ib = blk % NBI;
+#pragma unroll
+            for (int ks = 0; ks < BN / 16; ++ks) {
+                const char* pa = zt + (ib * 32 + r32) * ZST + (2 * ks + khalf) * 32;
+                const bf16x8_t h = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)pa);
+                const bf16x8_t l = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(pa + 16));
+                const bf16x8_t b = __builtin_bit_cast(bf16x8_t, wf[u][ks]);
+                lg[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(h, b, lg[u], 0, 0, 0);
+                lg[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(l, b, lg[u], 0, 0, 0);
+            }
+        }
+    }
+
+    // 3) the column tiles of the row block meet; the last to arrive sums the
+    //    shares in column order (share layout: float4 q of lane l of block
+    //    blk at (blk 4 + q) 64 + l).  It reads its own share back too (its
+    //    stores have completed), so every load is unconditional; tiles past
+    //    the last read 0 (an offset past the buffer); the sum starts at -0,
+    //    which adds exactly.
+    if (a.tiles_n > 1) {
+        const uint32_t share = (uint32_t)nblk * 1024u;            // floats per share
+        const __amdgpu_buffer_rsrc_t rl =
+            fu_rsrc(a.lpart + (size_t)w.tm * a.tiles_n * share, (uint32_t)a.tiles_n * share * 4u);
+#pragma unroll
+        for (int u = 0; u < MAXB; ++u) {
+            const int blk = wid + u * NW;
+            if (blk < nblk)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    fu_store(fu_chunk(lg[u], q), rl,
+                             (uint32_t)w.tn * share * 4u + (uint32_t)((blk * 4 + q) * 64 + lane) * 16u);
+        }
+        fu_wait_stores();
+        if (!fu_last_arrival(&a.tix_row[w.tm], (uint32_t)a.tiles_n, &s_ticket)) return;
+        constexpr int G = 8;                  // shares loaded together
+#pragma unroll
+        for (int u = 0; u < MAXB; ++u) {
+            const int blk = wid + u * NW;
+            if (blk >= nblk) continue;
+            f32x4 sum[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) sum[q] = f32x4{-0.0f, -0.0f, -0.0f, -0.0f};
+#pragma unroll 1
+            for (int t0 = 0; t0 < a.tiles_n; t0 += G) {
+                f32x4 v[G][4];
+#pragma unroll
+                for (int g = 0; g < G; ++g)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int t = t0 + g;
+                        const uint32_t off = (uint32_t)t * share * 4u +
+                                             (uint32_t)((blk * 4 + q) * 64 + lane) * 16u;
+                        v[g][q] = fu_load(rl, t < a.tiles_n ? off : kFuOob);
+                    }
+#pragma unroll
+                for (int g = 0; g < G; ++g)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) sum[q] += v[g][q];
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) lg[u][4 * q + e] = sum[q][e];
+        }
+    }
+
+    // 4) logits into LDS rows [BM][FU_NBP], the bin values and b2 beside
+    //    them; then LPR lanes per row: + b2, softmax, mean over the bin
+    //    values, EMA, integerisation
+    __syncthreads();                          // every wave has read a1 from LDS
+    float* zl = (float*)&lds[0][0];
+    float* sbin = zl + BM * FU_NBP;           // [FU_NB_MAX] bin values, then [FU_NB_MAX] b2
+    if (tid < FU_NB_MAX) {
+        sbin[tid] = binv;
+        sbin[FU_NB_MAX + tid] = b2v;
+    }
+#pragma unroll
+    for (int u = 0; u < MAXB; ++u) {
+        const int blk = wid + u * NW;
+        if (blk >= nblk) continue;
+        const int ib = blk % NBI, jb = blk / NBI;
+        const int j = jb * 32 + r32;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int row = ib * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
+            zl[row * FU_NBP + j] = lg[u][v];
+        }
+    }
+    __syncthreads();
+    const float* zr = zl + r * FU_NBP;
+    float zmax = -INFINITY;
+#pragma unroll 4
+    for (int j = sub; j < a.nb; j += LPR) zmax = fmaxf(zmax, zr[j] + sbin[FU_NB_MAX + j]);
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) zmax = fmaxf(zmax, __shfl_xor(zmax, o, LPR));
+    float den = 0.0f, num = 0.0f;
+#pragma unroll 4
+    for (int j = sub; j < a.nb; j += LPR) {
+        const float e = expf(zr[j] + sbin[FU_NB_MAX + j] - zmax);
+        den += e;
+        num += e * sbin[j];
+    }
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) {
+        den += __shfl_xor(den, o, LPR);
+        num += __shfl_xor(num, o, LPR);
+    }
+    if (sub == 0 && gr < a.M) {
+        const float E = num / den;
+        a.expected[gr] = E;
+        float y = E;
+        if (a.ema_alpha > 0.0f) {
+            y = a.ema_init ? E : a.ema_alpha * E + (1.0f - a.ema_alpha) * ema_prev;
+            a.ema_state[gr] = y;
+        }
+        if (a.rem_len) {
+            const float q = rintf(y);
+            int32_t li;
+            if (!(q >= 1.0f)) li = 1;
+            else if (q >= (float)a.len_max) li = a.len_max;
+            else li = (int32_t)q;
+            a.rem_len[gr] = li;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // (f3) between the regression head's first two layers: fixed-order split-K
 // reduction, bias, ReLU, and the operand of the next product (bf16, round
 // to nearest even, or fp32)
@@ -1006,7 +1482,23 @@ GemmPlan plan_gemm(int M, int N, int K, int elem) {
     return best;
 }
 
-PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok) {
+// Products the fused kernel takes: one K-slice (no split-K), a tile shape
+// with an LDS epilogue, at most FU_NB_MAX bins, and a counter per row block
+// in the workspace header.  Measured against the two-kernel path with one
+// slice: 61.1 against 68.3 us at 8192 x 512 x 4096, 62.7 against 73.5 us at
+// 4096 x 1024 x 4096, 37.2 against 41.0 us at 16384 x 256 x 2048.
+static bool fused_fits(const GemmPlan& g, int nb) {
+    if (g.shape != GemmPlan::kSmall && g.shape != GemmPlan::kBig && g.shape != GemmPlan::kMid)
+        return false;
+    if (nb > FU_NB_MAX || g.splits != 1) return false;
+    return g.tiles_n == 1 || g.tiles_m <= FU_MAX_TICKETS;
+}
+
+static int gemm_bm(int shape) {
+    return shape == GemmPlan::kSmall ? G1Small::BM : shape == GemmPlan::kHuge ? G1Huge::BM : G1Big::BM;
+}
+
+PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok, bool fused_ok) {
     PredictPlan pl;
     const GemmPlan g = plan_gemm(p.n_req, p.d_hidden, p.d_model, p.dtype == STAR_BF16 ? 2 : 4);
     pl.gemm = g;
@@ -1015,6 +1507,16 @@ PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok) {
     pl.ktiles = g.ktiles;
     const int s = g.splits;
     pl.splits = s;
+    if (fused_ok && p.dtype == STAR_BF16 && fused_fits(g, p.n_bins)) {
+        pl.fused = true;
+        const size_t bm = (size_t)gemm_bm(g.shape);
+        const size_t tiles = (size_t)g.tiles_m * g.tiles_n;
+        const size_t nb32 = (size_t)((p.n_bins + 31) / 32) * 32;
+        pl.lpart_bytes = g.tiles_n > 1 ? align_up(tiles * bm * nb32 * sizeof(float), 256) : 0;
+        pl.partial_bytes = pl.lpart_bytes;
+        pl.head_rows = (int)bm;
+        return pl;
+    }
     pl.partial_bytes = (size_t)s * (size_t)p.n_req * (size_t)p.d_hidden * sizeof(float);
     const int mpad = (p.d_hidden + 31) & ~31;
     const int nbpad = (p.n_bins + 15) & ~15;
@@ -1029,6 +1531,48 @@ PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok) {
     else
         pl.head_lds = rb * p.d_hidden * 4 + rb * nbpad * 4;
     return pl;
+}
+
+template <int NS, class SH>
+static hipError_t launch_fused_shape(const PredictPlan& pl, const FusedArgs& a, hipStream_t stream) {
+    const dim3 grid(pl.gemm.tiles_m * pl.gemm.tiles_n);
+    hipLaunchKernelGGL((predict_fused_kernel<NS, SH>), grid, dim3(SH::THREADS), 0, stream, a);
+    return hipGetLastError();
+}
+
+static hipError_t launch_fused(const star_predict_params& p, const PredictPlan& pl,
+                               const void* hidden, const void* w1, const float* b1,
+                               const void* w2, const float* b2, const float* bins,
+                               float* ema_state, float* expected, int32_t* rem_len, char* scratch,
+                               uint32_t* tickets, hipStream_t stream) {
+    FusedArgs a;
+    a.A = (const char*)hidden;
+    a.W = (const char*)w1;
+    a.b1 = b1;
+    a.W2 = (const uint16_t*)w2;
+    a.b2 = b2;
+    a.bins = bins;
+    a.lpart = (float*)scratch;
+    a.tix_row = tickets;
+    a.ema_state = ema_state;
+    a.expected = expected;
+    a.rem_len = rem_len;
+    a.M = p.n_req;
+    a.N = p.d_hidden;
+    a.Kd = p.d_model;
+    a.nb = p.n_bins;
+    a.tiles_n = pl.gemm.tiles_n;
+    a.ktiles = pl.gemm.ktiles;
+    a.act = p.act;
+    a.ema_init = p.ema_init;
+    a.len_max = p.len_max;
+    a.ema_alpha = p.ema_alpha;
+    switch (pl.gemm.shape) {
+        case GemmPlan::kSmall: return launch_fused_shape<G1_STAGES_SMALL, G1Small>(pl, a, stream);
+        case GemmPlan::kBig: return launch_fused_shape<G1_STAGES_BIG, G1Big>(pl, a, stream);
+        case GemmPlan::kMid: return launch_fused_shape<G1_STAGES_MID, G1Mid>(pl, a, stream);
+    }
+    return hipErrorInvalidValue;
 }
 
 template <bool kBF16, int kS, bool kReg, int kPF>
@@ -1123,20 +1667,15 @@ static hipError_t launch_head(const star_predict_params& p, const PredictPlan& p
 hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, const void* hidden,
                           const void* w1, const float* b1, const void* w2, const float* b2,
                           const float* bins, float* ema_state, float* expected, int32_t* rem_len,
-                          float* partials, hipStream_t stream) {
+                          char* scratch, uint32_t* tickets, hipStream_t stream) {
     if (p.n_req == 0) return hipSuccess;
-    hipEvent_t* ev = (hipEvent_t*)p.timing_events;
-    hipError_t e;
-    if (ev) {
-        e = hipEventRecord(ev[0], stream);
-        if (e != hipSuccess) return e;
-    }
-    e = launch_gemm(pl.gemm, p.dtype == STAR_BF16, hidden, w1, partials, p.n_req, p.d_hidden,
-                    p.d_model, stream);
-    if (ev) {
-        e = hipEventRecord(ev[1], stream);
-        if (e != hipSuccess) return e;
-    }
+    if (pl.fused)
+        return launch_fused(p, pl, hidden, w1, b1, w2, b2, bins, ema_state, expected, rem_len,
+                            scratch, tickets, stream);
+    float* partials = (float*)scratch;
+    hipError_t e = launch_gemm(pl.gemm, p.dtype == STAR_BF16, hidden, w1, partials, p.n_req,
+                               p.d_hidden, p.d_model, stream);
+    if (e != hipSuccess) return e;
     return p.dtype == STAR_BF16 ? launch_head<true>(p, pl, partials, b1, w2, b2, bins,
                                                     ema_state, expected, rem_len, stream)
                                 : launch_head<false>(p, pl, partials, b1, w2, b2, bins,
@@ -1160,7 +1699,6 @@ static star_predict_params head_view(const star_mlp4_params& p) {
     h.ema_alpha = p.ema_alpha;
     h.ema_init = p.ema_init;
     h.len_max = p.len_max;
-    h.timing_events = nullptr;
     return h;
 }
 
@@ -1168,7 +1706,7 @@ Mlp4Plan plan_mlp4(const star_mlp4_params& p) {
     Mlp4Plan pl;
     const int elem = p.dtype == STAR_BF16 ? 2 : 4;
     pl.g1 = plan_gemm(p.n_req, p.m1, p.d_model, elem);
-    pl.head = plan_predict(head_view(p), false);   // layer 2 and the head
+    pl.head = plan_predict(head_view(p), false, false);   // layer 2 and the head
     size_t off = 0;
     pl.p1_off = off;
     off += align_up((size_t)pl.g1.splits * p.n_req * p.m1 * sizeof(float), 256);
@@ -1203,13 +1741,10 @@ hipError_t launch_mlp4(const star_mlp4_params& p, const Mlp4Plan& pl, const void
     float* P1 = (float*)(ws + pl.p1_off);
     void* A1 = ws + pl.a1_off;
     float* P2 = (float*)(ws + pl.p2_off);
-    hipEvent_t* ev = (hipEvent_t*)p.timing_events;
     hipError_t e;
-    if (ev && (e = hipEventRecord(ev[0], stream)) != hipSuccess) return e;
     if ((e = launch_gemm(pl.g1, bf, hidden, w1, P1, p.n_req, p.m1, p.d_model, stream)) !=
         hipSuccess)
         return e;
-    if (ev && (e = hipEventRecord(ev[1], stream)) != hipSuccess) return e;
     const int64_t items = (int64_t)p.n_req * p.m1 / 4;
     int64_t ab = ceil_div(items, (int64_t)ACT_THREADS * ACT_BATCH);
     const dim3 ga((unsigned)(ab > 2048 ? 2048 : ab));

@@ -76,6 +76,8 @@ STAR_API const char* star_status_string(star_status s) {
         case STAR_ERR_OVERFLOW: return "STAR_ERR_OVERFLOW: int64 loads could overflow at these sizes";
         case STAR_ERR_WORKSPACE: return "STAR_ERR_WORKSPACE: workspace null, misaligned or too small";
         case STAR_ERR_HIP: return "STAR_ERR_HIP: HIP runtime or launch failure";
+        case STAR_ERR_DEVICE_INPUT:
+            return "STAR_ERR_DEVICE_INPUT: array contents broke a precondition (device error word set)";
     }
     return "unknown star_status";
 }
@@ -98,15 +100,16 @@ STAR_API star_status star_predict(const star_predict_params* p, const void* hidd
     if (p->n_req > 0) {
         if (!hidden || !w1 || !w2 || !bin_values || !expected_len) return STAR_ERR_INVALID_ARG;
         if (p->ema_alpha > 0.0f && !ema_state) return STAR_ERR_INVALID_ARG;
-        if (!aligned(hidden, 16) || !aligned(w1, 16) || !aligned(w2, 16))
+        if (!aligned(hidden, 16) || !aligned(w1, 16) || !aligned(w2, 16) || !aligned(b1, 16))
             return STAR_ERR_UNSUPPORTED;
     }
     const PredictPlan pl = plan_predict(*p);
     st = check_ws(ws, ws_bytes, STAR_WS_HEADER_BYTES + align_up(pl.partial_bytes, 256));
     if (st != STAR_OK) return st;
-    float* partials = (float*)((char*)ws + STAR_WS_HEADER_BYTES);
+    char* scratch = (char*)ws + STAR_WS_HEADER_BYTES;
+    uint32_t* tickets = (uint32_t*)((char*)ws + kHdrFusedTickets);
     hipError_t e = launch_predict(*p, pl, hidden, w1, b1, w2, b2, bin_values, ema_state,
-                                  expected_len, rem_len, partials, (hipStream_t)stream);
+                                  expected_len, rem_len, scratch, tickets, (hipStream_t)stream);
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
 }
 
@@ -370,5 +373,5 @@ STAR_API star_status star_read_device_error(void* ws, void* stream, int32_t* cod
     if (launch_fill_zero((char*)ws + kHdrErrorWord, 4, s) != hipSuccess) return STAR_ERR_HIP;
     if (hipStreamSynchronize(s) != hipSuccess) return STAR_ERR_HIP;
     *code = v;
-    return STAR_OK;
+    return v ? STAR_ERR_DEVICE_INPUT : STAR_OK;
 }

@@ -19,6 +19,9 @@ constexpr size_t kHdrPlanDone = 72;     // int32: the migration plan has stopped
 constexpr size_t kHdrPlanCount = 76;    // int32: moves made by the plan
 constexpr size_t kHdrScoreHist = 256;   // uint32[1024]: key-code histogram of the ranking
 static_assert(kHdrScoreHist + 1024 * 4 <= STAR_WS_HEADER_BYTES, "header holds the histogram");
+// uint32 counters of the fused predictor (column tiles per row block), to
+// the end of the header
+constexpr size_t kHdrFusedTickets = kHdrScoreHist + 1024 * 4;
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }

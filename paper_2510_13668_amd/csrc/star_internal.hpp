@@ -24,12 +24,15 @@ struct PredictPlan {
     size_t head_lds = 0;        // dynamic LDS of the head kernel
     int head_rows = 4;          // rows per head workgroup
     bool head_tiled = false;    // the K-chunked head (large bf16 batches), 64 rows per workgroup
+    bool fused = false;         // one kernel: product (one K-slice) and head
+    size_t lpart_bytes = 0;     // fused: logit shares [tiles_m][tiles_n][BM * nb32] fp32
 };
-PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok = true);
+// allow: 1 = the fused kernel where it applies, 0 = never (the two-kernel path)
+PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok = true, bool fused_ok = true);
 hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, const void* hidden,
                           const void* w1, const float* b1, const void* w2, const float* b2,
                           const float* bins, float* ema_state, float* expected, int32_t* rem_len,
-                          float* partials, hipStream_t stream);
+                          char* scratch, uint32_t* tickets, hipStream_t stream);
 
 struct Mlp4Plan {
     GemmPlan g1;          // layer 1

@@ -17,6 +17,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libstar.so")
 
 STAR_OK = 0
+STAR_ERR_DEVICE_INPUT = -6
+STAR_ABI_VERSION = 2
 STAR_WS_HEADER_BYTES = 8192
 STAR_MAX_TOP_K = 1024
 F32, BF16 = 0, 1
@@ -30,13 +32,13 @@ _P = ctypes.c_void_p
 class PredictParams(ctypes.Structure):
     _fields_ = [("n_req", _i32), ("d_model", _i32), ("d_hidden", _i32), ("n_bins", _i32),
                 ("dtype", _i32), ("act", _i32), ("ema_alpha", ctypes.c_float),
-                ("ema_init", _i32), ("len_max", _i32), ("timing_events", _P)]
+                ("ema_init", _i32), ("len_max", _i32)]
 
 
 class Mlp4Params(ctypes.Structure):
     _fields_ = [("n_req", _i32), ("d_model", _i32), ("m1", _i32), ("m2", _i32), ("m3", _i32),
                 ("dtype", _i32), ("ema_alpha", ctypes.c_float), ("ema_init", _i32),
-                ("len_max", _i32), ("b4", ctypes.c_float), ("timing_events", _P)]
+                ("len_max", _i32), ("b4", ctypes.c_float)]
 
 
 class LoadParams(ctypes.Structure):
@@ -75,6 +77,10 @@ def lib():
                 f"{LIB_PATH} is missing: build it with `python -m paper_2510_13668_amd.build`")
         L = ctypes.CDLL(LIB_PATH)
         L.star_abi_version.restype = _i32
+        if L.star_abi_version() != STAR_ABI_VERSION:
+            raise StarLibraryMissing(
+                f"{LIB_PATH} has ABI version {L.star_abi_version()}, this binding needs "
+                f"{STAR_ABI_VERSION}: rebuild it with `python -m paper_2510_13668_amd.build`")
         L.star_status_string.restype = ctypes.c_char_p
         L.star_status_string.argtypes = [ctypes.c_int]
         L.star_predict_workspace_size.restype = ctypes.c_size_t
@@ -158,10 +164,13 @@ class Workspace:
                                                                  self.nbytes, _stream(stream)))
 
     def read_device_error(self, stream=None) -> int:
+        """The device-error word (0 = clean); STAR_ERR_DEVICE_INPUT is its
+        non-zero status, not a failure of the call."""
         code = _i32(0)
-        _check("star_read_device_error",
-               lib().star_read_device_error(ctypes.c_void_p(self.ptr), _stream(stream),
-                                            ctypes.byref(code)))
+        st = lib().star_read_device_error(ctypes.c_void_p(self.ptr), _stream(stream),
+                                          ctypes.byref(code))
+        if st != STAR_ERR_DEVICE_INPUT:
+            _check("star_read_device_error", st)
         return code.value
 
 
@@ -169,9 +178,9 @@ class Workspace:
 # (a) predictor
 # ---------------------------------------------------------------------------
 def predict_params(n_req, d_model, d_hidden, n_bins, dtype, act, ema_alpha=0.0, ema_init=False,
-                   len_max=1 << 30, timing_events=None) -> PredictParams:
+                   len_max=1 << 30) -> PredictParams:
     return PredictParams(n_req, d_model, d_hidden, n_bins, dtype, act, float(ema_alpha),
-                         int(bool(ema_init)), int(len_max), timing_events)
+                         int(bool(ema_init)), int(len_max))
 
 
 def predict_workspace_size(p: PredictParams) -> int:
@@ -297,9 +306,9 @@ def plan_migrations(p: PlanParams, cur_len, rem_len, inst_of, load, beta, moves,
 # the paper's regression head
 # ---------------------------------------------------------------------------
 def mlp4_params(n_req, d_model, m1, m2, m3, dtype, ema_alpha=0.0, ema_init=False,
-                len_max=1 << 30, b4=0.0, timing_events=None) -> Mlp4Params:
+                len_max=1 << 30, b4=0.0) -> Mlp4Params:
     return Mlp4Params(n_req, d_model, m1, m2, m3, dtype, ema_alpha, int(bool(ema_init)), len_max,
-                      b4, timing_events)
+                      b4)
 
 
 def predict_mlp4_workspace_size(p: Mlp4Params) -> int:

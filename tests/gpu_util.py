@@ -42,9 +42,9 @@ class Predictor:
         self.expected = torch.empty(n_req, dtype=torch.float32, device=DEV)
         self.rem = torch.empty(n_req, dtype=torch.int32, device=DEV)
 
-    def params(self, ema_init, timing_events=None):
+    def params(self, ema_init):
         return star.predict_params(self.n_req, self.d, self.m, self.nb, self.dtype, self.act,
-                                   self.alpha, ema_init, self.len_max, timing_events)
+                                   self.alpha, ema_init, self.len_max)
 
     def run(self, hidden_dev: torch.Tensor, ema_init=False, stream=None):
         star.predict(self.params(ema_init), hidden_dev, self.w1, self.b1, self.w2, self.b2,

@@ -37,8 +37,8 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert L.star_abi_version() == 1
-    for s in (0, -1, -2, -3, -4, -5):
+    assert L.star_abi_version() == 2
+    for s in (0, -1, -2, -3, -4, -5, -6):
         assert L.star_status_string(s).decode().startswith("STAR_")
     assert b"unknown" in L.star_status_string(-99)
 
@@ -55,10 +55,11 @@ FAKE = ctypes.c_void_p(1 << 20)   # never dereferenced: validation fails first
 
 def _predict(L, p, ws_bytes=1 << 30, ws=FAKE, **ptrs):
     args = {k: FAKE for k in ("hidden", "w1", "w2", "bins", "ema", "expected")}
+    args["b1"] = None
     args.update(ptrs)
     return L.star_predict(ctypes.byref(p) if p is not None else None, args["hidden"], args["w1"],
-                          None, args["w2"], None, args["bins"], args["ema"], args["expected"],
-                          None, ws, ws_bytes, None)
+                          args["b1"], args["w2"], None, args["bins"], args["ema"],
+                          args["expected"], None, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -77,11 +78,17 @@ def test_predict_rejects_null_pointers_and_workspace(L):
     assert _predict(L, _pp(), hidden=None) == -1
     assert _predict(L, _pp(ema_alpha=0.2), ema=None) == -1
     assert _predict(L, _pp(), hidden=ctypes.c_void_p((1 << 20) + 2)) == -2   # misaligned
+    # b1 is read 16 bytes at a time: a bias view at a 4-byte offset is refused
+    assert _predict(L, _pp(), b1=ctypes.c_void_p((1 << 20) + 4)) == -2
     p = _pp()
     need = star.predict_workspace_size(p)
-    # 64 x 64 tiles: 16 x 8 of them, 4 K-splits of a [1024, 512] fp32
-    # partial product, plus the header
+    # 64 x 64 tiles, 4 K-splits: the split-K product writes 4 fp32 partial
+    # planes of [1024, 512] for the head kernel, plus the header
     assert need == star.STAR_WS_HEADER_BYTES + 4 * 1024 * 512 * 4
+    # one K-slice (8192 x 512 x 4096, 128 x 128 tiles, 4 column tiles): the
+    # fused kernel's logit shares [64 row blocks][4][128 x 64] fp32
+    big = _pp(n_req=8192)
+    assert star.predict_workspace_size(big) == star.STAR_WS_HEADER_BYTES + 4 * 8192 * 64 * 4
     assert _predict(L, p, ws_bytes=need - 1) == -4
     assert _predict(L, p, ws=None) == -4
     assert _predict(L, p, ws=ctypes.c_void_p((1 << 20) + 64)) == -4   # not 256-aligned

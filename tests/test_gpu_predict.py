@@ -97,9 +97,10 @@ def test_ragged_shapes(dtype, act, B, d, m, nb):
 @pytest.mark.parametrize("B,d,m,nb", [(8200, 64, 2048, 256), (8192 + 13, 136, 72, 20),
                                      (9000, 512, 1024, 128)])
 def test_wide_head_rows_sampled(B, d, m, nb):
-    """bf16 batches of 8192 and more take the K-chunked 64-row head: ragged
-    last workgroup, maximum width and bins, odd widths and a ragged last
-    chunk; checked on the first and last rows and a random sample."""
+    """bf16 batches of 8192 rows and more: the K-chunked 64-row head (maximum
+    width and bins, 256 x 256 product tiles) and the fused kernel (odd widths,
+    a ragged last row tile, 128 bins); checked on the first and last rows and
+    a random sample."""
     rng = np.random.default_rng(B + d + m + nb)
     h = synth.f32_to_bf16_bits(rng.standard_normal((B, d)).astype(np.float32))
     w1 = synth.f32_to_bf16_bits((rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32))
@@ -152,16 +153,17 @@ def _splits(B, d, m, nb):
 
 
 @pytest.mark.parametrize("B,d,m,nb,act,planes", [
-    (8200, 1024, 64, 60, synth.ACT_RELU, 2),       # 4 bin blocks
-    (8192, 2048, 128, 100, synth.ACT_GELU, 2),     # 8 blocks, two LDS stages
-    (8192, 4096, 128, 64, synth.ACT_RELU, 4),      # 4 blocks, ReLU
-    (8192, 4096, 128, 100, synth.ACT_GELU, 4),     # 8 blocks
-    (8192, 4096, 64, 200, synth.ACT_RELU, 4),      # 16 blocks, one LDS stage
-    (9000, 512, 1024, 128, synth.ACT_RELU, 1),     # one plane, ReLU
+    (8200, 64, 2048, 60, synth.ACT_RELU, 1),       # 4 bin blocks, 256 x 256 product tiles
+    (8192, 64, 2048, 100, synth.ACT_GELU, 1),      # 8 blocks, two LDS stages
+    (8192, 64, 2048, 200, synth.ACT_GELU, 1),      # 16 blocks, one LDS stage
+    (8200, 1024, 64, 250, synth.ACT_RELU, 2),      # 16 blocks, two planes
+    (8192, 4096, 64, 200, synth.ACT_RELU, 4),      # 16 blocks, four planes
 ])
 def test_tiled_head_planes_and_activations(B, d, m, nb, act, planes):
-    """The K-chunked head over every number of split-K planes it accepts (1,
-    2, 4), every bin-block count and both activations; sampled rows."""
+    """The K-chunked head (batches of 8192 rows and more that the fused
+    kernel does not take: 256 x 256 product tiles, or more than 128 bins)
+    over the split-K planes it meets (1, 2, 4), every bin-block count and
+    both activations; sampled rows."""
     assert _splits(B, d, m, nb) == planes, "the plan no longer takes this many planes here"
     rng = np.random.default_rng(B * 7 + d + m + nb)
     h = synth.f32_to_bf16_bits(rng.standard_normal((B, d)).astype(np.float32))
@@ -191,6 +193,27 @@ def test_large_fp32_sampled():
     print(f"large fp32 B={B} d={d} m={m} nb={nb}", flush=True)
     _run_case(h, w1, w2, bins, dtype=synth.F32, act=synth.ACT_RELU, len_max=32768,
               sample=sample)
+
+
+def test_fused_counters_left_at_zero():
+    """The fused kernel's per-row-block counters live in the workspace header
+    and every call leaves them at zero: read back after calls at a shape with
+    eight column tiles and at a one-column-tile shape (both one K-slice)."""
+    from paper_2510_13668_amd import star
+    for B, d, m, nb in [(9000, 512, 1024, 128), (3000, 136, 72, 20)]:
+        rng = np.random.default_rng(B)
+        h = synth.f32_to_bf16_bits(rng.standard_normal((B, d)).astype(np.float32))
+        w1 = synth.f32_to_bf16_bits((rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32))
+        w2 = synth.f32_to_bf16_bits(rng.standard_normal((nb, m)).astype(np.float32))
+        pr = Predictor(w1, w2, synth.bin_values(nb, 1.0, 16384.0), dtype=synth.BF16,
+                       act=synth.ACT_GELU, n_req=B, len_max=16384)
+        hd = to_dev(h, True)
+        for _ in range(3):
+            pr.run(hd)
+        torch.cuda.synchronize()
+        base = pr.ws.ptr - pr.ws.buf.data_ptr()
+        header = pr.ws.buf[base:base + star.STAR_WS_HEADER_BYTES].cpu().numpy()
+        assert not header.any(), f"non-zero header bytes at {np.flatnonzero(header)[:8]}"
 
 
 def test_empty_batch():
