@@ -55,8 +55,10 @@ typedef enum {
     STAR_ERR_OVERFLOW = -3,      /* sizes whose int64 loads could overflow */
     STAR_ERR_WORKSPACE = -4,     /* workspace null, misaligned or too small */
     STAR_ERR_HIP = -5,           /* a HIP runtime call or kernel launch failed */
-    STAR_ERR_DEVICE_INPUT = -6   /* star_read_device_error: array contents broke a precondition
+    STAR_ERR_DEVICE_INPUT = -6,  /* star_read_device_error: array contents broke a precondition
                                     (the device error word was non-zero) */
+    STAR_ERR_SCRATCH_LIMIT = -7  /* star_predict_noalloc: the call needs more scratch than
+                                    STAR_NOALLOC_SCRATCH_BYTES */
 } star_status;
 
 /* bits of the device-error word */
@@ -110,6 +112,28 @@ star_status star_predict(const star_predict_params* p, const void* hidden, const
                          const float* b1, const void* w2, const float* b2,
                          const float* bin_values, float* ema_state, float* expected_len,
                          int32_t* rem_len, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * (a) without allocation, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, results and kernels as star_predict, minus
+ * the workspace: the scratch (split-K partials or logit shares, and the
+ * fused kernel's counters) is a fixed array of STAR_NOALLOC_SCRATCH_BYTES in
+ * device memory, one per GPU, held until the process ends.  The call
+ * allocates and frees nothing; its first call on a GPU looks up the array's
+ * device address and clears its counters (one small kernel on `stream`).
+ * Calls on one GPU share that array, so they must not overlap (same stream,
+ * or synchronised); overlapping calls race.  Sizes whose scratch exceeds the
+ * array return STAR_ERR_SCRATCH_LIMIT before anything is launched (batches of
+ * 512 to 4096 rows at d = 4096-5120, m = 512 fit; 32768 rows at m = 1024 do
+ * not).
+ * ---------------------------------------------------------------------- */
+#define STAR_NOALLOC_SCRATCH_BYTES (32 << 20)
+
+star_status star_predict_noalloc(const star_predict_params* p, const void* hidden,
+                                 const void* w1, const float* b1, const void* w2,
+                                 const float* b2, const float* bin_values, float* ema_state,
+                                 float* expected_len, int32_t* rem_len, void* stream);
 
 /* ------------------------------------------------------------------------
  * (f3) The paper's regression head.

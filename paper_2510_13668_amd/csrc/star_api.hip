@@ -4,6 +4,9 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "star_common.hpp"
 #include "star_internal.hpp"
 
@@ -78,6 +81,9 @@ STAR_API const char* star_status_string(star_status s) {
         case STAR_ERR_HIP: return "STAR_ERR_HIP: HIP runtime or launch failure";
         case STAR_ERR_DEVICE_INPUT:
             return "STAR_ERR_DEVICE_INPUT: array contents broke a precondition (device error word set)";
+        case STAR_ERR_SCRATCH_LIMIT:
+            return "STAR_ERR_SCRATCH_LIMIT: the call needs more than the built-in scratch of the "
+                   "allocation-free entry point (STAR_NOALLOC_SCRATCH_BYTES)";
     }
     return "unknown star_status";
 }
@@ -110,6 +116,64 @@ STAR_API star_status star_predict(const star_predict_params* p, const void* hidd
     uint32_t* tickets = (uint32_t*)((char*)ws + kHdrFusedTickets);
     hipError_t e = launch_predict(*p, pl, hidden, w1, b1, w2, b2, bin_values, ema_state,
                                   expected_len, rem_len, scratch, tickets, (hipStream_t)stream);
+    return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// predictor without allocation: the scratch is a fixed array in device
+// memory, one copy per GPU (each GPU that runs it holds the array until the
+// process ends).  Its device address is looked up once per device, with that
+// device current; host code never uses the array's own name as a device
+// address.  Calls on one GPU share the array: they must not overlap.
+// ---------------------------------------------------------------------------
+__device__ __attribute__((aligned(256))) char scratch[STAR_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<char*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// The device address of `scratch` on the current device, or nullptr on a
+// HIP error.  The first call on a device also clears the header (the fused
+// predictor's counters start at zero; every call leaves them at zero).
+char* noalloc_scratch(hipStream_t stream) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    char* p = g_scratch[dev].load(std::memory_order_acquire);
+    if (p) return p;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (p) return p;
+    void* addr = nullptr;
+    if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || !addr) return nullptr;
+    if (launch_fill_zero(addr, STAR_WS_HEADER_BYTES, stream) != hipSuccess) return nullptr;
+    p = (char*)addr;
+    g_scratch[dev].store(p, std::memory_order_release);
+    return p;
+}
+}  // namespace
+
+STAR_API star_status star_predict_noalloc(const star_predict_params* p, const void* hidden,
+                                          const void* w1, const float* b1, const void* w2,
+                                          const float* b2, const float* bin_values,
+                                          float* ema_state, float* expected_len,
+                                          int32_t* rem_len, void* stream) {
+    star_status st = check_predict_params(p);
+    if (st != STAR_OK) return st;
+    if (p->n_req > 0) {
+        if (!hidden || !w1 || !w2 || !bin_values || !expected_len) return STAR_ERR_INVALID_ARG;
+        if (p->ema_alpha > 0.0f && !ema_state) return STAR_ERR_INVALID_ARG;
+        if (!aligned(hidden, 16) || !aligned(w1, 16) || !aligned(w2, 16) || !aligned(b1, 16))
+            return STAR_ERR_UNSUPPORTED;
+    }
+    const PredictPlan pl = plan_predict(*p);
+    if (STAR_WS_HEADER_BYTES + align_up(pl.partial_bytes, 256) > (size_t)STAR_NOALLOC_SCRATCH_BYTES)
+        return STAR_ERR_SCRATCH_LIMIT;
+    char* ws = noalloc_scratch((hipStream_t)stream);
+    if (!ws) return STAR_ERR_HIP;
+    hipError_t e = launch_predict(*p, pl, hidden, w1, b1, w2, b2, bin_values, ema_state,
+                                  expected_len, rem_len, ws + STAR_WS_HEADER_BYTES,
+                                  (uint32_t*)(ws + kHdrFusedTickets), (hipStream_t)stream);
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
 }
 

@@ -18,6 +18,8 @@ LIB_PATH = os.path.join(_HERE, "libstar.so")
 
 STAR_OK = 0
 STAR_ERR_DEVICE_INPUT = -6
+STAR_ERR_SCRATCH_LIMIT = -7
+STAR_NOALLOC_SCRATCH_BYTES = 32 << 20
 STAR_ABI_VERSION = 2
 STAR_WS_HEADER_BYTES = 8192
 STAR_MAX_TOP_K = 1024
@@ -91,6 +93,7 @@ def lib():
         L.star_score_workspace_size.argtypes = [ctypes.POINTER(ScoreParams)]
         L.star_predict.restype = ctypes.c_int
         L.star_predict.argtypes = [ctypes.POINTER(PredictParams)] + [_P] * 10 + [ctypes.c_size_t, _P]
+        L.star_predict_noalloc.argtypes = [ctypes.POINTER(PredictParams)] + [_P] * 10
         L.star_project_load.restype = ctypes.c_int
         L.star_project_load.argtypes = [ctypes.POINTER(LoadParams)] + [_P] * 5 + [ctypes.c_size_t, _P]
         L.star_score_migrations.restype = ctypes.c_int
@@ -194,6 +197,15 @@ def predict(p: PredictParams, hidden, w1, b1, w2, b2, bin_values, ema_state, exp
         ctypes.byref(p), _ptr(hidden), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
         _ptr(bin_values), _ptr(ema_state), _ptr(expected_len), _ptr(rem_len),
         ctypes.c_void_p(ws.ptr), ws.nbytes, _stream(stream)))
+
+
+def predict_noalloc(p: PredictParams, hidden, w1, b1, w2, b2, bin_values, ema_state,
+                    expected_len, rem_len, stream=None):
+    """star_predict without a workspace (the library's fixed device scratch)."""
+    _dev(hidden, w1, b1, w2, b2, bin_values, ema_state, expected_len, rem_len)
+    _check("star_predict_noalloc", lib().star_predict_noalloc(
+        ctypes.byref(p), _ptr(hidden), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
+        _ptr(bin_values), _ptr(ema_state), _ptr(expected_len), _ptr(rem_len), _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

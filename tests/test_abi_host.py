@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(L):
 
 def test_abi_version_and_status_strings(L):
     assert L.star_abi_version() == 2
-    for s in (0, -1, -2, -3, -4, -5, -6):
+    for s in (0, -1, -2, -3, -4, -5, -6, -7):
         assert L.star_status_string(s).decode().startswith("STAR_")
     assert b"unknown" in L.star_status_string(-99)
 
@@ -92,6 +92,25 @@ def test_predict_rejects_null_pointers_and_workspace(L):
     assert _predict(L, p, ws_bytes=need - 1) == -4
     assert _predict(L, p, ws=None) == -4
     assert _predict(L, p, ws=ctypes.c_void_p((1 << 20) + 64)) == -4   # not 256-aligned
+
+
+def test_predict_noalloc_validation_and_scratch_limit(L):
+    """The allocation-free predictor validates like star_predict and refuses,
+    before launching anything, sizes whose scratch exceeds its fixed array
+    (32768 rows at m = 1024 need 128 MiB of split-K partials)."""
+    def call(p, **ptrs):
+        a = {k: FAKE for k in ("hidden", "w1", "w2", "bins", "ema", "expected")}
+        a.update(ptrs)
+        return L.star_predict_noalloc(ctypes.byref(p) if p is not None else None, a["hidden"],
+                                      a["w1"], None, a["w2"], None, a["bins"], a["ema"],
+                                      a["expected"], None, None)
+    assert call(None) == -1
+    assert call(_pp(n_bins=0)) == -1
+    assert call(_pp(), hidden=None) == -1
+    assert call(_pp(), w1=ctypes.c_void_p((1 << 20) + 8)) == -2
+    big = _pp(n_req=32768, d_model=8192, d_hidden=1024, n_bins=128)
+    assert call(big) == star.STAR_ERR_SCRATCH_LIMIT == -7
+    assert L.star_status_string(-7).decode().startswith("STAR_ERR_SCRATCH_LIMIT")
 
 
 def test_load_and_score_validation(L):
