@@ -27,6 +27,7 @@ namespace star {
 // ---------------------------------------------------------------------------
 constexpr int G1_KBYTES = 128;                 // bytes of K per LDS row
 constexpr int G1_ROW = G1_KBYTES + 16;         // padded LDS row (bytes)
+constexpr int G1_CPR = G1_KBYTES / 16;         // 16-byte chunks per row
 // K-tiles of global loads in flight ahead of the multiply: three for the
 // 128 x 128 shape (one 8-wave workgroup per CU), two for the 64 x 64 one,
 // which runs two workgroups per CU that share the CU's load path (measured:
@@ -39,9 +40,9 @@ constexpr int G1_WIDE_MIN_TILES = 1024;   // 128 x 128 tiles from which G1Wide r
 constexpr int G1_STAGES_HUGE = 1;
 constexpr int G1_HUGE_MIN_TILES = 256;    // 256 x 256 tiles (no split) from which G1Huge is used
 
-template <int kElemBytes> struct G1Elem;
-template <> struct G1Elem<2> { static constexpr int BK = 64; };   // bf16
-template <> struct G1Elem<4> { static constexpr int BK = 32; };   // fp32
+template <int kElemBytes> struct G1Elem {
+    static constexpr int BK = G1_KBYTES / kElemBytes;   // K elements per K-tile
+};
 
 // Map blockIdx to a logical tile index so that consecutive logical indices
 // run on the same XCD (workgroups are dealt round-robin over the 8 XCDs):
@@ -108,8 +109,8 @@ struct G1Ctx {
 __device__ __forceinline__ uint4 g1_load(const G1Ctx& c, const char* base, int rows, int row0,
                                          int p, int64_t kb) {
     const int ch = c.tid + p * c.threads;
-    const int row = row0 + (ch >> 3);
-    const int64_t off = kb + (ch & 7) * 16;
+    const int row = row0 + ch / G1_CPR;
+    const int64_t off = kb + (ch % G1_CPR) * 16;
     const int64_t ko = off < c.row_bytes ? off : 0;
     return *(const uint4*)(base + (int64_t)(row < rows ? row : rows - 1) * c.row_bytes + ko);
 }
@@ -127,8 +128,8 @@ __device__ __forceinline__ void g1_load_stage(const G1Ctx& c, int kt, G1Stage<SH
 __device__ __forceinline__ void g1_store_chunk(const G1Ctx& c, char* l, int p, int64_t kb,
                                                int row0, int rows, uint4 v) {
     const int ch = c.tid + p * c.threads;
-    const int row = ch >> 3;
-    const int cb = (ch & 7) * 16;
+    const int row = ch / G1_CPR;
+    const int cb = (ch % G1_CPR) * 16;
     // bitwise masks, not a select of uint4 structs (which would go through memory)
     const uint32_t m = (kb + cb < c.row_bytes && row0 + row < rows) ? 0xFFFFFFFFu : 0u;
     *(uint4*)(l + row * G1_ROW + cb) = make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
@@ -335,14 +336,14 @@ __device__ __forceinline__ void g1_mainloop_interior(const G1Ctx& c, const G1Wor
 #pragma unroll
     for (int p = 0; p < SH::CA; ++p) {
         const int ch = c.tid + p * c.threads;
-        f.ga[p] = (uint32_t)((c.tm * SH::BM + (ch >> 3)) * c.row_bytes + (ch & 7) * 16);
-        f.la[p] = (uint32_t)((ch >> 3) * G1_ROW + (ch & 7) * 16);
+        f.ga[p] = (uint32_t)((c.tm * SH::BM + ch / G1_CPR) * c.row_bytes + (ch % G1_CPR) * 16);
+        f.la[p] = (uint32_t)((ch / G1_CPR) * G1_ROW + (ch % G1_CPR) * 16);
     }
 #pragma unroll
     for (int p = 0; p < SH::CB; ++p) {
         const int ch = c.tid + p * c.threads;
-        f.gb[p] = (uint32_t)((c.tn * SH::BN + (ch >> 3)) * c.row_bytes + (ch & 7) * 16);
-        f.lb[p] = (uint32_t)(SH::LDS_A + (ch >> 3) * G1_ROW + (ch & 7) * 16);
+        f.gb[p] = (uint32_t)((c.tn * SH::BN + ch / G1_CPR) * c.row_bytes + (ch % G1_CPR) * 16);
+        f.lb[p] = (uint32_t)(SH::LDS_A + (ch / G1_CPR) * G1_ROW + (ch % G1_CPR) * 16);
     }
     const int nk = w.nk, kt0 = w.kt0;
     if (nk > 0) {
