@@ -76,8 +76,9 @@ def _parse():
                          "4-layer regression head; sim: the event-driven simulation; configs: "
                          "per-call times at every workload's shape")
     ap.add_argument("--moves", type=int, default=16, help="max_moves of --path plan")
-    ap.add_argument("--workload", default="rebalance_scan",
-                    help="workload of --path variance")
+    ap.add_argument("--workload", default=None,
+                    help="workload of --path variance / plan (default rebalance_scan) or the "
+                         "one workload --path configs measures (default: all five)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device-to-device copy of known size (the "
                          "reference for scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -291,7 +292,7 @@ def bench_variance(args):
     from paper_2510_13668_amd import star, synth
 
     dev = "cuda"
-    wl = synth.WORKLOADS[args.workload]
+    wl = synth.WORKLOADS[args.workload or "rebalance_scan"]
     N, n, b, K = wl.n_req, wl.n_inst, wl.bucket, wl.n_buckets
     cur_h, rem_h, inst_h = variance_inputs(wl)
     beta_h = synth.bucket_weights(K)
@@ -423,7 +424,7 @@ def bench_plan(args):
     from paper_2510_13668_amd import star, synth
 
     dev = "cuda"
-    wl = synth.WORKLOADS[args.workload]
+    wl = synth.WORKLOADS[args.workload or "rebalance_scan"]
     N, n, b, K = wl.n_req, wl.n_inst, wl.bucket, wl.n_buckets
     M = args.moves
     x = synth.make_inputs(wl, steps=1, n_req=1)
@@ -634,7 +635,7 @@ def bench_configs(args):
     stream = torch.cuda.Stream()
     he = HipEvents()
     rows = []
-    for name in synth.WORKLOAD_ORDER:
+    for name in ([args.workload] if args.workload else synth.WORKLOAD_ORDER):
         wl = synth.WORKLOADS[name]
         x = synth.make_inputs(wl, steps=1)
         N, d, m, nb = wl.n_req, wl.d_model, wl.d_hidden, wl.n_bins

@@ -1355,6 +1355,179 @@ __device__ __forceinline__ int select_best_by_code(const TopkArgs& a, int ib1, S
     return select_gathered<TK_RJ1>(a, g, ib1, sh, cl, base, ws_s, ws_i, smin, smax_w);
 }
 
+// Counting sort of the pruned top-k: up to TK_SORT_CAP keys placed in LDS by
+// their codes (sh.hist holds each code's offset, sh.fill its count), then
+// ranked among the keys that share their code.
+constexpr int TK_SORT_CAP = TK_THREADS;
+constexpr int TK_CODE_V = 4;                            // 16-byte code reads per thread
+constexpr int TK_CODE_REG = TK_CODE_V * 8 * TK_THREADS; // best-key codes held in registers
+struct SortLds {
+    int64_t s[TK_SORT_CAP];
+    uint32_t i[TK_SORT_CAP];
+    uint16_t c[TK_SORT_CAP];
+};
+
+// Slot t's place in key order: its code's offset plus the number of keys of
+// the same code below it.
+__device__ __forceinline__ int sorted_pos(const SelShared<TK_THREADS>& sh, const SortLds& sl, int t,
+                                          int64_t s, uint32_t i) {
+    const int c = sl.c[t];
+    const int lo = sh.hist[c], hi = lo + sh.fill[c];
+    int rank = 0;
+    for (int j = lo; j < hi; ++j) rank += key_less(sl.s[j], sl.i[j], s, i) ? 1 : 0;
+    return lo + rank;
+}
+
+// Code u (0..7) of eight consecutive 2-byte codes read as one 16-byte word.
+__device__ __forceinline__ uint16_t code_of(const uint4& v, int u) {
+    const uint32_t w = u < 2 ? v.x : u < 4 ? v.y : u < 6 ? v.z : v.w;
+    return (uint16_t)((u & 1) ? w >> 16 : w & 0xFFFFu);
+}
+
+// Stage 1 with every best-key code in registers (N <= TK_CODE_REG): the code
+// histogram gives c*, the code of the k-th smallest best key; every best key
+// of code <= c* is placed by the counting sort, so (ws_s, ws_i)[0, nr) holds
+// the nr = min(k, keys) smallest best keys in key order and *smax_w the
+// largest of them.  Returns -1 (with the workgroup synchronised) when more
+// than TK_SORT_CAP best keys have codes <= c*.
+__device__ __forceinline__ int best_sorted(const TopkArgs& a, SelShared<TK_THREADS>& sh,
+                                           SortLds& sl, int64_t* ws_s, uint32_t* ws_i,
+                                           int64_t* smax_w) {
+    static_assert(RK_CODES == TK_THREADS && TK_SORT_CAP <= TK_THREADS, "one code per thread");
+    const int tid = threadIdx.x;
+    const uint4* cp = reinterpret_cast<const uint4*>(a.bcode);   // 256-byte aligned, padded
+    const int nv = (a.N + 7) >> 3;
+    uint4 cv[TK_CODE_V];
+#pragma unroll
+    for (int j = 0; j < TK_CODE_V; ++j) {
+        const int v = j * TK_THREADS + tid;
+        cv[j] = cp[v < nv ? v : 0];
+    }
+    sh.hist[tid] = 0;
+    sh.fill[tid] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < TK_CODE_V; ++j) {
+        const int v = j * TK_THREADS + tid;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const uint16_t c = code_of(cv[j], u);
+            if (v < nv && v * 8 + u < a.N && c != kNoCode) atomicAdd(&sh.hist[c], 1);
+        }
+    }
+    __syncthreads();
+    const int h = sh.hist[tid];
+    int total;
+    const int before = block_excl_i32<TK_THREADS>(h, sh, &total);
+    const bool all = total <= a.top_k;
+    if (all ? tid == RK_CODES - 1 : (before < a.top_k && before + h >= a.top_k)) {
+        sh.bcast[0] = tid;                                // c*
+        sh.bcast[1] = before + h;                         // best keys of code <= c*
+    }
+    sh.hist[tid] = before;                                // code offsets
+    __syncthreads();
+    const uint32_t cstar = (uint32_t)sh.bcast[0];
+    const int nle = sh.bcast[1];
+    if (nle > TK_SORT_CAP) {
+        __syncthreads();
+        return -1;
+    }
+#pragma unroll
+    for (int j = 0; j < TK_CODE_V; ++j) {
+        const int v = j * TK_THREADS + tid;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const uint16_t c = code_of(cv[j], u);
+            if (v < nv && v * 8 + u < a.N && c <= cstar) {
+                const int slot = sh.hist[c] + atomicAdd(&sh.fill[c], 1);
+                sl.i[slot] = (uint32_t)(v * 8 + u);
+                sl.c[slot] = c;
+            }
+        }
+    }
+    __syncthreads();
+    int64_t s = 0;
+    uint32_t r = 0;
+    if (tid < nle) {
+        r = sl.i[tid];
+        s = a.best_score[r];
+        sl.s[tid] = s;
+    }
+    __syncthreads();
+    const int nr = a.top_k < nle ? a.top_k : nle;
+    if (tid < nle) {
+        const int pos = sorted_pos(sh, sl, tid, s, r);
+        if (pos < nr) {
+            ws_s[pos] = s;
+            ws_i[pos] = r;
+        }
+    }
+    __syncthreads();
+    *smax_w = nr > 0 ? ws_s[nr - 1] : -1;
+    return nr;
+}
+
+// Stage 2 from registers: the k smallest migrations of the nr requests,
+// written in key order.  When nr = k, the k requests' best keys are k
+// distinct migrations, so the k-th smallest migration is at most the largest
+// of them (smax_w) and only migrations scored at most smax_w can win; when
+// nr < k every migration of the nr requests is a candidate.  The candidates
+// are counting-sorted on their codes.  Returns false, with nothing written
+// and the workgroup synchronised, when more than TK_SORT_CAP are candidates.
+template <int RJ>
+__device__ __forceinline__ bool pruned_sorted_write(const RegKeys<RJ>& keys, const TopkArgs& a,
+                                                    int nr, int64_t smax_w, int64_t base,
+                                                    SelShared<TK_THREADS>& sh, SortLds& sl) {
+    constexpr uint16_t kNone = 0xFFFF;
+    const int tid = threadIdx.x;
+    const int64_t thr = nr == a.top_k ? smax_w : kInfS;
+    sh.hist[tid] = 0;
+    sh.fill[tid] = 0;
+    __syncthreads();
+    uint16_t code[RJ];
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+        const bool cand = keys.s[j] != kInfS && keys.s[j] <= thr;
+        code[j] = cand ? (uint16_t)key_code((uint64_t)(keys.s[j] - base)) : kNone;
+        if (cand) atomicAdd(&sh.hist[code[j]], 1);
+    }
+    __syncthreads();
+    const int h = sh.hist[tid];
+    int P;
+    const int before = block_excl_i32<TK_THREADS>(h, sh, &P);
+    if (P > TK_SORT_CAP) return false;                    // block_excl_i32 ends synchronised
+    sh.hist[tid] = before;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+        if (code[j] != kNone) {
+            const int slot = sh.hist[code[j]] + atomicAdd(&sh.fill[code[j]], 1);
+            sl.s[slot] = keys.s[j];
+            sl.i[slot] = keys.i[j];
+            sl.c[slot] = code[j];
+        }
+    }
+    __syncthreads();
+    const int kk = a.top_k < P ? a.top_k : P;
+    if (tid < P) {
+        const int64_t s = sl.s[tid];
+        const uint32_t i = sl.i[tid];
+        const int pos = sorted_pos(sh, sl, tid, s, i);
+        if (pos < kk) {
+            const uint32_t r = fast_div(i, (uint32_t)a.n, a.magic_n);
+            a.topk_req[pos] = (int32_t)r;
+            a.topk_tgt[pos] = (int32_t)(i - r * (uint32_t)a.n);
+            a.topk_score[pos] = s;
+        }
+    }
+    for (int q = kk + tid; q < a.top_k; q += TK_THREADS) {
+        a.topk_req[q] = -1;
+        a.topk_tgt[q] = -1;
+        a.topk_score[q] = -1;
+    }
+    return true;
+}
+
 // How the pruned top-k finds the k requests with the smallest best keys: all
 // best keys in registers, or those the code histogram leaves.
 enum : int { kStage1Reg = 0, kStage1Code = 1 };
@@ -1371,6 +1544,7 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
     __shared__ int32_t rk_inst[STAR_MAX_TOP_K];
     __shared__ int gcount;
     __shared__ CodeLds cl;
+    __shared__ SortLds sl;
     int nr;
     int64_t smin, smax_w;
     const int64_t base = *a.bbase;
@@ -1380,7 +1554,10 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
         load_best(keys, a);
         nr = select_by_code<TK_RJ1>(keys, a.top_k, base, ib1, sh, cl, ws_s, ws_i, &smin, &smax_w);
     } else {
-        nr = select_best_by_code(a, ib1, sh, cl, ws_s, ws_i, &smin, &smax_w, &gcount);
+        // (the streamed stage 2 keeps the histogram-and-gather stage 1: the
+        // two together exceed the registers of a 1024-thread workgroup)
+        nr = kRJ2 > 0 && a.N <= TK_CODE_REG ? best_sorted(a, sh, sl, ws_s, ws_i, &smax_w) : -1;
+        if (nr < 0) nr = select_best_by_code(a, ib1, sh, cl, ws_s, ws_i, &smin, &smax_w, &gcount);
     }
     for (int q = threadIdx.x; q < nr; q += TK_THREADS) {
         const int r = (int)ws_i[q];
@@ -1394,6 +1571,7 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
     if constexpr (kRJ2 > 0) {
         RegKeys<kRJ2> keys;
         load_pruned(keys, a, rk, rk_inst, M);
+        if (pruned_sorted_write<kRJ2>(keys, a, nr, smax_w, base, sh, sl)) return;
         nw = select_by_code<kRJ2>(keys, a.top_k, base, ib2, sh, cl, ws_s, ws_i, &smin, &smax_w);
     } else {
         PrunedKeys pk{&a, rk, rk_inst, M};
