@@ -191,6 +191,11 @@ typedef struct {
     int32_t n_buckets;  /* K >= 1; b * K <= 2^30 */
 } star_load_params;
 
+/* The header, plus, for long request streams (n_req >= 8192, n_buckets <=
+ * 1024, n_inst <= 960), per-instance histograms of each request slice that
+ * the last workgroup of the instance sums; the request arrays are then read
+ * in 16-byte groups when all three are 16-byte aligned (other alignments
+ * take a kernel that needs no more than the header). */
 size_t star_project_load_workspace_size(const star_load_params* p);
 
 star_status star_project_load(const star_load_params* p, const int32_t* cur_len,
@@ -236,7 +241,10 @@ star_status star_score_migrations(const star_score_params* p, const int32_t* cur
  * share one workspace of star_project_and_score_workspace_size() bytes.
  * Rounds whose curves fit on-chip (and with at most 8192 requests) skip
  * the projection kernel: every scoring workgroup builds the curves itself
- * and one of them writes `load`; other sizes run the projection first.
+ * and one of them writes `load`; other sizes run the projection first, and
+ * where it takes request slices (see star_project_load_workspace_size) and
+ * the curves do not fit on-chip, it also writes the scoring's bucket-major
+ * curve terms, so no separate preparation pass runs.
  * ---------------------------------------------------------------------- */
 size_t star_project_and_score_workspace_size(const star_score_params* p);
 

@@ -1057,13 +1057,8 @@ __global__ __launch_bounds__(HD_THREADS) void head_tiled_kernel(
 // arrival order) and finishes its rows: b2, softmax over the bins, mean over
 // the bin values, EMA, round half to even, clamp.  z1 never leaves the chip.
 //
-// No cache maintenance: the shares are stored and loaded with the
-// device-coherent cache policy (sc1), every storer waits for its stores to
-// complete before its counter increment, and the last arriver loads only
-// after its own increment has returned.  So the shares never need an L2
-// write-back (release) or invalidation (acquire), which would also throw out
-// the operands the other workgroups of the XCD are still reading.  The
-// counters live in the workspace header, and every call leaves them at zero.
+// The shares meet through the cache-maintenance-free exchange of the common
+// header (device-coherent stores and loads, a counter per row block).
 //
 // Products that need a K-split take the two-kernel path instead (split-K
 // product, then the head kernel): meeting the K-slices in this kernel as
@@ -1072,40 +1067,13 @@ __global__ __launch_bounds__(HD_THREADS) void head_tiled_kernel(
 // ---------------------------------------------------------------------------
 constexpr int FU_NB_MAX = 128;            // bins of the fused head (its logits fit the LDS)
 constexpr int FU_NBP = FU_NB_MAX + 4;     // fp32 per LDS row of logits (banks spread by rows)
-constexpr int FU_MAX_TICKETS = (int)((STAR_WS_HEADER_BYTES - kHdrFusedTickets) / 4);
-constexpr int kCpolCoherent = 16;         // buffer cache policy bits: sc1 (device scope)
-constexpr uint32_t kFuOob = 0x7FFFFFF0u;  // a buffer offset past every share: reads 0
+constexpr int FU_MAX_TICKETS = kMaxTickets;
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ inline __amdgpu_buffer_rsrc_t fu_rsrc(const void* base, uint32_t bytes) {
-    // raw buffer (stride 0); out-of-range accesses read 0 and drop writes
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
-                                             0x00020000);
-}
 __device__ inline void fu_store(f32x4 v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)off, 0,
-                                           kCpolCoherent);
+    xch_store(__builtin_bit_cast(u32x4, v), r, off);
 }
 __device__ inline f32x4 fu_load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0,
-                                                                           kCpolCoherent));
-}
-// every store this thread issued has completed (is visible device-wide)
-__device__ inline void fu_wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-
-// One workgroup's arrival at a counter that `expect` workgroups reach: true
-// for the last to arrive, which also resets the counter.  Call after the
-// workgroup's coherent stores have completed (fu_wait_stores in every thread).
-__device__ inline bool fu_last_arrival(uint32_t* counter, uint32_t expect, uint32_t* s_ticket) {
-    __syncthreads();
-    if (threadIdx.x == 0)
-        *s_ticket = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __syncthreads();
-    const bool last = *s_ticket == expect - 1;
-    if (last && threadIdx.x == 0)
-        __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return last;
+    return __builtin_bit_cast(f32x4, xch_load(r, off));
 }
 
 __device__ inline f32x4 fu_chunk(const f32x16& a, int q) {
@@ -1271,7 +1239,7 @@ __global__ __launch_bounds__(SH::THREADS) void predict_fused_kernel(FusedArgs a)
     if (a.tiles_n > 1) {
         const uint32_t share = (uint32_t)nblk * 1024u;            // floats per share
         const __amdgpu_buffer_rsrc_t rl =
-            fu_rsrc(a.lpart + (size_t)w.tm * a.tiles_n * share, (uint32_t)a.tiles_n * share * 4u);
+            xch_rsrc(a.lpart + (size_t)w.tm * a.tiles_n * share, (uint32_t)a.tiles_n * share * 4u);
 #pragma unroll
         for (int u = 0; u < MAXB; ++u) {
             const int blk = wid + u * NW;
@@ -1281,8 +1249,8 @@ __global__ __launch_bounds__(SH::THREADS) void predict_fused_kernel(FusedArgs a)
                     fu_store(fu_chunk(lg[u], q), rl,
                              (uint32_t)w.tn * share * 4u + (uint32_t)((blk * 4 + q) * 64 + lane) * 16u);
         }
-        fu_wait_stores();
-        if (!fu_last_arrival(&a.tix_row[w.tm], (uint32_t)a.tiles_n, &s_ticket)) return;
+        xch_wait_stores();
+        if (!xch_last_arrival(&a.tix_row[w.tm], (uint32_t)a.tiles_n, &s_ticket)) return;
         constexpr int G = 8;                  // shares loaded together
 #pragma unroll
         for (int u = 0; u < MAXB; ++u) {
@@ -1301,7 +1269,7 @@ __global__ __launch_bounds__(SH::THREADS) void predict_fused_kernel(FusedArgs a)
                         const int t = t0 + g;
                         const uint32_t off = (uint32_t)t * share * 4u +
                                              (uint32_t)((blk * 4 + q) * 64 + lane) * 16u;
-                        v[g][q] = fu_load(rl, t < a.tiles_n ? off : kFuOob);
+                        v[g][q] = fu_load(rl, t < a.tiles_n ? off : kXchOob);
                     }
 #pragma unroll
                 for (int g = 0; g < G; ++g)

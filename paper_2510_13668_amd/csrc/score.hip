@@ -83,6 +83,7 @@ constexpr int64_t kInfS = INT64_MAX;
 constexpr uint32_t kInfI = 0xFFFFFFFFu;
 
 __device__ inline int64_t imax(int64_t a, int64_t b) { return a > b ? a : b; }
+__device__ inline int64_t imin64(int64_t a, int64_t b) { return a < b ? a : b; }
 
 __device__ inline bool key_less(int64_t s0, uint32_t i0, int64_t s1, uint32_t i1) {
     return s0 < s1 || (s0 == s1 && i0 < i1);
@@ -433,52 +434,86 @@ __device__ inline int64_t move_score(const int64_t* pm_t, const int64_t* sm_t, i
 }
 
 // ---------------------------------------------------------------------------
-// prep (large curve sets): PM_t[0..K] (PM_t[0] unused), SM_t[0..K] (SM_t[K] unused)
+// prep (large curve sets): bucket-major planes of every instance's PM, L and
+// SM, so that one request's reads for all targets t at its k_e are
+// contiguous.  With K1 = K + 1 rows of n entries:
+//     TPM[k][t] = PM_t[k]                    (k = 0..K; PM_t[K] = max over all j)
+//     TL[k][t]  = L_t[k], -inf at k = K
+//     TSM[k][t] = SM_t[min(k + 1, K)]        (SM_t[K] = -inf)
+//     PEAK[t]   = SM_t[0], the instance's peak
+// One workgroup per instance; the column writes are n entries apart.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(PREP_THREADS) void score_prep_kernel(const int64_t* __restrict__ load,
-                                                                  int K, int b,
-                                                                  int64_t* __restrict__ PM,
-                                                                  int64_t* __restrict__ SM) {
+                                                                  int n, int K, int b,
+                                                                  int64_t* __restrict__ TPM,
+                                                                  int64_t* __restrict__ TL,
+                                                                  int64_t* __restrict__ TSM,
+                                                                  int64_t* __restrict__ PEAK) {
     __shared__ int64_t tmp[PREP_THREADS / 64 + 1];
     const int tid = threadIdx.x;
     const int t = blockIdx.x;
     const int64_t* L = load + (int64_t)t * K;
-    int64_t* pm = PM + (int64_t)t * (K + 1);
-    int64_t* sm = SM + (int64_t)t * (K + 1);
     const int64_t bb = (int64_t)b * b;
     constexpr int CH = PREP_THREADS * PREP_SEG;
 
     int64_t carry = INT64_MIN;                 // exclusive prefix max of L[j] + b^2 j
     for (int base = 0; base < K; base += CH) {
         const int j0 = base + tid * PREP_SEG;
+        int64_t x[PREP_SEG];
         int64_t loc = INT64_MIN;
-        for (int j = j0; j < j0 + PREP_SEG && j < K; ++j) loc = imax(loc, L[j] + bb * j);
+#pragma unroll
+        for (int u = 0; u < PREP_SEG; ++u) {
+            const int j = j0 + u;
+            x[u] = j < K ? L[j] : 0;
+            if (j < K) loc = imax(loc, x[u] + bb * j);
+        }
         int64_t tot;
         int64_t ex = block_exclusive_scan_i64<PREP_THREADS>(loc, OpMax(), INT64_MIN, tmp, &tot);
         int64_t run = imax(carry, ex);
-        for (int j = j0; j < j0 + PREP_SEG && j < K; ++j) {
-            pm[j] = run;
-            run = imax(run, L[j] + bb * j);
+#pragma unroll
+        for (int u = 0; u < PREP_SEG; ++u) {
+            const int j = j0 + u;
+            if (j < K) {
+                TPM[(int64_t)j * n + t] = run;
+                TL[(int64_t)j * n + t] = x[u];
+                run = imax(run, x[u] + bb * j);
+            }
         }
         carry = imax(carry, tot);
     }
-    if (tid == 0) pm[K] = carry;
+    if (tid == 0) {
+        TPM[(int64_t)K * n + t] = carry;
+        TL[(int64_t)K * n + t] = INT64_MIN;
+        TSM[(int64_t)(K - 1) * n + t] = INT64_MIN;
+        TSM[(int64_t)K * n + t] = INT64_MIN;
+    }
 
     carry = INT64_MIN;                         // inclusive suffix max of L[j]
     for (int base = 0; base < K; base += CH) {
         const int p0 = base + tid * PREP_SEG;  // reversed position p <-> j = K-1-p
+        int64_t x[PREP_SEG];
         int64_t loc = INT64_MIN;
-        for (int p = p0; p < p0 + PREP_SEG && p < K; ++p) loc = imax(loc, L[K - 1 - p]);
+#pragma unroll
+        for (int u = 0; u < PREP_SEG; ++u) {
+            const int p = p0 + u;
+            x[u] = p < K ? L[K - 1 - p] : INT64_MIN;
+            loc = imax(loc, x[u]);
+        }
         int64_t tot;
         int64_t ex = block_exclusive_scan_i64<PREP_THREADS>(loc, OpMax(), INT64_MIN, tmp, &tot);
         int64_t run = imax(carry, ex);
-        for (int p = p0; p < p0 + PREP_SEG && p < K; ++p) {
-            run = imax(run, L[K - 1 - p]);
-            sm[K - 1 - p] = run;
+#pragma unroll
+        for (int u = 0; u < PREP_SEG; ++u) {
+            const int p = p0 + u;
+            if (p < K) {
+                run = imax(run, x[u]);
+                const int j = K - 1 - p;       // SM_t[j] = run
+                if (j > 0) TSM[(int64_t)(j - 1) * n + t] = run;
+                else PEAK[t] = run;
+            }
         }
         carry = imax(carry, tot);
     }
-    if (tid == 0) sm[K] = INT64_MIN;
 }
 
 // ---------------------------------------------------------------------------
@@ -489,8 +524,6 @@ struct ScoreArgs {
     const int32_t* rem;
     const int32_t* inst;
     const int64_t* load;
-    const int64_t* PM;            // global PM/SM (non-fused path)
-    const int64_t* SM;
     int64_t* scores;              // caller's array or workspace copy
     int32_t* best_target;         // caller's array or workspace copy
     int64_t* best_score;
@@ -502,7 +535,8 @@ struct ScoreArgs {
     uint32_t magic_K, magic_n;
 };
 
-template <bool kFused>
+// Curve sets that fit the LDS: every workgroup builds PM/SM of every
+// instance there, then scores its rpb requests against every target.
 __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int tid = threadIdx.x;
@@ -512,11 +546,11 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
     const int cand = a.cand;                       // rpb * n keys in this workgroup
     const int rpb = a.rpb;
 
-    // LDS: [L | PM | SM] (fused), keys, per-request values
+    // LDS: [L | PM | SM], keys, per-request values
     int64_t* lL = (int64_t*)smem;
-    int64_t* lPM = lL + (kFused ? n * K1 : 0);
-    int64_t* lSM = lPM + (kFused ? n * K1 : 0);
-    int64_t* ks = lSM + (kFused ? n * K1 : 0);
+    int64_t* lPM = lL + n * K1;
+    int64_t* lSM = lPM + n * K1;
+    int64_t* ks = lSM + n * K1;
     int64_t* r_alpha = ks + cand;
     int64_t* r_p = r_alpha + rpb;
     uint32_t* ki = (uint32_t*)(r_p + rpb);
@@ -532,12 +566,10 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
     int32_t bad = 0;
     int64_t lv[SC_LBATCH];
     const int nK = n * K;
-    if constexpr (kFused) {
 #pragma unroll
-        for (int j = 0; j < SC_LBATCH; ++j) {
-            const int e = j * SC_THREADS + tid;
-            lv[j] = a.load[e < nK ? e : nK - 1];
-        }
+    for (int j = 0; j < SC_LBATCH; ++j) {
+        const int e = j * SC_THREADS + tid;
+        lv[j] = a.load[e < nK ? e : nK - 1];
     }
     for (int q0 = 0; q0 < rpb; q0 += SC_THREADS * 2) {
         int sv[2], cv[2], rv[2];
@@ -565,22 +597,18 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
     }
     bad = wave_or_i32(bad);
     if (lane == 0) report_error(a.err_word, bad);
-    if constexpr (kFused) {
 #pragma unroll
-        for (int j = 0; j < SC_LBATCH; ++j) {
-            const int e = j * SC_THREADS + tid;
-            if (e < nK) {
-                const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
-                lL[t * K1 + (e - t * K)] = lv[j];
-            }
+    for (int j = 0; j < SC_LBATCH; ++j) {
+        const int e = j * SC_THREADS + tid;
+        if (e < nK) {
+            const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
+            lL[t * K1 + (e - t * K)] = lv[j];
         }
-        for (int t = tid; t < n; t += SC_THREADS) lL[t * K1 + K] = INT64_MIN;
-        __syncthreads();
-        build_pm_sm<SC_THREADS>(lL, lPM, lSM, n, K, bb);
     }
+    for (int t = tid; t < n; t += SC_THREADS) lL[t * K1 + K] = INT64_MIN;
     __syncthreads();
-    const int64_t* gPM = kFused ? lPM : a.PM;
-    const int64_t* gSM = kFused ? lSM : a.SM;
+    build_pm_sm<SC_THREADS>(lL, lPM, lSM, n, K, bb);
+    __syncthreads();
 
     // 1) candidates -> scores and keys (self-candidates and invalid requests
     //    get the +inf key)
@@ -592,14 +620,9 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
         if (r < a.N) {
             const int s = r_s[q];
             const int ke = r_ke[q];
-            int64_t l_ke;
-            if constexpr (kFused) {
-                l_ke = lL[t * K1 + ke];                    // entry K is -inf
-            } else {
-                l_ke = ke < K ? a.load[(int64_t)t * K + (ke < K ? ke : K - 1)] : INT64_MIN;
-            }
-            const int64_t* pm_t = gPM + (int64_t)t * K1;
-            const int64_t* sm_t = gSM + (int64_t)t * K1;
+            const int64_t l_ke = lL[t * K1 + ke];          // entry K is -inf
+            const int64_t* pm_t = lPM + t * K1;
+            const int64_t* sm_t = lSM + t * K1;
             const int64_t mv = move_score(pm_t, sm_t, l_ke, ke, K, r_alpha[q], r_p[q]);
             const int64_t sc = s < 0 ? -1 : (t == s ? sm_t[0] : mv);
             if (s >= 0 && t != s) {
@@ -619,7 +642,7 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
     if (a.bbase) {
         __shared__ int64_t wmin[SC_THREADS / 64];
         for (int t = tid; t < n; t += SC_THREADS) {
-            const int64_t v = gSM[(int64_t)t * K1];
+            const int64_t v = lSM[t * K1];
             base = v < base ? v : base;
         }
         base = -readlane_i64(wave_incl_max_i64(-base), 63);
@@ -645,6 +668,165 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
         if (a.best_score) a.best_score[r] = none ? -1 : bs;
         if (a.bcode) a.bcode[r] = none ? kNoCode : (uint16_t)key_code((uint64_t)(bs - base));
     }
+}
+
+// ---------------------------------------------------------------------------
+// score from the bucket-major planes (curve sets too large for LDS)
+// ---------------------------------------------------------------------------
+// One group of G lanes per request, lane l of the group scoring targets
+// t = l + G c (c < TPL; G = 16 when n > 16, else the power of two >= n;
+// more than 16 TPL targets are taken TPL per lane at a time).  The planes
+// put every target's PM, L and SM at a request's k_e side by side, so a
+// request's reads are a few contiguous lines.  A lane keeps the smallest
+// (score, t) of its targets (t ascends, so the first minimum stays), and
+// the group minimum is taken with DPP moves inside the 16-lane row.  Each
+// group takes REQ consecutive requests, whose reads are issued together.
+constexpr int SP_THREADS = 256;
+constexpr int SP_ROW = 16;                 // lanes per request when n > 16
+
+struct PlanarArgs {
+    const int32_t* cur;
+    const int32_t* rem;
+    const int32_t* inst;
+    const int64_t* tpm;           // [K+1][n] bucket-major planes (score_prep_kernel)
+    const int64_t* tl;
+    const int64_t* tsm;
+    const int64_t* peak;          // [n]
+    int64_t* scores;              // [N, n] or null
+    int32_t* best_target;         // [N] or null
+    int64_t* best_score;          // [N] or null
+    int32_t* err_word;
+    int64_t* bbase;               // code base of the best keys (workgroup 0 writes), or null
+    uint16_t* bcode;              // [N] code of each request's best key, or null
+    int N, n, b, K, lg;           // G = 2^lg lanes per request
+};
+
+template <int TPL, int REQ>
+__global__ __launch_bounds__(SP_THREADS) void score_planar_kernel(PlanarArgs a) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int n = a.n, b = a.b, K = a.K;
+    const int G = 1 << a.lg;
+    const int gl = lane & (G - 1);
+    const int gpw = 64 >> a.lg;                          // groups per wave
+    const int wave = blockIdx.x * (SP_THREADS / 64) + (tid >> 6);
+    const int64_t H = (int64_t)b * K;
+    const int64_t alpha0 = (int64_t)b * (b - 1) / 2;
+
+    int rv[REQ], sv[REQ], cv[REQ], lv[REQ];
+#pragma unroll
+    for (int j = 0; j < REQ; ++j) {
+        rv[j] = (wave * REQ + j) * gpw + (lane >> a.lg);
+        const int rc = rv[j] < a.N ? rv[j] : a.N - 1;
+        sv[j] = a.inst[rc];
+        cv[j] = a.cur[rc];
+        lv[j] = a.rem[rc];
+    }
+    // the code base: the smallest peak (no migration scores below it)
+    int64_t base = INT64_MAX;
+    if (a.bbase) {
+        for (int t = lane; t < n; t += 64) base = imin64(base, a.peak[t]);
+        base = -readlane_i64(wave_incl_max_i64(-base), 63);
+        if (blockIdx.x == 0 && tid == 0) *a.bbase = base;
+    }
+    // request terms (Section 5.2's load model, as the projection takes them)
+    int32_t bad = 0;
+    int ke[REQ], s[REQ];
+    int64_t al[REQ], pp[REQ];
+#pragma unroll
+    for (int j = 0; j < REQ; ++j) {
+        int32_t f = 0;
+        if (sv[j] < 0 || sv[j] >= n) f |= STAR_DEV_BAD_INST;
+        if (cv[j] < 1) f |= STAR_DEV_BAD_CUR;
+        if (lv[j] < 1) f |= STAR_DEV_BAD_REM;
+        const bool live = rv[j] < a.N;
+        bad |= live ? f : 0;
+        const uint32_t lp = (uint32_t)((int64_t)lv[j] < H ? (int64_t)lv[j] : H);
+        const uint32_t k = lp / (uint32_t)b;
+        const int64_t mu = (int64_t)(lp - k * (uint32_t)b);
+        const bool ok = f == 0;
+        s[j] = ok && live ? sv[j] : -1;
+        ke[j] = ok ? (int)k : 0;
+        al[j] = (int64_t)b * cv[j] + alpha0;
+        pp[j] = mu * cv[j] + mu * (int64_t)k * b + mu * (mu - 1) / 2;
+    }
+    bad = wave_or_i32(bad);
+    if (lane == 0) report_error(a.err_word, bad);
+
+    int64_t bs[REQ];
+    int bt[REQ];
+#pragma unroll
+    for (int j = 0; j < REQ; ++j) {
+        bs[j] = kInfS;
+        bt[j] = -1;
+    }
+    for (int t0 = 0; t0 < n; t0 += G * TPL) {
+        int tv[TPL];
+        int64_t pk[TPL];
+        int64_t xm[REQ][TPL], xl[REQ][TPL], xs[REQ][TPL];
+#pragma unroll
+        for (int c = 0; c < TPL; ++c) {
+            tv[c] = t0 + gl + G * c;
+            const int tc = tv[c] < n ? tv[c] : n - 1;
+            pk[c] = a.peak[tc];
+#pragma unroll
+            for (int j = 0; j < REQ; ++j) {
+                const int64_t idx = (int64_t)ke[j] * n + tc;
+                xm[j][c] = a.tpm[idx];
+                xl[j][c] = a.tl[idx];
+                xs[j][c] = a.tsm[idx];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < REQ; ++j) {
+#pragma unroll
+            for (int c = 0; c < TPL; ++c) {
+                const int t = tv[c];
+                const int64_t mv = imax(imax(xm[j][c] + al[j], xl[j][c] + pp[j]), xs[j][c]);
+                const int64_t sc = s[j] < 0 ? -1 : (t == s[j] ? pk[c] : mv);
+                const bool tin = t < n;
+                if (tin && rv[j] < a.N && a.scores) a.scores[(int64_t)rv[j] * n + t] = sc;
+                if (tin && s[j] >= 0 && t != s[j] && sc < bs[j]) {
+                    bs[j] = sc;
+                    bt[j] = t;
+                }
+            }
+        }
+    }
+    // best (score, t) of each request over its group
+#pragma unroll
+    for (int j = 0; j < REQ; ++j) {
+        const uint64_t u = bt[j] >= 0 ? (uint64_t)bs[j] ^ 0x8000000000000000ull : ~0ull;
+        const uint64_t um = group_min_u64(u, G);
+        const uint64_t tt = bt[j] >= 0 && u == um ? (uint64_t)(uint32_t)bt[j] : ~0ull;
+        const uint64_t tm = group_min_u64(tt, G);
+        if (gl == 0 && rv[j] < a.N) {
+            const bool none = um == ~0ull;
+            const int64_t best = (int64_t)(um ^ 0x8000000000000000ull);
+            if (a.best_target) a.best_target[rv[j]] = none ? -1 : (int32_t)tm;
+            if (a.best_score) a.best_score[rv[j]] = none ? -1 : best;
+            if (a.bcode) a.bcode[rv[j]] = none ? kNoCode : (uint16_t)key_code((uint64_t)(best - base));
+        }
+    }
+}
+
+// Targets per lane and requests per group of the planar scoring: about a
+// dozen plane reads in flight per lane.
+static int planar_tpl(int n) { return n <= SP_ROW ? 1 : n <= 2 * SP_ROW ? 2 : 4; }
+
+static hipError_t launch_planar(const PlanarArgs& q, int groups, int tpl, hipStream_t stream) {
+    switch (tpl) {
+    case 1:
+        hipLaunchKernelGGL((score_planar_kernel<1, 4>), dim3(groups), dim3(SP_THREADS), 0, stream, q);
+        break;
+    case 2:
+        hipLaunchKernelGGL((score_planar_kernel<2, 2>), dim3(groups), dim3(SP_THREADS), 0, stream, q);
+        break;
+    default:
+        hipLaunchKernelGGL((score_planar_kernel<4, 1>), dim3(groups), dim3(SP_THREADS), 0, stream, q);
+        break;
+    }
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -1355,26 +1537,52 @@ __device__ __forceinline__ int select_best_by_code(const TopkArgs& a, int ib1, S
     return select_gathered<TK_RJ1>(a, g, ib1, sh, cl, base, ws_s, ws_i, smin, smax_w);
 }
 
-// Counting sort of the pruned top-k: up to TK_SORT_CAP keys placed in LDS by
-// their codes (sh.hist holds each code's offset, sh.fill its count), then
+// Counting sort of the pruned top-k: up to TK_SORT_CAP candidate keys,
+// first compacted in thread order (each thread's count, a block prefix, then
+// plain LDS writes: no per-key atomic round trips), then placed in slots
+// grouped by code (sh.hist holds each code's offset, sh.fill its count) and
 // ranked among the keys that share their code.
 constexpr int TK_SORT_CAP = TK_THREADS;
 constexpr int TK_CODE_V = 4;                            // 16-byte code reads per thread
 constexpr int TK_CODE_REG = TK_CODE_V * 8 * TK_THREADS; // best-key codes held in registers
 struct SortLds {
-    int64_t s[TK_SORT_CAP];
+    int64_t s[TK_SORT_CAP];       // keys in code order
     uint32_t i[TK_SORT_CAP];
     uint16_t c[TK_SORT_CAP];
+    int64_t cs[TK_SORT_CAP];      // the candidates, compacted in thread order
+    uint32_t ci[TK_SORT_CAP];
+    uint16_t cc[TK_SORT_CAP];
 };
 
-// Slot t's place in key order: its code's offset plus the number of keys of
-// the same code below it.
-__device__ __forceinline__ int sorted_pos(const SelShared<TK_THREADS>& sh, const SortLds& sl, int t,
-                                          int64_t s, uint32_t i) {
-    const int c = sl.c[t];
+// Thread t's key (s, i) of code c goes to the next slot of its code (t < P;
+// sh.hist: code offsets, sh.fill: zero); returns its place in key order: the
+// code's offset plus the number of keys of the code below it (-1 for t >= P).
+__device__ __forceinline__ int sort_place(SelShared<TK_THREADS>& sh, SortLds& sl, int P, int64_t s,
+                                          uint32_t i, uint16_t c) {
+    const int tid = threadIdx.x;
+    if (tid < P) {
+        const int slot = sh.hist[c] + atomicAdd(&sh.fill[c], 1);
+        sl.s[slot] = s;
+        sl.i[slot] = i;
+        sl.c[slot] = c;
+    }
+    __syncthreads();
+    if (tid >= P) return -1;
     const int lo = sh.hist[c], hi = lo + sh.fill[c];
     int rank = 0;
-    for (int j = lo; j < hi; ++j) rank += key_less(sl.s[j], sl.i[j], s, i) ? 1 : 0;
+    int j = lo;
+    for (; j + 4 <= hi; j += 4) {                       // four LDS reads in flight
+        int64_t xs[4];
+        uint32_t xi[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            xs[u] = sl.s[j + u];
+            xi[u] = sl.i[j + u];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) rank += key_less(xs[u], xi[u], s, i) ? 1 : 0;
+    }
+    for (; j < hi; ++j) rank += key_less(sl.s[j], sl.i[j], s, i) ? 1 : 0;
     return lo + rank;
 }
 
@@ -1386,10 +1594,10 @@ __device__ __forceinline__ uint16_t code_of(const uint4& v, int u) {
 
 // Stage 1 with every best-key code in registers (N <= TK_CODE_REG): the code
 // histogram gives c*, the code of the k-th smallest best key; every best key
-// of code <= c* is placed by the counting sort, so (ws_s, ws_i)[0, nr) holds
-// the nr = min(k, keys) smallest best keys in key order and *smax_w the
-// largest of them.  Returns -1 (with the workgroup synchronised) when more
-// than TK_SORT_CAP best keys have codes <= c*.
+// of code <= c* is compacted and counting-sorted, so (ws_s, ws_i)[0, nr)
+// holds the nr = min(k, keys) smallest best keys in key order and *smax_w
+// the largest of them.  Returns -1 (with the workgroup synchronised) when
+// more than TK_SORT_CAP best keys have codes <= c*.
 __device__ __forceinline__ int best_sorted(const TopkArgs& a, SelShared<TK_THREADS>& sh,
                                            SortLds& sl, int64_t* ws_s, uint32_t* ws_i,
                                            int64_t* smax_w) {
@@ -1406,15 +1614,18 @@ __device__ __forceinline__ int best_sorted(const TopkArgs& a, SelShared<TK_THREA
     sh.hist[tid] = 0;
     sh.fill[tid] = 0;
     __syncthreads();
-#pragma unroll
-    for (int j = 0; j < TK_CODE_V; ++j) {
+    // code u of group j (kNoCode past N)
+    auto code = [&](int j, int u) -> uint16_t {
         const int v = j * TK_THREADS + tid;
+        return v < nv && v * 8 + u < a.N ? code_of(cv[j], u) : kNoCode;
+    };
+#pragma unroll
+    for (int j = 0; j < TK_CODE_V; ++j)
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-            const uint16_t c = code_of(cv[j], u);
-            if (v < nv && v * 8 + u < a.N && c != kNoCode) atomicAdd(&sh.hist[c], 1);
+            const uint16_t c = code(j, u);
+            if (c != kNoCode) atomicAdd(&sh.hist[c], 1);
         }
-    }
     __syncthreads();
     const int h = sh.hist[tid];
     int total;
@@ -1432,35 +1643,38 @@ __device__ __forceinline__ int best_sorted(const TopkArgs& a, SelShared<TK_THREA
         __syncthreads();
         return -1;
     }
+    int cnt = 0;
 #pragma unroll
-    for (int j = 0; j < TK_CODE_V; ++j) {
-        const int v = j * TK_THREADS + tid;
+    for (int j = 0; j < TK_CODE_V; ++j)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) cnt += code(j, u) <= cstar ? 1 : 0;
+    int tot;
+    int pos = block_excl_i32<TK_THREADS>(cnt, sh, &tot);
+#pragma unroll
+    for (int j = 0; j < TK_CODE_V; ++j)
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-            const uint16_t c = code_of(cv[j], u);
-            if (v < nv && v * 8 + u < a.N && c <= cstar) {
-                const int slot = sh.hist[c] + atomicAdd(&sh.fill[c], 1);
-                sl.i[slot] = (uint32_t)(v * 8 + u);
-                sl.c[slot] = c;
+            const uint16_t c = code(j, u);
+            if (c <= cstar) {
+                sl.ci[pos] = (uint32_t)((j * TK_THREADS + tid) * 8 + u);
+                sl.cc[pos] = c;
+                ++pos;
             }
         }
-    }
     __syncthreads();
     int64_t s = 0;
     uint32_t r = 0;
+    uint16_t c = 0;
     if (tid < nle) {
-        r = sl.i[tid];
+        r = sl.ci[tid];
+        c = sl.cc[tid];
         s = a.best_score[r];
-        sl.s[tid] = s;
     }
-    __syncthreads();
     const int nr = a.top_k < nle ? a.top_k : nle;
-    if (tid < nle) {
-        const int pos = sorted_pos(sh, sl, tid, s, r);
-        if (pos < nr) {
-            ws_s[pos] = s;
-            ws_i[pos] = r;
-        }
+    const int p = sort_place(sh, sl, nle, s, r, c);
+    if (p >= 0 && p < nr) {
+        ws_s[p] = s;
+        ws_i[p] = r;
     }
     __syncthreads();
     *smax_w = nr > 0 ? ws_s[nr - 1] : -1;
@@ -1472,53 +1686,54 @@ __device__ __forceinline__ int best_sorted(const TopkArgs& a, SelShared<TK_THREA
 // distinct migrations, so the k-th smallest migration is at most the largest
 // of them (smax_w) and only migrations scored at most smax_w can win; when
 // nr < k every migration of the nr requests is a candidate.  The candidates
-// are counting-sorted on their codes.  Returns false, with nothing written
-// and the workgroup synchronised, when more than TK_SORT_CAP are candidates.
+// are compacted and counting-sorted on their codes.  Returns false, with
+// nothing written and the workgroup synchronised, when more than
+// TK_SORT_CAP are candidates.
 template <int RJ>
 __device__ __forceinline__ bool pruned_sorted_write(const RegKeys<RJ>& keys, const TopkArgs& a,
                                                     int nr, int64_t smax_w, int64_t base,
                                                     SelShared<TK_THREADS>& sh, SortLds& sl) {
-    constexpr uint16_t kNone = 0xFFFF;
     const int tid = threadIdx.x;
     const int64_t thr = nr == a.top_k ? smax_w : kInfS;
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) cnt += keys.s[j] != kInfS && keys.s[j] <= thr ? 1 : 0;
+    int P;
+    int pos = block_excl_i32<TK_THREADS>(cnt, sh, &P);
+    if (P > TK_SORT_CAP) return false;                    // block_excl_i32 ends synchronised
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+        if (keys.s[j] != kInfS && keys.s[j] <= thr) {
+            sl.cs[pos] = keys.s[j];
+            sl.ci[pos] = keys.i[j];
+            ++pos;
+        }
+    }
     sh.hist[tid] = 0;
     sh.fill[tid] = 0;
     __syncthreads();
-    uint16_t code[RJ];
-#pragma unroll
-    for (int j = 0; j < RJ; ++j) {
-        const bool cand = keys.s[j] != kInfS && keys.s[j] <= thr;
-        code[j] = cand ? (uint16_t)key_code((uint64_t)(keys.s[j] - base)) : kNone;
-        if (cand) atomicAdd(&sh.hist[code[j]], 1);
+    int64_t s = 0;
+    uint32_t i = 0;
+    uint16_t c = 0;
+    if (tid < P) {
+        s = sl.cs[tid];
+        i = sl.ci[tid];
+        c = (uint16_t)key_code((uint64_t)(s - base));
+        atomicAdd(&sh.hist[c], 1);
     }
     __syncthreads();
     const int h = sh.hist[tid];
-    int P;
-    const int before = block_excl_i32<TK_THREADS>(h, sh, &P);
-    if (P > TK_SORT_CAP) return false;                    // block_excl_i32 ends synchronised
+    int tot;
+    const int before = block_excl_i32<TK_THREADS>(h, sh, &tot);
     sh.hist[tid] = before;
     __syncthreads();
-#pragma unroll
-    for (int j = 0; j < RJ; ++j) {
-        if (code[j] != kNone) {
-            const int slot = sh.hist[code[j]] + atomicAdd(&sh.fill[code[j]], 1);
-            sl.s[slot] = keys.s[j];
-            sl.i[slot] = keys.i[j];
-            sl.c[slot] = code[j];
-        }
-    }
-    __syncthreads();
     const int kk = a.top_k < P ? a.top_k : P;
-    if (tid < P) {
-        const int64_t s = sl.s[tid];
-        const uint32_t i = sl.i[tid];
-        const int pos = sorted_pos(sh, sl, tid, s, i);
-        if (pos < kk) {
-            const uint32_t r = fast_div(i, (uint32_t)a.n, a.magic_n);
-            a.topk_req[pos] = (int32_t)r;
-            a.topk_tgt[pos] = (int32_t)(i - r * (uint32_t)a.n);
-            a.topk_score[pos] = s;
-        }
+    const int p = sort_place(sh, sl, P, s, i, c);
+    if (p >= 0 && p < kk) {
+        const uint32_t r = fast_div(i, (uint32_t)a.n, a.magic_n);
+        a.topk_req[p] = (int32_t)r;
+        a.topk_tgt[p] = (int32_t)(i - r * (uint32_t)a.n);
+        a.topk_score[p] = s;
     }
     for (int q = kk + tid; q < a.top_k; q += TK_THREADS) {
         a.topk_req[q] = -1;
@@ -2269,10 +2484,19 @@ ScorePlan plan_score(const star_score_params& p, bool project) {
         pl.cand = pl.rpb * n;
         pl.groups = (int)ceil_div(N, pl.rpb);
     }
-    pl.pm_off = off;
-    if (!pl.fused) off = align_up(off + (size_t)n * K1 * 8, 256);
-    pl.sm_off = off;
-    if (!pl.fused) off = align_up(off + (size_t)n * K1 * 8, 256);
+    if (!pl.fused) {                              // bucket-major planes and peaks
+        const size_t plane = align_up((size_t)n * K1 * 8, 256);
+        pl.tpm_off = off;
+        pl.tl_off = off + plane;
+        pl.tsm_off = off + 2 * plane;
+        pl.peak_off = off + 3 * plane;
+        off = align_up(pl.peak_off + (size_t)n * 8, 256);
+        pl.lg = 0;
+        while ((1 << pl.lg) < n && (1 << pl.lg) < SP_ROW) ++pl.lg;
+        const int tpl = planar_tpl(n);
+        const int per_wg = (SP_THREADS / 64) * (4 / tpl) * (64 >> pl.lg);
+        pl.groups = N > 0 ? (int)ceil_div(N, per_wg) : 0;
+    }
     pl.scores_off = off;                          // used when the caller passes no scores
     off = align_up(off + (size_t)N * n * 8, 256);
     pl.bscore_off = off;
@@ -2294,7 +2518,7 @@ ScorePlan plan_score(const star_score_params& p, bool project) {
         off = align_up(off + (size_t)TK_REG_BEST * 4, 256);
     }
     pl.total = off;
-    pl.lds = (pl.fused ? (size_t)3 * n * K1 * 8 : 0) + (size_t)pl.cand * 12 + (size_t)pl.rpb * 24;
+    pl.lds = pl.fused ? (size_t)3 * n * K1 * 8 + (size_t)pl.cand * 12 + (size_t)pl.rpb * 24 : 0;
     return pl;
 }
 
@@ -2305,11 +2529,10 @@ static hipError_t set_lds(const void* fn, size_t lds, size_t static_lds) {
     return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
 }
 
-template <bool kFused>
 static hipError_t launch_score_kernel(const ScorePlan& pl, const ScoreArgs& a, hipStream_t stream) {
-    hipError_t e = set_lds((const void*)score_kernel<kFused>, pl.lds, 64);
+    hipError_t e = set_lds((const void*)score_kernel, pl.lds, 64);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(score_kernel<kFused>, dim3(pl.groups), dim3(SC_THREADS), pl.lds, stream, a);
+    hipLaunchKernelGGL(score_kernel, dim3(pl.groups), dim3(SC_THREADS), pl.lds, stream, a);
     return hipGetLastError();
 }
 
@@ -2331,11 +2554,22 @@ static hipError_t launch_topk_pruned(const TopkArgs& a, int rj2, hipStream_t str
                         : launch_topk_pruned1<S1, 0>(a, stream);
 }
 
+CurvePlanes score_planes(const ScorePlan& pl, char* ws) {
+    CurvePlanes c;
+    if (pl.fused) return c;
+    c.tpm = (int64_t*)(ws + pl.tpm_off);
+    c.tl = (int64_t*)(ws + pl.tl_off);
+    c.tsm = (int64_t*)(ws + pl.tsm_off);
+    c.peak = (int64_t*)(ws + pl.peak_off);
+    return c;
+}
+
 hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const int32_t* cur,
                         const int32_t* rem, const int32_t* inst, const int64_t* load,
                         int64_t* scores, int32_t* best_target, int64_t* best_score,
                         int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score, char* ws,
-                        int32_t* err_word, hipStream_t stream, int64_t* load_out) {
+                        int32_t* err_word, hipStream_t stream, int64_t* load_out,
+                        bool planes_ready) {
     const star_load_params& lp = p.load;
     if (lp.n_req == 0) {
         if (p.top_k > 0) {                       // no candidates: top-k is all -1
@@ -2399,8 +2633,6 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     const bool need_all = p.top_k > 0;           // the top-k kernel reads scores and best moves
     ScoreArgs a = {};
     a.cur = cur; a.rem = rem; a.inst = inst; a.load = load;
-    a.PM = (const int64_t*)(ws + pl.pm_off);
-    a.SM = (const int64_t*)(ws + pl.sm_off);
     a.scores = scores ? scores : (need_all ? (int64_t*)(ws + pl.scores_off) : nullptr);
     a.best_target = best_target ? best_target : (need_all ? (int32_t*)(ws + pl.btarget_off) : nullptr);
     a.best_score = best_score ? best_score : (need_all ? (int64_t*)(ws + pl.bscore_off) : nullptr);
@@ -2413,13 +2645,23 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     if (pl.topk_hist) a.bcode = (uint16_t*)(ws + pl.bcode_off);
     hipError_t e;
     if (pl.fused) {
-        e = launch_score_kernel<true>(pl, a, stream);
+        e = launch_score_kernel(pl, a, stream);
     } else {
-        hipLaunchKernelGGL(score_prep_kernel, dim3(lp.n_inst), dim3(PREP_THREADS), 0, stream, load,
-                           lp.n_buckets, lp.bucket, (int64_t*)(ws + pl.pm_off),
-                           (int64_t*)(ws + pl.sm_off));
-        e = hipGetLastError();
-        if (e == hipSuccess) e = launch_score_kernel<false>(pl, a, stream);
+        const CurvePlanes cp = score_planes(pl, ws);
+        PlanarArgs q = {};
+        q.cur = cur; q.rem = rem; q.inst = inst;
+        q.tpm = cp.tpm; q.tl = cp.tl; q.tsm = cp.tsm; q.peak = cp.peak;
+        q.scores = a.scores; q.best_target = a.best_target; q.best_score = a.best_score;
+        q.err_word = err_word; q.bbase = a.bbase; q.bcode = a.bcode;
+        q.N = lp.n_req; q.n = lp.n_inst; q.b = lp.bucket; q.K = lp.n_buckets; q.lg = pl.lg;
+        e = hipSuccess;
+        if (!planes_ready) {
+            hipLaunchKernelGGL(score_prep_kernel, dim3(lp.n_inst), dim3(PREP_THREADS), 0, stream,
+                               load, lp.n_inst, lp.n_buckets, lp.bucket, cp.tpm, cp.tl, cp.tsm,
+                               cp.peak);
+            e = hipGetLastError();
+        }
+        if (e == hipSuccess && pl.groups > 0) e = launch_planar(q, pl.groups, planar_tpl(lp.n_inst), stream);
     }
     if (e != hipSuccess || p.top_k == 0) return e;
     if (lp.n_inst == 1) {                        // nowhere to migrate to

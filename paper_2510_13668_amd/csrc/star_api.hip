@@ -113,7 +113,7 @@ STAR_API star_status star_predict(const star_predict_params* p, const void* hidd
     st = check_ws(ws, ws_bytes, STAR_WS_HEADER_BYTES + align_up(pl.partial_bytes, 256));
     if (st != STAR_OK) return st;
     char* scratch = (char*)ws + STAR_WS_HEADER_BYTES;
-    uint32_t* tickets = (uint32_t*)((char*)ws + kHdrFusedTickets);
+    uint32_t* tickets = (uint32_t*)((char*)ws + kHdrTickets);
     hipError_t e = launch_predict(*p, pl, hidden, w1, b1, w2, b2, bin_values, ema_state,
                                   expected_len, rem_len, scratch, tickets, (hipStream_t)stream);
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
@@ -173,7 +173,7 @@ STAR_API star_status star_predict_noalloc(const star_predict_params* p, const vo
     if (!ws) return STAR_ERR_HIP;
     hipError_t e = launch_predict(*p, pl, hidden, w1, b1, w2, b2, bin_values, ema_state,
                                   expected_len, rem_len, ws + STAR_WS_HEADER_BYTES,
-                                  (uint32_t*)(ws + kHdrFusedTickets), (hipStream_t)stream);
+                                  (uint32_t*)(ws + kHdrTickets), (hipStream_t)stream);
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
 }
 
@@ -228,7 +228,7 @@ STAR_API star_status star_predict_mlp4(const star_mlp4_params* p, const void* hi
 // ---------------------------------------------------------------------------
 STAR_API size_t star_project_load_workspace_size(const star_load_params* p) {
     if (check_load_params(p) != STAR_OK) return 0;
-    return STAR_WS_HEADER_BYTES;
+    return STAR_WS_HEADER_BYTES + plan_load(*p).part_bytes;
 }
 
 STAR_API star_status star_project_load(const star_load_params* p, const int32_t* cur_len,
@@ -238,11 +238,11 @@ STAR_API star_status star_project_load(const star_load_params* p, const int32_t*
     if (st != STAR_OK) return st;
     if (!load) return STAR_ERR_INVALID_ARG;
     if (p->n_req > 0 && (!cur_len || !rem_len || !inst_of)) return STAR_ERR_INVALID_ARG;
-    st = check_ws(ws, ws_bytes, STAR_WS_HEADER_BYTES);
-    if (st != STAR_OK) return st;
     const LoadPlan pl = plan_load(*p);
-    int32_t* err = (int32_t*)((char*)ws + kHdrErrorWord);
-    hipError_t e = launch_project_load(*p, pl, cur_len, rem_len, inst_of, load, err,
+    st = check_ws(ws, ws_bytes, STAR_WS_HEADER_BYTES + pl.part_bytes);
+    if (st != STAR_OK) return st;
+    hipError_t e = launch_project_load(*p, pl, cur_len, rem_len, inst_of, load, (char*)ws,
+                                       (char*)ws + STAR_WS_HEADER_BYTES, nullptr, nullptr,
                                        (hipStream_t)stream);
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
 }
@@ -289,9 +289,17 @@ STAR_API star_status star_score_migrations(const star_score_params* p, const int
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
 }
 
+// The split projection's histograms follow the scoring's scratch (its last
+// workgroups write the scoring's curve planes while others still read them).
+static size_t project_and_score_part(const ScorePlan& pl) { return align_up(pl.total, 256); }
+static size_t project_and_score_bytes(const star_score_params& p, const ScorePlan& pl) {
+    if (pl.project_in) return pl.total;
+    return project_and_score_part(pl) + plan_load(p.load).part_bytes;
+}
+
 STAR_API size_t star_project_and_score_workspace_size(const star_score_params* p) {
     if (check_score_params(p) != STAR_OK) return 0;
-    return plan_score(*p, true).total;
+    return project_and_score_bytes(*p, plan_score(*p, true));
 }
 
 STAR_API star_status star_project_and_score(const star_score_params* p, const int32_t* cur_len,
@@ -308,17 +316,21 @@ STAR_API star_status star_project_and_score(const star_score_params* p, const in
     const bool all_topk = topk_req && topk_tgt && topk_score;
     if (p->top_k > 0 ? !all_topk : any_topk) return STAR_ERR_INVALID_ARG;
     const ScorePlan pl = plan_score(*p, true);
-    st = check_ws(ws, ws_bytes, pl.total);
+    st = check_ws(ws, ws_bytes, project_and_score_bytes(*p, pl));
     if (st != STAR_OK) return st;
     int32_t* err = (int32_t*)((char*)ws + kHdrErrorWord);
     hipError_t e = hipSuccess;
-    if (!pl.project_in)
-        e = launch_project_load(p->load, plan_load(p->load), cur_len, rem_len, inst_of, load, err,
-                                (hipStream_t)stream);
+    bool planes_ready = false;
+    if (!pl.project_in) {
+        const CurvePlanes cp = score_planes(pl, (char*)ws);
+        e = launch_project_load(p->load, plan_load(p->load), cur_len, rem_len, inst_of, load,
+                                (char*)ws, (char*)ws + project_and_score_part(pl),
+                                cp.tpm ? &cp : nullptr, &planes_ready, (hipStream_t)stream);
+    }
     if (e == hipSuccess)
         e = launch_score(*p, pl, cur_len, rem_len, inst_of, load, scores, best_target, best_score,
                          topk_req, topk_tgt, topk_score, (char*)ws, err, (hipStream_t)stream,
-                         pl.project_in ? load : nullptr);
+                         pl.project_in ? load : nullptr, planes_ready);
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
 }
 

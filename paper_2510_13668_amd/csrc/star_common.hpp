@@ -19,9 +19,11 @@ constexpr size_t kHdrPlanDone = 72;     // int32: the migration plan has stopped
 constexpr size_t kHdrPlanCount = 76;    // int32: moves made by the plan
 constexpr size_t kHdrScoreHist = 256;   // uint32[1024]: key-code histogram of the ranking
 static_assert(kHdrScoreHist + 1024 * 4 <= STAR_WS_HEADER_BYTES, "header holds the histogram");
-// uint32 counters of the fused predictor (column tiles per row block), to
-// the end of the header
-constexpr size_t kHdrFusedTickets = kHdrScoreHist + 1024 * 4;
+// uint32 arrival counters of the calls whose workgroups meet through a
+// last-arriver exchange (the fused predictor's row blocks, the split
+// projection's instances), to the end of the header
+constexpr size_t kHdrTickets = kHdrScoreHist + 1024 * 4;
+constexpr int kMaxTickets = (int)((STAR_WS_HEADER_BYTES - kHdrTickets) / 4);
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -109,6 +111,68 @@ __device__ inline int64_t wave_incl_max_i64(int64_t v) {
     return v;
 }
 
+// v plus the value of its DPP source lane (0 where there is none).
+template <int kCtrl, int kRowMask>
+__device__ inline int64_t dpp_add_i64(int64_t v) {
+    const int lo = dpp_i32<kCtrl, kRowMask>((int)(uint32_t)v, 0);
+    const int hi = dpp_i32<kCtrl, kRowMask>((int)(v >> 32), 0);
+    return v + (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// Inclusive prefix sum of an int64 over the 64 lanes (lane order).
+__device__ inline int64_t wave_incl_add_i64(int64_t v) {
+    v = dpp_add_i64<kDppRowShr1, 0xF>(v);
+    v = dpp_add_i64<kDppRowShr2, 0xF>(v);
+    v = dpp_add_i64<kDppRowShr4, 0xF>(v);
+    v = dpp_add_i64<kDppRowShr8, 0xF>(v);
+    v = dpp_add_i64<kDppRowBcast15, 0xA>(v);
+    v = dpp_add_i64<kDppRowBcast31, 0xC>(v);
+    return v;
+}
+
+// Inclusive prefix sums of two int64 per thread over a block of kT threads
+// (thread order, every thread taking part); tmp: 2 kT/64 int64 of LDS.
+template <int kT>
+__device__ inline void block_incl_add2_i64(int64_t& x, int64_t& y, int64_t* tmp) {
+    constexpr int W = kT / kWave;
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    x = wave_incl_add_i64(x);
+    y = wave_incl_add_i64(y);
+    if (lane == kWave - 1) {
+        tmp[wid] = x;
+        tmp[W + wid] = y;
+    }
+    __syncthreads();
+    int64_t bx = 0, by = 0;
+    for (int w = 0; w < wid; ++w) {
+        bx += tmp[w];
+        by += tmp[W + w];
+    }
+    x += bx;
+    y += by;
+    __syncthreads();
+}
+
+// Inclusive prefix maxima of two int64 per thread over a block of kT threads
+// (thread order, every thread taking part); tmp: 2 kT/64 int64 of LDS.
+template <int kT>
+__device__ inline void block_incl_max2_i64(int64_t& x, int64_t& y, int64_t* tmp) {
+    constexpr int W = kT / kWave;
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    x = wave_incl_max_i64(x);
+    y = wave_incl_max_i64(y);
+    if (lane == kWave - 1) {
+        tmp[wid] = x;
+        tmp[W + wid] = y;
+    }
+    __syncthreads();
+    for (int w = 0; w < wid; ++w) {
+        x = tmp[w] > x ? tmp[w] : x;
+        y = tmp[W + w] > y ? tmp[W + w] : y;
+    }
+    __syncthreads();
+}
+
 // Inclusive scan across the wave (lane order), for a commutative,
 // associative op on int64.
 template <class Op>
@@ -191,6 +255,53 @@ __device__ inline ReqTerms request_terms(int s, int c, int l, int n, int b, int6
     q.alpha = ok ? (int64_t)b * c + (int64_t)b * (b - 1) / 2 : 0;
     q.p = ok ? mu * c + mu * ke * b + mu * (mu - 1) / 2 : 0;
     return q;
+}
+
+// ---------------------------------------------------------------------------
+// Exchange between the workgroups of one launch without cache maintenance:
+// shares are stored and loaded with the device-coherent cache policy (sc1)
+// through raw buffer resources, every storer waits for its stores to
+// complete before its counter increment, and the last arriver loads only
+// after its own increment has returned.  So the shares never need an L2
+// write-back (release) or invalidation (acquire), which would also throw out
+// what the other workgroups of the XCD are still reading.  The counters live
+// in the workspace header, and every call leaves them at zero.
+// ---------------------------------------------------------------------------
+constexpr int kCpolCoherent = 16;          // buffer cache policy bits: sc1 (device scope)
+constexpr uint32_t kXchOob = 0x7FFFFFF0u;  // a buffer offset past every share: reads 0
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ inline __amdgpu_buffer_rsrc_t xch_rsrc(const void* base, uint32_t bytes) {
+    // raw buffer (stride 0); out-of-range accesses read 0 and drop writes
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+__device__ inline void xch_store(u32x4 v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)off, 0, kCpolCoherent);
+}
+__device__ inline u32x4 xch_load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kCpolCoherent);
+}
+__device__ inline u32x2 xch_load_b64(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, kCpolCoherent);
+}
+// every store this thread issued has completed (is visible device-wide)
+__device__ inline void xch_wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// One workgroup's arrival at a counter that `expect` workgroups reach: true
+// for the last to arrive, which also resets the counter.  Call after the
+// workgroup's coherent stores have completed (xch_wait_stores in every thread).
+__device__ inline bool xch_last_arrival(uint32_t* counter, uint32_t expect, uint32_t* s_ticket) {
+    __syncthreads();
+    if (threadIdx.x == 0)
+        *s_ticket = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const bool last = *s_ticket == expect - 1;
+    if (last && threadIdx.x == 0)
+        __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return last;
 }
 
 // Device-error reporting: OR `bits` into the workspace error word.

@@ -48,11 +48,33 @@ hipError_t launch_mlp4(const star_mlp4_params& p, const Mlp4Plan& pl, const void
 struct LoadPlan {
     int chunk = 0;       // buckets per workgroup
     int n_chunks = 0;
+    bool split = false;  // request slices per instance, met by a last arriver (16-byte
+                         // aligned request arrays; otherwise the chunked kernel)
+    int slices = 0, slice_len = 0, kp = 0;
+    size_t part_bytes = 0;  // the slices' histograms, after the workspace header
 };
 LoadPlan plan_load(const star_load_params& p);
+
+// Bucket-major planes of every instance's curve terms, for scoring from
+// them (K1 = K + 1 rows of n entries):
+//     tpm[k][t] = PM_t[k] = max_{j < k} (L_t[j] + b^2 j)   (-inf at k = 0)
+//     tl[k][t]  = L_t[k], -inf at k = K
+//     tsm[k][t] = SM_t[min(k + 1, K)], SM_t[k] = max_{j >= k} L_t[j], SM_t[K] = -inf
+//     peak[t]   = SM_t[0]
+struct CurvePlanes {
+    int64_t* tpm = nullptr;
+    int64_t* tl = nullptr;
+    int64_t* tsm = nullptr;
+    int64_t* peak = nullptr;
+};
+
+// ws: the workspace (its header); part: part_bytes for the split projection's
+// histograms.  With planes set, the split projection writes them as well and
+// sets *planes_written.
 hipError_t launch_project_load(const star_load_params& p, const LoadPlan& pl,
                                const int32_t* cur, const int32_t* rem, const int32_t* inst,
-                               int64_t* load, int32_t* err_word, hipStream_t stream);
+                               int64_t* load, char* ws, char* part, const CurvePlanes* planes,
+                               bool* planes_written, hipStream_t stream);
 
 struct ScorePlan {
     bool fused = false;   // PM/SM built in LDS by the scoring kernel
@@ -73,15 +95,21 @@ struct ScorePlan {
     bool topk_hist = false;    // pruned top-k, best keys beyond registers: the top-k counts
                                // their codes and gathers those up to the k-th
     size_t bcode_off = 0, gs_off = 0, gi_off = 0;  // topk_hist: best-key codes, gathered keys
-    size_t pm_off = 0, sm_off = 0, scores_off = 0, bscore_off = 0, btarget_off = 0, total = 0;
+    size_t tpm_off = 0, tl_off = 0, tsm_off = 0, peak_off = 0;  // bucket-major planes (not fused)
+    int lg = 0;           // planar scoring: 2^lg lanes per request
+    size_t scores_off = 0, bscore_off = 0, btarget_off = 0, total = 0;
     size_t lds = 0;       // dynamic LDS of the scoring kernel (or of the small path's one)
 };
 ScorePlan plan_score(const star_score_params& p, bool project = false);
+// The planes of the non-fused path, inside ws.
+CurvePlanes score_planes(const ScorePlan& pl, char* ws);
+// planes_ready: the projection has already written the planes.
 hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const int32_t* cur,
                         const int32_t* rem, const int32_t* inst, const int64_t* load,
                         int64_t* scores, int32_t* best_target, int64_t* best_score,
                         int32_t* topk_req, int32_t* topk_tgt, int64_t* topk_score, char* ws,
-                        int32_t* err_word, hipStream_t stream, int64_t* load_out = nullptr);
+                        int32_t* err_word, hipStream_t stream, int64_t* load_out = nullptr,
+                        bool planes_ready = false);
 
 struct VarPlan {
     int lg = 0;           // lanes per request = 2^lg (<= 16)

@@ -116,6 +116,17 @@ def test_predict_noalloc_validation_and_scratch_limit(L):
 def test_load_and_score_validation(L):
     lp = star.load_params(1024, 8, 64, 256)
     assert star.project_load_workspace_size(lp) == star.STAR_WS_HEADER_BYTES
+    # long streams (8192+ requests, at most 1024 buckets, at most 960
+    # instances) keep one histogram triple per (instance, request slice):
+    # 32768 requests on 64 instances take 4 slices of 8192
+    H = star.STAR_WS_HEADER_BYTES
+    big_lp = star.load_params(32768, 64, 64, 1024)
+    assert star.project_load_workspace_size(big_lp) == H + 64 * 4 * 3 * 1026 * 8
+    assert star.project_load_workspace_size(star.load_params(32768, 64, 64, 1025)) == H
+    assert star.project_load_workspace_size(star.load_params(32768, 961, 64, 1024)) == H
+    assert star.project_load_workspace_size(star.load_params(8191, 64, 64, 1024)) == H
+    assert L.star_project_load(ctypes.byref(big_lp), f := FAKE, f, f, f, f,
+                               H + 64 * 4 * 3 * 1026 * 8 - 1, None) == -4
     f = FAKE
     assert L.star_project_load(ctypes.byref(star.load_params(1, 0, 1, 1)), f, f, f, f, f, 256, None) == -1
     assert L.star_project_load(ctypes.byref(star.load_params(1, 1, 0, 1)), f, f, f, f, f, 256, None) == -1
@@ -156,6 +167,10 @@ def test_project_and_score_validation(L):
     need = star.project_and_score_workspace_size(sp)
     # the same workspace layout as scoring alone
     assert need == star.score_workspace_size(sp)
+    # with the split projection, its histograms follow the scoring's scratch
+    big = star.score_params(32768, 64, 64, 1024, 256)
+    assert star.project_and_score_workspace_size(big) == (
+        star.score_workspace_size(big) + 64 * 4 * 3 * 1026 * 8)
     args = [f] * 10
     assert L.star_project_and_score(None, *args, f, need, None) == -1
     assert L.star_project_and_score(ctypes.byref(sp), *args, f, need - 1, None) == -4

@@ -158,6 +158,28 @@ def test_crowded_best_code_takes_streamed_stage(fused):
     _check(cur, rem, inst, n, 64, 32, 256, fused=fused)
 
 
+# (N, n, b, K): the split projection (request slices met by a last arriver)
+# at its boundaries -- the smallest stream, a ragged last slice with a tail
+# of one request, the largest curve -- and the chunked kernel beyond them
+# (more than 1024 buckets, more instances than arrival counters)
+PROJECTION_REGIMES = [
+    (8192, 64, 64, 1024),
+    (8193, 3, 16, 1024),
+    (12001, 200, 8, 300),
+    (9000, 7, 4, 1025),
+    (9000, 1000, 2, 50),
+    (40000, 2, 1, 1),
+]
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+@pytest.mark.parametrize("N,n,b,K", PROJECTION_REGIMES)
+def test_projection_regimes(N, n, b, K, fused):
+    rng = np.random.default_rng(N * 7 + n)
+    cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=5000, len_hi=b * K + 7)
+    _check(cur, rem, inst, n, b, K, 256, fused=fused)
+
+
 def _key_bits(ref, inst, n):
     """Bits of the widest packed ranking key: score range, then r*n + t."""
     sc = ref["scores"]
