@@ -158,6 +158,9 @@ __device__ inline void build_pm_sm(const int64_t* lL, int64_t* lPM, int64_t* lSM
     const int S = ((K + 31) >> 5) | 1;
     for (int t0 = 0; t0 < n; t0 += kT / 32) {
         const int t = t0 + (int)(threadIdx.x >> 5);
+        // waves whose two instances are both past n sit out (no barrier
+        // inside: the DPP moves stay within the wave)
+        if (t0 + 2 * (int)(threadIdx.x >> 6) >= n) continue;
         const bool live = t < n;
         const int tc = live ? t : 0;
         const int64_t* L = lL + tc * K1;
@@ -291,6 +294,9 @@ __device__ inline void build_curves_pm_sm(const int64_t* hA, const int64_t* hN, 
     const int S = ((K + 31) >> 5) | 1;
     for (int t0 = 0; t0 < n; t0 += kT / 32) {
         const int t = t0 + (int)(threadIdx.x >> 5);
+        // waves whose two instances are both past n sit out (no barrier
+        // inside: the DPP moves stay within the wave)
+        if (t0 + 2 * (int)(threadIdx.x >> 6) >= n) continue;
         const bool live = t < n;
         const int tc = live ? t : 0;
         const int64_t* A = hA + tc * K1;
@@ -394,6 +400,126 @@ __device__ inline void build_curves_pm_sm(const int64_t* hA, const int64_t* hN, 
         }
     }
 }
+
+// Exclusive maximum over the lanes above this one (lanes l+1..63), -inf for
+// lane 63: the wave reversed by an LDS permute, a DPP prefix maximum, and
+// the result gathered back by a second permute.
+__device__ inline int64_t perm_i64(int64_t x, int src_lane) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute(src_lane * 4, (int)(uint32_t)x);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(src_lane * 4, (int)(x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+__device__ inline int64_t wave_excl_max_above_i64(int64_t v) {
+    const int l = threadIdx.x & 63;
+    const int64_t inc = wave_incl_max_i64(perm_i64(v, 63 - l));   // lane l: max of v[63-l..63]
+    const int64_t x = perm_i64(inc, l < 63 ? 62 - l : 0);
+    return l < 63 ? x : INT64_MIN;
+}
+
+// build_curves_pm_sm with a whole wave per instance (runs of S = ceil(K/64),
+// made odd, buckets per lane): half the serial depth, and every wave of a
+// larger workgroup takes an instance.
+template <int kT>
+__device__ inline void build_curves_pm_sm_w(const int64_t* hA, const int64_t* hN, int64_t* hPL,
+                                            int64_t* lPM, int64_t* lSM, int n, int K,
+                                            int64_t bb) {
+    const int l = threadIdx.x & 63;
+    const int K1 = K + 1;
+    const int S = ((K + 63) >> 6) | 1;
+    for (int t = (int)(threadIdx.x >> 6); t < n; t += kT / 64) {   // wave-uniform
+        const int64_t* A = hA + t * K1;
+        const int64_t* C = hN + t * K1;
+        int64_t* L = hPL + t * K1;
+        const int j0 = l * S;
+        const int j1 = j0 + S < K ? j0 + S : K;
+        const int q0 = K - 1 - j0, q1 = K - j1;      // buckets [q1, q0] (none when j0 >= K)
+        // 1) run sums
+        int64_t sa = 0, sn = 0;
+        for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {
+            int64_t xa[PMSM_BATCH], xn[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u >= q1 ? jb - u : q0;
+                xa[u] = A[q + 1];
+                xn[u] = C[q + 1];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u)
+                if (jb - u >= q1) {
+                    sa += xa[u];
+                    sn += xn[u];
+                }
+        }
+        int64_t ra = wave_shr1_i64(wave_incl_add_i64(sa), 0);   // sums over the lanes below
+        int64_t rn = wave_shr1_i64(wave_incl_add_i64(sn), 0);
+        // 2) L over the run (downwards) and the run's maxima
+        int64_t smax = INT64_MIN, pmax = INT64_MIN;
+        for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {
+            int64_t xa[PMSM_BATCH], xn[PMSM_BATCH], xp[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u >= q1 ? jb - u : q0;
+                xa[u] = A[q + 1];
+                xn[u] = C[q + 1];
+                xp[u] = L[q];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u;
+                if (q >= q1) {
+                    ra += xa[u];
+                    rn += xn[u];
+                    const int64_t v = ra + bb * q * rn + xp[u];
+                    L[q] = v;
+                    smax = imax(smax, v);
+                    pmax = imax(pmax, v + bb * q);
+                }
+            }
+        }
+        // 3) SM from the lanes below (higher buckets), PM from the lanes above
+        int64_t srun = wave_shr1_i64(wave_incl_max_i64(smax), INT64_MIN);
+        int64_t prun = wave_excl_max_above_i64(pmax);
+        const int64_t ptot = imax(prun, pmax);       // lane 0: max over every bucket
+        for (int jb = q0; jb >= q1; jb -= PMSM_BATCH) {         // SM downwards
+            int64_t x[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u >= q1 ? jb - u : q0;
+                x[u] = L[q];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb - u;
+                if (q >= q1) {
+                    srun = imax(srun, x[u]);
+                    lSM[t * K1 + q] = srun;
+                }
+            }
+        }
+        for (int jb = q1; jb <= q0; jb += PMSM_BATCH) {         // PM upwards, exclusive
+            int64_t x[PMSM_BATCH];
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb + u <= q0 ? jb + u : q1;
+                x[u] = L[q];
+            }
+#pragma unroll
+            for (int u = 0; u < PMSM_BATCH; ++u) {
+                const int q = jb + u;
+                if (q <= q0) {
+                    lPM[t * K1 + q] = prun;
+                    prun = imax(prun, x[u] + bb * q);
+                }
+            }
+        }
+        if (l == 0) {
+            L[K] = INT64_MIN;
+            lSM[t * K1 + K] = INT64_MIN;
+            lPM[t * K1 + K] = ptot;
+        }
+    }
+}
+
 
 // Minimum of a 64-bit value over aligned groups of g lanes (g a power of
 // two, 2..64); every lane of a group gets it.  DPP quad permutes for lane
@@ -2426,6 +2552,249 @@ void score_small_kernel(SmallArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// one workgroup scores and ranks a whole round (up to 1024 requests on up to
+// 8 instances, curves in LDS)
+// ---------------------------------------------------------------------------
+// Thread r takes request r: it adds its terms to the LDS histograms by k_e
+// (or the curves are read), the curves and PM/SM are built in LDS, and the
+// thread scores its request against every target, keeping the migration
+// keys in registers.  The top-k takes the code histogram of those keys and
+// c*, the code of the k-th smallest; every key of code <= c* is compacted
+// and counting-sorted, so the k smallest come out in key order (more than
+// TK_SORT_CAP keys up to c* take the radix selection instead).  One kernel,
+// no global round trip between scoring and ranking.
+constexpr int SO_THREADS = TK_THREADS;
+constexpr int SO_MAX_N = 8;                  // instances (keys per thread)
+constexpr int SO_LB = (SC_FUSED_ENTRIES + SO_THREADS - 1) / SO_THREADS;  // curve reads per thread
+constexpr size_t SO_STATIC_LDS =
+    sizeof(SelShared<TK_THREADS>) + sizeof(SortLds) + STAR_MAX_TOP_K * (8 + 4 + 8);
+
+struct OneArgs {
+    const int32_t* cur;
+    const int32_t* rem;
+    const int32_t* inst;
+    const int64_t* load;          // the curves, when not projecting
+    int64_t* load_out;            // the curves built here, when projecting
+    int64_t* scores;              // [N, n] or NULL
+    int32_t* best_target;         // [N] or NULL
+    int64_t* best_score;          // [N] or NULL
+    int32_t* topk_req;            // [top_k] (top_k > 0)
+    int32_t* topk_tgt;
+    int64_t* topk_score;
+    int32_t* err_word;
+    int N, n, b, K, top_k, ibits;
+    uint32_t magic_n, magic_K;
+};
+
+template <bool kProject>
+__global__ __launch_bounds__(SO_THREADS) void score_one_kernel(OneArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ SelShared<TK_THREADS> sh;
+    __shared__ SortLds sl;
+    __shared__ int64_t ws_s[STAR_MAX_TOP_K];
+    __shared__ uint32_t ws_i[STAR_MAX_TOP_K];
+    __shared__ uint64_t sv[STAR_MAX_TOP_K];
+    static_assert(RK_CODES == SO_THREADS, "one code per thread");
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int N = a.N, n = a.n, K = a.K, b = a.b;
+    const int K1 = K + 1, nK = n * K;
+    const int64_t H = (int64_t)b * K;
+    const int64_t bb = (int64_t)b * b;
+    int64_t* lL = (int64_t*)smem;
+    int64_t* lPM = lL + n * K1;
+    int64_t* lSM = lPM + n * K1;
+
+    // 0) this thread's request (and the curves when given); reads first
+    const int r = tid;
+    const bool live = r < N;
+    const int rc = live ? r : N - 1;
+    const int sr = a.inst[rc], cr = a.cur[rc], lr = a.rem[rc];
+    int64_t lv[kProject ? 1 : SO_LB];
+    if constexpr (!kProject) {
+#pragma unroll
+        for (int j = 0; j < SO_LB; ++j) {
+            const int e = j * SO_THREADS + tid;
+            lv[j] = a.load[e < nK ? e : nK - 1];
+        }
+    } else {
+        for (int e = tid; e < 3 * n * K1; e += SO_THREADS) lL[e] = 0;
+    }
+    int32_t f = 0;
+    if (sr < 0 || sr >= n) f |= STAR_DEV_BAD_INST;
+    if (cr < 1) f |= STAR_DEV_BAD_CUR;
+    if (lr < 1) f |= STAR_DEV_BAD_REM;
+    const bool ok = live && f == 0;
+    const uint32_t lp = (uint32_t)((int64_t)lr < H ? (int64_t)lr : H);
+    const uint32_t kq = lp / (uint32_t)b;
+    const int64_t mu = (int64_t)(lp - kq * (uint32_t)b);
+    const int s = ok ? sr : -1;
+    const int ke = ok ? (int)kq : 0;
+    const int64_t alpha = (int64_t)b * cr + (int64_t)b * (b - 1) / 2;
+    const int64_t pr = mu * cr + mu * (int64_t)kq * b + mu * (mu - 1) / 2;
+    const int32_t bad = wave_or_i32(live ? f : 0);
+    if (lane == 0) report_error(a.err_word, bad);
+    __syncthreads();
+
+    // 1) curves, PM, SM in LDS
+    if constexpr (kProject) {
+        // histograms by k_e: alpha in PM's rows, counts in SM's, partial
+        // buckets in L's (build_curves_pm_sm reads them there)
+        if (ok) {
+            const int row = s * K1;
+            if (ke > 0) {
+                atomicAdd((unsigned long long*)&lPM[row + ke], (unsigned long long)alpha);
+                atomicAdd((unsigned long long*)&lSM[row + ke], 1ull);
+            }
+            if (pr != 0) atomicAdd((unsigned long long*)&lL[row + ke], (unsigned long long)pr);
+        }
+        __syncthreads();
+        build_curves_pm_sm_w<SO_THREADS>(lPM, lSM, lL, lPM, lSM, n, K, bb);
+        __syncthreads();
+    } else {
+#pragma unroll
+        for (int j = 0; j < SO_LB; ++j) {
+            const int e = j * SO_THREADS + tid;
+            if (e < nK) {
+                const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
+                lL[t * K1 + (e - t * K)] = lv[j];
+            }
+        }
+        for (int t = tid; t < n; t += SO_THREADS) lL[t * K1 + K] = INT64_MIN;
+        __syncthreads();
+        build_pm_sm<SO_THREADS>(lL, lPM, lSM, n, K, bb);
+        __syncthreads();
+    }
+
+    // 2) scores of request r against every target; its best migration
+    int64_t base = INT64_MAX;                     // smallest target peak
+    for (int t = 0; t < n; ++t) base = imin64(base, lSM[t * K1]);
+    int64_t sc[SO_MAX_N];
+    int64_t bs = kInfS;
+    int bt = -1;
+#pragma unroll
+    for (int t = 0; t < SO_MAX_N; ++t) {
+        sc[t] = -1;
+        if (t < n) {
+            const int64_t* pm_t = lPM + t * K1;
+            const int64_t* sm_t = lSM + t * K1;
+            const int64_t mv = move_score(pm_t, sm_t, lL[t * K1 + ke], ke, K, alpha, pr);
+            sc[t] = s < 0 ? -1 : (t == s ? sm_t[0] : mv);
+            if (s >= 0 && t != s && sc[t] < bs) {  // t ascends: the first minimum stays
+                bs = sc[t];
+                bt = t;
+            }
+        }
+    }
+    // the round's global writes, issued last: a barrier waits for every
+    // store issued before it
+    auto write_round = [&]() {
+        if (live && a.scores) {
+            int64_t* out = a.scores + (int64_t)r * n;
+            if ((n & 1) == 0) {                   // 16-byte aligned pairs
+#pragma unroll
+                for (int t = 0; t < SO_MAX_N; t += 2)
+                    if (t < n) *(longlong2*)(out + t) = make_longlong2(sc[t], sc[t + 1]);
+            } else {
+#pragma unroll
+                for (int t = 0; t < SO_MAX_N; ++t)
+                    if (t < n) out[t] = sc[t];
+            }
+        }
+        if (live && a.best_target) a.best_target[r] = bt;
+        if (live && a.best_score) a.best_score[r] = bt < 0 ? -1 : bs;
+        if constexpr (kProject)
+            for (int e = tid; e < nK; e += SO_THREADS) {
+                const int t = (int)fast_div((uint32_t)e, (uint32_t)K, a.magic_K);
+                a.load_out[e] = lL[t * K1 + (e - t * K)];
+            }
+    };
+    if (a.top_k == 0) {
+        write_round();
+        return;
+    }
+
+    // 3) top-k over the migration keys (sc[t], r n + t), t != s
+    constexpr uint16_t kNone = 0xFFFF;
+    sh.hist[tid] = 0;
+    sh.fill[tid] = 0;
+    __syncthreads();
+    uint16_t code[SO_MAX_N];
+#pragma unroll
+    for (int t = 0; t < SO_MAX_N; ++t) {
+        const bool mig = t < n && s >= 0 && t != s;
+        code[t] = mig ? (uint16_t)key_code((uint64_t)(sc[t] - base)) : kNone;
+        if (mig) atomicAdd(&sh.hist[code[t]], 1);
+    }
+    __syncthreads();
+    const int h = sh.hist[tid];
+    int total;
+    const int before = block_excl_i32<TK_THREADS>(h, sh, &total);
+    const bool all = total <= a.top_k;
+    if (all ? tid == RK_CODES - 1 : (before < a.top_k && before + h >= a.top_k)) {
+        sh.bcast[0] = tid;                        // c*
+        sh.bcast[1] = before + h;                 // keys of code <= c*
+    }
+    sh.hist[tid] = before;                        // code offsets
+    __syncthreads();
+    const uint32_t cstar = (uint32_t)sh.bcast[0];
+    const int nle = sh.bcast[1];
+    if (nle <= TK_SORT_CAP) {
+        int cnt = 0;
+#pragma unroll
+        for (int t = 0; t < SO_MAX_N; ++t) cnt += code[t] <= cstar ? 1 : 0;
+        int tot;
+        int pos = block_excl_i32<TK_THREADS>(cnt, sh, &tot);
+#pragma unroll
+        for (int t = 0; t < SO_MAX_N; ++t) {
+            if (code[t] <= cstar) {
+                sl.cs[pos] = sc[t];
+                sl.ci[pos] = (uint32_t)(r * n + t);
+                sl.cc[pos] = code[t];
+                ++pos;
+            }
+        }
+        __syncthreads();
+        int64_t ks = 0;
+        uint32_t ki = 0;
+        uint16_t kc = 0;
+        if (tid < nle) {
+            ks = sl.cs[tid];
+            ki = sl.ci[tid];
+            kc = sl.cc[tid];
+        }
+        const int kk = a.top_k < total ? a.top_k : total;
+        const int p = sort_place(sh, sl, nle, ks, ki, kc);
+        if (p >= 0 && p < kk) {
+            const uint32_t rr = fast_div(ki, (uint32_t)n, a.magic_n);
+            a.topk_req[p] = (int32_t)rr;
+            a.topk_tgt[p] = (int32_t)(ki - rr * (uint32_t)n);
+            a.topk_score[p] = ks;
+        }
+        for (int q = kk + tid; q < a.top_k; q += SO_THREADS) {
+            a.topk_req[q] = -1;
+            a.topk_tgt[q] = -1;
+            a.topk_score[q] = -1;
+        }
+        write_round();
+        return;
+    }
+    // a crowded code c*: radix selection over the registers
+    RegKeys<SO_MAX_N> keys;
+#pragma unroll
+    for (int t = 0; t < SO_MAX_N; ++t) {
+        const bool mig = code[t] != kNone;
+        keys.s[t] = mig ? sc[t] : kInfS;
+        keys.i[t] = mig ? (uint32_t)(r * n + t) : kInfI;
+    }
+    int64_t smin, smax_w;
+    const int nw = select_top<TK_THREADS>(keys, a.top_k, a.ibits, sh, ws_s, ws_i, &smin, &smax_w);
+    order_and_write<TK_THREADS>(ws_s, ws_i, nw, smin, smax_w, a.ibits, n, a.magic_n, a.topk_req,
+                                a.topk_tgt, a.topk_score, a.top_k, sh, sv);
+    write_round();
+}
+
 __global__ void fill_i32_kernel(int32_t* p, int count, int32_t v) {
     for (int i = blockIdx.x * 256 + threadIdx.x; i < count; i += gridDim.x * 256) p[i] = v;
 }
@@ -2456,6 +2825,15 @@ ScorePlan plan_score(const star_score_params& p, bool project) {
     size_t off = STAR_WS_HEADER_BYTES;
     // fused scoring with the two-stage ranking: the scoring workgroups sort
     // their keys by code, one workgroup ranks
+    // a whole round in one workgroup: up to 1024 requests on up to 8 instances
+    pl.one = pl.fused && N > 0 && N <= SO_THREADS && n <= SO_MAX_N;
+    if (pl.one) {
+        pl.small = false;
+        pl.project_in = project;
+        pl.total = off;
+        pl.lds = (size_t)3 * n * K1 * 8;
+        return pl;
+    }
     pl.rank2 = pl.fused && p.top_k > 0 && pl.groups <= RK_MAX_GROUPS && pl.cand <= SC_THREADS;
     if (pl.rank2) {
         pl.small = false;
@@ -2579,6 +2957,27 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
             return e;
         }
         return hipSuccess;
+    }
+    if (pl.one) {
+        OneArgs o = {};
+        o.cur = cur; o.rem = rem; o.inst = inst; o.load = load; o.load_out = load_out;
+        o.scores = scores; o.best_target = best_target; o.best_score = best_score;
+        o.topk_req = topk_req; o.topk_tgt = topk_tgt; o.topk_score = topk_score;
+        o.err_word = err_word;
+        o.N = lp.n_req; o.n = lp.n_inst; o.b = lp.bucket; o.K = lp.n_buckets; o.top_k = p.top_k;
+        o.ibits = 0;
+        for (int64_t x = (int64_t)lp.n_req * lp.n_inst - 1; x > 0; x >>= 1) ++o.ibits;
+        o.magic_n = div_magic((uint32_t)lp.n_inst);
+        o.magic_K = div_magic((uint32_t)lp.n_buckets);
+        const void* kern = load_out ? (const void*)score_one_kernel<true>
+                                    : (const void*)score_one_kernel<false>;
+        hipError_t e = set_lds(kern, pl.lds, SO_STATIC_LDS);
+        if (e != hipSuccess) return e;
+        if (load_out)
+            hipLaunchKernelGGL(score_one_kernel<true>, dim3(1), dim3(SO_THREADS), pl.lds, stream, o);
+        else
+            hipLaunchKernelGGL(score_one_kernel<false>, dim3(1), dim3(SO_THREADS), pl.lds, stream, o);
+        return hipGetLastError();
     }
     if (pl.rank2) {
         ScoreArgs a = {};

@@ -78,6 +78,8 @@ hipError_t launch_project_load(const star_load_params& p, const LoadPlan& pl,
 
 struct ScorePlan {
     bool fused = false;   // PM/SM built in LDS by the scoring kernel
+    bool one = false;     // one 1024-thread workgroup projects, scores and ranks everything
+                          // (up to 1024 requests on up to 8 instances)
     bool small = false;   // one workgroup scores and ranks everything
     bool rank2 = false;   // fused scoring that code-sorts its keys, then one ranking workgroup
     bool project_in = false; // rank2: the scoring workgroups project the curves themselves

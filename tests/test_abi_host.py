@@ -141,11 +141,14 @@ def test_load_and_score_validation(L):
     assert L.star_project_load(ctypes.byref(big), f, f, f, f, f, 256, None) == -3
 
     # ranking keeps per-workgroup sorted keys (or scores and best moves, and
-    # PM/SM for large curve sets) in the workspace; without a top-k and with
-    # the curves in LDS only the header is needed
+    # the curve planes for large curve sets) in the workspace; a round that
+    # one workgroup takes whole (up to 1024 requests on up to 8 instances,
+    # curves in LDS) needs only the header
     H = star.STAR_WS_HEADER_BYTES
-    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 0)) >= H
-    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 256)) > H
+    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 0)) == H
+    assert star.score_workspace_size(star.score_params(1024, 8, 64, 256, 256)) == H
+    assert star.score_workspace_size(star.score_params(1025, 8, 64, 256, 256)) > H
+    assert star.score_workspace_size(star.score_params(1024, 9, 64, 256, 256)) > H
     sp = star.score_params(4096, 16, 64, 512, 256)
     need = star.score_workspace_size(sp)
     assert need > H
