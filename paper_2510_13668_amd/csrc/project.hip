@@ -317,12 +317,11 @@ __global__ __launch_bounds__(PS_THREADS) void project_split_kernel(SplitArgs a) 
     if (live) a.load[(int64_t)i * K + q] = Lq;
     if (!a.planes.tpm) return;
 
-    // The scoring's bucket-major planes of this instance (see CurvePlanes):
+    // The scoring's planes of this instance (see CurvePlanes):
     // SM (suffix max of L) is the inclusive prefix max in this thread order;
     // PM (max of L[j] + b^2 j over j < k) takes the forward order j = t,
     // with L passed through LDS.
     const CurvePlanes& pl = a.planes;
-    const int n = a.n;
     if (live) hA[q] = Lq;
     __syncthreads();
     const int j = tid;
@@ -332,16 +331,16 @@ __global__ __launch_bounds__(PS_THREADS) void project_split_kernel(SplitArgs a) 
     hN[j] = pm;                                   // inclusive; PM[j] is thread j-1's
     __syncthreads();
     if (live) {
-        pl.tl[(int64_t)q * n + i] = Lq;
-        if (q > 0) pl.tsm[(int64_t)(q - 1) * n + i] = sm;
+        pl.tl[q * pl.sk + i * pl.st] = Lq;
+        if (q > 0) pl.tsm[(q - 1) * pl.sk + i * pl.st] = sm;
         else pl.peak[i] = sm;
     }
-    if (j < K) pl.tpm[(int64_t)j * n + i] = j > 0 ? hN[j - 1] : INT64_MIN;
+    if (j < K) pl.tpm[j * pl.sk + i * pl.st] = j > 0 ? hN[j - 1] : INT64_MIN;
     if (tid == 0) {
-        pl.tpm[(int64_t)K * n + i] = hN[K - 1];
-        pl.tl[(int64_t)K * n + i] = INT64_MIN;
-        pl.tsm[(int64_t)(K - 1) * n + i] = INT64_MIN;
-        pl.tsm[(int64_t)K * n + i] = INT64_MIN;
+        pl.tpm[K * pl.sk + i * pl.st] = hN[K - 1];
+        pl.tl[K * pl.sk + i * pl.st] = INT64_MIN;
+        pl.tsm[(K - 1) * pl.sk + i * pl.st] = INT64_MIN;
+        pl.tsm[K * pl.sk + i * pl.st] = INT64_MIN;
     }
 }
 

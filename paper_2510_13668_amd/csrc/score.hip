@@ -560,17 +560,20 @@ __device__ inline int64_t move_score(const int64_t* pm_t, const int64_t* sm_t, i
 }
 
 // ---------------------------------------------------------------------------
-// prep (large curve sets): bucket-major planes of every instance's PM, L and
-// SM, so that one request's reads for all targets t at its k_e are
-// contiguous.  With K1 = K + 1 rows of n entries:
-//     TPM[k][t] = PM_t[k]                    (k = 0..K; PM_t[K] = max over all j)
-//     TL[k][t]  = L_t[k], -inf at k = K
-//     TSM[k][t] = SM_t[min(k + 1, K)]        (SM_t[K] = -inf)
+// prep (large curve sets): planes of every instance's PM, L and SM, entry
+// (k, t) at k sk + t st (k = 0..K):
+//     TPM(k, t) = PM_t[k]                    (PM_t[K] = max over all j)
+//     TL(k, t)  = L_t[k], -inf at k = K
+//     TSM(k, t) = SM_t[min(k + 1, K)]        (SM_t[K] = -inf)
 //     PEAK[t]   = SM_t[0], the instance's peak
-// One workgroup per instance; the column writes are n entries apart.
+// Bucket-major (sk = n, st = 1) puts one request's reads for every target
+// at its k_e side by side; instance-major (sk = 1, st = K + 1) makes these
+// writes contiguous, for rounds with few requests per bucket.  One workgroup
+// per instance.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(PREP_THREADS) void score_prep_kernel(const int64_t* __restrict__ load,
-                                                                  int n, int K, int b,
+                                                                  int K, int b, int64_t sk,
+                                                                  int64_t st,
                                                                   int64_t* __restrict__ TPM,
                                                                   int64_t* __restrict__ TL,
                                                                   int64_t* __restrict__ TSM,
@@ -600,18 +603,18 @@ __global__ __launch_bounds__(PREP_THREADS) void score_prep_kernel(const int64_t*
         for (int u = 0; u < PREP_SEG; ++u) {
             const int j = j0 + u;
             if (j < K) {
-                TPM[(int64_t)j * n + t] = run;
-                TL[(int64_t)j * n + t] = x[u];
+                TPM[j * sk + t * st] = run;
+                TL[j * sk + t * st] = x[u];
                 run = imax(run, x[u] + bb * j);
             }
         }
         carry = imax(carry, tot);
     }
     if (tid == 0) {
-        TPM[(int64_t)K * n + t] = carry;
-        TL[(int64_t)K * n + t] = INT64_MIN;
-        TSM[(int64_t)(K - 1) * n + t] = INT64_MIN;
-        TSM[(int64_t)K * n + t] = INT64_MIN;
+        TPM[K * sk + t * st] = carry;
+        TL[K * sk + t * st] = INT64_MIN;
+        TSM[(K - 1) * sk + t * st] = INT64_MIN;
+        TSM[K * sk + t * st] = INT64_MIN;
     }
 
     carry = INT64_MIN;                         // inclusive suffix max of L[j]
@@ -634,7 +637,7 @@ __global__ __launch_bounds__(PREP_THREADS) void score_prep_kernel(const int64_t*
             if (p < K) {
                 run = imax(run, x[u]);
                 const int j = K - 1 - p;       // SM_t[j] = run
-                if (j > 0) TSM[(int64_t)(j - 1) * n + t] = run;
+                if (j > 0) TSM[(j - 1) * sk + t * st] = run;
                 else PEAK[t] = run;
             }
         }
@@ -801,9 +804,9 @@ __global__ __launch_bounds__(SC_THREADS) void score_kernel(ScoreArgs a) {
 // ---------------------------------------------------------------------------
 // One group of G lanes per request, lane l of the group scoring targets
 // t = l + G c (c < TPL; G = 16 when n > 16, else the power of two >= n;
-// more than 16 TPL targets are taken TPL per lane at a time).  The planes
-// put every target's PM, L and SM at a request's k_e side by side, so a
-// request's reads are a few contiguous lines.  A lane keeps the smallest
+// more than 16 TPL targets are taken TPL per lane at a time).  Bucket-major
+// planes put every target's PM, L and SM at a request's k_e side by side, so
+// a request's reads are a few contiguous lines.  A lane keeps the smallest
 // (score, t) of its targets (t ascends, so the first minimum stays), and
 // the group minimum is taken with DPP moves inside the 16-lane row.  Each
 // group takes REQ consecutive requests, whose reads are issued together.
@@ -814,10 +817,11 @@ struct PlanarArgs {
     const int32_t* cur;
     const int32_t* rem;
     const int32_t* inst;
-    const int64_t* tpm;           // [K+1][n] bucket-major planes (score_prep_kernel)
+    const int64_t* tpm;           // planes of PM, L, SM: entry (k, t) at k sk + t st
     const int64_t* tl;
     const int64_t* tsm;
     const int64_t* peak;          // [n]
+    int64_t sk, st;
     int64_t* scores;              // [N, n] or null
     int32_t* best_target;         // [N] or null
     int64_t* best_score;          // [N] or null
@@ -897,7 +901,7 @@ __global__ __launch_bounds__(SP_THREADS) void score_planar_kernel(PlanarArgs a) 
             pk[c] = a.peak[tc];
 #pragma unroll
             for (int j = 0; j < REQ; ++j) {
-                const int64_t idx = (int64_t)ke[j] * n + tc;
+                const int64_t idx = ke[j] * a.sk + tc * a.st;
                 xm[j][c] = a.tpm[idx];
                 xl[j][c] = a.tl[idx];
                 xs[j][c] = a.tsm[idx];
@@ -2862,7 +2866,10 @@ ScorePlan plan_score(const star_score_params& p, bool project) {
         pl.cand = pl.rpb * n;
         pl.groups = (int)ceil_div(N, pl.rpb);
     }
-    if (!pl.fused) {                              // bucket-major planes and peaks
+    if (!pl.fused) {                              // planes and peaks
+        // bucket-major when requests outnumber buckets (the scoring gathers
+        // dominate), else instance-major (the preparation's writes do)
+        pl.by_bucket = N >= p.load.n_buckets;
         const size_t plane = align_up((size_t)n * K1 * 8, 256);
         pl.tpm_off = off;
         pl.tl_off = off + plane;
@@ -2932,13 +2939,15 @@ static hipError_t launch_topk_pruned(const TopkArgs& a, int rj2, hipStream_t str
                         : launch_topk_pruned1<S1, 0>(a, stream);
 }
 
-CurvePlanes score_planes(const ScorePlan& pl, char* ws) {
+CurvePlanes score_planes(const star_score_params& p, const ScorePlan& pl, char* ws) {
     CurvePlanes c;
     if (pl.fused) return c;
     c.tpm = (int64_t*)(ws + pl.tpm_off);
     c.tl = (int64_t*)(ws + pl.tl_off);
     c.tsm = (int64_t*)(ws + pl.tsm_off);
     c.peak = (int64_t*)(ws + pl.peak_off);
+    c.sk = pl.by_bucket ? p.load.n_inst : 1;
+    c.st = pl.by_bucket ? 1 : p.load.n_buckets + 1;
     return c;
 }
 
@@ -3046,17 +3055,18 @@ hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const i
     if (pl.fused) {
         e = launch_score_kernel(pl, a, stream);
     } else {
-        const CurvePlanes cp = score_planes(pl, ws);
+        const CurvePlanes cp = score_planes(p, pl, ws);
         PlanarArgs q = {};
         q.cur = cur; q.rem = rem; q.inst = inst;
         q.tpm = cp.tpm; q.tl = cp.tl; q.tsm = cp.tsm; q.peak = cp.peak;
+        q.sk = cp.sk; q.st = cp.st;
         q.scores = a.scores; q.best_target = a.best_target; q.best_score = a.best_score;
         q.err_word = err_word; q.bbase = a.bbase; q.bcode = a.bcode;
         q.N = lp.n_req; q.n = lp.n_inst; q.b = lp.bucket; q.K = lp.n_buckets; q.lg = pl.lg;
         e = hipSuccess;
         if (!planes_ready) {
             hipLaunchKernelGGL(score_prep_kernel, dim3(lp.n_inst), dim3(PREP_THREADS), 0, stream,
-                               load, lp.n_inst, lp.n_buckets, lp.bucket, cp.tpm, cp.tl, cp.tsm,
+                               load, lp.n_buckets, lp.bucket, cp.sk, cp.st, cp.tpm, cp.tl, cp.tsm,
                                cp.peak);
             e = hipGetLastError();
         }

@@ -322,7 +322,7 @@ STAR_API star_status star_project_and_score(const star_score_params* p, const in
     hipError_t e = hipSuccess;
     bool planes_ready = false;
     if (!pl.project_in) {
-        const CurvePlanes cp = score_planes(pl, (char*)ws);
+        const CurvePlanes cp = score_planes(*p, pl, (char*)ws);
         e = launch_project_load(p->load, plan_load(p->load), cur_len, rem_len, inst_of, load,
                                 (char*)ws, (char*)ws + project_and_score_part(pl),
                                 cp.tpm ? &cp : nullptr, &planes_ready, (hipStream_t)stream);

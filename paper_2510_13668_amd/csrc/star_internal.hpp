@@ -55,17 +55,19 @@ struct LoadPlan {
 };
 LoadPlan plan_load(const star_load_params& p);
 
-// Bucket-major planes of every instance's curve terms, for scoring from
-// them (K1 = K + 1 rows of n entries):
-//     tpm[k][t] = PM_t[k] = max_{j < k} (L_t[j] + b^2 j)   (-inf at k = 0)
-//     tl[k][t]  = L_t[k], -inf at k = K
-//     tsm[k][t] = SM_t[min(k + 1, K)], SM_t[k] = max_{j >= k} L_t[j], SM_t[K] = -inf
+// Planes of every instance's curve terms, for scoring from them; entry
+// (k, t), k = 0..K, at k sk + t st (bucket-major: sk = n, st = 1;
+// instance-major: sk = 1, st = K + 1):
+//     tpm(k, t) = PM_t[k] = max_{j < k} (L_t[j] + b^2 j)   (-inf at k = 0)
+//     tl(k, t)  = L_t[k], -inf at k = K
+//     tsm(k, t) = SM_t[min(k + 1, K)], SM_t[k] = max_{j >= k} L_t[j], SM_t[K] = -inf
 //     peak[t]   = SM_t[0]
 struct CurvePlanes {
     int64_t* tpm = nullptr;
     int64_t* tl = nullptr;
     int64_t* tsm = nullptr;
     int64_t* peak = nullptr;
+    int64_t sk = 0, st = 0;
 };
 
 // ws: the workspace (its header); part: part_bytes for the split projection's
@@ -97,14 +99,15 @@ struct ScorePlan {
     bool topk_hist = false;    // pruned top-k, best keys beyond registers: the top-k counts
                                // their codes and gathers those up to the k-th
     size_t bcode_off = 0, gs_off = 0, gi_off = 0;  // topk_hist: best-key codes, gathered keys
-    size_t tpm_off = 0, tl_off = 0, tsm_off = 0, peak_off = 0;  // bucket-major planes (not fused)
+    size_t tpm_off = 0, tl_off = 0, tsm_off = 0, peak_off = 0;  // curve planes (not fused)
+    bool by_bucket = false;  // the planes bucket-major (else instance-major)
     int lg = 0;           // planar scoring: 2^lg lanes per request
     size_t scores_off = 0, bscore_off = 0, btarget_off = 0, total = 0;
     size_t lds = 0;       // dynamic LDS of the scoring kernel (or of the small path's one)
 };
 ScorePlan plan_score(const star_score_params& p, bool project = false);
 // The planes of the non-fused path, inside ws.
-CurvePlanes score_planes(const ScorePlan& pl, char* ws);
+CurvePlanes score_planes(const star_score_params& p, const ScorePlan& pl, char* ws);
 // planes_ready: the projection has already written the planes.
 hipError_t launch_score(const star_score_params& p, const ScorePlan& pl, const int32_t* cur,
                         const int32_t* rem, const int32_t* inst, const int64_t* load,
