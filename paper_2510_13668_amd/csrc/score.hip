@@ -2610,6 +2610,9 @@ __global__ __launch_bounds__(SO_THREADS) void score_one_kernel(OneArgs a) {
     int64_t* lPM = lL + n * K1;
     int64_t* lSM = lPM + n * K1;
 
+    // the top-k's code histogram and fill counters (one code per thread)
+    sh.hist[tid] = 0;
+    sh.fill[tid] = 0;
     // 0) this thread's request (and the curves when given); reads first
     const int r = tid;
     const bool live = r < N;
@@ -2674,20 +2677,29 @@ __global__ __launch_bounds__(SO_THREADS) void score_one_kernel(OneArgs a) {
     // 2) scores of request r against every target; its best migration
     int64_t base = INT64_MAX;                     // smallest target peak
     for (int t = 0; t < n; ++t) base = imin64(base, lSM[t * K1]);
+    // and the key code of each migration, counted in the top-k's histogram
+    constexpr uint16_t kNone = 0xFFFF;
     int64_t sc[SO_MAX_N];
+    uint16_t code[SO_MAX_N];
     int64_t bs = kInfS;
     int bt = -1;
 #pragma unroll
     for (int t = 0; t < SO_MAX_N; ++t) {
         sc[t] = -1;
+        code[t] = kNone;
         if (t < n) {
             const int64_t* pm_t = lPM + t * K1;
             const int64_t* sm_t = lSM + t * K1;
             const int64_t mv = move_score(pm_t, sm_t, lL[t * K1 + ke], ke, K, alpha, pr);
             sc[t] = s < 0 ? -1 : (t == s ? sm_t[0] : mv);
-            if (s >= 0 && t != s && sc[t] < bs) {  // t ascends: the first minimum stays
+            const bool mig = s >= 0 && t != s;
+            if (mig && sc[t] < bs) {              // t ascends: the first minimum stays
                 bs = sc[t];
                 bt = t;
+            }
+            if (mig && a.top_k > 0) {
+                code[t] = (uint16_t)key_code((uint64_t)(sc[t] - base));
+                atomicAdd(&sh.hist[code[t]], 1);
             }
         }
     }
@@ -2720,17 +2732,6 @@ __global__ __launch_bounds__(SO_THREADS) void score_one_kernel(OneArgs a) {
     }
 
     // 3) top-k over the migration keys (sc[t], r n + t), t != s
-    constexpr uint16_t kNone = 0xFFFF;
-    sh.hist[tid] = 0;
-    sh.fill[tid] = 0;
-    __syncthreads();
-    uint16_t code[SO_MAX_N];
-#pragma unroll
-    for (int t = 0; t < SO_MAX_N; ++t) {
-        const bool mig = t < n && s >= 0 && t != s;
-        code[t] = mig ? (uint16_t)key_code((uint64_t)(sc[t] - base)) : kNone;
-        if (mig) atomicAdd(&sh.hist[code[t]], 1);
-    }
     __syncthreads();
     const int h = sh.hist[tid];
     int total;
