@@ -9,11 +9,13 @@ from paper_2510_13668_amd import star, synth
 
 DEV = "cuda"
 E_RTOL = 2e-2        # predicted-length tolerance (relative): the contract
-# A sharper bound the arithmetic supports (derivation in the design notes):
-# with bf16-exact operands, fp32 accumulation and a1 carried as a bf16 hi/lo
-# pair, E's relative error is at most twice the largest absolute logit error,
-# which scales with the second layer's weight norm.  E_TIGHT applies at unit
-# weight scale (W2 ~ N(0, 1/m)); tests scale it by the norm they use.
+# A sharper bound the arithmetic supports: with bf16-exact operands (exact
+# fp32 products), fp32 accumulation and a1 carried as a bf16 hi/lo pair
+# (about 2^-16 relative), a logit's error is at most sum_j |w2_j| |da1_j|,
+# about rms(W2) sqrt(m) max|da1|; since d log p_k / dz = e_k - p, E's
+# relative error is at most twice the largest absolute logit error.  E_TIGHT
+# applies at unit weight scale (W2 ~ N(0, 1/m)); tests scale it by the norm
+# they use.
 E_TIGHT = 1e-3
 
 
