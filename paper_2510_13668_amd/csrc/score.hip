@@ -1811,6 +1811,79 @@ __device__ __forceinline__ int best_sorted(const TopkArgs& a, SelShared<TK_THREA
     return nr;
 }
 
+// The k smallest of a register source's keys (no key below base), in key
+// order: the code histogram gives c*, and every key of code <= c* is
+// compacted and counting-sorted, so (ws_s, ws_i)[0, nr) holds the nr =
+// min(k, keys) smallest and *smax_w the largest of them.  Returns -1 (with
+// the workgroup synchronised) when more than TK_SORT_CAP keys have codes
+// <= c*.
+template <int RJ>
+__device__ __forceinline__ int regs_sorted(const RegKeys<RJ>& keys, int k, int64_t base,
+                                           SelShared<TK_THREADS>& sh, SortLds& sl,
+                                           int64_t* ws_s, uint32_t* ws_i, int64_t* smax_w) {
+    constexpr uint16_t kNone = 0xFFFF;
+    const int tid = threadIdx.x;
+    sh.hist[tid] = 0;
+    sh.fill[tid] = 0;
+    __syncthreads();
+    uint16_t code[RJ];
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+        const bool ok = keys.s[j] != kInfS;
+        code[j] = ok ? (uint16_t)key_code((uint64_t)(keys.s[j] - base)) : kNone;
+        if (ok) atomicAdd(&sh.hist[code[j]], 1);
+    }
+    __syncthreads();
+    const int h = sh.hist[tid];
+    int total;
+    const int before = block_excl_i32<TK_THREADS>(h, sh, &total);
+    const bool all = total <= k;
+    if (all ? tid == RK_CODES - 1 : (before < k && before + h >= k)) {
+        sh.bcast[0] = tid;                                // c*
+        sh.bcast[1] = before + h;                         // keys of code <= c*
+    }
+    sh.hist[tid] = before;                                // code offsets
+    __syncthreads();
+    const uint32_t cstar = (uint32_t)sh.bcast[0];
+    const int nle = sh.bcast[1];
+    if (nle > TK_SORT_CAP) {
+        __syncthreads();
+        return -1;
+    }
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) cnt += code[j] <= cstar ? 1 : 0;
+    int tot;
+    int pos = block_excl_i32<TK_THREADS>(cnt, sh, &tot);
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+        if (code[j] <= cstar) {
+            sl.cs[pos] = keys.s[j];
+            sl.ci[pos] = keys.i[j];
+            sl.cc[pos] = code[j];
+            ++pos;
+        }
+    }
+    __syncthreads();
+    int64_t ks = 0;
+    uint32_t ki = 0;
+    uint16_t kc = 0;
+    if (tid < nle) {
+        ks = sl.cs[tid];
+        ki = sl.ci[tid];
+        kc = sl.cc[tid];
+    }
+    const int nr = k < nle ? k : nle;
+    const int p = sort_place(sh, sl, nle, ks, ki, kc);
+    if (p >= 0 && p < nr) {
+        ws_s[p] = ks;
+        ws_i[p] = ki;
+    }
+    __syncthreads();
+    *smax_w = nr > 0 ? ws_s[nr - 1] : -1;
+    return nr;
+}
+
 // Stage 2 from registers: the k smallest migrations of the nr requests,
 // written in key order.  When nr = k, the k requests' best keys are k
 // distinct migrations, so the k-th smallest migration is at most the largest
@@ -1897,7 +1970,10 @@ __global__ __launch_bounds__(TK_THREADS) void topk_pruned_kernel(TopkArgs a) {
     if constexpr (kStage1 == kStage1Reg) {
         RegKeys<TK_RJ1> keys;
         load_best(keys, a);
-        nr = select_by_code<TK_RJ1>(keys, a.top_k, base, ib1, sh, cl, ws_s, ws_i, &smin, &smax_w);
+        nr = kRJ2 > 0 ? regs_sorted<TK_RJ1>(keys, a.top_k, base, sh, sl, ws_s, ws_i, &smax_w) : -1;
+        if (nr < 0)
+            nr = select_by_code<TK_RJ1>(keys, a.top_k, base, ib1, sh, cl, ws_s, ws_i, &smin,
+                                        &smax_w);
     } else {
         // (the streamed stage 2 keeps the histogram-and-gather stage 1: the
         // two together exceed the registers of a 1024-thread workgroup)

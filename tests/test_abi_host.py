@@ -125,6 +125,9 @@ def test_load_and_score_validation(L):
     assert star.project_load_workspace_size(star.load_params(32768, 64, 64, 1025)) == H
     assert star.project_load_workspace_size(star.load_params(32768, 961, 64, 1024)) == H
     assert star.project_load_workspace_size(star.load_params(8191, 64, 64, 1024)) == H
+    # 16384 requests on 16 instances: 8 slices of 2048
+    assert star.project_load_workspace_size(star.load_params(16384, 16, 64, 512)) == (
+        H + 16 * 8 * 3 * 514 * 8)
     assert L.star_project_load(ctypes.byref(big_lp), f := FAKE, f, f, f, f,
                                H + 64 * 4 * 3 * 1026 * 8 - 1, None) == -4
     f = FAKE

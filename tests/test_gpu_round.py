@@ -161,8 +161,10 @@ def test_crowded_best_code_takes_streamed_stage(fused):
 # (N, n, b, K): the split projection (request slices met by a last arriver)
 # at its boundaries -- the smallest stream, a ragged last slice with a tail
 # of one request, the largest curve -- and the chunked kernel beyond them
-# (more than 1024 buckets, more instances than arrival counters)
+# (one request fewer, more than 1024 buckets, more instances than arrival
+# counters)
 PROJECTION_REGIMES = [
+    (8191, 5, 16, 700),
     (8192, 64, 64, 1024),
     (8193, 3, 16, 1024),
     (12001, 200, 8, 300),
