@@ -62,11 +62,11 @@ def _parse():
     ap.add_argument("--mode", choices=("graph_pipelined", "pipelined", "eager", "graph"),
                     default="graph_pipelined",
                     help="which timing gives `value` (the others are reported beside it): "
-                         "pipelined = prediction of the next round on one stream while the "
-                         "current round is projected and scored on a second (eagerly "
-                         "launched); graph_pipelined = the same, 40 rounds per captured HIP "
-                         "graph; eager = one stream, round after round; graph = one captured "
-                         "graph per round")
+                         "pipelined = predictions on one stream while earlier rounds are "
+                         "projected and scored on a second (eagerly launched); "
+                         "graph_pipelined = the same, 40 rounds per captured HIP graph; "
+                         "eager = one stream, round after round; graph = one captured graph "
+                         "per round")
     ap.add_argument("--cpu-rounds", type=int, default=200,
                     help="rounds of the CPU oracle timed for the baseline (0 = skip)")
     ap.add_argument("--path", choices=("round", "variance", "plan", "mlp4", "sim", "configs"),
@@ -892,15 +892,20 @@ def main():
         return t0.elapsed_time(t1) / args.steps
 
     # Pipelined rounds: round i's prediction needs only round i-1's EMA state,
-    # so it runs on `stream` while round i-1 is projected and scored on
-    # `sched`.  Per-round outputs rotate through NSLOT buffers; an event keeps
-    # a buffer from being overwritten before its scheduling has finished, so
-    # round i's prediction waits for round i - NSLOT's scheduling.
-    # (Measured, graph-replayed: 29.7 us per round with two buffers, 28.1
-    # with three, 28.2 with four; a buffer per round of a captured chunk,
-    # which drops these events, was slower still.)
+    # so it runs on `stream` while earlier rounds are projected and scored on
+    # `sched`.  Scheduling waits for the predictions SCHED_BATCH rounds at a
+    # time (one cross-stream event per batch), then projects and scores each
+    # of them.  Per-round outputs rotate through NSLOT buffers; an event
+    # keeps a buffer from being overwritten before its scheduling has
+    # finished, so round i's prediction waits for round i - NSLOT's
+    # scheduling.  (Measured, graph-replayed, on the current kernels: 28.3 us
+    # per round with three buffers and a wait per round, 27.0 with six
+    # buffers and waits for two rounds at a time, 26.9 for three; without
+    # the buffer-release waits, 33.0.)
     sched = torch.cuda.Stream()
-    NSLOT = 3
+    SCHED_BATCH = 2
+    NSLOT = 6
+    assert NSLOT >= SCHED_BATCH
     slot_buf = []
     for _ in range(NSLOT):
         slot_buf.append(dict(
@@ -915,33 +920,48 @@ def main():
             ts=torch.empty(top_k, dtype=torch.int64, device=dev)))
     ev_pred = [torch.cuda.Event() for _ in range(NSLOT)]
     ev_done = [torch.cuda.Event() for _ in range(NSLOT)]
-    used = [False] * NSLOT
 
-    def pipelined_round(i):
-        step = (i + 1) % S
-        k = i % NSLOT
+    def predict_into(step, k, wait):
         sb = slot_buf[k]
-        if used[k]:
+        if wait:
             stream.wait_event(ev_done[k])
         star.predict(pp, hid[step], w1, None, w2, None, bins, ema, sb["expected"], sb["rem"],
                      ws_p, stream)
-        ev_pred[k].record(stream)
-        sched.wait_event(ev_pred[k])
-        star.project_and_score(sp, cur_steps[step], sb["rem"], inst, sb["load"], sb["scores"],
-                               sb["best_t"], sb["best_s"], sb["tr"], sb["tt"], sb["ts"], ws_s,
-                               sched)
-        ev_done[k].record(sched)
+
+    def schedule(batch):
+        """Scheduling of the rounds in `batch` ((step, slot) pairs, all predicted)."""
+        k_last = batch[-1][1]
+        ev_pred[k_last].record(stream)
+        sched.wait_event(ev_pred[k_last])
+        for step, k in batch:
+            sb = slot_buf[k]
+            star.project_and_score(sp, cur_steps[step], sb["rem"], inst, sb["load"], sb["scores"],
+                                   sb["best_t"], sb["best_s"], sb["tr"], sb["tt"], sb["ts"], ws_s,
+                                   sched)
+            ev_done[k].record(sched)
+
+    used = [False] * NSLOT
+    pending = []
+
+    def pipelined_round(i, last=False):
+        step = (i + 1) % S
+        k = i % NSLOT
+        predict_into(step, k, used[k])
         used[k] = True
+        pending.append((step, k))
+        if len(pending) == SCHED_BATCH or last:
+            schedule(list(pending))
+            pending.clear()
 
     def timed_pipelined():
         for i in range(args.warmup):
-            pipelined_round(i)
+            pipelined_round(i, last=i == args.warmup - 1)
         torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record(stream)
         for i in range(args.steps):
-            pipelined_round(args.warmup + i)
+            pipelined_round(args.warmup + i, last=i == args.steps - 1)
         for k in range(NSLOT):
             stream.wait_event(ev_done[k])
         t1.record(stream)
@@ -960,20 +980,15 @@ def main():
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
             sched.wait_stream(stream)
+            batch = []
             for j in range(length):
                 step = (c0 + j) % S
                 k = j % NSLOT
-                sb = slot_buf[k]
-                if j >= NSLOT:
-                    stream.wait_event(ev_done[k])
-                star.predict(pp, hid[step], w1, None, w2, None, bins, ema, sb["expected"],
-                             sb["rem"], ws_p, stream)
-                ev_pred[k].record(stream)
-                sched.wait_event(ev_pred[k])
-                star.project_and_score(sp, cur_steps[step], sb["rem"], inst, sb["load"],
-                                       sb["scores"], sb["best_t"], sb["best_s"], sb["tr"],
-                                       sb["tt"], sb["ts"], ws_s, sched)
-                ev_done[k].record(sched)
+                predict_into(step, k, j >= NSLOT)
+                batch.append((step, k))
+                if len(batch) == SCHED_BATCH or j == length - 1:
+                    schedule(batch)
+                    batch = []
             stream.wait_stream(sched)
         return g
 
@@ -1070,9 +1085,11 @@ def main():
         "us_per_round_graph": ms_mode["graph"] * 1e3,
         "timing": {"headline": args.mode, "rounds_timed": args.steps,
                    "warmup_rounds": args.warmup,
-                   "overlap": "graph_pipelined and pipelined time throughput: round i+1's "
-                              "prediction runs while round i is projected and scored; "
-                              "us_per_round_eager (p50/p99) is one round's latency"},
+                   "overlap": "graph_pipelined and pipelined time throughput: later rounds' "
+                              "predictions run while earlier rounds are projected and scored "
+                              "(scheduling waits for the predictions %d rounds at a time, outputs "
+                              "rotate through %d buffers); us_per_round_eager (p50/p99) is one "
+                              "round's latency" % (SCHED_BATCH, NSLOT)},
         "roofline": {"kernel": "star_predict = gemm1_splitk_kernel (bf16 MFMA, H[1024,4096] x "
                                "W1[512,4096]^T, 4 K-splits) + head_kernel (split reduction, GELU, "
                                "x W2[64,512]^T, softmax, EMA)",

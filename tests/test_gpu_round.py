@@ -345,18 +345,19 @@ def test_graph_replay_matches_eager():
 
 
 def test_pipelined_graph_rounds_match_eager():
-    """Rounds pipelined on two streams: round i is predicted on one stream
-    while round i-1 is projected and scored on a second.  The per-round
-    outputs rotate through three buffers, as in the benchmark, and events
-    order the rounds.  The whole chunk is captured as one HIP graph, as the
-    benchmark runs it.  Every replay (with eager work and synchronisations
-    between replays) must leave the last three rounds' outputs and the EMA
-    state equal to eight eager rounds run one after another.  The pipelined
-    rounds use the fused projection-and-scoring call, the eager ones the two
-    separate calls."""
+    """Rounds pipelined on two streams, as the benchmark runs them: the
+    predictions run on one stream while earlier rounds are projected and
+    scored on a second, which waits for the predictions two rounds at a
+    time.  The per-round outputs rotate through six buffers, and events
+    order the rounds.  The whole chunk is captured as one HIP graph.  Every
+    replay (with eager work and synchronisations between replays) must leave
+    the last six rounds' outputs and the EMA state equal to eight eager
+    rounds run one after another.  The pipelined rounds use the fused
+    projection-and-scoring call, the eager ones the two separate calls."""
     wl = synth.WORKLOADS["continuous"]
     R = 8
-    NS = 3
+    NS = 6
+    BATCH = 2
     x = synth.make_inputs(wl, steps=R + 1)
     hid = to_dev(x.hidden, True)
     N = wl.n_req
@@ -387,16 +388,21 @@ def test_pipelined_graph_rounds_match_eager():
 
     def chunk():
         S2.wait_stream(P)
+        batch = []
         for j in range(R):
             k = j % NS
             if j >= NS:
                 P.wait_event(ev_done[k])
             star.predict(pp, hid[j + 1], pr.w1, pr.b1, pr.w2, pr.b2, pr.bins, pr.ema, exps[k],
                          rems[k], pr.ws, P)
-            ev_pred[k].record(P)
-            S2.wait_event(ev_pred[k])
-            slots[k].run(curs[j + 1], rems[k], inst, stream=S2)
-            ev_done[k].record(S2)
+            batch.append((j, k))
+            if len(batch) == BATCH or j == R - 1:
+                ev_pred[k].record(P)
+                S2.wait_event(ev_pred[k])
+                for bj, bk in batch:
+                    slots[bk].run(curs[bj + 1], rems[bk], inst, stream=S2)
+                    ev_done[bk].record(S2)
+                batch = []
         P.wait_stream(S2)
 
     torch.cuda.synchronize()
@@ -415,7 +421,7 @@ def test_pipelined_graph_rounds_match_eager():
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        for j in (R - 3, R - 2, R - 1):
+        for j in range(R - NS, R):
             assert_round_equal(slots[j % NS].result(), want[j])
         np.testing.assert_array_equal(pr.ema.cpu().numpy(), want_ema)
         _ = torch.ones(1000, device="cuda").sum().item()    # unrelated eager work between replays
