@@ -344,3 +344,58 @@ def test_random_shapes_every_head_variant():
               flush=True)
         _run_case(h, w1, w2, synth.bin_values(nb, 1.0, 32768.0), dtype=dtype, act=act, b1=b1,
                   b2=b2, len_max=32768, sample=sample)
+
+
+def _gelu64(z):
+    from scipy.special import erf
+    return 0.5 * z * (1.0 + erf(z / np.sqrt(2.0)))
+
+
+@pytest.mark.parametrize("B,d,m,dtype", [(1024, 4096, 512, synth.BF16), (8192, 4096, 512, synth.BF16),
+                                         (300, 2048, 1024, synth.BF16),
+                                         (8200, 512, 2048, synth.BF16),
+                                         (64, 1024, 256, synth.F32)])
+def test_first_layer_activations_read_through_two_bins(B, d, m, dtype):
+    """The first layer's activations a1 = act(H W1^T), element by element.
+    With two bins, W2 = [0; e_i] and bin values (1, 2), the head computes
+    E = 1 + sigmoid(a1_i), so a1_i = logit(E - 1) for every row.  Four hidden
+    units per shape (both ends, the middle, one past a 64-column tile edge),
+    against fp64 H W1^T and an exact erf (ReLU for fp32, as the tiny
+    workload).  A dropped K-tile, a misplaced column or a wrong activation
+    moves a1 by orders of magnitude more than the bound, which is the bf16
+    hi/lo pair carrying a1 (about 2^-16 relative) plus fp32 accumulation and
+    the fp32 softmax."""
+    rng = np.random.default_rng(B + d + m)
+    bf = dtype == synth.BF16
+    hf = rng.standard_normal((B, d)).astype(np.float32)
+    wf = (rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32)
+    if bf:
+        hb, wb = synth.f32_to_bf16_bits(hf), synth.f32_to_bf16_bits(wf)
+        h = synth.bf16_bits_to_f32(hb).astype(np.float64)
+        w = synth.bf16_bits_to_f32(wb).astype(np.float64)
+        act = synth.ACT_GELU
+    else:
+        hb, wb = hf, wf
+        h, w = hf.astype(np.float64), wf.astype(np.float64)
+        act = synth.ACT_RELU
+    bins = np.array([1.0, 2.0], np.float32)
+    units = [0, 65, m // 2, m - 1]
+    z = h @ w[units].T                               # [B, 4]
+    a_ref = _gelu64(z) if bf else np.maximum(z, 0.0)
+    hd = to_dev(hb, bf)
+    worst = 0.0
+    for q, i in enumerate(units):
+        w2 = np.zeros((2, m), np.float32)
+        w2[1, i] = 1.0
+        pr = Predictor(wb, synth.f32_to_bf16_bits(w2) if bf else w2, bins, dtype=dtype,
+                       act=act, n_req=B, len_max=2)
+        pr.run(hd)
+        torch.cuda.synchronize()
+        p1 = pr.expected.cpu().numpy().astype(np.float64) - 1.0
+        a_gpu = np.log(p1 / (1.0 - p1))
+        err = np.abs(a_gpu - a_ref[:, q]) / np.maximum(1.0, np.abs(a_ref[:, q]))
+        worst = max(worst, float(err.max()))
+        print(f"  B={B} d={d} m={m} unit {i}: max err {err.max():.2e}", flush=True)
+    # fp32 E near 1.5 resolves p1 to ~1.2e-7, i.e. a1 to ~5e-7; the hi/lo
+    # pair and the accumulation stay below 1e-4 of max(1, |a1|)
+    assert worst < 1e-4
