@@ -399,3 +399,35 @@ def test_first_layer_activations_read_through_two_bins(B, d, m, dtype):
     # fp32 E near 1.5 resolves p1 to ~1.2e-7, i.e. a1 to ~5e-7; the hi/lo
     # pair and the accumulation stay below 1e-4 of max(1, |a1|)
     assert worst < 1e-4
+
+
+@pytest.mark.parametrize("B,d,m,dtype", [(1024, 4096, 512, synth.BF16), (8200, 512, 2048, synth.BF16),
+                                         (64, 1024, 256, synth.F32)])
+def test_second_layer_logit_read_through_two_bins(B, d, m, dtype):
+    """The second product for random weights: with two bins of values (1, 2),
+    E = 1 + sigmoid(z_1 - z_0), so every row's logit difference
+    (w2_1 - w2_0) . a1 is read back as logit(E - 1) and compared with fp64
+    (H W1^T, exact erf or ReLU, then the product)."""
+    rng = np.random.default_rng(7 * B + m)
+    bf = dtype == synth.BF16
+    hf = rng.standard_normal((B, d)).astype(np.float32)
+    wf = (rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32)
+    w2f = (rng.standard_normal((2, m)) / np.sqrt(m)).astype(np.float32)
+    if bf:
+        hb, wb, w2b = (synth.f32_to_bf16_bits(a) for a in (hf, wf, w2f))
+        h, w, w2 = (synth.bf16_bits_to_f32(a).astype(np.float64) for a in (hb, wb, w2b))
+        a1 = _gelu64(h @ w.T)
+    else:
+        hb, wb, w2b = hf, wf, w2f
+        h, w, w2 = hf.astype(np.float64), wf.astype(np.float64), w2f.astype(np.float64)
+        a1 = np.maximum(h @ w.T, 0.0)
+    zd_ref = a1 @ (w2[1] - w2[0])
+    pr = Predictor(wb, w2b, np.array([1.0, 2.0], np.float32), dtype=dtype,
+                   act=synth.ACT_GELU if bf else synth.ACT_RELU, n_req=B, len_max=2)
+    pr.run(to_dev(hb, bf))
+    torch.cuda.synchronize()
+    p1 = pr.expected.cpu().numpy().astype(np.float64) - 1.0
+    zd = np.log(p1 / (1.0 - p1))
+    err = np.abs(zd - zd_ref) / np.maximum(1.0, np.abs(zd_ref))
+    print(f"  B={B} d={d} m={m}: max logit-difference err {err.max():.2e}", flush=True)
+    assert err.max() < 1e-4
