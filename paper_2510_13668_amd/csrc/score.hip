@@ -1743,12 +1743,21 @@ __device__ __forceinline__ int best_sorted(const TopkArgs& a, SelShared<TK_THREA
     }
     sh.hist[tid] = 0;
     sh.fill[tid] = 0;
-    __syncthreads();
-    // code u of group j (kNoCode past N)
-    auto code = [&](int j, int u) -> uint16_t {
+    // codes past N read as kNoCode from here on (masked once, in registers)
+#pragma unroll
+    for (int j = 0; j < TK_CODE_V; ++j) {
         const int v = j * TK_THREADS + tid;
-        return v < nv && v * 8 + u < a.N ? code_of(cv[j], u) : kNoCode;
-    };
+        const int valid = v < nv ? a.N - v * 8 : 0;      // codes of this group below N
+        auto pad = [valid](int d) -> uint32_t {      // kNoCode in slots 2d, 2d+1 past N
+            return (2 * d >= valid ? 0x0000FFFFu : 0u) | (2 * d + 1 >= valid ? 0xFFFF0000u : 0u);
+        };
+        cv[j].x |= pad(0);
+        cv[j].y |= pad(1);
+        cv[j].z |= pad(2);
+        cv[j].w |= pad(3);
+    }
+    __syncthreads();
+    auto code = [&](int j, int u) -> uint16_t { return code_of(cv[j], u); };
 #pragma unroll
     for (int j = 0; j < TK_CODE_V; ++j)
 #pragma unroll
@@ -1773,24 +1782,26 @@ __device__ __forceinline__ int best_sorted(const TopkArgs& a, SelShared<TK_THREA
         __syncthreads();
         return -1;
     }
-    int cnt = 0;
+    // which of this thread's codes are <= c*, as one bit each; their
+    // compacted positions follow a block prefix of the bit counts
+    uint32_t sel = 0;
 #pragma unroll
     for (int j = 0; j < TK_CODE_V; ++j)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) cnt += code(j, u) <= cstar ? 1 : 0;
+        for (int u = 0; u < 8; ++u) sel |= (code(j, u) <= cstar ? 1u : 0u) << (j * 8 + u);
     int tot;
-    int pos = block_excl_i32<TK_THREADS>(cnt, sh, &tot);
+    int pos = block_excl_i32<TK_THREADS>(__builtin_popcount(sel), sh, &tot);
+    if (sel) {                                            // few threads have any
 #pragma unroll
-    for (int j = 0; j < TK_CODE_V; ++j)
+        for (int j = 0; j < TK_CODE_V; ++j)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const uint16_t c = code(j, u);
-            if (c <= cstar) {
-                sl.ci[pos] = (uint32_t)((j * TK_THREADS + tid) * 8 + u);
-                sl.cc[pos] = c;
-                ++pos;
-            }
-        }
+            for (int u = 0; u < 8; ++u)
+                if (sel & (1u << (j * 8 + u))) {
+                    sl.ci[pos] = (uint32_t)((j * TK_THREADS + tid) * 8 + u);
+                    sl.cc[pos] = code(j, u);
+                    ++pos;
+                }
+    }
     __syncthreads();
     int64_t s = 0;
     uint32_t r = 0;
