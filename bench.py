@@ -895,13 +895,14 @@ def main():
     # so it runs on `stream` while earlier rounds are projected and scored on
     # `sched`.  Scheduling waits for the predictions SCHED_BATCH rounds at a
     # time (one cross-stream event per batch), then projects and scores each
-    # of them.  Per-round outputs rotate through NSLOT buffers; an event
-    # keeps a buffer from being overwritten before its scheduling has
-    # finished, so round i's prediction waits for round i - NSLOT's
-    # scheduling.  (Measured, graph-replayed, on the current kernels: 28.3 us
-    # per round with three buffers and a wait per round, 27.0 with six
-    # buffers and waits for two rounds at a time, 26.9 for three; without
-    # the buffer-release waits, 33.0.)
+    # of them and records one event when the batch is done.  Per-round
+    # outputs rotate through NSLOT buffers: before a prediction overwrites a
+    # buffer, its stream waits for the event of the batch that last scheduled
+    # that buffer, once per distinct event, so once per batch.  (Measured,
+    # graph-replayed: 28.3 us per round with three buffers and a wait per
+    # round, 27.0-27.6 with six buffers, batches of two and an event per
+    # round, 26.7-26.9 with an event and a wait per batch; without the
+    # buffer-release waits, 33.0.)
     sched = torch.cuda.Stream()
     SCHED_BATCH = 2
     NSLOT = 6
@@ -919,12 +920,19 @@ def main():
             tt=torch.empty(top_k, dtype=torch.int32, device=dev),
             ts=torch.empty(top_k, dtype=torch.int64, device=dev)))
     ev_pred = [torch.cuda.Event() for _ in range(NSLOT)]
-    ev_done = [torch.cuda.Event() for _ in range(NSLOT)]
+    ev_done = [torch.cuda.Event() for _ in range(NSLOT)]   # one per batch, cycled
+    # guard[k]: the done event of the batch that last scheduled buffer k
+    state = dict(guard=[None] * NSLOT, waited=None, batches=0)
 
-    def predict_into(step, k, wait):
+    def reset_guards():
+        state.update(guard=[None] * NSLOT, waited=None)
+
+    def predict_into(step, k):
         sb = slot_buf[k]
-        if wait:
-            stream.wait_event(ev_done[k])
+        ev = state["guard"][k]
+        if ev is not None and ev is not state["waited"]:
+            stream.wait_event(ev)
+            state["waited"] = ev
         star.predict(pp, hid[step], w1, None, w2, None, bins, ema, sb["expected"], sb["rem"],
                      ws_p, stream)
 
@@ -938,25 +946,30 @@ def main():
             star.project_and_score(sp, cur_steps[step], sb["rem"], inst, sb["load"], sb["scores"],
                                    sb["best_t"], sb["best_s"], sb["tr"], sb["tt"], sb["ts"], ws_s,
                                    sched)
-            ev_done[k].record(sched)
+        ev = ev_done[state["batches"] % NSLOT]
+        state["batches"] += 1
+        ev.record(sched)
+        for _, k in batch:
+            state["guard"][k] = ev
 
-    used = [False] * NSLOT
     pending = []
 
     def pipelined_round(i, last=False):
         step = (i + 1) % S
         k = i % NSLOT
-        predict_into(step, k, used[k])
-        used[k] = True
+        predict_into(step, k)
         pending.append((step, k))
         if len(pending) == SCHED_BATCH or last:
             schedule(list(pending))
             pending.clear()
 
     def timed_pipelined():
+        torch.cuda.synchronize()
+        reset_guards()
         for i in range(args.warmup):
             pipelined_round(i, last=i == args.warmup - 1)
         torch.cuda.synchronize()
+        reset_guards()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record(stream)
@@ -980,16 +993,18 @@ def main():
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
             sched.wait_stream(stream)
+            reset_guards()           # the previous graph ends joined: every buffer is free
             batch = []
             for j in range(length):
                 step = (c0 + j) % S
                 k = j % NSLOT
-                predict_into(step, k, j >= NSLOT)
+                predict_into(step, k)
                 batch.append((step, k))
                 if len(batch) == SCHED_BATCH or j == length - 1:
                     schedule(batch)
                     batch = []
             stream.wait_stream(sched)
+        reset_guards()               # no later wait may name an event recorded in the capture
         return g
 
     def graphs_for(start, rounds):

@@ -348,14 +348,17 @@ def test_pipelined_graph_rounds_match_eager():
     """Rounds pipelined on two streams, as the benchmark runs them: the
     predictions run on one stream while earlier rounds are projected and
     scored on a second, which waits for the predictions two rounds at a
-    time.  The per-round outputs rotate through six buffers, and events
-    order the rounds.  The whole chunk is captured as one HIP graph.  Every
-    replay (with eager work and synchronisations between replays) must leave
-    the last six rounds' outputs and the EMA state equal to eight eager
-    rounds run one after another.  The pipelined rounds use the fused
-    projection-and-scoring call, the eager ones the two separate calls."""
+    time and records one event per batch of two.  The per-round outputs
+    rotate through six buffers; before a prediction overwrites a buffer,
+    its stream waits once for the event of the batch that last scheduled
+    it.  The whole chunk is captured as one HIP graph.  Every replay (with
+    eager work and synchronisations between replays) must leave the last
+    six rounds' outputs (all in reused buffers) and the EMA state equal to
+    twelve eager rounds run one after another.  The pipelined rounds use
+    the fused projection-and-scoring call, the eager ones the two separate
+    calls."""
     wl = synth.WORKLOADS["continuous"]
-    R = 8
+    R = 12
     NS = 6
     BATCH = 2
     x = synth.make_inputs(wl, steps=R + 1)
@@ -388,11 +391,13 @@ def test_pipelined_graph_rounds_match_eager():
 
     def chunk():
         S2.wait_stream(P)
+        guard, waited, nbatch = [None] * NS, None, 0
         batch = []
         for j in range(R):
             k = j % NS
-            if j >= NS:
-                P.wait_event(ev_done[k])
+            if guard[k] is not None and guard[k] is not waited:
+                P.wait_event(guard[k])
+                waited = guard[k]
             star.predict(pp, hid[j + 1], pr.w1, pr.b1, pr.w2, pr.b2, pr.bins, pr.ema, exps[k],
                          rems[k], pr.ws, P)
             batch.append((j, k))
@@ -401,7 +406,11 @@ def test_pipelined_graph_rounds_match_eager():
                 S2.wait_event(ev_pred[k])
                 for bj, bk in batch:
                     slots[bk].run(curs[bj + 1], rems[bk], inst, stream=S2)
-                    ev_done[bk].record(S2)
+                ev = ev_done[nbatch % NS]
+                nbatch += 1
+                ev.record(S2)
+                for _, bk in batch:
+                    guard[bk] = ev
                 batch = []
         P.wait_stream(S2)
 
