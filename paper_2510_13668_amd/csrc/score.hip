@@ -112,12 +112,6 @@ __device__ inline uint32_t fast_div(uint32_t x, uint32_t d, uint32_t m) {
 }
 static uint32_t div_magic(uint32_t d) { return d == 1 ? 0u : (uint32_t)(0xFFFFFFFFull / d) + 1u; }
 
-__device__ inline int64_t readlane_i64(int64_t v, int lane) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), lane);
-    return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
 // Value of lane l - 1 (lane 0 gets `ident`): DPP wave_shr:1.
 __device__ inline int64_t wave_shr1_i64(int64_t v, int64_t ident) {
     constexpr int kWaveShr1 = 0x138;

@@ -111,6 +111,13 @@ __device__ inline int64_t wave_incl_max_i64(int64_t v) {
     return v;
 }
 
+// The value of `lane` (wave-uniform) broadcast to every lane.
+__device__ inline int64_t readlane_i64(int64_t v, int lane) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), lane);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 // v plus the value of its DPP source lane (0 where there is none).
 template <int kCtrl, int kRowMask>
 __device__ inline int64_t dpp_add_i64(int64_t v) {
@@ -135,6 +142,7 @@ __device__ inline int64_t wave_incl_add_i64(int64_t v) {
 template <int kT>
 __device__ inline void block_incl_add2_i64(int64_t& x, int64_t& y, int64_t* tmp) {
     constexpr int W = kT / kWave;
+    static_assert(W <= kWave, "one wave reads every wave's total");
     const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
     x = wave_incl_add_i64(x);
     y = wave_incl_add_i64(y);
@@ -143,13 +151,11 @@ __device__ inline void block_incl_add2_i64(int64_t& x, int64_t& y, int64_t* tmp)
         tmp[W + wid] = y;
     }
     __syncthreads();
-    int64_t bx = 0, by = 0;
-    for (int w = 0; w < wid; ++w) {
-        bx += tmp[w];
-        by += tmp[W + w];
-    }
-    x += bx;
-    y += by;
+    // the totals of the waves before this one: lane w < wid reads wave w's,
+    // all at once, and a wave sum adds them
+    const int64_t tx = lane < W ? tmp[lane] : 0, ty = lane < W ? tmp[W + lane] : 0;
+    x += readlane_i64(wave_incl_add_i64(lane < wid ? tx : 0), kWave - 1);
+    y += readlane_i64(wave_incl_add_i64(lane < wid ? ty : 0), kWave - 1);
     __syncthreads();
 }
 
@@ -158,6 +164,7 @@ __device__ inline void block_incl_add2_i64(int64_t& x, int64_t& y, int64_t* tmp)
 template <int kT>
 __device__ inline void block_incl_max2_i64(int64_t& x, int64_t& y, int64_t* tmp) {
     constexpr int W = kT / kWave;
+    static_assert(W <= kWave, "one wave reads every wave's maximum");
     const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
     x = wave_incl_max_i64(x);
     y = wave_incl_max_i64(y);
@@ -166,10 +173,12 @@ __device__ inline void block_incl_max2_i64(int64_t& x, int64_t& y, int64_t* tmp)
         tmp[W + wid] = y;
     }
     __syncthreads();
-    for (int w = 0; w < wid; ++w) {
-        x = tmp[w] > x ? tmp[w] : x;
-        y = tmp[W + w] > y ? tmp[W + w] : y;
-    }
+    // the maxima of the waves before this one, read all at once
+    const int64_t tx = lane < W ? tmp[lane] : INT64_MIN, ty = lane < W ? tmp[W + lane] : INT64_MIN;
+    const int64_t mx = readlane_i64(wave_incl_max_i64(lane < wid ? tx : INT64_MIN), kWave - 1);
+    const int64_t my = readlane_i64(wave_incl_max_i64(lane < wid ? ty : INT64_MIN), kWave - 1);
+    x = mx > x ? mx : x;
+    y = my > y ? my : y;
     __syncthreads();
 }
 
