@@ -482,6 +482,50 @@ def test_random_rounds_every_ranking_regime():
             _check(cur, rem, inst, n, b, K, top_k, fused=fused)
 
 
+def _wide_round_case(rng, kind):
+    """Sizes beyond the ranking regimes: the split projection near its
+    largest K, fewer requests than buckets (instance-major planes), the
+    one-workgroup round, and broad mixes; top_k = 0 included."""
+    if kind == 0:     # 8192+ requests, K up to 1024: the sliced projection
+        N, n, K = int(rng.integers(8192, 40000)), int(rng.integers(1, 100)), int(rng.integers(200, 1025))
+    elif kind == 1:   # fewer requests than buckets
+        N, n, K = int(rng.integers(1, 2000)), int(rng.integers(2, 70)), int(rng.integers(1000, 4097))
+    elif kind == 2:   # the whole round in one workgroup
+        N, n = int(rng.integers(1, 1025)), int(rng.integers(1, 9))
+        K = int(rng.integers(1, 2600 // n))
+    else:
+        N, n, K = int(rng.integers(1, 20000)), int(rng.integers(1, 129)), int(rng.integers(1, 1100))
+    while N * n * K > 1.5e9:
+        K = max(1, K // 2)
+    b = int(rng.choice([1, 3, 16, 64]))
+    top_k = int(rng.choice([0, 1, 17, 256, 1024]))
+    H = b * K
+    if rng.random() < 0.4:
+        d = int(rng.integers(1, 6))
+        cv = rng.integers(1, 5000, size=d)
+        lv = rng.integers(1, H + 10, size=d)
+        pick = rng.integers(0, d, size=N)
+        cur, rem = cv[pick].astype(np.int32), lv[pick].astype(np.int32)
+        live = max(1, n - int(rng.integers(0, 2)))
+        inst = rng.integers(0, live, size=N).astype(np.int32)
+    else:
+        cur, rem, inst = synth.random_requests(rng, N, n, cur_hi=int(rng.integers(1, 30000)),
+                                               len_hi=int(rng.integers(1, 3 * H + 2)))
+    return cur, rem, inst, n, b, K, top_k
+
+
+def test_random_rounds_wide_regimes():
+    """40 seeded random rounds over the projection and scoring paths (sliced
+    projection up to K = 1024, instance-major planes up to K = 4096, the
+    one-workgroup round, broad mixes, with and without a top-k), each as two
+    calls and as one; bit-exact."""
+    rng = np.random.default_rng(13668)
+    for c in range(40):
+        cur, rem, inst, n, b, K, top_k = _wide_round_case(rng, c % 4)
+        for fused in (False, True):
+            _check(cur, rem, inst, n, b, K, top_k, fused=fused)
+
+
 @pytest.mark.parametrize("N", [3, 4099, 8195])
 def test_projection_of_misaligned_request_arrays(N):
     """Request arrays that start 4 bytes past a 16-byte boundary take the
