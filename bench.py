@@ -849,6 +849,9 @@ def main():
     sp = star.score_params(N, n, b, K, top_k)
     ws_p = star.Workspace(star.predict_workspace_size(pp))
     ws_s = star.Workspace(star.project_and_score_workspace_size(sp))
+    # the pipelined modes' predictions: star_predict_overlap with the split-K
+    # partials alternating between two workspaces
+    ws_ov = [ws_p, star.Workspace(star.predict_workspace_size(pp))]
 
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()
@@ -893,7 +896,9 @@ def main():
 
     # Pipelined rounds: round i's prediction needs only round i-1's EMA state,
     # so it runs on `stream` while earlier rounds are projected and scored on
-    # `sched`.  Scheduling waits for the predictions SCHED_BATCH rounds at a
+    # `sched`.  The predictions go through star_predict_overlap: one launch
+    # runs round i's head and round i+1's first-layer product (a sequence
+    # starts with a product-only call and ends with a head-only one).  Scheduling waits for the predictions SCHED_BATCH rounds at a
     # time (one cross-stream event per batch), then projects and scores each
     # of them and records one event when the batch is done.  Per-round
     # outputs rotate through NSLOT buffers: before a prediction overwrites a
@@ -927,14 +932,23 @@ def main():
     def reset_guards():
         state.update(guard=[None] * NSLOT, waited=None)
 
-    def predict_into(step, k):
+    def prime(step, j):
+        """The product of the first round j of a sequence (no head)."""
+        star.predict_overlap(pp, hid[step], ws_ov[j % 2], None, w1, None, w2, None, bins,
+                             None, None, None, stream)
+
+    def predict_into(step_next, j, k):
+        """Round j's head into buffer k, and round j+1's product (step_next,
+        or none at the end of a sequence)."""
         sb = slot_buf[k]
         ev = state["guard"][k]
         if ev is not None and ev is not state["waited"]:
             stream.wait_event(ev)
             state["waited"] = ev
-        star.predict(pp, hid[step], w1, None, w2, None, bins, ema, sb["expected"], sb["rem"],
-                     ws_p, stream)
+        nxt = hid[step_next] if step_next is not None else None
+        star.predict_overlap(pp, nxt, ws_ov[(j + 1) % 2] if nxt is not None else None,
+                             ws_ov[j % 2], w1, None, w2, None, bins, ema, sb["expected"],
+                             sb["rem"], stream)
 
     def schedule(batch):
         """Scheduling of the rounds in `batch` ((step, slot) pairs, all predicted)."""
@@ -954,10 +968,12 @@ def main():
 
     pending = []
 
-    def pipelined_round(i, last=False):
+    def pipelined_round(i, first=False, last=False):
         step = (i + 1) % S
         k = i % NSLOT
-        predict_into(step, k)
+        if first:
+            prime(step, i)
+        predict_into(None if last else (i + 2) % S, i, k)
         pending.append((step, k))
         if len(pending) == SCHED_BATCH or last:
             schedule(list(pending))
@@ -967,14 +983,14 @@ def main():
         torch.cuda.synchronize()
         reset_guards()
         for i in range(args.warmup):
-            pipelined_round(i, last=i == args.warmup - 1)
+            pipelined_round(i, first=i == 0, last=i == args.warmup - 1)
         torch.cuda.synchronize()
         reset_guards()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record(stream)
         for i in range(args.steps):
-            pipelined_round(args.warmup + i, last=i == args.steps - 1)
+            pipelined_round(args.warmup + i, first=i == 0, last=i == args.steps - 1)
         for k in range(NSLOT):
             stream.wait_event(ev_done[k])
         t1.record(stream)
@@ -995,10 +1011,11 @@ def main():
             sched.wait_stream(stream)
             reset_guards()           # the previous graph ends joined: every buffer is free
             batch = []
+            prime(c0 % S, 0)
             for j in range(length):
                 step = (c0 + j) % S
                 k = j % NSLOT
-                predict_into(step, k)
+                predict_into((c0 + j + 1) % S if j + 1 < length else None, j, k)
                 batch.append((step, k))
                 if len(batch) == SCHED_BATCH or j == length - 1:
                     schedule(batch)
@@ -1058,14 +1075,22 @@ def main():
     ms_mode["graph_pipelined"] = timed_graph_pipelined()
     ms_step = ms_mode[args.mode]
 
-    # Dominant work of the round: the predictor, star_predict.  At this size
-    # it is two kernels (the split-K first-layer product, then the head that
-    # reduces the splits and runs the second product, softmax and EMA); one
-    # pair of HIP events brackets each call on the stream it is launched on,
-    # over `steps` calls of the round's own inputs.  The split between the
-    # two kernels comes from the committed rocprofv3 summary.
+    # Dominant work of the round: the predictions.  The pipelined modes make
+    # them with star_predict_overlap, one launch of predict_overlap_kernel
+    # per round (one batch's split-K first-layer product and the previous
+    # batch's head: split reduction, GELU, second product, softmax, EMA).
+    # One pair of HIP events brackets each call on the stream it is launched
+    # on, over `steps` back-to-back calls of the round's own inputs.
+    # star_predict (the two kernels one after the other) is timed the same
+    # way beside it.
     he = HipEvents()
-    kern_s = he.time_calls(lambda i: star.predict(pp, hid[(i + 1) % S], w1, None, w2, None, bins,
+    with torch.cuda.stream(stream):
+        prime(1, 0)
+    kern_s = he.time_calls(
+        lambda i: star.predict_overlap(pp, hid[(i + 2) % S], ws_ov[(i + 1) % 2], ws_ov[i % 2],
+                                       w1, None, w2, None, bins, ema, expected, rem, stream),
+        args.steps, stream)
+    pred_s = he.time_calls(lambda i: star.predict(pp, hid[(i + 1) % S], w1, None, w2, None, bins,
                                                   ema, expected, rem, ws_p, stream),
                            args.steps, stream)
     flops = 2.0 * N * d * m + 2.0 * N * m * nb
@@ -1105,14 +1130,17 @@ def main():
                               "(scheduling waits for the predictions %d rounds at a time, outputs "
                               "rotate through %d buffers); us_per_round_eager (p50/p99) is one "
                               "round's latency" % (SCHED_BATCH, NSLOT)},
-        "roofline": {"kernel": "star_predict = gemm1_splitk_kernel (bf16 MFMA, H[1024,4096] x "
-                               "W1[512,4096]^T, 4 K-splits) + head_kernel (split reduction, GELU, "
-                               "x W2[64,512]^T, softmax, EMA)",
+        "roofline": {"kernel": "predict_overlap_kernel<4> (star_predict_overlap): one batch's "
+                               "first-layer product, bf16 MFMA H[1024,4096] x W1[512,4096]^T in 4 "
+                               "K-splits, and the previous batch's head (split reduction, GELU, "
+                               "x W2[64,512]^T, softmax, EMA) in one launch",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic(),
                      "avg_call_us": kern_s * 1e6, "algorithmic_flop": flops,
-                     "kernels": committed_kernel_split()},
+                     "kernels": committed_kernel_split(),
+                     "star_predict_call_us": pred_s * 1e6,
+                     "star_predict_tflops": flops / pred_s / 1e12},
     }
     if args.cpu_rounds > 0:
         out["cpu_baseline"] = cpu_baseline(x, wl, min(args.cpu_rounds, S),

@@ -114,6 +114,44 @@ star_status star_predict(const star_predict_params* p, const void* hidden, const
                          int32_t* rem_len, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * (a) across consecutive batches: the same results as star_predict, with
+ * one batch's head and the next batch's first-layer product in one launch.
+ * Section 4.3 re-predicts at every decode step, and the first layer of step
+ * i + 1 needs only that step's hidden states, not step i's outputs.
+ *
+ * star_predict splits into a product (hidden -> the split-K partials in the
+ * workspace) and a head (partials -> E, EMA, rem_len).  A call does:
+ *   - ws_prev != NULL: the head of the batch whose product an earlier call
+ *     left in ws_prev, writing expected_len, ema_state and rem_len;
+ *   - hidden_next != NULL: the product of hidden_next into ws_next.
+ * At least one of the two.  A sequence over batches h_0, h_1, ... with
+ * workspaces alternating between two buffers A and B:
+ *     (h_0 -> A), (A -> out_0, h_1 -> B), (B -> out_1, h_2 -> A), ...,
+ *     (last -> out_last)
+ * gives out_i equal to star_predict on h_i, bit for bit, with the EMA
+ * carried across the calls in order.  Every call's w1, b1, w2, b2,
+ * bin_values and params (p) must be the same, except p->ema_init, which
+ * applies to the head the call runs.
+ *
+ * Arguments as for star_predict.  w1 may be NULL when hidden_next is NULL;
+ * w2, bin_values, expected_len, ema_state and rem_len may be NULL when
+ * ws_prev is NULL.  ws_next and ws_prev: each star_predict_workspace_size(p)
+ * bytes (ws_bytes), 256-byte aligned, not overlapping; ws_prev keeps the
+ * product of the call that filled it until its head has run.
+ * Errors: STAR_ERR_UNSUPPORTED for shapes star_predict runs as one kernel
+ * (one K-slice) or with the K-chunked head (bf16 batches of 8192 rows and
+ * more with at most 4 K-splits); STAR_ERR_INVALID_ARG when both sides are
+ * NULL or the workspaces overlap; otherwise as star_predict.
+ * One launch where the product takes 64 x 64 tiles (bf16), else the head
+ * and the product as two launches on `stream`.
+ * ---------------------------------------------------------------------- */
+star_status star_predict_overlap(const star_predict_params* p, const void* hidden_next,
+                                 void* ws_next, const void* ws_prev, const void* w1,
+                                 const float* b1, const void* w2, const float* b2,
+                                 const float* bin_values, float* ema_state, float* expected_len,
+                                 int32_t* rem_len, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * (a) without allocation, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc).  Same arguments, results and kernels as star_predict, minus

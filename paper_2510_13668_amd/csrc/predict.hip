@@ -245,10 +245,10 @@ __device__ __forceinline__ void g1_step(const G1Ctx& c, char (*lds)[SH::LDS_A + 
 struct G1Work {
     int split, tile, tm, tn, kt0, nk;
 };
-__device__ inline G1Work g1_work(int splits, int tiles_n, int ktiles) {
+__device__ inline G1Work g1_work(int splits, int tiles_n, int ktiles, int bid, int nblocks) {
     G1Work w;
-    const int logical = xcd_logical_block(blockIdx.x, gridDim.x);
-    const int tiles = gridDim.x / splits;
+    const int logical = xcd_logical_block(bid, nblocks);
+    const int tiles = nblocks / splits;
     w.split = logical / tiles;
     w.tile = logical % tiles;
     w.tm = w.tile / tiles_n;
@@ -393,19 +393,20 @@ __device__ __forceinline__ void g1_mainloop(const char* A, const char* W, int M,
         g1_mainloop_edge<kElemBytes, NS, SH>(c, w, lds, wm, wn, lane, acc);
 }
 
-// Split-K product P[split] = A[:, Ks] W[:, Ks]^T over one BM x BN tile.
+// Split-K product P[split] = A[:, Ks] W[:, Ks]^T over one BM x BN tile: the
+// work of block `bid` of a grid of `nblocks` product blocks.
 template <int kElemBytes, int NS, class SH>
-__global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
-    const char* __restrict__ A, const char* __restrict__ W, float* __restrict__ P,
-    int M, int N, int Kd, int splits, int tiles_n, int ktiles) {
+__device__ __forceinline__ void gemm1_tile(const char* __restrict__ A, const char* __restrict__ W,
+                                           float* __restrict__ P, int M, int N, int Kd,
+                                           int splits, int tiles_n, int ktiles, int bid,
+                                           int nblocks,
+                                           char (*lds)[SH::LDS_A + SH::LDS_B]) {
     constexpr int MI = SH::MI, NJ = SH::NJ;
-    __shared__ __attribute__((aligned(16))) char lds[2][SH::LDS_A + SH::LDS_B];
-
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
     const int wm = wid / SH::WN, wn = wid % SH::WN;
-    const G1Work w = g1_work(splits, tiles_n, ktiles);
+    const G1Work w = g1_work(splits, tiles_n, ktiles, bid, nblocks);
     const int split = w.split, tm = w.tm, tn = w.tn;
     f32x16 acc[MI][NJ];
     g1_mainloop<kElemBytes, NS, SH>(A, W, M, N, Kd, w, lds, acc);
@@ -465,6 +466,15 @@ __global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
             __builtin_nontemporal_store(*(const f32x4*)&otile[row * SH::OUT_ROW + c4 * 4],
                                         (f32x4*)&out[(int64_t)grow * N + gcol]);
     }
+}
+
+template <int kElemBytes, int NS, class SH>
+__global__ __launch_bounds__(SH::THREADS) void gemm1_splitk_kernel(
+    const char* __restrict__ A, const char* __restrict__ W, float* __restrict__ P,
+    int M, int N, int Kd, int splits, int tiles_n, int ktiles) {
+    __shared__ __attribute__((aligned(16))) char lds[2][SH::LDS_A + SH::LDS_B];
+    gemm1_tile<kElemBytes, NS, SH>(A, W, P, M, N, Kd, splits, tiles_n, ktiles, blockIdx.x,
+                                   gridDim.x, lds);
 }
 
 // Launch of the split-K product with the plan's tile shape.
@@ -553,18 +563,20 @@ __device__ inline float apply_act(float x, int act) {
 // kReg: the regression head's last two layers instead of the binned one
 // (the nb "bin logits" are the third layer's outputs, `bins` holds w4 and
 // phase 3 computes relu(z) . w4 + b4 in place of the softmax mean).
-template <bool kBF16, int kS, bool kReg = false, int kPF = HD_W2PF>
-__global__ __launch_bounds__(HD_THREADS) void head_kernel(
+// The head over rows [blk HD_RB, (blk + 1) HD_RB), its buffers in `smem`
+// (head_lds bytes).
+template <bool kBF16, int kS, bool kReg, int kPF>
+__device__ __forceinline__ void head_rows(
     const float* __restrict__ P, int B, int m, int nb, const float* __restrict__ b1,
     const void* __restrict__ w2, const float* __restrict__ b2, const float* __restrict__ bins,
     int act, float ema_alpha, int ema_init, float* __restrict__ ema_state,
-    float* __restrict__ expected, int32_t* __restrict__ rem_len, int len_max, float b4 = 0.0f) {
-    extern __shared__ __attribute__((aligned(16))) char smem[];
+    float* __restrict__ expected, int32_t* __restrict__ rem_len, int len_max, float b4, int blk,
+    char* smem) {
     constexpr int kBatch = hd_batch<kS>();
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
-    const int row0 = blockIdx.x * HD_RB;
+    const int row0 = blk * HD_RB;
     const int mpad = (m + 31) & ~31;
     const int astride = mpad + 8;                 // bf16 elements per LDS row
     const int nbpad = (nb + 15) & ~15;
@@ -781,6 +793,17 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
             }
         }
     }
+}
+
+template <bool kBF16, int kS, bool kReg = false, int kPF = HD_W2PF>
+__global__ __launch_bounds__(HD_THREADS) void head_kernel(
+    const float* __restrict__ P, int B, int m, int nb, const float* __restrict__ b1,
+    const void* __restrict__ w2, const float* __restrict__ b2, const float* __restrict__ bins,
+    int act, float ema_alpha, int ema_init, float* __restrict__ ema_state,
+    float* __restrict__ expected, int32_t* __restrict__ rem_len, int len_max, float b4 = 0.0f) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    head_rows<kBF16, kS, kReg, kPF>(P, B, m, nb, b1, w2, b2, bins, act, ema_alpha, ema_init,
+                                    ema_state, expected, rem_len, len_max, b4, blockIdx.x, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -1123,7 +1146,7 @@ __global__ __launch_bounds__(SH::THREADS) void predict_fused_kernel(FusedArgs a)
     const int wm = wid / SH::WN, wn = wid % SH::WN;
     const int r32 = lane & 31;
     const int khalf = lane >> 5;
-    const G1Work w = g1_work(1, a.tiles_n, a.ktiles);
+    const G1Work w = g1_work(1, a.tiles_n, a.ktiles, blockIdx.x, gridDim.x);
     f32x16 acc[MI][NJ];
     g1_mainloop<2, NS, SH>(a.A, a.W, a.M, a.N, a.Kd, w, lds, acc);
 
@@ -1649,6 +1672,123 @@ hipError_t launch_predict(const star_predict_params& p, const PredictPlan& pl, c
                                                     ema_state, expected, rem_len, stream)
                                 : launch_head<false>(p, pl, partials, b1, w2, b2, bins,
                                                      ema_state, expected, rem_len, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Two batches in one launch.  Blocks [0, gemm_blocks) compute the next
+// batch's first-layer split-K partials (64 x 64 tiles); the blocks after
+// them run the previous batch's head from its partials.  The roles share no
+// data, and each block takes one role for its whole life, so they need no
+// synchronisation.  One launch removes the kernel boundary between the
+// previous batch's head and the next batch's product, and the head's
+// workgroups take the CUs as the product's workgroups leave them.
+// ---------------------------------------------------------------------------
+struct OverlapArgs {
+    // the next batch's product
+    const char* A;
+    const char* W1;
+    float* Pn;
+    int M, N, Kd, splits, tiles_n, ktiles, gemm_blocks;
+    // the previous batch's head
+    const float* Pp;
+    const float* b1;
+    const void* w2;
+    const float* b2;
+    const float* bins;
+    float* ema_state;
+    float* expected;
+    int32_t* rem_len;
+    int B, m, nb, act, ema_init, len_max;
+    float ema_alpha;
+};
+constexpr size_t OV_LDS = 2 * (size_t)(G1Small::LDS_A + G1Small::LDS_B);
+// W2 fragments the head role prefetches: 4 keeps the kernel at 90 VGPRs, so
+// head workgroups fit beside the product's two per CU from the start
+// (measured at 1024 x 4096 -> 512 -> 64 bins, per batch: 12.9-13.6 us with
+// 4, 13.4-13.8 with 8 (124 VGPRs), 16.6-17.5 with 16 (214 VGPRs, two
+// workgroups per CU, heads waiting for products to end), against 18.1-18.2
+// for star_predict).
+constexpr int OV_W2PF = 4;
+
+template <int kS>
+__global__ __launch_bounds__(HD_THREADS) void predict_overlap_kernel(OverlapArgs a) {
+    static_assert(G1Small::THREADS == HD_THREADS, "one block size for both roles");
+    __shared__ __attribute__((aligned(16))) char lds[2][G1Small::LDS_A + G1Small::LDS_B];
+    if ((int)blockIdx.x < a.gemm_blocks)
+        gemm1_tile<2, G1_STAGES_SMALL, G1Small>(a.A, a.W1, a.Pn, a.M, a.N, a.Kd, a.splits,
+                                                a.tiles_n, a.ktiles, blockIdx.x, a.gemm_blocks,
+                                                lds);
+    else
+        head_rows<true, kS, false, OV_W2PF>(a.Pp, a.B, a.m, a.nb, a.b1, a.w2, a.b2, a.bins,
+                                            a.act, a.ema_alpha, a.ema_init, a.ema_state,
+                                            a.expected, a.rem_len, a.len_max, 0.0f,
+                                            (int)blockIdx.x - a.gemm_blocks, &lds[0][0]);
+}
+
+hipError_t launch_predict_overlap(const star_predict_params& p, const PredictPlan& pl,
+                                  const void* hidden_next, float* partials_next,
+                                  const float* partials_prev, const void* w1, const float* b1,
+                                  const void* w2, const float* b2, const float* bins,
+                                  float* ema_state, float* expected, int32_t* rem_len,
+                                  hipStream_t stream) {
+    if (pl.fused || pl.head_tiled) return hipErrorInvalidValue;
+    if (p.n_req == 0 || (!hidden_next && !partials_prev)) return hipSuccess;
+    const bool bf16 = p.dtype == STAR_BF16;
+    const GemmPlan& g = pl.gemm;
+    const int head_blocks = (int)ceil_div(p.n_req, HD_RB);
+    const bool one = hidden_next && partials_prev && bf16 && g.shape == GemmPlan::kSmall &&
+                     pl.head_rows == HD_RB && pl.head_lds <= OV_LDS &&
+                     head_blocks <= HD_LOWREG_GROUPS;
+    if (!one) {          // the two kernels one after the other, same results
+        if (partials_prev) {
+            const hipError_t e =
+                bf16 ? launch_head<true>(p, pl, partials_prev, b1, w2, b2, bins, ema_state,
+                                         expected, rem_len, stream)
+                     : launch_head<false>(p, pl, partials_prev, b1, w2, b2, bins, ema_state,
+                                          expected, rem_len, stream);
+            if (e != hipSuccess) return e;
+        }
+        if (hidden_next)
+            return launch_gemm(g, bf16, hidden_next, w1, partials_next, p.n_req, p.d_hidden,
+                               p.d_model, stream);
+        return hipSuccess;
+    }
+    OverlapArgs a;
+    a.A = (const char*)hidden_next;
+    a.W1 = (const char*)w1;
+    a.Pn = partials_next;
+    a.M = p.n_req;
+    a.N = p.d_hidden;
+    a.Kd = p.d_model;
+    a.splits = g.splits;
+    a.tiles_n = g.tiles_n;
+    a.ktiles = g.ktiles;
+    a.gemm_blocks = g.tiles_m * g.tiles_n * g.splits;
+    a.Pp = partials_prev;
+    a.b1 = b1;
+    a.w2 = w2;
+    a.b2 = b2;
+    a.bins = bins;
+    a.ema_state = ema_state;
+    a.expected = expected;
+    a.rem_len = rem_len;
+    a.B = p.n_req;
+    a.m = p.d_hidden;
+    a.nb = p.n_bins;
+    a.act = p.act;
+    a.ema_init = p.ema_init;
+    a.len_max = p.len_max;
+    a.ema_alpha = p.ema_alpha;
+    const dim3 grid((unsigned)(a.gemm_blocks + head_blocks));
+    switch (g.splits) {
+        case 1: hipLaunchKernelGGL(predict_overlap_kernel<1>, grid, dim3(HD_THREADS), 0, stream, a); break;
+        case 2: hipLaunchKernelGGL(predict_overlap_kernel<2>, grid, dim3(HD_THREADS), 0, stream, a); break;
+        case 4: hipLaunchKernelGGL(predict_overlap_kernel<4>, grid, dim3(HD_THREADS), 0, stream, a); break;
+        case 8: hipLaunchKernelGGL(predict_overlap_kernel<8>, grid, dim3(HD_THREADS), 0, stream, a); break;
+        case 16: hipLaunchKernelGGL(predict_overlap_kernel<16>, grid, dim3(HD_THREADS), 0, stream, a); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

@@ -119,6 +119,48 @@ STAR_API star_status star_predict(const star_predict_params* p, const void* hidd
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
 }
 
+STAR_API star_status star_predict_overlap(const star_predict_params* p, const void* hidden_next,
+                                          void* ws_next, const void* ws_prev, const void* w1,
+                                          const float* b1, const void* w2, const float* b2,
+                                          const float* bin_values, float* ema_state,
+                                          float* expected_len, int32_t* rem_len, size_t ws_bytes,
+                                          void* stream) {
+    star_status st = check_predict_params(p);
+    if (st != STAR_OK) return st;
+    if (!hidden_next && !ws_prev) return STAR_ERR_INVALID_ARG;
+    const PredictPlan pl = plan_predict(*p);
+    if (pl.fused || pl.head_tiled) return STAR_ERR_UNSUPPORTED;
+    const size_t need = STAR_WS_HEADER_BYTES + align_up(pl.partial_bytes, 256);
+    if (hidden_next) {
+        if (p->n_req > 0 && !w1) return STAR_ERR_INVALID_ARG;
+        if (p->n_req > 0 && (!aligned(hidden_next, 16) || !aligned(w1, 16)))
+            return STAR_ERR_UNSUPPORTED;
+        st = check_ws(ws_next, ws_bytes, need);
+        if (st != STAR_OK) return st;
+    }
+    if (ws_prev) {
+        if (p->n_req > 0) {
+            if (!w2 || !bin_values || !expected_len) return STAR_ERR_INVALID_ARG;
+            if (p->ema_alpha > 0.0f && !ema_state) return STAR_ERR_INVALID_ARG;
+            if (!aligned(w2, 16) || !aligned(b1, 16)) return STAR_ERR_UNSUPPORTED;
+        }
+        st = check_ws(ws_prev, ws_bytes, need);
+        if (st != STAR_OK) return st;
+    }
+    if (hidden_next && ws_prev) {             // the two workspaces must not overlap
+        const char* a = (const char*)ws_next;
+        const char* b = (const char*)ws_prev;
+        if (a < b + need && b < a + need) return STAR_ERR_INVALID_ARG;
+    }
+    float* next = hidden_next ? (float*)((char*)ws_next + STAR_WS_HEADER_BYTES) : nullptr;
+    const float* prev = ws_prev ? (const float*)((const char*)ws_prev + STAR_WS_HEADER_BYTES)
+                                : nullptr;
+    hipError_t e = launch_predict_overlap(*p, pl, hidden_next, next, prev, w1, b1, w2, b2,
+                                          bin_values, ema_state, expected_len, rem_len,
+                                          (hipStream_t)stream);
+    return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
+}
+
 // ---------------------------------------------------------------------------
 // predictor without allocation: the scratch is a fixed array in device
 // memory, one copy per GPU (each GPU that runs it holds the array until the

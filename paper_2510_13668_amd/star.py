@@ -94,6 +94,9 @@ def lib():
         L.star_predict.restype = ctypes.c_int
         L.star_predict.argtypes = [ctypes.POINTER(PredictParams)] + [_P] * 10 + [ctypes.c_size_t, _P]
         L.star_predict_noalloc.argtypes = [ctypes.POINTER(PredictParams)] + [_P] * 10
+        L.star_predict_overlap.argtypes = ([ctypes.POINTER(PredictParams)] + [_P] * 11 +
+                                           [ctypes.c_size_t, _P])
+        L.star_predict_overlap.restype = ctypes.c_int
         L.star_project_load.restype = ctypes.c_int
         L.star_project_load.argtypes = [ctypes.POINTER(LoadParams)] + [_P] * 5 + [ctypes.c_size_t, _P]
         L.star_score_migrations.restype = ctypes.c_int
@@ -206,6 +209,20 @@ def predict_noalloc(p: PredictParams, hidden, w1, b1, w2, b2, bin_values, ema_st
     _check("star_predict_noalloc", lib().star_predict_noalloc(
         ctypes.byref(p), _ptr(hidden), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
         _ptr(bin_values), _ptr(ema_state), _ptr(expected_len), _ptr(rem_len), _stream(stream)))
+
+
+def predict_overlap(p: PredictParams, hidden_next, ws_next, ws_prev, w1, b1, w2, b2,
+                    bin_values, ema_state, expected_len, rem_len, stream=None):
+    """star_predict_overlap: the head of the batch whose product `ws_prev`
+    holds (None: no head) and the product of `hidden_next` into `ws_next`
+    (None: no product), in one launch where the plan allows."""
+    _dev(hidden_next, w1, b1, w2, b2, bin_values, ema_state, expected_len, rem_len)
+    nbytes = (ws_next or ws_prev).nbytes
+    _check("star_predict_overlap", lib().star_predict_overlap(
+        ctypes.byref(p), _ptr(hidden_next), ctypes.c_void_p(ws_next.ptr if ws_next else None),
+        ctypes.c_void_p(ws_prev.ptr if ws_prev else None), _ptr(w1), _ptr(b1), _ptr(w2),
+        _ptr(b2), _ptr(bin_values), _ptr(ema_state), _ptr(expected_len), _ptr(rem_len), nbytes,
+        _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

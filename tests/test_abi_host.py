@@ -94,6 +94,35 @@ def test_predict_rejects_null_pointers_and_workspace(L):
     assert _predict(L, p, ws=ctypes.c_void_p((1 << 20) + 64)) == -4   # not 256-aligned
 
 
+def _overlap(L, p, hidden=FAKE, ws_next=FAKE, ws_prev=ctypes.c_void_p((1 << 20) + (1 << 26)),
+             ws_bytes=1 << 24, **ptrs):
+    args = {k: FAKE for k in ("w1", "w2", "bins", "ema", "expected")}
+    args.update(ptrs)
+    return L.star_predict_overlap(ctypes.byref(p) if p is not None else None, hidden, ws_next,
+                                  ws_prev, args["w1"], None, args["w2"], None, args["bins"],
+                                  args["ema"], args["expected"], None, ws_bytes, None)
+
+
+def test_predict_overlap_validation(L):
+    """The two-batch predictor call validates each side it is given, before
+    launching anything, and refuses what it does not run as a product plus
+    head: one-slice shapes (the fused kernel) and the K-chunked head."""
+    p = _pp()
+    need = star.predict_workspace_size(p)
+    assert _overlap(L, None) == -1
+    assert _overlap(L, p, hidden=None, ws_prev=None) == -1          # neither side
+    assert _overlap(L, p, ws_bytes=need - 1) == -4
+    assert _overlap(L, p, ws_next=None) == -4                        # product without a workspace
+    assert _overlap(L, p, ws_prev=ctypes.c_void_p((1 << 20) + (1 << 26) + 64)) == -4
+    assert _overlap(L, p, ws_prev=ctypes.c_void_p((1 << 20) + 256), ws_bytes=need) == -1
+    assert _overlap(L, p, w1=None) == -1                              # product needs w1
+    assert _overlap(L, p, hidden=None, w1=None, expected=None) == -1  # head needs its outputs
+    assert _overlap(L, p, ema=None) == -1                             # EMA on, no state
+    assert _overlap(L, p, hidden=ctypes.c_void_p((1 << 20) + 2)) == -2
+    assert _overlap(L, _pp(n_req=8192)) == -2                         # one K-slice: fused kernel
+    assert _overlap(L, _pp(n_req=8200, d_model=64, d_hidden=2048, n_bins=256)) == -2   # tiled head
+
+
 def test_predict_noalloc_validation_and_scratch_limit(L):
     """The allocation-free predictor validates like star_predict and refuses,
     before launching anything, sizes whose scratch exceeds its fixed array

@@ -431,3 +431,64 @@ def test_second_layer_logit_read_through_two_bins(B, d, m, dtype):
     err = np.abs(zd - zd_ref) / np.maximum(1.0, np.abs(zd_ref))
     print(f"  B={B} d={d} m={m}: max logit-difference err {err.max():.2e}", flush=True)
     assert err.max() < 1e-4
+
+
+@pytest.mark.parametrize("B,d,m,nb,dtype,alpha,steps", [
+    (1024, 4096, 512, 64, synth.BF16, 0.2, 5),   # continuous shape: one launch, 4 K-splits
+    (512, 4096, 512, 64, synth.BF16, 0.0, 3),    # one launch, 8 K-splits, no EMA
+    (1000, 4040, 400, 64, synth.BF16, 0.2, 3),   # one launch, ragged rows, columns and K
+    (4096, 5120, 512, 64, synth.BF16, 0.2, 2),   # 128 x 128 tiles: two launches
+    (64, 1024, 256, 32, synth.F32, 0.2, 3),      # fp32: two launches
+    (2100, 4096, 256, 64, synth.BF16, 0.2, 3),   # over 512 head workgroups: two launches
+])
+def test_overlap_sequence_equals_predict(B, d, m, nb, dtype, alpha, steps):
+    """star_predict_overlap over a sequence of batches, two workspaces in
+    turn (the first call only the product, the last only the head), gives
+    every batch's E, rem_len and EMA state bit for bit as star_predict on
+    that batch, the EMA carried in order; the first batch also against the
+    oracle.  (One-slice shapes, which star_predict runs as one fused kernel,
+    are refused: a host test covers that.)"""
+    from paper_2510_13668_amd import star
+    rng = np.random.default_rng(B + d + m + nb + steps)
+    bf = dtype == synth.BF16
+    w1 = (rng.standard_normal((m, d)) / np.sqrt(d)).astype(np.float32)
+    w2 = (rng.standard_normal((nb, m)) * 4 / np.sqrt(m)).astype(np.float32)
+    b1 = (rng.standard_normal(m) * 0.1).astype(np.float32)
+    b2 = (rng.standard_normal(nb) * 0.1).astype(np.float32)
+    hs = [rng.standard_normal((B, d)).astype(np.float32) for _ in range(steps)]
+    if bf:
+        w1, w2 = synth.f32_to_bf16_bits(w1), synth.f32_to_bf16_bits(w2)
+        hs = [synth.f32_to_bf16_bits(h) for h in hs]
+    bins = synth.bin_values(nb, 1.0, 32768.0)
+    pr = Predictor(w1, w2, bins, dtype=dtype, act=synth.ACT_GELU, b1=b1, b2=b2, n_req=B,
+                   len_max=32768, ema_alpha=alpha)
+    hd = [to_dev(h, bf) for h in hs]
+    want = []
+    for i in range(steps):
+        pr.run(hd[i], ema_init=(i == 0))
+        torch.cuda.synchronize()
+        want.append((pr.expected.cpu().numpy().copy(), pr.rem.cpu().numpy().copy(),
+                     pr.ema.cpu().numpy().copy()))
+    ref = oracle.predict(hs[0][:64], w1, w2, bins, dtype=dtype, act=synth.ACT_GELU, b1=b1, b2=b2,
+                         len_max=32768)
+    assert_lengths_close(want[0][0][:64], ref["expected"])
+
+    print(f"overlap B={B} d={d} m={m} nb={nb} dtype={dtype} steps={steps}", flush=True)
+    ws = [star.Workspace(pr.ws.nbytes), star.Workspace(pr.ws.nbytes)]
+    ema = torch.full((B,), -5.0, dtype=torch.float32, device="cuda")
+    exp = torch.empty(B, dtype=torch.float32, device="cuda")
+    rem = torch.empty(B, dtype=torch.int32, device="cuda")
+    ema_arg = ema if alpha > 0 else None
+    star.predict_overlap(pr.params(False), hd[0], ws[0], None, pr.w1, pr.b1, pr.w2, pr.b2,
+                         pr.bins, None, None, None)
+    for i in range(steps):
+        nxt = hd[i + 1] if i + 1 < steps else None
+        exp.fill_(-1.0)
+        rem.fill_(-1)
+        star.predict_overlap(pr.params(i == 0), nxt, ws[(i + 1) % 2] if nxt is not None else None,
+                             ws[i % 2], pr.w1, pr.b1, pr.w2, pr.b2, pr.bins, ema_arg, exp, rem)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(exp.cpu().numpy(), want[i][0], err_msg=f"E, batch {i}")
+        np.testing.assert_array_equal(rem.cpu().numpy(), want[i][1], err_msg=f"rem, batch {i}")
+        if alpha > 0:
+            np.testing.assert_array_equal(ema.cpu().numpy(), want[i][2], err_msg=f"EMA, batch {i}")

@@ -346,9 +346,10 @@ def test_graph_replay_matches_eager():
 
 def test_pipelined_graph_rounds_match_eager():
     """Rounds pipelined on two streams, as the benchmark runs them: the
-    predictions run on one stream while earlier rounds are projected and
-    scored on a second, which waits for the predictions two rounds at a
-    time and records one event per batch of two.  The per-round outputs
+    predictions run on one stream (star_predict_overlap: one round's head
+    and the next round's first-layer product per call) while earlier rounds
+    are projected and scored on a second, which waits for the predictions
+    two rounds at a time and records one event per batch of two.  The per-round outputs
     rotate through six buffers; before a prediction overwrites a buffer,
     its stream waits once for the event of the batch that last scheduled
     it.  The whole chunk is captured as one HIP graph.  Every replay (with
@@ -389,17 +390,24 @@ def test_pipelined_graph_rounds_match_eager():
     ev_done = [torch.cuda.Event() for _ in range(NS)]
     pp = pr.params(False)
 
+    wsp = [pr.ws, star.Workspace(pr.ws.nbytes)]
+
     def chunk():
         S2.wait_stream(P)
         guard, waited, nbatch = [None] * NS, None, 0
         batch = []
+        # round j's head and round j+1's product in one call
+        star.predict_overlap(pp, hid[1], wsp[0], None, pr.w1, pr.b1, pr.w2, pr.b2, pr.bins,
+                             None, None, None, P)
         for j in range(R):
             k = j % NS
             if guard[k] is not None and guard[k] is not waited:
                 P.wait_event(guard[k])
                 waited = guard[k]
-            star.predict(pp, hid[j + 1], pr.w1, pr.b1, pr.w2, pr.b2, pr.bins, pr.ema, exps[k],
-                         rems[k], pr.ws, P)
+            nxt = hid[j + 2] if j + 1 < R else None
+            star.predict_overlap(pp, nxt, wsp[(j + 1) % 2] if nxt is not None else None,
+                                 wsp[j % 2], pr.w1, pr.b1, pr.w2, pr.b2, pr.bins, pr.ema,
+                                 exps[k], rems[k], P)
             batch.append((j, k))
             if len(batch) == BATCH or j == R - 1:
                 ev_pred[k].record(P)
