@@ -514,6 +514,78 @@ __device__ inline void build_curves_pm_sm_w(const int64_t* hA, const int64_t* hN
     }
 }
 
+// The same with a run of at most kS buckets per lane (K <= 64 kS, S odd)
+// held in registers: every LDS read of the histograms and partial terms is
+// issued at once at the start, and L, SM and PM come from the registers, so
+// the lane reads LDS once instead of three times.
+constexpr int PMSM_REG_RUN = 5;
+template <int kT, int kS>
+__device__ inline void build_curves_pm_sm_wr(const int64_t* hA, const int64_t* hN, int64_t* hPL,
+                                             int64_t* lPM, int64_t* lSM, int n, int K,
+                                             int64_t bb) {
+    const int l = threadIdx.x & 63;
+    const int K1 = K + 1;
+    const int S = ((K + 63) >> 6) | 1;                 // <= kS (the caller checks)
+    for (int t = (int)(threadIdx.x >> 6); t < n; t += kT / 64) {   // wave-uniform
+        const int64_t* A = hA + t * K1;
+        const int64_t* C = hN + t * K1;
+        int64_t* L = hPL + t * K1;
+        const int j0 = l * S;
+        const int q0 = K - 1 - j0;                     // buckets q0, q0 - 1, ... (u < len)
+        const int len = j0 < K ? (K - j0 < S ? K - j0 : S) : 0;
+        int64_t xa[kS], xn[kS], xv[kS];
+#pragma unroll
+        for (int u = 0; u < kS; ++u) {
+            const int q = u < len ? q0 - u : 0;        // in range: read, then ignored
+            xa[u] = A[q + 1];
+            xn[u] = C[q + 1];
+            xv[u] = L[q];
+        }
+        int64_t sa = 0, sn = 0;
+#pragma unroll
+        for (int u = 0; u < kS; ++u)
+            if (u < len) {
+                sa += xa[u];
+                sn += xn[u];
+            }
+        int64_t ra = wave_shr1_i64(wave_incl_add_i64(sa), 0);   // sums over the lanes below
+        int64_t rn = wave_shr1_i64(wave_incl_add_i64(sn), 0);
+        int64_t smax = INT64_MIN, pmax = INT64_MIN;
+#pragma unroll
+        for (int u = 0; u < kS; ++u)
+            if (u < len) {
+                const int q = q0 - u;
+                ra += xa[u];
+                rn += xn[u];
+                xv[u] = ra + bb * q * rn + xv[u];      // L[q]
+                L[q] = xv[u];
+                smax = imax(smax, xv[u]);
+                pmax = imax(pmax, xv[u] + bb * q);
+            }
+        int64_t srun = wave_shr1_i64(wave_incl_max_i64(smax), INT64_MIN);
+        int64_t prun = wave_excl_max_above_i64(pmax);
+        const int64_t ptot = imax(prun, pmax);        // lane 0: max over every bucket
+#pragma unroll
+        for (int u = 0; u < kS; ++u)                   // SM downwards
+            if (u < len) {
+                srun = imax(srun, xv[u]);
+                lSM[t * K1 + q0 - u] = srun;
+            }
+#pragma unroll
+        for (int u = kS - 1; u >= 0; --u)              // PM upwards, exclusive
+            if (u < len) {
+                const int q = q0 - u;
+                lPM[t * K1 + q] = prun;
+                prun = imax(prun, xv[u] + bb * q);
+            }
+        if (l == 0) {
+            L[K] = INT64_MIN;
+            lSM[t * K1 + K] = INT64_MIN;
+            lPM[t * K1 + K] = ptot;
+        }
+    }
+}
+
 
 // Minimum of a 64-bit value over aligned groups of g lanes (g a power of
 // two, 2..64); every lane of a group gets it.  DPP quad permutes for lane
@@ -2741,7 +2813,10 @@ __global__ __launch_bounds__(SO_THREADS) void score_one_kernel(OneArgs a) {
             if (pr != 0) atomicAdd((unsigned long long*)&lL[row + ke], (unsigned long long)pr);
         }
         __syncthreads();
-        build_curves_pm_sm_w<SO_THREADS>(lPM, lSM, lL, lPM, lSM, n, K, bb);
+        if (K <= 64 * PMSM_REG_RUN)
+            build_curves_pm_sm_wr<SO_THREADS, PMSM_REG_RUN>(lPM, lSM, lL, lPM, lSM, n, K, bb);
+        else
+            build_curves_pm_sm_w<SO_THREADS>(lPM, lSM, lL, lPM, lSM, n, K, bb);
         __syncthreads();
     } else {
 #pragma unroll
