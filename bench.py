@@ -5,8 +5,12 @@ continuous-mode workload (1024 concurrent requests on 8 decode instances,
 bf16 hidden states [1024, 4096] from an AR(1) process, head 4096 -> 512
 (GELU) -> 64 length bins with EMA alpha 0.2, horizon 16384 steps in 64-step
 buckets, all 1024 x 8 candidates scored, top-256 ranked):
-    star_predict -> star_project_and_score (the load projection and the
+    a prediction -> star_project_and_score (the load projection and the
     migration scoring and ranking in one call).
+The reported mode (graph_pipelined) makes the predictions with
+star_predict_overlap, one launch per round holding that round's head and the
+next round's first-layer product; the eager and one-graph-per-round modes use
+star_predict.
 Inputs for 200 decode steps are staged in HBM before timing.  The metric is
 requests predicted + scored per second (= 1024 / seconds per round) and
 microseconds per round.
@@ -62,8 +66,10 @@ def _parse():
     ap.add_argument("--mode", choices=("graph_pipelined", "pipelined", "eager", "graph"),
                     default="graph_pipelined",
                     help="which timing gives `value` (the others are reported beside it): "
-                         "pipelined = predictions on one stream while earlier rounds are "
-                         "projected and scored on a second (eagerly launched); "
+                         "pipelined = predictions (star_predict_overlap: a round's head and "
+                         "the next round's first-layer product per launch) on one stream "
+                         "while earlier rounds are projected and scored on a second "
+                         "(eagerly launched); "
                          "graph_pipelined = the same, 40 rounds per captured HIP graph; "
                          "eager = one stream, round after round; graph = one captured graph "
                          "per round")
@@ -1128,8 +1134,11 @@ def main():
                    "overlap": "graph_pipelined and pipelined time throughput: later rounds' "
                               "predictions run while earlier rounds are projected and scored "
                               "(scheduling waits for the predictions %d rounds at a time, outputs "
-                              "rotate through %d buffers); us_per_round_eager (p50/p99) is one "
-                              "round's latency" % (SCHED_BATCH, NSLOT)},
+                              "rotate through %d buffers), and each prediction launch also runs "
+                              "the next round's first-layer product (star_predict_overlap); "
+                              "us_per_round_eager (p50/p99, star_predict then "
+                              "star_project_and_score) is one round's latency"
+                              % (SCHED_BATCH, NSLOT)},
         "roofline": {"kernel": "predict_overlap_kernel<4> (star_predict_overlap): one batch's "
                                "first-layer product, bf16 MFMA H[1024,4096] x W1[512,4096]^T in 4 "
                                "K-splits, and the previous batch's head (split reduction, GELU, "
