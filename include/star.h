@@ -128,23 +128,28 @@ star_status star_predict(const star_predict_params* p, const void* hidden, const
  * workspaces alternating between two buffers A and B:
  *     (h_0 -> A), (A -> out_0, h_1 -> B), (B -> out_1, h_2 -> A), ...,
  *     (last -> out_last)
- * gives out_i equal to star_predict on h_i, bit for bit, with the EMA
- * carried across the calls in order.  Every call's w1, b1, w2, b2,
- * bin_values and params (p) must be the same, except p->ema_init, which
- * applies to the head the call runs.
+ * gives out_i equal to star_predict on h_i with the EMA carried across the
+ * calls in order: bit for bit where star_predict runs the same two kernels
+ * (products with a K-split).  Products of one K-slice, which star_predict
+ * runs as one fused kernel that rounds the second product's sums in another
+ * order, run here as the product and the head; their results meet the same
+ * 2e-2 contract.  Every call's w1, b1, w2, b2, bin_values and params (p)
+ * must be the same, except p->ema_init, which applies to the head the call
+ * runs.
  *
  * Arguments as for star_predict.  w1 may be NULL when hidden_next is NULL;
  * w2, bin_values, expected_len, ema_state and rem_len may be NULL when
- * ws_prev is NULL.  ws_next and ws_prev: each star_predict_workspace_size(p)
- * bytes (ws_bytes), 256-byte aligned, not overlapping; ws_prev keeps the
- * product of the call that filled it until its head has run.
- * Errors: STAR_ERR_UNSUPPORTED for shapes star_predict runs as one kernel
- * (one K-slice) or with the K-chunked head (bf16 batches of 8192 rows and
- * more with at most 4 K-splits); STAR_ERR_INVALID_ARG when both sides are
- * NULL or the workspaces overlap; otherwise as star_predict.
- * One launch where the product takes 64 x 64 tiles (bf16), else the head
- * and the product as two launches on `stream`.
+ * ws_prev is NULL.  ws_next and ws_prev: each
+ * star_predict_overlap_workspace_size(p) bytes (ws_bytes; the same as
+ * star_predict_workspace_size(p) except for one-slice products), 256-byte
+ * aligned, not overlapping; ws_prev keeps the product of the call that
+ * filled it until its head has run.
+ * Errors: STAR_ERR_INVALID_ARG when both sides are NULL or the workspaces
+ * overlap; otherwise as star_predict.
+ * One launch where the product takes 64 x 64 tiles (bf16) and the head is
+ * the 4-row one, else the head and the product as two launches on `stream`.
  * ---------------------------------------------------------------------- */
+size_t star_predict_overlap_workspace_size(const star_predict_params* p);
 star_status star_predict_overlap(const star_predict_params* p, const void* hidden_next,
                                  void* ws_next, const void* ws_prev, const void* w1,
                                  const float* b1, const void* w2, const float* b2,

@@ -1731,13 +1731,13 @@ hipError_t launch_predict_overlap(const star_predict_params& p, const PredictPla
                                   const void* w2, const float* b2, const float* bins,
                                   float* ema_state, float* expected, int32_t* rem_len,
                                   hipStream_t stream) {
-    if (pl.fused || pl.head_tiled) return hipErrorInvalidValue;
+    if (pl.fused) return hipErrorInvalidValue;
     if (p.n_req == 0 || (!hidden_next && !partials_prev)) return hipSuccess;
     const bool bf16 = p.dtype == STAR_BF16;
     const GemmPlan& g = pl.gemm;
     const int head_blocks = (int)ceil_div(p.n_req, HD_RB);
     const bool one = hidden_next && partials_prev && bf16 && g.shape == GemmPlan::kSmall &&
-                     pl.head_rows == HD_RB && pl.head_lds <= OV_LDS &&
+                     !pl.head_tiled && pl.head_rows == HD_RB && pl.head_lds <= OV_LDS &&
                      head_blocks <= HD_LOWREG_GROUPS;
     if (!one) {          // the two kernels one after the other, same results
         if (partials_prev) {

@@ -119,6 +119,14 @@ STAR_API star_status star_predict(const star_predict_params* p, const void* hidd
     return e == hipSuccess ? STAR_OK : STAR_ERR_HIP;
 }
 
+// star_predict_overlap runs the two-kernel plan (product, then head) for
+// every shape: one-slice products, which star_predict runs as one fused
+// kernel, keep their fp32 partial plane in the workspace here.
+STAR_API size_t star_predict_overlap_workspace_size(const star_predict_params* p) {
+    if (check_predict_params(p) != STAR_OK) return 0;
+    return STAR_WS_HEADER_BYTES + align_up(plan_predict(*p, true, false).partial_bytes, 256);
+}
+
 STAR_API star_status star_predict_overlap(const star_predict_params* p, const void* hidden_next,
                                           void* ws_next, const void* ws_prev, const void* w1,
                                           const float* b1, const void* w2, const float* b2,
@@ -128,8 +136,7 @@ STAR_API star_status star_predict_overlap(const star_predict_params* p, const vo
     star_status st = check_predict_params(p);
     if (st != STAR_OK) return st;
     if (!hidden_next && !ws_prev) return STAR_ERR_INVALID_ARG;
-    const PredictPlan pl = plan_predict(*p);
-    if (pl.fused || pl.head_tiled) return STAR_ERR_UNSUPPORTED;
+    const PredictPlan pl = plan_predict(*p, true, false);
     const size_t need = STAR_WS_HEADER_BYTES + align_up(pl.partial_bytes, 256);
     if (hidden_next) {
         if (p->n_req > 0 && !w1) return STAR_ERR_INVALID_ARG;

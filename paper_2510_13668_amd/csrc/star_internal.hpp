@@ -30,9 +30,9 @@ struct PredictPlan {
 // allow: 1 = the fused kernel where it applies, 0 = never (the two-kernel path)
 PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok = true, bool fused_ok = true);
 // The head of a batch whose partials are `partials_prev` and the product of
-// the next batch into `partials_next`, in one launch where the plan allows
-// (two-kernel plans only; hipErrorInvalidValue for the others).  Either side
-// may be null.
+// the next batch into `partials_next`, in one launch where the plan allows,
+// else as two launches (two-kernel plans, plan_predict(p, true, false);
+// hipErrorInvalidValue for a fused plan).  Either side may be null.
 hipError_t launch_predict_overlap(const star_predict_params& p, const PredictPlan& pl,
                                   const void* hidden_next, float* partials_next,
                                   const float* partials_prev, const void* w1, const float* b1,

@@ -97,6 +97,8 @@ def lib():
         L.star_predict_overlap.argtypes = ([ctypes.POINTER(PredictParams)] + [_P] * 11 +
                                            [ctypes.c_size_t, _P])
         L.star_predict_overlap.restype = ctypes.c_int
+        L.star_predict_overlap_workspace_size.argtypes = [ctypes.POINTER(PredictParams)]
+        L.star_predict_overlap_workspace_size.restype = ctypes.c_size_t
         L.star_project_load.restype = ctypes.c_int
         L.star_project_load.argtypes = [ctypes.POINTER(LoadParams)] + [_P] * 5 + [ctypes.c_size_t, _P]
         L.star_score_migrations.restype = ctypes.c_int
@@ -209,6 +211,10 @@ def predict_noalloc(p: PredictParams, hidden, w1, b1, w2, b2, bin_values, ema_st
     _check("star_predict_noalloc", lib().star_predict_noalloc(
         ctypes.byref(p), _ptr(hidden), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
         _ptr(bin_values), _ptr(ema_state), _ptr(expected_len), _ptr(rem_len), _stream(stream)))
+
+
+def predict_overlap_workspace_size(p: PredictParams) -> int:
+    return lib().star_predict_overlap_workspace_size(ctypes.byref(p))
 
 
 def predict_overlap(p: PredictParams, hidden_next, ws_next, ws_prev, w1, b1, w2, b2,

@@ -105,10 +105,17 @@ def _overlap(L, p, hidden=FAKE, ws_next=FAKE, ws_prev=ctypes.c_void_p((1 << 20) 
 
 def test_predict_overlap_validation(L):
     """The two-batch predictor call validates each side it is given, before
-    launching anything, and refuses what it does not run as a product plus
-    head: one-slice shapes (the fused kernel) and the K-chunked head."""
+    launching anything.  Its workspace is star_predict's, except for
+    one-slice products, which it runs as a product and a head (one fp32
+    partial plane) instead of the fused kernel (logit shares)."""
     p = _pp()
-    need = star.predict_workspace_size(p)
+    need = star.predict_overlap_workspace_size(p)
+    assert need == star.predict_workspace_size(p)
+    one = _pp(n_req=8192)                                            # one K-slice
+    assert star.predict_overlap_workspace_size(one) == star.STAR_WS_HEADER_BYTES + 8192 * 512 * 4
+    assert star.predict_overlap_workspace_size(one) > star.predict_workspace_size(one)
+    assert _overlap(L, one, ws_bytes=star.predict_workspace_size(one)) == -4
+    assert star.predict_overlap_workspace_size(_pp(n_req=-1)) == 0
     assert _overlap(L, None) == -1
     assert _overlap(L, p, hidden=None, ws_prev=None) == -1          # neither side
     assert _overlap(L, p, ws_bytes=need - 1) == -4
@@ -119,8 +126,6 @@ def test_predict_overlap_validation(L):
     assert _overlap(L, p, hidden=None, w1=None, expected=None) == -1  # head needs its outputs
     assert _overlap(L, p, ema=None) == -1                             # EMA on, no state
     assert _overlap(L, p, hidden=ctypes.c_void_p((1 << 20) + 2)) == -2
-    assert _overlap(L, _pp(n_req=8192)) == -2                         # one K-slice: fused kernel
-    assert _overlap(L, _pp(n_req=8200, d_model=64, d_hidden=2048, n_bins=256)) == -2   # tiled head
 
 
 def test_predict_noalloc_validation_and_scratch_limit(L):

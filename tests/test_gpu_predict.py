@@ -433,21 +433,25 @@ def test_second_layer_logit_read_through_two_bins(B, d, m, dtype):
     assert err.max() < 1e-4
 
 
-@pytest.mark.parametrize("B,d,m,nb,dtype,alpha,steps", [
-    (1024, 4096, 512, 64, synth.BF16, 0.2, 5),   # continuous shape: one launch, 4 K-splits
-    (512, 4096, 512, 64, synth.BF16, 0.0, 3),    # one launch, 8 K-splits, no EMA
-    (1000, 4040, 400, 64, synth.BF16, 0.2, 3),   # one launch, ragged rows, columns and K
-    (4096, 5120, 512, 64, synth.BF16, 0.2, 2),   # 128 x 128 tiles: two launches
-    (64, 1024, 256, 32, synth.F32, 0.2, 3),      # fp32: two launches
-    (2100, 4096, 256, 64, synth.BF16, 0.2, 3),   # over 512 head workgroups: two launches
+@pytest.mark.parametrize("B,d,m,nb,dtype,alpha,steps,same", [
+    (1024, 4096, 512, 64, synth.BF16, 0.2, 5, True),   # continuous shape: one launch, 4 K-splits
+    (512, 4096, 512, 64, synth.BF16, 0.0, 3, True),    # one launch, 8 K-splits, no EMA
+    (1000, 4040, 400, 64, synth.BF16, 0.2, 3, True),   # one launch, ragged rows, columns and K
+    (4096, 5120, 512, 64, synth.BF16, 0.2, 2, True),   # 128 x 128 tiles: two launches
+    (64, 1024, 256, 32, synth.F32, 0.2, 3, True),      # fp32: two launches
+    (2100, 4096, 256, 64, synth.BF16, 0.2, 3, True),   # over 512 head workgroups: two launches
+    (8192, 3968, 64, 200, synth.BF16, 0.2, 2, True),   # the K-chunked head, 4 planes
+    (3000, 136, 72, 20, synth.BF16, 0.2, 3, False),    # one K-slice: star_predict fuses it
+    (9000, 512, 1024, 128, synth.BF16, 0.2, 2, False), # one K-slice, the K-chunked head here
 ])
-def test_overlap_sequence_equals_predict(B, d, m, nb, dtype, alpha, steps):
+def test_overlap_sequence_equals_predict(B, d, m, nb, dtype, alpha, steps, same):
     """star_predict_overlap over a sequence of batches, two workspaces in
-    turn (the first call only the product, the last only the head), gives
-    every batch's E, rem_len and EMA state bit for bit as star_predict on
-    that batch, the EMA carried in order; the first batch also against the
-    oracle.  (One-slice shapes, which star_predict runs as one fused kernel,
-    are refused: a host test covers that.)"""
+    turn (the first call only the product, the last only the head): where
+    star_predict runs the same two kernels (products with a K-split) every
+    batch's E, rem_len and EMA state equal star_predict's bit for bit, the
+    EMA carried in order; one-slice products, which star_predict runs as one
+    fused kernel, are checked against the oracle instead (sampled rows, the
+    2e-2 contract and the derived bound), and the first batch always is."""
     from paper_2510_13668_amd import star
     rng = np.random.default_rng(B + d + m + nb + steps)
     bf = dtype == synth.BF16
@@ -464,23 +468,25 @@ def test_overlap_sequence_equals_predict(B, d, m, nb, dtype, alpha, steps):
                    len_max=32768, ema_alpha=alpha)
     hd = [to_dev(h, bf) for h in hs]
     want = []
-    for i in range(steps):
-        pr.run(hd[i], ema_init=(i == 0))
-        torch.cuda.synchronize()
-        want.append((pr.expected.cpu().numpy().copy(), pr.rem.cpu().numpy().copy(),
-                     pr.ema.cpu().numpy().copy()))
-    ref = oracle.predict(hs[0][:64], w1, w2, bins, dtype=dtype, act=synth.ACT_GELU, b1=b1, b2=b2,
-                         len_max=32768)
-    assert_lengths_close(want[0][0][:64], ref["expected"])
+    if same:
+        for i in range(steps):
+            pr.run(hd[i], ema_init=(i == 0))
+            torch.cuda.synchronize()
+            want.append((pr.expected.cpu().numpy().copy(), pr.rem.cpu().numpy().copy(),
+                         pr.ema.cpu().numpy().copy()))
 
     print(f"overlap B={B} d={d} m={m} nb={nb} dtype={dtype} steps={steps}", flush=True)
-    ws = [star.Workspace(pr.ws.nbytes), star.Workspace(pr.ws.nbytes)]
+    nbytes = star.predict_overlap_workspace_size(pr.params(False))
+    ws = [star.Workspace(nbytes), star.Workspace(nbytes)]
     ema = torch.full((B,), -5.0, dtype=torch.float32, device="cuda")
     exp = torch.empty(B, dtype=torch.float32, device="cuda")
     rem = torch.empty(B, dtype=torch.int32, device="cuda")
     ema_arg = ema if alpha > 0 else None
     star.predict_overlap(pr.params(False), hd[0], ws[0], None, pr.w1, pr.b1, pr.w2, pr.b2,
                          pr.bins, None, None, None)
+    rows = np.unique(np.concatenate([np.arange(min(B, 40)), np.arange(max(0, B - 40), B),
+                                     rng.choice(B, min(B, 60), replace=False)]))
+    tight = E_TIGHT * max(1.0, w2_scale(w2, dtype))
     for i in range(steps):
         nxt = hd[i + 1] if i + 1 < steps else None
         exp.fill_(-1.0)
@@ -488,7 +494,17 @@ def test_overlap_sequence_equals_predict(B, d, m, nb, dtype, alpha, steps):
         star.predict_overlap(pr.params(i == 0), nxt, ws[(i + 1) % 2] if nxt is not None else None,
                              ws[i % 2], pr.w1, pr.b1, pr.w2, pr.b2, pr.bins, ema_arg, exp, rem)
         torch.cuda.synchronize()
-        np.testing.assert_array_equal(exp.cpu().numpy(), want[i][0], err_msg=f"E, batch {i}")
-        np.testing.assert_array_equal(rem.cpu().numpy(), want[i][1], err_msg=f"rem, batch {i}")
-        if alpha > 0:
-            np.testing.assert_array_equal(ema.cpu().numpy(), want[i][2], err_msg=f"EMA, batch {i}")
+        e = exp.cpu().numpy()
+        if i == 0 or not same:
+            ref = oracle.predict(hs[i][rows], w1, w2, bins, dtype=dtype, act=synth.ACT_GELU,
+                                 b1=b1, b2=b2, len_max=32768)
+            err = assert_lengths_close(e[rows], ref["expected"])
+            assert err <= tight, f"batch {i}: max rel err {err:.3e} above {tight:.1e}"
+            _check_rem(rem.cpu().numpy()[rows], ref["expected"] if alpha == 0 or i == 0
+                       else ema.cpu().numpy()[rows], 32768)
+        if same:
+            np.testing.assert_array_equal(e, want[i][0], err_msg=f"E, batch {i}")
+            np.testing.assert_array_equal(rem.cpu().numpy(), want[i][1], err_msg=f"rem, batch {i}")
+            if alpha > 0:
+                np.testing.assert_array_equal(ema.cpu().numpy(), want[i][2],
+                                              err_msg=f"EMA, batch {i}")
