@@ -807,117 +807,130 @@ __global__ __launch_bounds__(HD_THREADS) void head_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// The head for large bf16 batches, K-chunked: 64 rows per workgroup (16 per
-// wave).  For each chunk of 64 a1 columns the workgroup reduces that chunk's
-// partials (fixed order), adds b1, applies the activation and writes the
-// bf16 hi/lo pair to LDS, stages W2's chunk in LDS once for all four waves,
-// and runs the 16x16x32 MFMAs; the next chunk's partials and W2 are loaded
-// into registers meanwhile.  With up to 128 bins there are two LDS stages and
-// one barrier per chunk: the next chunk is activated (VALU) into one stage
-// while the products (MFMA) read the other.  The logits stay in registers
-// for the softmax: a row's bins are spread over 16 lanes, plus registers.
+// The head for large bf16 batches, K-chunked: 64 rows per workgroup of eight
+// waves.  Wave w takes the 16 rows of group w % 4 and the 32-wide half w / 4
+// of every chunk of 64 a1 columns.  Each lane loads from HBM exactly the 8
+// partials that it feeds to the 16x16x32 MFMA as its A operand (row
+// lane % 16 of the group, columns 8 (lane / 16) + 0..7 of the half), reduces
+// the planes in a fixed order, adds b1 (staged in LDS once), applies the
+// activation and splits the result into the bf16 hi/lo pair in registers:
+// a1 never passes through LDS and every activation is computed once.  W2's
+// chunk, the B operand the four row groups share, is staged in LDS in two
+// stages with one barrier per chunk.  The two halves' logits are summed once
+// at the end (lower half first), and the softmax runs on the logits in
+// registers: a row's bins are spread over 16 lanes, plus registers.
 // W2 is read once per 64 rows (the 4-row head reads it once per 4).
 // ---------------------------------------------------------------------------
 constexpr int HT_ROWS = 64;
 constexpr int HT_KC = 64;                   // a1 columns per chunk
-constexpr int HT_ASTR = HT_KC + 8;          // bf16 per LDS row (padding spreads banks)
+constexpr int HT_ASTR = HT_KC + 8;          // bf16 per LDS row of W2 (padding spreads banks)
+constexpr int HT_THREADS = 512;             // 4 row groups x 2 halves of each chunk
 constexpr int HT_MIN_REQ = 8192;            // batches from which the tiled head is used
-constexpr int HT_MAX_SPLITS = 4;            // its partial registers: 4 x splits float4
+constexpr int HT_MAX_SPLITS = 4;            // its partial registers: 2 float4 per plane
 
 // bin blocks of 16 the tiled head computes: 4, 8 or 16 (compile time, so that
 // every loop over them has a fixed trip count; blocks past nb carry zeros)
 static int head_tiled_blocks(int nb) { return nb <= 64 ? 4 : nb <= 128 ? 8 : 16; }
-// two LDS stages (the next chunk is written while the products read this
-// one) while two workgroups still fit a CU, i.e. up to 8 bin blocks
-constexpr bool head_tiled_two_stages(int nbb) { return nbb <= 8; }
-static size_t head_tiled_lds(int nb) {
-    const int nbb = head_tiled_blocks(nb);
-    return (size_t)(head_tiled_two_stages(nbb) ? 2 : 1) * (2 * HT_ROWS + nbb * 16) * HT_ASTR * 2;
+// two W2 stages, then b1 (m fp32); the halves' logits meet in the stages
+constexpr size_t head_tiled_stage_bytes(int nbb) { return (size_t)nbb * 16 * HT_ASTR * 2; }
+static size_t head_tiled_lds(int nb, int m) {
+    return 2 * head_tiled_stage_bytes(head_tiled_blocks(nb)) + (size_t)m * 4;
 }
-
-// One chunk's registers: 4 float4 of partials per plane (64 rows x 16
-// float4 per workgroup), their b1, and up to 8 16-byte pieces of W2.
-template <int kS, int kNBB>
-struct HtRegs {
-    float4 pv[4][kS];
-    float4 bv[4];
-    uint4 wv[kNBB / 2];      // kNBB x 16 bins x 8 pieces over 256 threads
-};
 
 struct HtArgs {
     const float4* P4;
-    const float* b1;
     const uint16_t* W2;
     int64_t plane4;
-    int B, m, m4, nb, row0;
+    int B, m, m4, nb;
 };
 
-template <int kS, int kNBB>
-__device__ __forceinline__ void ht_load(const HtArgs& a, int c, HtRegs<kS, kNBB>& g) {
-    const int tid = threadIdx.x;
-    const int k0 = c * HT_KC;
+// a lane's 8 partials of one chunk, per plane
+template <int kS>
+struct HtP {
+    float4 v[kS][2];
+};
+// the thread's 16-byte pieces of a W2 chunk (kNBB x 16 bins x 8 pieces over
+// the workgroup)
+template <int kNBB>
+struct HtW {
+    static constexpr int kU = kNBB * 16 * 8 / HT_THREADS;
+    static_assert(kU >= 1 && kU * HT_THREADS == kNBB * 128, "whole W2 pieces per thread");
+    uint4 v[kU];
+};
+
+// partials of row `row`, columns k .. k + 7 (m % 8 == 0: all in range or
+// none); rows past B and columns past m read offset 0 and are masked later
+template <int kS>
+__device__ __forceinline__ void ht_load_p(const HtArgs& a, int row, int k, HtP<kS>& g) {
+    const bool ok = row < a.B && k < a.m;
+    const int64_t off = ok ? (int64_t)row * a.m4 + (k >> 2) : 0;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int idx = u * HD_THREADS + tid;
-        const int r = idx >> 4, kc = k0 + (idx & 15) * 4;
-        const bool ok = a.row0 + r < a.B && kc < a.m;
-        const int64_t off = ok ? (int64_t)(a.row0 + r) * a.m4 + (kc >> 2) : 0;
-#pragma unroll
-        for (int q = 0; q < kS; ++q) {
-            const f32x4 t = __builtin_nontemporal_load((const f32x4*)&a.P4[q * a.plane4 + off]);
-            g.pv[u][q] = make_float4(t[0], t[1], t[2], t[3]);
-        }
-        g.bv[u] = (a.b1 && kc < a.m) ? *(const float4*)(a.b1 + kc) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int u = 0; u < kNBB / 2; ++u) {
-        const int it = u * HD_THREADS + tid;
-        const int j = it >> 3, kk = k0 + (it & 7) * 8;
-        const bool ok = j < a.nb && kk < a.m;      // m % 8 == 0: whole pieces
-        g.wv[u] = *(const uint4*)(a.W2 + (ok ? (int64_t)j * a.m + kk : 0));
+    for (int q = 0; q < kS; ++q) {
+        const f32x4 t0 = __builtin_nontemporal_load((const f32x4*)&a.P4[q * a.plane4 + off]);
+        const f32x4 t1 = __builtin_nontemporal_load((const f32x4*)&a.P4[q * a.plane4 + off + 1]);
+        g.v[q][0] = make_float4(t0[0], t0[1], t0[2], t0[3]);
+        g.v[q][1] = make_float4(t1[0], t1[1], t1[2], t1[3]);
     }
 }
 
-template <int kS, int kNBB, bool kGelu>
-__device__ __forceinline__ void ht_store(const HtArgs& a, int c, const HtRegs<kS, kNBB>& g,
-                                         uint16_t* ahi, uint16_t* alo, uint16_t* wl) {
+template <int kNBB>
+__device__ __forceinline__ void ht_load_w(const HtArgs& a, int c, HtW<kNBB>& g) {
     const int tid = threadIdx.x;
-    const int k0 = c * HT_KC;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int idx = u * HD_THREADS + tid;
-        const int r = idx >> 4, c4 = idx & 15, kc = k0 + c4 * 4;
-        const bool ok = a.row0 + r < a.B && kc < a.m;
-        float4 sum = g.pv[u][0];
-#pragma unroll
-        for (int q = 1; q < kS; ++q) {
-            sum.x += g.pv[u][q].x; sum.y += g.pv[u][q].y; sum.z += g.pv[u][q].z; sum.w += g.pv[u][q].w;
-        }
-        const float av[4] = {sum.x + g.bv[u].x, sum.y + g.bv[u].y, sum.z + g.bv[u].z, sum.w + g.bv[u].w};
-        uint32_t hw[2], lw[2];
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const float y0 = av[2 * e], y1 = av[2 * e + 1];
-            const float g0 = kGelu ? gelu_erf(y0) : fmaxf(y0, 0.0f);
-            const float g1 = kGelu ? gelu_erf(y1) : fmaxf(y1, 0.0f);
-            split_bf16x2(ok ? g0 : 0.0f, ok ? g1 : 0.0f, hw[e], lw[e]);
-        }
-        const int o = r * HT_ASTR + c4 * 4;
-        *(uint2*)(ahi + o) = make_uint2(hw[0], hw[1]);
-        *(uint2*)(alo + o) = make_uint2(lw[0], lw[1]);
+    for (int u = 0; u < HtW<kNBB>::kU; ++u) {
+        const int it = u * HT_THREADS + tid;
+        const int j = it >> 3, kk = c * HT_KC + (it & 7) * 8;
+        const bool ok = j < a.nb && kk < a.m;
+        g.v[u] = *(const uint4*)(a.W2 + (ok ? (int64_t)j * a.m + kk : 0));
     }
+}
+
+template <int kNBB>
+__device__ __forceinline__ void ht_store_w(const HtArgs& a, int c, const HtW<kNBB>& g,
+                                           uint16_t* wl) {
+    const int tid = threadIdx.x;
 #pragma unroll
-    for (int u = 0; u < kNBB / 2; ++u) {
-        const int it = u * HD_THREADS + tid;       // row j < kNBB x 16 of the W2 chunk
-        const int j = it >> 3, kk = k0 + (it & 7) * 8;
+    for (int u = 0; u < HtW<kNBB>::kU; ++u) {
+        const int it = u * HT_THREADS + tid;       // row j < kNBB x 16 of the W2 chunk
+        const int j = it >> 3, kk = c * HT_KC + (it & 7) * 8;
         const uint32_t z = (j < a.nb && kk < a.m) ? 0xFFFFFFFFu : 0u;
         *(uint4*)(wl + j * HT_ASTR + (it & 7) * 8) =
-            make_uint4(g.wv[u].x & z, g.wv[u].y & z, g.wv[u].z & z, g.wv[u].w & z);
+            make_uint4(g.v[u].x & z, g.v[u].y & z, g.v[u].z & z, g.v[u].w & z);
     }
 }
 
+// a1 = act(sum of the planes + b1) for the lane's 8 columns as the bf16
+// hi/lo pair (zeros outside the batch and past m)
+template <int kS, bool kGelu>
+__device__ __forceinline__ void ht_act(const HtP<kS>& g, const float* b1s, int k, bool ok,
+                                       bf16x8& hi, bf16x8& lo) {
+    float4 s0 = g.v[0][0], s1 = g.v[0][1];
+#pragma unroll
+    for (int q = 1; q < kS; ++q) {
+        s0.x += g.v[q][0].x; s0.y += g.v[q][0].y; s0.z += g.v[q][0].z; s0.w += g.v[q][0].w;
+        s1.x += g.v[q][1].x; s1.y += g.v[q][1].y; s1.z += g.v[q][1].z; s1.w += g.v[q][1].w;
+    }
+    const float4 c0 = *(const float4*)(b1s + (ok ? k : 0));
+    const float4 c1 = *(const float4*)(b1s + (ok ? k : 0) + 4);
+    const float av[8] = {s0.x + c0.x, s0.y + c0.y, s0.z + c0.z, s0.w + c0.w,
+                         s1.x + c1.x, s1.y + c1.y, s1.z + c1.z, s1.w + c1.w};
+    uint32_t hw[4], lw[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float y0 = av[2 * e], y1 = av[2 * e + 1];
+        const float g0 = kGelu ? gelu_erf(y0) : fmaxf(y0, 0.0f);
+        const float g1 = kGelu ? gelu_erf(y1) : fmaxf(y1, 0.0f);
+        split_bf16x2(ok ? g0 : 0.0f, ok ? g1 : 0.0f, hw[e], lw[e]);
+    }
+    hi = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
+    lo = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
+}
+
+// up to 128 bins and two planes, two workgroups per CU (four waves per
+// SIMD, at most 128 VGPRs)
 template <int kS, int kNBB, bool kGelu>
-__global__ __launch_bounds__(HD_THREADS) void head_tiled_kernel(
+__global__ __launch_bounds__(HT_THREADS)
+__attribute__((amdgpu_waves_per_eu(kNBB <= 8 && kS <= 2 ? 4 : 1))) void head_tiled_kernel(
     const float* __restrict__ P, int B, int m, int nb, const float* __restrict__ b1,
     const uint16_t* __restrict__ W2, const float* __restrict__ b2,
     const float* __restrict__ bins, float ema_alpha, int ema_init,
@@ -928,86 +941,102 @@ __global__ __launch_bounds__(HD_THREADS) void head_tiled_kernel(
     const int lane = tid & 63;
     const int wid = tid >> 6;
     const int row0 = blockIdx.x * HT_ROWS;
-    // a stage: A hi [64][HT_ASTR], A lo [64][HT_ASTR], W2 [kNBB * 16][HT_ASTR]
-    constexpr int kStage = (2 * HT_ROWS + kNBB * 16) * HT_ASTR;
-    constexpr bool kTwo = head_tiled_two_stages(kNBB);
+    constexpr int kStage = (int)(head_tiled_stage_bytes(kNBB) / 2);   // bf16 per stage
     uint16_t* const st0 = (uint16_t*)smem;
-    uint16_t* const st1 = st0 + (kTwo ? kStage : 0);
+    uint16_t* const st1 = st0 + kStage;
+    float* const b1s = (float*)(st1 + kStage);
     HtArgs a;
     a.P4 = (const float4*)P;
-    a.b1 = b1;
     a.W2 = W2;
     a.m = m;
     a.m4 = m >> 2;
     a.B = B;
     a.plane4 = (int64_t)B * a.m4;
     a.nb = nb;
-    a.row0 = row0;
     const int nchunk = (m + HT_KC - 1) / HT_KC;
-    // loads past the last chunk read offset 0 (masked), so none is guarded
-    HtRegs<kS, kNBB> g;
+    // wave wid: rows of group rg, K half kh of every chunk
+    const int rg = wid & 3;
+    const int kh = wid >> 2;
+    const int row = row0 + rg * 16 + (lane & 15);   // the lane's A row (MFMA row lane % 16)
+    const int kofs = kh * 32 + (lane >> 4) * 8;     // its 8 columns within a chunk
+    const bool row_ok = row < B;
 
     f32x4 acc[kNBB];
 #pragma unroll
     for (int j = 0; j < kNBB; ++j) acc[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    const int ar = wid * 16 + (lane & 15);          // this lane's A row (MFMA row lane % 16)
-    const int kq = (lane >> 4) * 8;                 // its 8 k values within a 32-wide step
 
-    // the products of one chunk: 16 rows of this wave x kNBB bin blocks
-    auto products = [&](const uint16_t* stage) {
-        const uint16_t* ahi = stage;
-        const uint16_t* alo = stage + HT_ROWS * HT_ASTR;
-        const uint16_t* wl = stage + 2 * HT_ROWS * HT_ASTR;
+    // the products of one chunk: the lane's A pair x kNBB bin blocks of W2
+    auto products = [&](const uint16_t* wl, const bf16x8& h, const bf16x8& l) {
+        // per group of 4 blocks, the hi products, then the lo ones:
+        // consecutive MFMAs are independent
+        constexpr int kG = kNBB < 4 ? kNBB : 4;
 #pragma unroll
-        for (int sstep = 0; sstep < HT_KC / 32; ++sstep) {
-            const int ka = sstep * 32 + kq;
-            const bf16x8 h = *(const bf16x8*)(ahi + ar * HT_ASTR + ka);
-            const bf16x8 l = *(const bf16x8*)(alo + ar * HT_ASTR + ka);
-            // per group of up to 8 blocks, the hi products, then the lo ones:
-            // consecutive MFMAs are independent
-            constexpr int kG = kNBB < 8 ? kNBB : 8;
+        for (int j0 = 0; j0 < kNBB; j0 += kG) {
+            bf16x8_t wb[kG];
 #pragma unroll
-            for (int j0 = 0; j0 < kNBB; j0 += kG) {
-                bf16x8_t wb[kG];
+            for (int j = 0; j < kG; ++j)
+                wb[j] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(wl + ((j0 + j) * 16 + (lane & 15)) * HT_ASTR + kofs));
 #pragma unroll
-                for (int j = 0; j < kG; ++j)
-                    wb[j] = __builtin_bit_cast(bf16x8_t, *(const bf16x8*)(wl + ((j0 + j) * 16 + (lane & 15)) * HT_ASTR + ka));
+            for (int j = 0; j < kG; ++j)
+                acc[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, h), wb[j], acc[j0 + j], 0, 0, 0);
 #pragma unroll
-                for (int j = 0; j < kG; ++j)
-                    acc[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, h), wb[j], acc[j0 + j], 0, 0, 0);
-#pragma unroll
-                for (int j = 0; j < kG; ++j)
-                    acc[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, l), wb[j], acc[j0 + j], 0, 0, 0);
-            }
+            for (int j = 0; j < kG; ++j)
+                acc[j0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, l), wb[j], acc[j0 + j], 0, 0, 0);
         }
     };
-    auto store = [&](int c, uint16_t* stage) {
-        ht_store<kS, kNBB, kGelu>(a, c, g, stage, stage + HT_ROWS * HT_ASTR, stage + 2 * HT_ROWS * HT_ASTR);
-    };
 
-    ht_load(a, 0, g);
-    if constexpr (kTwo) {
-        // one barrier per chunk: chunk c + 1 is activated and written to the
-        // other stage (VALU) while chunk c's products run (MFMA); that stage
-        // was last read before the previous barrier
-        store(0, st0);
-        ht_load(a, 1, g);
+    // The partials and W2's chunks are loaded one chunk ahead (chunk c + 1's
+    // partials are requested once chunk c is activated).  Loads complete in
+    // issue order for the wait counter, so in each step W2, needed sooner,
+    // is requested before the partials.
+    // workgroups start at different chunks (block index mod chunks), so that
+    // at any time the chip reads every column range of the partial rows, not
+    // one 256-byte range of all of them (rows 4 KiB apart would meet on few
+    // HBM channels); the chunks' order in each row's sums changes with it
+    const int rot = (int)(blockIdx.x % (unsigned)nchunk);
+    auto chunk = [&](int c) { return c + rot < nchunk ? c + rot : c + rot - nchunk; };
+    HtP<kS> p0;
+    HtW<kNBB> w;
+    ht_load_w(a, chunk(0), w);
+    ht_load_p(a, row, chunk(0) * HT_KC + kofs, p0);
+    for (int i = tid; i < m; i += HT_THREADS) b1s[i] = b1 ? b1[i] : 0.0f;
+    ht_store_w(a, chunk(0), w, st0);
+    if (nchunk > 1) ht_load_w(a, chunk(1), w);
+    __syncthreads();
+
+    // step c: activate chunk c and request chunk c + 1's partials, chunk c's
+    // products on stage c % 2, W2 of chunk c + 1 into the other stage (last
+    // read before the previous barrier)
+    int c = 0;
+    for (;; ++c) {
+        const int k = chunk(c) * HT_KC + kofs;
+        bf16x8 h, l;
+        ht_act<kS, kGelu>(p0, b1s, k, row_ok && k < m, h, l);
+        if (c + 1 < nchunk) ht_load_p(a, row, chunk(c + 1) * HT_KC + kofs, p0);
+        products((c & 1) ? st1 : st0, h, l);
+        if (c + 1 == nchunk) break;
+        ht_store_w(a, chunk(c + 1), w, (c & 1) ? st0 : st1);
+        if (c + 2 < nchunk) ht_load_w(a, chunk(c + 2), w);
         __syncthreads();
-        int c = 0;
-        for (; c + 1 < nchunk; ++c) {
-            products((c & 1) ? st1 : st0);
-            store(c + 1, (c & 1) ? st0 : st1);
-            ht_load(a, c + 2, g);
-            __syncthreads();
+    }
+
+    // the upper K half's logits join the lower half's, in that order, through
+    // the stages (kNBB x 4 KiB; two stages hold kNBB x 4.5 KiB)
+    {
+        static_assert(4 * kNBB * 64 * 16 <= 2 * kStage * 2, "exchange fits the stages");
+        f32x4* const xs = (f32x4*)smem;
+        __syncthreads();                        // every wave's last products are done
+        if (kh == 1) {
+#pragma unroll
+            for (int j = 0; j < kNBB; ++j) xs[(rg * kNBB + j) * 64 + lane] = acc[j];
         }
-        products((c & 1) ? st1 : st0);
-    } else {
-        for (int c = 0; c < nchunk; ++c) {
-            store(c, st0);
-            __syncthreads();
-            ht_load(a, c + 1, g);                   // in flight during the products
-            products(st0);
-            __syncthreads();                        // before the next chunk overwrites LDS
+        __syncthreads();
+        if (kh == 1) return;                    // no barrier follows
+#pragma unroll
+        for (int j = 0; j < kNBB; ++j) {
+            const f32x4 o = xs[(rg * kNBB + j) * 64 + lane];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[j][v] += o[v];
         }
     }
 
@@ -1045,7 +1074,7 @@ __global__ __launch_bounds__(HD_THREADS) void head_tiled_kernel(
             den += __shfl_xor(den, o, 16);
             num += __shfl_xor(num, o, 16);
         }
-        const int gr = row0 + wid * 16 + 4 * (lane >> 4) + v;
+        const int gr = row0 + rg * 16 + 4 * (lane >> 4) + v;
         if ((lane & 15) == 0 && gr < B) {
             const float E = num / den;
             expected[gr] = E;
@@ -1517,7 +1546,7 @@ PredictPlan plan_predict(const star_predict_params& p, bool tiled_ok, bool fused
     pl.head_rows = pl.head_tiled ? HT_ROWS : HD_RB;
     const size_t rb = (size_t)pl.head_rows;
     if (pl.head_tiled)
-        pl.head_lds = head_tiled_lds(p.n_bins);
+        pl.head_lds = head_tiled_lds(p.n_bins, p.d_hidden);
     else if (p.dtype == STAR_BF16)
         pl.head_lds = 2 * rb * (mpad + 8) * 2 + rb * nbpad * 4;
     else
@@ -1598,7 +1627,7 @@ static hipError_t launch_head_tiled_act(const star_predict_params& p, const Pred
         if (e != hipSuccess) return e;
     }
     const dim3 grid((unsigned)ceil_div(p.n_req, HT_ROWS));
-    hipLaunchKernelGGL((head_tiled_kernel<kS, kNBB, kGelu>), grid, dim3(HD_THREADS), pl.head_lds, stream,
+    hipLaunchKernelGGL((head_tiled_kernel<kS, kNBB, kGelu>), grid, dim3(HT_THREADS), pl.head_lds, stream,
                        partials, p.n_req, p.d_hidden, p.n_bins, b1, (const uint16_t*)w2, b2, bins,
                        p.ema_alpha, p.ema_init, ema_state, expected, rem_len, p.len_max);
     return hipGetLastError();
