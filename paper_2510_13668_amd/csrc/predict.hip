@@ -86,7 +86,8 @@ using G1Wide = G1Shape<128, 128, 2, 2>;
 // 8 waves, 64 x 128 slabs of a 256 x 256 tile: four times G1Big's matrix-core
 // work per byte loaded, one workgroup per CU (147 KiB of LDS); one K-tile in
 // flight keeps it within 256 registers.  For products with hundreds of such
-// tiles (measured: 448-483 us, 46-49% of peak, at 32768 x 1024 x 8192).
+// tiles (measured at 32768 x 1024 x 8192: 511-715 us per call, 570 us on
+// average over 70 calls, 39% of peak, the matrix cores busy half the time).
 using G1Huge = G1Shape<256, 256, 4, 2>;
 
 // One K-tile of both operands staged in registers (constant indices only,

@@ -163,12 +163,17 @@ def _splits(B, d, m, nb):
     (8192, 64, 2048, 200, synth.ACT_GELU, 1),      # 16 blocks, one LDS stage
     (8200, 1024, 64, 250, synth.ACT_RELU, 2),      # 16 blocks, two planes
     (8192, 4096, 64, 200, synth.ACT_RELU, 4),      # 16 blocks, four planes
+    (16400, 64, 1000, 100, synth.ACT_GELU, 1),     # ragged m: last chunk 40 columns, 8 blocks
+    (8200, 64, 1000, 200, synth.ACT_RELU, 1),      # ragged m, 16 blocks
+    (8192, 64, 8, 200, synth.ACT_GELU, 1),         # one chunk of 8 columns
 ])
 def test_tiled_head_planes_and_activations(B, d, m, nb, act, planes):
     """The K-chunked head (batches of 8192 rows and more that the fused
     kernel does not take: 256 x 256 product tiles, or more than 128 bins)
-    over the split-K planes it meets (1, 2, 4), every bin-block count and
-    both activations; sampled rows."""
+    over the split-K planes it meets (1, 2, 4), every bin-block count, both
+    activations, ragged row and column counts (the workgroups start at
+    different column chunks and wrap around) and a single chunk; sampled
+    rows."""
     assert _splits(B, d, m, nb) == planes, "the plan no longer takes this many planes here"
     rng = np.random.default_rng(B * 7 + d + m + nb)
     h = synth.f32_to_bf16_bits(rng.standard_normal((B, d)).astype(np.float32))
