@@ -2862,8 +2862,9 @@ __global__ __launch_bounds__(SO_THREADS) void score_one_kernel(OneArgs a) {
             }
         }
     }
-    // the round's global writes, issued last: a barrier waits for every
-    // store issued before it
+    // the round's global writes, issued last.  Barriers do not wait for
+    // stores here, but issuing these right after the scoring, under the
+    // ranking's phases, measured slower (12.1-12.2 against 11.8 us a call)
     auto write_round = [&]() {
         if (live && a.scores) {
             int64_t* out = a.scores + (int64_t)r * n;
